@@ -1,0 +1,207 @@
+/*
+ * attn_abft.h - C ABI of the ABFT-protected multi-head attention layer
+ * (EEC-ABFT, ATTNChecker: arXiv 2410.11720) on AMD MI355X (gfx950).
+ *
+ * The layer (paper Sec. 2.1, Eq. 1-2, Fig. 1) with GPT-2 style packed
+ * weights:
+ *   [Q | K | V] = X Wqkv,  AS_h = Q_h K_h^T,  AP_h = softmax(scale * AS_h [causal mask]),
+ *   CL_h = AP_h V_h,       O = CL Wo,
+ * and its backward. Every GEMM output carries unweighted and weighted
+ * checksums (weights 1..R inside R-row blocks, Sec. 2.3) that are encoded
+ * once per protection section and passed through the section's GEMMs
+ * (Sec. 4.4), then verified with EEC-ABFT (Sec. 4.2, 4.3): INF, NaN and
+ * near-INF errors are detected, located and corrected in place.
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ * - Pointers marked (device) are caller-owned device memory on the current
+ *   HIP device; the library allocates nothing and keeps no state between
+ *   calls. Pointers marked (host) are read during the call only.
+ * - `stream` is a hipStream_t (NULL = the null stream). All GPU work is
+ *   enqueued asynchronously on it; outputs and the report are valid after
+ *   the caller synchronises the stream.
+ * - Layouts are dense row-major (C order), dimensions listed outermost first.
+ * - bf16 storage is IEEE bfloat16 (round-to-nearest-even when produced);
+ *   accumulation and all checksums are fp32.
+ * - Return value: ABFT_OK, or a negative status covering argument and
+ *   launch errors only. On an argument error nothing is enqueued. Detected,
+ *   corrected and uncorrectable faults are NOT status codes: they are
+ *   reported in the abft_report (device) and read after a sync;
+ *   n_uncorrectable > 0 is the caller's cue to fall back to
+ *   checkpoint/restore.
+ */
+#ifndef ATTN_ABFT_H
+#define ATTN_ABFT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define ABFT_OK               0
+#define ABFT_ERR_INVALID     -1   /* null pointer, bad shape, R does not divide seq, ... */
+#define ABFT_ERR_UNSUPPORTED -2   /* dtype / mode not implemented, not a gfx950 device */
+#define ABFT_ERR_HIP         -3   /* a kernel launch failed */
+#define ABFT_ERR_WORKSPACE   -4   /* workspace smaller than attn_abft_workspace_bytes() */
+
+/* ---- storage dtypes -------------------------------------------------- */
+#define ABFT_BF16 0
+#define ABFT_FP32 1
+
+/* ---- protection sections (Sec. 4.4), the per-step enable mask that the
+ *      adaptive frequencies of Sec. 4.5 act on ---------------------------- */
+#define ABFT_SEC_AS  1u   /* X W^Q, X W^K, Q K^T            */
+#define ABFT_SEC_CL  2u   /* X W^V, AP V                    */
+#define ABFT_SEC_O   4u   /* CL W^O                         */
+#define ABFT_SEC_BWD 8u   /* every backward GEMM            */
+#define ABFT_SEC_ALL 15u
+
+/* ---- flags ----------------------------------------------------------- */
+#define ABFT_FLAG_ROOT_CHECK    1u  /* verify Q, K, V right after the projection */
+#define ABFT_FLAG_REPORT_APPEND 2u  /* keep the report's contents at entry        */
+#define ABFT_FLAG_UNPROTECTED   4u  /* no checksums and no verification: the same
+                                       kernels without ABFT (overhead baseline)  */
+
+/* ---- op tags of protected GEMM outputs (paper Table 1 + backward) ----- */
+enum abft_op {
+  ABFT_OP_Q = 0, ABFT_OP_K, ABFT_OP_V, ABFT_OP_AS, ABFT_OP_CL, ABFT_OP_O,
+  ABFT_OP_DCL, ABFT_OP_DWO, ABFT_OP_DAP, ABFT_OP_DV, ABFT_OP_DQ, ABFT_OP_DK,
+  ABFT_OP_DWQ, ABFT_OP_DWK, ABFT_OP_DWV, ABFT_OP_DX, ABFT_NUM_OPS
+};
+/* extreme-value class of a located element (Sec. 2.2) */
+enum abft_kind { ABFT_KIND_NUMERIC = 0, ABFT_KIND_NEAR_INF = 1, ABFT_KIND_INF = 2,
+                 ABFT_KIND_NAN = 3, ABFT_KIND_NONE = 4 };
+/* what was done about it */
+enum abft_action { ABFT_ACT_RECOMPUTE = 0, ABFT_ACT_DELTA = 1, ABFT_ACT_RECONSTRUCT = 2,
+                   ABFT_ACT_UNCORRECTABLE = 3 };
+
+/* Coordinates (b, h, row, col) of an element of op's output:
+ *   Q K V CL dCL dV dQ dK : b, head h, token row in [0,seq), col in [0,head_dim)
+ *   AS dAP                : b, head h, query row, key col (both in [0,seq))
+ *   O dX                  : b, h = 0, token row, col in [0,hidden)
+ *   dWO dWQ dWK dWV       : b = h = 0, row in [0,hidden) (input feature),
+ *                           col in [0,hidden) (output feature of that block)
+ * For an UNCORRECTABLE event of a column vector, row is the first row of
+ * its checksum block; of a row vector, col is the first column of its block. */
+
+typedef struct {
+  int32_t batch, seq, hidden, heads; /* hidden = heads * head_dim            */
+  int32_t dtype;                     /* ABFT_BF16 | ABFT_FP32 (activation storage) */
+  int32_t causal;                    /* 1: key j > query i is masked          */
+  int32_t block_rows;                /* R: checksum block on token axes; a power
+                                        of two, 16 <= R <= 128, R | seq        */
+  float   scale;                     /* softmax scale; 0 -> 1/sqrt(head_dim)   */
+  float   t_near_inf;                /* Sec. 4.2, default 1e10 (compared as stored) */
+  float   t_correct;                 /* Sec. 4.2, default 1e5                   */
+  float   e_rel;                     /* detection bound E = e_rel * sum|v|; 0 ->
+                                        2^-4 (bf16) / 2^-13 (fp32)              */
+  uint32_t sections;                 /* ABFT_SEC_* enabled this call; a forward
+                                        whose backward is protected must have
+                                        ABFT_SEC_BWD set (it saves the checksums
+                                        the backward propagates)                */
+  uint32_t flags;                    /* ABFT_FLAG_*                             */
+} attn_abft_config;
+
+/* One injected extreme value (test-only fault injector, Sec. 5.1): element
+ * (b, h, row, col) of op's output is overwritten with `value` rounded to
+ * storage, after the output is rounded and before it is verified. */
+typedef struct { int32_t op, b, h, row, col; float value; } abft_fault;
+
+typedef struct {
+  int32_t op, b, h, row, col, kind, action, reserved;
+  float observed;                    /* the stored value that was located    */
+  float reserved2;
+} abft_event;
+
+typedef struct {
+  int32_t n_events;                  /* events appended (may exceed capacity) */
+  int32_t n_corrected;
+  int32_t n_uncorrectable;
+  int32_t capacity;                  /* set by attn_abft_report_init          */
+  int32_t overflow;                  /* 1 if events were dropped              */
+  int32_t reserved[3];
+  abft_event events[];               /* capacity entries, unordered          */
+} abft_report;
+
+/* Bytes of device workspace attn_abft_forward needs and attn_abft_backward
+ * reuses (saved Q/K/V, AP, CL, propagated checksums and backward scratch).
+ * 0 if the config is invalid. */
+size_t attn_abft_workspace_bytes(const attn_abft_config* cfg /* host */);
+
+/* Bytes of a report able to hold `capacity` events. */
+size_t attn_abft_report_bytes(int32_t capacity);
+
+/* Initialise a report (device) for `capacity` events: zero counters, set
+ * capacity. Must be called once after allocating it. */
+int attn_abft_report_init(abft_report* report, int32_t capacity, void* stream);
+
+/* Protected forward (Sec. 4.4).
+ *   X    [batch, seq, hidden]    (device, dtype)
+ *   Wqkv [hidden, 3*hidden]      (device, dtype)  Q|K|V column blocks
+ *   Wo   [hidden, hidden]        (device, dtype)
+ *   O    [batch, seq, hidden]    (device, dtype)  output
+ *   workspace (device, >= attn_abft_workspace_bytes) receives the saved
+ *   tensors; it must stay untouched until the matching backward.
+ *   faults (device) n_faults entries, may be NULL when n_faults == 0.
+ *   report (device) initialised report; reset at entry unless
+ *   ABFT_FLAG_REPORT_APPEND. */
+int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wqkv,
+                      const void* Wo, void* O, void* workspace, size_t workspace_bytes,
+                      const abft_fault* faults, int32_t n_faults, abft_report* report,
+                      void* stream);
+
+/* Protected backward (extension: every backward GEMM output gets a
+ * propagated column checksum and a column pass).
+ *   dO [batch, seq, hidden] (device, dtype); X, Wqkv, Wo as in forward;
+ *   workspace: the one the forward filled (its backward scratch is reused);
+ *   dX [batch, seq, hidden] (device, dtype); dWqkv [hidden, 3*hidden] and
+ *   dWo [hidden, hidden] (device, fp32). */
+int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* X,
+                       const void* Wqkv, const void* Wo, void* workspace,
+                       size_t workspace_bytes, void* dX, float* dWqkv, float* dWo,
+                       const abft_fault* faults, int32_t n_faults, abft_report* report,
+                       void* stream);
+
+/* Checksum encoder (Sec. 4.6, "Encoding"). A is `batch` matrices of
+ * rows x cols (element (b, i, j) at A + b*batch_stride + i*ld + j, in
+ * elements of dtype). Writes, when the pointer is not NULL,
+ *   col_chk [batch][rows/block_rows][2][cols]  unweighted and weighted
+ *           (weights 1..block_rows) sums of every column in each row block,
+ *   row_chk [batch][rows][cols/block_cols][2]  the same along rows,
+ * both fp32 (device). block_rows | rows, block_cols | cols. */
+int encode_checksums(const void* A, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,
+                     int64_t ld, int64_t batch_stride, int32_t block_rows, int32_t block_cols,
+                     float* col_chk, float* row_chk, void* stream);
+
+/* Standalone EEC-ABFT detection and correction (Sec. 4.2, 4.3) of C
+ * (device, same addressing as encode_checksums) against propagated
+ * checksums in the encode_checksums layouts. col_chk is required; with
+ * row_chk also given the column pass is followed by the row pass and the
+ * checksum refresh of Sec. 4.3. With no operands at hand, located elements
+ * are corrected from the checksums (DELTA if |d1| <= t_correct, else
+ * RECONSTRUCT); events carry op_tag, b = batch index, h = 0. t_near_inf is
+ * compared as stored in dtype; e_rel as in attn_abft_config (0 = default).
+ * The report is appended to. */
+int verify_and_correct(void* C, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,
+                       int64_t ld, int64_t batch_stride, int32_t block_rows, int32_t block_cols,
+                       float* col_chk, float* row_chk, float t_near_inf, float t_correct,
+                       float e_rel, int32_t op_tag, abft_report* report, void* stream);
+
+/* Byte offsets of the saved tensors inside the workspace (for inspection):
+ * QKV [batch, seq, 3*hidden] dtype, AP [batch, heads, seq, seq] dtype
+ * (only blocks with key block <= query block are written under a causal
+ * mask), CL [batch, seq, hidden] dtype. Returns ABFT_OK or ABFT_ERR_INVALID. */
+int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
+                                size_t* ap_offset, size_t* cl_offset);
+
+/* Human-readable text of a status code (static storage). */
+const char* attn_abft_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTN_ABFT_H */

@@ -1,0 +1,189 @@
+// Device-side helpers: storage conversions, EEC-ABFT on one vector, event
+// recording. Included by the kernel translation units only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "attn_abft.h"
+
+namespace abft {
+
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+// float -> bfloat16, round to nearest even; NaN becomes the quiet NaN 0x7FC0.
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return bf16_t(0x7fc0u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return bf16_t(u >> 16);
+}
+
+template <class T> struct Storage;
+template <> struct Storage<bf16_t> {
+  __device__ static float load(bf16_t v) { return bf2f(v); }
+  __device__ static bf16_t store(float f) { return f2bf(f); }
+  __device__ static float round(float f) { return bf2f(f2bf(f)); }
+};
+template <> struct Storage<float> {
+  __device__ static float load(float v) { return v; }
+  __device__ static float store(float f) { return f; }
+  __device__ static float round(float f) { return f; }
+};
+
+__device__ __forceinline__ bool is_finite(float x) {
+  return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
+}
+__device__ __forceinline__ bool is_nan(float x) {
+  return (__float_as_uint(x) & 0x7fffffffu) > 0x7f800000u;
+}
+__device__ __forceinline__ bool is_inf(float x) {
+  return (__float_as_uint(x) & 0x7fffffffu) == 0x7f800000u;
+}
+
+// Extreme-value class of a stored value (paper Sec. 2.2); tn is the
+// near-INF threshold as stored.
+__device__ __forceinline__ int classify(float v, float tn) {
+  if (is_nan(v)) return ABFT_KIND_NAN;
+  if (is_inf(v)) return ABFT_KIND_INF;
+  if (fabsf(v) >= tn) return ABFT_KIND_NEAR_INF;
+  return ABFT_KIND_NUMERIC;
+}
+
+// Detection rule (Sec. 2.3): flagged unless d1 is finite and |d1| <= E,
+// E = e_rel * sum|v| over finite v (+ a tiny floor).
+__device__ __forceinline__ bool flagged(float d1, float abs_sum, float e_rel) {
+  const float E = e_rel * abs_sum + 1e-30f;
+  return !(is_finite(d1) && fabsf(d1) <= E);
+}
+
+enum { EEC_CLEAN = 0, EEC_LOCATED = 1, EEC_PROPAGATED = 2 };
+struct EecResult {
+  int status;
+  int index;
+  float d1;
+};
+
+// EEC-ABFT on one vector of n stored values v[k * stride] (Sec. 4.2 cases
+// 1-4 with the mixed-type candidate sets of Sec. 4.3). c1, c2: propagated
+// unweighted and weighted (1-based weights) checksums.
+template <class T>
+__device__ EecResult eec_locate(const T* v, int stride, int n, float c1, float c2, float e_rel,
+                                float tn) {
+  float r1 = 0.f, r2 = 0.f, sa = 0.f;
+  for (int k = 0; k < n; ++k) {
+    const float x = Storage<T>::load(v[k * stride]);
+    r1 += x;
+    r2 += float(k + 1) * x;
+    if (is_finite(x)) sa += fabsf(x);
+  }
+  const float d1 = c1 - r1, d2 = c2 - r2;
+  EecResult res{EEC_CLEAN, -1, d1};
+  if (!flagged(d1, sa, e_rel)) return res;
+  const int mode = is_finite(d1) ? 1 : (is_inf(d1) ? 2 : 3);
+  int cnt = 0, idx = -1;
+  for (int k = 0; k < n; ++k) {
+    const float x = Storage<T>::load(v[k * stride]);
+    const bool fin = is_finite(x);
+    const bool nearv = fin && fabsf(x) >= tn;
+    const bool cand = mode == 1 ? nearv : (mode == 2 ? (is_inf(x) || nearv) : (!fin || nearv));
+    if (cand) { ++cnt; idx = k; }
+  }
+  res.status = EEC_PROPAGATED;
+  if (cnt >= 2) return res;
+  if (mode == 1) {
+    if (cnt == 1) {
+      if (is_finite(d2)) {
+        const float q = d2 / d1;
+        if (!(fabsf(q - float(idx + 1)) < 0.25f)) return res;
+      }
+      res.status = EEC_LOCATED;
+      res.index = idx;
+      return res;
+    }
+    if (!is_finite(d2)) return res;
+    const float q = d2 / d1;
+    if (!(q >= 0.5f && q < float(n) + 0.5f)) return res;
+    const float qi = rintf(q);
+    if (!(fabsf(q - qi) < 0.25f)) return res;
+    res.status = EEC_LOCATED;
+    res.index = int(qi) - 1;
+    return res;
+  }
+  if (cnt == 1) {
+    res.status = EEC_LOCATED;
+    res.index = idx;
+  }
+  return res;
+}
+
+// Correction from the checksums alone (Sec. 4.2): DELTA when |d1| <=
+// t_correct, otherwise RECONSTRUCT v_i = c1 - sum_{k != i} v_k.
+template <class T>
+__device__ float fix_by_checksum(const T* v, int stride, int n, int i, float c1, float d1,
+                                 float tc, int* action) {
+  if (is_finite(d1) && fabsf(d1) <= tc) {
+    *action = ABFT_ACT_DELTA;
+    return Storage<T>::load(v[i * stride]) + d1;
+  }
+  float s = 0.f;
+  for (int k = 0; k < n; ++k)
+    if (k != i) s += Storage<T>::load(v[k * stride]);
+  *action = ABFT_ACT_RECONSTRUCT;
+  return c1 - s;
+}
+
+// Unweighted and weighted sums of a vector (checksum refresh, Sec. 4.3).
+template <class T>
+__device__ void vec_checksums(const T* v, int stride, int n, float* c1, float* c2) {
+  float r1 = 0.f, r2 = 0.f;
+  for (int k = 0; k < n; ++k) {
+    const float x = Storage<T>::load(v[k * stride]);
+    r1 += x;
+    r2 += float(k + 1) * x;
+  }
+  *c1 = r1;
+  *c2 = r2;
+}
+
+template <class T>
+__device__ bool vec_flagged(const T* v, int stride, int n, float c1, float e_rel) {
+  float r1 = 0.f, sa = 0.f;
+  for (int k = 0; k < n; ++k) {
+    const float x = Storage<T>::load(v[k * stride]);
+    r1 += x;
+    if (is_finite(x)) sa += fabsf(x);
+  }
+  return flagged(c1 - r1, sa, e_rel);
+}
+
+__device__ inline void record_event(abft_report* rep, int op, int b, int h, int row, int col,
+                                    int kind, int action, float observed) {
+  if (rep == nullptr) return;
+  const int slot = atomicAdd(&rep->n_events, 1);
+  if (action == ABFT_ACT_UNCORRECTABLE)
+    atomicAdd(&rep->n_uncorrectable, 1);
+  else
+    atomicAdd(&rep->n_corrected, 1);
+  if (slot < rep->capacity) {
+    abft_event* e = &rep->events[slot];
+    e->op = op;
+    e->b = b;
+    e->h = h;
+    e->row = row;
+    e->col = col;
+    e->kind = kind;
+    e->action = action;
+    e->reserved = 0;
+    e->observed = observed;
+    e->reserved2 = 0.f;
+  } else {
+    atomicOr(&rep->overflow, 1);
+  }
+}
+
+}  // namespace abft

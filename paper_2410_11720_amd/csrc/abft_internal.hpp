@@ -1,0 +1,115 @@
+// Internal declarations shared by the kernels and the host orchestration of
+// the ABFT-protected attention layer. Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "attn_abft.h"
+
+namespace abft {
+
+enum class Layout : int { KMajor = 0, MNMajor = 1 };
+
+// How a protected GEMM maps its output element (z, m, n) to the event
+// coordinates (op, b, h, row, col) of the public ABI:
+//   op  = op_base + n / op_span,   nn = n % op_span
+//   z-batched (nb1 > 0): b = z / nb1, h = z % nb1, row = m, col = nn
+//   token-major       : b = m / rows_per_b, row = m % rows_per_b (or b = 0,
+//                       row = m when rows_per_b == 0); h = nn / head_cols,
+//                       col = nn % head_cols (or h = 0, col = nn).
+struct CoordMap {
+  int op_base = 0;
+  int op_span = 1 << 30;
+  int nb1 = 0;
+  int rows_per_b = 0;
+  int head_cols = 0;
+};
+
+// C[z](m, n) = sum_k A[z](m, k) * B[z](k, n) with z = b0 * nb1 + b1.
+// Element addresses (in elements of the storage type):
+//   A(m,k): A + b0*sA0 + b1*sA1 + (A K-major ? m*lda + k : k*lda + m)
+//   B(k,n): B + b0*sB0 + b1*sB1 + (B K-major ? n*ldb + k : k*ldb + n)
+//   C(m,n): C + b0*sC0 + b1*sC1 + m*ldc + n
+// Column-checksum side (paper Sec. 2.3 A^c, carried as extra MFMA rows):
+//   Ac(r,k) fp32, r in [0, 2M/Rm): laid out like A (K-major: r*ldac + k)
+//   Cc(r,n) fp32 optional store of the propagated C^c = A^c B
+// Row-checksum side (B^r, extra MFMA columns), for columns n >= cr_n_begin:
+//   Br(k,q) fp32, q in [0, 2(N - cr_n_begin)/Rn): laid out like B
+//   Cr(m,q) fp32 optional store of the propagated C^r = A B^r
+struct GemmDesc {
+  int M = 0, N = 0, K = 0;
+  int nb0 = 1, nb1 = 1;
+  const void* A = nullptr; int64_t lda = 0, sA0 = 0, sA1 = 0;
+  const void* B = nullptr; int64_t ldb = 0, sB0 = 0, sB1 = 0;
+  void* C = nullptr; int64_t ldc = 0, sC0 = 0, sC1 = 0;
+
+  const float* Ac = nullptr; int64_t ldac = 0, sAc0 = 0, sAc1 = 0;
+  float* Cc = nullptr; int64_t ldcc = 0, sCc0 = 0, sCc1 = 0;
+  int Rm = 128;
+
+  const float* Br = nullptr; int64_t ldbr = 0, sBr0 = 0, sBr1 = 0;
+  float* Cr = nullptr; int64_t ldcr = 0, sCr0 = 0, sCr1 = 0;
+  int Rn = 128;
+  int cr_n_begin = 0;
+
+  // 0: dense; 1: skip tiles strictly above the block diagonal (score-shaped
+  // outputs, key > query); 2: K range ends at the tile's last row (A is a
+  // masked probability matrix, keys <= query); 3: K range starts at the
+  // tile's first row (A is the transpose of such a matrix).
+  int causal = 0;
+  // 0: no verification; 1: column pass; 2: column pass, row pass and the
+  // checksum refresh of Sec. 4.3 (two-sided outputs).
+  int verify = 0;
+  int verify_n_lo = 0, verify_n_hi = 1 << 30;  // only columns in [lo, hi) are verified
+  int recompute = 1;  // correct by recomputing from A and B, else from checksums
+  float e_rel = 0.f, tn = 0.f, tc = 0.f;
+  CoordMap map;
+  const abft_fault* faults = nullptr;
+  int n_faults = 0;
+  abft_report* report = nullptr;
+};
+
+// Tile shapes the GEMM is instantiated for.
+enum class Tile : int { T256x128 = 0, T128x128 = 1, T128x64 = 2 };
+
+// Launch one protected (or, with no checksum operands, plain) GEMM.
+// dtype: ABFT_BF16 or ABFT_FP32 operands; c_fp32: output stored as fp32.
+hipError_t launch_gemm(const GemmDesc& g, int dtype, bool c_fp32, Layout la, Layout lb,
+                       Tile tile, hipStream_t stream);
+
+// Softmax over keys with checksum carry-through (fwd) and its backward.
+struct SoftmaxDesc {
+  int B = 0, nh = 0, S = 0, R = 128;
+  int causal = 0;
+  // Under a causal mask a query block's row is produced up to the end of
+  // the score-GEMM tile holding its diagonal (keys past the diagonal are
+  // written as exact zeros), so the consumers' K ranges only read written
+  // data.
+  int kv_align = 128;
+  float scale = 1.f;
+  const void* AS = nullptr;   // [B,nh,S,S] fwd input (unscaled scores)
+  void* AP = nullptr;         // [B,nh,S,S] fwd output / bwd input
+  const void* dAP = nullptr;  // [B,nh,S,S] bwd input
+  void* dAS = nullptr;        // [B,nh,S,S] bwd output
+  float* col_chk = nullptr;   // [B,nh,S/R,2,S] of the produced matrix (may be null)
+  float* row_chk = nullptr;   // [B,nh,S,S/R,2] of the produced matrix (may be null)
+};
+hipError_t launch_softmax_fwd(const SoftmaxDesc& d, int dtype, hipStream_t stream);
+hipError_t launch_softmax_bwd(const SoftmaxDesc& d, int dtype, hipStream_t stream);
+
+// Checksum encoder (public encode_checksums) and standalone verifier.
+hipError_t launch_encode(const void* A, int dtype, int64_t batch, int64_t rows, int64_t cols,
+                         int64_t ld, int64_t batch_stride, int Rb, int Cb, float* col_chk,
+                         float* row_chk, hipStream_t stream);
+hipError_t launch_verify(void* C, int dtype, int64_t batch, int64_t rows, int64_t cols,
+                         int64_t ld, int64_t batch_stride, int Rb, int Cb, float* col_chk,
+                         float* row_chk, float tn, float tc, float e_rel, int op_tag,
+                         abft_report* report, hipStream_t stream);
+hipError_t launch_report_reset(abft_report* report, int capacity, bool set_capacity,
+                               hipStream_t stream);
+
+// Threshold as the storage dtype represents it (round to nearest even).
+float stored_threshold(float t, int dtype);
+
+}  // namespace abft

@@ -1,0 +1,582 @@
+// Host orchestration of the ABFT-protected attention layer and the C ABI
+// (include/attn_abft.h).
+//
+// Forward, per the protection sections of paper Sec. 4.4:
+//   encode  W^V row checksums per head; X column checksums per R-token
+//           block and row checksums per head block (the latter for dW)
+//   S_AS    [Q|K|V] = X Wqkv with Q^c|K^c|V^c = X^c Wqkv as extra MFMA rows
+//           and V^r = X W^V r as extra MFMA columns on the V tiles; root
+//           check of Q, K, V (column pass, corrected by recompute)
+//           AS = Q K^T per head, AS^c = Q^c K^T, AS^r = Q (K^c)^T, two-sided
+//           verification (Sec. 4.3)
+//   softmax AP with column checksums AP^c (and row checksums for dV)
+//   S_CL    CL = AP V per head, CL^c = AP^c V, CL^r = AP V^r, two-sided
+//   S_O     O = CL Wo, O^c = CL^c Wo, column pass
+// Backward (extension): every GEMM output carries a propagated column
+// checksum and gets a column pass; see attn_abft_backward below.
+#include <cmath>
+#include <cstring>
+#include <mutex>
+
+#include "abft_internal.hpp"
+
+namespace abft {
+
+float stored_threshold(float t, int dtype) {
+  if (dtype == ABFT_FP32) return t;
+  uint32_t u;
+  std::memcpy(&u, &t, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return t;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  u &= 0xffff0000u;
+  float r;
+  std::memcpy(&r, &u, 4);
+  return r;
+}
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+struct Dims {
+  int64_t B, S, H, nh, d, R, nq, T;
+  size_t es;
+};
+
+struct Layout_ {
+  size_t qkv, ap, cl, as, das, dcl, dqkv;
+  size_t xc, xr, wvr, qkvc, vr, apc, apr, clc, clr, doc, dclc, dasc, dasr, dqkvc;
+  size_t total;
+};
+
+bool make_dims(const attn_abft_config* c, Dims* d) {
+  if (!c || c->batch < 1 || c->seq < 1 || c->hidden < 1 || c->heads < 1) return false;
+  if (c->hidden % c->heads) return false;
+  d->B = c->batch;
+  d->S = c->seq;
+  d->H = c->hidden;
+  d->nh = c->heads;
+  d->d = c->hidden / c->heads;
+  d->R = c->block_rows;
+  if (d->R < 1 || d->S % d->R) return false;
+  d->nq = d->S / d->R;
+  d->T = d->B * d->S;
+  d->es = c->dtype == ABFT_FP32 ? 4 : 2;
+  return true;
+}
+
+Layout_ make_layout(const Dims& d) {
+  Layout_ L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  const size_t SS = size_t(d.B) * d.nh * d.S * d.S;
+  L.qkv = take(size_t(d.T) * 3 * d.H * d.es);
+  L.ap = take(SS * d.es);
+  L.cl = take(size_t(d.T) * d.H * d.es);
+  L.as = take(SS * d.es);
+  L.das = take(SS * d.es);
+  L.dcl = take(size_t(d.T) * d.H * d.es);
+  L.dqkv = take(size_t(d.T) * 3 * d.H * d.es);
+  const size_t f = 4;
+  L.xc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.xr = take(size_t(d.T) * d.nh * 2 * f);
+  L.wvr = take(size_t(d.H) * d.nh * 2 * f);
+  L.qkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
+  L.vr = take(size_t(d.T) * d.nh * 2 * f);
+  L.apc = take(size_t(d.B) * d.nh * d.nq * 2 * d.S * f);
+  L.apr = take(size_t(d.B) * d.nh * d.S * d.nq * 2 * f);
+  L.clc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.clr = take(size_t(d.T) * d.nh * 2 * f);
+  L.doc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.dclc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.dasc = take(size_t(d.B) * d.nh * d.nq * 2 * d.S * f);
+  L.dasr = take(size_t(d.B) * d.nh * d.S * d.nq * 2 * f);
+  L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
+  L.total = off;
+  return L;
+}
+
+int validate(const attn_abft_config* c, Dims* d) {
+  if (!make_dims(c, d)) return ABFT_ERR_INVALID;
+  if (c->dtype != ABFT_BF16 && c->dtype != ABFT_FP32) return ABFT_ERR_UNSUPPORTED;
+  if (c->causal != 0 && c->causal != 1) return ABFT_ERR_INVALID;
+  const int64_t R = d->R;
+  if ((R & (R - 1)) != 0 || R > 128 || R < (c->dtype == ABFT_FP32 ? 16 : 32))
+    return ABFT_ERR_UNSUPPORTED;
+  if (d->d != 64 && d->d != 128) return ABFT_ERR_UNSUPPORTED;
+  if (d->S % 8 || d->H % 8) return ABFT_ERR_UNSUPPORTED;
+  if (d->S > 4096) return ABFT_ERR_UNSUPPORTED;  // softmax keeps a row in registers
+  if (!(c->t_near_inf >= 0.f) || !(c->t_correct >= 0.f) || !(c->e_rel >= 0.f))
+    return ABFT_ERR_INVALID;
+  return ABFT_OK;
+}
+
+int check_device() {
+  static std::mutex mu;
+  static int cached[64];
+  static bool init[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ABFT_ERR_HIP;
+  if (dev < 0 || dev >= 64) return ABFT_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!init[dev]) {
+    hipDeviceProp_t p;
+    if (hipGetDeviceProperties(&p, dev) != hipSuccess) return ABFT_ERR_HIP;
+    cached[dev] = std::strncmp(p.gcnArchName, "gfx950", 6) == 0 ? ABFT_OK : ABFT_ERR_UNSUPPORTED;
+    init[dev] = true;
+  }
+  return cached[dev];
+}
+
+struct Params {
+  float e_rel, tn, tc, scale;
+  bool prot, root, sec_as, sec_cl, sec_o, sec_bwd;
+};
+
+Params make_params(const attn_abft_config* c, const Dims& d) {
+  Params p;
+  p.e_rel = c->e_rel > 0.f ? c->e_rel : (c->dtype == ABFT_FP32 ? std::ldexp(1.f, -13)
+                                                                : std::ldexp(1.f, -4));
+  p.tn = stored_threshold(c->t_near_inf > 0.f ? c->t_near_inf : 1e10f, c->dtype);
+  p.tc = c->t_correct > 0.f ? c->t_correct : 1e5f;
+  p.scale = c->scale > 0.f ? c->scale : 1.f / std::sqrt(float(d.d));
+  p.prot = !(c->flags & ABFT_FLAG_UNPROTECTED);
+  p.root = (c->flags & ABFT_FLAG_ROOT_CHECK) != 0;
+  p.sec_as = p.prot && (c->sections & ABFT_SEC_AS);
+  p.sec_cl = p.prot && (c->sections & ABFT_SEC_CL);
+  p.sec_o = p.prot && (c->sections & ABFT_SEC_O);
+  p.sec_bwd = p.prot && (c->sections & ABFT_SEC_BWD);
+  return p;
+}
+
+// Tile for a token-major projection: the larger tile when it still yields
+// at least one full wave of workgroups and the checksum strip fits.
+Tile proj_tile(int64_t M, int64_t N, int64_t R, int num_cu, int dtype) {
+  const int64_t t256 = ((M + 255) / 256) * ((N + 127) / 128);
+  if (dtype == ABFT_BF16 && R >= 64 && t256 >= num_cu) return Tile::T256x128;
+  return Tile::T128x128;
+}
+
+int num_cus() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0;
+    hipDeviceProp_t p;
+    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&p, dev) == hipSuccess)
+      n = p.multiProcessorCount;
+    else
+      n = 256;
+  }
+  return n;
+}
+
+#define CK(x)                                          \
+  do {                                                 \
+    hipError_t e_ = (x);                               \
+    if (e_ != hipSuccess) return ABFT_ERR_HIP;         \
+  } while (0)
+
+GemmDesc base_desc(const Params& p, const abft_fault* faults, int n_faults, abft_report* rep) {
+  GemmDesc g;
+  g.e_rel = p.e_rel;
+  g.tn = p.tn;
+  g.tc = p.tc;
+  g.recompute = p.root ? 1 : 0;
+  g.faults = faults;
+  g.n_faults = n_faults;
+  g.report = rep;
+  return g;
+}
+
+}  // namespace
+}  // namespace abft
+
+using namespace abft;
+
+extern "C" {
+
+size_t attn_abft_workspace_bytes(const attn_abft_config* cfg) {
+  Dims d;
+  if (validate(cfg, &d) != ABFT_OK) return 0;
+  return make_layout(d).total;
+}
+
+size_t attn_abft_report_bytes(int32_t capacity) {
+  if (capacity < 0) return 0;
+  return sizeof(abft_report) + size_t(capacity) * sizeof(abft_event);
+}
+
+int attn_abft_report_init(abft_report* report, int32_t capacity, void* stream) {
+  if (!report || capacity < 0) return ABFT_ERR_INVALID;
+  CK(launch_report_reset(report, capacity, true, static_cast<hipStream_t>(stream)));
+  return ABFT_OK;
+}
+
+int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
+                                size_t* ap_offset, size_t* cl_offset) {
+  Dims d;
+  if (validate(cfg, &d) != ABFT_OK) return ABFT_ERR_INVALID;
+  const Layout_ L = make_layout(d);
+  if (qkv_offset) *qkv_offset = L.qkv;
+  if (ap_offset) *ap_offset = L.ap;
+  if (cl_offset) *cl_offset = L.cl;
+  return ABFT_OK;
+}
+
+int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wqkv,
+                      const void* Wo, void* O, void* workspace, size_t workspace_bytes,
+                      const abft_fault* faults, int32_t n_faults, abft_report* report,
+                      void* stream) {
+  Dims d;
+  int st = validate(cfg, &d);
+  if (st != ABFT_OK) return st;
+  if (!X || !Wqkv || !Wo || !O || !workspace || !report || n_faults < 0 ||
+      (n_faults > 0 && !faults))
+    return ABFT_ERR_INVALID;
+  const Layout_ L = make_layout(d);
+  if (workspace_bytes < L.total) return ABFT_ERR_WORKSPACE;
+  if ((st = check_device()) != ABFT_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Params p = make_params(cfg, d);
+  const int dt = cfg->dtype;
+  char* ws = static_cast<char*>(workspace);
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
+  const char* Xc = static_cast<const char*>(X);
+  const char* Wc = static_cast<const char*>(Wqkv);
+  const int64_t B = d.B, S = d.S, H = d.H, nh = d.nh, hd = d.d, R = d.R, nq = d.nq, T = d.T;
+  const size_t es = d.es;
+  const int ncu = num_cus();
+
+  if (!(cfg->flags & ABFT_FLAG_REPORT_APPEND)) CK(launch_report_reset(report, 0, false, s));
+
+  // Checksum operands, each computed when any enabled section consumes it
+  // (the backward's propagated checksums come from the forward: X^r for dW,
+  // AP^r for dV, CL^r for dWo; a forward that precedes a protected backward
+  // must have ABFT_SEC_BWD set).
+  const bool need_xc = p.sec_as || (p.root && p.sec_cl);  // Q^c, K^c; V root check
+  const bool need_vr = p.sec_cl || p.sec_bwd;             // V^r -> CL^r
+  const bool need_apc = p.sec_cl || p.sec_o;              // AP^c -> CL^c -> O^c
+  // encode (Sec. 4.6): W^V row checksums per head; X column and row checksums
+  if (need_vr)
+    CK(launch_encode(Wc + 2 * H * es, dt, 1, H, H, 3 * H, 0, int(H), int(hd), nullptr,
+                     F(L.wvr), s));
+  if (need_xc || p.sec_bwd)
+    CK(launch_encode(X, dt, B, S, H, H, S * H, int(R), int(hd), need_xc ? F(L.xc) : nullptr,
+                     p.sec_bwd ? F(L.xr) : nullptr, s));
+
+  // [Q|K|V] = X Wqkv
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(T); g.N = int(3 * H); g.K = int(H);
+    g.A = X; g.lda = H;
+    g.B = Wqkv; g.ldb = 3 * H;
+    g.C = ws + L.qkv; g.ldc = 3 * H;
+    if (need_xc) {
+      g.Ac = F(L.xc); g.ldac = H; g.Rm = int(R);
+      g.Cc = F(L.qkvc); g.ldcc = 3 * H;
+    }
+    if (need_vr) {
+      g.Br = F(L.wvr); g.ldbr = 2 * nh; g.Rn = int(hd); g.cr_n_begin = int(2 * H);
+      g.Cr = F(L.vr); g.ldcr = 2 * nh;
+    }
+    if (p.root && (p.sec_as || p.sec_cl)) {
+      g.verify = 1;
+      g.verify_n_lo = p.sec_as ? 0 : int(2 * H);
+      g.verify_n_hi = p.sec_cl ? int(3 * H) : int(2 * H);
+    }
+    g.map.op_base = ABFT_OP_Q; g.map.op_span = int(H); g.map.rows_per_b = int(S);
+    g.map.head_cols = int(hd);
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(T, 3 * H, R, ncu, dt), s));
+  }
+  // AS = Q K^T per head (unscaled, before the mask), two-sided checksums
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(S); g.N = int(S); g.K = int(hd);
+    g.nb0 = int(B); g.nb1 = int(nh);
+    g.A = ws + L.qkv; g.lda = 3 * H; g.sA0 = S * 3 * H; g.sA1 = hd;
+    g.B = ws + L.qkv + H * es; g.ldb = 3 * H; g.sB0 = S * 3 * H; g.sB1 = hd;
+    g.C = ws + L.as; g.ldc = S; g.sC0 = nh * S * S; g.sC1 = S * S;
+    if (p.sec_as) {
+      g.Ac = F(L.qkvc); g.ldac = 3 * H; g.sAc0 = nq * 2 * 3 * H; g.sAc1 = hd; g.Rm = int(R);
+      g.Br = F(L.qkvc) + H; g.ldbr = 3 * H; g.sBr0 = nq * 2 * 3 * H; g.sBr1 = hd; g.Rn = int(R);
+      g.verify = 2;
+    }
+    g.causal = cfg->causal ? 1 : 0;
+    g.map.op_base = ABFT_OP_AS; g.map.nb1 = int(nh);
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, Tile::T128x128, s));
+  }
+  // AP = softmax(scale * AS) with column (and row) checksums
+  {
+    SoftmaxDesc sd;
+    sd.B = int(B); sd.nh = int(nh); sd.S = int(S); sd.R = int(R); sd.causal = cfg->causal;
+    sd.kv_align = 128;
+    sd.scale = p.scale;
+    sd.AS = ws + L.as; sd.AP = ws + L.ap;
+    sd.col_chk = need_apc ? F(L.apc) : nullptr;
+    sd.row_chk = p.sec_bwd ? F(L.apr) : nullptr;
+    CK(launch_softmax_fwd(sd, dt, s));
+  }
+  // CL = AP V per head, CL^c = AP^c V, CL^r = AP V^r
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(S); g.N = int(hd); g.K = int(S);
+    g.nb0 = int(B); g.nb1 = int(nh);
+    g.A = ws + L.ap; g.lda = S; g.sA0 = nh * S * S; g.sA1 = S * S;
+    g.B = ws + L.qkv + 2 * H * es; g.ldb = 3 * H; g.sB0 = S * 3 * H; g.sB1 = hd;
+    g.C = ws + L.cl; g.ldc = H; g.sC0 = S * H; g.sC1 = hd;
+    if (need_apc) {
+      g.Ac = F(L.apc); g.ldac = S; g.sAc0 = nh * nq * 2 * S; g.sAc1 = nq * 2 * S; g.Rm = int(R);
+      g.Cc = F(L.clc); g.ldcc = H; g.sCc0 = nq * 2 * H; g.sCc1 = hd;
+    }
+    if (need_vr) {
+      g.Br = F(L.vr); g.ldbr = 2 * nh; g.sBr0 = S * 2 * nh; g.sBr1 = 2; g.Rn = int(hd);
+      g.Cr = F(L.clr); g.ldcr = 2 * nh; g.sCr0 = S * 2 * nh; g.sCr1 = 2;
+    }
+    if (p.sec_cl) g.verify = 2;
+    g.causal = cfg->causal ? 2 : 0;
+    g.map.op_base = ABFT_OP_CL; g.map.nb1 = int(nh);
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor,
+                   hd == 64 ? Tile::T128x64 : Tile::T128x128, s));
+  }
+  // O = CL Wo, O^c = CL^c Wo
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(T); g.N = int(H); g.K = int(H);
+    g.A = ws + L.cl; g.lda = H;
+    g.B = Wo; g.ldb = H;
+    g.C = O; g.ldc = H;
+    if (p.sec_o) {
+      g.Ac = F(L.clc); g.ldac = H; g.Rm = int(R);
+      g.verify = 1;
+    }
+    g.map.op_base = ABFT_OP_O; g.map.rows_per_b = int(S);
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(T, H, R, ncu, dt), s));
+  }
+  return ABFT_OK;
+}
+
+int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* X,
+                       const void* Wqkv, const void* Wo, void* workspace,
+                       size_t workspace_bytes, void* dX, float* dWqkv, float* dWo,
+                       const abft_fault* faults, int32_t n_faults, abft_report* report,
+                       void* stream) {
+  Dims d;
+  int st = validate(cfg, &d);
+  if (st != ABFT_OK) return st;
+  if (!dO || !X || !Wqkv || !Wo || !workspace || !dX || !dWqkv || !dWo || !report ||
+      n_faults < 0 || (n_faults > 0 && !faults))
+    return ABFT_ERR_INVALID;
+  const Layout_ L = make_layout(d);
+  if (workspace_bytes < L.total) return ABFT_ERR_WORKSPACE;
+  if ((st = check_device()) != ABFT_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Params p = make_params(cfg, d);
+  const int dt = cfg->dtype;
+  char* ws = static_cast<char*>(workspace);
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
+  const int64_t B = d.B, S = d.S, H = d.H, nh = d.nh, hd = d.d, R = d.R, nq = d.nq, T = d.T;
+  const size_t es = d.es;
+  const bool pb = p.sec_bwd;
+  const int ncu = num_cus();
+
+  if (!(cfg->flags & ABFT_FLAG_REPORT_APPEND)) CK(launch_report_reset(report, 0, false, s));
+  if (pb) CK(launch_encode(dO, dt, B, S, H, H, S * H, int(R), int(hd), F(L.doc), nullptr, s));
+
+  // dCL = dO Wo^T, dCL^c = dO^c Wo^T
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(T); g.N = int(H); g.K = int(H);
+    g.A = dO; g.lda = H;
+    g.B = Wo; g.ldb = H;
+    g.C = ws + L.dcl; g.ldc = H;
+    if (pb) {
+      g.Ac = F(L.doc); g.ldac = H; g.Rm = int(R);
+      g.Cc = F(L.dclc); g.ldcc = H;
+      g.verify = 1;
+    }
+    g.map.op_base = ABFT_OP_DCL; g.map.rows_per_b = int(S); g.map.head_cols = int(hd);
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(T, H, R, ncu, dt), s));
+  }
+  // dWo = CL^T dO, column checksums over head blocks of rows from CL^r
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(H); g.N = int(H); g.K = int(T);
+    g.A = ws + L.cl; g.lda = H;
+    g.B = dO; g.ldb = H;
+    g.C = dWo; g.ldc = H;
+    if (pb) {
+      g.Ac = F(L.clr); g.ldac = 2 * nh; g.Rm = int(hd);
+      g.verify = 1;
+    }
+    g.map.op_base = ABFT_OP_DWO;
+    CK(launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s));
+  }
+  // dAP = dCL_h V_h^T, dAP^c = dCL_h^c V_h^T
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(S); g.N = int(S); g.K = int(hd);
+    g.nb0 = int(B); g.nb1 = int(nh);
+    g.A = ws + L.dcl; g.lda = H; g.sA0 = S * H; g.sA1 = hd;
+    g.B = ws + L.qkv + 2 * H * es; g.ldb = 3 * H; g.sB0 = S * 3 * H; g.sB1 = hd;
+    g.C = ws + L.as; g.ldc = S; g.sC0 = nh * S * S; g.sC1 = S * S;
+    if (pb) {
+      g.Ac = F(L.dclc); g.ldac = H; g.sAc0 = nq * 2 * H; g.sAc1 = hd; g.Rm = int(R);
+      g.verify = 1;
+    }
+    g.causal = cfg->causal ? 1 : 0;
+    g.map.op_base = ABFT_OP_DAP; g.map.nb1 = int(nh);
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, Tile::T128x128, s));
+  }
+  const Tile td = hd == 64 ? Tile::T128x64 : Tile::T128x128;
+  // dV = AP^T dCL_h, column checksums over key blocks from AP^r
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(S); g.N = int(hd); g.K = int(S);
+    g.nb0 = int(B); g.nb1 = int(nh);
+    g.A = ws + L.ap; g.lda = S; g.sA0 = nh * S * S; g.sA1 = S * S;
+    g.B = ws + L.dcl; g.ldb = H; g.sB0 = S * H; g.sB1 = hd;
+    g.C = ws + L.dqkv + 2 * H * es; g.ldc = 3 * H; g.sC0 = S * 3 * H; g.sC1 = hd;
+    if (pb) {
+      g.Ac = F(L.apr); g.ldac = nq * 2; g.sAc0 = nh * S * nq * 2; g.sAc1 = S * nq * 2;
+      g.Rm = int(R);
+      g.Cc = F(L.dqkvc) + 2 * H; g.ldcc = 3 * H; g.sCc0 = nq * 2 * 3 * H; g.sCc1 = hd;
+      g.verify = 1;
+    }
+    g.causal = cfg->causal ? 3 : 0;
+    g.map.op_base = ABFT_OP_DV; g.map.nb1 = int(nh);
+    CK(launch_gemm(g, dt, false, Layout::MNMajor, Layout::MNMajor, td, s));
+  }
+  // dAS = scale * AP * (dAP - rowdot), with column and row checksums
+  {
+    SoftmaxDesc sd;
+    sd.B = int(B); sd.nh = int(nh); sd.S = int(S); sd.R = int(R); sd.causal = cfg->causal;
+    sd.kv_align = 128;
+    sd.scale = p.scale;
+    sd.AP = ws + L.ap; sd.dAP = ws + L.as; sd.dAS = ws + L.das;
+    sd.col_chk = pb ? F(L.dasc) : nullptr;
+    sd.row_chk = pb ? F(L.dasr) : nullptr;
+    CK(launch_softmax_bwd(sd, dt, s));
+  }
+  // dQ = dAS K_h, dQ^c = dAS^c K_h
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(S); g.N = int(hd); g.K = int(S);
+    g.nb0 = int(B); g.nb1 = int(nh);
+    g.A = ws + L.das; g.lda = S; g.sA0 = nh * S * S; g.sA1 = S * S;
+    g.B = ws + L.qkv + H * es; g.ldb = 3 * H; g.sB0 = S * 3 * H; g.sB1 = hd;
+    g.C = ws + L.dqkv; g.ldc = 3 * H; g.sC0 = S * 3 * H; g.sC1 = hd;
+    if (pb) {
+      g.Ac = F(L.dasc); g.ldac = S; g.sAc0 = nh * nq * 2 * S; g.sAc1 = nq * 2 * S; g.Rm = int(R);
+      g.Cc = F(L.dqkvc); g.ldcc = 3 * H; g.sCc0 = nq * 2 * 3 * H; g.sCc1 = hd;
+      g.verify = 1;
+    }
+    g.causal = cfg->causal ? 2 : 0;
+    g.map.op_base = ABFT_OP_DQ; g.map.nb1 = int(nh);
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, td, s));
+  }
+  // dK = dAS^T Q_h, column checksums over key blocks from dAS^r
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(S); g.N = int(hd); g.K = int(S);
+    g.nb0 = int(B); g.nb1 = int(nh);
+    g.A = ws + L.das; g.lda = S; g.sA0 = nh * S * S; g.sA1 = S * S;
+    g.B = ws + L.qkv; g.ldb = 3 * H; g.sB0 = S * 3 * H; g.sB1 = hd;
+    g.C = ws + L.dqkv + H * es; g.ldc = 3 * H; g.sC0 = S * 3 * H; g.sC1 = hd;
+    if (pb) {
+      g.Ac = F(L.dasr); g.ldac = nq * 2; g.sAc0 = nh * S * nq * 2; g.sAc1 = S * nq * 2;
+      g.Rm = int(R);
+      g.Cc = F(L.dqkvc) + H; g.ldcc = 3 * H; g.sCc0 = nq * 2 * 3 * H; g.sCc1 = hd;
+      g.verify = 1;
+    }
+    g.causal = cfg->causal ? 3 : 0;
+    g.map.op_base = ABFT_OP_DK; g.map.nb1 = int(nh);
+    CK(launch_gemm(g, dt, false, Layout::MNMajor, Layout::MNMajor, td, s));
+  }
+  // dWqkv = X^T dQKV, column checksums over head blocks of rows from X^r
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(H); g.N = int(3 * H); g.K = int(T);
+    g.A = X; g.lda = H;
+    g.B = ws + L.dqkv; g.ldb = 3 * H;
+    g.C = dWqkv; g.ldc = 3 * H;
+    if (pb) {
+      g.Ac = F(L.xr); g.ldac = 2 * nh; g.Rm = int(hd);
+      g.verify = 1;
+    }
+    g.map.op_base = ABFT_OP_DWQ; g.map.op_span = int(H);
+    CK(launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s));
+  }
+  // dX = dQKV Wqkv^T, dX^c = dQKV^c Wqkv^T
+  {
+    GemmDesc g = base_desc(p, faults, n_faults, report);
+    g.M = int(T); g.N = int(H); g.K = int(3 * H);
+    g.A = ws + L.dqkv; g.lda = 3 * H;
+    g.B = Wqkv; g.ldb = 3 * H;
+    g.C = dX; g.ldc = H;
+    if (pb) {
+      g.Ac = F(L.dqkvc); g.ldac = 3 * H; g.Rm = int(R);
+      g.verify = 1;
+    }
+    g.map.op_base = ABFT_OP_DX; g.map.rows_per_b = int(S);
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(T, H, R, ncu, dt), s));
+  }
+  return ABFT_OK;
+}
+
+int encode_checksums(const void* A, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,
+                     int64_t ld, int64_t batch_stride, int32_t block_rows, int32_t block_cols,
+                     float* col_chk, float* row_chk, void* stream) {
+  if (!A || batch < 0 || rows < 0 || cols < 0 || ld < cols) return ABFT_ERR_INVALID;
+  if (dtype != ABFT_BF16 && dtype != ABFT_FP32) return ABFT_ERR_UNSUPPORTED;
+  if (col_chk && (block_rows < 1 || rows % block_rows)) return ABFT_ERR_INVALID;
+  if (row_chk && (block_cols < 1 || cols % block_cols)) return ABFT_ERR_INVALID;
+  if (!col_chk && !row_chk) return ABFT_OK;
+  int st = check_device();
+  if (st != ABFT_OK) return st;
+  const int Rb = col_chk ? block_rows : int(rows > 0 ? rows : 1);
+  CK(launch_encode(A, dtype, batch, rows, cols, ld, batch_stride, Rb, block_cols, col_chk, row_chk,
+                   static_cast<hipStream_t>(stream)));
+  return ABFT_OK;
+}
+
+int verify_and_correct(void* C, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,
+                       int64_t ld, int64_t batch_stride, int32_t block_rows, int32_t block_cols,
+                       float* col_chk, float* row_chk, float t_near_inf, float t_correct,
+                       float e_rel, int32_t op_tag, abft_report* report, void* stream) {
+  if (!C || !col_chk || !report || batch < 0 || rows < 0 || cols < 0 || ld < cols)
+    return ABFT_ERR_INVALID;
+  if (dtype != ABFT_BF16 && dtype != ABFT_FP32) return ABFT_ERR_UNSUPPORTED;
+  if (block_rows < 1 || rows % block_rows) return ABFT_ERR_INVALID;
+  if (row_chk && (block_cols < 1 || cols % block_cols)) return ABFT_ERR_INVALID;
+  if (!(t_near_inf >= 0.f) || !(t_correct >= 0.f) || !(e_rel >= 0.f)) return ABFT_ERR_INVALID;
+  if (size_t(block_rows) * (row_chk ? cols / block_cols : 0) + (row_chk ? cols : 0) >
+      size_t(150 * 1024 / 4))
+    return ABFT_ERR_UNSUPPORTED;
+  int st = check_device();
+  if (st != ABFT_OK) return st;
+  const float er = e_rel > 0.f ? e_rel : (dtype == ABFT_FP32 ? std::ldexp(1.f, -13)
+                                                              : std::ldexp(1.f, -4));
+  const float tn = stored_threshold(t_near_inf > 0.f ? t_near_inf : 1e10f, dtype);
+  const float tc = t_correct > 0.f ? t_correct : 1e5f;
+  CK(launch_verify(C, dtype, batch, rows, cols, ld, batch_stride, block_rows, block_cols, col_chk,
+                   row_chk, tn, tc, er, op_tag, report, static_cast<hipStream_t>(stream)));
+  return ABFT_OK;
+}
+
+const char* attn_abft_strerror(int status) {
+  switch (status) {
+    case ABFT_OK: return "ok";
+    case ABFT_ERR_INVALID: return "invalid argument";
+    case ABFT_ERR_UNSUPPORTED: return "unsupported configuration or device";
+    case ABFT_ERR_HIP: return "HIP launch error";
+    case ABFT_ERR_WORKSPACE: return "workspace too small";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,301 @@
+// Checksum encoder (paper Sec. 4.6 "Encoding") and the standalone EEC-ABFT
+// verifier (Sec. 4.2, 4.3) behind encode_checksums / verify_and_correct.
+//
+// Encoder: one workgroup owns an Rb-row block of one batch matrix and a
+// slab of columns; a thread owns 16-byte column chunks (coalesced row
+// reads) and accumulates the column checksums of its chunk in registers;
+// row checksums of each Cb-column block are reduced across the lanes that
+// hold the block. The whole operand is read exactly once.
+//
+// Verifier: one workgroup per (batch, Rb-row block); one thread per vector
+// (the paper's Fig. 4 thread-per-vector mapping); a clean block costs one
+// coalesced read. Corrections use the checksums only (DELTA or
+// RECONSTRUCT), since no operands are at hand.
+#include "abft_internal.hpp"
+#include "abft_device.hpp"
+
+namespace abft {
+namespace {
+
+constexpr int NT = 256;
+
+template <class T, int V>
+__device__ __forceinline__ void load_vec(const T* p, float* out) {
+  if constexpr (V == 8 && sizeof(T) == 2) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      out[2 * q] = __uint_as_float(w[q] << 16);
+      out[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+    }
+  } else if constexpr (V == 4 && sizeof(T) == 4) {
+    const float4 v = *reinterpret_cast<const float4*>(p);
+    out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < V; ++e) out[e] = Storage<T>::load(p[e]);
+  }
+}
+
+__device__ __forceinline__ float group_sum(float x, int width) {
+  for (int o = 1; o < width; o <<= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// grid: (ceil(cols / (NT*V)), rows/Rb, batch). Row checksums are produced
+// here only when Cb/V lanes form an aligned group of at most 64.
+template <class T, int V>
+__global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, int64_t cols,
+                                                    int64_t ld, int64_t bstride, int Rb, int Cb,
+                                                    float* col_chk, float* row_chk) {
+  const int tid = threadIdx.x;
+  const int64_t b = blockIdx.z;
+  const int64_t rb = blockIdx.y;
+  const int64_t c0 = (int64_t(blockIdx.x) * NT + tid) * V;
+  const bool live = c0 < cols;
+  const T* base = A + b * bstride;
+  const int lanes = Cb / V;
+  float c1[V], c2[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) c1[e] = c2[e] = 0.f;
+  for (int r = 0; r < Rb; ++r) {
+    const int64_t row = rb * Rb + r;
+    float x[V];
+    if (live) load_vec<T, V>(base + row * ld + c0, x);
+    else {
+#pragma unroll
+      for (int e = 0; e < V; ++e) x[e] = 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      c1[e] += x[e];
+      c2[e] += float(r + 1) * x[e];
+    }
+    if (row_chk != nullptr) {
+      float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        s1 += x[e];
+        s2 += float(((c0 + e) % Cb) + 1) * x[e];
+      }
+      s1 = group_sum(s1, lanes);
+      s2 = group_sum(s2, lanes);
+      if (live && (c0 % Cb) == 0) {
+        float* rc = row_chk + ((b * rows + row) * (cols / Cb) + c0 / Cb) * 2;
+        rc[0] = s1;
+        rc[1] = s2;
+      }
+    }
+  }
+  if (col_chk != nullptr && live) {
+    float* cc = col_chk + ((b * (rows / Rb) + rb) * 2) * cols;
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      cc[c0 + e] = c1[e];
+      cc[cols + c0 + e] = c2[e];
+    }
+  }
+}
+
+// Row checksums for block widths the lane-group reduction cannot cover:
+// one thread per (row, block), sequential sums.
+template <class T>
+__global__ __launch_bounds__(NT) void row_chk_kernel(const T* A, int64_t batch, int64_t rows,
+                                                     int64_t cols, int64_t ld, int64_t bstride,
+                                                     int Cb, float* row_chk) {
+  const int64_t nb = cols / Cb;
+  const int64_t idx = int64_t(blockIdx.x) * NT + threadIdx.x;
+  if (idx >= batch * rows * nb) return;
+  const int64_t cb = idx % nb, row = (idx / nb) % rows, b = idx / (nb * rows);
+  const T* p = A + b * bstride + row * ld + cb * Cb;
+  float s1 = 0.f, s2 = 0.f;
+  for (int k = 0; k < Cb; ++k) {
+    const float x = Storage<T>::load(p[k]);
+    s1 += x;
+    s2 += float(k + 1) * x;
+  }
+  row_chk[idx * 2] = s1;
+  row_chk[idx * 2 + 1] = s2;
+}
+
+template <class T>
+hipError_t encode_t(const T* A, int64_t batch, int64_t rows, int64_t cols, int64_t ld,
+                    int64_t bs, int Rb, int Cb, float* col_chk, float* row_chk, hipStream_t s) {
+  constexpr int VV = 16 / sizeof(T);
+  const bool aligned = (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (ld % VV == 0) &&
+                       (cols % VV == 0) && (bs % VV == 0);
+  const bool vec = aligned && (!row_chk || (Cb % VV == 0 && Cb / VV <= 64 &&
+                                            ((Cb / VV) & (Cb / VV - 1)) == 0));
+  const bool scal_rows = row_chk && (Cb > 64 || (Cb & (Cb - 1)) != 0);
+  float* rc_inline = scal_rows ? nullptr : row_chk;
+  if (col_chk != nullptr || rc_inline != nullptr) {
+    if (vec) {
+      dim3 grid((cols + NT * VV - 1) / (NT * VV), rows / Rb, batch);
+      hipLaunchKernelGGL((encode_kernel<T, VV>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs, Rb,
+                         Cb, col_chk, rc_inline);
+    } else {
+      dim3 grid((cols + NT - 1) / NT, rows / Rb, batch);
+      hipLaunchKernelGGL((encode_kernel<T, 1>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs, Rb,
+                         Cb, col_chk, rc_inline);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (scal_rows) {
+    const int64_t n = batch * rows * (cols / Cb);
+    hipLaunchKernelGGL((row_chk_kernel<T>), dim3((n + NT - 1) / NT), dim3(NT), 0, s, A, batch,
+                       rows, cols, ld, bs, Cb, row_chk);
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
+// ---- standalone verify-and-correct ---------------------------------------
+
+// Global-memory reads in the verifier must observe corrections made by
+// other threads of the workgroup: they go through the device-coherent
+// level after a workgroup barrier with a device-scope fence.
+__device__ __forceinline__ void wg_sync_global() {
+  __threadfence();
+  __syncthreads();
+  __threadfence();
+}
+
+template <class T>
+__global__ __launch_bounds__(NT) void verify_kernel(T* C, int64_t rows, int64_t cols, int64_t ld,
+                                                    int64_t bstride, int Rb, int Cb,
+                                                    float* col_chk, float* row_chk, float tn,
+                                                    float tc, float e_rel, int op_tag,
+                                                    abft_report* rep) {
+  extern __shared__ __align__(16) char smem[];
+  int* rowcnt = reinterpret_cast<int*>(smem);          // [Rb][cols/Cb]
+  const int64_t b = blockIdx.y, rb = blockIdx.x;
+  const int64_t nrb = row_chk ? cols / Cb : 0;
+  int* colcnt = rowcnt + Rb * nrb;                     // [cols]
+  T* M = C + b * bstride + rb * Rb * ld;
+  float* cc = col_chk + ((b * (rows / Rb) + rb) * 2) * cols;
+  float* rc = row_chk ? row_chk + (b * rows + rb * Rb) * nrb * 2 : nullptr;
+  const int tid = threadIdx.x;
+  for (int64_t e = tid; e < Rb * nrb + (row_chk ? cols : 0); e += NT) rowcnt[e] = 0;
+
+  // quick clean check: any flagged vector?
+  bool my = false;
+  for (int64_t n = tid; n < cols; n += NT)
+    my |= vec_flagged<T>(M + n, int(ld), Rb, cc[n], e_rel);
+  if (row_chk)
+    for (int64_t u = tid; u < Rb * nrb; u += NT)
+      my |= vec_flagged<T>(M + (u / nrb) * ld + (u % nrb) * Cb, 1, Cb, rc[u * 2], e_rel);
+  if (!__syncthreads_or(my)) return;
+
+  auto fix = [&](T* vec, int stride, int n, int idx, float c1, float d1, int row, int col) {
+    const float old = Storage<T>::load(vec[idx * stride]);
+    int action;
+    const float val = fix_by_checksum<T>(vec, stride, n, idx, c1, d1, tc, &action);
+    vec[idx * stride] = Storage<T>::store(val);
+    record_event(rep, op_tag, int(b), 0, row, col, classify(old, tn), action, old);
+  };
+  // 1. column pass
+  for (int64_t n = tid; n < cols; n += NT) {
+    T* vec = M + n;
+    const EecResult r = eec_locate<T>(vec, int(ld), Rb, cc[n], cc[cols + n], e_rel, tn);
+    if (r.status == EEC_LOCATED) {
+      fix(vec, int(ld), Rb, r.index, cc[n], r.d1, int(rb * Rb + r.index), int(n));
+      if (row_chk) atomicAdd(&rowcnt[r.index * nrb + n / Cb], 1);
+    }
+  }
+  wg_sync_global();
+  if (row_chk) {
+    // 2a. refresh row checksums of 1R-corrected row vectors
+    for (int64_t u = tid; u < Rb * nrb; u += NT)
+      if (rowcnt[u] >= 2)
+        vec_checksums<T>(M + (u / nrb) * ld + (u % nrb) * Cb, 1, Cb, &rc[u * 2], &rc[u * 2 + 1]);
+    wg_sync_global();
+    // 2b. row pass
+    for (int64_t u = tid; u < Rb * nrb; u += NT) {
+      const int64_t row = u / nrb, cb = u % nrb;
+      T* vec = M + row * ld + cb * Cb;
+      const EecResult r = eec_locate<T>(vec, 1, Cb, rc[u * 2], rc[u * 2 + 1], e_rel, tn);
+      if (r.status == EEC_LOCATED) {
+        fix(vec, 1, Cb, r.index, rc[u * 2], r.d1, int(rb * Rb + row), int(cb * Cb + r.index));
+        atomicAdd(&colcnt[cb * Cb + r.index], 1);
+      }
+    }
+    wg_sync_global();
+    // 2c. refresh column checksums of 1C-corrected column vectors
+    for (int64_t n = tid; n < cols; n += NT)
+      if (colcnt[n] >= 2) vec_checksums<T>(M + n, int(ld), Rb, &cc[n], &cc[cols + n]);
+    wg_sync_global();
+  }
+  // 3. final check
+  for (int64_t n = tid; n < cols; n += NT)
+    if (vec_flagged<T>(M + n, int(ld), Rb, cc[n], e_rel))
+      record_event(rep, op_tag, int(b), 0, int(rb * Rb), int(n), ABFT_KIND_NONE,
+                   ABFT_ACT_UNCORRECTABLE, 0.f);
+  if (row_chk)
+    for (int64_t u = tid; u < Rb * nrb; u += NT)
+      if (vec_flagged<T>(M + (u / nrb) * ld + (u % nrb) * Cb, 1, Cb, rc[u * 2], e_rel))
+        record_event(rep, op_tag, int(b), 0, int(rb * Rb + u / nrb), int((u % nrb) * Cb),
+                     ABFT_KIND_NONE, ABFT_ACT_UNCORRECTABLE, 0.f);
+}
+
+__global__ void report_reset_kernel(abft_report* rep, int capacity, int set_capacity) {
+  if (threadIdx.x == 0) {
+    rep->n_events = 0;
+    rep->n_corrected = 0;
+    rep->n_uncorrectable = 0;
+    rep->overflow = 0;
+    if (set_capacity) {
+      rep->capacity = capacity;
+      rep->reserved[0] = rep->reserved[1] = rep->reserved[2] = 0;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_encode(const void* A, int dtype, int64_t batch, int64_t rows, int64_t cols,
+                         int64_t ld, int64_t batch_stride, int Rb, int Cb, float* col_chk,
+                         float* row_chk, hipStream_t s) {
+  if (batch == 0 || rows == 0 || cols == 0) return hipSuccess;
+  if (dtype == ABFT_FP32)
+    return encode_t<float>(static_cast<const float*>(A), batch, rows, cols, ld, batch_stride, Rb,
+                           Cb, col_chk, row_chk, s);
+  return encode_t<bf16_t>(static_cast<const bf16_t*>(A), batch, rows, cols, ld, batch_stride, Rb,
+                          Cb, col_chk, row_chk, s);
+}
+
+hipError_t launch_verify(void* C, int dtype, int64_t batch, int64_t rows, int64_t cols,
+                         int64_t ld, int64_t batch_stride, int Rb, int Cb, float* col_chk,
+                         float* row_chk, float tn, float tc, float e_rel, int op_tag,
+                         abft_report* report, hipStream_t s) {
+  if (batch == 0 || rows == 0 || cols == 0) return hipSuccess;
+  const int64_t nrb = row_chk ? cols / Cb : 0;
+  const size_t lds = size_t(Rb * nrb + (row_chk ? cols : 0)) * sizeof(int);
+  dim3 grid(rows / Rb, batch);
+  if (dtype == ABFT_FP32) {
+    auto k = verify_kernel<float>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, grid, dim3(NT), lds, s, static_cast<float*>(C), rows, cols, ld,
+                       batch_stride, Rb, Cb, col_chk, row_chk, tn, tc, e_rel, op_tag, report);
+  } else {
+    auto k = verify_kernel<bf16_t>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, grid, dim3(NT), lds, s, static_cast<bf16_t*>(C), rows, cols, ld,
+                       batch_stride, Rb, Cb, col_chk, row_chk, tn, tc, e_rel, op_tag, report);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_report_reset(abft_report* report, int capacity, bool set_capacity,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(report_reset_kernel, dim3(1), dim3(64), 0, s, report, capacity,
+                     set_capacity ? 1 : 0);
+  return hipGetLastError();
+}
+
+}  // namespace abft
