@@ -165,6 +165,40 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
                        const abft_fault* faults, int32_t n_faults, abft_report* report,
                        void* stream);
 
+/* Stages of the chains, for profiling one kernel at a time with
+ * attn_abft_forward_stages / attn_abft_backward_stages. */
+#define ABFT_STAGE_ENCODE      0x001u  /* checksum encoders (fwd: W^V, X; bwd: dO) */
+#define ABFT_STAGE_QKV         0x002u  /* fwd: [Q|K|V] = X Wqkv                     */
+#define ABFT_STAGE_SCORE       0x004u  /* fwd: AS = Q K^T                           */
+#define ABFT_STAGE_SOFTMAX     0x008u  /* fwd: AP = softmax(scale AS)               */
+#define ABFT_STAGE_CONTEXT     0x010u  /* fwd: CL = AP V                            */
+#define ABFT_STAGE_OUT         0x020u  /* fwd: O = CL Wo                            */
+#define ABFT_STAGE_DCL         0x002u  /* bwd: dCL = dO Wo^T                        */
+#define ABFT_STAGE_DWO         0x004u  /* bwd: dWo = CL^T dO                        */
+#define ABFT_STAGE_DAP         0x008u  /* bwd: dAP = dCL V^T                        */
+#define ABFT_STAGE_DV          0x010u  /* bwd: dV = AP^T dCL                        */
+#define ABFT_STAGE_SOFTMAX_BWD 0x020u  /* bwd: dAS = scale AP (dAP - rowdot)        */
+#define ABFT_STAGE_DQ          0x040u  /* bwd: dQ = dAS K                           */
+#define ABFT_STAGE_DK          0x080u  /* bwd: dK = dAS^T Q                         */
+#define ABFT_STAGE_DWQKV       0x100u  /* bwd: dWqkv = X^T [dQ|dK|dV]               */
+#define ABFT_STAGE_DX          0x200u  /* bwd: dX = [dQ|dK|dV] Wqkv^T               */
+#define ABFT_STAGE_ALL         0x3ffu
+
+/* attn_abft_forward / attn_abft_backward restricted to the stages in the
+ * mask (profiling). A stage reads what earlier stages left in the
+ * workspace, so a full call on the same workspace must come first; the
+ * report is reset at entry unless ABFT_FLAG_REPORT_APPEND. Arguments and
+ * errors as for the full calls. */
+int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const void* Wqkv,
+                             const void* Wo, void* O, void* workspace, size_t workspace_bytes,
+                             const abft_fault* faults, int32_t n_faults, abft_report* report,
+                             uint32_t stages, void* stream);
+int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const void* X,
+                              const void* Wqkv, const void* Wo, void* workspace,
+                              size_t workspace_bytes, void* dX, float* dWqkv, float* dWo,
+                              const abft_fault* faults, int32_t n_faults, abft_report* report,
+                              uint32_t stages, void* stream);
+
 /* Checksum encoder (Sec. 4.6, "Encoding"). A is `batch` matrices of
  * rows x cols (element (b, i, j) at A + b*batch_stride + i*ld + j, in
  * elements of dtype). Writes, when the pointer is not NULL,

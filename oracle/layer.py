@@ -29,6 +29,15 @@ masked probabilities are exactly zero. Under a causal mask the checksums
 cover only the block-lower-triangular region at the checksum-block
 granularity (key block <= query block), the part a tiled score GEMM
 computes.
+
+Masked products (a reading; the paper uses dense products): a product
+over keys with a causally masked factor (AP V, dAS K, and over queries
+AP^T dCL, dAS^T Q) is formed per tile of KEY_TILE = 128 queries (keys):
+query i takes keys j < the end of the 128-key tile that holds i, and key
+j takes queries from the start of the tile that holds j. The terms left
+out are exact zeros, so this equals the dense product whenever the other
+factor is finite; it differs only where a masked zero would meet an INF
+or NaN (0 * INF = NaN), i.e. in the unprotected or paper-literal modes.
 """
 from __future__ import annotations
 
@@ -41,6 +50,71 @@ from .numerics import round_to, stored_threshold
 from .eec import col_checksums, row_checksums, Verifier
 
 SECTIONS = ("AS", "CL", "O", "BWD")
+KEY_TILE = 128
+
+
+def _kend(i, S):
+    """End (exclusive) of the key range query i multiplies under a mask."""
+    return min(S, (i // KEY_TILE + 1) * KEY_TILE)
+
+
+def _kstart(j):
+    """Start of the query range key j multiplies under a mask."""
+    return (j // KEY_TILE) * KEY_TILE
+
+
+def masked_rows_product(P, M, causal):
+    """C_i = sum_j P_ij M_j over the key range of query i (dense if not
+    causal). P [..., S, S], M [..., S, n]."""
+    if not causal:
+        return P @ M
+    S = P.shape[-1]
+    out = np.empty(P.shape[:-1] + M.shape[-1:])
+    with np.errstate(invalid="ignore", over="ignore"):
+        for t0 in range(0, S, KEY_TILE):
+            t1 = min(S, t0 + KEY_TILE)
+            out[..., t0:t1, :] = P[..., t0:t1, :t1] @ M[..., :t1, :]
+    return out
+
+
+def masked_cols_product(P, M, causal):
+    """C_j = sum_i P_ij M_i over the query range of key j (dense P^T M if
+    not causal)."""
+    if not causal:
+        return P.swapaxes(-1, -2) @ M
+    S = P.shape[-1]
+    out = np.empty(P.shape[:-2] + (S, M.shape[-1]))
+    with np.errstate(invalid="ignore", over="ignore"):
+        for t0 in range(0, S, KEY_TILE):
+            t1 = min(S, t0 + KEY_TILE)
+            out[..., t0:t1, :] = P[..., t0:, t0:t1].swapaxes(-1, -2) @ M[..., t0:, :]
+    return out
+
+
+def masked_block_rows_product(Pc, M, R, causal):
+    """Checksum rows of a rows-product: Pc [..., nq, 2, S] are checksum rows
+    over R-query blocks; block qb takes the key range of its queries."""
+    if not causal:
+        return Pc @ M[..., None, :, :]
+    nq, S = Pc.shape[-3], Pc.shape[-1]
+    out = np.empty(Pc.shape[:-1] + M.shape[-1:])
+    with np.errstate(invalid="ignore", over="ignore"):
+        for qb in range(nq):
+            e = _kend(qb * R, S)
+            out[..., qb, :, :] = Pc[..., qb, :, :e] @ M[..., :e, :]
+    return out
+
+
+def masked_block_cols_product(Pr, M, R, causal):
+    """Checksum rows of a cols-product: Pr [..., S, nq, 2] are row checksums
+    over R-key blocks; block kb takes the query range of its keys."""
+    S, nq = Pr.shape[-3], Pr.shape[-2]
+    out = np.empty(Pr.shape[:-3] + (nq, 2, M.shape[-1]))
+    with np.errstate(invalid="ignore", over="ignore"):
+        for kb in range(nq):
+            s0 = _kstart(kb * R) if causal else 0
+            out[..., kb, :, :] = Pr[..., s0:, kb, :].swapaxes(-1, -2) @ M[..., s0:, :]
+    return out
 
 
 @dataclasses.dataclass
@@ -151,6 +225,18 @@ class _Run:
             self.events.append((op, int(b), int(h), int(r), int(c), "-", "UNCORRECTABLE"))
 
 
+def _row_dot(prow, mcol, i, S, causal):
+    """One element of a rows-product over query i's key range."""
+    e = _kend(i, S) if causal else S
+    return prow[:e] @ mcol[:e]
+
+
+def _col_dot(pcol, mcol, j, causal):
+    """One element of a cols-product over key j's query range."""
+    s0 = _kstart(j) if causal else 0
+    return pcol[s0:] @ mcol[s0:]
+
+
 def _causal_valid(n, S, R):
     """Which checksum vectors of a causal score-shaped output are computed:
     column vectors (query block qb, key j) with j // R <= qb and row vectors
@@ -238,16 +324,19 @@ def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
     APr = row_checksums(AP, R)                                 # [B,nh,S,nq,2]
 
     # context GEMM CL = AP V, two-sided checksums (row side via V^r)
-    CLh = rnd(AP @ Vh)                                         # [B,nh,S,d]
-    CLc = APc @ Vh[:, :, None]                                 # [B,nh,nq,2,d]
-    CLr = np.ascontiguousarray((AP @ Vr.transpose(0, 2, 1, 3))[:, :, :, None, :])  # [B,nh,S,1,2]
+    cz = p.causal
+    CLh = rnd(masked_rows_product(AP, Vh, cz))                 # [B,nh,S,d]
+    CLc = masked_block_rows_product(APc, Vh, R, cz)            # [B,nh,nq,2,d]
+    CLr = np.ascontiguousarray(
+        masked_rows_product(AP, Vr.transpose(0, 2, 1, 3), cz)[:, :, :, None, :])  # [B,nh,S,1,2]
     run.inject("CL", CLh, lambda b, h, r, c: (b, h, r, c))
     if run.on("CL"):
         CLh3 = CLh.reshape(B * nh, S, d)
         run.verify(CLh3, CLc.reshape(B * nh, nq, 2, d), R,
                    lambda k, i, j: ("CL", k // nh, k % nh, i, j),
                    Cr=CLr.reshape(B * nh, S, 1, 2), Cb=d,
-                   recompute=lambda k, i, j: AP[k // nh, k % nh, i] @ Vh[k // nh, k % nh, :, j])
+                   recompute=lambda k, i, j: _row_dot(AP[k // nh, k % nh, i],
+                                                      Vh[k // nh, k % nh, :, j], i, S, cz))
     CL = CLh.transpose(0, 2, 1, 3).reshape(B, S, H)
     CLc_full = CLc.transpose(0, 2, 3, 1, 4).reshape(B, nq, 2, H)
     CLr_full = CLr[:, :, :, 0, :].transpose(0, 2, 1, 3)        # [B,S,nh,2]
@@ -321,13 +410,15 @@ def backward(fwd: dict, dO, p: OracleParams, faults=()):
                    recompute=lambda k, i, j: dCLh[k // nh, k % nh, i] @ Vh[k // nh, k % nh, j])
 
     # dV = AP^T dCL_h; column checksums over key blocks from AP^r
-    dVh = rnd(AP.swapaxes(-1, -2) @ dCLh)                      # [B,nh,S,d]
-    dVc = (fwd["APr"].reshape(B, nh, S, 2 * nq).swapaxes(-1, -2) @ dCLh).reshape(B, nh, nq, 2, d)
+    cz = p.causal
+    dVh = rnd(masked_cols_product(AP, dCLh, cz))               # [B,nh,S,d]
+    dVc = masked_block_cols_product(fwd["APr"], dCLh, R, cz)   # [B,nh,nq,2,d]
     run.inject("dV", dVh, lambda b, h, r, c: (b, h, r, c))
     if on:
         run.verify(dVh.reshape(B * nh, S, d), dVc.reshape(B * nh, nq, 2, d), R,
                    lambda k, i, j: ("dV", k // nh, k % nh, i, j),
-                   recompute=lambda k, i, j: AP[k // nh, k % nh, :, i] @ dCLh[k // nh, k % nh, :, j])
+                   recompute=lambda k, i, j: _col_dot(AP[k // nh, k % nh, :, i],
+                                                      dCLh[k // nh, k % nh, :, j], i, cz))
 
     # softmax backward (unprotected), masked entries selected to zero
     mask = np.tril(np.ones((S, S), dtype=bool)) if p.causal else np.ones((S, S), dtype=bool)
@@ -338,22 +429,24 @@ def backward(fwd: dict, dO, p: OracleParams, faults=()):
     dASr = row_checksums(dAS, R)                               # [B,nh,S,nq,2]
 
     # dQ = dAS K_h
-    dQh = rnd(dAS @ Kh)
-    dQc = dASc @ Kh[:, :, None]                                # [B,nh,nq,2,d]
+    dQh = rnd(masked_rows_product(dAS, Kh, cz))
+    dQc = masked_block_rows_product(dASc, Kh, R, cz)           # [B,nh,nq,2,d]
     run.inject("dQ", dQh, lambda b, h, r, c: (b, h, r, c))
     if on:
         run.verify(dQh.reshape(B * nh, S, d), dQc.reshape(B * nh, nq, 2, d), R,
                    lambda k, i, j: ("dQ", k // nh, k % nh, i, j),
-                   recompute=lambda k, i, j: dAS[k // nh, k % nh, i] @ Kh[k // nh, k % nh, :, j])
+                   recompute=lambda k, i, j: _row_dot(dAS[k // nh, k % nh, i],
+                                                      Kh[k // nh, k % nh, :, j], i, S, cz))
 
     # dK = dAS^T Q_h; column checksums over key blocks from dAS^r
-    dKh = rnd(dAS.swapaxes(-1, -2) @ Qh)
-    dKc = (dASr.reshape(B, nh, S, 2 * nq).swapaxes(-1, -2) @ Qh).reshape(B, nh, nq, 2, d)
+    dKh = rnd(masked_cols_product(dAS, Qh, cz))
+    dKc = masked_block_cols_product(dASr, Qh, R, cz)           # [B,nh,nq,2,d]
     run.inject("dK", dKh, lambda b, h, r, c: (b, h, r, c))
     if on:
         run.verify(dKh.reshape(B * nh, S, d), dKc.reshape(B * nh, nq, 2, d), R,
                    lambda k, i, j: ("dK", k // nh, k % nh, i, j),
-                   recompute=lambda k, i, j: dAS[k // nh, k % nh, :, i] @ Qh[k // nh, k % nh, :, j])
+                   recompute=lambda k, i, j: _col_dot(dAS[k // nh, k % nh, :, i],
+                                                      Qh[k // nh, k % nh, :, j], i, cz))
 
     def merge(Mh):          # [B,nh,S,d] -> [B,S,H]
         return Mh.transpose(0, 2, 1, 3).reshape(B, S, H)

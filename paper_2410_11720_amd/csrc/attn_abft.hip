@@ -228,10 +228,10 @@ int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
   return ABFT_OK;
 }
 
-int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wqkv,
-                      const void* Wo, void* O, void* workspace, size_t workspace_bytes,
-                      const abft_fault* faults, int32_t n_faults, abft_report* report,
-                      void* stream) {
+int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const void* Wqkv,
+                             const void* Wo, void* O, void* workspace, size_t workspace_bytes,
+                             const abft_fault* faults, int32_t n_faults, abft_report* report,
+                             uint32_t stages, void* stream) {
   Dims d;
   int st = validate(cfg, &d);
   if (st != ABFT_OK) return st;
@@ -262,15 +262,15 @@ int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wq
   const bool need_vr = p.sec_cl || p.sec_bwd;             // V^r -> CL^r
   const bool need_apc = p.sec_cl || p.sec_o;              // AP^c -> CL^c -> O^c
   // encode (Sec. 4.6): W^V row checksums per head; X column and row checksums
-  if (need_vr)
+  if ((stages & ABFT_STAGE_ENCODE) && need_vr)
     CK(launch_encode(Wc + 2 * H * es, dt, 1, H, H, 3 * H, 0, int(H), int(hd), nullptr,
                      F(L.wvr), s));
-  if (need_xc || p.sec_bwd)
+  if ((stages & ABFT_STAGE_ENCODE) && (need_xc || p.sec_bwd))
     CK(launch_encode(X, dt, B, S, H, H, S * H, int(R), int(hd), need_xc ? F(L.xc) : nullptr,
                      p.sec_bwd ? F(L.xr) : nullptr, s));
 
   // [Q|K|V] = X Wqkv
-  {
+  if (stages & ABFT_STAGE_QKV) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(3 * H); g.K = int(H);
     g.A = X; g.lda = H;
@@ -294,7 +294,7 @@ int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wq
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(T, 3 * H, R, ncu, dt), s));
   }
   // AS = Q K^T per head (unscaled, before the mask), two-sided checksums
-  {
+  if (stages & ABFT_STAGE_SCORE) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(S); g.K = int(hd);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -311,7 +311,7 @@ int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wq
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, Tile::T128x128, s));
   }
   // AP = softmax(scale * AS) with column (and row) checksums
-  {
+  if (stages & ABFT_STAGE_SOFTMAX) {
     SoftmaxDesc sd;
     sd.B = int(B); sd.nh = int(nh); sd.S = int(S); sd.R = int(R); sd.causal = cfg->causal;
     sd.kv_align = 128;
@@ -322,7 +322,7 @@ int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wq
     CK(launch_softmax_fwd(sd, dt, s));
   }
   // CL = AP V per head, CL^c = AP^c V, CL^r = AP V^r
-  {
+  if (stages & ABFT_STAGE_CONTEXT) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(hd); g.K = int(S);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -344,7 +344,7 @@ int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wq
                    hd == 64 ? Tile::T128x64 : Tile::T128x128, s));
   }
   // O = CL Wo, O^c = CL^c Wo
-  {
+  if (stages & ABFT_STAGE_OUT) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(H);
     g.A = ws + L.cl; g.lda = H;
@@ -360,11 +360,11 @@ int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wq
   return ABFT_OK;
 }
 
-int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* X,
-                       const void* Wqkv, const void* Wo, void* workspace,
-                       size_t workspace_bytes, void* dX, float* dWqkv, float* dWo,
-                       const abft_fault* faults, int32_t n_faults, abft_report* report,
-                       void* stream) {
+int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const void* X,
+                              const void* Wqkv, const void* Wo, void* workspace,
+                              size_t workspace_bytes, void* dX, float* dWqkv, float* dWo,
+                              const abft_fault* faults, int32_t n_faults, abft_report* report,
+                              uint32_t stages, void* stream) {
   Dims d;
   int st = validate(cfg, &d);
   if (st != ABFT_OK) return st;
@@ -385,10 +385,10 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
   const int ncu = num_cus();
 
   if (!(cfg->flags & ABFT_FLAG_REPORT_APPEND)) CK(launch_report_reset(report, 0, false, s));
-  if (pb) CK(launch_encode(dO, dt, B, S, H, H, S * H, int(R), int(hd), F(L.doc), nullptr, s));
+  if ((stages & ABFT_STAGE_ENCODE) && pb) CK(launch_encode(dO, dt, B, S, H, H, S * H, int(R), int(hd), F(L.doc), nullptr, s));
 
   // dCL = dO Wo^T, dCL^c = dO^c Wo^T
-  {
+  if (stages & ABFT_STAGE_DCL) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(H);
     g.A = dO; g.lda = H;
@@ -403,7 +403,7 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(T, H, R, ncu, dt), s));
   }
   // dWo = CL^T dO, column checksums over head blocks of rows from CL^r
-  {
+  if (stages & ABFT_STAGE_DWO) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(H); g.N = int(H); g.K = int(T);
     g.A = ws + L.cl; g.lda = H;
@@ -417,7 +417,7 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
     CK(launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s));
   }
   // dAP = dCL_h V_h^T, dAP^c = dCL_h^c V_h^T
-  {
+  if (stages & ABFT_STAGE_DAP) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(S); g.K = int(hd);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -434,7 +434,7 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
   }
   const Tile td = hd == 64 ? Tile::T128x64 : Tile::T128x128;
   // dV = AP^T dCL_h, column checksums over key blocks from AP^r
-  {
+  if (stages & ABFT_STAGE_DV) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(hd); g.K = int(S);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -452,7 +452,7 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
     CK(launch_gemm(g, dt, false, Layout::MNMajor, Layout::MNMajor, td, s));
   }
   // dAS = scale * AP * (dAP - rowdot), with column and row checksums
-  {
+  if (stages & ABFT_STAGE_SOFTMAX_BWD) {
     SoftmaxDesc sd;
     sd.B = int(B); sd.nh = int(nh); sd.S = int(S); sd.R = int(R); sd.causal = cfg->causal;
     sd.kv_align = 128;
@@ -463,7 +463,7 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
     CK(launch_softmax_bwd(sd, dt, s));
   }
   // dQ = dAS K_h, dQ^c = dAS^c K_h
-  {
+  if (stages & ABFT_STAGE_DQ) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(hd); g.K = int(S);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -480,7 +480,7 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, td, s));
   }
   // dK = dAS^T Q_h, column checksums over key blocks from dAS^r
-  {
+  if (stages & ABFT_STAGE_DK) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(hd); g.K = int(S);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -498,7 +498,7 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
     CK(launch_gemm(g, dt, false, Layout::MNMajor, Layout::MNMajor, td, s));
   }
   // dWqkv = X^T dQKV, column checksums over head blocks of rows from X^r
-  {
+  if (stages & ABFT_STAGE_DWQKV) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(H); g.N = int(3 * H); g.K = int(T);
     g.A = X; g.lda = H;
@@ -512,7 +512,7 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
     CK(launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s));
   }
   // dX = dQKV Wqkv^T, dX^c = dQKV^c Wqkv^T
-  {
+  if (stages & ABFT_STAGE_DX) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(3 * H);
     g.A = ws + L.dqkv; g.lda = 3 * H;
@@ -526,6 +526,23 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(T, H, R, ncu, dt), s));
   }
   return ABFT_OK;
+}
+
+int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wqkv,
+                      const void* Wo, void* O, void* workspace, size_t workspace_bytes,
+                      const abft_fault* faults, int32_t n_faults, abft_report* report,
+                      void* stream) {
+  return attn_abft_forward_stages(cfg, X, Wqkv, Wo, O, workspace, workspace_bytes, faults,
+                                  n_faults, report, ABFT_STAGE_ALL, stream);
+}
+
+int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* X,
+                       const void* Wqkv, const void* Wo, void* workspace,
+                       size_t workspace_bytes, void* dX, float* dWqkv, float* dWo,
+                       const abft_fault* faults, int32_t n_faults, abft_report* report,
+                       void* stream) {
+  return attn_abft_backward_stages(cfg, dO, X, Wqkv, Wo, workspace, workspace_bytes, dX, dWqkv,
+                                   dWo, faults, n_faults, report, ABFT_STAGE_ALL, stream);
 }
 
 int encode_checksums(const void* A, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,

@@ -317,3 +317,29 @@ def test_disabled_section_leaves_faults_in_place():
     assert np.isnan(f["O"][0, 9]).all()
     f = forward(inp["X"], inp["Wqkv"], inp["Wo"], p, [W.Fault("CL", 0, 0, 9, 3, np.inf)])
     assert [e[:5] for e in f["events"]] == [("CL", 0, 0, 9, 3)]
+
+
+def test_masked_products_equal_dense_products_on_finite_inputs():
+    """The per-tile key ranges of masked products leave out exact zeros
+    only, so on finite inputs they equal the dense products."""
+    from oracle.layer import (masked_rows_product, masked_cols_product,
+                              masked_block_rows_product, masked_block_cols_product)
+    rng = np.random.default_rng(4)
+    S, R, n = 320, 64, 5
+    P = np.tril(rng.standard_normal((2, S, S)))
+    M = rng.standard_normal((2, S, n))
+    assert np.allclose(masked_rows_product(P, M, True), P @ M, rtol=1e-12, atol=1e-12)
+    assert np.allclose(masked_cols_product(P, M, True), P.swapaxes(-1, -2) @ M,
+                       rtol=1e-12, atol=1e-12)
+    Pc = col_checksums(P, R)
+    assert np.allclose(masked_block_rows_product(Pc, M, R, True), Pc @ M[:, None],
+                       rtol=1e-12, atol=1e-9)
+    from oracle.eec import row_checksums
+    Pr = row_checksums(P, R)
+    dense = (Pr.reshape(2, S, -1).swapaxes(-1, -2) @ M).reshape(2, S // R, 2, n)
+    assert np.allclose(masked_block_cols_product(Pr, M, R, True), dense, rtol=1e-12, atol=1e-9)
+    # an INF meets masked zeros only inside the tile holding the diagonal
+    M2 = M.copy()
+    M2[0, 200, 1] = np.inf
+    C = masked_rows_product(P, M2, True)
+    assert np.all(np.isfinite(C[0, :128, 1])) and np.all(~np.isfinite(C[0, 128:256, 1]))
