@@ -58,8 +58,8 @@ class Event(ctypes.Structure):
 REPORT_HEADER = 32  # bytes before the event array
 assert ctypes.sizeof(Event) == 40 and ctypes.sizeof(Fault) == 24
 
-_vp, _sz, _i32, _i64, _f32 = (ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32,
-                              ctypes.c_int64, ctypes.c_float)
+_vp, _sz, _i32, _i64, _f32, _u32 = (ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32,
+                                   ctypes.c_int64, ctypes.c_float, ctypes.c_uint32)
 _P = ctypes.POINTER(Config)
 _sig = {
     "attn_abft_workspace_bytes": (_sz, [_P]),
@@ -68,6 +68,10 @@ _sig = {
     "attn_abft_forward": (ctypes.c_int, [_P, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _i32, _vp, _vp]),
     "attn_abft_backward": (ctypes.c_int, [_P, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _vp, _vp,
                                           _vp, _i32, _vp, _vp]),
+    "attn_abft_forward_stages": (ctypes.c_int, [_P, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _i32, _vp,
+                                                _u32, _vp]),
+    "attn_abft_backward_stages": (ctypes.c_int, [_P, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _vp, _vp,
+                                                 _vp, _i32, _vp, _u32, _vp]),
     "encode_checksums": (ctypes.c_int, [_vp, _i32, _i64, _i64, _i64, _i64, _i64, _i32, _i32,
                                         _vp, _vp, _vp]),
     "verify_and_correct": (ctypes.c_int, [_vp, _i32, _i64, _i64, _i64, _i64, _i64, _i32, _i32,
@@ -175,6 +179,34 @@ def attn_abft_backward(cfg: LayerConfig, dO, X, Wqkv, Wo, workspace, dX, dWqkv, 
                                    _ptr(workspace), workspace.numel() * workspace.element_size(),
                                    _ptr(dX), _ptr(dWqkv), _ptr(dWo), _ptr(faults), n_faults,
                                    _ptr(report), _stream(stream)), "attn_abft_backward")
+
+
+STAGE_ALL = 0x3FF
+FWD_STAGES = {"encode": 0x001, "qkv": 0x002, "score": 0x004, "softmax": 0x008,
+              "context": 0x010, "out": 0x020}
+BWD_STAGES = {"encode": 0x001, "dCL": 0x002, "dWo": 0x004, "dAP": 0x008, "dV": 0x010,
+              "softmax_bwd": 0x020, "dQ": 0x040, "dK": 0x080, "dWqkv": 0x100, "dX": 0x200}
+
+
+def attn_abft_forward_stages(cfg: LayerConfig, X, Wqkv, Wo, O, workspace, faults, n_faults,
+                             report, stages, stream=None, append=False):
+    c = cfg.to_c(append)
+    _check(_lib.attn_abft_forward_stages(ctypes.byref(c), _ptr(X), _ptr(Wqkv), _ptr(Wo), _ptr(O),
+                                         _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(),
+                                         _ptr(faults), n_faults, _ptr(report), stages,
+                                         _stream(stream)), "attn_abft_forward_stages")
+
+
+def attn_abft_backward_stages(cfg: LayerConfig, dO, X, Wqkv, Wo, workspace, dX, dWqkv, dWo,
+                              faults, n_faults, report, stages, stream=None, append=False):
+    c = cfg.to_c(append)
+    _check(_lib.attn_abft_backward_stages(ctypes.byref(c), _ptr(dO), _ptr(X), _ptr(Wqkv),
+                                          _ptr(Wo), _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(),
+                                          _ptr(dX), _ptr(dWqkv), _ptr(dWo), _ptr(faults),
+                                          n_faults, _ptr(report), stages, _stream(stream)),
+           "attn_abft_backward_stages")
 
 
 def encode_checksums(A, dtype, batch, rows, cols, ld, batch_stride, block_rows, block_cols,

@@ -263,8 +263,7 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
   const bool need_apc = p.sec_cl || p.sec_o;              // AP^c -> CL^c -> O^c
   // encode (Sec. 4.6): W^V row checksums per head; X column and row checksums
   if ((stages & ABFT_STAGE_ENCODE) && need_vr)
-    CK(launch_encode(Wc + 2 * H * es, dt, 1, H, H, 3 * H, 0, int(H), int(hd), nullptr,
-                     F(L.wvr), s));
+    CK(launch_encode(Wc + 2 * H * es, dt, 1, H, H, 3 * H, 0, 32, int(hd), nullptr, F(L.wvr), s));
   if ((stages & ABFT_STAGE_ENCODE) && (need_xc || p.sec_bwd))
     CK(launch_encode(X, dt, B, S, H, H, S * H, int(R), int(hd), need_xc ? F(L.xc) : nullptr,
                      p.sec_bwd ? F(L.xr) : nullptr, s));
@@ -555,7 +554,11 @@ int encode_checksums(const void* A, int32_t dtype, int64_t batch, int64_t rows, 
   if (!col_chk && !row_chk) return ABFT_OK;
   int st = check_device();
   if (st != ABFT_OK) return st;
-  const int Rb = col_chk ? block_rows : int(rows > 0 ? rows : 1);
+  int Rb = block_rows;
+  if (!col_chk) {  // only row checksums: any row block works; pick one with many workgroups
+    Rb = 1;
+    while (Rb < 32 && rows % (2 * Rb) == 0) Rb *= 2;
+  }
   CK(launch_encode(A, dtype, batch, rows, cols, ld, batch_stride, Rb, block_cols, col_chk, row_chk,
                    static_cast<hipStream_t>(stream)));
   return ABFT_OK;

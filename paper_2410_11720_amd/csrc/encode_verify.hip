@@ -43,57 +43,83 @@ __device__ __forceinline__ float group_sum(float x, int width) {
   return x;
 }
 
-// grid: (ceil(cols / (NT*V)), rows/Rb, batch). Row checksums are produced
-// here only when Cb/V lanes form an aligned group of at most 64.
+// grid: (ceil(cols / (64*V)), rows/Rb, batch). A wave owns a 64*V-column
+// slab (lane = one 16-byte chunk); the four waves of the workgroup split
+// the Rb rows of the block (wave w takes rows w, w+4, ...) and keep UN
+// rows in flight. Column checksums are combined across waves in LDS in a
+// fixed order; row checksums of each Cb-column block are reduced across
+// the Cb/V lanes that hold it (Cb/V a power of two <= 64 dividing 64*V).
 template <class T, int V>
 __global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, int64_t cols,
                                                     int64_t ld, int64_t bstride, int Rb, int Cb,
                                                     float* col_chk, float* row_chk) {
-  const int tid = threadIdx.x;
+  constexpr int UN = 8;
+  __shared__ float part[4][64][V][2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t b = blockIdx.z;
   const int64_t rb = blockIdx.y;
-  const int64_t c0 = (int64_t(blockIdx.x) * NT + tid) * V;
+  const int64_t c0 = (int64_t(blockIdx.x) * 64 + lane) * V;
   const bool live = c0 < cols;
-  const T* base = A + b * bstride;
+  const T* base = A + b * bstride + rb * Rb * ld;
   const int lanes = Cb / V;
   float c1[V], c2[V];
 #pragma unroll
   for (int e = 0; e < V; ++e) c1[e] = c2[e] = 0.f;
-  for (int r = 0; r < Rb; ++r) {
-    const int64_t row = rb * Rb + r;
-    float x[V];
-    if (live) load_vec<T, V>(base + row * ld + c0, x);
-    else {
+  for (int r0 = wave; r0 < Rb; r0 += 4 * UN) {
+    float x[UN][V];
 #pragma unroll
-      for (int e = 0; e < V; ++e) x[e] = 0.f;
+    for (int u = 0; u < UN; ++u) {
+      const int r = r0 + 4 * u;
+      if (live && r < Rb) load_vec<T, V>(base + r * ld + c0, x[u]);
+      else {
+#pragma unroll
+        for (int e = 0; e < V; ++e) x[u][e] = 0.f;
+      }
     }
 #pragma unroll
-    for (int e = 0; e < V; ++e) {
-      c1[e] += x[e];
-      c2[e] += float(r + 1) * x[e];
-    }
-    if (row_chk != nullptr) {
-      float s1 = 0.f, s2 = 0.f;
+    for (int u = 0; u < UN; ++u) {
+      const int r = r0 + 4 * u;
 #pragma unroll
       for (int e = 0; e < V; ++e) {
-        s1 += x[e];
-        s2 += float(((c0 + e) % Cb) + 1) * x[e];
+        c1[e] += x[u][e];
+        c2[e] += float(r + 1) * x[u][e];
       }
-      s1 = group_sum(s1, lanes);
-      s2 = group_sum(s2, lanes);
-      if (live && (c0 % Cb) == 0) {
-        float* rc = row_chk + ((b * rows + row) * (cols / Cb) + c0 / Cb) * 2;
-        rc[0] = s1;
-        rc[1] = s2;
+      if (row_chk != nullptr && r0 + 4 * u < Rb) {   // uniform across the wave
+        float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          s1 += x[u][e];
+          s2 += float(((c0 + e) % Cb) + 1) * x[u][e];
+        }
+        s1 = group_sum(s1, lanes);
+        s2 = group_sum(s2, lanes);
+        if (live && (c0 % Cb) == 0) {
+          float* rc = row_chk + ((b * rows + rb * Rb + r) * (cols / Cb) + c0 / Cb) * 2;
+          rc[0] = s1;
+          rc[1] = s2;
+        }
       }
     }
   }
-  if (col_chk != nullptr && live) {
-    float* cc = col_chk + ((b * (rows / Rb) + rb) * 2) * cols;
+  if (col_chk != nullptr) {
 #pragma unroll
     for (int e = 0; e < V; ++e) {
-      cc[c0 + e] = c1[e];
-      cc[cols + c0 + e] = c2[e];
+      part[wave][lane][e][0] = c1[e];
+      part[wave][lane][e][1] = c2[e];
+    }
+    __syncthreads();
+    if (wave == 0 && live) {
+      float* cc = col_chk + ((b * (rows / Rb) + rb) * 2) * cols;
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        float s1 = part[0][lane][e][0], s2 = part[0][lane][e][1];
+        for (int w = 1; w < 4; ++w) {
+          s1 += part[w][lane][e][0];
+          s2 += part[w][lane][e][1];
+        }
+        cc[c0 + e] = s1;
+        cc[cols + c0 + e] = s2;
+      }
     }
   }
 }
@@ -123,19 +149,21 @@ template <class T>
 hipError_t encode_t(const T* A, int64_t batch, int64_t rows, int64_t cols, int64_t ld,
                     int64_t bs, int Rb, int Cb, float* col_chk, float* row_chk, hipStream_t s) {
   constexpr int VV = 16 / sizeof(T);
+  auto lane_ok = [&](int v) {  // Cb/v lanes: a power of two dividing the 64-lane slab
+    return Cb % v == 0 && Cb / v <= 64 && ((Cb / v) & (Cb / v - 1)) == 0;
+  };
   const bool aligned = (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (ld % VV == 0) &&
                        (cols % VV == 0) && (bs % VV == 0);
-  const bool vec = aligned && (!row_chk || (Cb % VV == 0 && Cb / VV <= 64 &&
-                                            ((Cb / VV) & (Cb / VV - 1)) == 0));
-  const bool scal_rows = row_chk && (Cb > 64 || (Cb & (Cb - 1)) != 0);
+  const bool vec = aligned && (!row_chk || lane_ok(VV));
+  const bool scal_rows = row_chk && !vec && !lane_ok(1);
   float* rc_inline = scal_rows ? nullptr : row_chk;
   if (col_chk != nullptr || rc_inline != nullptr) {
     if (vec) {
-      dim3 grid((cols + NT * VV - 1) / (NT * VV), rows / Rb, batch);
+      dim3 grid((cols + 64 * VV - 1) / (64 * VV), rows / Rb, batch);
       hipLaunchKernelGGL((encode_kernel<T, VV>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs, Rb,
                          Cb, col_chk, rc_inline);
     } else {
-      dim3 grid((cols + NT - 1) / NT, rows / Rb, batch);
+      dim3 grid((cols + 63) / 64, rows / Rb, batch);
       hipLaunchKernelGGL((encode_kernel<T, 1>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs, Rb,
                          Cb, col_chk, rc_inline);
     }

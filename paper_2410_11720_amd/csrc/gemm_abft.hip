@@ -270,9 +270,10 @@ struct Gemm {
   static constexpr size_t CNT = BM * (BN / 16) + (BM / 16) * BN;
   static constexpr size_t EPI_BYTES = R0 + (CCV + RCV) * 4 + CNT * 4;
   static constexpr size_t LDS_BYTES =
-      PROT ? (MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES) : MAIN_BYTES;
+      PROT ? (MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES)
+           : (MAIN_BYTES > R0_TILE ? MAIN_BYTES : R0_TILE);
 
-  __device__ static void run(const GemmDesc& g, char* smem) {
+  __device__ static __forceinline__ void run(const GemmDesc& g, char* smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int ntn = (g.N + BN - 1) / BN;
@@ -367,15 +368,27 @@ struct Gemm {
 #pragma unroll
           for (int j = 0; j < JN; ++j) acc[i][j] = Mfma<T>::mma(af[i], bfr[j], acc[i][j]);
         if (PROT) {
+          // wave-uniform branches keep every fragment index a compile-time
+          // constant (a runtime index would send the arrays to scratch)
           if (cc) {
             const auto sf = Mfma<T>::load(sS + fr * LDK + kk + fk);
+            if (wm == 0) {
 #pragma unroll
-            for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[wm * JS + j], accs[j]);
+              for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[j], accs[j]);
+            } else {
+#pragma unroll
+              for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[JS + j], accs[j]);
+            }
           }
           if (cr) {
             const auto rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
+            if (wn == 0) {
 #pragma unroll
-            for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[wn * IS + i], accr[i]);
+              for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[i], accr[i]);
+            } else {
+#pragma unroll
+              for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[IS + i], accr[i]);
+            }
           }
         }
       }
@@ -397,25 +410,14 @@ struct Gemm {
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[i][j][r] = Storage<TC>::round(acc[i][j][r]);
 
+    // A tile that an injected fault aims at takes the LDS path, where the
+    // fault is written into the rounded tile before any verification.
+    bool faulty = false;
     for (int f = 0; f < g.n_faults; ++f) {
-      const abft_fault ft = g.faults[f];
       int fz, fm, fn;
-      if (!fault_target(g.map, g.N, ft, &fz, &fm, &fn)) continue;
-      if (fz != z || fm < m0 || fm >= m0 + BM || fn < n0 || fn >= n0 + BN) continue;
-      const int lrw = fm - m0, lcl = fn - n0;
-      if (lrw / WM != wm || lcl / WN != wn) continue;
-      const int fi = (lrw % WM) / 16, fj = (lcl % WN) / 16;
-      const int fl = ((lrw & 15) >> 2) * 16 + (lcl & 15), frr = lrw & 3;
-      const float fv = Storage<TC>::round(ft.value);
-      if (lane == fl) {
-#pragma unroll
-        for (int i = 0; i < IM; ++i)
-#pragma unroll
-          for (int j = 0; j < JN; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (i == fi && j == fj && r == frr) acc[i][j][r] = fv;
-      }
+      if (fault_target(g.map, g.N, g.faults[f], &fz, &fm, &fn) && fz == z && fm >= m0 &&
+          fm < m0 + BM && fn >= n0 && fn < n0 + BN)
+        faulty = true;
     }
 
     const int verify = PROT ? g.verify : 0;
@@ -568,7 +570,7 @@ struct Gemm {
       any = __syncthreads_or(my_flag);
     }
 
-    if (!any) {
+    if (!any && !faulty) {
       // fast path: store straight from registers
 #pragma unroll
       for (int i = 0; i < IM; ++i)
@@ -581,7 +583,7 @@ struct Gemm {
             if (m < g.M && n < g.N) C[int64_t(m) * g.ldc + n] = Storage<TC>::store(acc[i][j][r]);
           }
     } else {
-      TC* tile = reinterpret_cast<TC*>(smem);  // overlays the dead partial sums
+      TC* tile = reinterpret_cast<TC*>(smem);  // overlays dead partial sums / operand stages
       __syncthreads();
 #pragma unroll
       for (int i = 0; i < IM; ++i)
@@ -592,7 +594,7 @@ struct Gemm {
             tile[(wm * WM + i * 16 + (lane >> 4) * 4 + r) * BN + wn * WN + j * 16 + fr] =
                 Storage<TC>::store(acc[i][j][r]);
       slow_path(g, tile, A, B, C, z, m0, n0, k_lo, k_hi, ccv, rcv, rowcnt, colcnt, nrb, ncb,
-                verify, tid);
+                cc ? verify : 0, tid);
     }
 
     // propagated checksums for the consumers downstream
@@ -620,12 +622,36 @@ struct Gemm {
 
   // Slow path: the tile goes to LDS and EEC-ABFT runs there (one thread per
   // vector, as in the paper's Fig. 4), then the tile is stored.
-  __device__ static __attribute__((noinline)) void slow_path(
+  __device__ static __forceinline__ void slow_path(
       const GemmDesc& g, TC* tile, const T* A, const T* B, TC* C, int z, int m0, int n0,
       int k_lo, int k_hi, float* ccv, float* rcv, int* rowcnt, int* colcnt, int nrb, int ncb,
       int verify, int tid) {
-    for (int e = tid; e < BM * (BN / 16) + (BM / 16) * BN; e += NT) rowcnt[e] = 0;
+    // injected faults (test-only), after rounding to storage
+    if (tid == 0) {
+      for (int f = 0; f < g.n_faults; ++f) {
+        const abft_fault ft = g.faults[f];
+        int fz, fm, fn;
+        if (fault_target(g.map, g.N, ft, &fz, &fm, &fn) && fz == z && fm >= m0 &&
+            fm < m0 + BM && fn >= n0 && fn < n0 + BN)
+          tile[(fm - m0) * BN + fn - n0] = Storage<TC>::store(Storage<TC>::round(ft.value));
+      }
+    }
+    if (verify >= 1)
+      for (int e = tid; e < BM * (BN / 16) + (BM / 16) * BN; e += NT) rowcnt[e] = 0;
     __syncthreads();
+    if (verify >= 1) passes(g, tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, rowcnt, colcnt, nrb,
+                            ncb, verify, tid);
+    for (int e = tid; e < BM * BN; e += NT) {
+      const int row = e / BN, col = e % BN;
+      if (m0 + row < g.M && n0 + col < g.N) C[int64_t(m0 + row) * g.ldc + n0 + col] = tile[e];
+    }
+  }
+
+  // EEC-ABFT on the LDS tile, one thread per vector (as in the paper's Fig. 4).
+  __device__ static __forceinline__ void passes(
+      const GemmDesc& g, TC* tile, const T* A, const T* B, int z, int m0, int n0, int k_lo,
+      int k_hi, float* ccv, float* rcv, int* rowcnt, int* colcnt, int nrb, int ncb, int verify,
+      int tid) {
 
     const int Rm = g.Rm, Rn = g.Rn;
     auto in_col = [&](int blk, int n) {
@@ -713,10 +739,6 @@ struct Gemm {
       }
     }
     __syncthreads();
-    for (int e = tid; e < BM * BN; e += NT) {
-      const int row = e / BN, col = e % BN;
-      if (m0 + row < g.M && n0 + col < g.N) C[int64_t(m0 + row) * g.ldc + n0 + col] = tile[e];
-    }
   }
 };
 

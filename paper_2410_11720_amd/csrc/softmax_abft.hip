@@ -71,8 +71,9 @@ __device__ __forceinline__ float group_sum(float x, int width) {
   return x;
 }
 
-// CH: 16-byte chunks per lane per row (S <= 64 * CH * VEC).
-template <class T, int CH, bool BWD>
+// CH: 16-byte chunks per lane per row (S <= 64 * CH * VEC); RPI rows per
+// iteration per wave; PF: prefetch the next iteration's rows.
+template <class T, int CH, bool BWD, int RPI, bool PF>
 __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   constexpr int V = Vec<T>::N;
   extern __shared__ __align__(16) char smem[];
@@ -97,99 +98,131 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
     for (int e = 0; e < V; ++e) c1[t][e] = c2[t][e] = 0.f;
 
   const float l2e = 1.4426950408889634f;
-  for (int rl = wave; rl < R; rl += 4) {
-    const int i = qb * R + rl;
-    const T* row = src + int64_t(i) * S;
-    float x[CH][V], y[CH][V];
+  // Rows of this wave: rl = wave + 4 * (it * RPI + u), u < RPI. With PF the
+  // loads of iteration it + 1 are issued before iteration it is computed
+  // (two register buffers, the loop unrolled by two so that buffer indices
+  // stay compile-time constants).
+  auto load_rows = [&](float (&x)[RPI][CH][V], float (&y)[RPI][CH][V], int it) {
 #pragma unroll
-    for (int t = 0; t < CH; ++t) {
-      const int j0 = (lane + 64 * t) * V;
-      if (j0 < s_valid) {
-        Vec<T>::load(row + j0, x[t]);
-        if (BWD) Vec<T>::load(src2 + int64_t(i) * S + j0, y[t]);
+    for (int u = 0; u < RPI; ++u) {
+      const int i = qb * R + wave + 4 * (it * RPI + u);
+#pragma unroll
+      for (int t = 0; t < CH; ++t) {
+        const int j0 = (lane + 64 * t) * V;
+        if (j0 < s_valid) {
+          Vec<T>::load(src + int64_t(i) * S + j0, x[u][t]);
+          if (BWD) Vec<T>::load(src2 + int64_t(i) * S + j0, y[u][t]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < V; ++e) x[u][t][e] = y[u][t][e] = 0.f;
+        }
+      }
+    }
+  };
+  auto process_rows = [&](float (&xr)[RPI][CH][V], float (&yr)[RPI][CH][V], int it) {
+#pragma unroll
+    for (int u = 0; u < RPI; ++u) {
+      const int rl = wave + 4 * (it * RPI + u);
+      const int i = qb * R + rl;
+      float (&x)[CH][V] = xr[u];
+      float (&y)[CH][V] = yr[u];
+      if (!BWD) {
+        // AP = softmax(scale * AS) over unmasked keys, in base 2
+        const float sc = d.scale * l2e;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < CH; ++t)
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const int j = (lane + 64 * t) * V + e;
+            const bool live = j < s_valid && (!d.causal || j <= i);
+            x[t][e] = live ? x[t][e] * sc : -INFINITY;
+            mx = nanmax(mx, x[t][e]);
+          }
+        mx = wave_max(mx);
+        float sum = 0.f;
+#pragma unroll
+        for (int t = 0; t < CH; ++t)
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const int j = (lane + 64 * t) * V + e;
+            const bool live = j < s_valid && (!d.causal || j <= i);
+            const float ev = live ? exp2f(x[t][e] - mx) : 0.f;
+            x[t][e] = ev;
+            sum += ev;
+          }
+        sum = wave_sum(sum);
+        const float inv = 1.f / sum;
+#pragma unroll
+        for (int t = 0; t < CH; ++t)
+#pragma unroll
+          for (int e = 0; e < V; ++e) x[t][e] = Storage<T>::round(x[t][e] * inv);
       } else {
+        // dAS = scale * AP * (dAP - D), D = sum_j AP_j dAP_j over unmasked keys
+        float dot = 0.f;
 #pragma unroll
-        for (int e = 0; e < V; ++e) x[t][e] = y[t][e] = 0.f;
+        for (int t = 0; t < CH; ++t)
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const int j = (lane + 64 * t) * V + e;
+            const bool live = j < s_valid && (!d.causal || j <= i);
+            dot += live ? x[t][e] * y[t][e] : 0.f;
+          }
+        dot = wave_sum(dot);
+#pragma unroll
+        for (int t = 0; t < CH; ++t)
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const int j = (lane + 64 * t) * V + e;
+            const bool live = j < s_valid && (!d.causal || j <= i);
+            x[t][e] = live ? Storage<T>::round(d.scale * x[t][e] * (y[t][e] - dot)) : 0.f;
+          }
+      }
+      // store, accumulate column checksums, emit row checksums per key block
+      const float wr = float(rl + 1);
+#pragma unroll
+      for (int t = 0; t < CH; ++t) {
+        const int j0 = (lane + 64 * t) * V;
+        float r1 = 0.f, r2 = 0.f;
+        if (j0 < s_valid) {
+          Vec<T>::store(dst + int64_t(i) * S + j0, x[t]);
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            c1[t][e] += x[t][e];
+            c2[t][e] += wr * x[t][e];
+            r1 += x[t][e];
+            r2 += float(((j0 + e) & (R - 1)) + 1) * x[t][e];
+          }
+        }
+        if (d.row_chk != nullptr && (64 * t * V) < s_valid) {
+          r1 = group_sum(r1, lanes_per_kb);
+          r2 = group_sum(r2, lanes_per_kb);
+          const int kb = j0 / R;
+          if ((lane % lanes_per_kb) == 0 && j0 < s_valid) {
+            float* rc = d.row_chk + ((int64_t(z) * S + i) * nq + kb) * 2;
+            rc[0] = r1;
+            rc[1] = r2;
+          }
+        }
       }
     }
-    if (!BWD) {
-      // AP = softmax(scale * AS) over unmasked keys, in base 2
-      const float sc = d.scale * l2e;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int t = 0; t < CH; ++t)
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-          const int j = (lane + 64 * t) * V + e;
-          const bool live = j < s_valid && (!d.causal || j <= i);
-          x[t][e] = live ? x[t][e] * sc : -INFINITY;
-          mx = nanmax(mx, x[t][e]);
-        }
-      mx = wave_max(mx);
-      float sum = 0.f;
-#pragma unroll
-      for (int t = 0; t < CH; ++t)
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-          const int j = (lane + 64 * t) * V + e;
-          const bool live = j < s_valid && (!d.causal || j <= i);
-          const float ev = live ? exp2f(x[t][e] - mx) : 0.f;
-          x[t][e] = ev;
-          sum += ev;
-        }
-      sum = wave_sum(sum);
-      const float inv = 1.f / sum;
-#pragma unroll
-      for (int t = 0; t < CH; ++t)
-#pragma unroll
-        for (int e = 0; e < V; ++e) x[t][e] = Storage<T>::round(x[t][e] * inv);
-    } else {
-      // dAS = scale * AP * (dAP - D), D = sum_j AP_j dAP_j over unmasked keys
-      float dot = 0.f;
-#pragma unroll
-      for (int t = 0; t < CH; ++t)
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-          const int j = (lane + 64 * t) * V + e;
-          const bool live = j < s_valid && (!d.causal || j <= i);
-          dot += live ? x[t][e] * y[t][e] : 0.f;
-        }
-      dot = wave_sum(dot);
-#pragma unroll
-      for (int t = 0; t < CH; ++t)
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-          const int j = (lane + 64 * t) * V + e;
-          const bool live = j < s_valid && (!d.causal || j <= i);
-          x[t][e] = live ? Storage<T>::round(d.scale * x[t][e] * (y[t][e] - dot)) : 0.f;
-        }
+  };
+
+  const int n_it = R / (4 * RPI);
+  float xa[RPI][CH][V], ya[RPI][CH][V];
+  if constexpr (PF) {
+    float xb[RPI][CH][V], yb[RPI][CH][V];
+    load_rows(xa, ya, 0);
+    for (int it = 0; it < n_it; it += 2) {
+      if (it + 1 < n_it) load_rows(xb, yb, it + 1);
+      process_rows(xa, ya, it);
+      if (it + 2 < n_it) load_rows(xa, ya, it + 2);
+      if (it + 1 < n_it) process_rows(xb, yb, it + 1);
     }
-    // store, accumulate column checksums, emit row checksums per key block
-    const float wr = float(rl + 1);
-#pragma unroll
-    for (int t = 0; t < CH; ++t) {
-      const int j0 = (lane + 64 * t) * V;
-      float r1 = 0.f, r2 = 0.f;
-      if (j0 < s_valid) {
-        Vec<T>::store(dst + int64_t(i) * S + j0, x[t]);
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-          c1[t][e] += x[t][e];
-          c2[t][e] += wr * x[t][e];
-          r1 += x[t][e];
-          r2 += float(((j0 + e) & (R - 1)) + 1) * x[t][e];
-        }
-      }
-      if (d.row_chk != nullptr && (64 * t * V) < s_valid) {
-        r1 = group_sum(r1, lanes_per_kb);
-        r2 = group_sum(r2, lanes_per_kb);
-        const int kb = j0 / R;
-        if ((lane % lanes_per_kb) == 0 && j0 < s_valid) {
-          float* rc = d.row_chk + ((int64_t(z) * S + i) * nq + kb) * 2;
-          rc[0] = r1;
-          rc[1] = r2;
-        }
-      }
+  } else {
+    for (int it = 0; it < n_it; ++it) {
+      load_rows(xa, ya, it);
+      process_rows(xa, ya, it);
     }
   }
 
@@ -231,7 +264,7 @@ hipError_t launch_sm(const SoftmaxDesc& d, int dtype, hipStream_t s) {
   const size_t lds = size_t(d.S) * 2 * sizeof(float);
 #define SM_CASE(TT, CHV)                                                                      \
   if (ch <= CHV) {                                                                            \
-    auto k = softmax_kernel<TT, CHV, BWD>;                                                    \
+    auto k = softmax_kernel<TT, CHV, BWD, (CHV == 1 ? 2 : 1), (CHV <= 2)>;                    \
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),                       \
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)); \
     if (e != hipSuccess) return e;                                                            \

@@ -92,7 +92,14 @@ def compare(shape, g, o, ob, events=True):
     assert_close(g["O"], o["O"], rtol, "O")
     assert_close(g["QKV"], o["QKV"], rtol, "QKV")
     assert_close(g["CL"], o["CL"], rtol, "CL")
-    assert_close(g["AP"], o["AP"], rtol, "AP", mask=np.broadcast_to(tri, g["AP"].shape))
+    # AP inherits the storage rounding of AS through exp: the two sides may
+    # round an AS entry to adjacent values (<= 2^-7 |AS| apart), which moves
+    # AP by up to scale * 2^-7 |AS| relative, on top of AP's own rounding.
+    rtol_ap = rtol
+    if shape.dtype == "bf16":
+        as_max = float(np.max(np.abs(o["AS"][..., tri])))
+        rtol_ap = 2.0 ** -7 + o["scale"] * as_max * 2.0 ** -7
+    assert_close(g["AP"], o["AP"], rtol_ap, "AP", mask=np.broadcast_to(tri, g["AP"].shape))
     if shape.causal:  # masked probabilities are exact zeros wherever they are written
         written = np.zeros((S, S), dtype=bool)
         for i in range(S):
