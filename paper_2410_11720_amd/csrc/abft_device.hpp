@@ -15,12 +15,10 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(uint32_t(h) << 16); }
 
-// float -> bfloat16, round to nearest even; NaN becomes the quiet NaN 0x7FC0.
+// float -> bfloat16, round to nearest even (gfx950 converts in hardware,
+// v_cvt_pk_bf16_f32; NaN stays a quiet NaN, overflow becomes INF).
 __device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return bf16_t(0x7fc0u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return bf16_t(u >> 16);
+  return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f));
 }
 
 template <class T> struct Storage;
@@ -150,13 +148,17 @@ __device__ void vec_checksums(const T* v, int stride, int n, float* c1, float* c
   *c2 = r2;
 }
 
+// Detection only. The magnitude sum may include non-finite elements: any
+// INF or NaN makes r1, hence d1, non-finite, which is flagged whatever E is,
+// so the decision equals the rule with E over finite elements.
 template <class T>
 __device__ bool vec_flagged(const T* v, int stride, int n, float c1, float e_rel) {
   float r1 = 0.f, sa = 0.f;
+#pragma unroll 8
   for (int k = 0; k < n; ++k) {
     const float x = Storage<T>::load(v[k * stride]);
     r1 += x;
-    if (is_finite(x)) sa += fabsf(x);
+    sa += fabsf(x);
   }
   return flagged(c1 - r1, sa, e_rel);
 }

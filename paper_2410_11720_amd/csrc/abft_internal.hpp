@@ -68,15 +68,29 @@ struct GemmDesc {
   const abft_fault* faults = nullptr;
   int n_faults = 0;
   abft_report* report = nullptr;
+  // Split-K (dense, fp32 output only): blockIdx.z takes K slice kz and the
+  // kernel writes raw fp32 partials to C + kz*sCk and C^c to Cc + kz*sCck,
+  // without rounding, faults or verification; launch_splitk_reduce sums the
+  // slices and verifies.
+  int splitk = 1;
+  int64_t sCk = 0, sCck = 0;
 };
 
-// Tile shapes the GEMM is instantiated for.
-enum class Tile : int { T256x128 = 0, T128x128 = 1, T128x64 = 2 };
+// Tile shapes the GEMM is instantiated for (S1: one LDS stage, for short K
+// such as the head dimension, so that more workgroups fit on a CU).
+enum class Tile : int { T256x128 = 0, T128x128 = 1, T128x64 = 2, T128x128S1 = 3 };
 
 // Launch one protected (or, with no checksum operands, plain) GEMM.
 // dtype: ABFT_BF16 or ABFT_FP32 operands; c_fp32: output stored as fp32.
 hipError_t launch_gemm(const GemmDesc& g, int dtype, bool c_fp32, Layout la, Layout lb,
                        Tile tile, hipStream_t stream);
+
+// Sum the split-K partials of a protected GEMM (fixed order), apply
+// injected faults, run the column pass (recompute correction from A and B)
+// and store C. g describes the full GEMM with its final C, Rm, map, faults
+// and report; P and Pc are the partials the split launch wrote.
+hipError_t launch_splitk_reduce(const GemmDesc& g, const float* P, const float* Pc, int dtype,
+                                Layout la, Layout lb, hipStream_t stream);
 
 // Softmax over keys with checksum carry-through (fwd) and its backward.
 struct SoftmaxDesc {

@@ -47,8 +47,18 @@ struct Dims {
 struct Layout_ {
   size_t qkv, ap, cl, as, das, dcl, dqkv;
   size_t xc, xr, wvr, qkvc, vr, apc, apr, clc, clr, doc, dclc, dasc, dasr, dqkvc;
+  size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t total;
 };
+
+// K slices for a weight-gradient GEMM (M x N tiles of 128 x 128, long K):
+// enough slices to give about 512 workgroups, each slice at least 512 deep.
+int splitk_for(int64_t M, int64_t N, int64_t K) {
+  const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  int ks = 1;
+  while (tiles * ks < 512 && K / (2 * ks) >= 512 && ks < 16) ks *= 2;
+  return ks;
+}
 
 bool make_dims(const attn_abft_config* c, Dims* d) {
   if (!c || c->batch < 1 || c->seq < 1 || c->hidden < 1 || c->heads < 1) return false;
@@ -97,6 +107,13 @@ Layout_ make_layout(const Dims& d) {
   L.dasc = take(size_t(d.B) * d.nh * d.nq * 2 * d.S * f);
   L.dasr = take(size_t(d.B) * d.nh * d.S * d.nq * 2 * f);
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
+  const int ks1 = splitk_for(d.H, 3 * d.H, d.T), ks2 = splitk_for(d.H, d.H, d.T);
+  const size_t p1 = ks1 > 1 ? size_t(ks1) * d.H * 3 * d.H : 0;
+  const size_t p2 = ks2 > 1 ? size_t(ks2) * d.H * d.H : 0;
+  const size_t c1 = ks1 > 1 ? size_t(ks1) * 2 * d.nh * 3 * d.H : 0;
+  const size_t c2 = ks2 > 1 ? size_t(ks2) * 2 * d.nh * d.H : 0;
+  L.skp = take((p1 > p2 ? p1 : p2) * f);
+  L.skc = take((c1 > c2 ? c1 : c2) * f);
   L.total = off;
   return L;
 }
@@ -180,6 +197,29 @@ int num_cus() {
     hipError_t e_ = (x);                               \
     if (e_ != hipSuccess) return ABFT_ERR_HIP;         \
   } while (0)
+
+// A weight-gradient GEMM (MN-major operands, fp32 output): split over K
+// into partials when that fills the GPU better, then reduced and verified.
+hipError_t launch_wgrad(const GemmDesc& g, int dt, float* part, float* part_c, hipStream_t s) {
+  const int ks = splitk_for(g.M, g.N, g.K);
+  if (ks <= 1)
+    return launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s);
+  GemmDesc sg = g;
+  sg.splitk = ks;
+  sg.C = part;
+  sg.ldc = g.N;
+  sg.sCk = int64_t(g.M) * g.N;
+  sg.Cc = g.Ac != nullptr ? part_c : nullptr;
+  sg.ldcc = g.N;
+  sg.sCck = int64_t(2 * (g.M / g.Rm)) * g.N;
+  sg.n_faults = 0;
+  sg.faults = nullptr;
+  hipError_t e = launch_gemm(sg, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s);
+  if (e != hipSuccess) return e;
+  GemmDesc rg = g;
+  rg.splitk = ks;
+  return launch_splitk_reduce(rg, part, part_c, dt, Layout::MNMajor, Layout::MNMajor, s);
+}
 
 GemmDesc base_desc(const Params& p, const abft_fault* faults, int n_faults, abft_report* rep) {
   GemmDesc g;
@@ -307,7 +347,7 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
     }
     g.causal = cfg->causal ? 1 : 0;
     g.map.op_base = ABFT_OP_AS; g.map.nb1 = int(nh);
-    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, Tile::T128x128, s));
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, Tile::T128x128S1, s));
   }
   // AP = softmax(scale * AS) with column (and row) checksums
   if (stages & ABFT_STAGE_SOFTMAX) {
@@ -413,7 +453,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DWO;
-    CK(launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s));
+    CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
   // dAP = dCL_h V_h^T, dAP^c = dCL_h^c V_h^T
   if (stages & ABFT_STAGE_DAP) {
@@ -429,7 +469,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     }
     g.causal = cfg->causal ? 1 : 0;
     g.map.op_base = ABFT_OP_DAP; g.map.nb1 = int(nh);
-    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, Tile::T128x128, s));
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, Tile::T128x128S1, s));
   }
   const Tile td = hd == 64 ? Tile::T128x64 : Tile::T128x128;
   // dV = AP^T dCL_h, column checksums over key blocks from AP^r
@@ -508,7 +548,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DWQ; g.map.op_span = int(H);
-    CK(launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s));
+    CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
   // dX = dQKV Wqkv^T, dX^c = dQKV^c Wqkv^T
   if (stages & ABFT_STAGE_DX) {

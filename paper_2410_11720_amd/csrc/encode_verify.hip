@@ -44,17 +44,20 @@ __device__ __forceinline__ float group_sum(float x, int width) {
 }
 
 // grid: (ceil(cols / (64*V)), rows/Rb, batch). A wave owns a 64*V-column
-// slab (lane = one 16-byte chunk); the four waves of the workgroup split
-// the Rb rows of the block (wave w takes rows w, w+4, ...) and keep UN
-// rows in flight. Column checksums are combined across waves in LDS in a
+// slab (lane = one 16-byte chunk); the ENC_WAVES waves of the workgroup
+// split the Rb rows of the block (wave w takes rows w, w+ENC_WAVES, ...)
+// and keep UN rows in flight. Column checksums are combined across waves in LDS in a
 // fixed order; row checksums of each Cb-column block are reduced across
 // the Cb/V lanes that hold it (Cb/V a power of two <= 64 dividing 64*V).
+constexpr int ENC_WAVES = 8;
+
 template <class T, int V>
-__global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, int64_t cols,
-                                                    int64_t ld, int64_t bstride, int Rb, int Cb,
-                                                    float* col_chk, float* row_chk) {
+__global__ __launch_bounds__(ENC_WAVES * 64) void encode_kernel(const T* A, int64_t rows,
+                                                                int64_t cols, int64_t ld,
+                                                                int64_t bstride, int Rb, int Cb,
+                                                                float* col_chk, float* row_chk) {
   constexpr int UN = 8;
-  __shared__ float part[4][64][V][2];
+  __shared__ float part[ENC_WAVES][64][V][2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t b = blockIdx.z;
   const int64_t rb = blockIdx.y;
@@ -65,11 +68,11 @@ __global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, in
   float c1[V], c2[V];
 #pragma unroll
   for (int e = 0; e < V; ++e) c1[e] = c2[e] = 0.f;
-  for (int r0 = wave; r0 < Rb; r0 += 4 * UN) {
+  for (int r0 = wave; r0 < Rb; r0 += ENC_WAVES * UN) {
     float x[UN][V];
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
-      const int r = r0 + 4 * u;
+      const int r = r0 + ENC_WAVES * u;
       if (live && r < Rb) load_vec<T, V>(base + r * ld + c0, x[u]);
       else {
 #pragma unroll
@@ -78,13 +81,13 @@ __global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, in
     }
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
-      const int r = r0 + 4 * u;
+      const int r = r0 + ENC_WAVES * u;
 #pragma unroll
       for (int e = 0; e < V; ++e) {
         c1[e] += x[u][e];
         c2[e] += float(r + 1) * x[u][e];
       }
-      if (row_chk != nullptr && r0 + 4 * u < Rb) {   // uniform across the wave
+      if (row_chk != nullptr && r < Rb) {   // uniform across the wave
         float s1 = 0.f, s2 = 0.f;
 #pragma unroll
         for (int e = 0; e < V; ++e) {
@@ -113,7 +116,7 @@ __global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, in
 #pragma unroll
       for (int e = 0; e < V; ++e) {
         float s1 = part[0][lane][e][0], s2 = part[0][lane][e][1];
-        for (int w = 1; w < 4; ++w) {
+        for (int w = 1; w < ENC_WAVES; ++w) {
           s1 += part[w][lane][e][0];
           s2 += part[w][lane][e][1];
         }
@@ -160,12 +163,12 @@ hipError_t encode_t(const T* A, int64_t batch, int64_t rows, int64_t cols, int64
   if (col_chk != nullptr || rc_inline != nullptr) {
     if (vec) {
       dim3 grid((cols + 64 * VV - 1) / (64 * VV), rows / Rb, batch);
-      hipLaunchKernelGGL((encode_kernel<T, VV>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs, Rb,
-                         Cb, col_chk, rc_inline);
+      hipLaunchKernelGGL((encode_kernel<T, VV>), grid, dim3(ENC_WAVES * 64), 0, s, A, rows, cols,
+                         ld, bs, Rb, Cb, col_chk, rc_inline);
     } else {
       dim3 grid((cols + 63) / 64, rows / Rb, batch);
-      hipLaunchKernelGGL((encode_kernel<T, 1>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs, Rb,
-                         Cb, col_chk, rc_inline);
+      hipLaunchKernelGGL((encode_kernel<T, 1>), grid, dim3(ENC_WAVES * 64), 0, s, A, rows, cols,
+                         ld, bs, Rb, Cb, col_chk, rc_inline);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -7,14 +7,15 @@
 // (C^r = A B^r). fp32 checksums enter a bf16 MFMA as a hi + lo bf16 pair,
 // so the propagated checksum keeps ~16 significant bits.
 //
-// The epilogue rounds the tile to storage, applies injected faults, and
-// compares recomputed against propagated checksums with wavefront
-// reductions (detection, Sec. 2.3). A clean tile is stored directly. A
-// flagged tile takes the slow path in LDS: EEC-ABFT on every column vector
-// (Sec. 4.2), and for two-sided outputs the row pass with the checksum
-// refresh of Sec. 4.3, then a final check; located elements are recomputed
-// from A and B (or corrected from the checksums when the operands are not
-// trusted) and every action is appended to the device report.
+// The epilogue rounds the tile to storage and stages it in LDS, applies
+// injected faults, and compares recomputed against propagated checksums,
+// one thread per checksum vector (detection, Sec. 2.3). A flagged tile is
+// corrected in LDS: EEC-ABFT on every column vector (Sec. 4.2), and for
+// two-sided outputs the row pass with the checksum refresh of Sec. 4.3,
+// then a final check; located elements are recomputed from A and B (or
+// corrected from the checksums when the operands are not trusted) and
+// every action is appended to the device report. The tile then leaves LDS
+// in 16-byte coalesced stores.
 #include "abft_internal.hpp"
 #include "abft_device.hpp"
 
@@ -182,19 +183,6 @@ struct StripLoader {
   }
 };
 
-__device__ __forceinline__ float wsum16(float x) {  // sum over lanes with equal lane%16
-  x += __shfl_xor(x, 16, 64);
-  x += __shfl_xor(x, 32, 64);
-  return x;
-}
-__device__ __forceinline__ float wsum_row(float x) {  // sum over the 16 lanes of a row
-  x += __shfl_xor(x, 1, 64);
-  x += __shfl_xor(x, 2, 64);
-  x += __shfl_xor(x, 4, 64);
-  x += __shfl_xor(x, 8, 64);
-  return x;
-}
-
 struct EvCoord {
   int op, b, h, row, col;
 };
@@ -244,7 +232,7 @@ __device__ float recompute_elem(const GemmDesc& g, const T* A, const T* B, int m
   return s;
 }
 
-template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT>
+template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE>
 struct Gemm {
   static constexpr int BK = Mfma<T>::BK;
   static constexpr int KI = Mfma<T>::KI;
@@ -258,20 +246,19 @@ struct Gemm {
   // LDS map of the main loop (two stages)
   static constexpr int A_ELEMS = BM * LDK, B_ELEMS = BN * LDK, S_ELEMS = 16 * LDK;
   static constexpr int STAGE = A_ELEMS + B_ELEMS + (PROT ? 2 * S_ELEMS : 0);
-  static constexpr size_t MAIN_BYTES = size_t(2) * STAGE * sizeof(T);
-  // LDS map of the epilogue: region 0 (strip results and partial sums, later
-  // the slow-path tile) then region 1 (combined checksums and counters).
+  static constexpr size_t MAIN_BYTES = size_t(NSTAGE) * STAGE * sizeof(T);
+  // LDS map of the epilogue (overlays the operand stages once the K loop is
+  // done): the rounded tile [BM][LDT], the strip results, the combined
+  // propagated checksums and the correction counters.
+  static constexpr int MINB = sizeof(T) == 2 ? 32 : 16;  // smallest checksum block
+  static constexpr int TPAD = 16 / sizeof(TC);
+  static constexpr int LDT = BN + TPAD;
+  static constexpr size_t TILE_BYTES = size_t(BM) * LDT * sizeof(TC);
   static constexpr size_t CSL = 16 * BN, RSL = BM * 16;
-  static constexpr size_t COLP = (BM / 16) * BN * 3, ROWP = (BN / 16) * BM * 3;
-  static constexpr size_t R0_PART = (CSL + RSL + COLP + ROWP) * 4;
-  static constexpr size_t R0_TILE = size_t(BM) * BN * sizeof(TC);
-  static constexpr size_t R0 = R0_PART > R0_TILE ? R0_PART : R0_TILE;
-  static constexpr size_t CCV = (BM / 16) * BN * 2, RCV = BM * (BN / 16) * 2;
-  static constexpr size_t CNT = BM * (BN / 16) + (BM / 16) * BN;
-  static constexpr size_t EPI_BYTES = R0 + (CCV + RCV) * 4 + CNT * 4;
-  static constexpr size_t LDS_BYTES =
-      PROT ? (MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES)
-           : (MAIN_BYTES > R0_TILE ? MAIN_BYTES : R0_TILE);
+  static constexpr size_t CCV = (BM / MINB) * BN * 2, RCV = BM * (BN / MINB) * 2;
+  static constexpr size_t CNT = BM * (BN / MINB) + (BM / MINB) * BN;
+  static constexpr size_t EPI_BYTES = TILE_BYTES + (PROT ? (CSL + RSL + CCV + RCV + CNT) * 4 : 0);
+  static constexpr size_t LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
 
   __device__ static __forceinline__ void run(const GemmDesc& g, char* smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -286,10 +273,16 @@ struct Gemm {
     int k_lo = 0, k_hi = g.K;
     if (g.causal == 2) k_hi = min(g.K, m0 + BM);
     if (g.causal == 3) k_lo = min(g.K, m0);
+    const bool split = g.splitk > 1;
+    if (split) {  // K slice of this workgroup, a multiple of BK
+      const int kc = ((g.K + g.splitk - 1) / g.splitk + BK - 1) / BK * BK;
+      k_lo = min(g.K, int(blockIdx.z) * kc);
+      k_hi = min(g.K, k_lo + kc);
+    }
 
     const T* A = static_cast<const T*>(g.A) + b0 * g.sA0 + b1 * g.sA1;
     const T* B = static_cast<const T*>(g.B) + b0 * g.sB0 + b1 * g.sB1;
-    TC* C = static_cast<TC*>(g.C) + b0 * g.sC0 + b1 * g.sC1;
+    TC* C = static_cast<TC*>(g.C) + b0 * g.sC0 + b1 * g.sC1 + int64_t(blockIdx.z) * g.sCk;
 
     const bool cc = PROT && g.Ac != nullptr;
     const bool cr = PROT && g.Br != nullptr && n0 >= g.cr_n_begin;
@@ -321,10 +314,10 @@ struct Gemm {
 
     const int nk = k_hi > k_lo ? (k_hi - k_lo + BK - 1) / BK : 0;
     if (nk > 0) {
-      if (PROT) {  // zero both stages of both strips once; loads rewrite only used rows
+      if (PROT) {  // zero the strips of every stage once; loads rewrite only used rows
         for (int e = tid; e < 2 * S_ELEMS; e += NT) {
           lds[A_ELEMS + B_ELEMS + e] = T(0);
-          lds[STAGE + A_ELEMS + B_ELEMS + e] = T(0);
+          if (NSTAGE == 2) lds[STAGE + A_ELEMS + B_ELEMS + e] = T(0);
         }
         __syncthreads();
       }
@@ -341,7 +334,7 @@ struct Gemm {
 
     const int fr = lane & 15, fk = (lane >> 4) * FRAG;
     for (int kt = 0; kt < nk; ++kt) {
-      const int cur = kt & 1;
+      const int cur = NSTAGE == 2 ? (kt & 1) : 0;
       const bool more = kt + 1 < nk;
       if (more) {
         const int kn = k_lo + (kt + 1) * BK;
@@ -393,7 +386,8 @@ struct Gemm {
         }
       }
       if (more) {
-        T* nA = lds + (cur ^ 1) * STAGE;
+        if (NSTAGE == 1) __syncthreads();  // every wave is done reading the one stage
+        T* nA = lds + (NSTAGE == 2 ? (cur ^ 1) : 0) * STAGE;
         la.store(nA, tid);
         lb.store(nA + A_ELEMS, tid);
         if (cc) ls.store(nA + A_ELEMS + B_ELEMS, nc, tid);
@@ -402,149 +396,65 @@ struct Gemm {
       __syncthreads();
     }
 
-    // ---- epilogue: round to storage, inject faults ----
+    // ---- epilogue ----
+    // 1. round to storage and stage the tile (and the strip results) in LDS
+    TC* tile = reinterpret_cast<TC*>(smem);
+    float* CsL = reinterpret_cast<float*>(smem + TILE_BYTES);
+    float* RsL = CsL + CSL;
+    float* ccv = RsL + RSL;
+    float* rcv = ccv + CCV;
+    int* rowcnt = reinterpret_cast<int*>(rcv + RCV);
+    int* colcnt = rowcnt + BM * (BN / MINB);
 #pragma unroll
     for (int i = 0; i < IM; ++i)
 #pragma unroll
       for (int j = 0; j < JN; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[i][j][r] = Storage<TC>::round(acc[i][j][r]);
-
-    // A tile that an injected fault aims at takes the LDS path, where the
-    // fault is written into the rounded tile before any verification.
-    bool faulty = false;
-    for (int f = 0; f < g.n_faults; ++f) {
-      int fz, fm, fn;
-      if (fault_target(g.map, g.N, g.faults[f], &fz, &fm, &fn) && fz == z && fm >= m0 &&
-          fm < m0 + BM && fn >= n0 && fn < n0 + BN)
-        faulty = true;
+        for (int r = 0; r < 4; ++r)
+          tile[(wm * WM + i * 16 + (lane >> 4) * 4 + r) * LDT + wn * WN + j * 16 + fr] =
+              Storage<TC>::store(acc[i][j][r]);  // fp32 partials stay unrounded
+    if (PROT && cc) {
+#pragma unroll
+      for (int j = 0; j < JS; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          CsL[((lane >> 4) * 4 + r) * BN + wn * WN + (wm * JS + j) * 16 + fr] = accs[j][r];
     }
-
-    const int verify = PROT ? g.verify : 0;
-    bool any = false;
-    float* ccv = nullptr;
-    float* rcv = nullptr;
-    int* rowcnt = nullptr;
-    int* colcnt = nullptr;
-    const int nrb = BN / g.Rn > 0 ? BN / g.Rn : 1;   // row blocks per tile row
-    const int ncb = BM / g.Rm;                       // column blocks per tile column
-    if (PROT && (cc || cr)) {
-      float* CsL = reinterpret_cast<float*>(smem);
-      float* RsL = CsL + CSL;
-      float* colp = RsL + RSL;
-      float* rowp = colp + COLP;
-      ccv = reinterpret_cast<float*>(smem + R0);
-      rcv = ccv + CCV;
-      rowcnt = reinterpret_cast<int*>(rcv + RCV);
-      colcnt = rowcnt + BM * (BN / 16);
-
-      // strip results to LDS
-      if (cc) {
+    if (PROT && cr) {
 #pragma unroll
-        for (int j = 0; j < JS; ++j)
+      for (int i = 0; i < IS; ++i)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            CsL[((lane >> 4) * 4 + r) * BN + wn * WN + (wm * JS + j) * 16 + fr] = accs[j][r];
-      }
-      if (cr) {
-#pragma unroll
-        for (int i = 0; i < IS; ++i)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            RsL[(wm * WM + (wn * IS + i) * 16 + fr) * 16 + (lane >> 4) * 4 + r] = accr[i][r];
-      }
-      // column partial sums per segment of min(Rm, WM) rows
-      if (verify >= 1) {
-        const int seg = g.Rm < WM ? g.Rm : WM;
-#pragma unroll
-        for (int j = 0; j < JN; ++j) {
-          float s1 = 0.f, s2 = 0.f, sa = 0.f;
-#pragma unroll
-          for (int i = 0; i < IM; ++i) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int row = wm * WM + i * 16 + (lane >> 4) * 4 + r;
-              const float v = acc[i][j][r];
-              s1 += v;
-              s2 += float((row & (g.Rm - 1)) + 1) * v;
-              sa += is_finite(v) ? fabsf(v) : 0.f;
-            }
-            if (((i + 1) * 16) % seg == 0) {
-              const float t1 = wsum16(s1), t2 = wsum16(s2), ta = wsum16(sa);
-              const int c = (wm * WM + (i + 1) * 16 - seg) / 16;
-              if (lane < 16) {
-                float* p = colp + (c * BN + wn * WN + j * 16 + lane) * 3;
-                p[0] = t1;
-                p[1] = t2;
-                p[2] = ta;
-              }
-              s1 = s2 = sa = 0.f;
-            }
-          }
-        }
-      }
-      if (verify == 2) {
-        const int seg = g.Rn < WN ? g.Rn : WN;
-#pragma unroll
-        for (int i = 0; i < IM; ++i) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = wm * WM + i * 16 + (lane >> 4) * 4 + r;
-            float s1 = 0.f, s2 = 0.f, sa = 0.f;
-#pragma unroll
-            for (int j = 0; j < JN; ++j) {
-              const int col = wn * WN + j * 16 + fr;
-              const float v = acc[i][j][r];
-              s1 += v;
-              s2 += float((col & (g.Rn - 1)) + 1) * v;
-              sa += is_finite(v) ? fabsf(v) : 0.f;
-              if (((j + 1) * 16) % seg == 0) {
-                const float t1 = wsum_row(s1), t2 = wsum_row(s2), ta = wsum_row(sa);
-                const int c = (wn * WN + (j + 1) * 16 - seg) / 16;
-                if (fr == 0) {
-                  float* p = rowp + (c * BM + row) * 3;
-                  p[0] = t1;
-                  p[1] = t2;
-                  p[2] = ta;
-                }
-                s1 = s2 = sa = 0.f;
-              }
-            }
-          }
-        }
-      }
+        for (int r = 0; r < 4; ++r)
+          RsL[(wm * WM + (wn * IS + i) * 16 + fr) * 16 + (lane >> 4) * 4 + r] = accr[i][r];
+    }
+    // injected faults (test-only): written into the rounded tile before any
+    // verification
+    if (g.n_faults > 0 && !split) {
       __syncthreads();
-      // combine: propagated checksums (hi + lo) and detection per vector
-      bool my_flag = false;
-      if (cc) {
-        const int segm = g.Rm < WM ? g.Rm : WM;
-        for (int v = tid; v < ncb * BN; v += NT) {
-          const int blk = v / BN, n = v % BN;
-          float c1, c2;
-          if constexpr (sizeof(T) == 2) {
-            c1 = CsL[(2 * blk) * BN + n] + CsL[(nc + 2 * blk) * BN + n];
-            c2 = CsL[(2 * blk + 1) * BN + n] + CsL[(nc + 2 * blk + 1) * BN + n];
-          } else {
-            c1 = CsL[(2 * blk) * BN + n];
-            c2 = CsL[(2 * blk + 1) * BN + n];
-          }
-          ccv[v * 2] = c1;
-          ccv[v * 2 + 1] = c2;
-          if (verify >= 1 && m0 + blk * g.Rm < g.M && n0 + n < g.N && n0 + n >= g.verify_n_lo &&
-              n0 + n < g.verify_n_hi) {
-            float s1 = 0.f, sa = 0.f;
-            for (int s = 0; s < g.Rm / segm; ++s) {
-              const int c = (blk * g.Rm + s * segm) / 16;
-              s1 += colp[(c * BN + n) * 3];
-              sa += colp[(c * BN + n) * 3 + 2];
-            }
-            if (flagged(c1 - s1, sa, g.e_rel)) my_flag = true;
-          }
+      if (tid == 0) {
+        for (int f = 0; f < g.n_faults; ++f) {
+          const abft_fault ft = g.faults[f];
+          int fz, fm, fn;
+          if (fault_target(g.map, g.N, ft, &fz, &fm, &fn) && fz == z && fm >= m0 &&
+              fm < m0 + BM && fn >= n0 && fn < n0 + BN)
+            tile[(fm - m0) * LDT + fn - n0] = Storage<TC>::store(Storage<TC>::round(ft.value));
         }
       }
-      if (cr) {
-        const int segn = g.Rn < WN ? g.Rn : WN;
-        for (int u = tid; u < BM * nrb; u += NT) {
+    }
+    __syncthreads();
+
+    // 2. detection: recomputed against propagated checksums, one thread per
+    //    vector (Sec. 2.3 detection rule)
+    const int verify = (PROT && cc && !split) ? g.verify : 0;
+    const int nrb = cr ? BN / g.Rn : 0;   // row blocks per tile row
+    const int ncb = cc ? BM / g.Rm : 0;   // column blocks per tile column
+    if (PROT && (cc || cr)) {
+      bool my_flag = false;
+      // column vectors then row vectors, spread over all threads
+      const int ncv = ncb * BN, nrv = BM * nrb;
+      for (int w = tid; w < ncv + nrv; w += NT) {
+        if (w >= ncv) {
+          const int u = w - ncv;
           const int row = u / nrb, rb = u % nrb;
           float c1, c2;
           if constexpr (sizeof(T) == 2) {
@@ -556,50 +466,53 @@ struct Gemm {
           }
           rcv[u * 2] = c1;
           rcv[u * 2 + 1] = c2;
-          if (verify == 2 && m0 + row < g.M && n0 + rb * g.Rn < g.N) {
-            float s1 = 0.f, sa = 0.f;
-            for (int s = 0; s < g.Rn / segn; ++s) {
-              const int c = (rb * g.Rn + s * segn) / 16;
-              s1 += rowp[(c * BM + row) * 3];
-              sa += rowp[(c * BM + row) * 3 + 2];
-            }
-            if (flagged(c1 - s1, sa, g.e_rel)) my_flag = true;
-          }
+          if (verify == 2 && m0 + row < g.M && n0 + rb * g.Rn < g.N)
+            my_flag |= vec_flagged<TC>(tile + row * LDT + rb * g.Rn, 1, g.Rn, c1, g.e_rel);
+          continue;
         }
+        const int v = w;
+        const int blk = v / BN, n = v % BN;
+        float c1, c2;
+        if constexpr (sizeof(T) == 2) {
+          c1 = CsL[(2 * blk) * BN + n] + CsL[(nc + 2 * blk) * BN + n];
+          c2 = CsL[(2 * blk + 1) * BN + n] + CsL[(nc + 2 * blk + 1) * BN + n];
+        } else {
+          c1 = CsL[(2 * blk) * BN + n];
+          c2 = CsL[(2 * blk + 1) * BN + n];
+        }
+        ccv[v * 2] = c1;
+        ccv[v * 2 + 1] = c2;
+        if (verify >= 1 && m0 + blk * g.Rm < g.M && n0 + n < g.N && n0 + n >= g.verify_n_lo &&
+            n0 + n < g.verify_n_hi)
+          my_flag |= vec_flagged<TC>(tile + blk * g.Rm * LDT + n, LDT, g.Rm, c1, g.e_rel);
       }
-      any = __syncthreads_or(my_flag);
+      // 3. correction, only for a tile with a flagged vector
+      if (__syncthreads_or(my_flag))
+        passes(g, tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, rowcnt, colcnt, nrb, ncb, verify,
+               tid);
     }
 
-    if (!any && !faulty) {
-      // fast path: store straight from registers
-#pragma unroll
-      for (int i = 0; i < IM; ++i)
-#pragma unroll
-        for (int j = 0; j < JN; ++j)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + r;
-            const int n = n0 + wn * WN + j * 16 + fr;
-            if (m < g.M && n < g.N) C[int64_t(m) * g.ldc + n] = Storage<TC>::store(acc[i][j][r]);
-          }
-    } else {
-      TC* tile = reinterpret_cast<TC*>(smem);  // overlays dead partial sums / operand stages
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < IM; ++i)
-#pragma unroll
-        for (int j = 0; j < JN; ++j)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            tile[(wm * WM + i * 16 + (lane >> 4) * 4 + r) * BN + wn * WN + j * 16 + fr] =
-                Storage<TC>::store(acc[i][j][r]);
-      slow_path(g, tile, A, B, C, z, m0, n0, k_lo, k_hi, ccv, rcv, rowcnt, colcnt, nrb, ncb,
-                cc ? verify : 0, tid);
+    // 4. store the tile with 16-byte coalesced chunks
+    {
+      constexpr int V = 16 / sizeof(TC);
+      constexpr int CPR = BN / V;  // chunks per tile row
+      for (int c = tid; c < BM * CPR; c += NT) {
+        const int row = c / CPR, col = (c % CPR) * V;
+        const int m = m0 + row, n = n0 + col;
+        if (m >= g.M) continue;
+        const TC* srcp = tile + row * LDT + col;
+        TC* dstp = C + int64_t(m) * g.ldc + n;
+        if (n + V <= g.N) {
+          *reinterpret_cast<uint4*>(dstp) = *reinterpret_cast<const uint4*>(srcp);
+        } else {
+          for (int e = 0; e < V && n + e < g.N; ++e) dstp[e] = srcp[e];
+        }
+      }
     }
 
     // propagated checksums for the consumers downstream
     if (PROT && cc && g.Cc != nullptr) {
-      float* Cc = g.Cc + b0 * g.sCc0 + b1 * g.sCc1;
+      float* Cc = g.Cc + b0 * g.sCc0 + b1 * g.sCc1 + int64_t(blockIdx.z) * g.sCck;
       for (int v = tid; v < ncb * BN; v += NT) {
         const int blk = v / BN, n = v % BN;
         if (m0 + blk * g.Rm < g.M && n0 + n < g.N) {
@@ -620,39 +533,15 @@ struct Gemm {
     }
   }
 
-  // Slow path: the tile goes to LDS and EEC-ABFT runs there (one thread per
-  // vector, as in the paper's Fig. 4), then the tile is stored.
-  __device__ static __forceinline__ void slow_path(
-      const GemmDesc& g, TC* tile, const T* A, const T* B, TC* C, int z, int m0, int n0,
-      int k_lo, int k_hi, float* ccv, float* rcv, int* rowcnt, int* colcnt, int nrb, int ncb,
-      int verify, int tid) {
-    // injected faults (test-only), after rounding to storage
-    if (tid == 0) {
-      for (int f = 0; f < g.n_faults; ++f) {
-        const abft_fault ft = g.faults[f];
-        int fz, fm, fn;
-        if (fault_target(g.map, g.N, ft, &fz, &fm, &fn) && fz == z && fm >= m0 &&
-            fm < m0 + BM && fn >= n0 && fn < n0 + BN)
-          tile[(fm - m0) * BN + fn - n0] = Storage<TC>::store(Storage<TC>::round(ft.value));
-      }
-    }
-    if (verify >= 1)
-      for (int e = tid; e < BM * (BN / 16) + (BM / 16) * BN; e += NT) rowcnt[e] = 0;
-    __syncthreads();
-    if (verify >= 1) passes(g, tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, rowcnt, colcnt, nrb,
-                            ncb, verify, tid);
-    for (int e = tid; e < BM * BN; e += NT) {
-      const int row = e / BN, col = e % BN;
-      if (m0 + row < g.M && n0 + col < g.N) C[int64_t(m0 + row) * g.ldc + n0 + col] = tile[e];
-    }
-  }
-
-  // EEC-ABFT on the LDS tile, one thread per vector (as in the paper's Fig. 4).
+  // EEC-ABFT on the LDS tile, one thread per vector (as in the paper's
+  // Fig. 4): column pass, refresh of 1R-corrupted row checksums, row pass,
+  // refresh of 1C-corrupted column checksums, final check (Sec. 4.2, 4.3).
   __device__ static __forceinline__ void passes(
       const GemmDesc& g, TC* tile, const T* A, const T* B, int z, int m0, int n0, int k_lo,
       int k_hi, float* ccv, float* rcv, int* rowcnt, int* colcnt, int nrb, int ncb, int verify,
       int tid) {
-
+    for (int e = tid; e < BM * (BN / MINB) + (BM / MINB) * BN; e += NT) rowcnt[e] = 0;
+    __syncthreads();
     const int Rm = g.Rm, Rn = g.Rn;
     auto in_col = [&](int blk, int n) {
       return m0 + blk * Rm < g.M && n0 + n < g.N && n0 + n >= g.verify_n_lo &&
@@ -661,7 +550,7 @@ struct Gemm {
     auto in_row = [&](int row, int rb) { return m0 + row < g.M && n0 + rb * Rn < g.N; };
     auto correct = [&](int lr, int lc, const TC* vec, int stride, int nvec, int idx, float c1,
                        float d1) {
-      const float old = Storage<TC>::load(tile[lr * BN + lc]);
+      const float old = Storage<TC>::load(tile[lr * LDT + lc]);
       int action;
       float val;
       if (g.recompute) {
@@ -670,7 +559,7 @@ struct Gemm {
       } else {
         val = fix_by_checksum<TC>(vec, stride, nvec, idx, c1, d1, g.tc, &action);
       }
-      tile[lr * BN + lc] = Storage<TC>::store(val);
+      tile[lr * LDT + lc] = Storage<TC>::store(val);
       const EvCoord ec = map_coord(g.map, z, m0 + lr, n0 + lc);
       record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(old, g.tn), action, old);
     };
@@ -679,11 +568,11 @@ struct Gemm {
     for (int v = tid; v < ncb * BN; v += NT) {
       const int blk = v / BN, n = v % BN;
       if (!in_col(blk, n)) continue;
-      const TC* vec = tile + blk * Rm * BN + n;
-      const EecResult res = eec_locate<TC>(vec, BN, Rm, ccv[v * 2], ccv[v * 2 + 1], g.e_rel, g.tn);
+      const TC* vec = tile + blk * Rm * LDT + n;
+      const EecResult res = eec_locate<TC>(vec, LDT, Rm, ccv[v * 2], ccv[v * 2 + 1], g.e_rel, g.tn);
       if (res.status == EEC_LOCATED) {
         const int lr = blk * Rm + res.index;
-        correct(lr, n, vec, BN, Rm, res.index, ccv[v * 2], res.d1);
+        correct(lr, n, vec, LDT, Rm, res.index, ccv[v * 2], res.d1);
         if (verify == 2) atomicAdd(&rowcnt[lr * nrb + n / Rn], 1);
       }
     }
@@ -693,14 +582,14 @@ struct Gemm {
       for (int u = tid; u < BM * nrb; u += NT) {
         const int row = u / nrb, rb = u % nrb;
         if (in_row(row, rb) && rowcnt[u] >= 2)
-          vec_checksums<TC>(tile + row * BN + rb * Rn, 1, Rn, &rcv[u * 2], &rcv[u * 2 + 1]);
+          vec_checksums<TC>(tile + row * LDT + rb * Rn, 1, Rn, &rcv[u * 2], &rcv[u * 2 + 1]);
       }
       __syncthreads();
       // 2b. row pass
       for (int u = tid; u < BM * nrb; u += NT) {
         const int row = u / nrb, rb = u % nrb;
         if (!in_row(row, rb)) continue;
-        const TC* vec = tile + row * BN + rb * Rn;
+        const TC* vec = tile + row * LDT + rb * Rn;
         const EecResult res = eec_locate<TC>(vec, 1, Rn, rcv[u * 2], rcv[u * 2 + 1], g.e_rel, g.tn);
         if (res.status == EEC_LOCATED) {
           const int lc = rb * Rn + res.index;
@@ -713,7 +602,7 @@ struct Gemm {
       for (int v = tid; v < ncb * BN; v += NT) {
         const int blk = v / BN, n = v % BN;
         if (in_col(blk, n) && colcnt[v] >= 2)
-          vec_checksums<TC>(tile + blk * Rm * BN + n, BN, Rm, &ccv[v * 2], &ccv[v * 2 + 1]);
+          vec_checksums<TC>(tile + blk * Rm * LDT + n, LDT, Rm, &ccv[v * 2], &ccv[v * 2 + 1]);
       }
       __syncthreads();
     }
@@ -721,7 +610,7 @@ struct Gemm {
     for (int v = tid; v < ncb * BN; v += NT) {
       const int blk = v / BN, n = v % BN;
       if (!in_col(blk, n)) continue;
-      if (vec_flagged<TC>(tile + blk * Rm * BN + n, BN, Rm, ccv[v * 2], g.e_rel)) {
+      if (vec_flagged<TC>(tile + blk * Rm * LDT + n, LDT, Rm, ccv[v * 2], g.e_rel)) {
         const EvCoord ec = map_coord(g.map, z, m0 + blk * Rm, n0 + n);
         record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, ABFT_KIND_NONE,
                      ABFT_ACT_UNCORRECTABLE, 0.f);
@@ -731,7 +620,7 @@ struct Gemm {
       for (int u = tid; u < BM * nrb; u += NT) {
         const int row = u / nrb, rb = u % nrb;
         if (!in_row(row, rb)) continue;
-        if (vec_flagged<TC>(tile + row * BN + rb * Rn, 1, Rn, rcv[u * 2], g.e_rel)) {
+        if (vec_flagged<TC>(tile + row * LDT + rb * Rn, 1, Rn, rcv[u * 2], g.e_rel)) {
           const EvCoord ec = map_coord(g.map, z, m0 + row, n0 + rb * Rn);
           record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, ABFT_KIND_NONE,
                        ABFT_ACT_UNCORRECTABLE, 0.f);
@@ -742,16 +631,16 @@ struct Gemm {
   }
 };
 
-template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT>
+template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE>
 __global__ __launch_bounds__(NT) void gemm_kernel(GemmDesc g) {
   extern __shared__ __align__(16) char smem[];
-  Gemm<T, TC, AK, BKM, BM, BN, PROT>::run(g, smem);
+  Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>::run(g, smem);
 }
 
-template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT>
+template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE = 2>
 hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
-  using G = Gemm<T, TC, AK, BKM, BM, BN, PROT>;
-  auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT>;
+  using G = Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
+  auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
   const size_t lds = G::LDS_BYTES;
   if (lds > 160 * 1024) return hipErrorInvalidValue;  // this tile does not fit gfx950 LDS
   static bool attr_set = false;  // per instantiation; harmless if repeated
@@ -762,7 +651,7 @@ hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
     attr_set = true;
   }
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  dim3 grid(tiles, g.nb0 * g.nb1);
+  dim3 grid(tiles, g.nb0 * g.nb1, g.splitk > 1 ? g.splitk : 1);
   if (tiles == 0 || g.nb0 * g.nb1 == 0) return hipSuccess;
   hipLaunchKernelGGL(kern, grid, dim3(NT), lds, s, g);
   return hipGetLastError();
@@ -774,6 +663,7 @@ hipError_t launch_tile(const GemmDesc& g, Tile tile, hipStream_t s) {
     case Tile::T256x128: return launch_t<T, TC, AK, BKM, 256, 128, PROT>(g, s);
     case Tile::T128x128: return launch_t<T, TC, AK, BKM, 128, 128, PROT>(g, s);
     case Tile::T128x64: return launch_t<T, TC, AK, BKM, 128, 64, PROT>(g, s);
+    case Tile::T128x128S1: return launch_t<T, TC, AK, BKM, 128, 128, PROT, 1>(g, s);
   }
   return hipErrorInvalidValue;
 }
@@ -787,7 +677,94 @@ hipError_t launch_layout(const GemmDesc& g, Layout la, Layout lb, Tile tile, hip
   return hipErrorInvalidValue;  // (MN-major A, K-major B) is not used by the layer
 }
 
+// Split-K reduction: every element is the fixed-order sum of its K slices
+// (deterministic); a thread sums four consecutive columns. Injected faults
+// land on the summed (stored) value.
+__global__ __launch_bounds__(256) void splitk_sum_kernel(GemmDesc g, const float* P) {
+  const int64_t q = int64_t(blockIdx.x) * 256 + threadIdx.x;  // float4 index
+  const int64_t MN = int64_t(g.M) * g.N;
+  if (q * 4 >= MN) return;
+  const int m = int(q * 4 / g.N), n = int(q * 4 % g.N);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s = 0; s < g.splitk; ++s) {
+    const float4 v = reinterpret_cast<const float4*>(P + s * MN)[q];
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  float out[4] = {acc.x, acc.y, acc.z, acc.w};
+  for (int f = 0; f < g.n_faults; ++f) {
+    int fz, fm, fn;
+    if (fault_target(g.map, g.N, g.faults[f], &fz, &fm, &fn) && fm == m && fn >= n && fn < n + 4)
+      out[fn - n] = g.faults[f].value;
+  }
+  float* C = static_cast<float*>(g.C) + int64_t(m) * g.ldc + n;
+  *reinterpret_cast<float4*>(C) = make_float4(out[0], out[1], out[2], out[3]);
+}
+
+// Column pass on a reduced split-K output: one thread per Rm-row column
+// vector; it sums the checksum slices, checks the stored column, and on a
+// flag runs EEC-ABFT (Sec. 4.2) with recompute correction and the final
+// check. Only the owning thread reads or writes its column.
+template <class T, bool AK, bool BKM>
+__global__ __launch_bounds__(256) void splitk_check_kernel(GemmDesc g, const float* Pc) {
+  const int64_t v = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int nrb = g.M / g.Rm;
+  if (v >= int64_t(nrb) * g.N) return;
+  const int rb = int(v / g.N), n = int(v % g.N);
+  const int64_t slc = int64_t(2 * nrb) * g.N;
+  float c1 = 0.f, c2 = 0.f;
+  for (int s = 0; s < g.splitk; ++s) {
+    c1 += Pc[s * slc + int64_t(2 * rb) * g.N + n];
+    c2 += Pc[s * slc + int64_t(2 * rb + 1) * g.N + n];
+  }
+  float* col = static_cast<float*>(g.C) + int64_t(rb) * g.Rm * g.ldc + n;
+  const int ld = int(g.ldc);
+  if (!vec_flagged<float>(col, ld, g.Rm, c1, g.e_rel)) return;
+  const EecResult res = eec_locate<float>(col, ld, g.Rm, c1, c2, g.e_rel, g.tn);
+  if (res.status == EEC_LOCATED) {
+    const int lr = res.index;
+    const float old = col[int64_t(lr) * ld];
+    int action;
+    float val;
+    if (g.recompute) {
+      val = recompute_elem<T, float, AK, BKM>(g, static_cast<const T*>(g.A),
+                                             static_cast<const T*>(g.B), rb * g.Rm + lr, n, 0, g.K);
+      action = ABFT_ACT_RECOMPUTE;
+    } else {
+      val = fix_by_checksum<float>(col, ld, g.Rm, lr, c1, res.d1, g.tc, &action);
+    }
+    col[int64_t(lr) * ld] = val;
+    const EvCoord ec = map_coord(g.map, 0, rb * g.Rm + lr, n);
+    record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(old, g.tn), action, old);
+  }
+  if (vec_flagged<float>(col, ld, g.Rm, c1, g.e_rel)) {
+    const EvCoord ec = map_coord(g.map, 0, rb * g.Rm, n);
+    record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, ABFT_KIND_NONE,
+                 ABFT_ACT_UNCORRECTABLE, 0.f);
+  }
+}
+
+template <class T>
+hipError_t reduce_t(const GemmDesc& g, const float* P, const float* Pc, Layout la, Layout lb,
+                    hipStream_t s) {
+  if (la != Layout::MNMajor || lb != Layout::MNMajor) return hipErrorInvalidValue;
+  if (g.N % 4 != 0 || g.ldc != g.N) return hipErrorInvalidValue;
+  const int64_t quads = int64_t(g.M) * g.N / 4;
+  hipLaunchKernelGGL(splitk_sum_kernel, dim3((quads + 255) / 256), dim3(256), 0, s, g, P);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || g.verify < 1 || g.Ac == nullptr) return e;
+  const int64_t nv = int64_t(g.M / g.Rm) * g.N;
+  hipLaunchKernelGGL((splitk_check_kernel<T, false, false>), dim3((nv + 255) / 256), dim3(256), 0,
+                     s, g, Pc);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_splitk_reduce(const GemmDesc& g, const float* P, const float* Pc, int dtype,
+                                Layout la, Layout lb, hipStream_t stream) {
+  if (dtype == ABFT_FP32) return reduce_t<float>(g, P, Pc, la, lb, stream);
+  return reduce_t<bf16_t>(g, P, Pc, la, lb, stream);
+}
 
 hipError_t launch_gemm(const GemmDesc& g, int dtype, bool c_fp32, Layout la, Layout lb,
                        Tile tile, hipStream_t stream) {

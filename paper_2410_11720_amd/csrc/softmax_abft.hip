@@ -147,7 +147,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
           for (int e = 0; e < V; ++e) {
             const int j = (lane + 64 * t) * V + e;
             const bool live = j < s_valid && (!d.causal || j <= i);
-            const float ev = live ? exp2f(x[t][e] - mx) : 0.f;
+            const float ev = live ? __builtin_amdgcn_exp2f(x[t][e] - mx) : 0.f;
             x[t][e] = ev;
             sum += ev;
           }

@@ -143,6 +143,7 @@ SHAPES = [
     W.make_shape(1, 384, 256, 4, causal=True, block_rows=64),  # R = 64, seq not a power of two
     W.make_shape(2, 192, 128, 2, causal=True, block_rows=64),  # seq 192: ragged score tiles
     W.make_shape(1, 256, 64, 1, causal=False, block_rows=32),
+    W.make_shape(4, 512, 128, 2, causal=True),                 # long K: split-K weight gradients
 ]
 
 
@@ -169,6 +170,14 @@ def test_bf16_multi_fault_step():
     faults = W.draw_faults(shape, 4242, 16, W.ALL_OPS, ["inf", "nan", "1e6", "1e10", "1e30"])
     g, o, ob = run_pair(shape, faults)
     got = sorted(e[:5] for e in g["rep_f"]["events"] + g["rep_b"]["events"])
+    assert got == sorted(f.as_tuple()[:5] for f in faults)
+
+
+def test_bf16_split_k_weight_gradients_with_faults():
+    shape = W.make_shape(4, 512, 128, 2, causal=True)
+    faults = W.draw_faults(shape, 321, 4, ["dWQ", "dWK", "dWV", "dWO"], ["inf", "nan", "1e10", "1e6"])
+    g, o, ob = run_pair(shape, faults)
+    got = sorted(e[:5] for e in g["rep_b"]["events"])
     assert got == sorted(f.as_tuple()[:5] for f in faults)
 
 
