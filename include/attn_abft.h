@@ -93,7 +93,7 @@ typedef struct {
   int32_t causal;                    /* 1: key j > query i is masked          */
   int32_t block_rows;                /* R: checksum block on token axes; a power
                                         of two, 16 <= R <= 128, R | seq        */
-  float   scale;                     /* softmax scale; 0 -> 1/sqrt(head_dim)   */
+  float   scale;                     /* softmax scale; <= 0 -> 1/sqrt(head_dim) */
   float   t_near_inf;                /* Sec. 4.2, default 1e10 (compared as stored) */
   float   t_correct;                 /* Sec. 4.2, default 1e5                   */
   float   e_rel;                     /* detection bound E = e_rel * sum|v|; 0 ->

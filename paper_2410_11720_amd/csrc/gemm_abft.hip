@@ -232,6 +232,61 @@ __device__ float recompute_elem(const GemmDesc& g, const T* A, const T* B, int m
   return s;
 }
 
+// Work item of a workgroup. The grid is one-dimensional and the hardware
+// deals consecutive workgroup ids round-robin to the 8 XCDs (each with its
+// own L2), so the decode decides both the balance and the L2 locality:
+//  - batched GEMMs (one per batch x head) put the head index fastest, so
+//    each XCD gets whole heads (their operands stay in its L2) and every
+//    XCD sees the same mix of tile costs;
+//  - causally trimmed K ranges run the most expensive tile rows first;
+//  - a causal score GEMM (whole tiles above the diagonal skipped)
+//    enumerates only the lower-triangle tiles;
+//  - unbatched GEMMs give each XCD one contiguous range of tiles (rows of
+//    tiles sharing their A rows; split-K slices sharing their K range).
+struct TileIdx {
+  int mt, nt, bh, ks;
+};
+
+__host__ __device__ inline bool tri_tiles(const GemmDesc& g, int bm, int bn) {
+  return g.causal == 1 && bm == bn && g.M == g.N;
+}
+
+template <int BM, int BN>
+__device__ __forceinline__ TileIdx tile_of(const GemmDesc& g) {
+  const int ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
+  const int nb = g.nb0 * g.nb1;
+  const int lin = blockIdx.x;
+  TileIdx t;
+  int r;
+  if (nb == 1) {
+    const int total = gridDim.x, q = total / 8, rem = total % 8;
+    const int x = lin % 8, j = lin / 8;
+    const int v = x * q + min(x, rem) + j;
+    const int per = tri_tiles(g, BM, BN) ? ntm * (ntm + 1) / 2 : ntm * ntn;
+    t.bh = 0;
+    t.ks = v / per;
+    r = v % per;
+  } else {
+    t.bh = lin % nb;
+    t.ks = 0;
+    r = lin / nb;
+  }
+  if (tri_tiles(g, BM, BN)) {  // r -> (mt, nt) with nt <= mt
+    int mt = int((sqrtf(8.f * r + 1.f) - 1.f) * 0.5f);
+    while ((mt + 1) * (mt + 2) / 2 <= r) ++mt;
+    while (mt * (mt + 1) / 2 > r) --mt;
+    t.mt = mt;
+    t.nt = r - mt * (mt + 1) / 2;
+  } else if (g.causal == 2) {  // K range grows with the tile row
+    t.mt = ntm - 1 - r / ntn;
+    t.nt = r % ntn;
+  } else {
+    t.mt = r / ntn;
+    t.nt = r % ntn;
+  }
+  return t;
+}
+
 template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE>
 struct Gemm {
   static constexpr int BK = Mfma<T>::BK;
@@ -243,10 +298,16 @@ struct Gemm {
   static_assert(IM >= 2 && JN >= 2, "tile too small");
   static constexpr int FRAG = KI / 4;  // operand elements per lane
 
-  // LDS map of the main loop (two stages)
+  // LDS map of the main loop: per stage the A and B tiles, then the
+  // checksum strips the GEMM carries (column strip, row strip), so a GEMM
+  // with one strip keeps two workgroups per CU.
   static constexpr int A_ELEMS = BM * LDK, B_ELEMS = BN * LDK, S_ELEMS = 16 * LDK;
-  static constexpr int STAGE = A_ELEMS + B_ELEMS + (PROT ? 2 * S_ELEMS : 0);
-  static constexpr size_t MAIN_BYTES = size_t(NSTAGE) * STAGE * sizeof(T);
+  __host__ __device__ static constexpr int stage_elems(bool cc, bool cr) {
+    return A_ELEMS + B_ELEMS + (PROT ? ((cc ? S_ELEMS : 0) + (cr ? S_ELEMS : 0)) : 0);
+  }
+  __host__ __device__ static constexpr size_t main_bytes(bool cc, bool cr) {
+    return size_t(NSTAGE) * stage_elems(cc, cr) * sizeof(T);
+  }
   // LDS map of the epilogue (overlays the operand stages once the K loop is
   // done): the rounded tile [BM][LDT], the strip results, the combined
   // propagated checksums and the correction counters.
@@ -258,15 +319,16 @@ struct Gemm {
   static constexpr size_t CCV = (BM / MINB) * BN * 2, RCV = BM * (BN / MINB) * 2;
   static constexpr size_t CNT = BM * (BN / MINB) + (BM / MINB) * BN;
   static constexpr size_t EPI_BYTES = TILE_BYTES + (PROT ? (CSL + RSL + CCV + RCV + CNT) * 4 : 0);
-  static constexpr size_t LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+  __host__ __device__ static constexpr size_t lds_bytes(bool cc, bool cr) {
+    return main_bytes(cc, cr) > EPI_BYTES ? main_bytes(cc, cr) : EPI_BYTES;
+  }
 
   __device__ static __forceinline__ void run(const GemmDesc& g, char* smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int ntn = (g.N + BN - 1) / BN;
-    const int mt = blockIdx.x / ntn, nt = blockIdx.x % ntn;
-    const int m0 = mt * BM, n0 = nt * BN;
-    const int z = blockIdx.y;
+    const TileIdx ti = tile_of<BM, BN>(g);
+    const int m0 = ti.mt * BM, n0 = ti.nt * BN;
+    const int z = ti.bh, kslice = ti.ks;
     const int b0 = z / g.nb1, b1 = z % g.nb1;
     if (g.causal == 1 && n0 > m0 + BM - 1) return;  // whole tile above the diagonal
 
@@ -276,13 +338,13 @@ struct Gemm {
     const bool split = g.splitk > 1;
     if (split) {  // K slice of this workgroup, a multiple of BK
       const int kc = ((g.K + g.splitk - 1) / g.splitk + BK - 1) / BK * BK;
-      k_lo = min(g.K, int(blockIdx.z) * kc);
+      k_lo = min(g.K, kslice * kc);
       k_hi = min(g.K, k_lo + kc);
     }
 
     const T* A = static_cast<const T*>(g.A) + b0 * g.sA0 + b1 * g.sA1;
     const T* B = static_cast<const T*>(g.B) + b0 * g.sB0 + b1 * g.sB1;
-    TC* C = static_cast<TC*>(g.C) + b0 * g.sC0 + b1 * g.sC1 + int64_t(blockIdx.z) * g.sCk;
+    TC* C = static_cast<TC*>(g.C) + b0 * g.sC0 + b1 * g.sC1 + int64_t(kslice) * g.sCk;
 
     const bool cc = PROT && g.Ac != nullptr;
     const bool cr = PROT && g.Br != nullptr && n0 >= g.cr_n_begin;
@@ -296,6 +358,10 @@ struct Gemm {
     const float* Br = cr ? g.Br + b0 * g.sBr0 + b1 * g.sBr1 : nullptr;
 
     T* lds = reinterpret_cast<T*>(smem);
+    // stage stride and row-strip offset follow the strips this GEMM carries
+    const bool g_cc = PROT && g.Ac != nullptr, g_cr = PROT && g.Br != nullptr;
+    const int STAGE = stage_elems(g_cc, g_cr);
+    const int r_off = g_cc ? S_ELEMS : 0;
     TileLoader<T, AK, BM> la;
     TileLoader<T, BKM, BN> lb;
     StripLoader<T, AK> ls;
@@ -314,8 +380,9 @@ struct Gemm {
 
     const int nk = k_hi > k_lo ? (k_hi - k_lo + BK - 1) / BK : 0;
     if (nk > 0) {
-      if (PROT) {  // zero the strips of every stage once; loads rewrite only used rows
-        for (int e = tid; e < 2 * S_ELEMS; e += NT) {
+      if (PROT && (cc || cr)) {  // zero the strips of every stage once; loads rewrite only used rows
+        const int ns = (cc ? S_ELEMS : 0) + (cr ? S_ELEMS : 0);
+        for (int e = tid; e < ns; e += NT) {
           lds[A_ELEMS + B_ELEMS + e] = T(0);
           if (NSTAGE == 2) lds[STAGE + A_ELEMS + B_ELEMS + e] = T(0);
         }
@@ -328,7 +395,7 @@ struct Gemm {
       la.store(lds, tid);
       lb.store(lds + A_ELEMS, tid);
       if (cc) ls.store(lds + A_ELEMS + B_ELEMS, nc, tid);
-      if (cr) lr.store(lds + A_ELEMS + B_ELEMS + S_ELEMS, nq, tid);
+      if (cr) lr.store(lds + A_ELEMS + B_ELEMS + r_off, nq, tid);
       __syncthreads();
     }
 
@@ -346,7 +413,7 @@ struct Gemm {
       const T* sA = lds + cur * STAGE;
       const T* sB = sA + A_ELEMS;
       const T* sS = sB + B_ELEMS;
-      const T* sR = sS + S_ELEMS;
+      const T* sR = sS + r_off;
 #pragma unroll
       for (int kk = 0; kk < BK; kk += KI) {
         typename Mfma<T>::frag af[IM], bfr[JN];
@@ -391,7 +458,7 @@ struct Gemm {
         la.store(nA, tid);
         lb.store(nA + A_ELEMS, tid);
         if (cc) ls.store(nA + A_ELEMS + B_ELEMS, nc, tid);
-        if (cr) lr.store(nA + A_ELEMS + B_ELEMS + S_ELEMS, nq, tid);
+        if (cr) lr.store(nA + A_ELEMS + B_ELEMS + r_off, nq, tid);
       }
       __syncthreads();
     }
@@ -512,7 +579,7 @@ struct Gemm {
 
     // propagated checksums for the consumers downstream
     if (PROT && cc && g.Cc != nullptr) {
-      float* Cc = g.Cc + b0 * g.sCc0 + b1 * g.sCc1 + int64_t(blockIdx.z) * g.sCck;
+      float* Cc = g.Cc + b0 * g.sCc0 + b1 * g.sCc1 + int64_t(kslice) * g.sCck;
       for (int v = tid; v < ncb * BN; v += NT) {
         const int blk = v / BN, n = v % BN;
         if (m0 + blk * g.Rm < g.M && n0 + n < g.N) {
@@ -641,19 +708,24 @@ template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int N
 hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   using G = Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
   auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
-  const size_t lds = G::LDS_BYTES;
-  if (lds > 160 * 1024) return hipErrorInvalidValue;  // this tile does not fit gfx950 LDS
+  const size_t lds = G::lds_bytes(PROT && g.Ac != nullptr, PROT && g.Br != nullptr);
+  const size_t lds_max = G::lds_bytes(PROT, PROT);
+  if (lds_max > 160 * 1024) return hipErrorInvalidValue;  // this tile does not fit gfx950 LDS
   static bool attr_set = false;  // per instantiation; harmless if repeated
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_max));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  dim3 grid(tiles, g.nb0 * g.nb1, g.splitk > 1 ? g.splitk : 1);
-  if (tiles == 0 || g.nb0 * g.nb1 == 0) return hipSuccess;
-  hipLaunchKernelGGL(kern, grid, dim3(NT), lds, s, g);
+  const int64_t ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
+  const int64_t tiles = tri_tiles(g, BM, BN) ? ntm * (ntm + 1) / 2 : ntm * ntn;
+  const int64_t nb = int64_t(g.nb0) * g.nb1, ks = g.splitk > 1 ? g.splitk : 1;
+  if (tiles == 0 || nb == 0) return hipSuccess;
+  if (nb > 1 && ks > 1) return hipErrorInvalidValue;  // split-K is for unbatched GEMMs
+  const int64_t total = tiles * nb * ks;
+  if (total > 0x7fffffff / NT) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(kern, dim3(unsigned(total)), dim3(NT), lds, s, g);
   return hipGetLastError();
 }
 

@@ -52,23 +52,71 @@ template <> struct Vec<float> {
   }
 };
 
-__device__ __forceinline__ float nanmax(float a, float b) {  // NaN-propagating max
-  return (is_nan(a) || a > b) ? a : b;
+// Cross-lane reductions on DPP moves (no LDS round trip). After the steps
+// up to W every lane of an aligned group of W lanes holds the same value
+// (each step adds a value and its partner's, so both get the same sum).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
 }
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = nanmax(x, __shfl_xor(x, o, 64));
+constexpr int DPP_XOR1 = 0xb1;         // quad_perm [1,0,3,2]
+constexpr int DPP_XOR2 = 0x4e;         // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141; // lane i <- lane 7 - i within 8
+constexpr int DPP_MIRROR = 0x140;      // lane i <- lane 15 - i within 16
+
+template <int W>
+__device__ __forceinline__ float group_sum(float x) {
+  if constexpr (W >= 2) x += dpp<DPP_XOR1>(x);
+  if constexpr (W >= 4) x += dpp<DPP_XOR2>(x);
+  if constexpr (W >= 8) x += dpp<DPP_HALF_MIRROR>(x);
+  if constexpr (W >= 16) x += dpp<DPP_MIRROR>(x);
+  if constexpr (W >= 32) x += __shfl_xor(x, 16, 64);
+  if constexpr (W >= 64) x += __shfl_xor(x, 32, 64);
   return x;
+}
+__device__ __forceinline__ float lane_of(float x, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
 }
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
-  return x;
+  x = group_sum<16>(x);
+  return (lane_of(x, 0) + lane_of(x, 16)) + (lane_of(x, 32) + lane_of(x, 48));
 }
-// sum over aligned groups of `width` lanes (width a power of two <= 64)
-__device__ __forceinline__ float group_sum(float x, int width) {
-  for (int o = 1; o < width; o <<= 1) x += __shfl_xor(x, o, 64);
-  return x;
+// Row maximum. fmaxf skips a NaN, but a NaN still reaches every output
+// through the row sum (exp2 of NaN), exactly as a NaN-propagating maximum
+// would make it.
+__device__ __forceinline__ float wave_max(float x) {
+  x = fmaxf(x, dpp<DPP_XOR1>(x));
+  x = fmaxf(x, dpp<DPP_XOR2>(x));
+  x = fmaxf(x, dpp<DPP_HALF_MIRROR>(x));
+  x = fmaxf(x, dpp<DPP_MIRROR>(x));
+  return fmaxf(fmaxf(lane_of(x, 0), lane_of(x, 16)), fmaxf(lane_of(x, 32), lane_of(x, 48)));
+}
+// row checksum pair of a key block spread over w lanes (w uniform)
+__device__ __forceinline__ void kb_sums(float& r1, float& r2, int w) {
+  switch (w) {
+    case 2: r1 = group_sum<2>(r1); r2 = group_sum<2>(r2); break;
+    case 4: r1 = group_sum<4>(r1); r2 = group_sum<4>(r2); break;
+    case 8: r1 = group_sum<8>(r1); r2 = group_sum<8>(r2); break;
+    case 16: r1 = group_sum<16>(r1); r2 = group_sum<16>(r2); break;
+    default: r1 = group_sum<32>(r1); r2 = group_sum<32>(r2); break;
+  }
+}
+
+// Round a chunk to storage in place; `bits` receives the stored image.
+__device__ __forceinline__ void round_chunk(float (&x)[8], uint4& bits) {
+  uint32_t w[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    w[q] = uint32_t(f2bf(x[2 * q])) | (uint32_t(f2bf(x[2 * q + 1])) << 16);
+    x[2 * q] = __uint_as_float(w[q] << 16);
+    x[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+  }
+  bits = make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ __forceinline__ void round_chunk(float (&x)[4], uint4& bits) {
+  bits = make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
+                    __float_as_uint(x[3]));
 }
 
 // CH: 16-byte chunks per lane per row (S <= 64 * CH * VEC); RPI rows per
@@ -80,9 +128,13 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   float* colacc = reinterpret_cast<float*>(smem);  // [S][2]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int qb = blockIdx.x, z = blockIdx.y;
+  // One-dimensional grid, (batch, head) fastest: consecutive workgroups go
+  // to different XCDs, so every XCD gets whole heads and the same mix of
+  // block costs; under a causal mask the longest query blocks come first.
   const int S = d.S, R = d.R;
-  const int nq = S / R;
+  const int nq = S / R, nbh = d.B * d.nh;
+  const int z = blockIdx.x % nbh, r = blockIdx.x / nbh;
+  const int qb = d.causal ? nq - 1 - r : r;
   const int s_valid =
       d.causal ? min(S, ((qb + 1) * R + d.kv_align - 1) / d.kv_align * d.kv_align) : S;
   const int64_t mat = int64_t(z) * S * S;
@@ -119,6 +171,10 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
       }
     }
   };
+  // live keys of the chunk starting at j0 in query row i: a prefix of it
+  auto n_live = [&](int j0, int i) {
+    return d.causal ? min(V, max(0, i - j0 + 1)) : (j0 < S ? V : 0);
+  };
   auto process_rows = [&](float (&xr)[RPI][CH][V], float (&yr)[RPI][CH][V], int it) {
 #pragma unroll
     for (int u = 0; u < RPI; ++u) {
@@ -126,80 +182,88 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
       const int i = qb * R + rl;
       float (&x)[CH][V] = xr[u];
       float (&y)[CH][V] = yr[u];
+      // chunk t holds data only if 64 t V < s_valid (a wave-uniform test)
       if (!BWD) {
-        // AP = softmax(scale * AS) over unmasked keys, in base 2
+        // AP = softmax(scale * AS) over live keys, in base 2
         const float sc = d.scale * l2e;
         float mx = -INFINITY;
 #pragma unroll
-        for (int t = 0; t < CH; ++t)
+        for (int t = 0; t < CH; ++t) {
+          if (64 * t * V >= s_valid) continue;
+          const int nl = n_live((lane + 64 * t) * V, i);
 #pragma unroll
           for (int e = 0; e < V; ++e) {
-            const int j = (lane + 64 * t) * V + e;
-            const bool live = j < s_valid && (!d.causal || j <= i);
-            x[t][e] = live ? x[t][e] * sc : -INFINITY;
-            mx = nanmax(mx, x[t][e]);
+            x[t][e] = e < nl ? x[t][e] : -INFINITY;
+            mx = fmaxf(mx, x[t][e]);
           }
+        }
         mx = wave_max(mx);
+        const float mo = -mx * sc;
         float sum = 0.f;
 #pragma unroll
-        for (int t = 0; t < CH; ++t)
+        for (int t = 0; t < CH; ++t) {
+          if (64 * t * V >= s_valid) continue;
 #pragma unroll
           for (int e = 0; e < V; ++e) {
-            const int j = (lane + 64 * t) * V + e;
-            const bool live = j < s_valid && (!d.causal || j <= i);
-            const float ev = live ? __builtin_amdgcn_exp2f(x[t][e] - mx) : 0.f;
-            x[t][e] = ev;
-            sum += ev;
+            x[t][e] = __builtin_amdgcn_exp2f(fmaf(x[t][e], sc, mo));  // masked: exp2(-inf) = 0
+            sum += x[t][e];
           }
-        sum = wave_sum(sum);
-        const float inv = 1.f / sum;
+        }
+        const float inv = 1.f / wave_sum(sum);
 #pragma unroll
         for (int t = 0; t < CH; ++t)
 #pragma unroll
-          for (int e = 0; e < V; ++e) x[t][e] = Storage<T>::round(x[t][e] * inv);
+          for (int e = 0; e < V; ++e) x[t][e] *= inv;
       } else {
-        // dAS = scale * AP * (dAP - D), D = sum_j AP_j dAP_j over unmasked keys
+        // dAS = scale * AP * (dAP - D), D = sum_j AP_j dAP_j over live keys
         float dot = 0.f;
 #pragma unroll
-        for (int t = 0; t < CH; ++t)
+        for (int t = 0; t < CH; ++t) {
+          if (64 * t * V >= s_valid) continue;
+          const int nl = n_live((lane + 64 * t) * V, i);
 #pragma unroll
           for (int e = 0; e < V; ++e) {
-            const int j = (lane + 64 * t) * V + e;
-            const bool live = j < s_valid && (!d.causal || j <= i);
-            dot += live ? x[t][e] * y[t][e] : 0.f;
+            const float p = fmaf(x[t][e], y[t][e], dot);
+            dot = e < nl ? p : dot;
           }
+        }
         dot = wave_sum(dot);
 #pragma unroll
-        for (int t = 0; t < CH; ++t)
+        for (int t = 0; t < CH; ++t) {
+          if (64 * t * V >= s_valid) continue;
+          const int nl = n_live((lane + 64 * t) * V, i);
 #pragma unroll
           for (int e = 0; e < V; ++e) {
-            const int j = (lane + 64 * t) * V + e;
-            const bool live = j < s_valid && (!d.causal || j <= i);
-            x[t][e] = live ? Storage<T>::round(d.scale * x[t][e] * (y[t][e] - dot)) : 0.f;
+            const float v = d.scale * x[t][e] * (y[t][e] - dot);
+            x[t][e] = e < nl ? v : 0.f;
           }
+        }
       }
-      // store, accumulate column checksums, emit row checksums per key block
+      // round, store, accumulate column checksums, emit row checksums per
+      // key block (weights 1..R inside the block: base + e + 1)
       const float wr = float(rl + 1);
 #pragma unroll
       for (int t = 0; t < CH; ++t) {
+        if (64 * t * V >= s_valid) continue;
         const int j0 = (lane + 64 * t) * V;
-        float r1 = 0.f, r2 = 0.f;
+        uint4 bits;
+        round_chunk(x[t], bits);
+        float r1 = 0.f, rw = 0.f;
         if (j0 < s_valid) {
-          Vec<T>::store(dst + int64_t(i) * S + j0, x[t]);
+          *reinterpret_cast<uint4*>(dst + int64_t(i) * S + j0) = bits;
 #pragma unroll
           for (int e = 0; e < V; ++e) {
             c1[t][e] += x[t][e];
-            c2[t][e] += wr * x[t][e];
+            c2[t][e] = fmaf(wr, x[t][e], c2[t][e]);
             r1 += x[t][e];
-            r2 += float(((j0 + e) & (R - 1)) + 1) * x[t][e];
+            rw = fmaf(float(e), x[t][e], rw);
           }
         }
-        if (d.row_chk != nullptr && (64 * t * V) < s_valid) {
-          r1 = group_sum(r1, lanes_per_kb);
-          r2 = group_sum(r2, lanes_per_kb);
-          const int kb = j0 / R;
+        if (d.row_chk != nullptr) {
+          float r2 = fmaf(float((j0 & (R - 1)) + 1), r1, rw);
+          kb_sums(r1, r2, lanes_per_kb);
           if ((lane % lanes_per_kb) == 0 && j0 < s_valid) {
-            float* rc = d.row_chk + ((int64_t(z) * S + i) * nq + kb) * 2;
+            float* rc = d.row_chk + ((int64_t(z) * S + i) * nq + j0 / R) * 2;
             rc[0] = r1;
             rc[1] = r2;
           }
@@ -260,7 +324,7 @@ template <bool BWD>
 hipError_t launch_sm(const SoftmaxDesc& d, int dtype, hipStream_t s) {
   const int V = dtype == ABFT_FP32 ? 4 : 8;
   const int ch = (d.S + 64 * V - 1) / (64 * V);
-  dim3 grid(d.S / d.R, d.B * d.nh);
+  dim3 grid(unsigned((d.S / d.R) * d.B * d.nh));
   const size_t lds = size_t(d.S) * 2 * sizeof(float);
 #define SM_CASE(TT, CHV)                                                                      \
   if (ch <= CHV) {                                                                            \
