@@ -68,8 +68,8 @@ struct GemmDesc {
   const abft_fault* faults = nullptr;
   int n_faults = 0;
   abft_report* report = nullptr;
-  // Split-K (dense, fp32 output only): blockIdx.z takes K slice kz and the
-  // kernel writes raw fp32 partials to C + kz*sCk and C^c to Cc + kz*sCck,
+  // Split-K (dense, unbatched, fp32 output only): the workgroup of K slice
+  // kz writes raw fp32 partials to C + kz*sCk and C^c to Cc + kz*sCck,
   // without rounding, faults or verification; launch_splitk_reduce sums the
   // slices and verifies.
   int splitk = 1;

@@ -56,7 +56,9 @@ struct Layout_ {
 int splitk_for(int64_t M, int64_t N, int64_t K) {
   const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
   int ks = 1;
-  while (tiles * ks < 512 && K / (2 * ks) >= 512 && ks < 16) ks *= 2;
+  // smallest power of two that fills every CU once (fewer slices, less
+  // partial-sum traffic), with K slices of at least 256
+  while (tiles * ks < 256 && K / (2 * ks) >= 256 && ks < 16) ks *= 2;
   return ks;
 }
 

@@ -16,6 +16,8 @@
 // corrected from the checksums when the operands are not trusted) and
 // every action is appended to the device report. The tile then leaves LDS
 // in 16-byte coalesced stores.
+#include <algorithm>
+
 #include "abft_internal.hpp"
 #include "abft_device.hpp"
 
@@ -70,7 +72,18 @@ struct TileLoader {
 
   __device__ void load(const T* base, int64_t ld, int row0, int nrows, int k0, int kend,
                        int tid) {
+    // interior tiles (the common case) skip the per-chunk bounds tests
+    const bool full = row0 + ROWS <= nrows && k0 + BK <= kend;
     if constexpr (KMAJ) {
+      if (full && CHUNKS % NT == 0) {
+#pragma unroll
+        for (int p = 0; p < PER; ++p) {
+          const int c = tid + p * NT;
+          const int r = c / (BK / VEC), kc = (c % (BK / VEC)) * VEC;
+          reg[p] = *reinterpret_cast<const uint4*>(base + op_off<true>(row0 + r, k0 + kc, ld));
+        }
+        return;
+      }
 #pragma unroll
       for (int p = 0; p < PER; ++p) {
         const int c = tid + p * NT;
@@ -152,13 +165,21 @@ struct StripLoader {
   static constexpr int PER = (16 * BK + NT - 1) / NT;
   float reg[PER];
 
+  // Element e of the strip: consecutive threads walk the contiguous
+  // direction of the source (k for a K-major strip, the checksum row for an
+  // MN-major one), so the loads coalesce.
+  __device__ static void rk(int e, int& r, int& k) {
+    if (KMAJ) { r = e / BK; k = e % BK; }
+    else { r = e % 16; k = e / 16; }
+  }
   // rows r0 + r exist only for r < nvalid (the last tile may be ragged)
   __device__ void load(const float* base, int64_t ld, int r0, int nvalid, int k0, int kend,
                        int tid) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int e = tid + p * NT;
-      const int r = e / BK, k = e % BK;
+      int r, k;
+      rk(e, r, k);
       float v = 0.f;
       if (r < nvalid && k0 + k < kend) v = base[op_off<KMAJ>(r0 + r, k0 + k, ld)];
       reg[p] = v;
@@ -168,7 +189,8 @@ struct StripLoader {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int e = tid + p * NT;
-      const int r = e / BK, k = e % BK;
+      int r, k;
+      rk(e, r, k);
       if (r < nc) {
         if constexpr (sizeof(T) == 2) {
           const bf16_t hi = f2bf(reg[p]);
@@ -464,6 +486,48 @@ struct Gemm {
     }
 
     // ---- epilogue ----
+    if (split) {
+      // fp32 partials go straight from the accumulators to this slice; the
+      // column-checksum strip is combined (hi + lo) through a small LDS
+      // image that fits inside the freed operand stages
+#pragma unroll
+      for (int i = 0; i < IM; ++i)
+#pragma unroll
+        for (int j = 0; j < JN; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + r;
+            const int n = n0 + wn * WN + j * 16 + fr;
+            if (m < g.M && n < g.N) C[int64_t(m) * g.ldc + n] = TC(acc[i][j][r]);
+          }
+      if (PROT && cc && g.Cc != nullptr) {
+        float* CsL = reinterpret_cast<float*>(smem);
+#pragma unroll
+        for (int j = 0; j < JS; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            CsL[((lane >> 4) * 4 + r) * BN + wn * WN + (wm * JS + j) * 16 + fr] = accs[j][r];
+        __syncthreads();
+        float* Cc = g.Cc + b0 * g.sCc0 + b1 * g.sCc1 + int64_t(kslice) * g.sCck;
+        const int ncb = BM / g.Rm;
+        for (int v = tid; v < ncb * BN; v += NT) {
+          const int blk = v / BN, n = v % BN;
+          float c1, c2;
+          if constexpr (sizeof(T) == 2) {
+            c1 = CsL[(2 * blk) * BN + n] + CsL[(nc + 2 * blk) * BN + n];
+            c2 = CsL[(2 * blk + 1) * BN + n] + CsL[(nc + 2 * blk + 1) * BN + n];
+          } else {
+            c1 = CsL[(2 * blk) * BN + n];
+            c2 = CsL[(2 * blk + 1) * BN + n];
+          }
+          if (m0 + blk * g.Rm < g.M && n0 + n < g.N) {
+            Cc[int64_t(rc0 + 2 * blk) * g.ldcc + n0 + n] = c1;
+            Cc[int64_t(rc0 + 2 * blk + 1) * g.ldcc + n0 + n] = c2;
+          }
+        }
+      }
+      return;
+    }
     // 1. round to storage and stage the tile (and the strip results) in LDS
     TC* tile = reinterpret_cast<TC*>(smem);
     float* CsL = reinterpret_cast<float*>(smem + TILE_BYTES);
@@ -698,8 +762,14 @@ struct Gemm {
   }
 };
 
+// Tiles up to 128 x 128 keep two waves per SIMD (at most 256 registers,
+// arch + accumulation, per lane), so two workgroups share a CU.
+template <int BM, int BN>
+constexpr int gemm_waves_per_eu() { return BM * BN <= 128 * 128 ? 2 : 1; }
+
 template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE>
-__global__ __launch_bounds__(NT) void gemm_kernel(GemmDesc g) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<BM, BN>())))
+void gemm_kernel(GemmDesc g) {
   extern __shared__ __align__(16) char smem[];
   Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>::run(g, smem);
 }
@@ -708,7 +778,11 @@ template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int N
 hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   using G = Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
   auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
-  const size_t lds = G::lds_bytes(PROT && g.Ac != nullptr, PROT && g.Br != nullptr);
+  const bool gcc = PROT && g.Ac != nullptr, gcr = PROT && g.Br != nullptr;
+  // split-K slices skip the staged epilogue: only the operand stages (and
+  // the 16 x BN checksum strip image inside them) are needed
+  const size_t lds = g.splitk > 1 ? std::max(G::main_bytes(gcc, gcr), size_t(16 * BN * 4))
+                                  : G::lds_bytes(gcc, gcr);
   const size_t lds_max = G::lds_bytes(PROT, PROT);
   if (lds_max > 160 * 1024) return hipErrorInvalidValue;  // this tile does not fit gfx950 LDS
   static bool attr_set = false;  // per instantiation; harmless if repeated
@@ -749,85 +823,176 @@ hipError_t launch_layout(const GemmDesc& g, Layout la, Layout lb, Tile tile, hip
   return hipErrorInvalidValue;  // (MN-major A, K-major B) is not used by the layer
 }
 
-// Split-K reduction: every element is the fixed-order sum of its K slices
-// (deterministic); a thread sums four consecutive columns. Injected faults
-// land on the summed (stored) value.
-__global__ __launch_bounds__(256) void splitk_sum_kernel(GemmDesc g, const float* P) {
-  const int64_t q = int64_t(blockIdx.x) * 256 + threadIdx.x;  // float4 index
+// Split-K reduction fused with the column check. One workgroup owns a
+// block of RB rows (the checksum block, Rm rows, when verifying) and 64
+// columns; thread (c, q) sums the K slices of column c for rows q, q+4, ...
+// in a fixed order (deterministic), keeps the block in LDS and accumulates
+// the column's sum and magnitude sum. The four partials of a column are
+// combined in LDS; its checksums are the fixed-order sums of the slices'
+// checksum rows. A flagged column runs EEC-ABFT (Sec. 4.2) on the LDS block
+// with recompute correction and the final check; then the block is stored.
+constexpr int RED_COLS = 64;   // columns per workgroup (16 float4 quads)
+constexpr int RED_GROUPS = 16; // row groups per workgroup
+
+// RPT rows per thread (block of RB = 16 RPT rows), KS slices; both fixed at
+// compile time so that every load of a thread is in flight at once.
+template <class T, bool AK, bool BKM, int RPT, int KS>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const float* P,
+                                                            const float* Pc, int verify) {
+  constexpr int RB = RPT * RED_GROUPS;
+  __shared__ float blk[RB * RED_COLS];              // the reduced block
+  __shared__ float p1[RED_GROUPS * RED_COLS], p2[RED_GROUPS * RED_COLS];
+  __shared__ float pc[2][4][RED_COLS];              // checksum partials per slice group
+  const int cq = threadIdx.x % 16, rg = threadIdx.x / 16;
+  const int c0 = cq * 4, n = blockIdx.x * RED_COLS + c0;
+  const int rb = blockIdx.y, m_base = rb * RB;
   const int64_t MN = int64_t(g.M) * g.N;
-  if (q * 4 >= MN) return;
-  const int m = int(q * 4 / g.N), n = int(q * 4 % g.N);
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < g.splitk; ++s) {
-    const float4 v = reinterpret_cast<const float4*>(P + s * MN)[q];
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  const bool col_ok = n < g.N;  // N % 4 == 0: a quad is all in or all out
+
+  // checksum rows of the slices: thread (c, sg) sums slices sg, sg+4, ...
+  const bool chk = verify && m_base + RB <= g.M;
+  if (chk) {
+    const int c = threadIdx.x % RED_COLS, sg = threadIdx.x / RED_COLS;
+    const int nc = blockIdx.x * RED_COLS + c;
+    const int64_t slc = int64_t(2 * (g.M / g.Rm)) * g.N;
+    float a1 = 0.f, a2 = 0.f;
+    if (nc < g.N) {
+#pragma unroll
+      for (int sl = sg; sl < KS; sl += 4) {
+        a1 += Pc[sl * slc + int64_t(2 * rb) * g.N + nc];
+        a2 += Pc[sl * slc + int64_t(2 * rb + 1) * g.N + nc];
+      }
+    }
+    pc[0][sg][c] = a1;
+    pc[1][sg][c] = a2;
   }
-  float out[4] = {acc.x, acc.y, acc.z, acc.w};
-  for (int f = 0; f < g.n_faults; ++f) {
-    int fz, fm, fn;
-    if (fault_target(g.map, g.N, g.faults[f], &fz, &fm, &fn) && fm == m && fn >= n && fn < n + 4)
-      out[fn - n] = g.faults[f].value;
+
+  float4 v[RPT];
+#pragma unroll
+  for (int u = 0; u < RPT; ++u) v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (col_ok) {
+#pragma unroll
+    for (int sl = 0; sl < KS; ++sl)
+#pragma unroll
+      for (int u = 0; u < RPT; ++u) {
+        const int m = m_base + rg + RED_GROUPS * u;
+        if (m < g.M) {
+          const float4 t = *reinterpret_cast<const float4*>(P + sl * MN + int64_t(m) * g.N + n);
+          v[u].x += t.x; v[u].y += t.y; v[u].z += t.z; v[u].w += t.w;
+        }
+      }
   }
-  float* C = static_cast<float*>(g.C) + int64_t(m) * g.ldc + n;
-  *reinterpret_cast<float4*>(C) = make_float4(out[0], out[1], out[2], out[3]);
+  float r1[4] = {0.f, 0.f, 0.f, 0.f}, sa[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < RPT; ++u) {
+    const int rr = rg + RED_GROUPS * u, m = m_base + rr;
+    float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+    for (int f = 0; f < g.n_faults; ++f) {  // injected faults (tests only)
+      int fz, fm, fn;
+      if (col_ok && fault_target(g.map, g.N, g.faults[f], &fz, &fm, &fn) && fm == m &&
+          fn >= n && fn < n + 4) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          if (fn == n + w) e[w] = g.faults[f].value;
+      }
+    }
+    *reinterpret_cast<float4*>(blk + rr * RED_COLS + c0) = make_float4(e[0], e[1], e[2], e[3]);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      r1[w] += e[w];
+      sa[w] += fabsf(e[w]);
+    }
+  }
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    p1[rg * RED_COLS + c0 + w] = r1[w];
+    p2[rg * RED_COLS + c0 + w] = sa[w];
+  }
+  __syncthreads();
+  const int c = threadIdx.x, nc = blockIdx.x * RED_COLS + c;
+  if (chk && c < RED_COLS && nc < g.N) {
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int q = 0; q < RED_GROUPS; ++q) {
+      s1 += p1[q * RED_COLS + c];
+      s2 += p2[q * RED_COLS + c];
+    }
+    const float c1 = (pc[0][0][c] + pc[0][1][c]) + (pc[0][2][c] + pc[0][3][c]);
+    const float c2 = (pc[1][0][c] + pc[1][1][c]) + (pc[1][2][c] + pc[1][3][c]);
+    if (flagged(c1 - s1, s2, g.e_rel)) {
+      float* col = blk + c;
+      const EecResult res = eec_locate<float>(col, RED_COLS, RB, c1, c2, g.e_rel, g.tn);
+      if (res.status == EEC_LOCATED) {
+        const int lr = res.index;
+        const float old = col[lr * RED_COLS];
+        int action;
+        float val;
+        if (g.recompute) {
+          val = recompute_elem<T, float, AK, BKM>(g, static_cast<const T*>(g.A),
+                                                 static_cast<const T*>(g.B), m_base + lr, nc, 0,
+                                                 g.K);
+          action = ABFT_ACT_RECOMPUTE;
+        } else {
+          val = fix_by_checksum<float>(col, RED_COLS, RB, lr, c1, res.d1, g.tc, &action);
+        }
+        col[lr * RED_COLS] = val;
+        const EvCoord ec = map_coord(g.map, 0, m_base + lr, nc);
+        record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(old, g.tn), action,
+                     old);
+      }
+      if (vec_flagged<float>(col, RED_COLS, RB, c1, g.e_rel)) {
+        const EvCoord ec = map_coord(g.map, 0, m_base, nc);
+        record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, ABFT_KIND_NONE,
+                     ABFT_ACT_UNCORRECTABLE, 0.f);
+      }
+    }
+  }
+  __syncthreads();
+  if (!col_ok) return;
+  float* C = static_cast<float*>(g.C);
+#pragma unroll
+  for (int u = 0; u < RPT; ++u) {
+    const int rr = rg + RED_GROUPS * u, m = m_base + rr;
+    if (m < g.M)
+      *reinterpret_cast<float4*>(C + int64_t(m) * g.ldc + n) =
+          *reinterpret_cast<const float4*>(blk + rr * RED_COLS + c0);
+  }
 }
 
-// Column pass on a reduced split-K output: one thread per Rm-row column
-// vector; it sums the checksum slices, checks the stored column, and on a
-// flag runs EEC-ABFT (Sec. 4.2) with recompute correction and the final
-// check. Only the owning thread reads or writes its column.
-template <class T, bool AK, bool BKM>
-__global__ __launch_bounds__(256) void splitk_check_kernel(GemmDesc g, const float* Pc) {
-  const int64_t v = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  const int nrb = g.M / g.Rm;
-  if (v >= int64_t(nrb) * g.N) return;
-  const int rb = int(v / g.N), n = int(v % g.N);
-  const int64_t slc = int64_t(2 * nrb) * g.N;
-  float c1 = 0.f, c2 = 0.f;
-  for (int s = 0; s < g.splitk; ++s) {
-    c1 += Pc[s * slc + int64_t(2 * rb) * g.N + n];
-    c2 += Pc[s * slc + int64_t(2 * rb + 1) * g.N + n];
+template <class T, int RPT, int KS>
+hipError_t reduce_launch(const GemmDesc& g, const float* P, const float* Pc, int verify,
+                         hipStream_t s) {
+  constexpr int RB = RPT * RED_GROUPS;
+  dim3 grid((g.N + RED_COLS - 1) / RED_COLS, (g.M + RB - 1) / RB);
+  hipLaunchKernelGGL((splitk_reduce_kernel<T, false, false, RPT, KS>), grid, dim3(256), 0, s, g,
+                     P, Pc, verify);
+  return hipGetLastError();
+}
+
+template <class T, int RPT>
+hipError_t reduce_ks(const GemmDesc& g, const float* P, const float* Pc, int verify,
+                     hipStream_t s) {
+  switch (g.splitk) {
+    case 2: return reduce_launch<T, RPT, 2>(g, P, Pc, verify, s);
+    case 4: return reduce_launch<T, RPT, 4>(g, P, Pc, verify, s);
+    case 8: return reduce_launch<T, RPT, 8>(g, P, Pc, verify, s);
+    case 16: return reduce_launch<T, RPT, 16>(g, P, Pc, verify, s);
   }
-  float* col = static_cast<float*>(g.C) + int64_t(rb) * g.Rm * g.ldc + n;
-  const int ld = int(g.ldc);
-  if (!vec_flagged<float>(col, ld, g.Rm, c1, g.e_rel)) return;
-  const EecResult res = eec_locate<float>(col, ld, g.Rm, c1, c2, g.e_rel, g.tn);
-  if (res.status == EEC_LOCATED) {
-    const int lr = res.index;
-    const float old = col[int64_t(lr) * ld];
-    int action;
-    float val;
-    if (g.recompute) {
-      val = recompute_elem<T, float, AK, BKM>(g, static_cast<const T*>(g.A),
-                                             static_cast<const T*>(g.B), rb * g.Rm + lr, n, 0, g.K);
-      action = ABFT_ACT_RECOMPUTE;
-    } else {
-      val = fix_by_checksum<float>(col, ld, g.Rm, lr, c1, res.d1, g.tc, &action);
-    }
-    col[int64_t(lr) * ld] = val;
-    const EvCoord ec = map_coord(g.map, 0, rb * g.Rm + lr, n);
-    record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(old, g.tn), action, old);
-  }
-  if (vec_flagged<float>(col, ld, g.Rm, c1, g.e_rel)) {
-    const EvCoord ec = map_coord(g.map, 0, rb * g.Rm, n);
-    record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, ABFT_KIND_NONE,
-                 ABFT_ACT_UNCORRECTABLE, 0.f);
-  }
+  return hipErrorInvalidValue;
 }
 
 template <class T>
 hipError_t reduce_t(const GemmDesc& g, const float* P, const float* Pc, Layout la, Layout lb,
                     hipStream_t s) {
   if (la != Layout::MNMajor || lb != Layout::MNMajor) return hipErrorInvalidValue;
-  if (g.N % 4 != 0 || g.ldc != g.N) return hipErrorInvalidValue;
-  const int64_t quads = int64_t(g.M) * g.N / 4;
-  hipLaunchKernelGGL(splitk_sum_kernel, dim3((quads + 255) / 256), dim3(256), 0, s, g, P);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || g.verify < 1 || g.Ac == nullptr) return e;
-  const int64_t nv = int64_t(g.M / g.Rm) * g.N;
-  hipLaunchKernelGGL((splitk_check_kernel<T, false, false>), dim3((nv + 255) / 256), dim3(256), 0,
-                     s, g, Pc);
-  return hipGetLastError();
+  if (g.ldc < g.N || g.N % 4 != 0 || g.ldc % 4 != 0) return hipErrorInvalidValue;
+  const int verify = (g.verify >= 1 && g.Ac != nullptr && Pc != nullptr) ? 1 : 0;
+  // the checksum block is the row block (16 or 8 rows per thread group)
+  const int RB = verify ? g.Rm : 64;
+  if (verify && g.M % RB != 0) return hipErrorInvalidValue;
+  if (RB == 64) return reduce_ks<T, 4>(g, P, Pc, verify, s);
+  if (RB == 128) return reduce_ks<T, 8>(g, P, Pc, verify, s);
+  return hipErrorInvalidValue;  // head dimensions 64 and 128 only
 }
 
 }  // namespace
