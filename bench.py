@@ -11,12 +11,23 @@ Printed (one JSON line): protected-layer TFLOP/s (useful GEMM flops only;
 checksum work is overhead), the ABFT overhead against the same kernels
 unprotected, the dominant kernel's roofline fraction measured with HIP
 events, and the CPU oracle timed on a bounded sample on the host.
+
+Profiling helpers (they run committed code only):
+  --pmc-workload        launch the dominant kernel and a plain copy of known
+                        size, for `rocprofv3 --pmc FETCH_SIZE` / `WRITE_SIZE`
+  --summarize DIR...    print a short summary of rocprofv3 result databases
+  --traffic-from F W    HBM bytes per launch of the dominant kernel from the
+                        FETCH_SIZE (F) and WRITE_SIZE (W) runs, scaled by the
+                        counters' reading for the reference copy
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -27,6 +38,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+COPY_BYTES = 256 << 20      # reference copy for the counter scale factor
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "qkv_gemm_gpt2_causal_B8_S1024_traffic.md")
 
 
 def useful_flops(B, S, H, nh, causal, backward=True):
@@ -34,6 +47,19 @@ def useful_flops(B, S, H, nh, causal, backward=True):
     P = S * (S + 1) // 2 if causal else S * S
     fwd = 8 * B * S * H * H + 4 * B * nh * d * P
     return fwd * (3 if backward else 1)
+
+
+# stages made of more than one kernel launch (checksum encodes; split-K
+# weight gradients = slice GEMM + reduce/check): not used for the roofline
+MULTI_KERNEL = {"encode", "dWo", "dWqkv"}
+
+# kernel symbol (as rocprofv3 names it) of single-kernel stages at the
+# workload shape, protected instantiation
+KERNEL_OF_STAGE = {
+    "qkv": "gemm_kernel<unsigned short, unsigned short, true, false, 256, 128, true, 2>",
+    "softmax_bwd": "softmax_kernel<unsigned short, 2, true, 1, true>",
+    "softmax": "softmax_kernel<unsigned short, 2, false, 1, true>",
+}
 
 
 def stage_table(B, S, H, nh, causal, es=2):
@@ -63,10 +89,37 @@ def stage_table(B, S, H, nh, causal, es=2):
     ]
 
 
-def cpu_baseline(shape, seed):
-    """The oracle, as it stands, on two batch elements of the workload
-    (forward + backward with one injected fault); throughput in the
-    metric's unit."""
+def kernel_source_hash():
+    """Hash of every HIP source of the library: traffic counters taken on
+    other sources are stale."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2410_11720_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel):
+    """HBM traffic per launch of `kernel` from the committed counter summary,
+    or None when absent or taken on different kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    m = re.search(r"^traffic_json: (\{.*\})$", text, re.M)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_hash") != kernel_source_hash() or rec.get("kernel") != kernel:
+        return None
+    return rec
+
+
+def cpu_baseline(shape, seed, batch=None):
+    """The oracle, as it stands, on `batch` batch elements of the workload
+    (all of them by default; forward + backward with one injected fault);
+    throughput in the metric's unit."""
     import workloads as W
     from oracle import OracleParams, forward, backward
     try:
@@ -74,7 +127,8 @@ def cpu_baseline(shape, seed):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    sample = W.make_shape(2, shape.seq, shape.hidden, shape.heads, causal=shape.causal,
+    nb = batch or shape.batch
+    sample = W.make_shape(nb, shape.seq, shape.hidden, shape.heads, causal=shape.causal,
                           dtype=shape.dtype, block_rows=shape.block_rows)
     inp = W.make_inputs(sample, seed)
     faults = W.draw_faults(sample, seed + 1, 1, W.ALL_OPS, ["inf"])
@@ -85,10 +139,140 @@ def cpu_baseline(shape, seed):
     b = backward(f, inp["dO"], p, faults)
     dt = time.perf_counter() - t0
     assert len(f["events"]) + len(b["events"]) == 1
-    fl = useful_flops(2, sample.seq, sample.hidden, sample.heads, sample.causal)
+    fl = useful_flops(nb, sample.seq, sample.hidden, sample.heads, sample.causal)
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"2 of {shape.batch} batch elements ({sample.name}), fwd+bwd with one "
+            "sample": f"{nb} of {shape.batch} batch elements ({sample.name}), fwd+bwd with one "
                       f"injected fault, float64 numpy; {dt:.2f} s"}
+
+
+class Layer:
+    """The workload's layer on the GPU: inputs, outputs and one protected
+    and one unprotected instance of the library's layer."""
+
+    def __init__(self, key):
+        import torch
+        import workloads as W
+        from paper_2410_11720_amd import abft
+        self.torch, self.W, self.abft = torch, W, abft
+        self.key = key
+        self.shape = shape = W.CONFIGS[key]
+        B, S, H, nh = shape.batch, shape.seq, shape.hidden, shape.heads
+        dev = "cuda"
+        torch.cuda.set_device(0)
+        inp = W.make_inputs(shape, W.data_seed(key))
+        self.tdt = tdt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+        self.X, self.Wqkv, self.Wo, self.dO = (
+            torch.from_numpy(inp[k]).to(dev).to(tdt) for k in ("X", "Wqkv", "Wo", "dO"))
+
+        def make(protect):
+            cfg = abft.LayerConfig(B, S, H, nh, dtype=shape.dtype, causal=shape.causal,
+                                   block_rows=shape.block_rows, protect=protect)
+            return cfg, abft.ProtectedAttention(cfg, dev)
+
+        self.cfg_p, self.lay_p = make(True)
+        self.cfg_u, self.lay_u = make(False)
+        self.O = torch.empty((B, S, H), dtype=tdt, device=dev)
+        self.dX = torch.empty_like(self.O)
+        self.dWqkv = torch.empty((H, 3 * H), dtype=torch.float32, device=dev)
+        self.dWo = torch.empty((H, H), dtype=torch.float32, device=dev)
+        self.stream = torch.cuda.current_stream()
+
+    def step(self, lay, faults):
+        lay.forward(self.X, self.Wqkv, self.Wo, faults, O=self.O)
+        lay.backward(self.dO, self.X, self.Wqkv, self.Wo, faults, dX=self.dX, dWqkv=self.dWqkv,
+                     dWo=self.dWo)
+
+    def run_stage(self, mask, is_bwd):
+        a, lay = self.abft, self.lay_p
+        if is_bwd:
+            a.attn_abft_backward_stages(self.cfg_p, self.dO, self.X, self.Wqkv, self.Wo,
+                                        lay.workspace, self.dX, self.dWqkv, self.dWo, None, 0,
+                                        lay.report_bwd, mask, self.stream, append=True)
+        else:
+            a.attn_abft_forward_stages(self.cfg_p, self.X, self.Wqkv, self.Wo, self.O,
+                                       lay.workspace, None, 0, lay.report, mask, self.stream,
+                                       append=True)
+
+
+def pmc_workload(key, reps):
+    """Launches for the traffic counters: one protected step (so that the
+    workspace is consistent), `reps` launches of the dominant stage, then
+    `reps` plain copies of COPY_BYTES (reads and writes COPY_BYTES each)."""
+    L = Layer(key)
+    torch = L.torch
+    L.step(L.lay_p, (None, 0))
+    for _ in range(reps):
+        L.run_stage(0x002, False)   # QKV projection
+    src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda").normal_()
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        torch.mul(src, 1.0, out=dst)   # one elementwise kernel: reads and writes COPY_BYTES
+    torch.cuda.synchronize()
+    print(json.dumps({"pmc_workload": key, "reps": reps, "copy_bytes": COPY_BYTES}), flush=True)
+
+
+def collect(dirs):
+    """Per kernel: launches, mean duration and mean of every counter found,
+    over the rocprofv3 databases under the given directories."""
+    import sqlite3
+    out = {}
+    for d in dirs:
+        for db in glob.glob(os.path.join(d, "**", "*.db"), recursive=True):
+            con = sqlite3.connect(db)
+            n_pmc = con.execute("select count(*) from counters_collection").fetchone()[0]
+            if n_pmc > 0:
+                q = ("select kernel_name, counter_name, avg(value), count(*), avg(end-start) "
+                     "from counters_collection group by kernel_name, counter_name")
+                for k, c, v, n, dur in con.execute(q):
+                    e = out.setdefault(k, {})
+                    e[c] = v
+                    e["launches"] = n
+                    e.setdefault("avg_us", dur / 1e3)
+            else:
+                q = "select name, count(*), avg(end-start), sum(end-start) from kernels group by name"
+                for k, n, a, t in con.execute(q):
+                    e = out.setdefault(k, {})
+                    e.update({"launches": n, "avg_us": a / 1e3, "total_us": t / 1e3})
+    return out
+
+
+def short_name(k):
+    k = re.sub(r"abft::\(anonymous namespace\)::", "", k)
+    return re.sub(r"\(.*\)$", "", k).replace("void ", "")
+
+
+def summarize(dirs):
+    out = collect(dirs)
+    for k in sorted(out, key=lambda k: -out[k].get("total_us", out[k].get("avg_us", 0))):
+        vals = " ".join(f"{c}={v:.6g}" for c, v in sorted(out[k].items()))
+        print(f"{short_name(k)} | {vals}")
+
+
+def traffic_from(fetch_dir, write_dir, kernel=KERNEL_OF_STAGE["qkv"]):
+    """HBM bytes per launch of `kernel` from a FETCH_SIZE and a WRITE_SIZE
+    run of --pmc-workload, each counter scaled by what it reads for the
+    reference copy (COPY_BYTES in, COPY_BYTES out)."""
+    f, w = collect([fetch_dir]), collect([write_dir])
+
+    def pick(d, pred):
+        ks = [k for k in d if pred(short_name(k))]
+        if len(ks) != 1:
+            raise SystemExit(f"expected one matching kernel, found {ks}")
+        return d[ks[0]]
+
+    kf, kw = pick(f, lambda n: n == kernel), pick(w, lambda n: n == kernel)
+    cf, cw = pick(f, lambda n: "MulFunctor" in n), pick(w, lambda n: "MulFunctor" in n)
+    s_fetch = COPY_BYTES / (cf["FETCH_SIZE"] * 1024.0)
+    s_write = COPY_BYTES / (cw["WRITE_SIZE"] * 1024.0)
+    fetch = kf["FETCH_SIZE"] * 1024.0 * s_fetch
+    write = kw["WRITE_SIZE"] * 1024.0 * s_write
+    rec = {"kernel": kernel, "source_hash": kernel_source_hash(),
+           "fetch_kib": round(kf["FETCH_SIZE"], 1), "write_kib": round(kw["WRITE_SIZE"], 1),
+           "copy_fetch_kib": round(cf["FETCH_SIZE"], 1), "copy_write_kib": round(cw["WRITE_SIZE"], 1),
+           "scale_fetch": round(s_fetch, 4), "scale_write": round(s_write, 4),
+           "fetch_bytes": int(fetch), "write_bytes": int(write),
+           "bytes_per_launch": int(fetch + write)}
+    print("traffic_json: " + json.dumps(rec))
 
 
 def main():
@@ -99,36 +283,29 @@ def main():
     ap.add_argument("--config", default="c3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stage-reps", type=int, default=20)
+    ap.add_argument("--pmc-workload", action="store_true")
+    ap.add_argument("--summarize", nargs="+")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     args = ap.parse_args()
+    if args.summarize:
+        summarize(args.summarize)
+        return
+    if args.traffic_from:
+        traffic_from(*args.traffic_from)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the protected layer has no multi-GPU path)", file=sys.stderr)
         sys.exit(2)
-
-    import torch
-    import workloads as W
-    from paper_2410_11720_amd import abft
+    if args.pmc_workload:
+        pmc_workload(args.config, args.stage_reps)
+        return
 
     key = args.config
-    shape = W.CONFIGS[key]
+    L = Layer(key)
+    torch, W, abft = L.torch, L.W, L.abft
+    shape = L.shape
     B, S, H, nh = shape.batch, shape.seq, shape.hidden, shape.heads
-    dev = "cuda"
-    torch.cuda.set_device(0)
-    inp = W.make_inputs(shape, W.data_seed(key))
-    tdt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
-    X, Wqkv, Wo, dO = (torch.from_numpy(inp[k]).to(dev).to(tdt) for k in ("X", "Wqkv", "Wo", "dO"))
-
-    def make(protect):
-        cfg = abft.LayerConfig(B, S, H, nh, dtype=shape.dtype, causal=shape.causal,
-                               block_rows=shape.block_rows, protect=protect)
-        return cfg, abft.ProtectedAttention(cfg, dev)
-
-    cfg_p, lay_p = make(True)
-    cfg_u, lay_u = make(False)
-    O = torch.empty((B, S, H), dtype=tdt, device=dev)
-    dX = torch.empty_like(O)
-    dWqkv = torch.empty((H, 3 * H), dtype=torch.float32, device=dev)
-    dWo = torch.empty((H, H), dtype=torch.float32, device=dev)
 
     # fault schedule: 1-4 faults in one step of every ten, prepared on device
     sched = []
@@ -138,65 +315,64 @@ def main():
             rng = np.random.default_rng(W.fault_seed(key, k))
             fl = W.draw_faults(shape, W.fault_seed(key, k), int(rng.integers(1, 5)), W.ALL_OPS,
                                ["inf", "nan", "+1e10", "-1e10"])
-            sched.append((abft.faults_to_device(fl, dev), len(fl)))
+            sched.append(abft.faults_to_device(fl, "cuda"))
             n_faulty += 1
         else:
-            sched.append(((None, 0), 0))
-
-    def step(lay, faults):
-        lay.forward(X, Wqkv, Wo, faults, O=O)
-        lay.backward(dO, X, Wqkv, Wo, faults, dX=dX, dWqkv=dWqkv, dWo=dWo)
+            sched.append((None, 0))
 
     def timed(lay, schedule):
+        """Wall time per step over the whole loop, and per-step durations
+        from HIP events on the launch stream."""
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(schedule) + 1)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for f, _ in schedule:
-            step(lay, f)
+        ev[0].record(L.stream)
+        for i, f in enumerate(schedule):
+            L.step(lay, f)
+            ev[i + 1].record(L.stream)
         torch.cuda.synchronize()
-        return (time.perf_counter() - t0) / len(schedule) * 1e3
+        wall = (time.perf_counter() - t0) / len(schedule) * 1e3
+        per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(len(schedule))])
+        return wall, per
 
     for _ in range(args.warmup):
-        step(lay_p, (None, 0))
-        step(lay_u, (None, 0))
-    clean = [((None, 0), 0)] * args.steps
-    ms = timed(lay_p, sched)                       # the workload: faults 1 step in 10
-    ms_clean = timed(lay_p, clean)
-    ms_unprot = timed(lay_u, clean)
+        L.step(L.lay_p, (None, 0))
+        L.step(L.lay_u, (None, 0))
+    clean = [(None, 0)] * args.steps
+    ms, per = timed(L.lay_p, sched)                 # the workload: faults 1 step in 10
+    ms_clean, per_clean = timed(L.lay_p, clean)
+    ms_unprot, per_unprot = timed(L.lay_u, clean)
+    # correction cost: steps with exactly one fault (an INF in AS, located
+    # and recomputed) against the fault-free protected step
+    one = [abft.faults_to_device(W.draw_faults(shape, W.fault_seed(key, 10_000 + k), 1, ["AS"],
+                                               ["inf"]), "cuda") for k in range(10)]
+    ms_one, per_one = timed(L.lay_p, one * max(1, args.steps // 10))
 
     # every fault of a faulty step is detected and corrected
-    f0, n0 = sched[0]
-    step(lay_p, f0)
+    f0 = sched[0]
+    L.step(L.lay_p, f0)
     torch.cuda.synchronize()
-    rf, rb = abft.read_report(lay_p.report), abft.read_report(lay_p.report_bwd)
+    rf, rb = abft.read_report(L.lay_p.report), abft.read_report(L.lay_p.report_bwd)
     corrected = rf["n_corrected"] + rb["n_corrected"]
     uncorrectable = rf["n_uncorrectable"] + rb["n_uncorrectable"]
 
     # per-stage kernel durations with HIP events on the launch stream
-    stream = torch.cuda.current_stream()
     stages = []
     for name, is_bwd, mask, kind, amount in stage_table(B, S, H, nh, shape.causal):
-        def run_once(mask=mask, is_bwd=is_bwd):
-            if is_bwd:
-                abft.attn_abft_backward_stages(cfg_p, dO, X, Wqkv, Wo, lay_p.workspace, dX, dWqkv,
-                                               dWo, None, 0, lay_p.report_bwd, mask, stream,
-                                               append=True)
-            else:
-                abft.attn_abft_forward_stages(cfg_p, X, Wqkv, Wo, O, lay_p.workspace, None, 0,
-                                              lay_p.report, mask, stream, append=True)
-        run_once()
+        L.run_stage(mask, is_bwd)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
+        e0.record(L.stream)
         for _ in range(args.stage_reps):
-            run_once()
-        e1.record(stream)
+            L.run_stage(mask, is_bwd)
+        e1.record(L.stream)
         e1.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / args.stage_reps
         stages.append((name, kind, amount, us))
     # restore a consistent workspace after the stage runs
-    step(lay_p, (None, 0))
+    L.step(L.lay_p, (None, 0))
     torch.cuda.synchronize()
 
-    dom = max(stages, key=lambda s: s[3])
+    dom = max((s for s in stages if s[0] not in MULTI_KERNEL), key=lambda s: s[3])
     name, kind, amount, us = dom
     if kind == "flop":
         achieved = amount / (us * 1e-6) / 1e12
@@ -206,8 +382,18 @@ def main():
         achieved = amount / (us * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof.update({"traffic": None, "kernel": name, "avg_us": round(us, 2),
-                 "algorithmic": amount, "per_launch": "one call of the stage"})
+    kern = KERNEL_OF_STAGE.get(name)
+    tr = stored_traffic(kern) if kern else None
+    roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
+                 "kernel": name, "symbol": kern, "avg_us": round(us, 2),
+                 "algorithmic": amount, "per_launch": "one call of the stage (one kernel)"})
+    if tr:
+        roof["traffic_split"] = {"fetch": tr["fetch_bytes"], "write": tr["write_bytes"]}
+
+    def pct(a):
+        return {"p10": round(float(np.percentile(a, 10)), 4),
+                "p50": round(float(np.percentile(a, 50)), 4),
+                "p90": round(float(np.percentile(a, 90)), 4)}
 
     flops = useful_flops(B, S, H, nh, shape.causal)
     value = flops / (ms * 1e-3) / 1e12
@@ -222,12 +408,19 @@ def main():
                    "causal": shape.causal, "block_rows": shape.block_rows,
                    "parallelism": "single GPU"},
         "abft_overhead_pct": round((ms_clean - ms_unprot) / ms_unprot * 100, 2),
+        "abft_overhead_pct_p50": round(float((np.median(per_clean) - np.median(per_unprot))
+                                             / np.median(per_unprot) * 100), 2),
         "ms_per_step_protected_fault_free": round(ms_clean, 4),
         "ms_per_step_unprotected": round(ms_unprot, 4),
+        "ms_per_step_one_fault": round(ms_one, 4),
+        "correction_cost_pct": round(float((np.median(per_one) - np.median(per_clean))
+                                           / np.median(per_clean) * 100), 2),
+        "step_ms_events": {"workload": pct(per), "protected_fault_free": pct(per_clean),
+                           "unprotected": pct(per_unprot), "one_fault": pct(per_one)},
         "unprotected_tflops": round(flops / (ms_unprot * 1e-3) / 1e12, 3),
         "mfma_frac_layer": round(value / PEAK_BF16_TFLOPS, 4),
         "faulty_steps": n_faulty,
-        "check": {"faults_injected": n0, "corrected": corrected, "uncorrectable": uncorrectable},
+        "check": {"faults_injected": f0[1], "corrected": corrected, "uncorrectable": uncorrectable},
         "roofline": roof,
         "stages_us": {s[0]: round(s[3], 2) for s in stages},
     }
