@@ -163,6 +163,42 @@ __device__ bool vec_flagged(const T* v, int stride, int n, float c1, float e_rel
   return flagged(c1 - r1, sa, e_rel);
 }
 
+// Cross-lane sums on DPP moves (no LDS round trip). After group_sum<W>
+// every lane of an aligned group of W lanes holds the same value: each
+// step adds a value and its partner's, so both partners get the same sum.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+constexpr int DPP_XOR1 = 0xb1;         // quad_perm [1,0,3,2]
+constexpr int DPP_XOR2 = 0x4e;         // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141; // lane i <- lane 7 - i within 8
+constexpr int DPP_MIRROR = 0x140;      // lane i <- lane 15 - i within 16
+
+template <int W>
+__device__ __forceinline__ float group_sum(float x) {
+  if constexpr (W >= 2) x += dpp_mov<DPP_XOR1>(x);
+  if constexpr (W >= 4) x += dpp_mov<DPP_XOR2>(x);
+  if constexpr (W >= 8) x += dpp_mov<DPP_HALF_MIRROR>(x);
+  if constexpr (W >= 16) x += dpp_mov<DPP_MIRROR>(x);
+  if constexpr (W >= 32) x += __shfl_xor(x, 16, 64);
+  if constexpr (W >= 64) x += __shfl_xor(x, 32, 64);
+  return x;
+}
+// group_sum for a wave-uniform runtime width (a power of two <= 64)
+__device__ __forceinline__ float group_sum_n(float x, int w) {
+  switch (w) {
+    case 1: return x;
+    case 2: return group_sum<2>(x);
+    case 4: return group_sum<4>(x);
+    case 8: return group_sum<8>(x);
+    case 16: return group_sum<16>(x);
+    case 32: return group_sum<32>(x);
+    default: return group_sum<64>(x);
+  }
+}
+
 __device__ inline void record_event(abft_report* rep, int op, int b, int h, int row, int col,
                                     int kind, int action, float observed) {
   if (rep == nullptr) return;

@@ -38,65 +38,61 @@ __device__ __forceinline__ void load_vec(const T* p, float* out) {
   }
 }
 
-__device__ __forceinline__ float group_sum(float x, int width) {
-  for (int o = 1; o < width; o <<= 1) x += __shfl_xor(x, o, 64);
-  return x;
-}
-
-// grid: (ceil(cols / (64*V)), rows/Rb, batch). A wave owns a 64*V-column
-// slab (lane = one 16-byte chunk); the ENC_WAVES waves of the workgroup
-// split the Rb rows of the block (wave w takes rows w, w+ENC_WAVES, ...)
-// and keep UN rows in flight. Column checksums are combined across waves in LDS in a
-// fixed order; row checksums of each Cb-column block are reduced across
-// the Cb/V lanes that hold it (Cb/V a power of two <= 64 dividing 64*V).
-constexpr int ENC_WAVES = 8;
-
-template <class T, int V>
-__global__ __launch_bounds__(ENC_WAVES * 64) void encode_kernel(const T* A, int64_t rows,
-                                                                int64_t cols, int64_t ld,
-                                                                int64_t bstride, int Rb, int Cb,
-                                                                float* col_chk, float* row_chk) {
-  constexpr int UN = 8;
-  __shared__ float part[ENC_WAVES][64][V][2];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t b = blockIdx.z;
-  const int64_t rb = blockIdx.y;
-  const int64_t c0 = (int64_t(blockIdx.x) * 64 + lane) * V;
+// grid: (ceil(cols / (CPS*V)), rows/Rb, batch). A workgroup owns an
+// Rb-row block and a slab of CPS 16-byte chunks per row; thread (c, g)
+// holds chunk c of rows g, g+RG, ... (RG = 256/CPS row groups), all of its
+// loads in flight together. Column checksums are combined over the row
+// groups in LDS in a fixed order; row checksums of each Cb-column block
+// are reduced across the Cb/V lanes that hold it (consecutive lanes share
+// a row), which needs Cb/V a power of two dividing CPS.
+template <class T, int V, int CPS>
+__global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, int64_t cols,
+                                                    int64_t ld, int64_t bstride, int Rb, int Cb,
+                                                    float* col_chk, float* row_chk) {
+  constexpr int RG = NT / CPS, W = CPS * V;
+  __shared__ float part[RG][W][2];
+  const int c = threadIdx.x % CPS, g = threadIdx.x / CPS;
+  const int64_t b = blockIdx.z, rb = blockIdx.y;
+  const int64_t c0 = int64_t(blockIdx.x) * W + c * V;
   const bool live = c0 < cols;
   const T* base = A + b * bstride + rb * Rb * ld;
   const int lanes = Cb / V;
+  const float wb = float((c0 % Cb) + 1);  // weight of the chunk's first column in its block
   float c1[V], c2[V];
 #pragma unroll
   for (int e = 0; e < V; ++e) c1[e] = c2[e] = 0.f;
-  for (int r0 = wave; r0 < Rb; r0 += ENC_WAVES * UN) {
-    float x[UN][V];
+  for (int r0 = g; r0 < Rb; r0 += 4 * RG) {
+    // unconditional loads from clamped addresses, zeroed afterwards (a
+    // load under a divergent branch is waited for at the join)
+    float x[4][V];
+    const int64_t cc = live ? c0 : cols - V;
 #pragma unroll
-    for (int u = 0; u < UN; ++u) {
-      const int r = r0 + ENC_WAVES * u;
-      if (live && r < Rb) load_vec<T, V>(base + r * ld + c0, x[u]);
-      else {
-#pragma unroll
-        for (int e = 0; e < V; ++e) x[u][e] = 0.f;
-      }
+    for (int u = 0; u < 4; ++u) {
+      const int r = min(r0 + RG * u, Rb - 1);
+      load_vec<T, V>(base + r * ld + cc, x[u]);
     }
 #pragma unroll
-    for (int u = 0; u < UN; ++u) {
-      const int r = r0 + ENC_WAVES * u;
+    for (int u = 0; u < 4; ++u) {
+      const bool ok = live && r0 + RG * u < Rb;
+#pragma unroll
+      for (int e = 0; e < V; ++e) x[u][e] = ok ? x[u][e] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = r0 + RG * u;
+      float s1 = 0.f, sw = 0.f;
 #pragma unroll
       for (int e = 0; e < V; ++e) {
         c1[e] += x[u][e];
-        c2[e] += float(r + 1) * x[u][e];
+        c2[e] = fmaf(float(r + 1), x[u][e], c2[e]);
+        s1 += x[u][e];
+        sw = fmaf(float(e), x[u][e], sw);
       }
-      if (row_chk != nullptr && r < Rb) {   // uniform across the wave
-        float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-          s1 += x[u][e];
-          s2 += float(((c0 + e) % Cb) + 1) * x[u][e];
-        }
-        s1 = group_sum(s1, lanes);
-        s2 = group_sum(s2, lanes);
-        if (live && (c0 % Cb) == 0) {
+      if (row_chk != nullptr && r0 + RG * u - g < Rb) {  // uniform: the wave's rows exist
+        float s2 = fmaf(wb, s1, sw);
+        s1 = group_sum_n(s1, lanes);
+        s2 = group_sum_n(s2, lanes);
+        if (live && r < Rb && (c0 % Cb) == 0) {
           float* rc = row_chk + ((b * rows + rb * Rb + r) * (cols / Cb) + c0 / Cb) * 2;
           rc[0] = s1;
           rc[1] = s2;
@@ -107,22 +103,15 @@ __global__ __launch_bounds__(ENC_WAVES * 64) void encode_kernel(const T* A, int6
   if (col_chk != nullptr) {
 #pragma unroll
     for (int e = 0; e < V; ++e) {
-      part[wave][lane][e][0] = c1[e];
-      part[wave][lane][e][1] = c2[e];
+      part[g][c * V + e][0] = c1[e];
+      part[g][c * V + e][1] = c2[e];
     }
     __syncthreads();
-    if (wave == 0 && live) {
-      float* cc = col_chk + ((b * (rows / Rb) + rb) * 2) * cols;
-#pragma unroll
-      for (int e = 0; e < V; ++e) {
-        float s1 = part[0][lane][e][0], s2 = part[0][lane][e][1];
-        for (int w = 1; w < ENC_WAVES; ++w) {
-          s1 += part[w][lane][e][0];
-          s2 += part[w][lane][e][1];
-        }
-        cc[c0 + e] = s1;
-        cc[cols + c0 + e] = s2;
-      }
+    const int col = threadIdx.x % W, which = threadIdx.x / W;  // 2W <= NT threads
+    if (threadIdx.x < 2 * W && int64_t(blockIdx.x) * W + col < cols) {
+      float acc = 0.f;
+      for (int q = 0; q < RG; ++q) acc += part[q][col][which];
+      col_chk[((b * (rows / Rb) + rb) * 2 + which) * cols + int64_t(blockIdx.x) * W + col] = acc;
     }
   }
 }
@@ -152,31 +141,42 @@ template <class T>
 hipError_t encode_t(const T* A, int64_t batch, int64_t rows, int64_t cols, int64_t ld,
                     int64_t bs, int Rb, int Cb, float* col_chk, float* row_chk, hipStream_t s) {
   constexpr int VV = 16 / sizeof(T);
-  auto lane_ok = [&](int v) {  // Cb/v lanes: a power of two dividing the 64-lane slab
-    return Cb % v == 0 && Cb / v <= 64 && ((Cb / v) & (Cb / v - 1)) == 0;
-  };
   const bool aligned = (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (ld % VV == 0) &&
                        (cols % VV == 0) && (bs % VV == 0);
-  const bool vec = aligned && (!row_chk || lane_ok(VV));
-  const bool scal_rows = row_chk && !vec && !lane_ok(1);
-  float* rc_inline = scal_rows ? nullptr : row_chk;
-  if (col_chk != nullptr || rc_inline != nullptr) {
-    if (vec) {
-      dim3 grid((cols + 64 * VV - 1) / (64 * VV), rows / Rb, batch);
-      hipLaunchKernelGGL((encode_kernel<T, VV>), grid, dim3(ENC_WAVES * 64), 0, s, A, rows, cols,
-                         ld, bs, Rb, Cb, col_chk, rc_inline);
-    } else {
-      dim3 grid((cols + 63) / 64, rows / Rb, batch);
-      hipLaunchKernelGGL((encode_kernel<T, 1>), grid, dim3(ENC_WAVES * 64), 0, s, A, rows, cols,
-                         ld, bs, Rb, Cb, col_chk, rc_inline);
+  // slab of CPS chunks: 8, or 16 when a row-checksum block needs it
+  int cps = 8;
+  bool rows_inline = row_chk == nullptr;
+  if (aligned && row_chk != nullptr && Cb % VV == 0) {
+    const int l = Cb / VV;
+    if ((l & (l - 1)) == 0 && l <= 16) {
+      rows_inline = true;
+      cps = l > 8 ? 16 : 8;
     }
+  }
+  float* rc_inline = (row_chk != nullptr && rows_inline) ? row_chk : nullptr;
+  if (aligned && (col_chk != nullptr || rc_inline != nullptr)) {
+    const int W = cps * VV;
+    dim3 grid(unsigned((cols + W - 1) / W), unsigned(rows / Rb), unsigned(batch));
+    if (cps == 8)
+      hipLaunchKernelGGL((encode_kernel<T, VV, 8>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs,
+                         Rb, Cb, col_chk, rc_inline);
+    else
+      hipLaunchKernelGGL((encode_kernel<T, VV, 16>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs,
+                         Rb, Cb, col_chk, rc_inline);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+  } else if (col_chk != nullptr) {  // unaligned operand: scalar chunks (V = 1)
+    dim3 grid(unsigned((cols + 8 * 1 - 1) / 8), unsigned(rows / Rb), unsigned(batch));
+    hipLaunchKernelGGL((encode_kernel<T, 1, 8>), grid, dim3(NT), 0, s, A, rows, cols, ld, bs, Rb,
+                       Cb, col_chk, nullptr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    rows_inline = row_chk == nullptr;
   }
-  if (scal_rows) {
+  if (row_chk != nullptr && !(aligned && rows_inline)) {
     const int64_t n = batch * rows * (cols / Cb);
-    hipLaunchKernelGGL((row_chk_kernel<T>), dim3((n + NT - 1) / NT), dim3(NT), 0, s, A, batch,
-                       rows, cols, ld, bs, Cb, row_chk);
+    hipLaunchKernelGGL((row_chk_kernel<T>), dim3(unsigned((n + NT - 1) / NT)), dim3(NT), 0, s, A,
+                       batch, rows, cols, ld, bs, Cb, row_chk);
     return hipGetLastError();
   }
   return hipSuccess;

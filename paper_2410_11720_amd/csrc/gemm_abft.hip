@@ -263,8 +263,10 @@ __device__ float recompute_elem(const GemmDesc& g, const T* A, const T* B, int m
 //  - causally trimmed K ranges run the most expensive tile rows first;
 //  - a causal score GEMM (whole tiles above the diagonal skipped)
 //    enumerates only the lower-triangle tiles;
-//  - unbatched GEMMs give each XCD one contiguous range of tiles (rows of
-//    tiles sharing their A rows; split-K slices sharing their K range).
+//  - unbatched GEMMs give each XCD one contiguous range of tiles, walked
+//    in bands of GM tile rows, column by column (GM = 1024 / BM), so that
+//    the tiles an XCD runs at once share about 1024 rows of A and 1024
+//    columns of B in its L2; split-K slices keep their K range together.
 struct TileIdx {
   int mt, nt, bh, ks;
 };
@@ -293,7 +295,13 @@ __device__ __forceinline__ TileIdx tile_of(const GemmDesc& g) {
     t.ks = 0;
     r = lin / nb;
   }
-  if (tri_tiles(g, BM, BN)) {  // r -> (mt, nt) with nt <= mt
+  if (nb == 1 && g.causal == 0) {
+    constexpr int GM = BM >= 1024 ? 1 : 1024 / BM;
+    const int band = r / (GM * ntn), idx = r % (GM * ntn);
+    const int rows_in_band = min(GM, ntm - band * GM);
+    t.mt = band * GM + idx % rows_in_band;
+    t.nt = idx / rows_in_band;
+  } else if (tri_tiles(g, BM, BN)) {  // r -> (mt, nt) with nt <= mt
     int mt = int((sqrtf(8.f * r + 1.f) - 1.f) * 0.5f);
     while ((mt + 1) * (mt + 2) / 2 <= r) ++mt;
     while (mt * (mt + 1) / 2 > r) --mt;
@@ -855,33 +863,35 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
     const int c = threadIdx.x % RED_COLS, sg = threadIdx.x / RED_COLS;
     const int nc = blockIdx.x * RED_COLS + c;
     const int64_t slc = int64_t(2 * (g.M / g.Rm)) * g.N;
+    const int ncc = min(nc, g.N - 1);  // loads stay unconditional (see below)
     float a1 = 0.f, a2 = 0.f;
-    if (nc < g.N) {
 #pragma unroll
-      for (int sl = sg; sl < KS; sl += 4) {
-        a1 += Pc[sl * slc + int64_t(2 * rb) * g.N + nc];
-        a2 += Pc[sl * slc + int64_t(2 * rb + 1) * g.N + nc];
-      }
+    for (int sl = sg; sl < KS; sl += 4) {
+      a1 += Pc[sl * slc + int64_t(2 * rb) * g.N + ncc];
+      a2 += Pc[sl * slc + int64_t(2 * rb + 1) * g.N + ncc];
     }
     pc[0][sg][c] = a1;
     pc[1][sg][c] = a2;
   }
 
+  // Every load is unconditional, from a clamped (valid) address, and out
+  // of range values are dropped afterwards: a load under a divergent branch
+  // makes the compiler wait for it at the join, one load at a time.
   float4 v[RPT];
 #pragma unroll
   for (int u = 0; u < RPT; ++u) v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (col_ok) {
+  const int nclamp = min(n, g.N - 4);
 #pragma unroll
-    for (int sl = 0; sl < KS; ++sl)
+  for (int sl = 0; sl < KS; ++sl)
 #pragma unroll
-      for (int u = 0; u < RPT; ++u) {
-        const int m = m_base + rg + RED_GROUPS * u;
-        if (m < g.M) {
-          const float4 t = *reinterpret_cast<const float4*>(P + sl * MN + int64_t(m) * g.N + n);
-          v[u].x += t.x; v[u].y += t.y; v[u].z += t.z; v[u].w += t.w;
-        }
-      }
-  }
+    for (int u = 0; u < RPT; ++u) {
+      const int m = min(m_base + rg + RED_GROUPS * u, g.M - 1);
+      const float4 t = *reinterpret_cast<const float4*>(P + sl * MN + int64_t(m) * g.N + nclamp);
+      v[u].x += t.x; v[u].y += t.y; v[u].z += t.z; v[u].w += t.w;
+    }
+#pragma unroll
+  for (int u = 0; u < RPT; ++u)
+    if (!col_ok || m_base + rg + RED_GROUPS * u >= g.M) v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
   float r1[4] = {0.f, 0.f, 0.f, 0.f}, sa[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int u = 0; u < RPT; ++u) {

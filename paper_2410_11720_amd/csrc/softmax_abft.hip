@@ -25,6 +25,14 @@ constexpr int NT = 256;
 template <class T> struct Vec;
 template <> struct Vec<bf16_t> {
   static constexpr int N = 8;
+  __device__ static void unpack(const uint4& v, float* out) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      out[2 * q] = __uint_as_float(w[q] << 16);
+      out[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+    }
+  }
   __device__ static void load(const bf16_t* p, float* out) {
     const uint4 v = *reinterpret_cast<const uint4*>(p);
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -43,6 +51,10 @@ template <> struct Vec<bf16_t> {
 };
 template <> struct Vec<float> {
   static constexpr int N = 4;
+  __device__ static void unpack(const uint4& v, float* out) {
+    out[0] = __uint_as_float(v.x); out[1] = __uint_as_float(v.y);
+    out[2] = __uint_as_float(v.z); out[3] = __uint_as_float(v.w);
+  }
   __device__ static void load(const float* p, float* out) {
     const float4 v = *reinterpret_cast<const float4*>(p);
     out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
@@ -52,29 +64,6 @@ template <> struct Vec<float> {
   }
 };
 
-// Cross-lane reductions on DPP moves (no LDS round trip). After the steps
-// up to W every lane of an aligned group of W lanes holds the same value
-// (each step adds a value and its partner's, so both get the same sum).
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x) {
-  return __builtin_bit_cast(
-      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
-}
-constexpr int DPP_XOR1 = 0xb1;         // quad_perm [1,0,3,2]
-constexpr int DPP_XOR2 = 0x4e;         // quad_perm [2,3,0,1]
-constexpr int DPP_HALF_MIRROR = 0x141; // lane i <- lane 7 - i within 8
-constexpr int DPP_MIRROR = 0x140;      // lane i <- lane 15 - i within 16
-
-template <int W>
-__device__ __forceinline__ float group_sum(float x) {
-  if constexpr (W >= 2) x += dpp<DPP_XOR1>(x);
-  if constexpr (W >= 4) x += dpp<DPP_XOR2>(x);
-  if constexpr (W >= 8) x += dpp<DPP_HALF_MIRROR>(x);
-  if constexpr (W >= 16) x += dpp<DPP_MIRROR>(x);
-  if constexpr (W >= 32) x += __shfl_xor(x, 16, 64);
-  if constexpr (W >= 64) x += __shfl_xor(x, 32, 64);
-  return x;
-}
 __device__ __forceinline__ float lane_of(float x, int l) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
 }
@@ -86,21 +75,16 @@ __device__ __forceinline__ float wave_sum(float x) {
 // through the row sum (exp2 of NaN), exactly as a NaN-propagating maximum
 // would make it.
 __device__ __forceinline__ float wave_max(float x) {
-  x = fmaxf(x, dpp<DPP_XOR1>(x));
-  x = fmaxf(x, dpp<DPP_XOR2>(x));
-  x = fmaxf(x, dpp<DPP_HALF_MIRROR>(x));
-  x = fmaxf(x, dpp<DPP_MIRROR>(x));
+  x = fmaxf(x, dpp_mov<DPP_XOR1>(x));
+  x = fmaxf(x, dpp_mov<DPP_XOR2>(x));
+  x = fmaxf(x, dpp_mov<DPP_HALF_MIRROR>(x));
+  x = fmaxf(x, dpp_mov<DPP_MIRROR>(x));
   return fmaxf(fmaxf(lane_of(x, 0), lane_of(x, 16)), fmaxf(lane_of(x, 32), lane_of(x, 48)));
 }
 // row checksum pair of a key block spread over w lanes (w uniform)
 __device__ __forceinline__ void kb_sums(float& r1, float& r2, int w) {
-  switch (w) {
-    case 2: r1 = group_sum<2>(r1); r2 = group_sum<2>(r2); break;
-    case 4: r1 = group_sum<4>(r1); r2 = group_sum<4>(r2); break;
-    case 8: r1 = group_sum<8>(r1); r2 = group_sum<8>(r2); break;
-    case 16: r1 = group_sum<16>(r1); r2 = group_sum<16>(r2); break;
-    default: r1 = group_sum<32>(r1); r2 = group_sum<32>(r2); break;
-  }
+  r1 = group_sum_n(r1, w);
+  r2 = group_sum_n(r2, w);
 }
 
 // Round a chunk to storage in place; `bits` receives the stored image.
@@ -154,20 +138,19 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   // loads of iteration it + 1 are issued before iteration it is computed
   // (two register buffers, the loop unrolled by two so that buffer indices
   // stay compile-time constants).
-  auto load_rows = [&](float (&x)[RPI][CH][V], float (&y)[RPI][CH][V], int it) {
+  // Loads are unconditional (a chunk past s_valid reads the row's last
+  // valid chunk instead and is zeroed when unpacked), so every load of an
+  // iteration is in flight at once: a load under a divergent branch would
+  // make the compiler wait for it at the branch's join.
+  auto load_rows = [&](uint4 (&x)[RPI][CH], uint4 (&y)[RPI][CH], int it) {
 #pragma unroll
     for (int u = 0; u < RPI; ++u) {
       const int i = qb * R + wave + 4 * (it * RPI + u);
 #pragma unroll
       for (int t = 0; t < CH; ++t) {
-        const int j0 = (lane + 64 * t) * V;
-        if (j0 < s_valid) {
-          Vec<T>::load(src + int64_t(i) * S + j0, x[u][t]);
-          if (BWD) Vec<T>::load(src2 + int64_t(i) * S + j0, y[u][t]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < V; ++e) x[u][t][e] = y[u][t][e] = 0.f;
-        }
+        const int jc = min((lane + 64 * t) * V, s_valid - V);
+        x[u][t] = *reinterpret_cast<const uint4*>(src + int64_t(i) * S + jc);
+        if (BWD) y[u][t] = *reinterpret_cast<const uint4*>(src2 + int64_t(i) * S + jc);
       }
     }
   };
@@ -175,13 +158,23 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   auto n_live = [&](int j0, int i) {
     return d.causal ? min(V, max(0, i - j0 + 1)) : (j0 < S ? V : 0);
   };
-  auto process_rows = [&](float (&xr)[RPI][CH][V], float (&yr)[RPI][CH][V], int it) {
+  auto process_rows = [&](uint4 (&xr)[RPI][CH], uint4 (&yr)[RPI][CH], int it) {
 #pragma unroll
     for (int u = 0; u < RPI; ++u) {
       const int rl = wave + 4 * (it * RPI + u);
       const int i = qb * R + rl;
-      float (&x)[CH][V] = xr[u];
-      float (&y)[CH][V] = yr[u];
+      float x[CH][V], y[CH][V];
+#pragma unroll
+      for (int t = 0; t < CH; ++t) {
+        const bool in = (lane + 64 * t) * V < s_valid;
+        Vec<T>::unpack(xr[u][t], x[t]);
+        if (BWD) Vec<T>::unpack(yr[u][t], y[t]);
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          x[t][e] = in ? x[t][e] : 0.f;
+          if (BWD) y[t][e] = in ? y[t][e] : 0.f;
+        }
+      }
       // chunk t holds data only if 64 t V < s_valid (a wave-uniform test)
       if (!BWD) {
         // AP = softmax(scale * AS) over live keys, in base 2
@@ -273,9 +266,9 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   };
 
   const int n_it = R / (4 * RPI);
-  float xa[RPI][CH][V], ya[RPI][CH][V];
+  uint4 xa[RPI][CH], ya[RPI][CH];
   if constexpr (PF) {
-    float xb[RPI][CH][V], yb[RPI][CH][V];
+    uint4 xb[RPI][CH], yb[RPI][CH];
     load_rows(xa, ya, 0);
     for (int it = 0; it < n_it; it += 2) {
       if (it + 1 < n_it) load_rows(xb, yb, it + 1);

@@ -254,6 +254,29 @@ def test_encode_checksums_matches_oracle(dtype):
                        rtol=1e-5, atol=1e-3)
 
 
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("ld,cb", [(264, 64), (264, 128), (257, 64)])
+def test_encode_checksums_slabs_and_unaligned(dtype, ld, cb):
+    """Wide row-checksum blocks (16-chunk slabs), and an unaligned leading
+    dimension (scalar column path plus the per-row fallback)."""
+    abft = _abft()
+    rng = np.random.default_rng(ld + cb)
+    batch, rows, cols = 2, 384, 256
+    a = W.to_storage(rng.standard_normal((batch, rows, ld)).astype(np.float32), dtype)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    A = dev(a, tdt)
+    cc = torch.empty((batch, rows // 128, 2, cols), dtype=torch.float32, device="cuda")
+    rc = torch.empty((batch, rows, cols // cb, 2), dtype=torch.float32, device="cuda")
+    print(f"[case] encode {dtype} ld={ld} cb={cb}", flush=True)
+    abft.encode_checksums(A, abft.FP32 if dtype == "f32" else abft.BF16, batch, rows, cols, ld,
+                          rows * ld, 128, cb, cc, rc)
+    torch.cuda.synchronize()
+    ref = a[..., :cols].astype(np.float64)
+    assert np.allclose(host(cc), col_checksums(ref, 128), rtol=1e-5, atol=1e-3)
+    assert np.allclose(host(rc), row_checksums(ref, cb), rtol=1e-5, atol=1e-3)
+
+
 @pytest.mark.parametrize("two_sided", [False, True])
 def test_verify_and_correct_matches_oracle(two_sided):
     abft = _abft()
