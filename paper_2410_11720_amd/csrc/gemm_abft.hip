@@ -345,7 +345,10 @@ struct Gemm {
   static constexpr int TPAD = 16 / sizeof(TC);
   static constexpr int LDT = BN + TPAD;
   static constexpr size_t TILE_BYTES = size_t(BM) * LDT * sizeof(TC);
-  static constexpr size_t CSL = 16 * BN, RSL = BM * 16;
+  // strip images; after the checksums are read from them they hold the
+  // detection's segment sums ([BM/MINB][BN][2] and [BM][BN/MINB][2])
+  static constexpr size_t CSL = 16 * BN > 2 * BN * (BM / MINB) ? 16 * BN : 2 * BN * (BM / MINB);
+  static constexpr size_t RSL = 16 * BM > 2 * BM * (BN / MINB) ? 16 * BM : 2 * BM * (BN / MINB);
   static constexpr size_t CCV = (BM / MINB) * BN * 2, RCV = BM * (BN / MINB) * 2;
   static constexpr size_t CNT = BM * (BN / MINB) + (BM / MINB) * BN;
   static constexpr size_t EPI_BYTES = TILE_BYTES + (PROT ? (CSL + RSL + CCV + RCV + CNT) * 4 : 0);
@@ -582,48 +585,121 @@ struct Gemm {
     }
     __syncthreads();
 
-    // 2. detection: recomputed against propagated checksums, one thread per
-    //    vector (Sec. 2.3 detection rule)
+    // 2. detection (Sec. 2.3 rule): recomputed against propagated checksums
     const int verify = (PROT && cc && !split) ? g.verify : 0;
     const int nrb = cr ? BN / g.Rn : 0;   // row blocks per tile row
     const int ncb = cc ? BM / g.Rm : 0;   // column blocks per tile column
     if (PROT && (cc || cr)) {
-      bool my_flag = false;
-      // column vectors then row vectors, spread over all threads
-      const int ncv = ncb * BN, nrv = BM * nrb;
-      for (int w = tid; w < ncv + nrv; w += NT) {
-        if (w >= ncv) {
-          const int u = w - ncv;
-          const int row = u / nrb, rb = u % nrb;
-          float c1, c2;
-          if constexpr (sizeof(T) == 2) {
-            c1 = RsL[row * 16 + 2 * rb] + RsL[row * 16 + nq + 2 * rb];
-            c2 = RsL[row * 16 + 2 * rb + 1] + RsL[row * 16 + nq + 2 * rb + 1];
-          } else {
-            c1 = RsL[row * 16 + 2 * rb];
-            c2 = RsL[row * 16 + 2 * rb + 1];
-          }
-          rcv[u * 2] = c1;
-          rcv[u * 2 + 1] = c2;
-          if (verify == 2 && m0 + row < g.M && n0 + rb * g.Rn < g.N)
-            my_flag |= vec_flagged<TC>(tile + row * LDT + rb * g.Rn, 1, g.Rn, c1, g.e_rel);
-          continue;
-        }
-        const int v = w;
+      // 2a. propagated checksums of every vector (strip hi + lo rows)
+      for (int v = tid; v < ncb * BN; v += NT) {
         const int blk = v / BN, n = v % BN;
-        float c1, c2;
         if constexpr (sizeof(T) == 2) {
-          c1 = CsL[(2 * blk) * BN + n] + CsL[(nc + 2 * blk) * BN + n];
-          c2 = CsL[(2 * blk + 1) * BN + n] + CsL[(nc + 2 * blk + 1) * BN + n];
+          ccv[v * 2] = CsL[(2 * blk) * BN + n] + CsL[(nc + 2 * blk) * BN + n];
+          ccv[v * 2 + 1] = CsL[(2 * blk + 1) * BN + n] + CsL[(nc + 2 * blk + 1) * BN + n];
         } else {
-          c1 = CsL[(2 * blk) * BN + n];
-          c2 = CsL[(2 * blk + 1) * BN + n];
+          ccv[v * 2] = CsL[(2 * blk) * BN + n];
+          ccv[v * 2 + 1] = CsL[(2 * blk + 1) * BN + n];
         }
-        ccv[v * 2] = c1;
-        ccv[v * 2 + 1] = c2;
-        if (verify >= 1 && m0 + blk * g.Rm < g.M && n0 + n < g.N && n0 + n >= g.verify_n_lo &&
-            n0 + n < g.verify_n_hi)
-          my_flag |= vec_flagged<TC>(tile + blk * g.Rm * LDT + n, LDT, g.Rm, c1, g.e_rel);
+      }
+      for (int u = tid; u < BM * nrb; u += NT) {
+        const int row = u / nrb, rb = u % nrb;
+        if constexpr (sizeof(T) == 2) {
+          rcv[u * 2] = RsL[row * 16 + 2 * rb] + RsL[row * 16 + nq + 2 * rb];
+          rcv[u * 2 + 1] = RsL[row * 16 + 2 * rb + 1] + RsL[row * 16 + nq + 2 * rb + 1];
+        } else {
+          rcv[u * 2] = RsL[row * 16 + 2 * rb];
+          rcv[u * 2 + 1] = RsL[row * 16 + 2 * rb + 1];
+        }
+      }
+      __syncthreads();  // the strip images are consumed; their space is reused
+      // 2b. sums and magnitude sums of the stored tile over SEG-element
+      //     segments: column pairs read 4 (or 8) bytes per row, row
+      //     segments 16 bytes at a time, so every thread has a share
+      constexpr int SEG = MINB;
+      float* colp = CsL;  // [BM / SEG][BN][2]
+      float* rowp = RsL;  // [BM][BN / SEG][2]
+      if (verify >= 1) {
+        for (int w = tid; w < (BN / 2) * (BM / SEG); w += NT) {
+          const int cp = w % (BN / 2), sg = w / (BN / 2);
+          const TC* p = tile + sg * SEG * LDT + 2 * cp;
+          float s0 = 0.f, s1 = 0.f, a0 = 0.f, a1 = 0.f;
+#pragma unroll 8
+          for (int r = 0; r < SEG; ++r) {
+            float x0, x1;
+            if constexpr (sizeof(TC) == 2) {
+              const uint32_t wd = *reinterpret_cast<const uint32_t*>(p + r * LDT);
+              x0 = __uint_as_float(wd << 16);
+              x1 = __uint_as_float(wd & 0xffff0000u);
+            } else {
+              const float2 f = *reinterpret_cast<const float2*>(p + r * LDT);
+              x0 = f.x;
+              x1 = f.y;
+            }
+            s0 += x0; s1 += x1;
+            a0 += fabsf(x0); a1 += fabsf(x1);
+          }
+          float* o = colp + (sg * BN + 2 * cp) * 2;
+          o[0] = s0; o[1] = a0; o[2] = s1; o[3] = a1;
+        }
+      }
+      if (verify == 2) {
+        constexpr int PER16 = 16 / sizeof(TC);
+        for (int w = tid; w < BM * (BN / SEG); w += NT) {
+          const int row = w % BM, sg = w / BM;
+          const TC* p = tile + row * LDT + sg * SEG;
+          float s0 = 0.f, a0 = 0.f;
+#pragma unroll
+          for (int q = 0; q < SEG / PER16; ++q) {
+            const uint4 raw = *reinterpret_cast<const uint4*>(p + q * PER16);
+            const uint32_t wd[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              if constexpr (sizeof(TC) == 2) {
+                const float x0 = __uint_as_float(wd[k] << 16);
+                const float x1 = __uint_as_float(wd[k] & 0xffff0000u);
+                s0 += x0 + x1;
+                a0 += fabsf(x0) + fabsf(x1);
+              } else {
+                const float x0 = __uint_as_float(wd[k]);
+                s0 += x0;
+                a0 += fabsf(x0);
+              }
+            }
+          }
+          rowp[(row * (BN / SEG) + sg) * 2] = s0;
+          rowp[(row * (BN / SEG) + sg) * 2 + 1] = a0;
+        }
+      }
+      __syncthreads();
+      // 2c. decisions: one per checksum vector from its segments
+      bool my_flag = false;
+      if (verify >= 1) {
+        const int spb = g.Rm / SEG;  // segments per column block
+        for (int v = tid; v < ncb * BN; v += NT) {
+          const int blk = v / BN, n = v % BN;
+          if (!(m0 + blk * g.Rm < g.M && n0 + n < g.N && n0 + n >= g.verify_n_lo &&
+                n0 + n < g.verify_n_hi))
+            continue;
+          float r1 = 0.f, sa = 0.f;
+          for (int q = 0; q < spb; ++q) {
+            r1 += colp[((blk * spb + q) * BN + n) * 2];
+            sa += colp[((blk * spb + q) * BN + n) * 2 + 1];
+          }
+          my_flag |= flagged(ccv[v * 2] - r1, sa, g.e_rel);
+        }
+      }
+      if (verify == 2) {
+        const int spb = g.Rn / SEG;  // segments per row block
+        for (int u = tid; u < BM * nrb; u += NT) {
+          const int row = u / nrb, rb = u % nrb;
+          if (!(m0 + row < g.M && n0 + rb * g.Rn < g.N)) continue;
+          float r1 = 0.f, sa = 0.f;
+          for (int q = 0; q < spb; ++q) {
+            r1 += rowp[(row * (BN / SEG) + rb * spb + q) * 2];
+            sa += rowp[(row * (BN / SEG) + rb * spb + q) * 2 + 1];
+          }
+          my_flag |= flagged(rcv[u * 2] - r1, sa, g.e_rel);
+        }
       }
       // 3. correction, only for a tile with a flagged vector
       if (__syncthreads_or(my_flag))
