@@ -234,6 +234,57 @@ int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
 /* Human-readable text of a status code (static storage). */
 const char* attn_abft_strerror(int status);
 
+/* ---------------------------------------------------------------------------
+ * Adaptive detection frequencies (paper Sec. 4.5, Algorithm 1). Host-only
+ * calls (no device memory, no stream): they choose how often each
+ * protection section is checked and produce the `sections` mask of a
+ * training step.
+ *
+ * Coverage model: errors of type e (INF, NaN, near-INF, in this order)
+ * strike an operation of n flops as a Poisson process of rate lambda[e]
+ * per flop; a section survives no error, or exactly one error that is
+ * either handled (its checks run, a fraction f of the steps) or harmless
+ * (probability 1 - p[e], p from the paper's Table 4: the chance that one
+ * error of that type in that operation leads to a non-trainable state).
+ * Two or more errors in one section count as failure. The failure
+ * probability of one execution is U = 1 - prod_S FC_S(f_S).
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  double flops;   /* n: flops of the operation per execution (>= 0)          */
+  double p[3];    /* P(non-trainable | one error of type INF, NaN, near-INF) */
+} abft_freq_op;
+
+typedef struct {
+  int32_t n_ops;     /* operations in the section                            */
+  int32_t first_op;  /* index of its first operation in the op array         */
+  double  cost;      /* T_S: check time of the section when run every step   */
+} abft_freq_section;
+
+/* Failure probability per execution for frequencies freqs[n_secs] (each in
+ * [0, 1]). ops/secs/lambda[3]/freqs (host). n_secs in [1, 16]. Returns
+ * ABFT_ERR_INVALID for null pointers or values out of range. */
+int attn_abft_unsafe_probability(const abft_freq_op* ops, const abft_freq_section* secs,
+                                 int32_t n_secs, const double* lambda, const double* freqs,
+                                 double* unsafe_out);
+
+/* Algorithm 1: frequencies f_S (freqs_out[n_secs], host) that minimise the
+ * check time sum f_S T_S subject to a failure probability of at most
+ * fail_target (= 1 - FC_target) per execution. Sections are filled in
+ * descending order of coverage gained per unit of check time, wholly while
+ * the remaining deficit allows and then by the fraction that closes it
+ * (the greedy optimum of the first-order expansion of the product). A
+ * target that even full checking misses returns all ones. */
+int attn_abft_optimize_frequencies(const abft_freq_op* ops, const abft_freq_section* secs,
+                                   int32_t n_secs, const double* lambda, double fail_target,
+                                   double* freqs_out);
+
+/* The attn_abft_config.sections mask for training step `step` (>= 0) given
+ * the frequencies of S_AS, S_CL, S_O and S_BWD (freqs[4], host): section S
+ * is on when floor((step + 1) f_S) > floor(step f_S), i.e. on a fraction
+ * f_S of the steps, evenly spread (f >= 1: every step; f <= 0: never). The
+ * same mask must be used for the forward and the backward of the step. */
+uint32_t attn_abft_sections_for_step(const double* freqs, int64_t step);
+
 #ifdef __cplusplus
 }
 #endif

@@ -55,6 +55,15 @@ class Event(ctypes.Structure):
                 ("observed", ctypes.c_float), ("reserved2", ctypes.c_float)]
 
 
+class FreqOp(ctypes.Structure):
+    _fields_ = [("flops", ctypes.c_double), ("p", ctypes.c_double * 3)]
+
+
+class FreqSection(ctypes.Structure):
+    _fields_ = [("n_ops", ctypes.c_int32), ("first_op", ctypes.c_int32),
+                ("cost", ctypes.c_double)]
+
+
 REPORT_HEADER = 32  # bytes before the event array
 assert ctypes.sizeof(Event) == 40 and ctypes.sizeof(Fault) == 24
 
@@ -79,6 +88,13 @@ _sig = {
     "attn_abft_workspace_offsets": (ctypes.c_int, [_P, ctypes.POINTER(_sz),
                                                    ctypes.POINTER(_sz), ctypes.POINTER(_sz)]),
     "attn_abft_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "attn_abft_unsafe_probability": (ctypes.c_int, [ctypes.POINTER(FreqOp),
+                                                    ctypes.POINTER(FreqSection), _i32, _vp,
+                                                    _vp, _vp]),
+    "attn_abft_optimize_frequencies": (ctypes.c_int, [ctypes.POINTER(FreqOp),
+                                                      ctypes.POINTER(FreqSection), _i32, _vp,
+                                                      ctypes.c_double, _vp]),
+    "attn_abft_sections_for_step": (_u32, [_vp, _i64]),
 }
 for _name, (_res, _args) in _sig.items():
     _f = getattr(_lib, _name)
@@ -226,6 +242,42 @@ def verify_and_correct(C, dtype, batch, rows, cols, ld, batch_stride, block_rows
 
 
 # ---- conveniences for callers holding torch tensors -----------------------
+
+def _freq_args(sections):
+    """sections: [(cost, [(flops, (p_inf, p_nan, p_ninf)), ...]), ...]"""
+    ops, secs = [], []
+    for cost, sec_ops in sections:
+        secs.append(FreqSection(len(sec_ops), len(ops), float(cost)))
+        for flops, p in sec_ops:
+            ops.append(FreqOp(float(flops), (ctypes.c_double * 3)(*[float(x) for x in p])))
+    oa = (FreqOp * max(1, len(ops)))(*ops)
+    sa = (FreqSection * len(secs))(*secs)
+    return oa, sa, len(secs)
+
+
+def _doubles(xs):
+    return (ctypes.c_double * len(xs))(*[float(x) for x in xs])
+
+
+def attn_abft_unsafe_probability(sections, lam, freqs) -> float:
+    oa, sa, n = _freq_args(sections)
+    out = ctypes.c_double()
+    _check(_lib.attn_abft_unsafe_probability(oa, sa, n, _doubles(lam), _doubles(freqs),
+                                             ctypes.byref(out)), "unsafe_probability")
+    return out.value
+
+
+def attn_abft_optimize_frequencies(sections, lam, fail_target) -> list:
+    oa, sa, n = _freq_args(sections)
+    out = (ctypes.c_double * n)()
+    _check(_lib.attn_abft_optimize_frequencies(oa, sa, n, _doubles(lam), float(fail_target),
+                                               out), "optimize_frequencies")
+    return list(out)
+
+
+def attn_abft_sections_for_step(freqs4, step: int) -> int:
+    return int(_lib.attn_abft_sections_for_step(_doubles(freqs4), int(step)))
+
 
 def faults_to_device(faults, device="cuda"):
     """Pack (op, b, h, row, col, value) tuples into a device array of

@@ -22,7 +22,9 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for want in ("attn_abft_forward", "attn_abft_backward", "encode_checksums",
                  "verify_and_correct", "attn_abft_workspace_bytes", "attn_abft_report_bytes",
-                 "attn_abft_report_init", "attn_abft_workspace_offsets", "attn_abft_strerror"):
+                 "attn_abft_report_init", "attn_abft_workspace_offsets", "attn_abft_strerror",
+                 "attn_abft_unsafe_probability", "attn_abft_optimize_frequencies",
+                 "attn_abft_sections_for_step"):
         assert want in names
 
 
@@ -38,6 +40,7 @@ def test_struct_sizes_match_header_layout():
     assert ctypes.sizeof(abft.Config) == 13 * 4
     assert ctypes.sizeof(abft.Fault) == 24
     assert ctypes.sizeof(abft.Event) == 40
+    assert ctypes.sizeof(abft.FreqOp) == 32 and ctypes.sizeof(abft.FreqSection) == 16
     assert abft.attn_abft_report_bytes(0) == abft.REPORT_HEADER
     assert abft.attn_abft_report_bytes(10) == abft.REPORT_HEADER + 400
 
