@@ -275,6 +275,116 @@ def traffic_from(fetch_dir, write_dir, kernel=KERNEL_OF_STAGE["qkv"]):
     print("traffic_json: " + json.dumps(rec))
 
 
+FAIL_TARGET = 1e-11   # one failure per 1e11 executions of the layer (Sec. 5)
+SECTION_NAMES = ("AS", "CL", "O", "BWD")
+
+
+def adaptive_frequencies(L, timed, per_unprot, steps):
+    """Adaptive detection frequencies (Sec. 4.5) at the workload: the check
+    time of each section measured alone, the library's Algorithm 1 over a
+    sweep of error rates (GPT-2 vulnerabilities of Table 4; the backward
+    counted as fatal), and one measured run of the per-step masks at the
+    sweep point with fractional frequencies."""
+    from paper_2410_11720_amd import adaptive
+    abft, torch = L.abft, L.torch
+    shape = L.shape
+    bits = (abft.SEC_AS, abft.SEC_CL, abft.SEC_O, abft.SEC_BWD)
+    base = float(np.median(per_unprot))
+    clean = [(None, 0)] * steps
+    costs = []
+    for bit in bits:
+        L.lay_p.cfg.sections = bit
+        _, per_s = timed(L.lay_p, clean)
+        costs.append(max(0.0, float(np.median(per_s)) - base) * 1e3)
+    L.lay_p.cfg.sections = abft.SEC_ALL
+    secs = adaptive.layer_sections(shape.batch, shape.seq, shape.hidden, shape.heads,
+                                   shape.causal, costs, "GPT-2", backward=True)
+    sweep = []
+    for lam in np.logspace(-24, -19, 11):
+        f = abft.attn_abft_optimize_frequencies(secs, [lam] * 3, FAIL_TARGET)
+        u = abft.attn_abft_unsafe_probability(secs, [lam] * 3, f)
+        check = sum(fi * c for fi, c in zip(f, costs))
+        sweep.append({"lambda_per_flop": float(f"{lam:.3g}"),
+                      "freqs": {n: round(fi, 4) for n, fi in zip(SECTION_NAMES, f)},
+                      "fail_prob": float(f"{u:.4g}"), "check_us": round(check, 2),
+                      "overhead_pct": round(check / (base * 1e3) * 100, 2)})
+    pick = max(sweep, key=lambda r: (sum(0 < v < 1 for v in r["freqs"].values()),
+                                    sum(r["freqs"].values()) < 4))
+    freqs = [pick["freqs"][n] for n in SECTION_NAMES]
+    n = max(steps, 40)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record(L.stream)
+    for k in range(n):
+        L.lay_p.cfg.sections = abft.attn_abft_sections_for_step(freqs, k)
+        L.step(L.lay_p, (None, 0))
+    ev[1].record(L.stream)
+    ev[1].synchronize()
+    L.lay_p.cfg.sections = abft.SEC_ALL
+    mean_ms = ev[0].elapsed_time(ev[1]) / n
+    return {"fail_target": FAIL_TARGET, "vulnerability": "GPT-2 row of Table 4",
+            "section_cost_us": {nm: round(c, 2) for nm, c in zip(SECTION_NAMES, costs)},
+            "unprotected_step_us": round(base * 1e3, 2), "sweep": sweep,
+            "measured": {"lambda_per_flop": pick["lambda_per_flop"], "freqs": pick["freqs"],
+                         "steps": n, "predicted_overhead_pct": pick["overhead_pct"],
+                         "measured_overhead_pct": round((mean_ms - base) / base * 100, 2)}}
+
+
+def recovery_costs(L, timed, per_clean, steps):
+    """Recovery overhead per step (Sec. 5, recovery): correction by the
+    protected layer for one fault of a given class against fault-free
+    protected steps, and checkpoint/restore, which copies the layer's
+    inputs and weights back from a pinned host checkpoint and re-runs the
+    step (the paper's CR baseline, checkpoint taken every step)."""
+    abft, torch, W = L.abft, L.torch, L.W
+    shape, key = L.shape, L.key
+    base = float(np.median(per_clean))
+
+    def one(op, kinds, k):
+        return abft.faults_to_device(
+            W.draw_faults(shape, W.fault_seed(key, 20_000 + 97 * k), 1, [op], kinds), "cuda")
+
+    out = {}
+    cases = [("AS_0D", "AS", L.lay_p), ("O", "O", L.lay_p), ("dX", "dX", L.lay_p),
+             ("dWQ", "dWQ", L.lay_p), ("Q_root_check", "Q", L.lay_p)]
+    # the paper's own path for a Q fault: no root check, it reaches AS as a
+    # row (1R) and is corrected there by the row pass
+    cfg_lit = L.abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads,
+                                 dtype=shape.dtype, causal=shape.causal,
+                                 block_rows=shape.block_rows, root_check=False)
+    lay_lit = abft.ProtectedAttention(cfg_lit, "cuda")
+    _, per_lit = timed(lay_lit, [(None, 0)] * steps)
+    for name, op, lay in cases:
+        sched = [one(op, ["inf"], k) for k in range(steps)]
+        _, per = timed(lay, sched)
+        out[name] = round((float(np.median(per)) - base) / base * 100, 2)
+    sched = [one("Q", ["inf"], k) for k in range(steps)]
+    _, per = timed(lay_lit, sched)
+    out["Q_1R_no_root_check"] = round((float(np.median(per)) - float(np.median(per_lit)))
+                                      / float(np.median(per_lit)) * 100, 2)
+    # checkpoint/restore: pinned host copies of everything the step reads
+    ckpt = [t.detach().to("cpu").pin_memory() for t in (L.X, L.Wqkv, L.Wo, L.dO)]
+    dsts = (L.X, L.Wqkv, L.Wo, L.dO)
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    restore, rerun = [], []
+    for _ in range(max(5, steps // 2)):
+        e0.record(L.stream)
+        for d_, c_ in zip(dsts, ckpt):
+            d_.copy_(c_, non_blocking=True)
+        e1.record(L.stream)
+        L.step(L.lay_p, (None, 0))
+        e2.record(L.stream)
+        e2.synchronize()
+        restore.append(e0.elapsed_time(e1))
+        rerun.append(e1.elapsed_time(e2))
+    cr = (float(np.median(restore)) + float(np.median(rerun))) / base * 100
+    worst = max(out.values())
+    return {"correction_overhead_pct": out, "checkpoint_restore_overhead_pct": round(cr, 2),
+            "restore_us": round(float(np.median(restore)) * 1e3, 2),
+            "restore_bytes": int(sum(t.numel() * t.element_size() for t in ckpt)),
+            "cr_over_worst_correction": round(cr / worst, 1) if worst > 0 else None}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -283,6 +393,7 @@ def main():
     ap.add_argument("--config", default="c3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stage-reps", type=int, default=20)
+    ap.add_argument("--adaptive-steps", type=int, default=30)
     ap.add_argument("--pmc-workload", action="store_true")
     ap.add_argument("--summarize", nargs="+")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
@@ -372,6 +483,9 @@ def main():
     L.step(L.lay_p, (None, 0))
     torch.cuda.synchronize()
 
+    adaptive = adaptive_frequencies(L, timed, per_unprot, args.adaptive_steps)
+    recovery = recovery_costs(L, timed, per_clean, args.adaptive_steps)
+
     dom = max((s for s in stages if s[0] not in MULTI_KERNEL), key=lambda s: s[3])
     name, kind, amount, us = dom
     if kind == "flop":
@@ -423,6 +537,8 @@ def main():
         "check": {"faults_injected": f0[1], "corrected": corrected, "uncorrectable": uncorrectable},
         "roofline": roof,
         "stages_us": {s[0]: round(s[3], 2) for s in stages},
+        "adaptive_frequencies": adaptive,
+        "recovery": recovery,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, W.data_seed(key))

@@ -351,7 +351,12 @@ struct Gemm {
   static constexpr size_t RSL = 16 * BM > 2 * BM * (BN / MINB) ? 16 * BM : 2 * BM * (BN / MINB);
   static constexpr size_t CCV = (BM / MINB) * BN * 2, RCV = BM * (BN / MINB) * 2;
   static constexpr size_t CNT = BM * (BN / MINB) + (BM / MINB) * BN;
-  static constexpr size_t EPI_BYTES = TILE_BYTES + (PROT ? (CSL + RSL + CCV + RCV + CNT) * 4 : 0);
+  // recompute queue of the correction passes: count, QMAX x (row, col,
+  // observed value), and one partial sum per wave
+  static constexpr int QMAX = 32;
+  static constexpr size_t QUE = 1 + 3 * QMAX + NT / 64;
+  static constexpr size_t EPI_BYTES =
+      TILE_BYTES + (PROT ? (CSL + RSL + CCV + RCV + CNT + QUE) * 4 : 0);
   __host__ __device__ static constexpr size_t lds_bytes(bool cc, bool cr) {
     return main_bytes(cc, cr) > EPI_BYTES ? main_bytes(cc, cr) : EPI_BYTES;
   }
@@ -756,19 +761,36 @@ struct Gemm {
       int k_hi, float* ccv, float* rcv, int* rowcnt, int* colcnt, int nrb, int ncb, int verify,
       int tid) {
     for (int e = tid; e < BM * (BN / MINB) + (BM / MINB) * BN; e += NT) rowcnt[e] = 0;
+    int* qn = rowcnt + BM * (BN / MINB) + (BM / MINB) * BN;  // queue length
+    int* qe = qn + 1;                                         // queue entries
+    float* red = reinterpret_cast<float*>(qe + 3 * QMAX);     // per-wave partials
+    if (tid == 0) *qn = 0;
     __syncthreads();
     const int Rm = g.Rm, Rn = g.Rn;
+    const int lane = tid & 63, wave = tid >> 6;
     auto in_col = [&](int blk, int n) {
       return m0 + blk * Rm < g.M && n0 + n < g.N && n0 + n >= g.verify_n_lo &&
              n0 + n < g.verify_n_hi;
     };
     auto in_row = [&](int row, int rb) { return m0 + row < g.M && n0 + rb * Rn < g.N; };
+    // A located element is recomputed from A and B by the whole workgroup
+    // (its dot product split over the threads), so a correction costs a few
+    // microseconds whatever K is: it is queued here and the queue is
+    // drained after the pass. Corrections from the checksums alone are
+    // applied at once.
     auto correct = [&](int lr, int lc, const TC* vec, int stride, int nvec, int idx, float c1,
                        float d1) {
       const float old = Storage<TC>::load(tile[lr * LDT + lc]);
       int action;
       float val;
       if (g.recompute) {
+        const int slot = atomicAdd(qn, 1);
+        if (slot < QMAX) {
+          qe[3 * slot] = lr;
+          qe[3 * slot + 1] = lc;
+          qe[3 * slot + 2] = __float_as_int(old);
+          return;
+        }
         val = recompute_elem<T, TC, AK, BKM>(g, A, B, m0 + lr, n0 + lc, k_lo, k_hi);
         action = ABFT_ACT_RECOMPUTE;
       } else {
@@ -777,6 +799,33 @@ struct Gemm {
       tile[lr * LDT + lc] = Storage<TC>::store(val);
       const EvCoord ec = map_coord(g.map, z, m0 + lr, n0 + lc);
       record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(old, g.tn), action, old);
+    };
+    auto drain = [&]() {  // every thread of the workgroup
+      __syncthreads();
+      const int nq = min(*qn, QMAX);
+      for (int q = 0; q < nq; ++q) {
+        const int lr = qe[3 * q], lc = qe[3 * q + 1];
+        const int m = m0 + lr, n = n0 + lc;
+        float part = 0.f;
+        for (int k = k_lo + tid; k < k_hi; k += NT)
+          part = fmaf(Storage<T>::load(A[op_off<AK>(m, k, g.lda)]),
+                      Storage<T>::load(B[op_off<BKM>(n, k, g.ldb)]), part);
+        part = group_sum<64>(part);
+        if (lane == 0) red[wave] = part;
+        __syncthreads();
+        if (tid == 0) {
+          float val = 0.f;
+          for (int w = 0; w < NT / 64; ++w) val += red[w];
+          const float old = __int_as_float(qe[3 * q + 2]);
+          tile[lr * LDT + lc] = Storage<TC>::store(val);
+          const EvCoord ec = map_coord(g.map, z, m, n);
+          record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(old, g.tn),
+                       ABFT_ACT_RECOMPUTE, old);
+        }
+        __syncthreads();
+      }
+      if (tid == 0) *qn = 0;
+      __syncthreads();
     };
 
     // 1. column pass
@@ -791,7 +840,7 @@ struct Gemm {
         if (verify == 2) atomicAdd(&rowcnt[lr * nrb + n / Rn], 1);
       }
     }
-    __syncthreads();
+    drain();
     if (verify == 2) {
       // 2a. refresh row checksums of row vectors with >= 2 corrections (1R)
       for (int u = tid; u < BM * nrb; u += NT) {
@@ -812,7 +861,7 @@ struct Gemm {
           atomicAdd(&colcnt[(row / Rm) * BN + lc], 1);
         }
       }
-      __syncthreads();
+      drain();
       // 2c. refresh column checksums of column vectors with >= 2 corrections (1C)
       for (int v = tid; v < ncb * BN; v += NT) {
         const int blk = v / BN, n = v % BN;
@@ -995,7 +1044,17 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
     p2[rg * RED_COLS + c0 + w] = sa[w];
   }
   __syncthreads();
+  // decisions (one thread per column); a located element is recomputed
+  // over K by the whole workgroup afterwards, then its column is checked
+  // again
+  __shared__ int flag[RED_COLS], qrow[RED_COLS];
+  __shared__ float qold[RED_COLS], wsum[4];
   const int c = threadIdx.x, nc = blockIdx.x * RED_COLS + c;
+  float c1 = 0.f;
+  if (c < RED_COLS) {
+    flag[c] = 0;
+    qrow[c] = -1;
+  }
   if (chk && c < RED_COLS && nc < g.N) {
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
@@ -1003,35 +1062,55 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
       s1 += p1[q * RED_COLS + c];
       s2 += p2[q * RED_COLS + c];
     }
-    const float c1 = (pc[0][0][c] + pc[0][1][c]) + (pc[0][2][c] + pc[0][3][c]);
+    c1 = (pc[0][0][c] + pc[0][1][c]) + (pc[0][2][c] + pc[0][3][c]);
     const float c2 = (pc[1][0][c] + pc[1][1][c]) + (pc[1][2][c] + pc[1][3][c]);
     if (flagged(c1 - s1, s2, g.e_rel)) {
+      flag[c] = 1;
       float* col = blk + c;
       const EecResult res = eec_locate<float>(col, RED_COLS, RB, c1, c2, g.e_rel, g.tn);
       if (res.status == EEC_LOCATED) {
         const int lr = res.index;
         const float old = col[lr * RED_COLS];
-        int action;
-        float val;
         if (g.recompute) {
-          val = recompute_elem<T, float, AK, BKM>(g, static_cast<const T*>(g.A),
-                                                 static_cast<const T*>(g.B), m_base + lr, nc, 0,
-                                                 g.K);
-          action = ABFT_ACT_RECOMPUTE;
+          qrow[c] = lr;
+          qold[c] = old;
         } else {
-          val = fix_by_checksum<float>(col, RED_COLS, RB, lr, c1, res.d1, g.tc, &action);
+          int action;
+          col[lr * RED_COLS] = fix_by_checksum<float>(col, RED_COLS, RB, lr, c1, res.d1, g.tc,
+                                                      &action);
+          const EvCoord ec = map_coord(g.map, 0, m_base + lr, nc);
+          record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(old, g.tn), action,
+                       old);
         }
-        col[lr * RED_COLS] = val;
-        const EvCoord ec = map_coord(g.map, 0, m_base + lr, nc);
-        record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(old, g.tn), action,
-                     old);
-      }
-      if (vec_flagged<float>(col, RED_COLS, RB, c1, g.e_rel)) {
-        const EvCoord ec = map_coord(g.map, 0, m_base, nc);
-        record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, ABFT_KIND_NONE,
-                     ABFT_ACT_UNCORRECTABLE, 0.f);
       }
     }
+  }
+  __syncthreads();
+  for (int q = 0; q < RED_COLS; ++q) {  // uniform: every thread reads the same queue
+    const int lr = qrow[q];
+    if (lr < 0) continue;
+    const int m = m_base + lr, n = blockIdx.x * RED_COLS + q;
+    const T* A = static_cast<const T*>(g.A);
+    const T* B = static_cast<const T*>(g.B);
+    float part = 0.f;
+    for (int k = threadIdx.x; k < g.K; k += 256)
+      part = fmaf(Storage<T>::load(A[op_off<AK>(m, k, g.lda)]),
+                  Storage<T>::load(B[op_off<BKM>(n, k, g.ldb)]), part);
+    part = group_sum<64>(part);
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = part;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      blk[lr * RED_COLS + q] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+      const EvCoord ec = map_coord(g.map, 0, m, n);
+      record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, classify(qold[q], g.tn),
+                   ABFT_ACT_RECOMPUTE, qold[q]);
+    }
+    __syncthreads();
+  }
+  if (c < RED_COLS && flag[c] && vec_flagged<float>(blk + c, RED_COLS, RB, c1, g.e_rel)) {
+    const EvCoord ec = map_coord(g.map, 0, m_base, nc);
+    record_event(g.report, ec.op, ec.b, ec.h, ec.row, ec.col, ABFT_KIND_NONE,
+                 ABFT_ACT_UNCORRECTABLE, 0.f);
   }
   __syncthreads();
   if (!col_ok) return;

@@ -225,6 +225,39 @@ def test_unprotected_matches_fault_free_outputs():
     assert np.array_equal(host(dWqkv), g["dWqkv"])
 
 
+@pytest.mark.gpu
+def test_scheduled_section_masks_change_no_output_bit():
+    """Steps run with the per-step masks of the adaptive frequencies
+    (attn_abft_sections_for_step) give bit-identical outputs to full
+    protection on a fault-free layer, and a masked-off section lets its
+    fault through while a checked one corrects it."""
+    abft = _abft()
+    shape = W.make_shape(2, 256, 128, 2, causal=True)
+    g, o, ob = run_pair(shape)
+    inp = W.make_inputs(shape, 1)
+    X, Wqkv, Wo, dO = (dev(inp[k], torch.bfloat16) for k in ("X", "Wqkv", "Wo", "dO"))
+    cfg = abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads, causal=True)
+    layer = abft.ProtectedAttention(cfg)
+    freqs = [0.5, 0.25, 1 / 3, 0.75]
+    for step in range(6):
+        mask = abft.attn_abft_sections_for_step(freqs, step)
+        print(f"[case] step {step} sections {mask}", flush=True)
+        layer.cfg.sections = mask
+        O = layer.forward(X, Wqkv, Wo)
+        dX, dWqkv, dWo = layer.backward(dO, X, Wqkv, Wo)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(O), g["O"]) and np.array_equal(host(dX), g["dX"])
+        assert np.array_equal(host(dWqkv), g["dWqkv"]) and np.array_equal(host(dWo), g["dWo"])
+    fault = abft.faults_to_device([W.Fault("AS", 1, 0, 40, 7, np.inf)])
+    for mask, caught in ((abft.SEC_CL | abft.SEC_O | abft.SEC_BWD, False), (abft.SEC_ALL, True)):
+        layer.cfg.sections = mask
+        O = layer.forward(X, Wqkv, Wo, fault)
+        torch.cuda.synchronize()
+        rep = abft.read_report(layer.report)
+        assert (rep["n_corrected"] == 1) == caught
+        assert np.array_equal(host(O), g["O"]) == caught
+
+
 # ---- standalone entry points ----
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
