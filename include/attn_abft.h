@@ -105,10 +105,17 @@ typedef struct {
   uint32_t flags;                    /* ABFT_FLAG_*                             */
 } attn_abft_config;
 
-/* One injected extreme value (test-only fault injector, Sec. 5.1): element
- * (b, h, row, col) of op's output is overwritten with `value` rounded to
- * storage, after the output is rounded and before it is verified. */
-typedef struct { int32_t op, b, h, row, col; float value; } abft_fault;
+/* One injected fault (test-only injector, Sec. 5.1), applied to element
+ * (b, h, row, col) of op's output after the output is rounded to storage
+ * and before it is verified:
+ *   mode ABFT_FAULT_SET:  overwritten with `value` rounded to storage;
+ *   mode ABFT_FAULT_FLIP: the most significant exponent bit of the stored
+ *                         value is flipped (bit 14 of bf16, bit 30 of fp32;
+ *                         `value` is ignored) - the paper's way of making a
+ *                         near-INF value from a computed one. */
+#define ABFT_FAULT_SET  0
+#define ABFT_FAULT_FLIP 1
+typedef struct { int32_t op, b, h, row, col; float value; int32_t mode; } abft_fault;
 
 typedef struct {
   int32_t op, b, h, row, col, kind, action, reserved;
@@ -233,6 +240,14 @@ int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
 
 /* Human-readable text of a status code (static storage). */
 const char* attn_abft_strerror(int status);
+
+/* Byte offset inside the workspace of a saved tensor of the forward:
+ * which = 0: QKV [B, S, 3H]; 1: AS [B, nh, S, S] (valid from the forward
+ * until the next backward, which reuses its space); 2: AP [B, nh, S, S];
+ * 3: CL [B, S, H]; storage dtype, row-major. Under a causal mask only the
+ * key tiles up to the diagonal tile of each query block are written.
+ * Returns ABFT_ERR_INVALID for an invalid config or `which`. */
+int attn_abft_workspace_tensor(const attn_abft_config* cfg, int32_t which, size_t* offset);
 
 /* ---------------------------------------------------------------------------
  * Adaptive detection frequencies (paper Sec. 4.5, Algorithm 1). Host-only

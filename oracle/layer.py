@@ -46,7 +46,7 @@ from collections import defaultdict
 
 import numpy as np
 
-from .numerics import round_to, stored_threshold
+from .numerics import flip_exponent_msb, round_to, stored_threshold
 from .eec import col_checksums, row_checksums, Verifier
 
 SECTIONS = ("AS", "CL", "O", "BWD")
@@ -194,11 +194,19 @@ class _Run:
                               p.t_correct)
 
     def inject(self, op, M, place, wdtype=False):
-        """Overwrite M at the positions of op's faults with the fault value
-        rounded to storage. place(b, h, r, c) -> index tuple into M."""
+        """Apply op's faults to M (already rounded to storage): mode "set"
+        writes the fault value rounded to storage, mode "flip" flips the
+        exponent MSB of the stored value. place(b, h, r, c) -> index tuple
+        into M."""
         rnd = self.rndw if wdtype else self.rnd
-        for (b, h, r, c, val) in self.faults.get(op, ()):
-            M[place(b, h, r, c)] = rnd(np.array([val]))[0]
+        dt = _w_dtype(self.p.dtype) if wdtype else self.p.dtype
+        for t in self.faults.get(op, ()):
+            b, h, r, c, val = t[:5]
+            idx = place(b, h, r, c)
+            if len(t) > 5 and t[5] == "flip":
+                M[idx] = flip_exponent_msb(float(M[idx]), dt)
+            else:
+                M[idx] = rnd(np.array([val]))[0]
 
     def on(self, section):
         return self.p.protect and section in self.p.sections

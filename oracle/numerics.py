@@ -46,6 +46,19 @@ def round_to(x, dtype: str) -> np.ndarray:
     raise ValueError(f"unknown storage dtype {dtype!r}")
 
 
+def flip_exponent_msb(x: float, dtype: str) -> float:
+    """The fault injector's bit flip (Sec. 5.1): the most significant bit of
+    the exponent field of the value as stored in dtype (bf16: bit 14 of
+    the 16-bit word, f32: bit 30, f64: bit 62). x must already be rounded
+    to dtype."""
+    if dtype == "f64":
+        u = np.array([x], dtype=np.float64).view(np.uint64)
+        return float((u ^ np.uint64(1 << 62)).view(np.float64)[0])
+    u = np.array([x], dtype=np.float32).view(np.uint32)
+    bit = np.uint32(1 << 30)  # bf16 keeps the upper half of the f32 word: its bit 14
+    return float((u ^ bit).view(np.float32)[0])
+
+
 def stored_threshold(t: float, dtype: str) -> float:
     """A threshold as the storage dtype represents it (Sec. 4.2 constants
     compare against stored values)."""

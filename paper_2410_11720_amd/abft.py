@@ -43,9 +43,13 @@ class Config(ctypes.Structure):
                 ("flags", ctypes.c_uint32)]
 
 
+FAULT_SET, FAULT_FLIP = 0, 1
+
+
 class Fault(ctypes.Structure):
     _fields_ = [("op", ctypes.c_int32), ("b", ctypes.c_int32), ("h", ctypes.c_int32),
-                ("row", ctypes.c_int32), ("col", ctypes.c_int32), ("value", ctypes.c_float)]
+                ("row", ctypes.c_int32), ("col", ctypes.c_int32), ("value", ctypes.c_float),
+                ("mode", ctypes.c_int32)]
 
 
 class Event(ctypes.Structure):
@@ -65,7 +69,7 @@ class FreqSection(ctypes.Structure):
 
 
 REPORT_HEADER = 32  # bytes before the event array
-assert ctypes.sizeof(Event) == 40 and ctypes.sizeof(Fault) == 24
+assert ctypes.sizeof(Event) == 40 and ctypes.sizeof(Fault) == 28
 
 _vp, _sz, _i32, _i64, _f32, _u32 = (ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32,
                                    ctypes.c_int64, ctypes.c_float, ctypes.c_uint32)
@@ -88,6 +92,7 @@ _sig = {
     "attn_abft_workspace_offsets": (ctypes.c_int, [_P, ctypes.POINTER(_sz),
                                                    ctypes.POINTER(_sz), ctypes.POINTER(_sz)]),
     "attn_abft_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "attn_abft_workspace_tensor": (ctypes.c_int, [_P, _i32, ctypes.POINTER(_sz)]),
     "attn_abft_unsafe_probability": (ctypes.c_int, [ctypes.POINTER(FreqOp),
                                                     ctypes.POINTER(FreqSection), _i32, _vp,
                                                     _vp, _vp]),
@@ -280,13 +285,18 @@ def attn_abft_sections_for_step(freqs4, step: int) -> int:
 
 
 def faults_to_device(faults, device="cuda"):
-    """Pack (op, b, h, row, col, value) tuples into a device array of
-    abft_fault records. Returns (tensor or None, count)."""
+    """Pack (op, b, h, row, col, value[, mode]) tuples into a device array
+    of abft_fault records; mode "set" (default) or "flip". Returns (tensor
+    or None, count)."""
     faults = [f.as_tuple() if hasattr(f, "as_tuple") else tuple(f) for f in faults]
     if not faults:
         return None, 0
-    arr = (Fault * len(faults))(*[Fault(OP_ID[o] if isinstance(o, str) else int(o), b, h, r, c,
-                                        float(v)) for (o, b, h, r, c, v) in faults])
+
+    def rec(t):
+        o, b, h, r, c, v = t[:6]
+        mode = FAULT_FLIP if len(t) > 6 and t[6] == "flip" else FAULT_SET
+        return Fault(OP_ID[o] if isinstance(o, str) else int(o), b, h, r, c, float(v), mode)
+    arr = (Fault * len(faults))(*[rec(t) for t in faults])
     host = torch.frombuffer(bytearray(bytes(arr)), dtype=torch.uint8)
     return host.to(device), len(faults)
 
@@ -343,6 +353,24 @@ class ProtectedAttention:
         attn_abft_backward(c, dO, X, Wqkv, Wo, self.workspace, dX, dWqkv, dWo, f, n,
                            self.report_bwd)
         return dX, dWqkv, dWo
+
+    def tensor(self, which):
+        """View of a saved forward tensor in the workspace: "QKV", "AS",
+        "AP" or "CL" (AS until the next backward)."""
+        c = self.cfg
+        k = ("QKV", "AS", "AP", "CL").index(which)
+        off = ctypes.c_size_t()
+        _check(_lib.attn_abft_workspace_tensor(ctypes.byref(c.to_c()), k, ctypes.byref(off)),
+               "workspace_tensor")
+        es = 4 if c.dtype == "f32" else 2
+        B, S, H, nh = c.batch, c.seq, c.hidden, c.heads
+        shape = {"QKV": (B, S, 3 * H), "AS": (B, nh, S, S), "AP": (B, nh, S, S),
+                 "CL": (B, S, H)}[which]
+        n = 1
+        for x in shape:
+            n *= x
+        o = off.value
+        return self.workspace[o:o + n * es].view(c.torch_dtype).view(*shape)
 
     def saved(self):
         """Views of the saved QKV, AP and CL inside the workspace."""

@@ -21,6 +21,13 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
   return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f));
 }
 
+// The fault injector's bit flip: the most significant exponent bit of a
+// stored value (bit 14 of bf16, bit 30 of fp32).
+__device__ __forceinline__ bf16_t flip_exponent_msb(bf16_t v) { return bf16_t(v ^ 0x4000u); }
+__device__ __forceinline__ float flip_exponent_msb(float v) {
+  return __uint_as_float(__float_as_uint(v) ^ 0x40000000u);
+}
+
 template <class T> struct Storage;
 template <> struct Storage<bf16_t> {
   __device__ static float load(bf16_t v) { return bf2f(v); }

@@ -270,6 +270,19 @@ int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
   return ABFT_OK;
 }
 
+int attn_abft_workspace_tensor(const attn_abft_config* cfg, int32_t which, size_t* offset) {
+  Dims d;
+  if (validate(cfg, &d) != ABFT_OK || !offset) return ABFT_ERR_INVALID;
+  const Layout_ L = make_layout(d);
+  switch (which) {
+    case 0: *offset = L.qkv; return ABFT_OK;
+    case 1: *offset = L.as; return ABFT_OK;
+    case 2: *offset = L.ap; return ABFT_OK;
+    case 3: *offset = L.cl; return ABFT_OK;
+  }
+  return ABFT_ERR_INVALID;
+}
+
 int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const void* Wqkv,
                              const void* Wo, void* O, void* workspace, size_t workspace_bytes,
                              const abft_fault* faults, int32_t n_faults, abft_report* report,

@@ -584,7 +584,10 @@ struct Gemm {
           int fz, fm, fn;
           if (fault_target(g.map, g.N, ft, &fz, &fm, &fn) && fz == z && fm >= m0 &&
               fm < m0 + BM && fn >= n0 && fn < n0 + BN)
-            tile[(fm - m0) * LDT + fn - n0] = Storage<TC>::store(Storage<TC>::round(ft.value));
+            tile[(fm - m0) * LDT + fn - n0] =
+                ft.mode == ABFT_FAULT_FLIP
+                    ? flip_exponent_msb(tile[(fm - m0) * LDT + fn - n0])
+                    : Storage<TC>::store(Storage<TC>::round(ft.value));
         }
       }
     }
@@ -1028,7 +1031,9 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
           fn >= n && fn < n + 4) {
 #pragma unroll
         for (int w = 0; w < 4; ++w)
-          if (fn == n + w) e[w] = g.faults[f].value;
+          if (fn == n + w)
+            e[w] = g.faults[f].mode == ABFT_FAULT_FLIP ? flip_exponent_msb(e[w])
+                                                       : g.faults[f].value;
       }
     }
     *reinterpret_cast<float4*>(blk + rr * RED_COLS + c0) = make_float4(e[0], e[1], e[2], e[3]);

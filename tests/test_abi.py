@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 def test_struct_sizes_match_header_layout():
     from paper_2410_11720_amd import abft
     assert ctypes.sizeof(abft.Config) == 13 * 4
-    assert ctypes.sizeof(abft.Fault) == 24
+    assert ctypes.sizeof(abft.Fault) == 28
     assert ctypes.sizeof(abft.Event) == 40
     assert ctypes.sizeof(abft.FreqOp) == 32 and ctypes.sizeof(abft.FreqSection) == 16
     assert abft.attn_abft_report_bytes(0) == abft.REPORT_HEADER

@@ -288,6 +288,24 @@ def test_table2_propagation_patterns_unprotected():
     assert checked == 42
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_flip_fault_equals_writing_the_flipped_stored_value(dtype):
+    """Mode "flip" writes the stored value with its exponent MSB flipped:
+    the same run as mode "set" with that value computed by hand from the
+    IEEE bit layout (bit 30 of the f32 word; bf16 is its upper half)."""
+    sh = W.make_shape(1, 64, 64, 2, dtype=dtype, block_rows=64)
+    inp = W.make_inputs(sh, 4)
+    p = OracleParams(heads=2, dtype=dtype, block_rows=64, protect=False)
+    base = forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    stored = base["CL"][0, 9, 32 + 3]
+    word = np.array([stored], dtype=np.float32).view(np.uint32)[0]
+    flipped = float(np.array([word ^ 0x40000000], dtype=np.uint32).view(np.float32)[0])
+    a = forward(inp["X"], inp["Wqkv"], inp["Wo"], p, [W.Fault("CL", 0, 1, 9, 3, 0.0, mode="flip")])
+    b = forward(inp["X"], inp["Wqkv"], inp["Wo"], p, [W.Fault("CL", 0, 1, 9, 3, flipped)])
+    assert a["CL"][0, 9, 35] == flipped
+    assert np.array_equal(a["O"], b["O"], equal_nan=True)
+
+
 def test_paper_literal_mode_corrects_1d_patterns_in_as_and_cl():
     """Root check off: Q/K/V errors reach AS and CL as 1-D patterns and are
     corrected there from checksums (Sec. 4.3, Sec. 4.4)."""

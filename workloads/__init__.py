@@ -105,17 +105,21 @@ def make_inputs(shape: LayerShape, seed: int) -> dict:
 
 @dataclasses.dataclass(frozen=True)
 class Fault:
-    """One injected extreme value: overwrite element (row, col) of op's output
-    for batch b and head h (after the output is rounded to storage)."""
+    """One injected fault in element (row, col) of op's output for batch b
+    and head h, after the output is rounded to storage: mode "set"
+    overwrites it with value (rounded to storage), mode "flip" flips the
+    most significant exponent bit of the stored value (value unused)."""
     op: str
     b: int
     h: int
     row: int
     col: int
     value: float
+    mode: str = "set"
 
     def as_tuple(self):
-        return (self.op, self.b, self.h, self.row, self.col, self.value)
+        t = (self.op, self.b, self.h, self.row, self.col, self.value)
+        return t if self.mode == "set" else t + (self.mode,)
 
 
 def op_extent(shape: LayerShape, op: str):
