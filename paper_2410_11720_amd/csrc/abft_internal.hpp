@@ -74,6 +74,10 @@ struct GemmDesc {
   // slices and verifies.
   int splitk = 1;
   int64_t sCk = 0, sCck = 0;
+  // Operands go straight from global memory to LDS (bf16 only; set at
+  // launch when K ranges are whole 64-wide stages and every operand row is
+  // 16-byte aligned); otherwise through registers.
+  int direct = 0;
 };
 
 // Tile shapes the GEMM is instantiated for (S1: one LDS stage, for short K

@@ -317,6 +317,85 @@ __device__ __forceinline__ TileIdx tile_of(const GemmDesc& g) {
   return t;
 }
 
+// ---- direct-to-LDS operand path (bf16) ------------------------------------
+// A stage's operand tile goes from global memory straight into LDS
+// (global_load_lds_dwordx4: lane p of a wave instruction writes bytes
+// [16p, 16p + 16) of a 1-KB LDS run, from any 16-byte global address), so
+// no registers hold it and several stages can be in flight. The LDS images
+// are unpadded and XOR-swizzled at 16-byte granularity so that the MFMA
+// fragment reads do not conflict on banks:
+//  - K-major tile [ROWS][64]: chunk c of row r lives at chunk c ^ (r & 7)
+//    (the 8 rows a b128 read serves together hit 8 different chunks);
+//  - MN-major tile [64][ROWS] (one row per k): chunk c of k-row k lives at
+//    chunk c ^ 2 (k & 3) (the 4 k-rows a transposing read serves together
+//    hit 4 different chunk pairs).
+// MN-major fragments are read with ds_read_b64_tr_b16: in each group of 16
+// lanes, lane s supplies the 4 elements at (k0 + s/4, m0 + 4 (s%4)), and
+// lane i receives element i%4 of lanes i/4, i/4 + 4, i/4 + 8, i/4 + 12,
+// i.e. (k0 + v, m0 + i) for v = 0..3: the k-contiguous MFMA operand.
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) short4_t lds_short4;
+
+template <bool KMAJ, int ROWS>
+struct Direct {
+  static constexpr int BK = 64;
+  static constexpr int BYTES = ROWS * BK * 2;
+  static constexpr int PER_WAVE = BYTES / 1024 / (NT / 64);  // 1-KB instructions per wave
+  static_assert(BYTES % (1024 * (NT / 64)) == 0, "tile must split into whole wave runs");
+
+  // rows past nrows read a clamped (valid) row: their results are never stored
+  __device__ static __forceinline__ void issue(const bf16_t* base, int64_t ld, int row0, int nrows,
+                                               int k0, char* st, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < PER_WAVE; ++j) {
+      const int i = wave * PER_WAVE + j;
+      const bf16_t* src;
+      if constexpr (KMAJ) {
+        const int row = i * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ (row & 7);
+        src = base + int64_t(min(row0 + row, nrows - 1)) * ld + k0 + c * 8;
+      } else {
+        constexpr int CPR = ROWS / 8;       // 16-byte chunks per k-row
+        constexpr int KR = 64 / CPR;        // k-rows per 1-KB run
+        const int kr = i * KR + lane / CPR;
+        const int c = (lane % CPR) ^ (2 * (kr & 3));
+        src = base + int64_t(k0 + kr) * ld + min(row0 + c * 8, nrows - 8);
+      }
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(st + i * 1024), 16, 0, 0);
+    }
+  }
+
+  // MFMA 16x16x32 operand fragment: rows rb + (lane & 15), k = kk + 8 (lane >> 4) + 0..7
+  __device__ static __forceinline__ bf16x8 frag(const char* st, int rb, int kk, int lane) {
+    if constexpr (KMAJ) {
+      const int row = rb + (lane & 15);
+      const int c = (kk >> 3) + (lane >> 4);
+      return *reinterpret_cast<const bf16x8*>(st + row * 128 + ((c ^ (row & 7)) << 4));
+    } else {
+      const int s = lane & 15;
+      const int k = kk + 8 * (lane >> 4) + (s >> 2);
+      const int m = rb + 4 * (s & 3);
+      const int c = m >> 3, off = (m & 7) * 2;
+      const char* p0 = st + k * (ROWS * 2) + ((c ^ (2 * (k & 3))) << 4) + off;
+      const char* p1 = st + (k + 4) * (ROWS * 2) + ((c ^ (2 * ((k + 4) & 3))) << 4) + off;
+      const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p0);
+      const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p1);
+      typedef short short8_t __attribute__((ext_vector_type(8)));
+      const short8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      return __builtin_bit_cast(bf16x8, v);
+    }
+  }
+};
+
+// s_waitcnt that waits for the vector-memory counter only (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE>
 struct Gemm {
   static constexpr int BK = Mfma<T>::BK;
@@ -337,6 +416,15 @@ struct Gemm {
   }
   __host__ __device__ static constexpr size_t main_bytes(bool cc, bool cr) {
     return size_t(NSTAGE) * stage_elems(cc, cr) * sizeof(T);
+  }
+  // direct path: unpadded swizzled operand images, the strips as above
+  static constexpr int DA_BYTES = BM * 64 * 2, DB_BYTES = BN * 64 * 2;
+  __host__ __device__ static constexpr int d_stage_bytes(bool cc, bool cr) {
+    return DA_BYTES + DB_BYTES +
+           (PROT ? ((cc ? S_ELEMS : 0) + (cr ? S_ELEMS : 0)) * int(sizeof(T)) : 0);
+  }
+  __host__ __device__ static constexpr size_t d_main_bytes(bool cc, bool cr) {
+    return size_t(NSTAGE) * d_stage_bytes(cc, cr);
   }
   // LDS map of the epilogue (overlays the operand stages once the K loop is
   // done): the rounded tile [BM][LDT], the strip results, the combined
@@ -417,12 +505,129 @@ struct Gemm {
     for (int i = 0; i < IS; ++i) accr[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     const int nk = k_hi > k_lo ? (k_hi - k_lo + BK - 1) / BK : 0;
+    const int fr = lane & 15, fk = (lane >> 4) * FRAG;
+    // the MFMAs of one KI-wide k step: the tile, then the checksum strips
+    auto mma_kk = [&](const typename Mfma<T>::frag (&af)[IM],
+                      const typename Mfma<T>::frag (&bfr)[JN], const T* sS, const T* sR,
+                      int kk) {
+#pragma unroll
+      for (int i = 0; i < IM; ++i)
+#pragma unroll
+        for (int j = 0; j < JN; ++j) acc[i][j] = Mfma<T>::mma(af[i], bfr[j], acc[i][j]);
+      if (PROT) {
+        // wave-uniform branches keep every fragment index a compile-time
+        // constant (a runtime index would send the arrays to scratch)
+        if (cc) {
+          const auto sf = Mfma<T>::load(sS + fr * LDK + kk + fk);
+          if (wm == 0) {
+#pragma unroll
+            for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[j], accs[j]);
+          } else {
+#pragma unroll
+            for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[JS + j], accs[j]);
+          }
+        }
+        if (cr) {
+          const auto rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
+          if (wn == 0) {
+#pragma unroll
+            for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[i], accr[i]);
+          } else {
+#pragma unroll
+            for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[IS + i], accr[i]);
+          }
+        }
+      }
+    };
+
+    bool main_done = false;
+    if constexpr (sizeof(T) == 2) {
+      if (g.direct) {
+        // Direct path: NSTAGE LDS stages, operand loads issued NSTAGE - 1
+        // stages ahead; the strips go through registers one stage ahead,
+        // issued before the operand loads of the same iteration so that
+        // waiting for them never waits for later operand stages.
+        using DA = Direct<AK, BM>;
+        using DB = Direct<BKM, BN>;
+        constexpr int NDIR = DA::PER_WAVE + DB::PER_WAVE;  // vector-memory ops per wave and stage
+        const int DST = d_stage_bytes(g_cc, g_cr);
+        const bf16_t* Ab = reinterpret_cast<const bf16_t*>(A);
+        const bf16_t* Bb = reinterpret_cast<const bf16_t*>(B);
+        auto slot = [&](int kt) { return smem + (kt % NSTAGE) * DST; };
+        auto issue_dir = [&](int kt) {
+          char* st = slot(kt);
+          DA::issue(Ab, g.lda, m0, g.M, k_lo + kt * BK, st, wave, lane);
+          DB::issue(Bb, g.ldb, n0, g.N, k_lo + kt * BK, st + DA_BYTES, wave, lane);
+        };
+        auto issue_strip = [&](int kt) {
+          const int kn = k_lo + kt * BK;
+          if (cc) ls.load(Ac, g.ldac, rc0, nc_valid, kn, k_hi, tid);
+          if (cr) lr.load(Br, g.ldbr, qc0, nq_valid, kn, k_hi, tid);
+        };
+        auto commit_strip = [&](int kt) {
+          T* st = reinterpret_cast<T*>(slot(kt) + DA_BYTES + DB_BYTES);
+          if (cc) ls.store(st, nc, tid);
+          if (cr) lr.store(st + r_off, nq, tid);
+        };
+        auto compute_d = [&](const char* st) {
+          const T* sS = reinterpret_cast<const T*>(st + DA_BYTES + DB_BYTES);
+          const T* sR = sS + r_off;
+#pragma unroll
+          for (int kk = 0; kk < BK; kk += KI) {
+            typename Mfma<T>::frag af[IM], bfr[JN];
+#pragma unroll
+            for (int i = 0; i < IM; ++i) af[i] = DA::frag(st, wm * WM + i * 16, kk, lane);
+#pragma unroll
+            for (int j = 0; j < JN; ++j) bfr[j] = DB::frag(st + DA_BYTES, wn * WN + j * 16, kk, lane);
+            mma_kk(af, bfr, sS, sR, kk);
+          }
+        };
+        if (nk > 0 && PROT && (cc || cr)) {  // strip rows past the valid ones stay zero
+          const int ns = (cc ? S_ELEMS : 0) + (cr ? S_ELEMS : 0);
+          for (int sl = 0; sl < NSTAGE; ++sl) {
+            T* st = reinterpret_cast<T*>(smem + sl * DST + DA_BYTES + DB_BYTES);
+            for (int e = tid; e < ns; e += NT) st[e] = T(0);
+          }
+          __syncthreads();
+        }
+        if constexpr (NSTAGE == 1) {
+          for (int kt = 0; kt < nk; ++kt) {
+            if (PROT) issue_strip(kt);
+            issue_dir(kt);
+            wait_vmcnt<0>();
+            if (PROT) commit_strip(kt);
+            __syncthreads();
+            compute_d(slot(kt));
+            __syncthreads();
+          }
+        } else {
+          if (nk > 0 && PROT) issue_strip(0);
+          for (int sl = 0; sl < NSTAGE - 1 && sl < nk; ++sl) issue_dir(sl);
+          for (int kt = 0; kt < nk; ++kt) {
+            // stage kt is complete once only the later stages' loads remain
+            const int later = min(NSTAGE - 2, nk - 1 - kt);
+            if (later >= 2) wait_vmcnt<(2 * NDIR < 63 ? 2 * NDIR : 63)>();
+            else if (later == 1) wait_vmcnt<NDIR>();
+            else wait_vmcnt<0>();
+            if (PROT) commit_strip(kt);
+            __syncthreads();  // stage kt visible; every wave is done with stage kt - 1
+            if (PROT && kt + 1 < nk) issue_strip(kt + 1);
+            if (kt + NSTAGE - 1 < nk) issue_dir(kt + NSTAGE - 1);
+            compute_d(slot(kt));
+          }
+          __syncthreads();  // the epilogue reuses the stages
+        }
+        main_done = true;
+      }
+    }
+
+    if (!main_done) {
     if (nk > 0) {
       if (PROT && (cc || cr)) {  // zero the strips of every stage once; loads rewrite only used rows
         const int ns = (cc ? S_ELEMS : 0) + (cr ? S_ELEMS : 0);
         for (int e = tid; e < ns; e += NT) {
           lds[A_ELEMS + B_ELEMS + e] = T(0);
-          if (NSTAGE == 2) lds[STAGE + A_ELEMS + B_ELEMS + e] = T(0);
+          if (NSTAGE >= 2) lds[STAGE + A_ELEMS + B_ELEMS + e] = T(0);
         }
         __syncthreads();
       }
@@ -437,9 +642,8 @@ struct Gemm {
       __syncthreads();
     }
 
-    const int fr = lane & 15, fk = (lane >> 4) * FRAG;
     for (int kt = 0; kt < nk; ++kt) {
-      const int cur = NSTAGE == 2 ? (kt & 1) : 0;
+      const int cur = NSTAGE >= 2 ? (kt & 1) : 0;
       const bool more = kt + 1 < nk;
       if (more) {
         const int kn = k_lo + (kt + 1) * BK;
@@ -448,7 +652,7 @@ struct Gemm {
         if (cc) ls.load(Ac, g.ldac, rc0, nc_valid, kn, k_hi, tid);
         if (cr) lr.load(Br, g.ldbr, qc0, nq_valid, kn, k_hi, tid);
       }
-      const T* sA = lds + cur * STAGE;
+      const T* sA = lds + (NSTAGE >= 2 ? cur : 0) * STAGE;
       const T* sB = sA + A_ELEMS;
       const T* sS = sB + B_ELEMS;
       const T* sR = sS + r_off;
@@ -461,38 +665,11 @@ struct Gemm {
 #pragma unroll
         for (int j = 0; j < JN; ++j)
           bfr[j] = Mfma<T>::load(sB + (wn * WN + j * 16 + fr) * LDK + kk + fk);
-#pragma unroll
-        for (int i = 0; i < IM; ++i)
-#pragma unroll
-          for (int j = 0; j < JN; ++j) acc[i][j] = Mfma<T>::mma(af[i], bfr[j], acc[i][j]);
-        if (PROT) {
-          // wave-uniform branches keep every fragment index a compile-time
-          // constant (a runtime index would send the arrays to scratch)
-          if (cc) {
-            const auto sf = Mfma<T>::load(sS + fr * LDK + kk + fk);
-            if (wm == 0) {
-#pragma unroll
-              for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[j], accs[j]);
-            } else {
-#pragma unroll
-              for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[JS + j], accs[j]);
-            }
-          }
-          if (cr) {
-            const auto rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
-            if (wn == 0) {
-#pragma unroll
-              for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[i], accr[i]);
-            } else {
-#pragma unroll
-              for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[IS + i], accr[i]);
-            }
-          }
-        }
+        mma_kk(af, bfr, sS, sR, kk);
       }
       if (more) {
         if (NSTAGE == 1) __syncthreads();  // every wave is done reading the one stage
-        T* nA = lds + (NSTAGE == 2 ? (cur ^ 1) : 0) * STAGE;
+        T* nA = lds + (NSTAGE >= 2 ? (cur ^ 1) : 0) * STAGE;
         la.store(nA, tid);
         lb.store(nA + A_ELEMS, tid);
         if (cc) ls.store(nA + A_ELEMS + B_ELEMS, nc, tid);
@@ -500,6 +677,7 @@ struct Gemm {
       }
       __syncthreads();
     }
+    }  // register path
 
     // ---- epilogue ----
     if (split) {
@@ -910,16 +1088,36 @@ void gemm_kernel(GemmDesc g) {
   Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>::run(g, smem);
 }
 
+// The direct-to-LDS path needs bf16 operands, K ranges of whole 64-wide
+// stages (K a multiple of 64; causal K ranges and split-K slices then are
+// too), 16-byte aligned operand rows, and whole 8-element chunks along the
+// M or N extent of an MN-major operand.
+template <class T>
+bool direct_ok(const GemmDesc& g, bool ak, bool bk) {
+  if (sizeof(T) != 2 || g.K % 64 != 0) return false;
+  auto al = [](const void* p, int64_t ld, int64_t s0, int64_t s1) {
+    return reinterpret_cast<uintptr_t>(p) % 16 == 0 && ld % 8 == 0 && s0 % 8 == 0 && s1 % 8 == 0;
+  };
+  if (!al(g.A, g.lda, g.sA0, g.sA1) || !al(g.B, g.ldb, g.sB0, g.sB1)) return false;
+  if (!ak && (g.M % 8 != 0 || g.M < 8)) return false;
+  if (!bk && (g.N % 8 != 0 || g.N < 8)) return false;
+  return true;
+}
+
 template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE = 2>
 hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   using G = Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
   auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
   const bool gcc = PROT && g.Ac != nullptr, gcr = PROT && g.Br != nullptr;
+  GemmDesc gd = g;
+  gd.direct = direct_ok<T>(g, AK, BKM) ? 1 : 0;
+  const size_t main = gd.direct ? G::d_main_bytes(gcc, gcr) : G::main_bytes(gcc, gcr);
   // split-K slices skip the staged epilogue: only the operand stages (and
   // the 16 x BN checksum strip image inside them) are needed
-  const size_t lds = g.splitk > 1 ? std::max(G::main_bytes(gcc, gcr), size_t(16 * BN * 4))
-                                  : G::lds_bytes(gcc, gcr);
-  const size_t lds_max = G::lds_bytes(PROT, PROT);
+  const size_t lds = g.splitk > 1 ? std::max(main, size_t(16 * BN * 4))
+                                  : std::max(main, G::EPI_BYTES);
+  const size_t lds_max = std::max(G::lds_bytes(PROT, PROT),
+                                  sizeof(T) == 2 ? G::d_main_bytes(PROT, PROT) : size_t(0));
   if (lds_max > 160 * 1024) return hipErrorInvalidValue;  // this tile does not fit gfx950 LDS
   static bool attr_set = false;  // per instantiation; harmless if repeated
   if (!attr_set) {
@@ -935,7 +1133,7 @@ hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   if (nb > 1 && ks > 1) return hipErrorInvalidValue;  // split-K is for unbatched GEMMs
   const int64_t total = tiles * nb * ks;
   if (total > 0x7fffffff / NT) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(kern, dim3(unsigned(total)), dim3(NT), lds, s, g);
+  hipLaunchKernelGGL(kern, dim3(unsigned(total)), dim3(NT), lds, s, gd);
   return hipGetLastError();
 }
 
