@@ -414,8 +414,10 @@ struct Gemm {
   __host__ __device__ static constexpr int stage_elems(bool cc, bool cr) {
     return A_ELEMS + B_ELEMS + (PROT ? ((cc ? S_ELEMS : 0) + (cr ? S_ELEMS : 0)) : 0);
   }
+  // the register path uses at most two stages
+  static constexpr int RSTAGES = NSTAGE >= 2 ? 2 : 1;
   __host__ __device__ static constexpr size_t main_bytes(bool cc, bool cr) {
-    return size_t(NSTAGE) * stage_elems(cc, cr) * sizeof(T);
+    return size_t(RSTAGES) * stage_elems(cc, cr) * sizeof(T);
   }
   // direct path: unpadded swizzled operand images, the strips as above
   static constexpr int DA_BYTES = BM * 64 * 2, DB_BYTES = BN * 64 * 2;
