@@ -55,10 +55,13 @@ MULTI_KERNEL = {"encode", "dWo", "dWqkv"}
 
 # kernel symbol (as rocprofv3 names it) of single-kernel stages at the
 # workload shape, protected instantiation
+# (kernel symbol, grid size in workgroups): the QKV and output projections
+# share one instantiation and differ by grid
 KERNEL_OF_STAGE = {
-    "qkv": "gemm_kernel<unsigned short, unsigned short, true, false, 256, 128, true, 2>",
-    "softmax_bwd": "softmax_kernel<unsigned short, 2, true, 1, true>",
-    "softmax": "softmax_kernel<unsigned short, 2, false, 1, true>",
+    "qkv": ("gemm_kernel<unsigned short, unsigned short, true, false, 128, 128, true, 2>", 1152),
+    "softmax_bwd": ("softmax_kernel<unsigned short, 2, true, 1, true>", 768),
+    "softmax": ("softmax_kernel<unsigned short, 2, false, 1, true>", 768),
+    "score": ("gemm_kernel<unsigned short, unsigned short, true, true, 128, 128, true, 1>", 3456),
 }
 
 
@@ -111,7 +114,8 @@ def stored_traffic(kernel):
     if not m:
         return None
     rec = json.loads(m.group(1))
-    if rec.get("source_hash") != kernel_source_hash() or rec.get("kernel") != kernel:
+    if (rec.get("source_hash") != kernel_source_hash() or rec.get("kernel") != kernel[0]
+            or rec.get("grid") != kernel[1]):
         return None
     return rec
 
@@ -195,12 +199,13 @@ class Layer:
 
 
 def pmc_workload(key, reps):
-    """Launches for the traffic counters: one protected step (so that the
-    workspace is consistent), `reps` launches of the dominant stage, then
-    `reps` plain copies of COPY_BYTES (reads and writes COPY_BYTES each)."""
+    """Launches for the traffic counters: the checksum encode the QKV
+    projection reads, `reps` launches of the QKV projection (the only
+    launches of its kernel here), then `reps` plain copies of COPY_BYTES
+    (reads and writes COPY_BYTES each)."""
     L = Layer(key)
     torch = L.torch
-    L.step(L.lay_p, (None, 0))
+    L.run_stage(0x001, False)       # encode X^c, W^V r
     for _ in range(reps):
         L.run_stage(0x002, False)   # QKV projection
     src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda").normal_()
@@ -221,17 +226,23 @@ def collect(dirs):
             con = sqlite3.connect(db)
             n_pmc = con.execute("select count(*) from counters_collection").fetchone()[0]
             if n_pmc > 0:
-                q = ("select kernel_name, counter_name, avg(value), count(*), avg(end-start) "
-                     "from counters_collection group by kernel_name, counter_name")
-                for k, c, v, n, dur in con.execute(q):
-                    e = out.setdefault(k, {})
+                cols = [r[1] for r in con.execute("pragma table_info(counters_collection)")]
+                gx = "grid_size" if "grid_size" in cols else ("grid_x" if "grid_x" in cols else "0")
+                wx = "workgroup_size" if "workgroup_size" in cols else (
+                    "workgroup_x" if "workgroup_x" in cols else "1")
+                q = (f"select kernel_name, {gx} / {wx}, counter_name, avg(value), count(*), "
+                     f"avg(end-start) from counters_collection group by kernel_name, {gx}, "
+                     f"counter_name")
+                for k, grid, c, v, n, dur in con.execute(q):
+                    e = out.setdefault((k, int(grid)), {})
                     e[c] = v
                     e["launches"] = n
                     e.setdefault("avg_us", dur / 1e3)
             else:
-                q = "select name, count(*), avg(end-start), sum(end-start) from kernels group by name"
-                for k, n, a, t in con.execute(q):
-                    e = out.setdefault(k, {})
+                q = ("select name, grid_x / workgroup_x, count(*), avg(end-start), sum(end-start) "
+                     "from kernels group by name, grid_x")
+                for k, grid, n, a, t in con.execute(q):
+                    e = out.setdefault((k, int(grid)), {})
                     e.update({"launches": n, "avg_us": a / 1e3, "total_us": t / 1e3})
     return out
 
@@ -245,28 +256,32 @@ def summarize(dirs):
     out = collect(dirs)
     for k in sorted(out, key=lambda k: -out[k].get("total_us", out[k].get("avg_us", 0))):
         vals = " ".join(f"{c}={v:.6g}" for c, v in sorted(out[k].items()))
-        print(f"{short_name(k)} | {vals}")
+        print(f"{short_name(k[0])} | grid={k[1]} | {vals}")
 
 
 def traffic_from(fetch_dir, write_dir, kernel=KERNEL_OF_STAGE["qkv"]):
-    """HBM bytes per launch of `kernel` from a FETCH_SIZE and a WRITE_SIZE
-    run of --pmc-workload, each counter scaled by what it reads for the
-    reference copy (COPY_BYTES in, COPY_BYTES out)."""
+    """HBM bytes per launch of `kernel` (symbol, grid) from a FETCH_SIZE
+    and a WRITE_SIZE run of --pmc-workload, each counter scaled by what it
+    reads for the reference copy (COPY_BYTES in, COPY_BYTES out)."""
     f, w = collect([fetch_dir]), collect([write_dir])
 
     def pick(d, pred):
-        ks = [k for k in d if pred(short_name(k))]
+        ks = [k for k in d if pred(short_name(k[0]), k[1])]
         if len(ks) != 1:
             raise SystemExit(f"expected one matching kernel, found {ks}")
         return d[ks[0]]
 
-    kf, kw = pick(f, lambda n: n == kernel), pick(w, lambda n: n == kernel)
-    cf, cw = pick(f, lambda n: "MulFunctor" in n), pick(w, lambda n: "MulFunctor" in n)
+    sym, grid = kernel
+    # databases without grid sizes report grid 0; the workload launches the
+    # symbol only for this kernel
+    kf = pick(f, lambda n, gr: n == sym and gr in (grid, 0))
+    kw = pick(w, lambda n, gr: n == sym and gr in (grid, 0))
+    cf, cw = pick(f, lambda n, gr: "MulFunctor" in n), pick(w, lambda n, gr: "MulFunctor" in n)
     s_fetch = COPY_BYTES / (cf["FETCH_SIZE"] * 1024.0)
     s_write = COPY_BYTES / (cw["WRITE_SIZE"] * 1024.0)
     fetch = kf["FETCH_SIZE"] * 1024.0 * s_fetch
     write = kw["WRITE_SIZE"] * 1024.0 * s_write
-    rec = {"kernel": kernel, "source_hash": kernel_source_hash(),
+    rec = {"kernel": sym, "grid": grid, "source_hash": kernel_source_hash(),
            "fetch_kib": round(kf["FETCH_SIZE"], 1), "write_kib": round(kw["WRITE_SIZE"], 1),
            "copy_fetch_kib": round(cf["FETCH_SIZE"], 1), "copy_write_kib": round(cw["WRITE_SIZE"], 1),
            "scale_fetch": round(s_fetch, 4), "scale_write": round(s_write, 4),
@@ -499,7 +514,8 @@ def main():
     kern = KERNEL_OF_STAGE.get(name)
     tr = stored_traffic(kern) if kern else None
     roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
-                 "kernel": name, "symbol": kern, "avg_us": round(us, 2),
+                 "kernel": name, "symbol": kern[0] if kern else None,
+                 "grid": kern[1] if kern else None, "avg_us": round(us, 2),
                  "algorithmic": amount, "per_launch": "one call of the stage (one kernel)"})
     if tr:
         roof["traffic_split"] = {"fetch": tr["fetch_bytes"], "write": tr["write_bytes"]}
