@@ -74,15 +74,11 @@ struct GemmDesc {
   // slices and verifies.
   int splitk = 1;
   int64_t sCk = 0, sCck = 0;
-  // Operands go straight from global memory to LDS (bf16 only; set at
-  // launch when K ranges are whole 64-wide stages and every operand row is
-  // 16-byte aligned); otherwise through registers.
-  int direct = 0;
 };
 
 // Tile shapes the GEMM is instantiated for (S1: one LDS stage, for short K
 // such as the head dimension, so that more workgroups fit on a CU).
-enum class Tile : int { T256x128 = 0, T128x128 = 1, T128x64 = 2, T128x128S1 = 3 };
+enum class Tile : int { T128x128 = 1, T128x64 = 2, T128x128S1 = 3 };
 
 // Launch one protected (or, with no checksum operands, plain) GEMM.
 // dtype: ABFT_BF16 or ABFT_FP32 operands; c_fp32: output stored as fp32.

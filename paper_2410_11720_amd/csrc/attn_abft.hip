@@ -173,27 +173,9 @@ Params make_params(const attn_abft_config* c, const Dims& d) {
   return p;
 }
 
-// Tile for a token-major projection: the larger tile when it still yields
-// at least one full wave of workgroups and the checksum strip fits.
 // Projection tile: 128 x 128 (two workgroups per CU with the direct
-// operand path); the 256 x 128 tile fits one per CU and measured slower.
-Tile proj_tile(int64_t M, int64_t N, int64_t R, int num_cu, int dtype) {
-  (void)M; (void)N; (void)R; (void)num_cu; (void)dtype;
-  return Tile::T128x128;
-}
-
-int num_cus() {
-  static int n = 0;
-  if (n == 0) {
-    int dev = 0;
-    hipDeviceProp_t p;
-    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&p, dev) == hipSuccess)
-      n = p.multiProcessorCount;
-    else
-      n = 256;
-  }
-  return n;
-}
+// operand path); a 256 x 128 tile fits one per CU and measured slower.
+Tile proj_tile() { return Tile::T128x128; }
 
 #define CK(x)                                          \
   do {                                                 \
@@ -306,7 +288,6 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
   const char* Wc = static_cast<const char*>(Wqkv);
   const int64_t B = d.B, S = d.S, H = d.H, nh = d.nh, hd = d.d, R = d.R, nq = d.nq, T = d.T;
   const size_t es = d.es;
-  const int ncu = num_cus();
 
   if (!(cfg->flags & ABFT_FLAG_REPORT_APPEND)) CK(launch_report_reset(report, 0, false, s));
 
@@ -346,7 +327,7 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
     }
     g.map.op_base = ABFT_OP_Q; g.map.op_span = int(H); g.map.rows_per_b = int(S);
     g.map.head_cols = int(hd);
-    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(T, 3 * H, R, ncu, dt), s));
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(), s));
   }
   // AS = Q K^T per head (unscaled, before the mask), two-sided checksums
   if (stages & ABFT_STAGE_SCORE) {
@@ -410,7 +391,7 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_O; g.map.rows_per_b = int(S);
-    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(T, H, R, ncu, dt), s));
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(), s));
   }
   return ABFT_OK;
 }
@@ -437,7 +418,6 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   const int64_t B = d.B, S = d.S, H = d.H, nh = d.nh, hd = d.d, R = d.R, nq = d.nq, T = d.T;
   const size_t es = d.es;
   const bool pb = p.sec_bwd;
-  const int ncu = num_cus();
 
   if (!(cfg->flags & ABFT_FLAG_REPORT_APPEND)) CK(launch_report_reset(report, 0, false, s));
   if ((stages & ABFT_STAGE_ENCODE) && pb) CK(launch_encode(dO, dt, B, S, H, H, S * H, int(R), int(hd), F(L.doc), nullptr, s));
@@ -455,7 +435,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DCL; g.map.rows_per_b = int(S); g.map.head_cols = int(hd);
-    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(T, H, R, ncu, dt), s));
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(), s));
   }
   // dWo = CL^T dO, column checksums over head blocks of rows from CL^r
   if (stages & ABFT_STAGE_DWO) {
@@ -578,7 +558,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DX; g.map.rows_per_b = int(S);
-    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(T, H, R, ncu, dt), s));
+    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(), s));
   }
   return ABFT_OK;
 }

@@ -27,6 +27,21 @@ namespace {
 
 constexpr int NT = 256;  // threads per workgroup: 4 waves as 2 (M) x 2 (N)
 
+// The kernel's descriptor (its only argument, at the start of the
+// kernel-argument segment), reached through an opaque copy of the segment
+// address: fields read through it are loaded where they are used instead of
+// being held in scalar registers from the kernel's start.
+__device__ __forceinline__ const GemmDesc& desc_reload() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const GemmDesc* gp =
+      reinterpret_cast<const GemmDesc*>(__builtin_amdgcn_kernarg_segment_ptr());
+  asm volatile("" : "+s"(gp));
+  return *gp;
+#else
+  return *static_cast<const GemmDesc*>(nullptr);  // the host pass emits no device code
+#endif
+}
+
 template <class T> struct Mfma;
 template <> struct Mfma<bf16_t> {
   static constexpr int BK = 64;    // k per LDS stage (128 bytes per row)
@@ -157,7 +172,10 @@ struct TileLoader {
 };
 
 // Checksum strip loader: NC fp32 checksum rows (laid out like the operand)
-// for the tile, stored as NC hi rows and NC lo rows (bf16) or NC fp32 rows.
+// for the tile, stored as NC fp32 rows, or for bf16 operands as a hi and a
+// lo row each, interleaved (row 2r hi, 2r + 1 lo): the strip rows of
+// checksum block b are 4b (hi c1), 4b + 1 (lo c1), 4b + 2 (hi c2), 4b + 3
+// (lo c2).
 template <class T, bool KMAJ>
 struct StripLoader {
   static constexpr int BK = Mfma<T>::BK;
@@ -195,8 +213,8 @@ struct StripLoader {
         if constexpr (sizeof(T) == 2) {
           const bf16_t hi = f2bf(reg[p]);
           const bf16_t lo = f2bf(reg[p] - bf2f(hi));
-          lds[r * LDK + k] = hi;
-          lds[(nc + r) * LDK + k] = lo;
+          lds[(2 * r) * LDK + k] = hi;
+          lds[(2 * r + 1) * LDK + k] = lo;
         } else {
           lds[r * LDK + k] = reg[p];
         }
@@ -406,6 +424,8 @@ struct Gemm {
   static constexpr int JS = JN / 2, IS = IM / 2;  // strip blocks per wave
   static_assert(IM >= 2 && JN >= 2, "tile too small");
   static constexpr int FRAG = KI / 4;  // operand elements per lane
+  // bf16 operands and bf16 output: detection sums on the matrix cores
+  static constexpr bool MSUM = PROT && sizeof(T) == 2 && sizeof(TC) == 2;
 
   // LDS map of the main loop: per stage the A and B tiles, then the
   // checksum strips the GEMM carries (column strip, row strip), so a GEMM
@@ -429,28 +449,35 @@ struct Gemm {
     return size_t(NSTAGE) * d_stage_bytes(cc, cr);
   }
   // LDS map of the epilogue (overlays the operand stages once the K loop is
-  // done): the rounded tile [BM][LDT], the strip results, the combined
-  // propagated checksums and the correction counters.
+  // done): the rounded tile [BM][LDT], then one region that first holds
+  // the strip results ([16][BN] column strip, [BM][16] row strip), then,
+  // once those are read, the combined propagated checksums and the
+  // detection's segment sums, and last the correction counters and queue
+  // (in the segment sums' place). Sized so that a 128 x 128 bf16 tile keeps
+  // three workgroups per CU.
   static constexpr int MINB = sizeof(T) == 2 ? 32 : 16;  // smallest checksum block
   static constexpr int TPAD = 16 / sizeof(TC);
   static constexpr int LDT = BN + TPAD;
   static constexpr size_t TILE_BYTES = size_t(BM) * LDT * sizeof(TC);
-  // strip images; after the checksums are read from them they hold the
-  // detection's segment sums ([BM/MINB][BN][2] and [BM][BN/MINB][2])
-  static constexpr size_t CSL = 16 * BN > 2 * BN * (BM / MINB) ? 16 * BN : 2 * BN * (BM / MINB);
-  static constexpr size_t RSL = 16 * BM > 2 * BM * (BN / MINB) ? 16 * BM : 2 * BM * (BN / MINB);
+  static constexpr size_t STRIPS = 16 * BN + 16 * BM;
+  // checksum pairs ([BM/MINB][BN][2], [BM][BN/MINB][2]); the segment sums
+  // (sum, magnitude) have the same shapes
   static constexpr size_t CCV = (BM / MINB) * BN * 2, RCV = BM * (BN / MINB) * 2;
   static constexpr size_t CNT = BM * (BN / MINB) + (BM / MINB) * BN;
   // recompute queue of the correction passes: count, QMAX x (row, col,
   // observed value), and one partial sum per wave
   static constexpr int QMAX = 32;
   static constexpr size_t QUE = 1 + 3 * QMAX + NT / 64;
-  static constexpr size_t EPI_BYTES =
-      TILE_BYTES + (PROT ? (CSL + RSL + CCV + RCV + CNT + QUE) * 4 : 0);
+  static constexpr size_t WORK = CCV + RCV > CNT + QUE ? CCV + RCV : CNT + QUE;
+  static constexpr size_t EREG = STRIPS > CCV + RCV + WORK ? STRIPS : CCV + RCV + WORK;
+  static constexpr size_t EPI_BYTES = TILE_BYTES + (PROT ? EREG * 4 : 0);
   __host__ __device__ static constexpr size_t lds_bytes(bool cc, bool cr) {
     return main_bytes(cc, cr) > EPI_BYTES ? main_bytes(cc, cr) : EPI_BYTES;
   }
 
+  // DIR selects the direct-to-LDS operand path (bf16 only) at compile time,
+  // so each kernel carries the registers and code of one path only.
+  template <bool DIR>
   __device__ static __forceinline__ void run(const GemmDesc& g, char* smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -500,6 +527,7 @@ struct Gemm {
     for (int i = 0; i < IM; ++i)
 #pragma unroll
       for (int j = 0; j < JN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // strip results: the two waves sharing columns (rows) split them
     floatx4 accs[JS], accr[IS];
 #pragma unroll
     for (int j = 0; j < JS; ++j) accs[j] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -542,9 +570,9 @@ struct Gemm {
       }
     };
 
-    bool main_done = false;
-    if constexpr (sizeof(T) == 2) {
-      if (g.direct) {
+    if constexpr (DIR) {
+      static_assert(sizeof(T) == 2, "the direct path is for bf16 operands");
+      {
         // Direct path: NSTAGE LDS stages, operand loads issued NSTAGE - 1
         // stages ahead; the strips go through registers one stage ahead,
         // issued before the operand loads of the same iteration so that
@@ -584,14 +612,8 @@ struct Gemm {
             mma_kk(af, bfr, sS, sR, kk);
           }
         };
-        if (nk > 0 && PROT && (cc || cr)) {  // strip rows past the valid ones stay zero
-          const int ns = (cc ? S_ELEMS : 0) + (cr ? S_ELEMS : 0);
-          for (int sl = 0; sl < NSTAGE; ++sl) {
-            T* st = reinterpret_cast<T*>(smem + sl * DST + DA_BYTES + DB_BYTES);
-            for (int e = tid; e < ns; e += NT) st[e] = T(0);
-          }
-          __syncthreads();
-        }
+        // strip rows past the used ones are never written: each only feeds
+        // an MFMA result row of its own, which nothing reads
         if constexpr (NSTAGE == 1) {
           for (int kt = 0; kt < nk; ++kt) {
             if (PROT) issue_strip(kt);
@@ -619,20 +641,9 @@ struct Gemm {
           }
           __syncthreads();  // the epilogue reuses the stages
         }
-        main_done = true;
       }
-    }
-
-    if (!main_done) {
+    } else {
     if (nk > 0) {
-      if (PROT && (cc || cr)) {  // zero the strips of every stage once; loads rewrite only used rows
-        const int ns = (cc ? S_ELEMS : 0) + (cr ? S_ELEMS : 0);
-        for (int e = tid; e < ns; e += NT) {
-          lds[A_ELEMS + B_ELEMS + e] = T(0);
-          if (NSTAGE >= 2) lds[STAGE + A_ELEMS + B_ELEMS + e] = T(0);
-        }
-        __syncthreads();
-      }
       la.load(A, g.lda, m0, g.M, k_lo, k_hi, tid);
       lb.load(B, g.ldb, n0, g.N, k_lo, k_hi, tid);
       if (cc) ls.load(Ac, g.ldac, rc0, nc_valid, k_lo, k_hi, tid);
@@ -682,7 +693,9 @@ struct Gemm {
     }  // register path
 
     // ---- epilogue ----
-    if (split) {
+    {
+    const GemmDesc& g = desc_reload();  // not held across the main loop
+    if constexpr (sizeof(TC) == 4) if (split) {
       // fp32 partials go straight from the accumulators to this slice; the
       // column-checksum strip is combined (hi + lo) through a small LDS
       // image that fits inside the freed operand stages
@@ -710,8 +723,8 @@ struct Gemm {
           const int blk = v / BN, n = v % BN;
           float c1, c2;
           if constexpr (sizeof(T) == 2) {
-            c1 = CsL[(2 * blk) * BN + n] + CsL[(nc + 2 * blk) * BN + n];
-            c2 = CsL[(2 * blk + 1) * BN + n] + CsL[(nc + 2 * blk + 1) * BN + n];
+            c1 = CsL[(4 * blk) * BN + n] + CsL[(4 * blk + 1) * BN + n];
+            c2 = CsL[(4 * blk + 2) * BN + n] + CsL[(4 * blk + 3) * BN + n];
           } else {
             c1 = CsL[(2 * blk) * BN + n];
             c2 = CsL[(2 * blk + 1) * BN + n];
@@ -727,32 +740,49 @@ struct Gemm {
     // 1. round to storage and stage the tile (and the strip results) in LDS
     TC* tile = reinterpret_cast<TC*>(smem);
     float* CsL = reinterpret_cast<float*>(smem + TILE_BYTES);
-    float* RsL = CsL + CSL;
-    float* ccv = RsL + RSL;
+    float* RsL = CsL + 16 * BN;
+    float* ccv = CsL;         // after the strips are read
     float* rcv = ccv + CCV;
-    int* rowcnt = reinterpret_cast<int*>(rcv + RCV);
-    int* colcnt = rowcnt + BM * (BN / MINB);
+    float* colp = rcv + RCV;  // segment sums [BM / MINB][BN][2]
+    float* rowp = colp + CCV; //              [BN / MINB][BM][2]
+    // bf16 tiles take their segment sums on the matrix cores: the stored
+    // values, packed two per register, are the MFMA operands
+    uint32_t pk[MSUM ? IM : 1][MSUM ? JN : 1][2];
 #pragma unroll
     for (int i = 0; i < IM; ++i)
 #pragma unroll
-      for (int j = 0; j < JN; ++j)
+      for (int j = 0; j < JN; ++j) {
+        const int row = wm * WM + i * 16 + (lane >> 4) * 4, col = wn * WN + j * 16 + fr;
+        if constexpr (MSUM) {
+          bf16_t h[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          tile[(wm * WM + i * 16 + (lane >> 4) * 4 + r) * LDT + wn * WN + j * 16 + fr] =
-              Storage<TC>::store(acc[i][j][r]);  // fp32 partials stay unrounded
+          for (int r = 0; r < 4; ++r) {
+            h[r] = f2bf(acc[i][j][r]);
+            tile[(row + r) * LDT + col] = h[r];
+          }
+          pk[i][j][0] = uint32_t(h[0]) | (uint32_t(h[1]) << 16);
+          pk[i][j][1] = uint32_t(h[2]) | (uint32_t(h[3]) << 16);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)  // fp32 partials stay unrounded
+            tile[(row + r) * LDT + col] = Storage<TC>::store(acc[i][j][r]);
+        }
+      }
     if (PROT && cc) {
 #pragma unroll
       for (int j = 0; j < JS; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          CsL[((lane >> 4) * 4 + r) * BN + wn * WN + (wm * JS + j) * 16 + fr] = accs[j][r];
+          CsL[((lane >> 4) * 4 + r) * BN + wn * WN + (wm * JS + j) * 16 + fr] =
+              accs[j][r];
     }
     if (PROT && cr) {
 #pragma unroll
       for (int i = 0; i < IS; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          RsL[(wm * WM + (wn * IS + i) * 16 + fr) * 16 + (lane >> 4) * 4 + r] = accr[i][r];
+          RsL[(wm * WM + (wn * IS + i) * 16 + fr) * 16 + (lane >> 4) * 4 + r] =
+              accr[i][r];
     }
     // injected faults (test-only): written into the rounded tile before any
     // verification
@@ -770,6 +800,17 @@ struct Gemm {
                     : Storage<TC>::store(Storage<TC>::round(ft.value));
         }
       }
+      __syncthreads();
+      if constexpr (MSUM) {  // the packed values follow the tile
+#pragma unroll
+        for (int i = 0; i < IM; ++i)
+#pragma unroll
+          for (int j = 0; j < JN; ++j) {
+            const TC* t = tile + (wm * WM + i * 16 + (lane >> 4) * 4) * LDT + wn * WN + j * 16 + fr;
+            pk[i][j][0] = uint32_t(t[0]) | (uint32_t(t[LDT]) << 16);
+            pk[i][j][1] = uint32_t(t[2 * LDT]) | (uint32_t(t[3 * LDT]) << 16);
+          }
+      }
     }
     __syncthreads();
 
@@ -778,84 +819,150 @@ struct Gemm {
     const int nrb = cr ? BN / g.Rn : 0;   // row blocks per tile row
     const int ncb = cc ? BM / g.Rm : 0;   // column blocks per tile column
     if (PROT && (cc || cr)) {
-      // 2a. propagated checksums of every vector (strip hi + lo rows)
-      for (int v = tid; v < ncb * BN; v += NT) {
-        const int blk = v / BN, n = v % BN;
-        if constexpr (sizeof(T) == 2) {
-          ccv[v * 2] = CsL[(2 * blk) * BN + n] + CsL[(nc + 2 * blk) * BN + n];
-          ccv[v * 2 + 1] = CsL[(2 * blk + 1) * BN + n] + CsL[(nc + 2 * blk + 1) * BN + n];
-        } else {
-          ccv[v * 2] = CsL[(2 * blk) * BN + n];
-          ccv[v * 2 + 1] = CsL[(2 * blk + 1) * BN + n];
+      // 2a. propagated checksums of every vector (strip hi + lo rows), held
+      //     in registers until every thread has read the strips; row
+      //     vectors are walked row-fastest, so only shifts divide
+      constexpr int CI = int((CCV / 2 + NT - 1) / NT), RI = int((RCV / 2 + NT - 1) / NT);
+      float2 cv[CI], rv[RI];
+#pragma unroll
+      for (int i = 0; i < CI; ++i) {
+        const int v = tid + i * NT, blk = v / BN, n = v % BN;
+        if (v < ncb * BN) {
+          if constexpr (sizeof(T) == 2) {
+            cv[i].x = CsL[(4 * blk) * BN + n] + CsL[(4 * blk + 1) * BN + n];
+            cv[i].y = CsL[(4 * blk + 2) * BN + n] + CsL[(4 * blk + 3) * BN + n];
+          } else {
+            cv[i].x = CsL[(2 * blk) * BN + n];
+            cv[i].y = CsL[(2 * blk + 1) * BN + n];
+          }
         }
       }
-      for (int u = tid; u < BM * nrb; u += NT) {
-        const int row = u / nrb, rb = u % nrb;
-        if constexpr (sizeof(T) == 2) {
-          rcv[u * 2] = RsL[row * 16 + 2 * rb] + RsL[row * 16 + nq + 2 * rb];
-          rcv[u * 2 + 1] = RsL[row * 16 + 2 * rb + 1] + RsL[row * 16 + nq + 2 * rb + 1];
-        } else {
-          rcv[u * 2] = RsL[row * 16 + 2 * rb];
-          rcv[u * 2 + 1] = RsL[row * 16 + 2 * rb + 1];
+#pragma unroll
+      for (int i = 0; i < RI; ++i) {
+        const int w = tid + i * NT, row = w % BM, rb = w / BM;
+        if (w < BM * nrb) {
+          if constexpr (sizeof(T) == 2) {
+            rv[i].x = RsL[row * 16 + 4 * rb] + RsL[row * 16 + 4 * rb + 1];
+            rv[i].y = RsL[row * 16 + 4 * rb + 2] + RsL[row * 16 + 4 * rb + 3];
+          } else {
+            rv[i].x = RsL[row * 16 + 2 * rb];
+            rv[i].y = RsL[row * 16 + 2 * rb + 1];
+          }
         }
       }
       __syncthreads();  // the strip images are consumed; their space is reused
-      // 2b. sums and magnitude sums of the stored tile over SEG-element
-      //     segments: column pairs read 4 (or 8) bytes per row, row
-      //     segments 16 bytes at a time, so every thread has a share
-      constexpr int SEG = MINB;
-      float* colp = CsL;  // [BM / SEG][BN][2]
-      float* rowp = RsL;  // [BM][BN / SEG][2]
-      if (verify >= 1) {
-        for (int w = tid; w < (BN / 2) * (BM / SEG); w += NT) {
-          const int cp = w % (BN / 2), sg = w / (BN / 2);
-          const TC* p = tile + sg * SEG * LDT + 2 * cp;
-          float s0 = 0.f, s1 = 0.f, a0 = 0.f, a1 = 0.f;
-#pragma unroll 8
-          for (int r = 0; r < SEG; ++r) {
-            float x0, x1;
-            if constexpr (sizeof(TC) == 2) {
-              const uint32_t wd = *reinterpret_cast<const uint32_t*>(p + r * LDT);
-              x0 = __uint_as_float(wd << 16);
-              x1 = __uint_as_float(wd & 0xffff0000u);
-            } else {
-              const float2 f = *reinterpret_cast<const float2*>(p + r * LDT);
-              x0 = f.x;
-              x1 = f.y;
-            }
-            s0 += x0; s1 += x1;
-            a0 += fabsf(x0); a1 += fabsf(x1);
-          }
-          float* o = colp + (sg * BN + 2 * cp) * 2;
-          o[0] = s0; o[1] = a0; o[2] = s1; o[3] = a1;
-        }
+#pragma unroll
+      for (int i = 0; i < CI; ++i)
+        if (tid + i * NT < ncb * BN) reinterpret_cast<float2*>(ccv)[tid + i * NT] = cv[i];
+#pragma unroll
+      for (int i = 0; i < RI; ++i) {
+        const int w = tid + i * NT;
+        if (w < BM * nrb) reinterpret_cast<float2*>(rcv)[(w % BM) * nrb + w / BM] = rv[i];
       }
-      if (verify == 2) {
-        constexpr int PER16 = 16 / sizeof(TC);
-        for (int w = tid; w < BM * (BN / SEG); w += NT) {
-          const int row = w % BM, sg = w / BM;
-          const TC* p = tile + row * LDT + sg * SEG;
-          float s0 = 0.f, a0 = 0.f;
+      // 2b. sums and magnitude sums of the stored tile over SEG-element
+      //     segments
+      constexpr int SEG = MINB;
+      if constexpr (MSUM) {
+        // A ones operand sums the k extent of the other operand, whatever
+        // the order of k within it. Column segments: the 8 values of one
+        // column a lane holds for blocks i = 2s, 2s + 1 (rows 4g..4g+3 of
+        // each, g = lane / 16) are together the 32 rows of segment s.
+        const bf16x8 ones = __builtin_bit_cast(
+            bf16x8, uint4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+        const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+        if (verify >= 1) {
 #pragma unroll
-          for (int q = 0; q < SEG / PER16; ++q) {
-            const uint4 raw = *reinterpret_cast<const uint4*>(p + q * PER16);
-            const uint32_t wd[4] = {raw.x, raw.y, raw.z, raw.w};
+          for (int sg = 0; sg < IM / 2; ++sg)
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
+            for (int j = 0; j < JN; ++j) {
+              const uint4 u = {pk[2 * sg][j][0], pk[2 * sg][j][1], pk[2 * sg + 1][j][0],
+                               pk[2 * sg + 1][j][1]};
+              const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu,
+                                u.w & 0x7fff7fffu};
+              const floatx4 sm = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, u), zero);
+              const floatx4 mg = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, ua), zero);
+              if (lane < 16)
+                reinterpret_cast<float2*>(colp)[(wm * (WM / SEG) + sg) * BN + wn * WN + j * 16 +
+                                                lane] = float2{sm[0], mg[0]};
+            }
+        }
+        // row segments: 16 rows x 32 columns of the staged tile as the
+        // A operand (row lane % 16, 8 consecutive columns per lane group);
+        // lanes 0, 16, 32, 48 receive the sums of rows 4g..4g+3
+        if (verify == 2) {
+          constexpr int RG = BM / 16, UNITS = RG * (BN / SEG);
+          static_assert(UNITS % (NT / 64) == 0, "row units per wave");
+#pragma unroll
+          for (int q = 0; q < UNITS / (NT / 64); ++q) {
+            const int unit = wave * (UNITS / (NT / 64)) + q;
+            const int r0 = (unit % RG) * 16, sg = unit / RG;
+            const uint4 u = *reinterpret_cast<const uint4*>(
+                tile + (r0 + (lane & 15)) * LDT + sg * SEG + 8 * (lane >> 4));
+            const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu,
+                              u.w & 0x7fff7fffu};
+            const floatx4 sm = Mfma<T>::mma(__builtin_bit_cast(bf16x8, u), ones, zero);
+            const floatx4 mg = Mfma<T>::mma(__builtin_bit_cast(bf16x8, ua), ones, zero);
+            if ((lane & 15) == 0) {
+              float4* o = reinterpret_cast<float4*>(rowp + (sg * BM + r0 + 4 * (lane >> 4)) * 2);
+              o[0] = float4{sm[0], mg[0], sm[1], mg[1]};
+              o[1] = float4{sm[2], mg[2], sm[3], mg[3]};
+            }
+          }
+        }
+      } else {
+        // column pairs read 4 (or 8) bytes per row, row segments 16 bytes
+        // at a time, so every thread has a share
+        if (verify >= 1) {
+          for (int w = tid; w < (BN / 2) * (BM / SEG); w += NT) {
+            const int cp = w % (BN / 2), sg = w / (BN / 2);
+            const TC* p = tile + sg * SEG * LDT + 2 * cp;
+            float s0 = 0.f, s1 = 0.f, a0 = 0.f, a1 = 0.f;
+#pragma unroll 8
+            for (int r = 0; r < SEG; ++r) {
+              float x0, x1;
               if constexpr (sizeof(TC) == 2) {
-                const float x0 = __uint_as_float(wd[k] << 16);
-                const float x1 = __uint_as_float(wd[k] & 0xffff0000u);
-                s0 += x0 + x1;
-                a0 += fabsf(x0) + fabsf(x1);
+                const uint32_t wd = *reinterpret_cast<const uint32_t*>(p + r * LDT);
+                x0 = __uint_as_float(wd << 16);
+                x1 = __uint_as_float(wd & 0xffff0000u);
               } else {
-                const float x0 = __uint_as_float(wd[k]);
-                s0 += x0;
-                a0 += fabsf(x0);
+                const float2 f = *reinterpret_cast<const float2*>(p + r * LDT);
+                x0 = f.x;
+                x1 = f.y;
+              }
+              s0 += x0; s1 += x1;
+              a0 += fabsf(x0); a1 += fabsf(x1);
+            }
+            float* o = colp + (sg * BN + 2 * cp) * 2;
+            o[0] = s0; o[1] = a0; o[2] = s1; o[3] = a1;
+          }
+        }
+        if (verify == 2) {
+          constexpr int PER16 = 16 / sizeof(TC);
+          for (int w = tid; w < BM * (BN / SEG); w += NT) {
+            const int row = w % BM, sg = w / BM;
+            const TC* p = tile + row * LDT + sg * SEG;
+            float s0 = 0.f, a0 = 0.f;
+#pragma unroll
+            for (int q = 0; q < SEG / PER16; ++q) {
+              const uint4 raw = *reinterpret_cast<const uint4*>(p + q * PER16);
+              const uint32_t wd[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+              for (int k = 0; k < 4; ++k) {
+                if constexpr (sizeof(TC) == 2) {
+                  const float x0 = __uint_as_float(wd[k] << 16);
+                  const float x1 = __uint_as_float(wd[k] & 0xffff0000u);
+                  s0 += x0 + x1;
+                  a0 += fabsf(x0) + fabsf(x1);
+                } else {
+                  const float x0 = __uint_as_float(wd[k]);
+                  s0 += x0;
+                  a0 += fabsf(x0);
+                }
               }
             }
+            rowp[w * 2] = s0;
+            rowp[w * 2 + 1] = a0;
           }
-          rowp[(row * (BN / SEG) + sg) * 2] = s0;
-          rowp[(row * (BN / SEG) + sg) * 2 + 1] = a0;
         }
       }
       __syncthreads();
@@ -878,21 +985,21 @@ struct Gemm {
       }
       if (verify == 2) {
         const int spb = g.Rn / SEG;  // segments per row block
-        for (int u = tid; u < BM * nrb; u += NT) {
-          const int row = u / nrb, rb = u % nrb;
+        for (int w = tid; w < BM * nrb; w += NT) {
+          const int row = w % BM, rb = w / BM;
           if (!(m0 + row < g.M && n0 + rb * g.Rn < g.N)) continue;
           float r1 = 0.f, sa = 0.f;
           for (int q = 0; q < spb; ++q) {
-            r1 += rowp[(row * (BN / SEG) + rb * spb + q) * 2];
-            sa += rowp[(row * (BN / SEG) + rb * spb + q) * 2 + 1];
+            r1 += rowp[((rb * spb + q) * BM + row) * 2];
+            sa += rowp[((rb * spb + q) * BM + row) * 2 + 1];
           }
-          my_flag |= flagged(rcv[u * 2] - r1, sa, g.e_rel);
+          my_flag |= flagged(rcv[(row * nrb + rb) * 2] - r1, sa, g.e_rel);
         }
       }
       // 3. correction, only for a tile with a flagged vector
       if (__syncthreads_or(my_flag))
-        passes(g, tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, rowcnt, colcnt, nrb, ncb, verify,
-               tid);
+        passes(tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, reinterpret_cast<int*>(colp), nrb, ncb,
+               verify, tid);
     }
 
     // 4. store the tile with 16-byte coalesced chunks
@@ -934,17 +1041,20 @@ struct Gemm {
         }
       }
     }
+    }  // epilogue
   }
 
   // EEC-ABFT on the LDS tile, one thread per vector (as in the paper's
   // Fig. 4): column pass, refresh of 1R-corrupted row checksums, row pass,
   // refresh of 1C-corrupted column checksums, final check (Sec. 4.2, 4.3).
   __device__ static __forceinline__ void passes(
-      const GemmDesc& g, TC* tile, const T* A, const T* B, int z, int m0, int n0, int k_lo,
-      int k_hi, float* ccv, float* rcv, int* rowcnt, int* colcnt, int nrb, int ncb, int verify,
-      int tid) {
-    for (int e = tid; e < BM * (BN / MINB) + (BM / MINB) * BN; e += NT) rowcnt[e] = 0;
-    int* qn = rowcnt + BM * (BN / MINB) + (BM / MINB) * BN;  // queue length
+      TC* tile, const T* A, const T* B, int z, int m0, int n0, int k_lo, int k_hi, float* ccv,
+      float* rcv, int* work, int nrb, int ncb, int verify, int tid) {
+    const GemmDesc& g = desc_reload();
+    int* rowcnt = work;                        // [BM][BN / MINB]
+    int* colcnt = work + BM * (BN / MINB);     // [BM / MINB][BN]
+    for (int e = tid; e < int(CNT); e += NT) rowcnt[e] = 0;
+    int* qn = work + CNT;                      // queue length
     int* qe = qn + 1;                                         // queue entries
     float* red = reinterpret_cast<float*>(qe + 3 * QMAX);     // per-wave partials
     if (tid == 0) *qn = 0;
@@ -1079,15 +1189,20 @@ struct Gemm {
 };
 
 // Tiles up to 128 x 128 keep two waves per SIMD (at most 256 registers,
-// arch + accumulation, per lane), so two workgroups share a CU.
-template <int BM, int BN>
-constexpr int gemm_waves_per_eu() { return BM * BN <= 128 * 128 ? 2 : 1; }
+// arch + accumulation, per lane), so two workgroups share a CU; the
+// unprotected one-stage bf16 tile, which has no load in flight while it
+// computes, keeps three (at most 168 registers) to hide its loads behind
+// the other workgroups' work.
+template <class T, int BM, int BN, bool PROT, int NSTAGE>
+constexpr int gemm_waves_per_eu() {
+  return BM * BN > 128 * 128 ? 1 : (sizeof(T) == 2 && NSTAGE == 1 && !PROT ? 3 : 2);
+}
 
-template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<BM, BN>())))
+template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE, bool DIR>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<T, BM, BN, PROT, NSTAGE>())))
 void gemm_kernel(GemmDesc g) {
   extern __shared__ __align__(16) char smem[];
-  Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>::run(g, smem);
+  Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>::template run<DIR>(g, smem);
 }
 
 // The direct-to-LDS path needs bf16 operands, K ranges of whole 64-wide
@@ -1106,14 +1221,23 @@ bool direct_ok(const GemmDesc& g, bool ak, bool bk) {
   return true;
 }
 
+// Sets the dynamic-LDS limit of one kernel once (per instantiation).
+template <auto KERN>
+hipError_t set_lds_limit(size_t bytes) {
+  static bool done = false;  // harmless if repeated
+  if (done) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(KERN),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, int(bytes));
+  if (e == hipSuccess) done = true;
+  return e;
+}
+
 template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE = 2>
 hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   using G = Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
-  auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
   const bool gcc = PROT && g.Ac != nullptr, gcr = PROT && g.Br != nullptr;
-  GemmDesc gd = g;
-  gd.direct = direct_ok<T>(g, AK, BKM) ? 1 : 0;
-  const size_t main = gd.direct ? G::d_main_bytes(gcc, gcr) : G::main_bytes(gcc, gcr);
+  const bool direct = direct_ok<T>(g, AK, BKM);
+  const size_t main = direct ? G::d_main_bytes(gcc, gcr) : G::main_bytes(gcc, gcr);
   // split-K slices skip the staged epilogue: only the operand stages (and
   // the 16 x BN checksum strip image inside them) are needed
   const size_t lds = g.splitk > 1 ? std::max(main, size_t(16 * BN * 4))
@@ -1121,33 +1245,50 @@ hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   const size_t lds_max = std::max(G::lds_bytes(PROT, PROT),
                                   sizeof(T) == 2 ? G::d_main_bytes(PROT, PROT) : size_t(0));
   if (lds_max > 160 * 1024) return hipErrorInvalidValue;  // this tile does not fit gfx950 LDS
-  static bool attr_set = false;  // per instantiation; harmless if repeated
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_max));
-    if (e != hipSuccess) return e;
-    attr_set = true;
+  auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, false>;
+  hipError_t e = hipSuccess;
+  if constexpr (sizeof(T) == 2) {
+    if (direct) {
+      constexpr auto k = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, true>;
+      kern = k;
+      e = set_lds_limit<k>(lds_max);
+    }
   }
+  if (!direct) {
+    constexpr auto k = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, false>;
+    e = set_lds_limit<k>(lds_max);
+  }
+  if (e != hipSuccess) return e;
   const int64_t ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
   const int64_t tiles = tri_tiles(g, BM, BN) ? ntm * (ntm + 1) / 2 : ntm * ntn;
   const int64_t nb = int64_t(g.nb0) * g.nb1, ks = g.splitk > 1 ? g.splitk : 1;
   if (tiles == 0 || nb == 0) return hipSuccess;
   if (nb > 1 && ks > 1) return hipErrorInvalidValue;  // split-K is for unbatched GEMMs
+  if (ks > 1 && sizeof(TC) != 4) return hipErrorInvalidValue;  // fp32 partial slices
   const int64_t total = tiles * nb * ks;
   if (total > 0x7fffffff / NT) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(kern, dim3(unsigned(total)), dim3(NT), lds, s, gd);
+  hipLaunchKernelGGL(kern, dim3(unsigned(total)), dim3(NT), lds, s, g);
   return hipGetLastError();
 }
 
+// The (layout, tile) pairs the attention layer launches; bf16 GEMMs with
+// fp32 output are the split-K weight gradients only.
 template <class T, class TC, bool AK, bool BKM, bool PROT>
 hipError_t launch_tile(const GemmDesc& g, Tile tile, hipStream_t s) {
-  switch (tile) {
-    case Tile::T256x128: return launch_t<T, TC, AK, BKM, 256, 128, PROT>(g, s);
-    case Tile::T128x128: return launch_t<T, TC, AK, BKM, 128, 128, PROT>(g, s);
-    case Tile::T128x64: return launch_t<T, TC, AK, BKM, 128, 64, PROT>(g, s);
-    case Tile::T128x128S1: return launch_t<T, TC, AK, BKM, 128, 128, PROT, 1>(g, s);
+  constexpr bool wgrad = sizeof(T) == 2 && sizeof(TC) == 4;
+  if constexpr (wgrad) {
+    if constexpr (!AK && !BKM)
+      if (tile == Tile::T128x128) return launch_t<T, TC, AK, BKM, 128, 128, PROT>(g, s);
+    return hipErrorInvalidValue;
+  } else {
+    if (tile == Tile::T128x128) return launch_t<T, TC, AK, BKM, 128, 128, PROT>(g, s);
+    if constexpr (AK && BKM) {
+      if (tile == Tile::T128x128S1) return launch_t<T, TC, AK, BKM, 128, 128, PROT, 1>(g, s);
+    } else {
+      if (tile == Tile::T128x64) return launch_t<T, TC, AK, BKM, 128, 64, PROT>(g, s);
+    }
+    return hipErrorInvalidValue;
   }
-  return hipErrorInvalidValue;
 }
 
 template <class T, class TC, bool PROT>
