@@ -17,6 +17,8 @@ Modules:
   layer     - the protected layer forward (Sec. 4.4 protection sections) and
               the protected backward chain (an extension; the paper is silent)
   freq      - adaptive detection frequencies (Sec. 4.5, Algorithm 1)
+  fused     - the score/softmax/context core in an online-softmax form that
+              stores neither AS nor AP (an extension), row-side checks
 
 Parity pins are listed in the test files that check each function.
 """

@@ -258,14 +258,12 @@ def _causal_valid(n, S, R):
     return colv, rowv
 
 
-def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
-    """Protected forward of one attention layer. Inputs hold storage-dtype
-    values. Returns a dict with O, the saved tensors, propagated checksums
-    the backward reuses, and the event list."""
-    run = _Run(p, faults)
+def project(run, X, Wqkv, p: OracleParams):
+    """Encoding and the protected QKV projection (Sec. 4.4 S_AS / S_CL
+    members X W^Q, X W^K, X W^V), with the root check. Returns the
+    projection outputs, their checksums and the layer's dimensions."""
     X = np.asarray(X, dtype=np.float64)
     Wqkv = np.asarray(Wqkv, dtype=np.float64)
-    Wo = np.asarray(Wo, dtype=np.float64)
     B, S, H = X.shape
     nh = p.heads
     d = H // nh
@@ -299,6 +297,7 @@ def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
                        col_valid=np.broadcast_to(colmask, (B, nq, 3 * H)),
                        recompute=lambda k, i, j: X[k, i] @ Wqkv[:, j])
 
+
     def heads_of(M):        # [B,S,H] -> [B,nh,S,d]
         return M.reshape(B, S, nh, d).transpose(0, 2, 1, 3)
 
@@ -307,6 +306,35 @@ def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
 
     Qh, Kh, Vh = (heads_of(QKV[..., i * H:(i + 1) * H]) for i in range(3))
     Qch, Kch = heads_of_c(QKVc[..., :H]), heads_of_c(QKVc[..., H:2 * H])
+    return dict(X=X, Wqkv=Wqkv, B=B, S=S, H=H, nh=nh, d=d, R=R, nq=nq, scale=scale,
+                Xc=Xc, Xr=Xr, QKV=QKV, QKVc=QKVc, Vr=Vr, Qh=Qh, Kh=Kh, Vh=Vh,
+                Qch=Qch, Kch=Kch)
+
+
+def output_projection(run, CL, CLc_full, Wo, p: OracleParams):
+    """O = CL W^O with O^c = CL^c W^O and its column pass (Sec. 4.4 S_O)."""
+    rnd = run.rnd
+    O = rnd(CL @ Wo)
+    Oc = CLc_full @ Wo
+    run.inject("O", O, lambda b, h, r, c: (b, r, c))
+    if run.on("O"):
+        run.verify(O, Oc, p.block_rows, lambda k, i, j: ("O", k, 0, i, j),
+                   recompute=lambda k, i, j: CL[k, i] @ Wo[:, j])
+    return O, Oc
+
+
+def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
+    """Protected forward of one attention layer. Inputs hold storage-dtype
+    values. Returns a dict with O, the saved tensors, propagated checksums
+    the backward reuses, and the event list."""
+    run = _Run(p, faults)
+    pr = project(run, X, Wqkv, p)
+    X, Wqkv = pr["X"], pr["Wqkv"]
+    B, S, H, nh, d, R, nq, scale = (pr[k] for k in ("B", "S", "H", "nh", "d", "R", "nq", "scale"))
+    Xc, Xr, QKV, QKVc, Vr = (pr[k] for k in ("Xc", "Xr", "QKV", "QKVc", "Vr"))
+    Qh, Kh, Vh, Qch, Kch = (pr[k] for k in ("Qh", "Kh", "Vh", "Qch", "Kch"))
+    Wo = np.asarray(Wo, dtype=np.float64)
+    rnd = run.rnd
 
     # score GEMM AS = Q K^T (unscaled, before the mask), two-sided checksums
     AS = rnd(Qh @ Kh.swapaxes(-1, -2))                         # [B,nh,S,S]
@@ -350,12 +378,7 @@ def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
     CLr_full = CLr[:, :, :, 0, :].transpose(0, 2, 1, 3)        # [B,S,nh,2]
 
     # output projection O = CL Wo, column checksums O^c = CL^c Wo
-    O = rnd(CL @ Wo)
-    Oc = CLc_full @ Wo
-    run.inject("O", O, lambda b, h, r, c: (b, r, c))
-    if run.on("O"):
-        run.verify(O, Oc, R, lambda k, i, j: ("O", k, 0, i, j),
-                   recompute=lambda k, i, j: CL[k, i] @ Wo[:, j])
+    O, Oc = output_projection(run, CL, CLc_full, Wo, p)
 
     return dict(O=O, QKV=QKV, AS=AS, AP=AP, CL=CL, X=X, Wqkv=Wqkv, Wo=Wo,
                 Xc=Xc, Xr=Xr, QKVc=QKVc, Vr=Vr, APc=APc, APr=APr,

@@ -1,0 +1,156 @@
+"""Pins of the fused-attention oracle (oracle/fused.py) against facts that
+do not come from it: the materialised-attention oracle (itself pinned in
+test_oracle_layer.py) in the fp32 storage mode, closed forms of softmax
+attention, and the restoration of a fault-free run by the row checks."""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import OracleParams, forward
+from oracle.eec import col_checksums, row_checksums
+from oracle.fused import TK, TQ, fused_attention, fused_forward
+from oracle.layer import _Run
+
+
+def _inputs(S=256, H=128, nh=2, seed=3, dtype="bf16"):
+    sh = W.make_shape(1, S, H, nh, dtype=dtype)
+    return W.make_inputs(sh, seed)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("R", [128, 64])
+def test_matches_materialised_attention_in_fp32(causal, R):
+    """With fp32 storage the two forms differ only by where fp32 rounding
+    is applied (AS and AP stored vs P rounded per key tile)."""
+    inp = _inputs(dtype="f32")
+    p = OracleParams(heads=2, dtype="f32", causal=causal, block_rows=R)
+    a = forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    scale = np.abs(a["CL"]).max()
+    assert np.abs(a["CL"] - f["CL"]).max() <= 1e-6 * scale
+    assert np.abs(a["O"] - f["O"]).max() <= 1e-6 * np.abs(a["O"]).max()
+    assert a["events"] == [] and f["events"] == []
+    # CL^c is encoded from CL, so it equals the column sums of the result
+    assert np.allclose(f["CLc"], col_checksums(f["CL"], R), rtol=0, atol=0)
+
+
+def _direct(Q, K, V, causal, R=128, faults=(), root_check=True, dtype="f64"):
+    """fused_attention on hand-made Q, K, V of one head ([S, d] each), with
+    the checksums the projection would propagate computed from them."""
+    S, d = Q.shape
+    p = OracleParams(heads=1, dtype=dtype, causal=causal, block_rows=R, root_check=root_check)
+    run = _Run(p, faults)
+    nq = S // R
+    Kc = col_checksums(K, R)                                   # [nq, 2, d]
+    Vr = row_checksums(V, d)                                   # [S, 1, 2]
+    pr = dict(B=1, S=S, H=d, nh=1, d=d, R=R, nq=nq, scale=1.0 / np.sqrt(d),
+              Qh=Q[None, None], Kh=K[None, None], Vh=V[None, None],
+              Kch=Kc[None, None], Vr=Vr[None])
+    CL, CLc = fused_attention(run, pr, p)
+    return CL, run.events
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_zero_queries_give_the_mean_of_the_allowed_values(causal):
+    """Q = 0 makes every score equal: each query averages V over the keys
+    it may see (all keys, or keys 0..i under the causal mask)."""
+    rng = np.random.default_rng(0)
+    S, d = 256, 64
+    V = rng.standard_normal((S, d))
+    CL, ev = _direct(np.zeros((S, d)), rng.standard_normal((S, d)), V, causal)
+    want = np.cumsum(V, axis=0) / np.arange(1, S + 1)[:, None] if causal else \
+        np.broadcast_to(V.mean(axis=0), (S, d))
+    assert np.allclose(CL, want, rtol=1e-12, atol=1e-12)
+    assert ev == []
+
+
+def test_constant_values_pass_through_and_one_hot_scores_select():
+    """Rows of softmax sum to one (V constant -> CL constant), and a query
+    whose score with one key dominates every other by far returns that key's
+    value row."""
+    rng = np.random.default_rng(1)
+    S, d = 128, 64
+    Q, K = rng.standard_normal((S, d)), rng.standard_normal((S, d))
+    CL, _ = _direct(Q, K, np.full((S, d), 2.5), False)
+    assert np.allclose(CL, 2.5, rtol=1e-13)
+    K2 = np.zeros((S, d))
+    K2[37, 0] = 1.0
+    Q2 = np.zeros((S, d))
+    Q2[:, 0] = 8.0 * 60.0       # scale 1/8: key 37 scores 60 above the others
+    V = rng.standard_normal((S, d))
+    CL2, _ = _direct(Q2, K2, V, False)
+    assert np.allclose(CL2, np.broadcast_to(V[37], (S, d)), rtol=1e-20, atol=1e-20 + 1e-24)
+
+
+def _fault_case(kind):
+    return {"INF": np.inf, "NaN": np.nan, "near": 3e10, "numeric": 55.0}[kind]
+
+
+@pytest.mark.parametrize("kind", ["INF", "NaN", "near", "numeric", "flip"])
+@pytest.mark.parametrize("causal", [False, True])
+def test_score_fault_is_recomputed_and_the_run_restored(kind, causal):
+    inp = _inputs()
+    p = OracleParams(heads=2, dtype="bf16", causal=causal, block_rows=64)
+    f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    # a masked position of a diagonal tile under the mask, else a plain one
+    r, c = (150, 170) if causal else (150, 20)
+    fault = W.Fault("AS", 0, 1, r, c, 0.0, mode="flip") if kind == "flip" else \
+        W.Fault("AS", 0, 1, r, c, _fault_case(kind))
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, [fault])
+    assert [(e[0], e[1], e[2], e[3], e[4], e[6]) for e in f["events"]] == \
+        [("AS", 0, 1, r, c, "RECOMPUTE")]
+    assert np.array_equal(f["CL"], f0["CL"]) and np.array_equal(f["O"], f0["O"])
+
+
+def test_key_fault_without_root_check_is_corrected_along_its_column():
+    """Root check off: a K error corrupts one score column in every query
+    that sees the key (1C); each row vector locates it and fixes it from
+    the checksums (K^c came from the clean projection)."""
+    inp = _inputs()
+    p = OracleParams(heads=2, dtype="bf16", causal=False, block_rows=128, root_check=False)
+    f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, [W.Fault("K", 0, 0, 77, 5, 1e6)])
+    ev = [e for e in f["events"] if e[0] == "AS"]
+    assert len(ev) == 256 and {e[4] for e in ev} == {77} and {e[3] for e in ev} == set(range(256))
+    assert all(e[6] in ("DELTA", "RECONSTRUCT") for e in ev)
+    err = np.abs(f["CL"] - f0["CL"]).max()
+    assert err <= 2.0 ** -6 * np.abs(f0["CL"]).max()
+
+
+def test_query_fault_needs_the_root_check():
+    """A Q error corrupts a whole score row (1R) together with that row's
+    propagated checksums AS^r = Q (K^c)^T, so the row checks cannot see it:
+    with the root check off it reaches CL unnoticed; with the root check on
+    it is corrected at the projection and the run equals the fault-free
+    one."""
+    inp = _inputs()
+    fault = [W.Fault("Q", 0, 1, 200, 3, 1e8)]
+    p_off = OracleParams(heads=2, dtype="bf16", causal=True, block_rows=128, root_check=False)
+    f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p_off)
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p_off, fault)
+    assert [e for e in f["events"] if e[0] == "AS"] == []
+    assert not np.array_equal(f["CL"][0, 200, 64:], f0["CL"][0, 200, 64:])
+    p_on = OracleParams(heads=2, dtype="bf16", causal=True, block_rows=128)
+    g = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p_on, fault)
+    assert [(e[0], e[3], e[4], e[6]) for e in g["events"]] == [("Q", 200, 3, "RECOMPUTE")]
+    assert np.array_equal(g["CL"], f0["CL"])
+
+
+@pytest.mark.parametrize("val,action", [(np.inf, "RECONSTRUCT"), (np.nan, "RECONSTRUCT"),
+                                        (1e12, "RECONSTRUCT"), (40.0, "DELTA")])
+def test_context_fault_is_fixed_from_the_row_checksum(val, action):
+    inp = _inputs()
+    p = OracleParams(heads=2, dtype="bf16", causal=True, block_rows=128)
+    f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, [W.Fault("CL", 0, 0, 99, 17, val)])
+    assert [(e[0], e[3], e[4], e[6]) for e in f["events"]] == [("CL", 99, 17, action)]
+    # the fixed element is within bf16 rounding of its row's magnitude
+    row = f0["CL"][0, 99, :64]
+    assert abs(f["CL"][0, 99, 17] - f0["CL"][0, 99, 17]) <= 2.0 ** -7 * np.abs(row).sum()
+
+
+def test_tiles_cover_the_sequence():
+    assert TQ == TK == 128
+    with pytest.raises(ValueError):
+        fused_forward(*(_inputs(S=192)[k] for k in ("X", "Wqkv", "Wo")),
+                      OracleParams(heads=2, block_rows=64))
