@@ -64,6 +64,20 @@ extern "C" {
 #define ABFT_FLAG_REPORT_APPEND 2u  /* keep the report's contents at entry        */
 #define ABFT_FLAG_UNPROTECTED   4u  /* no checksums and no verification: the same
                                        kernels without ABFT (overhead baseline)  */
+#define ABFT_FLAG_FUSED         8u  /* forward: score, softmax and context in one
+                                       kernel that stores neither AS nor AP (an
+                                       extension of Sec. 4.4: AS checked on its
+                                       row side per R-key block against
+                                       Q (K^c)^T, CL against the V^r row
+                                       checksum carried through the online
+                                       softmax; CL^c encoded from the verified
+                                       CL). Needs bf16 storage and seq a
+                                       multiple of 128 (else
+                                       ABFT_ERR_UNSUPPORTED); the stage bits
+                                       SCORE, SOFTMAX and CONTEXT each select
+                                       that kernel. A backward after a fused
+                                       forward returns ABFT_ERR_UNSUPPORTED
+                                       (AP is not saved).                       */
 
 /* ---- op tags of protected GEMM outputs (paper Table 1 + backward) ----- */
 enum abft_op {

@@ -71,8 +71,9 @@ def _check_rows(v2, c1, c2, e_rel, tn, recompute, tc, store=lambda x: x):
     return events, unc
 
 
-def fused_attention(run: _Run, pr: dict, p: OracleParams):
-    """Steps 1-5 for every (batch, head). Returns CL [B,S,H] and CL^c
+def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None):
+    """Steps 1-5 for every (batch, head), or for the (batch, head) pairs in
+    `only` (the others' CL stays zero). Returns CL [B,S,H] and CL^c
     [B,nq,2,H]; events go to run.events."""
     B, S, H, nh, d, R, nq, scale = (pr[k] for k in ("B", "S", "H", "nh", "d", "R", "nq", "scale"))
     Qh, Kh, Vh, Kch, Vr = pr["Qh"], pr["Kh"], pr["Vh"], pr["Kch"], pr["Vr"]
@@ -88,6 +89,8 @@ def fused_attention(run: _Run, pr: dict, p: OracleParams):
     CLh = np.zeros((B, nh, S, d))
     for b in range(B):
         for h in range(nh):
+            if only is not None and (b, h) not in only:
+                continue
             Q, K, V = Qh[b, h], Kh[b, h], Vh[b, h]
             Kc = Kch[b, h]                      # [nq, 2, d]
             vr = Vr[b, :, h, :]                 # [S, 2]

@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libattn_abft.so")
-SOURCES = ["gemm_abft.hip", "softmax_abft.hip", "encode_verify.hip", "attn_abft.hip",
+SOURCES = ["gemm_abft.hip", "softmax_abft.hip", "encode_verify.hip", "fused_attn.hip", "attn_abft.hip",
            "adaptive.cpp"]
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"

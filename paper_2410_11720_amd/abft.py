@@ -25,7 +25,7 @@ ACTIONS = ("RECOMPUTE", "DELTA", "RECONSTRUCT", "UNCORRECTABLE")
 ABFT_OK = 0
 BF16, FP32 = 0, 1
 SEC_AS, SEC_CL, SEC_O, SEC_BWD, SEC_ALL = 1, 2, 4, 8, 15
-FLAG_ROOT_CHECK, FLAG_REPORT_APPEND, FLAG_UNPROTECTED = 1, 2, 4
+FLAG_ROOT_CHECK, FLAG_REPORT_APPEND, FLAG_UNPROTECTED, FLAG_FUSED = 1, 2, 4, 8
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
@@ -145,11 +145,13 @@ class LayerConfig:
     sections: int = SEC_ALL
     root_check: bool = True
     protect: bool = True
+    fused: bool = False          # forward attention core in one kernel (no AS/AP)
 
     def to_c(self, append=False) -> Config:
         flags = (FLAG_ROOT_CHECK if self.root_check else 0)
         flags |= (FLAG_REPORT_APPEND if append else 0)
         flags |= (0 if self.protect else FLAG_UNPROTECTED)
+        flags |= (FLAG_FUSED if self.fused else 0)
         return Config(self.batch, self.seq, self.hidden, self.heads,
                       FP32 if self.dtype == "f32" else BF16, int(self.causal), self.block_rows,
                       self.scale, self.t_near_inf, self.t_correct, self.e_rel, self.sections,

@@ -112,6 +112,26 @@ struct SoftmaxDesc {
 hipError_t launch_softmax_fwd(const SoftmaxDesc& d, int dtype, hipStream_t stream);
 hipError_t launch_softmax_bwd(const SoftmaxDesc& d, int dtype, hipStream_t stream);
 
+// Fused attention forward (score, softmax and context in one kernel, no
+// AS or AP in memory): bf16 storage, S a multiple of 128, head_dim 64 or
+// 128, R dividing 128.
+struct FusedDesc {
+  int B = 0, nh = 0, S = 0, H = 0, D = 0, R = 128;
+  int causal = 0;
+  float scale = 1.f;
+  const void* qkv = nullptr;   // [B*S][3H] bf16: Q | K | V column blocks
+  const float* qkvc = nullptr; // [B][S/R][2][3H] propagated column checksums (K^c used)
+  const float* vr = nullptr;   // [B*S][nh][2] propagated V^r (row checksums per head)
+  void* cl = nullptr;          // [B*S][H] bf16 output
+  int check_as = 0, check_cl = 0;
+  int recompute = 1;           // located score errors: recompute (else checksum fix)
+  float e_rel = 0.f, tn_s = 0.f, tn_cl = 0.f, tc = 0.f;  // thresholds as compared
+  const abft_fault* faults = nullptr;
+  int n_faults = 0;
+  abft_report* report = nullptr;
+};
+hipError_t launch_fused_fwd(const FusedDesc& d, hipStream_t stream);
+
 // Checksum encoder (public encode_checksums) and standalone verifier.
 hipError_t launch_encode(const void* A, int dtype, int64_t batch, int64_t rows, int64_t cols,
                          int64_t ld, int64_t batch_stride, int Rb, int Cb, float* col_chk,

@@ -130,6 +130,8 @@ int validate(const attn_abft_config* c, Dims* d) {
   if (d->d != 64 && d->d != 128) return ABFT_ERR_UNSUPPORTED;
   if (d->S % 8 || d->H % 8) return ABFT_ERR_UNSUPPORTED;
   if (d->S > 4096) return ABFT_ERR_UNSUPPORTED;  // softmax keeps a row in registers
+  if ((c->flags & ABFT_FLAG_FUSED) && (c->dtype != ABFT_BF16 || d->S % 128))
+    return ABFT_ERR_UNSUPPORTED;
   if (!(c->t_near_inf >= 0.f) || !(c->t_correct >= 0.f) || !(c->e_rel >= 0.f))
     return ABFT_ERR_INVALID;
   return ABFT_OK;
@@ -329,8 +331,31 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
     g.map.head_cols = int(hd);
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(), s));
   }
+  const bool fused = (cfg->flags & ABFT_FLAG_FUSED) != 0;
+  if (fused && (stages & (ABFT_STAGE_SCORE | ABFT_STAGE_SOFTMAX | ABFT_STAGE_CONTEXT))) {
+    // score, softmax and context in one kernel (no AS or AP in memory)
+    FusedDesc fd;
+    fd.B = int(B); fd.nh = int(nh); fd.S = int(S); fd.H = int(H); fd.D = int(hd); fd.R = int(R);
+    fd.causal = cfg->causal;
+    fd.scale = p.scale;
+    fd.qkv = ws + L.qkv;
+    fd.qkvc = p.sec_as ? F(L.qkvc) : nullptr;
+    fd.vr = p.sec_cl ? F(L.vr) : nullptr;
+    fd.cl = ws + L.cl;
+    fd.check_as = p.sec_as;
+    fd.check_cl = p.sec_cl;
+    fd.recompute = p.root;
+    fd.e_rel = p.e_rel;
+    fd.tn_s = stored_threshold(cfg->t_near_inf > 0.f ? cfg->t_near_inf : 1e10f, ABFT_FP32);
+    fd.tn_cl = p.tn;
+    fd.tc = p.tc;
+    fd.faults = faults; fd.n_faults = n_faults; fd.report = report;
+    CK(launch_fused_fwd(fd, s));
+    if (p.sec_o)  // CL^c for O^c = CL^c Wo, encoded from the verified CL
+      CK(launch_encode(ws + L.cl, dt, B, S, H, H, S * H, int(R), int(hd), F(L.clc), nullptr, s));
+  }
   // AS = Q K^T per head (unscaled, before the mask), two-sided checksums
-  if (stages & ABFT_STAGE_SCORE) {
+  if (!fused && (stages & ABFT_STAGE_SCORE)) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(S); g.K = int(hd);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -347,7 +372,7 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, Tile::T128x128S1, s));
   }
   // AP = softmax(scale * AS) with column (and row) checksums
-  if (stages & ABFT_STAGE_SOFTMAX) {
+  if (!fused && (stages & ABFT_STAGE_SOFTMAX)) {
     SoftmaxDesc sd;
     sd.B = int(B); sd.nh = int(nh); sd.S = int(S); sd.R = int(R); sd.causal = cfg->causal;
     sd.kv_align = 128;
@@ -358,7 +383,7 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
     CK(launch_softmax_fwd(sd, dt, s));
   }
   // CL = AP V per head, CL^c = AP^c V, CL^r = AP V^r
-  if (stages & ABFT_STAGE_CONTEXT) {
+  if (!fused && (stages & ABFT_STAGE_CONTEXT)) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(hd); g.K = int(S);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -407,6 +432,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   if (!dO || !X || !Wqkv || !Wo || !workspace || !dX || !dWqkv || !dWo || !report ||
       n_faults < 0 || (n_faults > 0 && !faults))
     return ABFT_ERR_INVALID;
+  if (cfg->flags & ABFT_FLAG_FUSED) return ABFT_ERR_UNSUPPORTED;  // AP was not saved
   const Layout_ L = make_layout(d);
   if (workspace_bytes < L.total) return ABFT_ERR_WORKSPACE;
   if ((st = check_device()) != ABFT_OK) return st;

@@ -1,0 +1,156 @@
+"""Parity of the fused attention forward (ABFT_FLAG_FUSED, through the C
+ABI) with the fused-attention oracle on the same seeded inputs.
+
+Bar: detection events identical as multisets (the key-fault case compares
+the corrected positions and classes; its DELTA / RECONSTRUCT choice sits on
+the T_correct boundary for some rows and may differ); O and CL within
+|gpu - oracle| <= 1e-2 * max(|oracle|, rms(oracle)) (bf16 storage; P is
+rounded to bf16 on both sides, from exponentials taken in fp32 here and
+fp64 there).
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import OracleParams
+from oracle.fused import fused_attention, fused_forward
+from oracle.layer import _Run, project
+
+pytestmark = pytest.mark.gpu
+RTOL = 1e-2
+
+
+def _abft():
+    from paper_2410_11720_amd import abft
+    return abft
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda").to(torch.bfloat16)
+
+
+def host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def assert_close(gpu, ref, name):
+    nf = ~np.isfinite(ref)
+    assert not nf.any() and np.isfinite(gpu).all(), name
+    scale = np.maximum(np.abs(ref), np.sqrt(np.mean(ref ** 2)) + 1e-300)
+    rel = np.abs(gpu - ref) / scale
+    assert rel.max() <= RTOL, f"{name}: max rel err {rel.max():.3g}"
+
+
+def run_fused(shape, faults=(), root_check=True, seed=1):
+    abft = _abft()
+    print(f"[case] fused {shape.name} causal={shape.causal} R={shape.block_rows} "
+          f"faults={len(faults)} root={root_check}", flush=True)
+    inp = W.make_inputs(shape, seed)
+    cfg = abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads,
+                           causal=shape.causal, block_rows=shape.block_rows,
+                           root_check=root_check, fused=True)
+    layer = abft.ProtectedAttention(cfg)
+    X, Wqkv, Wo = (dev(inp[k]) for k in ("X", "Wqkv", "Wo"))
+    O = layer.forward(X, Wqkv, Wo, abft.faults_to_device(list(faults)))
+    torch.cuda.synchronize()
+    g = dict(O=host(O), CL=host(layer.tensor("CL")), rep=abft.read_report(layer.report))
+    p = OracleParams(heads=shape.heads, causal=shape.causal, block_rows=shape.block_rows,
+                     root_check=root_check)
+    o = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, list(faults))
+    return g, o
+
+
+SHAPES = [W.make_shape(1, 256, 128, 2, causal=c, block_rows=r, name=f"d64c{int(c)}r{r}")
+          for c in (False, True) for r in (128, 32)] + \
+         [W.make_shape(1, 256, 256, 2, causal=c, block_rows=64, name=f"d128c{int(c)}")
+          for c in (False, True)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
+def test_fused_fault_free(shape):
+    g, o = run_fused(shape)
+    assert g["rep"]["events"] == [] and o["events"] == []
+    assert_close(g["CL"], o["CL"], "CL")
+    assert_close(g["O"], o["O"], "O")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_fused_score_faults(causal):
+    shape = W.make_shape(2, 256, 128, 2, causal=causal, block_rows=64, name="faults")
+    faults = [W.Fault("AS", 0, 0, 5, 3, np.inf), W.Fault("AS", 0, 1, 130, 129, np.nan),
+              W.Fault("AS", 1, 0, 200, 70, 3e10), W.Fault("AS", 1, 1, 255, 250, 55.0),
+              W.Fault("AS", 0, 1, 77, 12, 0.0, mode="flip"),
+              # past the diagonal of a diagonal tile (masked under the causal mask)
+              W.Fault("AS", 1, 0, 140, 180, np.inf)]
+    g, o = run_fused(shape, faults)
+    assert g["rep"]["overflow"] == 0
+    assert sorted(g["rep"]["events"]) == sorted(o["events"])
+    assert len(o["events"]) == 6
+    assert_close(g["CL"], o["CL"], "CL")
+    assert_close(g["O"], o["O"], "O")
+
+
+def test_fused_context_faults():
+    shape = W.make_shape(1, 256, 128, 2, causal=True, block_rows=128, name="clfaults")
+    faults = [W.Fault("CL", 0, 0, 99, 17, np.inf), W.Fault("CL", 0, 1, 3, 63, np.nan),
+              W.Fault("CL", 0, 0, 250, 0, 1e12), W.Fault("CL", 0, 1, 128, 40, 40.0),
+              W.Fault("CL", 0, 0, 17, 5, 0.0, mode="flip")]
+    g, o = run_fused(shape, faults)
+    assert sorted(g["rep"]["events"]) == sorted(o["events"])
+    assert len(o["events"]) == 5
+    assert_close(g["CL"], o["CL"], "CL")
+    assert_close(g["O"], o["O"], "O")
+
+
+def test_fused_key_fault_without_root_check():
+    shape = W.make_shape(1, 256, 128, 2, causal=False, block_rows=128, name="kfault")
+    faults = [W.Fault("K", 0, 0, 77, 5, 1e6)]
+    g, o = run_fused(shape, faults, root_check=False)
+    key = lambda e: e[:6]
+    assert sorted(map(key, g["rep"]["events"])) == sorted(map(key, o["events"]))
+    assert len([e for e in o["events"] if e[0] == "AS"]) == 256
+    assert all(e[6] in ("DELTA", "RECONSTRUCT") for e in g["rep"]["events"] if e[0] == "AS")
+    assert_close(g["CL"], o["CL"], "CL")
+
+
+def test_fused_gpt2_shape_sampled_heads():
+    """The benchmark shape (B8 S1024 H768, 12 heads of 64, causal, R 128):
+    no events on the GPU, and two sampled heads equal the oracle's."""
+    abft = _abft()
+    shape = W.CONFIGS["c3"]
+    inp = W.make_inputs(shape, W.data_seed("c3"))
+    cfg = abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads, causal=True,
+                           block_rows=shape.block_rows, fused=True)
+    layer = abft.ProtectedAttention(cfg)
+    print("[case] fused c3", flush=True)
+    X, Wqkv, Wo = (dev(inp[k]) for k in ("X", "Wqkv", "Wo"))
+    layer.forward(X, Wqkv, Wo)
+    torch.cuda.synchronize()
+    rep = abft.read_report(layer.report)
+    assert rep["events"] == [] and rep["n_uncorrectable"] == 0
+    CL = host(layer.tensor("CL"))
+    p = OracleParams(heads=shape.heads, causal=True, block_rows=shape.block_rows)
+    run = _Run(p, ())
+    pr = project(run, inp["X"], inp["Wqkv"], p)
+    only = {(0, 0), (7, 11)}
+    CLo, _ = fused_attention(run, pr, p, only=only)
+    d = shape.hidden // shape.heads
+    for (b, h) in only:
+        assert_close(CL[b, :, h * d:(h + 1) * d], CLo[b, :, h * d:(h + 1) * d], f"CL[{b},{h}]")
+    assert run.events == []
+
+
+def test_fused_rejects_unsupported_shapes_and_backward():
+    abft = _abft()
+    with pytest.raises(abft.AbftError):
+        abft.ProtectedAttention(abft.LayerConfig(1, 192, 128, 2, block_rows=64, fused=True))
+    with pytest.raises(abft.AbftError):
+        abft.ProtectedAttention(abft.LayerConfig(1, 256, 128, 2, dtype="f32", fused=True))
+    shape = W.make_shape(1, 256, 128, 2, name="bwd")
+    inp = W.make_inputs(shape, 1)
+    layer = abft.ProtectedAttention(abft.LayerConfig(1, 256, 128, 2, fused=True))
+    X, Wqkv, Wo, dO = (dev(inp[k]) for k in ("X", "Wqkv", "Wo", "dO"))
+    layer.forward(X, Wqkv, Wo)
+    with pytest.raises(abft.AbftError):
+        layer.backward(dO, X, Wqkv, Wo)
