@@ -39,7 +39,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 COPY_BYTES = 256 << 20      # reference copy for the counter scale factor
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "qkv_gemm_gpt2_causal_B8_S1024_traffic.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic_gpt2_causal_B8_S1024.md")
 
 
 def useful_flops(B, S, H, nh, causal, backward=True):
@@ -75,14 +75,15 @@ def stage_table(B, S, H, nh, causal, es=2):
     return [
         ("encode", False, 0x001, "byte", (T * H + 3 * H * H) * es + (B * S // 128 * 2 * H + 4 * T * nh) * 4),
         ("qkv", False, 0x002, "flop", 2 * T * H * 3 * H),
-        ("score", False, 0x004, "flop", 2 * sq * d),
+        # K = head_dim: the score-shaped output is the traffic
+        ("score", False, 0x004, "byte", sq * es + 2 * T * H * es),
         ("softmax", False, 0x008, "byte", 2 * sq * es),
         ("context", False, 0x010, "flop", 2 * sq * d),
         ("out", False, 0x020, "flop", 2 * T * H * H),
         ("encode_dO", True, 0x001, "byte", T * H * es),
         ("dCL", True, 0x002, "flop", 2 * T * H * H),
         ("dWo", True, 0x004, "flop", 2 * T * H * H),
-        ("dAP", True, 0x008, "flop", 2 * sq * d),
+        ("dAP", True, 0x008, "byte", sq * es + 2 * T * H * es),
         ("dV", True, 0x010, "flop", 2 * sq * d),
         ("softmax_bwd", True, 0x020, "byte", 3 * sq * es),
         ("dQ", True, 0x040, "flop", 2 * sq * d),
@@ -92,32 +93,36 @@ def stage_table(B, S, H, nh, causal, es=2):
     ]
 
 
+# the sources a GEMM kernel is built from: counters taken on other
+# versions of them are stale
+GEMM_SOURCES = ("paper_2410_11720_amd/csrc/gemm_abft.hip", "paper_2410_11720_amd/csrc/direct_lds.hpp",
+                "paper_2410_11720_amd/csrc/abft_device.hpp", "paper_2410_11720_amd/csrc/abft_internal.hpp",
+                "include/attn_abft.h")
+
+
 def kernel_source_hash():
-    """Hash of every HIP source of the library: traffic counters taken on
-    other sources are stale."""
+    """Hash of the sources the GEMM kernels are built from."""
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2410_11720_amd", "csrc", "*"))):
-        with open(f, "rb") as fh:
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(os.path.basename(f).encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
 
 
 def stored_traffic(kernel):
-    """HBM traffic per launch of `kernel` from the committed counter summary,
-    or None when absent or taken on different kernel sources."""
+    """HBM traffic per launch of `kernel` (symbol, grid) from the committed
+    counter summary, or None when absent or taken on different sources."""
     try:
         with open(TRAFFIC_FILE) as fh:
             text = fh.read()
     except OSError:
         return None
-    m = re.search(r"^traffic_json: (\{.*\})$", text, re.M)
-    if not m:
-        return None
-    rec = json.loads(m.group(1))
-    if (rec.get("source_hash") != kernel_source_hash() or rec.get("kernel") != kernel[0]
-            or rec.get("grid") != kernel[1]):
-        return None
-    return rec
+    for m in re.finditer(r"^traffic_json: (\{.*\})$", text, re.M):
+        rec = json.loads(m.group(1))
+        if (rec.get("source_hash") == kernel_source_hash() and rec.get("kernel") == kernel[0]
+                and rec.get("grid") == kernel[1]):
+            return rec
+    return None
 
 
 def cpu_baseline(shape, seed, batch=None):
@@ -200,14 +205,16 @@ class Layer:
 
 def pmc_workload(key, reps):
     """Launches for the traffic counters: the checksum encode the QKV
-    projection reads, `reps` launches of the QKV projection (the only
-    launches of its kernel here), then `reps` plain copies of COPY_BYTES
-    (reads and writes COPY_BYTES each)."""
+    projection reads, `reps` launches of the QKV projection, `reps` of the
+    score GEMM (the only launches of their kernels here), then `reps` plain
+    copies of COPY_BYTES (reads and writes COPY_BYTES each)."""
     L = Layer(key)
     torch = L.torch
     L.run_stage(0x001, False)       # encode X^c, W^V r
     for _ in range(reps):
         L.run_stage(0x002, False)   # QKV projection
+    for _ in range(reps):
+        L.run_stage(0x004, False)   # score GEMM
     src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda").normal_()
     dst = torch.empty_like(src)
     for _ in range(reps):
@@ -259,10 +266,11 @@ def summarize(dirs):
         print(f"{short_name(k[0])} | grid={k[1]} | {vals}")
 
 
-def traffic_from(fetch_dir, write_dir, kernel=KERNEL_OF_STAGE["qkv"]):
-    """HBM bytes per launch of `kernel` (symbol, grid) from a FETCH_SIZE
-    and a WRITE_SIZE run of --pmc-workload, each counter scaled by what it
-    reads for the reference copy (COPY_BYTES in, COPY_BYTES out)."""
+def traffic_from(fetch_dir, write_dir, stages=("qkv", "score")):
+    """HBM bytes per launch of the stages' kernels (symbol, grid) from a
+    FETCH_SIZE and a WRITE_SIZE run of --pmc-workload, each counter scaled
+    by what it reads for the reference copy (COPY_BYTES in, COPY_BYTES
+    out). One traffic_json line per kernel."""
     f, w = collect([fetch_dir]), collect([write_dir])
 
     def pick(d, pred):
@@ -271,27 +279,96 @@ def traffic_from(fetch_dir, write_dir, kernel=KERNEL_OF_STAGE["qkv"]):
             raise SystemExit(f"expected one matching kernel, found {ks}")
         return d[ks[0]]
 
-    sym, grid = kernel
-    # databases without grid sizes report grid 0; the workload launches the
-    # symbol only for this kernel
-    kf = pick(f, lambda n, gr: n == sym and gr in (grid, 0))
-    kw = pick(w, lambda n, gr: n == sym and gr in (grid, 0))
     cf, cw = pick(f, lambda n, gr: "MulFunctor" in n), pick(w, lambda n, gr: "MulFunctor" in n)
     s_fetch = COPY_BYTES / (cf["FETCH_SIZE"] * 1024.0)
     s_write = COPY_BYTES / (cw["WRITE_SIZE"] * 1024.0)
-    fetch = kf["FETCH_SIZE"] * 1024.0 * s_fetch
-    write = kw["WRITE_SIZE"] * 1024.0 * s_write
-    rec = {"kernel": sym, "grid": grid, "source_hash": kernel_source_hash(),
-           "fetch_kib": round(kf["FETCH_SIZE"], 1), "write_kib": round(kw["WRITE_SIZE"], 1),
-           "copy_fetch_kib": round(cf["FETCH_SIZE"], 1), "copy_write_kib": round(cw["WRITE_SIZE"], 1),
-           "scale_fetch": round(s_fetch, 4), "scale_write": round(s_write, 4),
-           "fetch_bytes": int(fetch), "write_bytes": int(write),
-           "bytes_per_launch": int(fetch + write)}
-    print("traffic_json: " + json.dumps(rec))
+    for st in stages:
+        sym, grid = KERNEL_OF_STAGE[st]
+        # databases without grid sizes report grid 0; the workload launches
+        # each symbol only for its stage
+        kf = pick(f, lambda n, gr: n == sym and gr in (grid, 0))
+        kw = pick(w, lambda n, gr: n == sym and gr in (grid, 0))
+        fetch = kf["FETCH_SIZE"] * 1024.0 * s_fetch
+        write = kw["WRITE_SIZE"] * 1024.0 * s_write
+        rec = {"kernel": sym, "grid": grid, "source_hash": kernel_source_hash(),
+               "fetch_kib": round(kf["FETCH_SIZE"], 1), "write_kib": round(kw["WRITE_SIZE"], 1),
+               "copy_fetch_kib": round(cf["FETCH_SIZE"], 1),
+               "copy_write_kib": round(cw["WRITE_SIZE"], 1),
+               "scale_fetch": round(s_fetch, 4), "scale_write": round(s_write, 4),
+               "fetch_bytes": int(fetch), "write_bytes": int(write),
+               "bytes_per_launch": int(fetch + write)}
+        print("traffic_json: " + json.dumps(rec))
 
 
 FAIL_TARGET = 1e-11   # one failure per 1e11 executions of the layer (Sec. 5)
 SECTION_NAMES = ("AS", "CL", "O", "BWD")
+
+
+def fused_forward(L, steps):
+    """The fused attention forward (ABFT_FLAG_FUSED: score, softmax and
+    context in one kernel) against the materialised forward, protected and
+    unprotected: whole-forward times and the fused kernel alone, with one
+    score fault to show it is corrected."""
+    torch, abft, W = L.torch, L.abft, L.W
+    shape = L.shape
+    B, S, H, nh = shape.batch, shape.seq, shape.hidden, shape.heads
+    d = H // nh
+    lays = {}
+    for prot in (True, False):
+        cfg = abft.LayerConfig(B, S, H, nh, dtype=shape.dtype, causal=shape.causal,
+                               block_rows=shape.block_rows, protect=prot, fused=True)
+        lays[prot] = (cfg, abft.ProtectedAttention(cfg, "cuda"))
+
+    def per_forward(lay, n):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        lay.forward(L.X, L.Wqkv, L.Wo, O=L.O)
+        torch.cuda.synchronize()
+        ev[0].record(L.stream)
+        for i in range(n):
+            lay.forward(L.X, L.Wqkv, L.Wo, O=L.O)
+            ev[i + 1].record(L.stream)
+        torch.cuda.synchronize()
+        return float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(n)]))
+
+    def core_us(cfg, lay, n):
+        run = lambda: abft.attn_abft_forward_stages(cfg, L.X, L.Wqkv, L.Wo, L.O, lay.workspace,
+                                                    None, 0, lay.report, 0x4, L.stream,
+                                                    append=True)
+        run()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(L.stream)
+        for _ in range(n):
+            run()
+        e1.record(L.stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    ms_fp, ms_fu = per_forward(lays[True][1], steps), per_forward(lays[False][1], steps)
+    ms_mp, ms_mu = per_forward(L.lay_p, steps), per_forward(L.lay_u, steps)
+    us_p = core_us(*lays[True], steps)
+    us_u = core_us(*lays[False], steps)
+    P = S * (S + 1) // 2 if shape.causal else S * S
+    core_flops = 4.0 * B * nh * d * P          # Q K^T and P V over the unmasked pairs
+    tf = core_flops / (us_p * 1e-6) / 1e12
+    fl = W.draw_faults(shape, W.fault_seed(L.key, 20_000), 1, ["AS"], ["inf"])
+    cfg_p, lay_p = lays[True]
+    lay_p.forward(L.X, L.Wqkv, L.Wo, abft.faults_to_device(fl, "cuda"), O=L.O)
+    torch.cuda.synchronize()
+    rep = abft.read_report(lay_p.report)
+    return {
+        "ms_forward_protected": round(ms_fp, 4), "ms_forward_unprotected": round(ms_fu, 4),
+        "abft_overhead_pct": round((ms_fp - ms_fu) / ms_fu * 100, 2),
+        "ms_forward_materialised_protected": round(ms_mp, 4),
+        "ms_forward_materialised_unprotected": round(ms_mu, 4),
+        "speedup_vs_materialised_protected": round(ms_mp / ms_fp, 3),
+        "kernel": "fused_attn_kernel<%d, true>" % d,
+        "kernel_us_protected": round(us_p, 2), "kernel_us_unprotected": round(us_u, 2),
+        "kernel_tflops_protected": round(tf, 2),
+        "kernel_frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+        "kernel_flops": core_flops,
+        "one_score_fault": {"corrected": rep["n_corrected"],
+                            "uncorrectable": rep["n_uncorrectable"]},
+    }
 
 
 def adaptive_frequencies(L, timed, per_unprot, steps):
@@ -498,6 +575,7 @@ def main():
     L.step(L.lay_p, (None, 0))
     torch.cuda.synchronize()
 
+    fused = fused_forward(L, args.stage_reps) if shape.dtype == "bf16" and S % 128 == 0 else None
     adaptive = adaptive_frequencies(L, timed, per_unprot, args.adaptive_steps)
     recovery = recovery_costs(L, timed, per_clean, args.adaptive_steps)
 
@@ -555,6 +633,7 @@ def main():
         "stages_us": {s[0]: round(s[3], 2) for s in stages},
         "adaptive_frequencies": adaptive,
         "recovery": recovery,
+        "fused_forward": fused,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, W.data_seed(key))
