@@ -336,15 +336,25 @@ __device__ __forceinline__ TileIdx tile_of(const GemmDesc& g) {
   return t;
 }
 
-template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE>
+// WLC: wave-local column check. The four waves split the tile's columns
+// (each holds all BM rows of BN / 4 columns), so every column checksum
+// block lies inside one wave: the wave sums, decides and stores its part
+// without a workgroup barrier (outputs checked on the column side only).
+// Otherwise the waves form a 2 x 2 grid.
+template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE,
+          bool WLC = false>
 struct Gemm {
   static constexpr int BK = Mfma<T>::BK;
   static constexpr int KI = Mfma<T>::KI;
   static constexpr int LDK = BK + Mfma<T>::PAD;
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int WGN = WLC ? 4 : 2, WGM = 4 / WGN;  // wave grid
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int IM = WM / 16, JN = WN / 16;
-  static constexpr int JS = JN / 2, IS = IM / 2;  // strip blocks per wave
-  static_assert(IM >= 2 && JN >= 2, "tile too small");
+  // strip blocks per wave: column strips of the wave's own columns (WLC)
+  // or split between the two waves sharing them; row strips split between
+  // the waves sharing the rows
+  static constexpr int JS = WLC ? JN : JN / 2, IS = IM / WGN;
+  static_assert(WLC ? (IM >= 4 && JN >= 1) : (IM >= 2 && JN >= 2), "tile too small");
   static constexpr int FRAG = KI / 4;  // operand elements per lane
   // bf16 operands and bf16 output: detection sums on the matrix cores
   static constexpr bool MSUM = PROT && sizeof(T) == 2 && sizeof(TC) == 2;
@@ -402,7 +412,7 @@ struct Gemm {
   template <bool DIR>
   __device__ static __forceinline__ void run(const GemmDesc& g, char* smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
     const TileIdx ti = tile_of<BM, BN>(g);
     const int m0 = ti.mt * BM, n0 = ti.nt * BN;
     const int z = ti.bh, kslice = ti.ks;
@@ -469,7 +479,11 @@ struct Gemm {
       if (PROT) {
         // wave-uniform branches keep every fragment index a compile-time
         // constant (a runtime index would send the arrays to scratch)
-        if (cc) {
+        if (cc && WLC) {
+          const auto sf = Mfma<T>::load(sS + fr * LDK + kk + fk);
+#pragma unroll
+          for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[j], accs[j]);
+        } else if (cc) {
           const auto sf = Mfma<T>::load(sS + fr * LDK + kk + fk);
           if (wm == 0) {
 #pragma unroll
@@ -479,7 +493,15 @@ struct Gemm {
             for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[JS + j], accs[j]);
           }
         }
-        if (cr) {
+        if (cr && WLC) {
+          const auto rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
+#pragma unroll
+          for (int w = 0; w < WGN; ++w)
+            if (wn == w) {
+#pragma unroll
+              for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[IS * w + i], accr[i]);
+            }
+        } else if (cr) {
           const auto rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
           if (wn == 0) {
 #pragma unroll
@@ -690,7 +712,7 @@ struct Gemm {
             tile[(row + r) * LDT + col] = Storage<TC>::store(acc[i][j][r]);
         }
       }
-    if (PROT && cc) {
+    if (PROT && cc && !WLC) {
 #pragma unroll
       for (int j = 0; j < JS; ++j)
 #pragma unroll
@@ -698,7 +720,7 @@ struct Gemm {
           CsL[((lane >> 4) * 4 + r) * BN + wn * WN + (wm * JS + j) * 16 + fr] =
               accs[j][r];
     }
-    if (PROT && cr) {
+    if (PROT && cr && !WLC) {
 #pragma unroll
       for (int i = 0; i < IS; ++i)
 #pragma unroll
@@ -733,6 +755,12 @@ struct Gemm {
             pk[i][j][1] = uint32_t(t[2 * LDT]) | (uint32_t(t[3 * LDT]) << 16);
           }
       }
+    }
+    if constexpr (WLC) {
+      static_assert(MSUM, "the wave-local check is for protected bf16 tiles");
+      epilogue_wlc(g, tile, A, B, C, z, m0, n0, k_lo, k_hi, cc, cr, rc0, qc0, pk, accs, accr,
+                   reinterpret_cast<float*>(smem + TILE_BYTES), tid);
+      return;
     }
     __syncthreads();
 
@@ -966,6 +994,135 @@ struct Gemm {
     }  // epilogue
   }
 
+  // Wave-local column check (WLC): the wave holds every row of its WN
+  // columns, so each column vector lies in the wave. Detection sums come
+  // from ones-operand MFMAs on the packed stored values (the 8 values of
+  // one column a lane holds for blocks i = 2s, 2s + 1 are the 32 rows of
+  // segment s); the propagated checksums of column block b are the strip
+  // rows 4b..4b+3, i.e. lane group b of the strip result (hi/lo c1, c2).
+  // The wave stores its part of the tile at once; a tile with a flagged
+  // vector then takes the workgroup through the correction passes and is
+  // stored again.
+  __device__ static __forceinline__ void epilogue_wlc(
+      const GemmDesc& g, TC* tile, const T* A, const T* B, TC* C, int z, int m0, int n0,
+      int k_lo, int k_hi, bool cc, bool cr, int rc0, int qc0, const uint32_t (&pk)[IM][JN][2],
+      const floatx4 (&accs)[JS], const floatx4 (&accr)[IS], float* region, int tid) {
+    const int lane = tid & 63, wn = tid >> 6;
+    const int fr = lane & 15, g4 = lane >> 4;
+    const int b0 = z / g.nb1, b1 = z % g.nb1;
+    constexpr int SEG = MINB;
+    const int verify = cc ? g.verify : 0;  // <= 1: no row verification here
+    // the wave reads back only what it wrote itself
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    const int lg_rm = cc ? __builtin_ctz(g.Rm) : 0;
+    const bool own_c = cc && g4 < (BM >> lg_rm) && m0 + (g4 << lg_rm) < g.M;
+    bool flag = false;
+    if (verify >= 1) {
+      const bf16x8 ones = __builtin_bit_cast(
+          bf16x8, uint4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+      const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < JN; ++j) {
+        float r1 = 0.f, sa = 0.f;
+#pragma unroll
+        for (int sg = 0; sg < IM / 2; ++sg) {
+          const uint4 u = {pk[2 * sg][j][0], pk[2 * sg][j][1], pk[2 * sg + 1][j][0],
+                           pk[2 * sg + 1][j][1]};
+          const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu,
+                            u.w & 0x7fff7fffu};
+          const floatx4 sm = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, u), zero);
+          const floatx4 mg = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, ua), zero);
+          if (((sg * SEG) >> lg_rm) == g4) {
+            r1 += sm[0];
+            sa += mg[0];
+          }
+        }
+        const int n = n0 + wn * WN + j * 16 + fr;
+        if (own_c && n < g.N && n >= g.verify_n_lo && n < g.verify_n_hi)
+          flag |= flagged(accs[j][0] + accs[j][1] - r1, sa, g.e_rel);
+      }
+    }
+
+    // store this wave's part: 16-byte chunks, WN / 8 lanes per row piece
+    constexpr int V = 16 / sizeof(TC), CPW = WN / V;
+    static_assert((WM * CPW) % 64 == 0, "whole wave passes");
+#pragma unroll
+    for (int q = 0; q < WM * CPW / 64; ++q) {
+      const int c = lane + q * 64;
+      const int row = c / CPW, col = wn * WN + (c % CPW) * V;
+      const int m = m0 + row, n = n0 + col;
+      if (m < g.M) {
+        const TC* srcp = tile + row * LDT + col;
+        TC* dstp = C + int64_t(m) * g.ldc + n;
+        if (n + V <= g.N) {
+          *reinterpret_cast<uint4*>(dstp) = *reinterpret_cast<const uint4*>(srcp);
+        } else {
+          for (int e = 0; e < V && n + e < g.N; ++e) dstp[e] = srcp[e];
+        }
+      }
+    }
+    // propagated checksums for the consumers downstream (a correction
+    // changes the output, not its propagated checksums)
+    if (cc && g.Cc != nullptr && own_c) {
+      float* Cc = g.Cc + b0 * g.sCc0 + b1 * g.sCc1;
+#pragma unroll
+      for (int j = 0; j < JN; ++j) {
+        const int n = n0 + wn * WN + j * 16 + fr;
+        if (n < g.N) {
+          Cc[int64_t(rc0 + 2 * g4) * g.ldcc + n] = accs[j][0] + accs[j][1];
+          Cc[int64_t(rc0 + 2 * g4 + 1) * g.ldcc + n] = accs[j][2] + accs[j][3];
+        }
+      }
+    }
+    if (cr && g.Cr != nullptr) {
+      const int nrb = BN / g.Rn;
+      if (g4 < nrb && n0 + g4 * g.Rn < g.N) {
+        float* Cr = g.Cr + b0 * g.sCr0 + b1 * g.sCr1;
+#pragma unroll
+        for (int i = 0; i < IS; ++i) {
+          const int m = m0 + (IS * wn + i) * 16 + fr;
+          if (m < g.M) {
+            Cr[int64_t(m) * g.ldcr + qc0 + 2 * g4] = accr[i][0] + accr[i][1];
+            Cr[int64_t(m) * g.ldcr + qc0 + 2 * g4 + 1] = accr[i][2] + accr[i][3];
+          }
+        }
+      }
+    }
+    if (!__syncthreads_or(flag)) return;
+
+    // a flagged vector: the column checksums go to LDS in the layout of the
+    // correction passes; the workgroup corrects and stores the tile again
+    const int ncb = cc ? BM / g.Rm : 0;
+    float* ccv = region;
+    float* rcv = ccv + CCV;
+    int* work = reinterpret_cast<int*>(rcv + RCV);
+    if (own_c) {
+#pragma unroll
+      for (int j = 0; j < JN; ++j) {
+        const int v = g4 * BN + wn * WN + j * 16 + fr;
+        ccv[v * 2] = accs[j][0] + accs[j][1];
+        ccv[v * 2 + 1] = accs[j][2] + accs[j][3];
+      }
+    }
+    __syncthreads();
+    passes(tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, work, 0, ncb, verify, tid);
+    for (int c = tid; c < BM * (BN / V); c += NT) {
+      const int row = c / (BN / V), col = (c % (BN / V)) * V;
+      const int m = m0 + row, n = n0 + col;
+      if (m >= g.M) continue;
+      const TC* srcp = tile + row * LDT + col;
+      TC* dstp = C + int64_t(m) * g.ldc + n;
+      if (n + V <= g.N) {
+        *reinterpret_cast<uint4*>(dstp) = *reinterpret_cast<const uint4*>(srcp);
+      } else {
+        for (int e = 0; e < V && n + e < g.N; ++e) dstp[e] = srcp[e];
+      }
+    }
+  }
+
   // EEC-ABFT on the LDS tile, one thread per vector (as in the paper's
   // Fig. 4): column pass, refresh of 1R-corrupted row checksums, row pass,
   // refresh of 1C-corrupted column checksums, final check (Sec. 4.2, 4.3).
@@ -1120,11 +1277,12 @@ constexpr int gemm_waves_per_eu() {
   return BM * BN > 128 * 128 ? 1 : (sizeof(T) == 2 && NSTAGE == 1 && !PROT ? 3 : 2);
 }
 
-template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE, bool DIR>
+template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE, bool DIR,
+          bool WLC>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<T, BM, BN, PROT, NSTAGE>())))
 void gemm_kernel(GemmDesc g) {
   extern __shared__ __align__(16) char smem[];
-  Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>::template run<DIR>(g, smem);
+  Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, WLC>::template run<DIR>(g, smem);
 }
 
 // The direct-to-LDS path needs bf16 operands, K ranges of whole 64-wide
@@ -1167,18 +1325,40 @@ hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   const size_t lds_max = std::max(G::lds_bytes(PROT, PROT),
                                   sizeof(T) == 2 ? G::d_main_bytes(PROT, PROT) : size_t(0));
   if (lds_max > 160 * 1024) return hipErrorInvalidValue;  // this tile does not fit gfx950 LDS
-  auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, false>;
+  // wave-local column check for protected bf16 outputs verified on the
+  // column side only (every checksum block of BM rows or less)
+  bool wlc = false;
+  if constexpr (G::MSUM) wlc = g.splitk <= 1 && g.verify <= 1 && (g.Ac == nullptr || g.Rm <= BM);
+  auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, false, false>;
   hipError_t e = hipSuccess;
   if constexpr (sizeof(T) == 2) {
     if (direct) {
-      constexpr auto k = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, true>;
-      kern = k;
-      e = set_lds_limit<k>(lds_max);
+      if constexpr (G::MSUM) {
+        if (wlc) {
+          constexpr auto k = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, true, true>;
+          kern = k;
+          e = set_lds_limit<k>(lds_max);
+        }
+      }
+      if (!wlc) {
+        constexpr auto k = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, true, false>;
+        kern = k;
+        e = set_lds_limit<k>(lds_max);
+      }
     }
   }
   if (!direct) {
-    constexpr auto k = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, false>;
-    e = set_lds_limit<k>(lds_max);
+    if constexpr (G::MSUM) {
+      if (wlc) {
+        constexpr auto k = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, false, true>;
+        kern = k;
+        e = set_lds_limit<k>(lds_max);
+      }
+    }
+    if (!wlc) {
+      constexpr auto k = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, false, false>;
+      e = set_lds_limit<k>(lds_max);
+    }
   }
   if (e != hipSuccess) return e;
   const int64_t ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
