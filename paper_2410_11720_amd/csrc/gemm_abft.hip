@@ -1000,9 +1000,13 @@ struct Gemm {
   // one column a lane holds for blocks i = 2s, 2s + 1 are the 32 rows of
   // segment s); the propagated checksums of column block b are the strip
   // rows 4b..4b+3, i.e. lane group b of the strip result (hi/lo c1, c2).
-  // The wave stores its part of the tile at once; a tile with a flagged
-  // vector then takes the workgroup through the correction passes and is
-  // stored again.
+  // The wave stores its part of the tile at once. A two-sided output also
+  // checks its rows: each wave sums its 32-column segments of every row
+  // (ones-operand MFMAs on the staged tile), the partial sums meet in LDS
+  // behind one barrier, and the lanes holding a row's propagated row
+  // checksums (lane group b of the row strip: row block b) decide it. A
+  // tile with a flagged vector then takes the workgroup through the
+  // correction passes and is stored again.
   __device__ static __forceinline__ void epilogue_wlc(
       const GemmDesc& g, TC* tile, const T* A, const T* B, TC* C, int z, int m0, int n0,
       int k_lo, int k_hi, bool cc, bool cr, int rc0, int qc0, const uint32_t (&pk)[IM][JN][2],
@@ -1011,7 +1015,7 @@ struct Gemm {
     const int fr = lane & 15, g4 = lane >> 4;
     const int b0 = z / g.nb1, b1 = z % g.nb1;
     constexpr int SEG = MINB;
-    const int verify = cc ? g.verify : 0;  // <= 1: no row verification here
+    const int verify = cc ? g.verify : 0;
     // the wave reads back only what it wrote itself
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -1091,9 +1095,53 @@ struct Gemm {
         }
       }
     }
+    const int nrb = (cr && verify == 2) ? BN / g.Rn : 0;  // row blocks per tile row
+    if constexpr (WN % SEG == 0) {
+      if (nrb > 0) {
+        // partial sums of each row over this wave's SEG-column segments:
+        // the staged rows as the B operand (column = row lane % 16, 8
+        // consecutive columns per lane group), so every lane gets a row sum
+        constexpr int TS = WN / SEG;                 // segments per wave
+        float2* part = reinterpret_cast<float2*>(region);  // [BN / SEG][BM]
+        const bf16x8 ones = __builtin_bit_cast(
+            bf16x8, uint4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+        const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < IM; ++i)
+#pragma unroll
+          for (int t = 0; t < TS; ++t) {
+            const uint4 u = *reinterpret_cast<const uint4*>(
+                tile + (i * 16 + fr) * LDT + wn * WN + t * SEG + 8 * g4);
+            const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu,
+                              u.w & 0x7fff7fffu};
+            const floatx4 sm = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, u), zero);
+            const floatx4 mg = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, ua), zero);
+            if (g4 == 0) part[(wn * TS + t) * BM + i * 16 + fr] = float2{sm[0], mg[0]};
+          }
+        __syncthreads();
+        // lane group g4 of the row strip holds row block g4 of rows
+        // (IS wn + i) 16 + lane % 16
+        const int spb = g.Rn / SEG;
+        if (g4 < nrb && n0 + g4 * g.Rn < g.N) {
+#pragma unroll
+          for (int i = 0; i < IS; ++i) {
+            const int row = (IS * wn + i) * 16 + fr;
+            if (m0 + row < g.M) {
+              float r1 = 0.f, sa = 0.f;
+              for (int q = 0; q < spb; ++q) {
+                const float2 pq = part[(g4 * spb + q) * BM + row];
+                r1 += pq.x;
+                sa += pq.y;
+              }
+              flag |= flagged(accr[i][0] + accr[i][1] - r1, sa, g.e_rel);
+            }
+          }
+        }
+      }
+    }
     if (!__syncthreads_or(flag)) return;
 
-    // a flagged vector: the column checksums go to LDS in the layout of the
+    // a flagged vector: the checksums go to LDS in the layout of the
     // correction passes; the workgroup corrects and stores the tile again
     const int ncb = cc ? BM / g.Rm : 0;
     float* ccv = region;
@@ -1107,8 +1155,16 @@ struct Gemm {
         ccv[v * 2 + 1] = accs[j][2] + accs[j][3];
       }
     }
+    if (g4 < nrb) {
+#pragma unroll
+      for (int i = 0; i < IS; ++i) {
+        const int u = ((IS * wn + i) * 16 + fr) * nrb + g4;
+        rcv[u * 2] = accr[i][0] + accr[i][1];
+        rcv[u * 2 + 1] = accr[i][2] + accr[i][3];
+      }
+    }
     __syncthreads();
-    passes(tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, work, 0, ncb, verify, tid);
+    passes(tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, work, nrb, ncb, verify, tid);
     for (int c = tid; c < BM * (BN / V); c += NT) {
       const int row = c / (BN / V), col = (c % (BN / V)) * V;
       const int m = m0 + row, n = n0 + col;
@@ -1119,6 +1175,28 @@ struct Gemm {
         *reinterpret_cast<uint4*>(dstp) = *reinterpret_cast<const uint4*>(srcp);
       } else {
         for (int e = 0; e < V && n + e < g.N; ++e) dstp[e] = srcp[e];
+      }
+    }
+    if (nrb > 0) {  // checksums the passes refreshed (1R / 1C) go downstream
+      if (cc && g.Cc != nullptr) {
+        float* Cc = g.Cc + b0 * g.sCc0 + b1 * g.sCc1;
+        for (int v = tid; v < ncb * BN; v += NT) {
+          const int blk = v / BN, n = v % BN;
+          if (m0 + blk * g.Rm < g.M && n0 + n < g.N) {
+            Cc[int64_t(rc0 + 2 * blk) * g.ldcc + n0 + n] = ccv[v * 2];
+            Cc[int64_t(rc0 + 2 * blk + 1) * g.ldcc + n0 + n] = ccv[v * 2 + 1];
+          }
+        }
+      }
+      if (g.Cr != nullptr) {
+        float* Cr = g.Cr + b0 * g.sCr0 + b1 * g.sCr1;
+        for (int u = tid; u < BM * nrb; u += NT) {
+          const int row = u / nrb, rb = u % nrb;
+          if (m0 + row < g.M && n0 + rb * g.Rn < g.N) {
+            Cr[int64_t(m0 + row) * g.ldcr + qc0 + 2 * rb] = rcv[u * 2];
+            Cr[int64_t(m0 + row) * g.ldcr + qc0 + 2 * rb + 1] = rcv[u * 2 + 1];
+          }
+        }
       }
     }
   }
@@ -1328,7 +1406,10 @@ hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   // wave-local column check for protected bf16 outputs verified on the
   // column side only (every checksum block of BM rows or less)
   bool wlc = false;
-  if constexpr (G::MSUM) wlc = g.splitk <= 1 && g.verify <= 1 && (g.Ac == nullptr || g.Rm <= BM);
+  // (two-sided outputs too when a wave's columns hold whole 32-column
+  // segments)
+  if constexpr (G::MSUM)
+    wlc = g.splitk <= 1 && (g.verify <= 1 || BN / 4 >= 32) && (g.Ac == nullptr || g.Rm <= BM);
   auto kern = gemm_kernel<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, false, false>;
   hipError_t e = hipSuccess;
   if constexpr (sizeof(T) == 2) {
