@@ -343,10 +343,40 @@ def fused_forward(L, steps):
         e1.synchronize()
         return e0.elapsed_time(e1) * 1e3 / n
 
+    def per_step(lay, n):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        L.step(lay, (None, 0))
+        torch.cuda.synchronize()
+        ev[0].record(L.stream)
+        for i in range(n):
+            L.step(lay, (None, 0))
+            ev[i + 1].record(L.stream)
+        torch.cuda.synchronize()
+        return float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(n)]))
+
+    def regen_us(cfg, lay, n):
+        run = lambda: abft.attn_abft_backward_stages(cfg, L.dO, L.X, L.Wqkv, L.Wo, lay.workspace,
+                                                     L.dX, L.dWqkv, L.dWo, None, 0,
+                                                     lay.report_bwd, 0x400, L.stream,
+                                                     append=True)
+        run()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(L.stream)
+        for _ in range(n):
+            run()
+        e1.record(L.stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
     ms_fp, ms_fu = per_forward(lays[True][1], steps), per_forward(lays[False][1], steps)
     ms_mp, ms_mu = per_forward(L.lay_p, steps), per_forward(L.lay_u, steps)
     us_p = core_us(*lays[True], steps)
     us_u = core_us(*lays[False], steps)
+    st_fp, st_fu = per_step(lays[True][1], steps), per_step(lays[False][1], steps)
+    st_mp, st_mu = per_step(L.lay_p, steps), per_step(L.lay_u, steps)
+    us_regen = regen_us(*lays[True], steps)
+    # the training step with the fused forward: useful flops as the workload's
+    step_flops = useful_flops(B, S, H, nh, shape.causal)
     P = S * (S + 1) // 2 if shape.causal else S * S
     core_flops = 4.0 * B * nh * d * P          # Q K^T and P V over the unmasked pairs
     tf = core_flops / (us_p * 1e-6) / 1e12
@@ -368,6 +398,14 @@ def fused_forward(L, steps):
         "kernel_flops": core_flops,
         "one_score_fault": {"corrected": rep["n_corrected"],
                             "uncorrectable": rep["n_uncorrectable"]},
+        "step": {"note": "fused forward, AP regenerated, protected backward chain",
+                 "ms_protected": round(st_fp, 4), "ms_unprotected": round(st_fu, 4),
+                 "abft_overhead_pct": round((st_fp - st_fu) / st_fu * 100, 2),
+                 "tflops_protected": round(step_flops / (st_fp * 1e-3) / 1e12, 3),
+                 "ms_materialised_protected": round(st_mp, 4),
+                 "ms_materialised_unprotected": round(st_mu, 4),
+                 "speedup_vs_materialised_protected": round(st_mp / st_fp, 3),
+                 "regen_kernel_us": round(us_regen, 2)},
     }
 
 

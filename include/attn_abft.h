@@ -75,9 +75,11 @@ extern "C" {
                                        multiple of 128 (else
                                        ABFT_ERR_UNSUPPORTED); the stage bits
                                        SCORE, SOFTMAX and CONTEXT each select
-                                       that kernel. A backward after a fused
-                                       forward returns ABFT_ERR_UNSUPPORTED
-                                       (AP is not saved).                       */
+                                       that kernel. It saves each query's
+                                       softmax max and sum and CL^r; a backward
+                                       with the same flag first regenerates AP
+                                       and AP^r from Q, K and them (stage
+                                       REGEN), then runs the protected chain.   */
 
 /* ---- op tags of protected GEMM outputs (paper Table 1 + backward) ----- */
 enum abft_op {
@@ -203,7 +205,9 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
 #define ABFT_STAGE_DK          0x080u  /* bwd: dK = dAS^T Q                         */
 #define ABFT_STAGE_DWQKV       0x100u  /* bwd: dWqkv = X^T [dQ|dK|dV]               */
 #define ABFT_STAGE_DX          0x200u  /* bwd: dX = [dQ|dK|dV] Wqkv^T               */
-#define ABFT_STAGE_ALL         0x3ffu
+#define ABFT_STAGE_REGEN       0x400u  /* bwd after a fused forward: AP, AP^r from
+                                          Q, K and the softmax statistics      */
+#define ABFT_STAGE_ALL         0x7ffu
 
 /* attn_abft_forward / attn_abft_backward restricted to the stages in the
  * mask (profiling). A stage reads what earlier stages left in the

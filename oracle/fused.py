@@ -29,6 +29,12 @@ keys, key tiles in increasing order (causal: key tiles up to the diagonal):
      is fixed from the checksum (DELTA / RECONSTRUCT, Sec. 4.2).
   5. CL^c, needed by the output projection, is encoded from the verified
      CL (column checksums per R-query block).
+For the backward (the materialised chain of the layer), the softmax
+statistics of every query (the final max m and sum l of step 3) are kept,
+and AP is regenerated from Q, K and them: AP = storage-rounded
+exp(scale Q K^T - m) / l on the unmasked pairs (0 on masked ones), with its
+row checksums AP^r encoded from the stored values; CL^r = A^r / l is the
+propagated row checksum of CL the backward's dW^O check takes.
 
 Rounding: S and the accumulators are kept unrounded (fp64 here, fp32 on
 the GPU); P is rounded to the storage dtype (it feeds the P V product);
@@ -39,7 +45,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .eec import col_checksums, eec_locate, fix_by_checksum
+from .eec import col_checksums, eec_locate, fix_by_checksum, row_checksums
 from .layer import OracleParams, _Run, project, output_projection
 from .numerics import classify, flip_exponent_msb, round_to, stored_threshold
 
@@ -71,10 +77,12 @@ def _check_rows(v2, c1, c2, e_rel, tn, recompute, tc, store=lambda x: x):
     return events, unc
 
 
-def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None):
+def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None, stats=None):
     """Steps 1-5 for every (batch, head), or for the (batch, head) pairs in
     `only` (the others' CL stays zero). Returns CL [B,S,H] and CL^c
-    [B,nq,2,H]; events go to run.events."""
+    [B,nq,2,H]; events go to run.events. With a dict `stats`, also stores
+    there the final max m and sum l of every query ([B,nh,S], natural
+    units) and CL^r = A^r / l ([B,S,nh,2])."""
     B, S, H, nh, d, R, nq, scale = (pr[k] for k in ("B", "S", "H", "nh", "d", "R", "nq", "scale"))
     Qh, Kh, Vh, Kch, Vr = pr["Qh"], pr["Kh"], pr["Vh"], pr["Kch"], pr["Vr"]
     if S % TQ or R > TK or TK % R:
@@ -87,6 +95,8 @@ def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None):
     faults_as = run.faults.get("AS", ())
     faults_cl = run.faults.get("CL", ())
     CLh = np.zeros((B, nh, S, d))
+    M_all, L_all = np.zeros((B, nh, S)), np.zeros((B, nh, S))
+    CLr_all = np.zeros((B, S, nh, 2))
     for b in range(B):
         for h in range(nh):
             if only is not None and (b, h) not in only:
@@ -141,6 +151,8 @@ def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None):
                     m = m_new
                 CLt = run.rnd(A / l[:, None])                           # 4.
                 CLr = Ar / l[:, None]
+                M_all[b, h, q0:q0 + TQ], L_all[b, h, q0:q0 + TQ] = m, l
+                CLr_all[b, q0:q0 + TQ, h] = CLr
                 for (fb, fh, fr, fc, val, *mode) in faults_cl:
                     if fb == b and fh == h and q0 <= fr < q0 + TQ:
                         i = fr - q0
@@ -159,7 +171,20 @@ def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None):
                 CLh[b, h, q0:q0 + TQ] = CLt
     CL = CLh.transpose(0, 2, 1, 3).reshape(B, S, H)
     CLc = col_checksums(CL, R)                                          # 5.
+    if stats is not None:
+        stats.update(m=M_all, l=L_all, CLr=CLr_all)
     return CL, CLc
+
+
+def regenerate_ap(run: _Run, pr: dict, p: OracleParams, m, l):
+    """AP = rounded exp(scale Q K^T - m) / l on the unmasked pairs (0 on
+    masked ones) and its row checksums per R-key block."""
+    Qh, Kh, scale, S, R = pr["Qh"], pr["Kh"], pr["scale"], pr["S"], pr["R"]
+    allowed = np.tril(np.ones((S, S), dtype=bool)) if p.causal else np.ones((S, S), dtype=bool)
+    with np.errstate(over="ignore", invalid="ignore"):
+        Z = scale * (Qh @ Kh.swapaxes(-1, -2))
+        AP = run.rnd(np.where(allowed, np.exp(Z - m[..., None]) / l[..., None], 0.0))
+    return AP, row_checksums(AP, R)
 
 
 def fused_forward(X, Wqkv, Wo, p: OracleParams, faults=()):
@@ -168,7 +193,13 @@ def fused_forward(X, Wqkv, Wo, p: OracleParams, faults=()):
     event list."""
     run = _Run(p, faults)
     pr = project(run, X, Wqkv, p)
-    CL, CLc = fused_attention(run, pr, p)
-    O, Oc = output_projection(run, CL, CLc, np.asarray(Wo, dtype=np.float64), p)
+    st = {}
+    CL, CLc = fused_attention(run, pr, p, stats=st)
+    Wo = np.asarray(Wo, dtype=np.float64)
+    O, Oc = output_projection(run, CL, CLc, Wo, p)
+    AP, APr = regenerate_ap(run, pr, p, st["m"], st["l"])
+    # the dict carries what the layer's backward takes from a forward
     return dict(O=O, CL=CL, CLc=CLc, Oc=Oc, QKV=pr["QKV"], QKVc=pr["QKVc"], Vr=pr["Vr"],
-                scale=pr["scale"], events=run.events, params=p)
+                X=pr["X"], Wqkv=pr["Wqkv"], Wo=Wo, Xc=pr["Xc"], Xr=pr["Xr"], AP=AP, APr=APr,
+                CLr=st["CLr"], m=st["m"], l=st["l"], scale=pr["scale"], events=run.events,
+                params=p)

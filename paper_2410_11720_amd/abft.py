@@ -204,7 +204,7 @@ def attn_abft_backward(cfg: LayerConfig, dO, X, Wqkv, Wo, workspace, dX, dWqkv, 
                                    _ptr(report), _stream(stream)), "attn_abft_backward")
 
 
-STAGE_ALL = 0x3FF
+STAGE_ALL = 0x7FF
 FWD_STAGES = {"encode": 0x001, "qkv": 0x002, "score": 0x004, "softmax": 0x008,
               "context": 0x010, "out": 0x020}
 BWD_STAGES = {"encode": 0x001, "dCL": 0x002, "dWo": 0x004, "dAP": 0x008, "dV": 0x010,

@@ -121,7 +121,8 @@ struct FusedDesc {
   float scale = 1.f;
   const void* qkv = nullptr;   // [B*S][3H] bf16: Q | K | V column blocks
   const float* qkvc = nullptr; // [B][S/R][2][3H] propagated column checksums (K^c used)
-  const float* vr = nullptr;   // [B*S][nh][2] propagated V^r (row checksums per head)
+  const float* vr = nullptr;   // [B*S][nh][2] propagated V^r (row checksums per head);
+                               // carried through P V when given (CL check, CL^r)
   void* cl = nullptr;          // [B*S][H] bf16 output
   int check_as = 0, check_cl = 0;
   int recompute = 1;           // located score errors: recompute (else checksum fix)
@@ -129,8 +130,28 @@ struct FusedDesc {
   const abft_fault* faults = nullptr;
   int n_faults = 0;
   abft_report* report = nullptr;
+  // for the backward (may be null): per query the log2-scaled running max
+  // and the sum of the online softmax [B][nh][S][2], and CL^r = A^r / l,
+  // the propagated row checksums of CL [B*S][nh][2]
+  float* stats = nullptr;
+  float* clr = nullptr;
 };
 hipError_t launch_fused_fwd(const FusedDesc& d, hipStream_t stream);
+
+// AP regenerated from Q, K and the fused forward's softmax statistics for
+// the backward: AP [B][nh][S][S] bf16 (key tiles up to the diagonal tile
+// under a causal mask, masked entries 0) and its row checksums
+// AP^r [B][nh][S][S/R][2] from the stored values.
+struct RegenDesc {
+  int B = 0, nh = 0, S = 0, H = 0, D = 0, R = 128;
+  int causal = 0;
+  float scale = 1.f;
+  const void* qkv = nullptr;
+  const float* stats = nullptr;
+  void* ap = nullptr;
+  float* apr = nullptr;
+};
+hipError_t launch_regen_ap(const RegenDesc& d, hipStream_t stream);
 
 // Checksum encoder (public encode_checksums) and standalone verifier.
 hipError_t launch_encode(const void* A, int dtype, int64_t batch, int64_t rows, int64_t cols,

@@ -48,6 +48,7 @@ struct Layout_ {
   size_t qkv, ap, cl, as, das, dcl, dqkv;
   size_t xc, xr, wvr, qkvc, vr, apc, apr, clc, clr, doc, dclc, dasc, dasr, dqkvc;
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
+  size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
   size_t total;
 };
 
@@ -116,6 +117,7 @@ Layout_ make_layout(const Dims& d) {
   const size_t c2 = ks2 > 1 ? size_t(ks2) * 2 * d.nh * d.H : 0;
   L.skp = take((p1 > p2 ? p1 : p2) * f);
   L.skc = take((c1 > c2 ? c1 : c2) * f);
+  L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
   L.total = off;
   return L;
 }
@@ -340,7 +342,7 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
     fd.scale = p.scale;
     fd.qkv = ws + L.qkv;
     fd.qkvc = p.sec_as ? F(L.qkvc) : nullptr;
-    fd.vr = p.sec_cl ? F(L.vr) : nullptr;
+    fd.vr = need_vr ? F(L.vr) : nullptr;   // V^r carried: CL check, CL^r for dW^O
     fd.cl = ws + L.cl;
     fd.check_as = p.sec_as;
     fd.check_cl = p.sec_cl;
@@ -350,6 +352,8 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
     fd.tn_cl = p.tn;
     fd.tc = p.tc;
     fd.faults = faults; fd.n_faults = n_faults; fd.report = report;
+    fd.stats = F(L.stats);
+    fd.clr = F(L.clr);
     CK(launch_fused_fwd(fd, s));
     if (p.sec_o)  // CL^c for O^c = CL^c Wo, encoded from the verified CL
       CK(launch_encode(ws + L.cl, dt, B, S, H, H, S * H, int(R), int(hd), F(L.clc), nullptr, s));
@@ -432,7 +436,6 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   if (!dO || !X || !Wqkv || !Wo || !workspace || !dX || !dWqkv || !dWo || !report ||
       n_faults < 0 || (n_faults > 0 && !faults))
     return ABFT_ERR_INVALID;
-  if (cfg->flags & ABFT_FLAG_FUSED) return ABFT_ERR_UNSUPPORTED;  // AP was not saved
   const Layout_ L = make_layout(d);
   if (workspace_bytes < L.total) return ABFT_ERR_WORKSPACE;
   if ((st = check_device()) != ABFT_OK) return st;
@@ -448,6 +451,19 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   if (!(cfg->flags & ABFT_FLAG_REPORT_APPEND)) CK(launch_report_reset(report, 0, false, s));
   if ((stages & ABFT_STAGE_ENCODE) && pb) CK(launch_encode(dO, dt, B, S, H, H, S * H, int(R), int(hd), F(L.doc), nullptr, s));
 
+  // after a fused forward: AP (and AP^r) regenerated from Q, K and the
+  // softmax statistics the forward saved
+  if ((cfg->flags & ABFT_FLAG_FUSED) && (stages & ABFT_STAGE_REGEN)) {
+    RegenDesc rd;
+    rd.B = int(B); rd.nh = int(nh); rd.S = int(S); rd.H = int(H); rd.D = int(hd); rd.R = int(R);
+    rd.causal = cfg->causal;
+    rd.scale = p.scale;
+    rd.qkv = ws + L.qkv;
+    rd.stats = F(L.stats);
+    rd.ap = ws + L.ap;
+    rd.apr = F(L.apr);
+    CK(launch_regen_ap(rd, s));
+  }
   // dCL = dO Wo^T, dCL^c = dO^c Wo^T
   if (stages & ABFT_STAGE_DCL) {
     GemmDesc g = base_desc(p, faults, n_faults, report);

@@ -179,7 +179,7 @@ struct FusedAttn {
             kcv[p] = ok ? v : 0.f;
           }
         }
-        if (fd.check_cl)
+        if (fd.vr != nullptr)
           vrv = fd.vr[((int64_t(b) * S + key0 + (tid >> 1)) * fd.nh + h) * 2 + (tid & 1)];
       }
     };
@@ -200,7 +200,7 @@ struct FusedAttn {
             }
           }
         }
-        if (fd.check_cl) {
+        if (fd.vr != nullptr) {
           bf16_t* vrs = reinterpret_cast<bf16_t*>(sb + K_BYTES + V_BYTES + KC_BYTES);
           const bf16_t hi = f2bf(vrv);
           const bf16_t lo = f2bf(vrv - bf2f(hi));
@@ -434,7 +434,7 @@ struct FusedAttn {
             o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb], o[db][qb], 0, 0, 0);
         }
         if constexpr (PROT) {
-          if (fd.check_cl) {
+          if (fd.vr != nullptr) {
             const bf16_t* vrs =
                 reinterpret_cast<const bf16_t*>(sb + K_BYTES + V_BYTES + KC_BYTES);
             const bf16x8 rf = vr_frag(vrs, 32 * t, lane);
@@ -452,7 +452,20 @@ struct FusedAttn {
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       const int q = qw + 16 * qb + lq;
-      const float inv = 1.f / group4_sum(l[qb]);
+      const float lsum = group4_sum(l[qb]);
+      const float inv = 1.f / lsum;
+      if (fd.stats != nullptr && g == 0) {
+        float* st = fd.stats + ((int64_t(b) * fd.nh + h) * S + q) * 2;
+        st[0] = m[qb];
+        st[1] = lsum;
+      }
+      if constexpr (PROT) {
+        if (fd.vr != nullptr && fd.clr != nullptr && g == 0) {
+          float* cr = fd.clr + ((int64_t(b) * S + q) * fd.nh + h) * 2;
+          cr[0] = (vra[qb][0] + vra[qb][1]) * inv;
+          cr[1] = (vra[qb][2] + vra[qb][3]) * inv;
+        }
+      }
       float ov[DB][4];
 #pragma unroll
       for (int db = 0; db < DB; ++db)
@@ -542,6 +555,134 @@ struct FusedAttn {
   }
 };
 
+// AP regeneration for the backward: per (batch, head, 128-query tile)
+// the same S^T = K Q^T products as the fused forward, then
+// AP = exp2(log2(e) scale S - m) / l (the forward's final max and sum of
+// each query) rounded to bf16 and stored, 0 past the diagonal under a
+// causal mask; AP^r (sum and 1-based weighted sum over each R-key block of
+// a row) from the stored values.
+template <int D>
+struct RegenAP {
+  static constexpr int KH = D / 64, KS = D / 32;
+  using DK = Direct<true, FT>;
+  static constexpr int STAGE_BYTES = KH * DK::BYTES;
+  static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+
+  __device__ static void run(const RegenDesc& rd, char* smem) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lq = lane & 15, g = lane >> 4;
+    const int nqt = rd.S / FT, nbh = rd.B * rd.nh;
+    const int z = blockIdx.x % nbh;
+    const int qt = rd.causal ? nqt - 1 - int(blockIdx.x) / nbh : int(blockIdx.x) / nbh;
+    const int b = z / rd.nh, h = z % rd.nh;
+    const int q0 = qt * FT, qw = q0 + wave * 32;
+    const int S = rd.S, H = rd.H, R = rd.R, NB = FT / R, nqR = S / R;
+    const int64_t ld = 3 * int64_t(H);
+    const bf16_t* base = static_cast<const bf16_t*>(rd.qkv) + int64_t(b) * S * ld;
+    const bf16_t* Qp = base + h * D;
+    const bf16_t* Kp = base + H + h * D;
+    const int nkt = rd.causal ? qt + 1 : nqt;
+    const float sl2 = rd.scale * 1.4426950408889634f;
+    const int lg_jpb = __builtin_ctz(R / 16);
+
+    bf16x8 qf[2][KS];
+    float mq[2], il[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int q = qw + 16 * qb + lq;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+        qf[qb][kk] = *reinterpret_cast<const bf16x8*>(Qp + int64_t(q) * ld + 32 * kk + 8 * g);
+      const float* st = rd.stats + ((int64_t(b) * rd.nh + h) * S + q) * 2;
+      mq[qb] = st[0];
+      il[qb] = 1.f / st[1];
+    }
+    auto issue = [&](int kt, int stg) {
+      char* sb = smem + stg * STAGE_BYTES;
+#pragma unroll
+      for (int hf = 0; hf < KH; ++hf)
+        DK::issue(Kp, ld, kt * FT, S, hf * 64, sb + hf * DK::BYTES, wave, lane);
+    };
+    bf16_t* AP = static_cast<bf16_t*>(rd.ap) + (int64_t(b) * rd.nh + h) * S * S;
+    float* APr = rd.apr + (int64_t(b) * rd.nh + h) * S * nqR * 2;
+
+    issue(0, 0);
+    for (int kt = 0; kt < nkt; ++kt) {
+      const int stg = kt & 1;
+      wait_vmcnt<0>();
+      __syncthreads();  // tile kt visible; every wave is done with tile kt - 1
+      if (kt + 1 < nkt) issue(kt + 1, stg ^ 1);
+      const char* sb = smem + stg * STAGE_BYTES;
+      const int key0 = kt * FT;
+      floatx4 s[8][2];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) s[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const char* sk = sb + (kk >> 1) * DK::BYTES;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const bf16x8 kf = DK::frag(sk, 16 * j, (kk & 1) * 32, lane);
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+            s[j][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][kk], s[j][qb], 0, 0, 0);
+        }
+      }
+      const bool diag = rd.causal && kt == qt;
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        const int q = qw + 16 * qb + lq;
+        float c1[4] = {0.f, 0.f, 0.f, 0.f}, c2[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          float a[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = key0 + 16 * j + 4 * g + r;
+            const float p = (diag && key > q)
+                                ? 0.f
+                                : __builtin_amdgcn_exp2f(s[j][qb][r] * sl2 - mq[qb]) * il[qb];
+            a[r] = bf2f(f2bf(p));
+          }
+          const uint2 w = {pack2(a[0], a[1]), pack2(a[2], a[3])};
+          *reinterpret_cast<uint2*>(AP + int64_t(q) * S + key0 + 16 * j + 4 * g) = w;
+          // the 16-key group j lies in block j >> lg_jpb; weights 1..R in it
+          const int wb = ((16 * j) & (R - 1)) + 4 * g + 1;
+          const float s1 = (a[0] + a[1]) + (a[2] + a[3]);
+          const float s2 = float(wb) * a[0] + float(wb + 1) * a[1] + float(wb + 2) * a[2] +
+                           float(wb + 3) * a[3];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if ((j >> lg_jpb) == i) {
+              c1[i] += s1;
+              c2[i] += s2;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (i < NB) {
+            const float t1 = group4_sum(c1[i]), t2 = group4_sum(c2[i]);
+            if (g == i) {
+              float* o = APr + (int64_t(q) * nqR + key0 / R + i) * 2;
+              o[0] = t1;
+              o[1] = t2;
+            }
+          }
+        }
+      }
+    }
+  }
+};
+
+template <int D>
+__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(2)))
+void regen_ap_kernel(RegenDesc rd) {
+  extern __shared__ __align__(16) char smem[];
+  RegenAP<D>::run(rd, smem);
+}
+
 template <int D, bool PROT>
 __global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(2)))
 void fused_attn_kernel(FusedDesc fd) {
@@ -567,12 +708,39 @@ hipError_t launch_d(const FusedDesc& fd, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int D>
+hipError_t launch_regen_d(const RegenDesc& rd, hipStream_t s) {
+  using F = RegenAP<D>;
+  static bool attr = false;
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(regen_ap_kernel<D>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             F::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int64_t grid = int64_t(rd.B) * rd.nh * (rd.S / FT);
+  if (grid == 0) return hipSuccess;
+  auto kern = regen_ap_kernel<D>;
+  hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(FNT), F::LDS_BYTES, s, rd);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_regen_ap(const RegenDesc& rd, hipStream_t s) {
+  if (rd.S % FT != 0 || rd.R < 16 || FT % rd.R != 0 || rd.H != rd.nh * rd.D ||
+      rd.stats == nullptr || rd.ap == nullptr || rd.apr == nullptr)
+    return hipErrorInvalidValue;
+  if (rd.D == 64) return launch_regen_d<64>(rd, s);
+  if (rd.D == 128) return launch_regen_d<128>(rd, s);
+  return hipErrorInvalidValue;
+}
 
 hipError_t launch_fused_fwd(const FusedDesc& fd, hipStream_t s) {
   if (fd.S % FT != 0 || fd.R < 16 || FT % fd.R != 0 || fd.H != fd.nh * fd.D)
     return hipErrorInvalidValue;
-  const bool prot = fd.check_as || fd.check_cl;
+  const bool prot = fd.check_as || fd.check_cl || fd.vr != nullptr;
   if (prot && fd.R < 32) return hipErrorInvalidValue;  // 4 strip rows per block, 16 rows
   if ((fd.check_as && fd.qkvc == nullptr) || (fd.check_cl && fd.vr == nullptr))
     return hipErrorInvalidValue;

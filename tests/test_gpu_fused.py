@@ -141,16 +141,70 @@ def test_fused_gpt2_shape_sampled_heads():
     assert run.events == []
 
 
-def test_fused_rejects_unsupported_shapes_and_backward():
+def test_fused_rejects_unsupported_shapes():
     abft = _abft()
     with pytest.raises(abft.AbftError):
         abft.ProtectedAttention(abft.LayerConfig(1, 192, 128, 2, block_rows=64, fused=True))
     with pytest.raises(abft.AbftError):
         abft.ProtectedAttention(abft.LayerConfig(1, 256, 128, 2, dtype="f32", fused=True))
-    shape = W.make_shape(1, 256, 128, 2, name="bwd")
-    inp = W.make_inputs(shape, 1)
-    layer = abft.ProtectedAttention(abft.LayerConfig(1, 256, 128, 2, fused=True))
+
+
+def run_fused_training(shape, faults=(), seed=1):
+    """Fused forward, then the backward (AP regenerated from the softmax
+    statistics), against the fused oracle followed by the layer oracle's
+    backward."""
+    abft = _abft()
+    print(f"[case] fused fwd+bwd {shape.name} causal={shape.causal} R={shape.block_rows} "
+          f"faults={len(faults)}", flush=True)
+    inp = W.make_inputs(shape, seed)
+    cfg = abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads,
+                           causal=shape.causal, block_rows=shape.block_rows, fused=True)
+    layer = abft.ProtectedAttention(cfg)
     X, Wqkv, Wo, dO = (dev(inp[k]) for k in ("X", "Wqkv", "Wo", "dO"))
-    layer.forward(X, Wqkv, Wo)
-    with pytest.raises(abft.AbftError):
-        layer.backward(dO, X, Wqkv, Wo)
+    fdev = abft.faults_to_device(list(faults))
+    O = layer.forward(X, Wqkv, Wo, fdev)
+    dX, dWqkv, dWo = layer.backward(dO, X, Wqkv, Wo, fdev)
+    torch.cuda.synchronize()
+    g = dict(O=host(O), AP=host(layer.tensor("AP")), dX=host(dX), dWqkv=host(dWqkv),
+             dWo=host(dWo), rep_f=abft.read_report(layer.report),
+             rep_b=abft.read_report(layer.report_bwd))
+    from oracle import backward
+    p = OracleParams(heads=shape.heads, causal=shape.causal, block_rows=shape.block_rows)
+    o = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, list(faults))
+    ob = backward(o, inp["dO"], p, list(faults))
+    return g, o, ob
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("R", [128, 64])
+def test_fused_forward_backward(causal, R):
+    shape = W.make_shape(2, 256, 128, 2, causal=causal, block_rows=R, name="train")
+    g, o, ob = run_fused_training(shape)
+    assert g["rep_f"]["events"] == [] and g["rep_b"]["events"] == []
+    assert o["events"] == [] and ob["events"] == []
+    # the regenerated probabilities where the backward reads them (key
+    # tiles up to the diagonal tile)
+    S = shape.seq
+    written = np.ones((S, S), dtype=bool)
+    if causal:
+        for i in range(S):
+            written[i, (i // 128 + 1) * 128:] = False
+    ap_g, ap_o = g["AP"][..., written], o["AP"][..., written]
+    # P is rounded to bf16 on both sides from exponentials taken in fp32
+    # and fp64: one bf16 step apart at most
+    assert np.abs(ap_g - ap_o).max() <= 2.0 ** -7 * np.abs(ap_o).max()
+    for k in ("O", "dX", "dWqkv", "dWo"):
+        ref = o[k] if k == "O" else ob[k]
+        assert_close(g[k], ref, k)
+
+
+def test_fused_backward_faults():
+    shape = W.make_shape(1, 256, 128, 2, causal=True, block_rows=128, name="trainf")
+    faults = [W.Fault("AS", 0, 1, 200, 3, np.inf), W.Fault("dV", 0, 0, 17, 9, np.nan),
+              W.Fault("dQ", 0, 1, 130, 60, 1e10), W.Fault("dX", 0, 0, 77, 100, np.inf)]
+    g, o, ob = run_fused_training(shape, faults)
+    assert sorted(g["rep_f"]["events"]) == sorted(o["events"])
+    assert sorted(g["rep_b"]["events"]) == sorted(ob["events"])
+    assert len(o["events"]) + len(ob["events"]) == 4
+    for k in ("dX", "dWqkv", "dWo"):
+        assert_close(g[k], ob[k], k)

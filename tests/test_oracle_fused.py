@@ -154,3 +154,27 @@ def test_tiles_cover_the_sequence():
     with pytest.raises(ValueError):
         fused_forward(*(_inputs(S=192)[k] for k in ("X", "Wqkv", "Wo")),
                       OracleParams(heads=2, block_rows=64))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_regenerated_probabilities_feed_the_backward(causal):
+    """The softmax statistics of the fused forward regenerate AP (and AP^r),
+    and with CL^r they let the layer's backward run after a fused forward:
+    in fp32 storage the gradients equal those after the materialised
+    forward."""
+    from oracle import backward
+    inp = _inputs(dtype="f32")
+    p = OracleParams(heads=2, dtype="f32", causal=causal, block_rows=128)
+    a = forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    assert np.abs(a["AP"] - f["AP"]).max() <= 1e-6
+    assert np.abs(a["CLr"] - f["CLr"]).max() <= 1e-5 * np.abs(a["CLr"]).max()
+    # every regenerated row is a probability distribution over its keys
+    S = 256
+    assert np.allclose(f["AP"].sum(axis=-1), 1.0, atol=1e-5)
+    if causal:
+        assert np.all(f["AP"][..., np.triu(np.ones((S, S), dtype=bool), 1)] == 0.0)
+    ba, bf = backward(a, inp["dO"], p), backward(f, inp["dO"], p)
+    for k in ("dX", "dWqkv", "dWo"):
+        assert np.abs(ba[k] - bf[k]).max() <= 1e-5 * np.abs(ba[k]).max(), k
+    assert ba["events"] == [] and bf["events"] == []
