@@ -34,10 +34,11 @@ constexpr int NT = 256;  // threads per workgroup: 4 waves as 2 (M) x 2 (N)
 // being held in scalar registers from the kernel's start.
 __device__ __forceinline__ const GemmDesc& desc_reload() {
 #if defined(__HIP_DEVICE_COMPILE__)
-  const GemmDesc* gp =
-      reinterpret_cast<const GemmDesc*>(__builtin_amdgcn_kernarg_segment_ptr());
+  // the copy stays in the constant address space, so the fields are read
+  // with scalar loads
+  auto gp = __builtin_amdgcn_kernarg_segment_ptr();
   asm volatile("" : "+s"(gp));
-  return *gp;
+  return *(const GemmDesc*)gp;
 #else
   return *static_cast<const GemmDesc*>(nullptr);  // the host pass emits no device code
 #endif
