@@ -34,6 +34,7 @@ struct CoordMap {
 // Column-checksum side (paper Sec. 2.3 A^c, carried as extra MFMA rows):
 //   Ac(r,k) fp32, r in [0, 2M/Rm): laid out like A (K-major: r*ldac + k)
 //   Cc(r,n) fp32 optional store of the propagated C^c = A^c B
+// (Rm and Rn, the checksum block sizes, are powers of two.)
 // Row-checksum side (B^r, extra MFMA columns), for columns n >= cr_n_begin:
 //   Br(k,q) fp32, q in [0, 2(N - cr_n_begin)/Rn): laid out like B
 //   Cr(m,q) fp32 optional store of the propagated C^r = A B^r

@@ -436,12 +436,14 @@ struct Gemm {
 
     const bool cc = PROT && g.Ac != nullptr;
     const bool cr = PROT && g.Br != nullptr && n0 >= g.cr_n_begin;
-    const int nc = cc ? 2 * BM / g.Rm : 0;           // checksum rows of this tile
-    const int nq = cr ? 2 * BN / g.Rn : 0;           // checksum cols of this tile
-    const int rc0 = 2 * (m0 / g.Rm);
-    const int qc0 = cr ? 2 * ((n0 - g.cr_n_begin) / g.Rn) : 0;
-    const int nc_valid = cc ? min(nc, 2 * (g.M / g.Rm) - rc0) : 0;
-    const int nq_valid = cr ? min(nq, 2 * ((g.N - g.cr_n_begin) / g.Rn) - qc0) : 0;
+    // checksum block sizes are powers of two (the launch checks): shifts
+    const int lg_rm = __builtin_ctz(g.Rm), lg_rn = __builtin_ctz(g.Rn);
+    const int nc = cc ? 2 * (BM >> lg_rm) : 0;       // checksum rows of this tile
+    const int nq = cr ? 2 * (BN >> lg_rn) : 0;       // checksum cols of this tile
+    const int rc0 = 2 * (m0 >> lg_rm);
+    const int qc0 = cr ? 2 * ((n0 - g.cr_n_begin) >> lg_rn) : 0;
+    const int nc_valid = cc ? min(nc, 2 * (g.M >> lg_rm) - rc0) : 0;
+    const int nq_valid = cr ? min(nq, 2 * ((g.N - g.cr_n_begin) >> lg_rn) - qc0) : 0;
     const float* Ac = cc ? g.Ac + b0 * g.sAc0 + b1 * g.sAc1 : nullptr;
     const float* Br = cr ? g.Br + b0 * g.sBr0 + b1 * g.sBr1 : nullptr;
 
@@ -663,7 +665,7 @@ struct Gemm {
             CsL[((lane >> 4) * 4 + r) * BN + wn * WN + (wm * JS + j) * 16 + fr] = accs[j][r];
         __syncthreads();
         float* Cc = g.Cc + b0 * g.sCc0 + b1 * g.sCc1 + int64_t(kslice) * g.sCck;
-        const int ncb = BM / g.Rm;
+        const int ncb = BM >> __builtin_ctz(g.Rm);
         for (int v = tid; v < ncb * BN; v += NT) {
           const int blk = v / BN, n = v % BN;
           float c1, c2;
@@ -759,7 +761,7 @@ struct Gemm {
     }
     if constexpr (WLC) {
       static_assert(MSUM, "the wave-local check is for protected bf16 tiles");
-      epilogue_wlc(g, tile, A, B, C, z, m0, n0, k_lo, k_hi, cc, cr, rc0, qc0, pk, accs, accr,
+      epilogue_wlc(g, tile, A, B, C, z, b0, b1, m0, n0, k_lo, k_hi, cc, cr, rc0, qc0, pk, accs, accr,
                    reinterpret_cast<float*>(smem + TILE_BYTES), tid);
       return;
     }
@@ -767,8 +769,8 @@ struct Gemm {
 
     // 2. detection (Sec. 2.3 rule): recomputed against propagated checksums
     const int verify = (PROT && cc && !split) ? g.verify : 0;
-    const int nrb = cr ? BN / g.Rn : 0;   // row blocks per tile row
-    const int ncb = cc ? BM / g.Rm : 0;   // column blocks per tile column
+    const int nrb = cr ? BN >> __builtin_ctz(g.Rn) : 0;   // row blocks per tile row
+    const int ncb = cc ? BM >> __builtin_ctz(g.Rm) : 0;   // column blocks per tile column
     if (PROT && (cc || cr)) {
       // 2a. propagated checksums of every vector (strip hi + lo rows), held
       //     in registers until every thread has read the strips; row
@@ -1009,12 +1011,12 @@ struct Gemm {
   // tile with a flagged vector then takes the workgroup through the
   // correction passes and is stored again.
   __device__ static __forceinline__ void epilogue_wlc(
-      const GemmDesc& g, TC* tile, const T* A, const T* B, TC* C, int z, int m0, int n0,
-      int k_lo, int k_hi, bool cc, bool cr, int rc0, int qc0, const uint32_t (&pk)[IM][JN][2],
+      const GemmDesc& g, TC* tile, const T* A, const T* B, TC* C, int z, int b0, int b1, int m0,
+      int n0, int k_lo, int k_hi, bool cc, bool cr, int rc0, int qc0,
+      const uint32_t (&pk)[IM][JN][2],
       const floatx4 (&accs)[JS], const floatx4 (&accr)[IS], float* region, int tid) {
     const int lane = tid & 63, wn = tid >> 6;
     const int fr = lane & 15, g4 = lane >> 4;
-    const int b0 = z / g.nb1, b1 = z % g.nb1;
     constexpr int SEG = MINB;
     const int verify = cc ? g.verify : 0;
     // the wave reads back only what it wrote itself
@@ -1083,7 +1085,7 @@ struct Gemm {
       }
     }
     if (cr && g.Cr != nullptr) {
-      const int nrb = BN / g.Rn;
+      const int nrb = BN >> __builtin_ctz(g.Rn);
       if (g4 < nrb && n0 + g4 * g.Rn < g.N) {
         float* Cr = g.Cr + b0 * g.sCr0 + b1 * g.sCr1;
 #pragma unroll
@@ -1096,7 +1098,7 @@ struct Gemm {
         }
       }
     }
-    const int nrb = (cr && verify == 2) ? BN / g.Rn : 0;  // row blocks per tile row
+    const int nrb = (cr && verify == 2) ? BN >> __builtin_ctz(g.Rn) : 0;  // row blocks per tile row
     if constexpr (WN % SEG == 0) {
       if (nrb > 0) {
         // partial sums of each row over this wave's SEG-column segments:
@@ -1144,7 +1146,7 @@ struct Gemm {
 
     // a flagged vector: the checksums go to LDS in the layout of the
     // correction passes; the workgroup corrects and stores the tile again
-    const int ncb = cc ? BM / g.Rm : 0;
+    const int ncb = cc ? BM >> lg_rm : 0;
     float* ccv = region;
     float* rcv = ccv + CCV;
     int* work = reinterpret_cast<int*>(rcv + RCV);
@@ -1700,6 +1702,8 @@ hipError_t launch_splitk_reduce(const GemmDesc& g, const float* P, const float* 
 
 hipError_t launch_gemm(const GemmDesc& g, int dtype, bool c_fp32, Layout la, Layout lb,
                        Tile tile, hipStream_t stream) {
+  auto pow2 = [](int x) { return x > 0 && (x & (x - 1)) == 0; };
+  if (!pow2(g.Rm) || !pow2(g.Rn)) return hipErrorInvalidValue;  // the kernels shift by them
   const bool prot = g.Ac != nullptr || g.Br != nullptr || g.verify != 0;
   if (dtype == ABFT_FP32) {
     return prot ? launch_layout<float, float, true>(g, la, lb, tile, stream)
