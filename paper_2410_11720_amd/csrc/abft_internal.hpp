@@ -165,6 +165,19 @@ hipError_t launch_verify(void* C, int dtype, int64_t batch, int64_t rows, int64_
 hipError_t launch_report_reset(abft_report* report, int capacity, bool set_capacity,
                                hipStream_t stream);
 
+// Up to two encodes (each as launch_encode) and, when `reset` is given, the
+// report's counters cleared as launch_report_reset(reset, 0, false) does;
+// in one launch when both take the vector path (else one launch each).
+struct EncodeJob {
+  const void* A = nullptr;
+  int64_t batch = 0, rows = 0, cols = 0, ld = 0, batch_stride = 0;
+  int Rb = 0, Cb = 0;
+  float* col_chk = nullptr;
+  float* row_chk = nullptr;
+};
+hipError_t launch_encode_jobs(const EncodeJob* jobs, int n, int dtype, abft_report* reset,
+                              hipStream_t stream);
+
 // Threshold as the storage dtype represents it (round to nearest even).
 float stored_threshold(float t, int dtype);
 

@@ -293,8 +293,6 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
   const int64_t B = d.B, S = d.S, H = d.H, nh = d.nh, hd = d.d, R = d.R, nq = d.nq, T = d.T;
   const size_t es = d.es;
 
-  if (!(cfg->flags & ABFT_FLAG_REPORT_APPEND)) CK(launch_report_reset(report, 0, false, s));
-
   // Checksum operands, each computed when any enabled section consumes it
   // (the backward's propagated checksums come from the forward: X^r for dW,
   // AP^r for dV, CL^r for dWo; a forward that precedes a protected backward
@@ -302,12 +300,26 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
   const bool need_xc = p.sec_as || (p.root && p.sec_cl);  // Q^c, K^c; V root check
   const bool need_vr = p.sec_cl || p.sec_bwd;             // V^r -> CL^r
   const bool need_apc = p.sec_cl || p.sec_o;              // AP^c -> CL^c -> O^c
-  // encode (Sec. 4.6): W^V row checksums per head; X column and row checksums
-  if ((stages & ABFT_STAGE_ENCODE) && need_vr)
-    CK(launch_encode(Wc + 2 * H * es, dt, 1, H, H, 3 * H, 0, 32, int(hd), nullptr, F(L.wvr), s));
-  if ((stages & ABFT_STAGE_ENCODE) && (need_xc || p.sec_bwd))
-    CK(launch_encode(X, dt, B, S, H, H, S * H, int(R), int(hd), need_xc ? F(L.xc) : nullptr,
-                     p.sec_bwd ? F(L.xr) : nullptr, s));
+  // encode (Sec. 4.6): W^V row checksums per head; X column and row
+  // checksums; the report is cleared in the same launch
+  {
+    EncodeJob jobs[2];
+    int nj = 0;
+    if ((stages & ABFT_STAGE_ENCODE) && need_vr) {
+      EncodeJob& e = jobs[nj++];
+      e.A = Wc + 2 * H * es; e.batch = 1; e.rows = H; e.cols = H; e.ld = 3 * H;
+      e.Rb = 32; e.Cb = int(hd); e.row_chk = F(L.wvr);
+    }
+    if ((stages & ABFT_STAGE_ENCODE) && (need_xc || p.sec_bwd)) {
+      EncodeJob& e = jobs[nj++];
+      e.A = X; e.batch = B; e.rows = S; e.cols = H; e.ld = H; e.batch_stride = S * H;
+      e.Rb = int(R); e.Cb = int(hd);
+      e.col_chk = need_xc ? F(L.xc) : nullptr;
+      e.row_chk = p.sec_bwd ? F(L.xr) : nullptr;
+    }
+    CK(launch_encode_jobs(jobs, nj, dt,
+                          (cfg->flags & ABFT_FLAG_REPORT_APPEND) ? nullptr : report, s));
+  }
 
   // [Q|K|V] = X Wqkv
   if (stages & ABFT_STAGE_QKV) {
@@ -448,8 +460,15 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   const size_t es = d.es;
   const bool pb = p.sec_bwd;
 
-  if (!(cfg->flags & ABFT_FLAG_REPORT_APPEND)) CK(launch_report_reset(report, 0, false, s));
-  if ((stages & ABFT_STAGE_ENCODE) && pb) CK(launch_encode(dO, dt, B, S, H, H, S * H, int(R), int(hd), F(L.doc), nullptr, s));
+  // dO^c (Sec. 4.6), with the report cleared in the same launch
+  {
+    EncodeJob e;
+    const int nj = ((stages & ABFT_STAGE_ENCODE) && pb) ? 1 : 0;
+    e.A = dO; e.batch = B; e.rows = S; e.cols = H; e.ld = H; e.batch_stride = S * H;
+    e.Rb = int(R); e.Cb = int(hd); e.col_chk = F(L.doc);
+    CK(launch_encode_jobs(&e, nj, dt, (cfg->flags & ABFT_FLAG_REPORT_APPEND) ? nullptr : report,
+                          s));
+  }
 
   // after a fused forward: AP (and AP^r) regenerated from Q, K and the
   // softmax statistics the forward saved

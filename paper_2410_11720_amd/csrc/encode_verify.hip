@@ -46,14 +46,13 @@ __device__ __forceinline__ void load_vec(const T* p, float* out) {
 // are reduced across the Cb/V lanes that hold it (consecutive lanes share
 // a row), which needs Cb/V a power of two dividing CPS.
 template <class T, int V, int CPS>
-__global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, int64_t cols,
-                                                    int64_t ld, int64_t bstride, int Rb, int Cb,
-                                                    float* col_chk, float* row_chk) {
+__device__ __forceinline__ void encode_block(const T* A, int64_t rows, int64_t cols, int64_t ld,
+                                             int64_t bstride, int Rb, int Cb, float* col_chk,
+                                             float* row_chk, int64_t bx, int64_t rb, int64_t b) {
   constexpr int RG = NT / CPS, W = CPS * V;
   __shared__ float part[RG][W][2];
   const int c = threadIdx.x % CPS, g = threadIdx.x / CPS;
-  const int64_t b = blockIdx.z, rb = blockIdx.y;
-  const int64_t c0 = int64_t(blockIdx.x) * W + c * V;
+  const int64_t c0 = bx * W + c * V;
   const bool live = c0 < cols;
   const T* base = A + b * bstride + rb * Rb * ld;
   const int lanes = Cb / V;
@@ -108,12 +107,58 @@ __global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, in
     }
     __syncthreads();
     const int col = threadIdx.x % W, which = threadIdx.x / W;  // 2W <= NT threads
-    if (threadIdx.x < 2 * W && int64_t(blockIdx.x) * W + col < cols) {
+    if (threadIdx.x < 2 * W && bx * W + col < cols) {
       float acc = 0.f;
       for (int q = 0; q < RG; ++q) acc += part[q][col][which];
-      col_chk[((b * (rows / Rb) + rb) * 2 + which) * cols + int64_t(blockIdx.x) * W + col] = acc;
+      col_chk[((b * (rows / Rb) + rb) * 2 + which) * cols + bx * W + col] = acc;
     }
   }
+}
+
+template <class T, int V, int CPS>
+__global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, int64_t cols,
+                                                    int64_t ld, int64_t bstride, int Rb, int Cb,
+                                                    float* col_chk, float* row_chk) {
+  encode_block<T, V, CPS>(A, rows, cols, ld, bstride, Rb, Cb, col_chk, row_chk, blockIdx.x,
+                          blockIdx.y, blockIdx.z);
+}
+
+__device__ __forceinline__ void clear_counters(abft_report* rep) {
+  rep->n_events = 0;
+  rep->n_corrected = 0;
+  rep->n_uncorrectable = 0;
+  rep->overflow = 0;
+}
+
+// Up to two encodes in one launch (a one-dimensional grid, the first job's
+// workgroups first), and optionally the report's counters cleared by the
+// first workgroup: nothing in an encode records events, and the kernels
+// after it in the stream start once it has finished.
+struct EncJob {
+  const void* A;
+  int64_t rows, cols, ld, bs;
+  int Rb, Cb;
+  float* col_chk;
+  float* row_chk;
+  unsigned gx, gy, nblk;  // workgroups: gx column slabs x gy row blocks x batch
+};
+
+template <class T, int V, int CPS>
+__device__ __forceinline__ void encode_job(const EncJob& j, unsigned id) {
+  const unsigned bx = id % j.gx, by = (id / j.gx) % j.gy, bz = id / (j.gx * j.gy);
+  encode_block<T, V, CPS>(static_cast<const T*>(j.A), j.rows, j.cols, j.ld, j.bs, j.Rb, j.Cb,
+                          j.col_chk, j.row_chk, bx, by, bz);
+}
+
+template <class T, int V, int CPS>
+__global__ __launch_bounds__(NT) void encode_jobs_kernel(EncJob j0, EncJob j1,
+                                                         abft_report* reset) {
+  const unsigned id = blockIdx.x;
+  if (reset != nullptr && id == 0 && threadIdx.x == 0) clear_counters(reset);
+  if (id < j0.nblk)
+    encode_job<T, V, CPS>(j0, id);
+  else
+    encode_job<T, V, CPS>(j1, id - j0.nblk);
 }
 
 // Row checksums for block widths the lane-group reduction cannot cover:
@@ -272,10 +317,7 @@ __global__ __launch_bounds__(NT) void verify_kernel(T* C, int64_t rows, int64_t 
 
 __global__ void report_reset_kernel(abft_report* rep, int capacity, int set_capacity) {
   if (threadIdx.x == 0) {
-    rep->n_events = 0;
-    rep->n_corrected = 0;
-    rep->n_uncorrectable = 0;
-    rep->overflow = 0;
+    clear_counters(rep);
     if (set_capacity) {
       rep->capacity = capacity;
       rep->reserved[0] = rep->reserved[1] = rep->reserved[2] = 0;
@@ -294,6 +336,78 @@ hipError_t launch_encode(const void* A, int dtype, int64_t batch, int64_t rows, 
                            Cb, col_chk, row_chk, s);
   return encode_t<bf16_t>(static_cast<const bf16_t*>(A), batch, rows, cols, ld, batch_stride, Rb,
                           Cb, col_chk, row_chk, s);
+}
+
+namespace {
+// The single-launch form applies when every job takes the vector path with
+// its row checksums inline and the same slab width.
+template <class T>
+bool job_of(const EncodeJob& e, EncJob& j, int& cps) {
+  constexpr int VV = 16 / sizeof(T);
+  const bool aligned = (reinterpret_cast<uintptr_t>(e.A) % 16 == 0) && (e.ld % VV == 0) &&
+                       (e.cols % VV == 0) && (e.batch_stride % VV == 0);
+  if (!aligned || (e.col_chk == nullptr && e.row_chk == nullptr)) return false;
+  cps = 8;
+  if (e.row_chk != nullptr) {
+    if (e.Cb % VV != 0) return false;
+    const int l = e.Cb / VV;
+    if ((l & (l - 1)) != 0 || l > 16) return false;
+    cps = l > 8 ? 16 : 8;
+  }
+  const int64_t W = int64_t(cps) * VV;
+  const int64_t gx = (e.cols + W - 1) / W, gy = e.rows / e.Rb, n = gx * gy * e.batch;
+  if (n <= 0 || n > (int64_t(1) << 30)) return false;
+  j = EncJob{e.A, e.rows, e.cols, e.ld, e.batch_stride, e.Rb, e.Cb, e.col_chk, e.row_chk,
+             unsigned(gx), unsigned(gy), unsigned(n)};
+  return true;
+}
+
+template <class T>
+hipError_t encode_jobs_t(const EncodeJob* jobs, int n, abft_report* reset, hipStream_t s) {
+  EncJob j[2] = {};
+  int cps[2] = {8, 8};
+  bool one = n >= 1 && n <= 2;
+  for (int i = 0; one && i < n; ++i) one = job_of<T>(jobs[i], j[i], cps[i]);
+  if (one && n == 2 && cps[0] != cps[1]) one = false;
+  if (!one) {  // separate launches
+    if (reset != nullptr) {
+      hipError_t e = launch_report_reset(reset, 0, false, s);
+      if (e != hipSuccess) return e;
+    }
+    for (int i = 0; i < n; ++i) {
+      const EncodeJob& e = jobs[i];
+      hipError_t r = launch_encode(e.A, sizeof(T) == 4 ? ABFT_FP32 : ABFT_BF16, e.batch, e.rows,
+                                   e.cols, e.ld, e.batch_stride, e.Rb, e.Cb, e.col_chk,
+                                   e.row_chk, s);
+      if (r != hipSuccess) return r;
+    }
+    return hipSuccess;
+  }
+  constexpr int VV = 16 / sizeof(T);
+  const unsigned total = j[0].nblk + (n == 2 ? j[1].nblk : 0u);
+  if (cps[0] == 8)
+    hipLaunchKernelGGL((encode_jobs_kernel<T, VV, 8>), dim3(total), dim3(NT), 0, s, j[0], j[1],
+                       reset);
+  else
+    hipLaunchKernelGGL((encode_jobs_kernel<T, VV, 16>), dim3(total), dim3(NT), 0, s, j[0], j[1],
+                       reset);
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_encode_jobs(const EncodeJob* jobs, int n, int dtype, abft_report* reset,
+                              hipStream_t s) {
+  // empty operands encode nothing
+  EncodeJob live[2];
+  int m = 0;
+  for (int i = 0; i < n; ++i)
+    if (jobs[i].batch > 0 && jobs[i].rows > 0 && jobs[i].cols > 0) {
+      if (m == 2) return hipErrorInvalidValue;
+      live[m++] = jobs[i];
+    }
+  if (m == 0) return reset != nullptr ? launch_report_reset(reset, 0, false, s) : hipSuccess;
+  if (dtype == ABFT_FP32) return encode_jobs_t<float>(live, m, reset, s);
+  return encode_jobs_t<bf16_t>(live, m, reset, s);
 }
 
 hipError_t launch_verify(void* C, int dtype, int64_t batch, int64_t rows, int64_t cols,
