@@ -1487,32 +1487,34 @@ hipError_t launch_layout(const GemmDesc& g, Layout la, Layout lb, Tile tile, hip
 }
 
 // Split-K reduction fused with the column check. One workgroup owns a
-// block of RB rows (the checksum block, Rm rows, when verifying) and 64
-// columns; thread (c, q) sums the K slices of column c for rows q, q+4, ...
-// in a fixed order (deterministic), keeps the block in LDS and accumulates
-// the column's sum and magnitude sum. The four partials of a column are
-// combined in LDS; its checksums are the fixed-order sums of the slices'
-// checksum rows. A flagged column runs EEC-ABFT (Sec. 4.2) on the LDS block
+// block of RB rows (the checksum block, Rm rows, when verifying) and 32
+// columns; each thread sums the K slices of one float4 column quad for
+// every 32nd row of the block in a fixed order (deterministic), keeps the
+// block in LDS and accumulates the columns' sums and magnitude sums. The
+// row groups' partials of a column are combined in LDS; its checksums are
+// the fixed-order sums of the slices' checksum rows. A flagged column runs EEC-ABFT (Sec. 4.2) on the LDS block
 // with recompute correction and the final check; then the block is stored.
-constexpr int RED_COLS = 64;   // columns per workgroup (16 float4 quads)
-constexpr int RED_GROUPS = 16; // row groups per workgroup
+constexpr int RED_CQ = 8;  // float4 quads per workgroup row piece (more workgroups than 16)
 
-// RPT rows per thread (block of RB = 16 RPT rows), KS slices; both fixed at
-// compile time so that every load of a thread is in flight at once.
-template <class T, bool AK, bool BKM, int RPT, int KS>
+// CQ quads (RED_COLS = 4 CQ columns) per workgroup, 256 / CQ row groups,
+// RPT rows per thread (block of RB rows), KS slices; all fixed at compile
+// time so that every load of a thread is in flight at once.
+template <class T, bool AK, bool BKM, int RPT, int KS, int CQ>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const float* P,
                                                             const float* Pc, int verify) {
+  constexpr int RED_COLS = 4 * CQ, RED_GROUPS = 256 / CQ;
+  constexpr int SG = 256 / RED_COLS;                // slice groups of the checksum rows
   constexpr int RB = RPT * RED_GROUPS;
   __shared__ float blk[RB * RED_COLS];              // the reduced block
   __shared__ float p1[RED_GROUPS * RED_COLS], p2[RED_GROUPS * RED_COLS];
-  __shared__ float pc[2][4][RED_COLS];              // checksum partials per slice group
-  const int cq = threadIdx.x % 16, rg = threadIdx.x / 16;
+  __shared__ float pc[2][SG][RED_COLS];             // checksum partials per slice group
+  const int cq = threadIdx.x % CQ, rg = threadIdx.x / CQ;
   const int c0 = cq * 4, n = blockIdx.x * RED_COLS + c0;
   const int rb = blockIdx.y, m_base = rb * RB;
   const int64_t MN = int64_t(g.M) * g.N;
   const bool col_ok = n < g.N;  // N % 4 == 0: a quad is all in or all out
 
-  // checksum rows of the slices: thread (c, sg) sums slices sg, sg+4, ...
+  // checksum rows of the slices: thread (c, sg) sums slices sg, sg+SG, ...
   const bool chk = verify && m_base + RB <= g.M;
   if (chk) {
     const int c = threadIdx.x % RED_COLS, sg = threadIdx.x / RED_COLS;
@@ -1521,7 +1523,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
     const int ncc = min(nc, g.N - 1);  // loads stay unconditional (see below)
     float a1 = 0.f, a2 = 0.f;
 #pragma unroll
-    for (int sl = sg; sl < KS; sl += 4) {
+    for (int sl = sg; sl < KS; sl += SG) {
       a1 += Pc[sl * slc + int64_t(2 * rb) * g.N + ncc];
       a2 += Pc[sl * slc + int64_t(2 * rb + 1) * g.N + ncc];
     }
@@ -1594,8 +1596,12 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
       s1 += p1[q * RED_COLS + c];
       s2 += p2[q * RED_COLS + c];
     }
-    c1 = (pc[0][0][c] + pc[0][1][c]) + (pc[0][2][c] + pc[0][3][c]);
-    const float c2 = (pc[1][0][c] + pc[1][1][c]) + (pc[1][2][c] + pc[1][3][c]);
+    float c2 = 0.f;
+#pragma unroll
+    for (int q = 0; q < SG && q < KS; ++q) {
+      c1 += pc[0][q][c];
+      c2 += pc[1][q][c];
+    }
     if (flagged(c1 - s1, s2, g.e_rel)) {
       flag[c] = 1;
       float* col = blk + c;
@@ -1659,10 +1665,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
 template <class T, int RPT, int KS>
 hipError_t reduce_launch(const GemmDesc& g, const float* P, const float* Pc, int verify,
                          hipStream_t s) {
-  constexpr int RB = RPT * RED_GROUPS;
+  constexpr int RED_COLS = 4 * RED_CQ, RB = RPT * (256 / RED_CQ);
   dim3 grid((g.N + RED_COLS - 1) / RED_COLS, (g.M + RB - 1) / RB);
-  hipLaunchKernelGGL((splitk_reduce_kernel<T, false, false, RPT, KS>), grid, dim3(256), 0, s, g,
-                     P, Pc, verify);
+  hipLaunchKernelGGL((splitk_reduce_kernel<T, false, false, RPT, KS, RED_CQ>), grid, dim3(256), 0,
+                     s, g, P, Pc, verify);
   return hipGetLastError();
 }
 
@@ -1684,11 +1690,13 @@ hipError_t reduce_t(const GemmDesc& g, const float* P, const float* Pc, Layout l
   if (la != Layout::MNMajor || lb != Layout::MNMajor) return hipErrorInvalidValue;
   if (g.ldc < g.N || g.N % 4 != 0 || g.ldc % 4 != 0) return hipErrorInvalidValue;
   const int verify = (g.verify >= 1 && g.Ac != nullptr && Pc != nullptr) ? 1 : 0;
-  // the checksum block is the row block (16 or 8 rows per thread group)
+  // the checksum block is the row block
   const int RB = verify ? g.Rm : 64;
   if (verify && g.M % RB != 0) return hipErrorInvalidValue;
-  if (RB == 64) return reduce_ks<T, 4>(g, P, Pc, verify, s);
-  if (RB == 128) return reduce_ks<T, 8>(g, P, Pc, verify, s);
+  constexpr int RG = 256 / RED_CQ;  // row groups
+  static_assert(64 % RG == 0, "a 64-row block covers the row groups");
+  if (RB == 64) return reduce_ks<T, 64 / RG>(g, P, Pc, verify, s);
+  if (RB == 128) return reduce_ks<T, 128 / RG>(g, P, Pc, verify, s);
   return hipErrorInvalidValue;  // head dimensions 64 and 128 only
 }
 
