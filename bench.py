@@ -59,8 +59,8 @@ MULTI_KERNEL = {"encode", "dWo", "dWqkv"}
 # share one instantiation and differ by grid
 KERNEL_OF_STAGE = {
     "qkv": ("gemm_kernel<unsigned short, unsigned short, true, false, 128, 128, true, 2, true>", 1152),
-    "softmax_bwd": ("softmax_kernel<unsigned short, 2, true, 1, true>", 768),
-    "softmax": ("softmax_kernel<unsigned short, 2, false, 1, true>", 768),
+    "softmax_bwd": ("softmax_kernel<unsigned short, 2, true, 1, true, true>", 768),
+    "softmax": ("softmax_kernel<unsigned short, 2, false, 1, true, true>", 768),
     "score": ("gemm_kernel<unsigned short, unsigned short, true, true, 128, 128, true, 1, true>", 3456),
 }
 

@@ -104,8 +104,9 @@ __device__ __forceinline__ void round_chunk(float (&x)[4], uint4& bits) {
 }
 
 // CH: 16-byte chunks per lane per row (S <= 64 * CH * VEC); RPI rows per
-// iteration per wave; PF: prefetch the next iteration's rows.
-template <class T, int CH, bool BWD, int RPI, bool PF>
+// iteration per wave; PF: prefetch the next iteration's rows; CHK: encode
+// the checksums (some of col_chk, row_chk given).
+template <class T, int CH, bool BWD, int RPI, bool PF, bool CHK>
 __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   constexpr int V = Vec<T>::N;
   extern __shared__ __align__(16) char smem[];
@@ -158,6 +159,13 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   auto n_live = [&](int j0, int i) {
     return d.causal ? min(V, max(0, i - j0 + 1)) : (j0 < S ? V : 0);
   };
+  // chunk t of row i is live in every lane (inside s_valid and, under the
+  // mask, at or before the diagonal): a wave-uniform test that skips the
+  // per-element selects
+  auto full = [&](int t, int i) {
+    const int hi = 64 * (t + 1) * V;
+    return hi <= s_valid && (!d.causal || hi - 1 <= i);
+  };
   auto process_rows = [&](uint4 (&xr)[RPI][CH], uint4 (&yr)[RPI][CH], int it) {
 #pragma unroll
     for (int u = 0; u < RPI; ++u) {
@@ -169,10 +177,12 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
         const bool in = (lane + 64 * t) * V < s_valid;
         Vec<T>::unpack(xr[u][t], x[t]);
         if (BWD) Vec<T>::unpack(yr[u][t], y[t]);
+        if (!full(t, i)) {
 #pragma unroll
-        for (int e = 0; e < V; ++e) {
-          x[t][e] = in ? x[t][e] : 0.f;
-          if (BWD) y[t][e] = in ? y[t][e] : 0.f;
+          for (int e = 0; e < V; ++e) {
+            x[t][e] = in ? x[t][e] : 0.f;
+            if (BWD) y[t][e] = in ? y[t][e] : 0.f;
+          }
         }
       }
       // chunk t holds data only if 64 t V < s_valid (a wave-uniform test)
@@ -183,12 +193,13 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
           if (64 * t * V >= s_valid) continue;
-          const int nl = n_live((lane + 64 * t) * V, i);
+          if (!full(t, i)) {
+            const int nl = n_live((lane + 64 * t) * V, i);
 #pragma unroll
-          for (int e = 0; e < V; ++e) {
-            x[t][e] = e < nl ? x[t][e] : -INFINITY;
-            mx = fmaxf(mx, x[t][e]);
+            for (int e = 0; e < V; ++e) x[t][e] = e < nl ? x[t][e] : -INFINITY;
           }
+#pragma unroll
+          for (int e = 0; e < V; ++e) mx = fmaxf(mx, x[t][e]);
         }
         mx = wave_max(mx);
         const float mo = -mx * sc;
@@ -213,22 +224,28 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
           if (64 * t * V >= s_valid) continue;
-          const int nl = n_live((lane + 64 * t) * V, i);
+          if (full(t, i)) {
 #pragma unroll
-          for (int e = 0; e < V; ++e) {
-            const float p = fmaf(x[t][e], y[t][e], dot);
-            dot = e < nl ? p : dot;
+            for (int e = 0; e < V; ++e) dot = fmaf(x[t][e], y[t][e], dot);
+          } else {
+            const int nl = n_live((lane + 64 * t) * V, i);
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+              const float p = fmaf(x[t][e], y[t][e], dot);
+              dot = e < nl ? p : dot;
+            }
           }
         }
         dot = wave_sum(dot);
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
           if (64 * t * V >= s_valid) continue;
+          const bool f = full(t, i);
           const int nl = n_live((lane + 64 * t) * V, i);
 #pragma unroll
           for (int e = 0; e < V; ++e) {
             const float v = d.scale * x[t][e] * (y[t][e] - dot);
-            x[t][e] = e < nl ? v : 0.f;
+            x[t][e] = (f || e < nl) ? v : 0.f;
           }
         }
       }
@@ -244,15 +261,17 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
         float r1 = 0.f, rw = 0.f;
         if (j0 < s_valid) {
           *reinterpret_cast<uint4*>(dst + int64_t(i) * S + j0) = bits;
+          if constexpr (CHK) {
 #pragma unroll
-          for (int e = 0; e < V; ++e) {
-            c1[t][e] += x[t][e];
-            c2[t][e] = fmaf(wr, x[t][e], c2[t][e]);
-            r1 += x[t][e];
-            rw = fmaf(float(e), x[t][e], rw);
+            for (int e = 0; e < V; ++e) {
+              c1[t][e] += x[t][e];
+              c2[t][e] = fmaf(wr, x[t][e], c2[t][e]);
+              r1 += x[t][e];
+              rw = fmaf(float(e), x[t][e], rw);
+            }
           }
         }
-        if (d.row_chk != nullptr) {
+        if (CHK && d.row_chk != nullptr) {
           float r2 = fmaf(float((j0 & (R - 1)) + 1), r1, rw);
           kb_sums(r1, r2, lanes_per_kb);
           if ((lane % lanes_per_kb) == 0 && j0 < s_valid) {
@@ -284,7 +303,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   }
 
   // combine the four waves' column checksums in a fixed order
-  if (d.col_chk != nullptr) {
+  if (CHK && d.col_chk != nullptr) {
     for (int w = 0; w < 4; ++w) {
       if (wave == w) {
 #pragma unroll
@@ -319,9 +338,11 @@ hipError_t launch_sm(const SoftmaxDesc& d, int dtype, hipStream_t s) {
   const int ch = (d.S + 64 * V - 1) / (64 * V);
   dim3 grid(unsigned((d.S / d.R) * d.B * d.nh));
   const size_t lds = size_t(d.S) * 2 * sizeof(float);
+  const bool chk = d.col_chk != nullptr || d.row_chk != nullptr;
 #define SM_CASE(TT, CHV)                                                                      \
   if (ch <= CHV) {                                                                            \
-    auto k = softmax_kernel<TT, CHV, BWD, (CHV == 1 ? 2 : 1), (CHV <= 2)>;                    \
+    auto k = chk ? softmax_kernel<TT, CHV, BWD, (CHV == 1 ? 2 : 1), (CHV <= 2), true>         \
+                 : softmax_kernel<TT, CHV, BWD, (CHV == 1 ? 2 : 1), (CHV <= 2), false>;       \
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),                       \
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)); \
     if (e != hipSuccess) return e;                                                            \
