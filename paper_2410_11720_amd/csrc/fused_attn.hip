@@ -79,6 +79,28 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Access to a kernel's descriptor, its only argument. With SEG, through
+// the address of the kernel-argument segment, and refresh() makes that
+// address opaque to the compiler, so fields read after it are loaded
+// (scalar loads) where they are used instead of being held in scalar
+// registers from an earlier read; without, plainly through the argument.
+template <class Desc, bool SEG>
+struct ArgRef {
+  const Desc* p;
+  __device__ explicit ArgRef(const Desc& d) : p(&d) {}
+  __device__ void refresh() {}
+  __device__ const Desc* operator->() const { return p; }
+};
+#if defined(__HIP_DEVICE_COMPILE__)  // the host pass emits no device code
+template <class Desc>
+struct ArgRef<Desc, true> {
+  decltype(__builtin_amdgcn_kernarg_segment_ptr()) p;
+  __device__ explicit ArgRef(const Desc&) : p(__builtin_amdgcn_kernarg_segment_ptr()) {}
+  __device__ void refresh() { asm volatile("" : "+s"(p)); }
+  __device__ const Desc* operator->() const { return (const Desc*)p; }
+};
+#endif
+
 template <int D, bool PROT>
 struct FusedAttn {
   static constexpr int NSTAGE = D == 64 ? 2 : 1;
@@ -126,24 +148,25 @@ struct FusedAttn {
   }
 
   __device__ static void run(const FusedDesc& fd, char* smem) {
+    ArgRef<FusedDesc, D == 64> arg(fd);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lq = lane & 15, g = lane >> 4;
-    const int nqt = fd.S / FT, nbh = fd.B * fd.nh;
+    const int nqt = arg->S / FT, nbh = arg->B * arg->nh;
     const int z = blockIdx.x % nbh;
     // causal: the heaviest query tiles (most key tiles) start first
-    const int qt = fd.causal ? nqt - 1 - int(blockIdx.x) / nbh : int(blockIdx.x) / nbh;
-    const int b = z / fd.nh, h = z % fd.nh;
+    const int qt = arg->causal ? nqt - 1 - int(blockIdx.x) / nbh : int(blockIdx.x) / nbh;
+    const int b = z / arg->nh, h = z % arg->nh;
     const int q0 = qt * FT, qw = q0 + wave * 32;
-    const int S = fd.S, H = fd.H;
+    const int S = arg->S, H = arg->H;
     const int64_t ld = 3 * int64_t(H);
-    const bf16_t* base = static_cast<const bf16_t*>(fd.qkv) + int64_t(b) * S * ld;
+    const bf16_t* base = static_cast<const bf16_t*>(arg->qkv) + int64_t(b) * S * ld;
     const bf16_t* Qp = base + h * D;
     const bf16_t* Kp = base + H + h * D;
     const bf16_t* Vp = base + 2 * H + h * D;
-    const int nkt = fd.causal ? qt + 1 : nqt;
-    const int R = fd.R, NB = FT / R;                  // checksum blocks per key tile
+    const int nkt = arg->causal ? qt + 1 : nqt;
+    const int R = arg->R, NB = FT / R;                  // checksum blocks per key tile
     const int lg_jpb = __builtin_ctz(R / 16);         // 16-key groups per block (log2)
-    const float sl2 = fd.scale * 1.4426950408889634f;
+    const float sl2 = arg->scale * 1.4426950408889634f;
 
     // Q as the B operand of S^T: query qw + 16 qb + lane % 16, dims 32 kk + 8 g..
     bf16x8 qf[2][KS];
@@ -166,7 +189,7 @@ struct FusedAttn {
       for (int im = 0; im < 2; ++im)
         DV::issue(Vp, ld, 0, D, key0 + 64 * im, sb + K_BYTES + im * DV::BYTES, wave, lane);
       if constexpr (PROT) {
-        if (fd.check_as) {
+        if (arg->check_as) {
           const int nqR = S / R;
 #pragma unroll
           for (int p = 0; p < 4; ++p) {
@@ -174,19 +197,19 @@ struct FusedAttn {
             const bool ok = e < NB * 2 * D;
             const int ee = ok ? e : 0;
             const int blk = ee / (2 * D), c = (ee / D) & 1, dd = ee % D;
-            const float v = fd.qkvc[((int64_t(b) * nqR + key0 / R + blk) * 2 + c) * ld + H +
+            const float v = arg->qkvc[((int64_t(b) * nqR + key0 / R + blk) * 2 + c) * ld + H +
                                     h * D + dd];
             kcv[p] = ok ? v : 0.f;
           }
         }
-        if (fd.vr != nullptr)
-          vrv = fd.vr[((int64_t(b) * S + key0 + (tid >> 1)) * fd.nh + h) * 2 + (tid & 1)];
+        if (arg->vr != nullptr)
+          vrv = arg->vr[((int64_t(b) * S + key0 + (tid >> 1)) * arg->nh + h) * 2 + (tid & 1)];
       }
     };
     auto commit = [&](int st) {
       if constexpr (PROT) {
         char* sb = smem + st * STAGE_BYTES;
-        if (fd.check_as) {
+        if (arg->check_as) {
           bf16_t* kcs = reinterpret_cast<bf16_t*>(sb + K_BYTES + V_BYTES);
 #pragma unroll
           for (int p = 0; p < 4; ++p) {
@@ -200,7 +223,7 @@ struct FusedAttn {
             }
           }
         }
-        if (fd.vr != nullptr) {
+        if (arg->vr != nullptr) {
           bf16_t* vrs = reinterpret_cast<bf16_t*>(sb + K_BYTES + V_BYTES + KC_BYTES);
           const bf16_t hi = f2bf(vrv);
           const bf16_t lo = f2bf(vrv - bf2f(hi));
@@ -230,6 +253,10 @@ struct FusedAttn {
 
     if (NSTAGE == 2) issue(0, 0);
     for (int kt = 0; kt < nkt; ++kt) {
+      // with head dim 64 the descriptor's fields are loaded per key tile
+      // (fewer scalar registers held across the loop); with 128 that costs
+      // more vector registers than it saves
+      arg.refresh();
       const int st = NSTAGE == 2 ? (kt & 1) : 0;
       if (NSTAGE == 1) issue(kt, 0);
       wait_vmcnt<0>();
@@ -257,7 +284,7 @@ struct FusedAttn {
             s[j][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][kk], s[j][qb], 0, 0, 0);
         }
         if constexpr (PROT) {
-          if (fd.check_as) {
+          if (arg->check_as) {
             const bf16_t* kcs = reinterpret_cast<const bf16_t*>(sb + K_BYTES + V_BYTES);
             const bf16x8 sf = *reinterpret_cast<const bf16x8*>(kcs + lq * KCL + 32 * kk + 8 * g);
 #pragma unroll
@@ -268,9 +295,9 @@ struct FusedAttn {
       }
 
       // injected score faults (test-only), on the unrounded scores
-      if (fd.n_faults > 0) {
-        for (int f = 0; f < fd.n_faults; ++f) {
-          const abft_fault ft = fd.faults[f];
+      if (arg->n_faults > 0) {
+        for (int f = 0; f < arg->n_faults; ++f) {
+          const abft_fault ft = arg->faults[f];
           if (ft.op != ABFT_OP_AS || ft.b != b || ft.h != h) continue;
           const int qi = ft.row - qw, ki = ft.col - key0;
           if (qi < 0 || qi >= 32 || ki < 0 || ki >= FT) continue;
@@ -288,7 +315,7 @@ struct FusedAttn {
 
       // row check of S per (query, R-key block)
       if constexpr (PROT) {
-        if (fd.check_as) {
+        if (arg->check_as) {
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb) {
             float sj[8], aj[8];
@@ -319,7 +346,7 @@ struct FusedAttn {
               }
             }
             const float c1 = ks[qb][0] + ks[qb][1];
-            const bool fl = g < NB && flagged(c1 - mine1, minea, fd.e_rel);
+            const bool fl = g < NB && flagged(c1 - mine1, minea, arg->e_rel);
             uint64_t mask = __ballot(fl);
             while (mask) {  // rare: locate and correct inside the wave
               const int L = __builtin_ctzll(mask);
@@ -337,7 +364,7 @@ struct FusedAttn {
               wave_sync_lds();
               if (lane == 0) {
                 const int q = qw + 16 * qb + vq;
-                const EecResult res = eec_locate<float>(scr, 1, R, v1, v2, fd.e_rel, fd.tn_s);
+                const EecResult res = eec_locate<float>(scr, 1, R, v1, v2, arg->e_rel, arg->tn_s);
                 int idx = -1;
                 float nv = 0.f;
                 if (res.status == EEC_LOCATED) {
@@ -345,20 +372,20 @@ struct FusedAttn {
                   const int key = key0 + vb * R + idx;
                   const float old = scr[idx];
                   int action = ABFT_ACT_RECOMPUTE;
-                  if (fd.recompute) {
+                  if (arg->recompute) {
                     float acc = 0.f;
                     for (int dd = 0; dd < D; ++dd)
                       acc = fmaf(bf2f(Qp[int64_t(q) * ld + dd]), bf2f(Kp[int64_t(key) * ld + dd]), acc);
                     nv = acc;
                   } else {
-                    nv = fix_by_checksum<float>(scr, 1, R, idx, v1, res.d1, fd.tc, &action);
+                    nv = fix_by_checksum<float>(scr, 1, R, idx, v1, res.d1, arg->tc, &action);
                   }
                   scr[idx] = nv;
-                  record_event(fd.report, ABFT_OP_AS, b, h, q, key, classify(old, fd.tn_s), action,
+                  record_event(arg->report, ABFT_OP_AS, b, h, q, key, classify(old, arg->tn_s), action,
                                old);
                 }
-                if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, R, v1, fd.e_rel))
-                  record_event(fd.report, ABFT_OP_AS, b, h, q, key0 + vb * R, ABFT_KIND_NONE,
+                if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, R, v1, arg->e_rel))
+                  record_event(arg->report, ABFT_OP_AS, b, h, q, key0 + vb * R, ABFT_KIND_NONE,
                                ABFT_ACT_UNCORRECTABLE, 0.f);
                 scr[R] = __int_as_float(idx);
                 scr[R + 1] = nv;
@@ -382,7 +409,7 @@ struct FusedAttn {
       }
 
       // online softmax, then O^T += V^T P^T (and the V^r rows)
-      const bool diag = fd.causal && kt == qt;
+      const bool diag = arg->causal && kt == qt;
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         const int q = qw + 16 * qb + lq;
@@ -434,7 +461,7 @@ struct FusedAttn {
             o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb], o[db][qb], 0, 0, 0);
         }
         if constexpr (PROT) {
-          if (fd.vr != nullptr) {
+          if (arg->vr != nullptr) {
             const bf16_t* vrs =
                 reinterpret_cast<const bf16_t*>(sb + K_BYTES + V_BYTES + KC_BYTES);
             const bf16x8 rf = vr_frag(vrs, 32 * t, lane);
@@ -448,20 +475,20 @@ struct FusedAttn {
     }
 
     // CL = O / l: round, check against A^r / l, store
-    bf16_t* CLp = static_cast<bf16_t*>(fd.cl) + int64_t(b) * S * H + h * D;
+    bf16_t* CLp = static_cast<bf16_t*>(arg->cl) + int64_t(b) * S * H + h * D;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       const int q = qw + 16 * qb + lq;
       const float lsum = group4_sum(l[qb]);
       const float inv = 1.f / lsum;
-      if (fd.stats != nullptr && g == 0) {
-        float* st = fd.stats + ((int64_t(b) * fd.nh + h) * S + q) * 2;
+      if (arg->stats != nullptr && g == 0) {
+        float* st = arg->stats + ((int64_t(b) * arg->nh + h) * S + q) * 2;
         st[0] = m[qb];
         st[1] = lsum;
       }
       if constexpr (PROT) {
-        if (fd.vr != nullptr && fd.clr != nullptr && g == 0) {
-          float* cr = fd.clr + ((int64_t(b) * S + q) * fd.nh + h) * 2;
+        if (arg->vr != nullptr && arg->clr != nullptr && g == 0) {
+          float* cr = arg->clr + ((int64_t(b) * S + q) * arg->nh + h) * 2;
           cr[0] = (vra[qb][0] + vra[qb][1]) * inv;
           cr[1] = (vra[qb][2] + vra[qb][3]) * inv;
         }
@@ -471,9 +498,9 @@ struct FusedAttn {
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int r = 0; r < 4; ++r) ov[db][r] = bf2f(f2bf(o[db][qb][r] * inv));
-      if (fd.n_faults > 0) {
-        for (int f = 0; f < fd.n_faults; ++f) {
-          const abft_fault ft = fd.faults[f];
+      if (arg->n_faults > 0) {
+        for (int f = 0; f < arg->n_faults; ++f) {
+          const abft_fault ft = arg->faults[f];
           if (ft.op != ABFT_OP_CL || ft.b != b || ft.h != h || ft.row != q) continue;
           const int dd = ft.col;
 #pragma unroll
@@ -486,7 +513,7 @@ struct FusedAttn {
         }
       }
       if constexpr (PROT) {
-        if (fd.check_cl) {
+        if (arg->check_cl) {
           // the four lanes of the query take its checksums from lane group 0
           const float c1 = __shfl((vra[qb][0] + vra[qb][1]) * inv, lq, 64);
           const float c2 = __shfl((vra[qb][2] + vra[qb][3]) * inv, lq, 64);
@@ -500,7 +527,7 @@ struct FusedAttn {
             }
           r1 = group4_sum(r1);
           ra = group4_sum(ra);
-          uint64_t mask = __ballot(g == 0 && flagged(c1 - r1, ra, fd.e_rel));
+          uint64_t mask = __ballot(g == 0 && flagged(c1 - r1, ra, arg->e_rel));
           while (mask) {
             const int L = __builtin_ctzll(mask);
             mask &= mask - 1;
@@ -514,20 +541,20 @@ struct FusedAttn {
             wave_sync_lds();
             if (lane == 0) {
               const int qq = qw + 16 * qb + L;
-              const EecResult res = eec_locate<float>(scr, 1, D, v1, v2, fd.e_rel, fd.tn_cl);
+              const EecResult res = eec_locate<float>(scr, 1, D, v1, v2, arg->e_rel, arg->tn_cl);
               int idx = -1;
               float nv = 0.f;
               if (res.status == EEC_LOCATED) {
                 idx = res.index;
                 const float old = scr[idx];
                 int action = 0;
-                nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, D, idx, v1, res.d1, fd.tc, &action)));
+                nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, D, idx, v1, res.d1, arg->tc, &action)));
                 scr[idx] = nv;
-                record_event(fd.report, ABFT_OP_CL, b, h, qq, idx, classify(old, fd.tn_cl), action,
+                record_event(arg->report, ABFT_OP_CL, b, h, qq, idx, classify(old, arg->tn_cl), action,
                              old);
               }
-              if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, D, v1, fd.e_rel))
-                record_event(fd.report, ABFT_OP_CL, b, h, qq, 0, ABFT_KIND_NONE,
+              if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, D, v1, arg->e_rel))
+                record_event(arg->report, ABFT_OP_CL, b, h, qq, 0, ABFT_KIND_NONE,
                              ABFT_ACT_UNCORRECTABLE, 0.f);
               scr[D] = __int_as_float(idx);
               scr[D + 1] = nv;
