@@ -13,10 +13,12 @@ unprotected, the dominant kernel's roofline fraction measured with HIP
 events, and the CPU oracle timed on a bounded sample on the host.
 
 Profiling helpers (they run committed code only):
-  --pmc-workload        launch the dominant kernel and a plain copy of known
-                        size, for `rocprofv3 --pmc FETCH_SIZE` / `WRITE_SIZE`
+  --pmc-workload        launch the largest kernels (QKV projection, score
+                        GEMM, softmax forward and backward) and a plain copy
+                        of known size, for `rocprofv3 --pmc FETCH_SIZE` /
+                        `WRITE_SIZE`
   --summarize DIR...    print a short summary of rocprofv3 result databases
-  --traffic-from F W    HBM bytes per launch of the dominant kernel from the
+  --traffic-from F W    HBM bytes per launch of those kernels from the
                         FETCH_SIZE (F) and WRITE_SIZE (W) runs, scaled by the
                         counters' reading for the reference copy
 """
@@ -39,7 +41,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 COPY_BYTES = 256 << 20      # reference copy for the counter scale factor
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic_gpt2_causal_B8_S1024.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_gpt2_causal_B8_S1024.md")
 
 
 def useful_flops(B, S, H, nh, causal, backward=True):
@@ -58,10 +60,10 @@ MULTI_KERNEL = {"encode", "dWo", "dWqkv"}
 # (kernel symbol, grid size in workgroups): the QKV and output projections
 # share one instantiation and differ by grid
 KERNEL_OF_STAGE = {
-    "qkv": ("gemm_kernel<unsigned short, unsigned short, true, false, 128, 128, true, 2, true>", 1152),
+    "qkv": ("gemm_kernel<unsigned short, unsigned short, true, false, 128, 128, true, 2, true, true>", 1152),
     "softmax_bwd": ("softmax_kernel<unsigned short, 2, true, 1, true, true>", 768),
     "softmax": ("softmax_kernel<unsigned short, 2, false, 1, true, true>", 768),
-    "score": ("gemm_kernel<unsigned short, unsigned short, true, true, 128, 128, true, 1, true>", 3456),
+    "score": ("gemm_kernel<unsigned short, unsigned short, true, true, 128, 128, true, 1, true, true>", 3456),
 }
 
 
@@ -93,17 +95,22 @@ def stage_table(B, S, H, nh, causal, es=2):
     ]
 
 
-# the sources a GEMM kernel is built from: counters taken on other
+# the sources each kernel family is built from: counters taken on other
 # versions of them are stale
-GEMM_SOURCES = ("paper_2410_11720_amd/csrc/gemm_abft.hip", "paper_2410_11720_amd/csrc/direct_lds.hpp",
-                "paper_2410_11720_amd/csrc/abft_device.hpp", "paper_2410_11720_amd/csrc/abft_internal.hpp",
-                "include/attn_abft.h")
+_COMMON_SOURCES = ("paper_2410_11720_amd/csrc/abft_device.hpp",
+                   "paper_2410_11720_amd/csrc/abft_internal.hpp", "include/attn_abft.h")
+KERNEL_SOURCES = {
+    "gemm_kernel": ("paper_2410_11720_amd/csrc/gemm_abft.hip",
+                    "paper_2410_11720_amd/csrc/direct_lds.hpp") + _COMMON_SOURCES,
+    "softmax_kernel": ("paper_2410_11720_amd/csrc/softmax_abft.hip",) + _COMMON_SOURCES,
+}
 
 
-def kernel_source_hash():
-    """Hash of the sources the GEMM kernels are built from."""
+def kernel_source_hash(symbol):
+    """Hash of the sources the kernel `symbol` is built from."""
+    files = KERNEL_SOURCES[symbol.split("<")[0]]
     h = hashlib.sha256()
-    for f in GEMM_SOURCES:
+    for f in files:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(os.path.basename(f).encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
@@ -119,8 +126,8 @@ def stored_traffic(kernel):
         return None
     for m in re.finditer(r"^traffic_json: (\{.*\})$", text, re.M):
         rec = json.loads(m.group(1))
-        if (rec.get("source_hash") == kernel_source_hash() and rec.get("kernel") == kernel[0]
-                and rec.get("grid") == kernel[1]):
+        if (rec.get("kernel") == kernel[0] and rec.get("grid") == kernel[1]
+                and rec.get("source_hash") == kernel_source_hash(kernel[0])):
             return rec
     return None
 
@@ -204,17 +211,17 @@ class Layer:
 
 
 def pmc_workload(key, reps):
-    """Launches for the traffic counters: the checksum encode the QKV
-    projection reads, `reps` launches of the QKV projection, `reps` of the
-    score GEMM (the only launches of their kernels here), then `reps` plain
-    copies of COPY_BYTES (reads and writes COPY_BYTES each)."""
+    """Launches for the traffic counters: one protected step (a consistent
+    workspace), then `reps` launches each of the QKV projection, the score
+    GEMM, the softmax forward and the softmax backward, then `reps` plain
+    copies of COPY_BYTES (reads and writes COPY_BYTES each). The step also
+    launches these kernels once; the per-launch means cover both."""
     L = Layer(key)
     torch = L.torch
-    L.run_stage(0x001, False)       # encode X^c, W^V r
-    for _ in range(reps):
-        L.run_stage(0x002, False)   # QKV projection
-    for _ in range(reps):
-        L.run_stage(0x004, False)   # score GEMM
+    L.step(L.lay_p, None)
+    for mask, is_bwd in ((0x002, False), (0x004, False), (0x008, False), (0x020, True)):
+        for _ in range(reps):
+            L.run_stage(mask, is_bwd)
     src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda").normal_()
     dst = torch.empty_like(src)
     for _ in range(reps):
@@ -266,7 +273,7 @@ def summarize(dirs):
         print(f"{short_name(k[0])} | grid={k[1]} | {vals}")
 
 
-def traffic_from(fetch_dir, write_dir, stages=("qkv", "score")):
+def traffic_from(fetch_dir, write_dir, stages=("qkv", "score", "softmax", "softmax_bwd")):
     """HBM bytes per launch of the stages' kernels (symbol, grid) from a
     FETCH_SIZE and a WRITE_SIZE run of --pmc-workload, each counter scaled
     by what it reads for the reference copy (COPY_BYTES in, COPY_BYTES
@@ -290,7 +297,7 @@ def traffic_from(fetch_dir, write_dir, stages=("qkv", "score")):
         kw = pick(w, lambda n, gr: n == sym and gr in (grid, 0))
         fetch = kf["FETCH_SIZE"] * 1024.0 * s_fetch
         write = kw["WRITE_SIZE"] * 1024.0 * s_write
-        rec = {"kernel": sym, "grid": grid, "source_hash": kernel_source_hash(),
+        rec = {"kernel": sym, "grid": grid, "source_hash": kernel_source_hash(sym),
                "fetch_kib": round(kf["FETCH_SIZE"], 1), "write_kib": round(kw["WRITE_SIZE"], 1),
                "copy_fetch_kib": round(cf["FETCH_SIZE"], 1),
                "copy_write_kib": round(cw["WRITE_SIZE"], 1),
