@@ -110,7 +110,7 @@ template <class T, int CH, bool BWD, int RPI, bool PF, bool CHK>
 __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   constexpr int V = Vec<T>::N;
   extern __shared__ __align__(16) char smem[];
-  float* colacc = reinterpret_cast<float*>(smem);  // [S][2]
+  float* colacc = reinterpret_cast<float*>(smem);  // [8][S]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // One-dimensional grid, (batch, head) fastest: consecutive workgroups go
@@ -139,17 +139,20 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   // loads of iteration it + 1 are issued before iteration it is computed
   // (two register buffers, the loop unrolled by two so that buffer indices
   // stay compile-time constants).
-  // Loads are unconditional (a chunk past s_valid reads the row's last
-  // valid chunk instead and is zeroed when unpacked), so every load of an
-  // iteration is in flight at once: a load under a divergent branch would
-  // make the compiler wait for it at the branch's join.
+  // Loads are unconditional (a chunk past s_valid, or under the causal
+  // mask wholly past the diagonal, reads the row's chunk holding the
+  // diagonal instead, an address another lane of the same load reads, and
+  // is zeroed or masked when unpacked), so every load of an iteration is
+  // in flight at once: a load under a divergent branch would make the
+  // compiler wait for it at the branch's join.
   auto load_rows = [&](uint4 (&x)[RPI][CH], uint4 (&y)[RPI][CH], int it) {
 #pragma unroll
     for (int u = 0; u < RPI; ++u) {
       const int i = qb * R + wave + 4 * (it * RPI + u);
+      const int last = d.causal ? min(s_valid - V, i / V * V) : s_valid - V;
 #pragma unroll
       for (int t = 0; t < CH; ++t) {
-        const int jc = min((lane + 64 * t) * V, s_valid - V);
+        const int jc = min((lane + 64 * t) * V, last);
         x[u][t] = *reinterpret_cast<const uint4*>(src + int64_t(i) * S + jc);
         if (BWD) y[u][t] = *reinterpret_cast<const uint4*>(src2 + int64_t(i) * S + jc);
       }
@@ -302,32 +305,27 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
     }
   }
 
-  // combine the four waves' column checksums in a fixed order
+  // combine the four waves' column checksums in a fixed order: each wave's
+  // partials go to a slab of its own, then every thread sums the four
+  // slabs for its columns
   if (CHK && d.col_chk != nullptr) {
-    for (int w = 0; w < 4; ++w) {
-      if (wave == w) {
+    float* p1 = colacc;          // [4][S]
+    float* p2 = colacc + 4 * S;  // [4][S]
 #pragma unroll
-        for (int t = 0; t < CH; ++t)
+    for (int t = 0; t < CH; ++t)
 #pragma unroll
-          for (int e = 0; e < V; ++e) {
-            const int j = (lane + 64 * t) * V + e;
-            if (j < s_valid) {
-              if (w == 0) {
-                colacc[2 * j] = c1[t][e];
-                colacc[2 * j + 1] = c2[t][e];
-              } else {
-                colacc[2 * j] += c1[t][e];
-                colacc[2 * j + 1] += c2[t][e];
-              }
-            }
-          }
+      for (int e = 0; e < V; ++e) {
+        const int j = (lane + 64 * t) * V + e;
+        if (j < s_valid) {
+          p1[wave * S + j] = c1[t][e];
+          p2[wave * S + j] = c2[t][e];
+        }
       }
-      __syncthreads();
-    }
+    __syncthreads();
     float* cc = d.col_chk + (int64_t(z) * nq + qb) * 2 * S;
     for (int j = tid; j < s_valid; j += NT) {
-      cc[j] = colacc[2 * j];
-      cc[S + j] = colacc[2 * j + 1];
+      cc[j] = ((p1[j] + p1[S + j]) + p1[2 * S + j]) + p1[3 * S + j];
+      cc[S + j] = ((p2[j] + p2[S + j]) + p2[2 * S + j]) + p2[3 * S + j];
     }
   }
 }
@@ -337,7 +335,7 @@ hipError_t launch_sm(const SoftmaxDesc& d, int dtype, hipStream_t s) {
   const int V = dtype == ABFT_FP32 ? 4 : 8;
   const int ch = (d.S + 64 * V - 1) / (64 * V);
   dim3 grid(unsigned((d.S / d.R) * d.B * d.nh));
-  const size_t lds = size_t(d.S) * 2 * sizeof(float);
+  const size_t lds = size_t(d.S) * 8 * sizeof(float);
   const bool chk = d.col_chk != nullptr || d.row_chk != nullptr;
 #define SM_CASE(TT, CHV)                                                                      \
   if (ch <= CHV) {                                                                            \
