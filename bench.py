@@ -643,6 +643,17 @@ def main():
     if tr:
         roof["traffic_split"] = {"fetch": tr["fetch_bytes"], "write": tr["write_bytes"]}
 
+    # roofline model of the step: each stage at its bound's peak (flops at
+    # the MFMA peak, bytes at the HBM peak), summed, over the measured
+    # fault-free protected step; and each stage's own fraction of its peak
+    model_s, stage_frac = 0.0, {}
+    for s_name, s_kind, s_amount, s_us in stages:
+        t = s_amount / (PEAK_BF16_TFLOPS * 1e12) if s_kind == "flop" else s_amount / (PEAK_HBM_GBS * 1e9)
+        model_s += t
+        stage_frac[s_name] = round(t / (s_us * 1e-6), 4)
+    roofline_model = {"model_us": round(model_s * 1e6, 2), "measured_us": round(ms_clean * 1e3, 2),
+                      "frac": round(model_s * 1e3 / ms_clean, 4)}
+
     def pct(a):
         return {"p10": round(float(np.percentile(a, 10)), 4),
                 "p50": round(float(np.percentile(a, 50)), 4),
@@ -676,6 +687,8 @@ def main():
         "check": {"faults_injected": f0[1], "corrected": corrected, "uncorrectable": uncorrectable},
         "roofline": roof,
         "stages_us": {s[0]: round(s[3], 2) for s in stages},
+        "stages_frac_of_peak": stage_frac,
+        "roofline_model": roofline_model,
         "adaptive_frequencies": adaptive,
         "recovery": recovery,
         "fused_forward": fused,

@@ -1056,18 +1056,53 @@ struct Gemm {
     // store this wave's part: 16-byte chunks, WN / 8 lanes per row piece
     constexpr int V = 16 / sizeof(TC), CPW = WN / V;
     static_assert((WM * CPW) % 64 == 0, "whole wave passes");
+    const int nrb = (cr && verify == 2) ? BN >> __builtin_ctz(g.Rn) : 0;  // row blocks per tile row
+    // with four chunks per row piece (WN = 4 V) and whole SEG-column
+    // segments, pass i stores rows 16 i + lane % 16 (lane group g4: chunk
+    // g4), and the same 16 bytes are the B operand of the row sums of a
+    // two-sided output: one LDS read for both
+    constexpr bool ROWS_IN_STORE = WN == 4 * V && WN == SEG;
+    if constexpr (ROWS_IN_STORE) {
+      const bf16x8 ones = __builtin_bit_cast(
+          bf16x8, uint4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+      const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+      float2* part = reinterpret_cast<float2*>(region);  // [BN / SEG][BM]
 #pragma unroll
-    for (int q = 0; q < WM * CPW / 64; ++q) {
-      const int c = lane + q * 64;
-      const int row = c / CPW, col = wn * WN + (c % CPW) * V;
-      const int m = m0 + row, n = n0 + col;
-      if (m < g.M) {
+      for (int i = 0; i < IM; ++i) {
+        const int row = i * 16 + fr, col = wn * WN + g4 * V;
+        const int m = m0 + row, n = n0 + col;
         const TC* srcp = tile + row * LDT + col;
-        TC* dstp = C + int64_t(m) * g.ldc + n;
-        if (n + V <= g.N) {
-          *reinterpret_cast<uint4*>(dstp) = *reinterpret_cast<const uint4*>(srcp);
-        } else {
-          for (int e = 0; e < V && n + e < g.N; ++e) dstp[e] = srcp[e];
+        const uint4 u = *reinterpret_cast<const uint4*>(srcp);
+        if (m < g.M) {
+          TC* dstp = C + int64_t(m) * g.ldc + n;
+          if (n + V <= g.N) {
+            *reinterpret_cast<uint4*>(dstp) = u;
+          } else {
+            for (int e = 0; e < V && n + e < g.N; ++e) dstp[e] = srcp[e];
+          }
+        }
+        if (nrb > 0) {
+          const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu,
+                            u.w & 0x7fff7fffu};
+          const floatx4 sm = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, u), zero);
+          const floatx4 mg = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, ua), zero);
+          if (g4 == 0) part[wn * BM + i * 16 + fr] = float2{sm[0], mg[0]};
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < WM * CPW / 64; ++q) {
+        const int c = lane + q * 64;
+        const int row = c / CPW, col = wn * WN + (c % CPW) * V;
+        const int m = m0 + row, n = n0 + col;
+        if (m < g.M) {
+          const TC* srcp = tile + row * LDT + col;
+          TC* dstp = C + int64_t(m) * g.ldc + n;
+          if (n + V <= g.N) {
+            *reinterpret_cast<uint4*>(dstp) = *reinterpret_cast<const uint4*>(srcp);
+          } else {
+            for (int e = 0; e < V && n + e < g.N; ++e) dstp[e] = srcp[e];
+          }
         }
       }
     }
@@ -1098,29 +1133,32 @@ struct Gemm {
         }
       }
     }
-    const int nrb = (cr && verify == 2) ? BN >> __builtin_ctz(g.Rn) : 0;  // row blocks per tile row
     if constexpr (WN % SEG == 0) {
       if (nrb > 0) {
         // partial sums of each row over this wave's SEG-column segments:
         // the staged rows as the B operand (column = row lane % 16, 8
         // consecutive columns per lane group), so every lane gets a row sum
+        // (taken with the store above when the wave's columns are one
+        // segment)
         constexpr int TS = WN / SEG;                 // segments per wave
         float2* part = reinterpret_cast<float2*>(region);  // [BN / SEG][BM]
-        const bf16x8 ones = __builtin_bit_cast(
-            bf16x8, uint4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
-        const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (!ROWS_IN_STORE) {
+          const bf16x8 ones = __builtin_bit_cast(
+              bf16x8, uint4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+          const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int i = 0; i < IM; ++i)
+          for (int i = 0; i < IM; ++i)
 #pragma unroll
-          for (int t = 0; t < TS; ++t) {
-            const uint4 u = *reinterpret_cast<const uint4*>(
-                tile + (i * 16 + fr) * LDT + wn * WN + t * SEG + 8 * g4);
-            const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu,
-                              u.w & 0x7fff7fffu};
-            const floatx4 sm = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, u), zero);
-            const floatx4 mg = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, ua), zero);
-            if (g4 == 0) part[(wn * TS + t) * BM + i * 16 + fr] = float2{sm[0], mg[0]};
-          }
+            for (int t = 0; t < TS; ++t) {
+              const uint4 u = *reinterpret_cast<const uint4*>(
+                  tile + (i * 16 + fr) * LDT + wn * WN + t * SEG + 8 * g4);
+              const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu,
+                                u.w & 0x7fff7fffu};
+              const floatx4 sm = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, u), zero);
+              const floatx4 mg = Mfma<T>::mma(ones, __builtin_bit_cast(bf16x8, ua), zero);
+              if (g4 == 0) part[(wn * TS + t) * BM + i * 16 + fr] = float2{sm[0], mg[0]};
+            }
+        }
         __syncthreads();
         // lane group g4 of the row strip holds row block g4 of rows
         // (IS wn + i) 16 + lane % 16
