@@ -30,6 +30,47 @@ typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) short4_t lds_short4;
 
+// ds_read_b64_tr_b16 as inline assembly. Through the compiler's intrinsic,
+// the read first waits for every outstanding direct-to-LDS load of the
+// wave (vmcnt 0), which serialises the next stage's loads with the
+// compute on the current one (the stage being read is already complete:
+// the loop's own wait and barrier see to that). The compiler does not see
+// this LDS access, so its result is read only after lds_wait_all() and
+// through tr_join(), which redefines it behind the wait.
+__device__ __forceinline__ short4_t ds_read_tr16(const void* p) {
+  short4_t r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"((const lds_short4*)p));
+  return r;
+}
+// Waits for every outstanding LDS access of the wave.
+__device__ __forceinline__ void lds_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Waits until at most the last two LDS accesses of the wave are outstanding
+// (LDS accesses complete in order, so every earlier one is done).
+__device__ __forceinline__ void lds_wait_but2() { asm volatile("s_waitcnt lgkmcnt(2)" ::: "memory"); }
+// The two transposed halves of an MN-major fragment (k rows 0..3 and 4..7
+// of the lane's 8), as read, before the wait.
+struct TrPair {
+  short4_t lo, hi;
+};
+__device__ __forceinline__ TrPair tr_pair(const void* p0, const void* p1) {
+  return TrPair{ds_read_tr16(p0), ds_read_tr16(p1)};
+}
+// The same through the compiler's intrinsic (it waits for the loads into
+// LDS itself; fewer registers where the assembly form spills).
+__device__ __forceinline__ TrPair tr_pair_intrinsic(const void* p0, const void* p1) {
+  return TrPair{__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p0),
+                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p1)};
+}
+// After lds_wait_all(): the fragment. The empty statements redefine both
+// halves behind the wait, so no copy of them is taken before it.
+__device__ __forceinline__ bf16x8 tr_join(TrPair& t) {
+  asm volatile("" : "+v"(t.lo));
+  asm volatile("" : "+v"(t.hi));
+  typedef short short8_t __attribute__((ext_vector_type(8)));
+  const short8_t v = {t.lo[0], t.lo[1], t.lo[2], t.lo[3], t.hi[0], t.hi[1], t.hi[2], t.hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
 template <bool KMAJ, int ROWS, int NT = 256>
 struct Direct {
   static constexpr int BK = 64;
@@ -60,24 +101,23 @@ struct Direct {
   }
 
   // MFMA 16x16x32 operand fragment: rows rb + (lane & 15), k = kk + 8 (lane >> 4) + 0..7
+  // (K-major image: a plain LDS read)
   __device__ static __forceinline__ bf16x8 frag(const char* st, int rb, int kk, int lane) {
-    if constexpr (KMAJ) {
-      const int row = rb + (lane & 15);
-      const int c = (kk >> 3) + (lane >> 4);
-      return *reinterpret_cast<const bf16x8*>(st + row * 128 + ((c ^ (row & 7)) << 4));
-    } else {
-      const int s = lane & 15;
-      const int k = kk + 8 * (lane >> 4) + (s >> 2);
-      const int m = rb + 4 * (s & 3);
-      const int c = m >> 3, off = (m & 7) * 2;
-      const char* p0 = st + k * (ROWS * 2) + ((c ^ (2 * (k & 3))) << 4) + off;
-      const char* p1 = st + (k + 4) * (ROWS * 2) + ((c ^ (2 * ((k + 4) & 3))) << 4) + off;
-      const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p0);
-      const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p1);
-      typedef short short8_t __attribute__((ext_vector_type(8)));
-      const short8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      return __builtin_bit_cast(bf16x8, v);
-    }
+    static_assert(KMAJ, "MN-major fragments: frag_tr, then lds_wait_all and tr_join");
+    const int row = rb + (lane & 15);
+    const int c = (kk >> 3) + (lane >> 4);
+    return *reinterpret_cast<const bf16x8*>(st + row * 128 + ((c ^ (row & 7)) << 4));
+  }
+  // the same fragment from an MN-major image, as two transposing reads
+  __device__ static __forceinline__ TrPair frag_tr(const char* st, int rb, int kk, int lane) {
+    static_assert(!KMAJ, "K-major fragments: frag");
+    const int s = lane & 15;
+    const int k = kk + 8 * (lane >> 4) + (s >> 2);
+    const int m = rb + 4 * (s & 3);
+    const int c = m >> 3, off = (m & 7) * 2;
+    const char* p0 = st + k * (ROWS * 2) + ((c ^ (2 * (k & 3))) << 4) + off;
+    const char* p1 = st + (k + 4) * (ROWS * 2) + ((c ^ (2 * ((k + 4) & 3))) << 4) + off;
+    return tr_pair(p0, p1);
   }
 };
 

@@ -122,29 +122,27 @@ struct FusedAttn {
   // V^T operand fragment for keys {kb + 4g + v, kb + 16 + 4g + v} (g = lane
   // group, v = 0..3), rows (dims) rb + lane % 16: the key order of the P^T
   // fragment a lane assembles from its S^T accumulators.
-  __device__ static __forceinline__ bf16x8 vt_frag(const char* st, int rb, int kb, int lane) {
+  // (transposing reads: valid after lds_wait_all(), through tr_join(); head
+  // dim 128 and the unprotected kernel keep the compiler's intrinsic, which
+  // measured faster there: its own waits cost less than the registers and
+  // coarser waits of the assembly form)
+  __device__ static __forceinline__ TrPair vt_frag(const char* st, int rb, int kb, int lane) {
     const int s = lane & 15, g = lane >> 4;
     const int k1 = kb + 4 * g + (s >> 2), k2 = k1 + 16;
     const int m = rb + 4 * (s & 3);
     const int c = m >> 3, off = (m & 7) * 2;
     const char* p0 = st + k1 * (D * 2) + ((c ^ (2 * (k1 & 3))) << 4) + off;
     const char* p1 = st + k2 * (D * 2) + ((c ^ (2 * (k2 & 3))) << 4) + off;
-    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p0);
-    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p1);
-    typedef short short8_t __attribute__((ext_vector_type(8)));
-    const short8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    return __builtin_bit_cast(bf16x8, v);
+    if constexpr (D == 64 && PROT) return tr_pair(p0, p1);
+    else return tr_pair_intrinsic(p0, p1);
   }
   // (V^r)^T fragment from the plain [128 keys][16] strip, same key order
-  __device__ static __forceinline__ bf16x8 vr_frag(const bf16_t* vrs, int kb, int lane) {
+  __device__ static __forceinline__ TrPair vr_frag(const bf16_t* vrs, int kb, int lane) {
     const int s = lane & 15, g = lane >> 4;
     const int k1 = kb + 4 * g + (s >> 2), k2 = k1 + 16;
     const int m = 4 * (s & 3);
-    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)(vrs + k1 * 16 + m));
-    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)(vrs + k2 * 16 + m));
-    typedef short short8_t __attribute__((ext_vector_type(8)));
-    const short8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    return __builtin_bit_cast(bf16x8, v);
+    if constexpr (D == 64 && PROT) return tr_pair(vrs + k1 * 16 + m, vrs + k2 * 16 + m);
+    else return tr_pair_intrinsic(vrs + k1 * 16 + m, vrs + k2 * 16 + m);
   }
 
   __device__ static void run(const FusedDesc& fd, char* smem) {
@@ -197,9 +195,9 @@ struct FusedAttn {
             const bool ok = e < NB * 2 * D;
             const int ee = ok ? e : 0;
             const int blk = ee / (2 * D), c = (ee / D) & 1, dd = ee % D;
-            const float v = arg->qkvc[((int64_t(b) * nqR + key0 / R + blk) * 2 + c) * ld + H +
-                                    h * D + dd];
-            kcv[p] = ok ? v : 0.f;
+            // (used by commit only where e is in range: no select here, which
+            // would wait for the load, and with it for the tile's loads)
+            kcv[p] = arg->qkvc[((int64_t(b) * nqR + key0 / R + blk) * 2 + c) * ld + H + h * D + dd];
           }
         }
         if (arg->vr != nullptr)
@@ -443,6 +441,10 @@ struct FusedAttn {
       }
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
+        const char* sv = sb + K_BYTES + (t >> 1) * DV::BYTES;
+        // the first V^T read goes out before P is packed; each later one
+        // before the MFMAs of the previous (one read pair in flight)
+        TrPair cur = vt_frag(sv, 0, (t & 1) * 32, lane);
         bf16x8 pf[2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
@@ -452,23 +454,38 @@ struct FusedAttn {
                            pack2(s[2 * t + 1][qb][2], s[2 * t + 1][qb][3])};
           pf[qb] = __builtin_bit_cast(bf16x8, u);
         }
-        const char* sv = sb + K_BYTES + (t >> 1) * DV::BYTES;
+        const bool with_vr = PROT && arg->vr != nullptr;
+        const bf16_t* vrs = reinterpret_cast<const bf16_t*>(sb + K_BYTES + V_BYTES + KC_BYTES);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const bf16x8 vf = vt_frag(sv, 16 * db, (t & 1) * 32, lane);
+          // (head dim 128: no read ahead, for registers)
+          constexpr bool AHEAD = D == 64 && PROT;
+          TrPair nxt = cur;
+          bool more = AHEAD;
+          if (!AHEAD) {
+            if (db > 0) cur = vt_frag(sv, 16 * db, (t & 1) * 32, lane);
+          } else if (db + 1 < DB) {
+            nxt = vt_frag(sv, 16 * (db + 1), (t & 1) * 32, lane);
+          } else if (with_vr) {
+            nxt = vr_frag(vrs, 32 * t, lane);
+          } else {
+            more = false;
+          }
+          if (more) lds_wait_but2();
+          else lds_wait_all();
+          const bf16x8 vf = tr_join(cur);
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb)
             o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb], o[db][qb], 0, 0, 0);
+          cur = nxt;
         }
-        if constexpr (PROT) {
-          if (arg->vr != nullptr) {
-            const bf16_t* vrs =
-                reinterpret_cast<const bf16_t*>(sb + K_BYTES + V_BYTES + KC_BYTES);
-            const bf16x8 rf = vr_frag(vrs, 32 * t, lane);
+        if (with_vr && !(D == 64 && PROT)) cur = vr_frag(vrs, 32 * t, lane);
+        if (with_vr) {
+          lds_wait_all();
+          const bf16x8 rf = tr_join(cur);
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
-              vra[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf[qb], vra[qb], 0, 0, 0);
-          }
+          for (int qb = 0; qb < 2; ++qb)
+            vra[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf[qb], vra[qb], 0, 0, 0);
         }
       }
       if (NSTAGE == 1) __syncthreads();  // the one stage is reloaded next

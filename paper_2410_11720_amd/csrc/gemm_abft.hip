@@ -182,7 +182,10 @@ template <class T, bool KMAJ>
 struct StripLoader {
   static constexpr int BK = Mfma<T>::BK;
   static constexpr int LDK = BK + Mfma<T>::PAD;
-  static constexpr int PER = (16 * BK + NT - 1) / NT;
+  // fp32 source rows a strip can hold: 16 strip rows, two (hi, lo) per
+  // source row for bf16 operands
+  static constexpr int NR = sizeof(T) == 2 ? 8 : 16;
+  static constexpr int PER = (NR * BK + NT - 1) / NT;
   float reg[PER];
 
   // Element e of the strip: consecutive threads walk the contiguous
@@ -190,7 +193,7 @@ struct StripLoader {
   // MN-major one), so the loads coalesce.
   __device__ static void rk(int e, int& r, int& k) {
     if (KMAJ) { r = e / BK; k = e % BK; }
-    else { r = e % 16; k = e / 16; }
+    else { r = e % NR; k = e / NR; }
   }
   // rows r0 + r exist only for r < nvalid (the last tile may be ragged)
   __device__ void load(const float* base, int64_t ld, int r0, int nvalid, int k0, int kend,
@@ -552,10 +555,30 @@ struct Gemm {
 #pragma unroll
           for (int kk = 0; kk < BK; kk += KI) {
             typename Mfma<T>::frag af[IM], bfr[JN];
+            // MN-major images are read with transposing reads that are
+            // waited for together
+            TrPair ap[AK ? 1 : IM], bp[BKM ? 1 : JN];
 #pragma unroll
-            for (int i = 0; i < IM; ++i) af[i] = DA::frag(st, wm * WM + i * 16, kk, lane);
+            for (int i = 0; i < IM; ++i) {
+              if constexpr (AK) af[i] = DA::frag(st, wm * WM + i * 16, kk, lane);
+              else ap[i] = DA::frag_tr(st, wm * WM + i * 16, kk, lane);
+            }
 #pragma unroll
-            for (int j = 0; j < JN; ++j) bfr[j] = DB::frag(st + DA_BYTES, wn * WN + j * 16, kk, lane);
+            for (int j = 0; j < JN; ++j) {
+              if constexpr (BKM) bfr[j] = DB::frag(st + DA_BYTES, wn * WN + j * 16, kk, lane);
+              else bp[j] = DB::frag_tr(st + DA_BYTES, wn * WN + j * 16, kk, lane);
+            }
+            if constexpr (!AK || !BKM) {
+              lds_wait_all();
+              if constexpr (!AK) {
+#pragma unroll
+                for (int i = 0; i < IM; ++i) af[i] = tr_join(ap[i]);
+              }
+              if constexpr (!BKM) {
+#pragma unroll
+                for (int j = 0; j < JN; ++j) bfr[j] = tr_join(bp[j]);
+              }
+            }
             mma_kk(af, bfr, sS, sR, kk);
           }
         };
