@@ -1411,17 +1411,18 @@ struct Gemm {
 
 // Tiles up to 128 x 128 keep two waves per SIMD (at most 256 registers,
 // arch + accumulation, per lane), so two workgroups share a CU; the
-// unprotected one-stage bf16 tile, which has no load in flight while it
-// computes, keeps three (at most 168 registers) to hide its loads behind
-// the other workgroups' work.
-template <class T, int BM, int BN, bool PROT, int NSTAGE>
+// one-stage bf16 tile, which has no load in flight while it computes, keeps
+// three (at most 168 registers) to hide its loads behind the other
+// workgroups' work: unprotected, or protected with the wave-local check on
+// the direct path (a few spills, far cheaper than the lost workgroup).
+template <class T, int BM, int BN, bool PROT, int NSTAGE, bool WLC>
 constexpr int gemm_waves_per_eu() {
-  return BM * BN > 128 * 128 ? 1 : (sizeof(T) == 2 && NSTAGE == 1 && !PROT ? 3 : 2);
+  return BM * BN > 128 * 128 ? 1 : (sizeof(T) == 2 && NSTAGE == 1 && (!PROT || WLC) ? 3 : 2);
 }
 
 template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE, bool DIR,
           bool WLC>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<T, BM, BN, PROT, NSTAGE>())))
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<T, BM, BN, PROT, NSTAGE, WLC && DIR>())))
 void gemm_kernel(GemmDesc g) {
   extern __shared__ __align__(16) char smem[];
   Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, WLC>::template run<DIR>(g, smem);
