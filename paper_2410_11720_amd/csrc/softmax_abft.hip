@@ -127,6 +127,20 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   const T* src2 = BWD ? static_cast<const T*>(d.dAP) + mat : nullptr;
   T* dst = static_cast<T*>(BWD ? d.dAS : d.AP) + mat;
   const int lanes_per_kb = R / V;  // lanes covering one key block
+  // bf16: lane l holds chunk lc = 4 (l % 16) + l / 16 of each 64-chunk run,
+  // so that the A operand of a 16x16x32 MFMA over a run's stored chunks
+  // has row m = 32-key quarter m of the run (lanes m, m+16, m+32, m+48 hold
+  // its four chunks): the row checksums per key block come from one MFMA
+  // per run against a constant [ones | in-quarter index] operand
+  constexpr bool PERM = V == 8;
+  const int lc = PERM ? (lane & 15) * 4 + (lane >> 4) : lane;
+  bf16x8 bsum;
+  if constexpr (PERM) {
+    const int n = lane & 15, gk = lane >> 4;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      bsum[e] = __builtin_bit_cast(__bf16, f2bf(n == 0 ? 1.f : (n == 1 ? float(8 * gk + e) : 0.f)));
+  }
 
   float c1[CH][V], c2[CH][V];
 #pragma unroll
@@ -152,7 +166,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
       const int last = d.causal ? min(s_valid - V, i / V * V) : s_valid - V;
 #pragma unroll
       for (int t = 0; t < CH; ++t) {
-        const int jc = min((lane + 64 * t) * V, last);
+        const int jc = min((lc + 64 * t) * V, last);
         x[u][t] = *reinterpret_cast<const uint4*>(src + int64_t(i) * S + jc);
         if (BWD) y[u][t] = *reinterpret_cast<const uint4*>(src2 + int64_t(i) * S + jc);
       }
@@ -177,7 +191,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
       float x[CH][V], y[CH][V];
 #pragma unroll
       for (int t = 0; t < CH; ++t) {
-        const bool in = (lane + 64 * t) * V < s_valid;
+        const bool in = (lc + 64 * t) * V < s_valid;
         Vec<T>::unpack(xr[u][t], x[t]);
         if (BWD) Vec<T>::unpack(yr[u][t], y[t]);
         if (!full(t, i)) {
@@ -197,7 +211,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
         for (int t = 0; t < CH; ++t) {
           if (64 * t * V >= s_valid) continue;
           if (!full(t, i)) {
-            const int nl = n_live((lane + 64 * t) * V, i);
+            const int nl = n_live((lc + 64 * t) * V, i);
 #pragma unroll
             for (int e = 0; e < V; ++e) x[t][e] = e < nl ? x[t][e] : -INFINITY;
           }
@@ -231,7 +245,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
 #pragma unroll
             for (int e = 0; e < V; ++e) dot = fmaf(x[t][e], y[t][e], dot);
           } else {
-            const int nl = n_live((lane + 64 * t) * V, i);
+            const int nl = n_live((lc + 64 * t) * V, i);
 #pragma unroll
             for (int e = 0; e < V; ++e) {
               const float p = fmaf(x[t][e], y[t][e], dot);
@@ -244,7 +258,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
         for (int t = 0; t < CH; ++t) {
           if (64 * t * V >= s_valid) continue;
           const bool f = full(t, i);
-          const int nl = n_live((lane + 64 * t) * V, i);
+          const int nl = n_live((lc + 64 * t) * V, i);
 #pragma unroll
           for (int e = 0; e < V; ++e) {
             const float v = d.scale * x[t][e] * (y[t][e] - dot);
@@ -258,7 +272,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
 #pragma unroll
       for (int t = 0; t < CH; ++t) {
         if (64 * t * V >= s_valid) continue;
-        const int j0 = (lane + 64 * t) * V;
+        const int j0 = (lc + 64 * t) * V;
         uint4 bits;
         round_chunk(x[t], bits);
         float r1 = 0.f, rw = 0.f;
@@ -269,12 +283,45 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
             for (int e = 0; e < V; ++e) {
               c1[t][e] += x[t][e];
               c2[t][e] = fmaf(wr, x[t][e], c2[t][e]);
-              r1 += x[t][e];
-              rw = fmaf(float(e), x[t][e], rw);
+              if constexpr (!PERM) {
+                r1 += x[t][e];
+                rw = fmaf(float(e), x[t][e], rw);
+              }
             }
           }
         }
-        if (CHK && d.row_chk != nullptr) {
+        if constexpr (PERM) {
+          if (CHK && d.row_chk != nullptr) {
+            // D[m][0] = sum of quarter m, D[m][1] = its in-quarter weighted
+            // sum; lane (n, g) holds rows 4g..4g+3 of column n, lane n = 1's
+            // column reaches lane n = 0 by a pair swap
+            const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+            const floatx4 dq =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bits), bsum, zero, 0, 0, 0);
+            floatx4 dw;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dw[r] = dpp_mov<DPP_XOR1>(dq[r]);
+            if ((lane & 15) == 0) {
+              const int gq = lane >> 4;
+              float b1 = 0.f, b2 = 0.f;
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int q0 = 64 * t * V + 128 * gq + 32 * r;  // first key of the quarter
+                const int pos = q0 & (R - 1);                    // its offset in the block
+                b1 += dq[r];
+                b2 += dw[r] + float(pos + 1) * dq[r];
+                if (((q0 + 32) & (R - 1)) == 0) {  // the block ends with this quarter
+                  if (q0 - pos < s_valid) {
+                    float* rc = d.row_chk + ((int64_t(z) * S + i) * nq + (q0 - pos) / R) * 2;
+                    rc[0] = b1;
+                    rc[1] = b2;
+                  }
+                  b1 = b2 = 0.f;
+                }
+              }
+            }
+          }
+        } else if (CHK && d.row_chk != nullptr) {
           float r2 = fmaf(float((j0 & (R - 1)) + 1), r1, rw);
           kb_sums(r1, r2, lanes_per_kb);
           if ((lane % lanes_per_kb) == 0 && j0 < s_valid) {
@@ -315,7 +362,7 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
     for (int t = 0; t < CH; ++t)
 #pragma unroll
       for (int e = 0; e < V; ++e) {
-        const int j = (lane + 64 * t) * V + e;
+        const int j = (lc + 64 * t) * V + e;
         if (j < s_valid) {
           p1[wave * S + j] = c1[t][e];
           p2[wave * S + j] = c2[t][e];
