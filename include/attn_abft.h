@@ -181,7 +181,11 @@ int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wq
  *   dO [batch, seq, hidden] (device, dtype); X, Wqkv, Wo as in forward;
  *   workspace: the one the forward filled (its backward scratch is reused);
  *   dX [batch, seq, hidden] (device, dtype); dWqkv [hidden, 3*hidden] and
- *   dWo [hidden, hidden] (device, fp32). */
+ *   dWo [hidden, hidden] (device, fp32).
+ * The weight gradients run on a second stream of the device (created on
+ * first use, default priority), forked from and joined back into `stream`
+ * with events: all work of the call is ordered before later work on
+ * `stream`, as for a single stream (also under graph capture). */
 int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* X,
                        const void* Wqkv, const void* Wo, void* workspace,
                        size_t workspace_bytes, void* dX, float* dWqkv, float* dWo,
