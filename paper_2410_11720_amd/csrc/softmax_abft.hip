@@ -257,12 +257,16 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
           if (64 * t * V >= s_valid) continue;
-          const bool f = full(t, i);
-          const int nl = n_live((lc + 64 * t) * V, i);
+          if (full(t, i)) {  // wave-uniform: no per-element select
 #pragma unroll
-          for (int e = 0; e < V; ++e) {
-            const float v = d.scale * x[t][e] * (y[t][e] - dot);
-            x[t][e] = (f || e < nl) ? v : 0.f;
+            for (int e = 0; e < V; ++e) x[t][e] = d.scale * x[t][e] * (y[t][e] - dot);
+          } else {
+            const int nl = n_live((lc + 64 * t) * V, i);
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+              const float v = d.scale * x[t][e] * (y[t][e] - dot);
+              x[t][e] = e < nl ? v : 0.f;
+            }
           }
         }
       }
