@@ -198,14 +198,15 @@ class Layer:
         lay.backward(self.dO, self.X, self.Wqkv, self.Wo, faults, dX=self.dX, dWqkv=self.dWqkv,
                      dWo=self.dWo)
 
-    def run_stage(self, mask, is_bwd):
-        a, lay = self.abft, self.lay_p
+    def run_stage(self, mask, is_bwd, protect=True):
+        a = self.abft
+        cfg, lay = (self.cfg_p, self.lay_p) if protect else (self.cfg_u, self.lay_u)
         if is_bwd:
-            a.attn_abft_backward_stages(self.cfg_p, self.dO, self.X, self.Wqkv, self.Wo,
+            a.attn_abft_backward_stages(cfg, self.dO, self.X, self.Wqkv, self.Wo,
                                         lay.workspace, self.dX, self.dWqkv, self.dWo, None, 0,
                                         lay.report_bwd, mask, self.stream, append=True)
         else:
-            a.attn_abft_forward_stages(self.cfg_p, self.X, self.Wqkv, self.Wo, self.O,
+            a.attn_abft_forward_stages(cfg, self.X, self.Wqkv, self.Wo, self.O,
                                        lay.workspace, None, 0, lay.report, mask, self.stream,
                                        append=True)
 
@@ -604,18 +605,23 @@ def main():
     corrected = rf["n_corrected"] + rb["n_corrected"]
     uncorrectable = rf["n_uncorrectable"] + rb["n_uncorrectable"]
 
-    # per-stage kernel durations with HIP events on the launch stream
-    stages = []
-    for name, is_bwd, mask, kind, amount in stage_table(B, S, H, nh, shape.causal):
-        L.run_stage(mask, is_bwd)
+    # per-stage kernel durations with HIP events on the launch stream, for
+    # the protected layer and (same kernels, checks off) the unprotected one
+    def stage_us(mask, is_bwd, protect):
+        L.run_stage(mask, is_bwd, protect)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(L.stream)
         for _ in range(args.stage_reps):
-            L.run_stage(mask, is_bwd)
+            L.run_stage(mask, is_bwd, protect)
         e1.record(L.stream)
         e1.synchronize()
-        us = e0.elapsed_time(e1) * 1e3 / args.stage_reps
-        stages.append((name, kind, amount, us))
+        return e0.elapsed_time(e1) * 1e3 / args.stage_reps
+
+    L.step(L.lay_u, None)
+    stages, stages_unprot = [], {}
+    for name, is_bwd, mask, kind, amount in stage_table(B, S, H, nh, shape.causal):
+        stages.append((name, kind, amount, stage_us(mask, is_bwd, True)))
+        stages_unprot[name] = round(stage_us(mask, is_bwd, False), 2)
     # restore a consistent workspace after the stage runs
     L.step(L.lay_p, (None, 0))
     torch.cuda.synchronize()
@@ -687,6 +693,7 @@ def main():
         "check": {"faults_injected": f0[1], "corrected": corrected, "uncorrectable": uncorrectable},
         "roofline": roof,
         "stages_us": {s[0]: round(s[3], 2) for s in stages},
+        "stages_us_unprotected": stages_unprot,
         "stages_frac_of_peak": stage_frac,
         "roofline_model": roofline_model,
         "adaptive_frequencies": adaptive,

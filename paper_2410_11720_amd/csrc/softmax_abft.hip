@@ -188,19 +188,14 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
     for (int u = 0; u < RPI; ++u) {
       const int rl = wave + 4 * (it * RPI + u);
       const int i = qb * R + rl;
+      // keys a chunk holds past s_valid, or past the diagonal, are the
+      // masked tail of its live prefix (n_live), which is all that the
+      // arithmetic below masks
       float x[CH][V], y[CH][V];
 #pragma unroll
       for (int t = 0; t < CH; ++t) {
-        const bool in = (lc + 64 * t) * V < s_valid;
         Vec<T>::unpack(xr[u][t], x[t]);
         if (BWD) Vec<T>::unpack(yr[u][t], y[t]);
-        if (!full(t, i)) {
-#pragma unroll
-          for (int e = 0; e < V; ++e) {
-            x[t][e] = in ? x[t][e] : 0.f;
-            if (BWD) y[t][e] = in ? y[t][e] : 0.f;
-          }
-        }
       }
       // chunk t holds data only if 64 t V < s_valid (a wave-uniform test)
       if (!BWD) {
@@ -236,35 +231,38 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
 #pragma unroll
           for (int e = 0; e < V; ++e) x[t][e] *= inv;
       } else {
-        // dAS = scale * AP * (dAP - D), D = sum_j AP_j dAP_j over live keys
+        // dAS = scale * AP * (dAP - D), D = sum_j AP_j dAP_j over live keys;
+        // masked keys are zeroed in both operands (so that they add nothing
+        // to D whatever they hold) and in the result (exactly zero even
+        // when D is not finite)
         float dot = 0.f;
+#pragma unroll
+        for (int t = 0; t < CH; ++t) {
+          if (64 * t * V >= s_valid) continue;
+          if (!full(t, i)) {  // wave-uniform: full chunks skip the selects
+            const int nl = n_live((lc + 64 * t) * V, i);
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+              x[t][e] = e < nl ? x[t][e] : 0.f;
+              y[t][e] = e < nl ? y[t][e] : 0.f;
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < V; ++e) dot = fmaf(x[t][e], y[t][e], dot);
+        }
+        dot = wave_sum(dot);
+        const float nsd = -d.scale * dot;
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
           if (64 * t * V >= s_valid) continue;
           if (full(t, i)) {
 #pragma unroll
-            for (int e = 0; e < V; ++e) dot = fmaf(x[t][e], y[t][e], dot);
+            for (int e = 0; e < V; ++e) x[t][e] *= fmaf(y[t][e], d.scale, nsd);
           } else {
             const int nl = n_live((lc + 64 * t) * V, i);
 #pragma unroll
             for (int e = 0; e < V; ++e) {
-              const float p = fmaf(x[t][e], y[t][e], dot);
-              dot = e < nl ? p : dot;
-            }
-          }
-        }
-        dot = wave_sum(dot);
-#pragma unroll
-        for (int t = 0; t < CH; ++t) {
-          if (64 * t * V >= s_valid) continue;
-          if (full(t, i)) {  // wave-uniform: no per-element select
-#pragma unroll
-            for (int e = 0; e < V; ++e) x[t][e] = d.scale * x[t][e] * (y[t][e] - dot);
-          } else {
-            const int nl = n_live((lc + 64 * t) * V, i);
-#pragma unroll
-            for (int e = 0; e < V; ++e) {
-              const float v = d.scale * x[t][e] * (y[t][e] - dot);
+              const float v = x[t][e] * fmaf(y[t][e], d.scale, nsd);
               x[t][e] = e < nl ? v : 0.f;
             }
           }
