@@ -109,6 +109,9 @@ struct SoftmaxDesc {
   void* dAS = nullptr;        // [B,nh,S,S] bwd output
   float* col_chk = nullptr;   // [B,nh,S/R,2,S] of the produced matrix (may be null)
   float* row_chk = nullptr;   // [B,nh,S,S/R,2] of the produced matrix (may be null)
+  // CUs per XCD of the device (set by the launcher; 0 keeps the plain
+  // workgroup order)
+  int xcd_cus = 0;
 };
 hipError_t launch_softmax_fwd(const SoftmaxDesc& d, int dtype, hipStream_t stream);
 hipError_t launch_softmax_bwd(const SoftmaxDesc& d, int dtype, hipStream_t stream);

@@ -14,6 +14,8 @@
 // checksums accumulate in registers. Masked entries (key > query under a
 // causal mask) are selected to zero; keys past the end of the score tile
 // that holds the diagonal are neither read nor written.
+#include <atomic>
+
 #include "abft_internal.hpp"
 #include "abft_device.hpp"
 
@@ -118,7 +120,21 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   // block costs; under a causal mask the longest query blocks come first.
   const int S = d.S, R = d.R;
   const int nq = S / R, nbh = d.B * d.nh;
-  const int z = blockIdx.x % nbh, r = blockIdx.x / nbh;
+  // Under a causal mask block costs differ up to nq times, and at these
+  // sizes the whole grid is resident at once: workgroups are dealt
+  // round-robin to the 8 XCDs and then to the CUs of each XCD, so the CU
+  // that takes arrival slot m of its XCD also takes slots m + n, m + 2n, ...
+  // (n CUs per XCD). Taking the cost order forwards in even rounds and
+  // backwards in odd ones (a snake deal) evens out the CUs' sums; the
+  // remap swaps pairs of workgroups inside a round, so it is a bijection
+  // for any grid.
+  int bid = blockIdx.x;
+  if (d.causal && d.xcd_cus > 0) {
+    const int n = d.xcd_cus, x = bid & 7, m = bid >> 3, rd = m / n, c = m - rd * n;
+    const int t = 8 * (rd * n + ((rd & 1) ? n - 1 - c : c)) + x;
+    if (t < int(gridDim.x)) bid = t;
+  }
+  const int z = bid % nbh, r = bid / nbh;
   const int qb = d.causal ? nq - 1 - r : r;
   const int s_valid =
       d.causal ? min(S, ((qb + 1) * R + d.kv_align - 1) / d.kv_align * d.kv_align) : S;
@@ -379,8 +395,30 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   }
 }
 
+// CUs per XCD of the current device (8 XCDs), read once per device
+int xcd_cus() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    v = cus / 8 > 0 ? cus / 8 : -1;
+    cache[dev].store(v, std::memory_order_relaxed);
+  }
+  return v > 0 ? v : 0;
+}
+
 template <bool BWD>
-hipError_t launch_sm(const SoftmaxDesc& d, int dtype, hipStream_t s) {
+hipError_t launch_sm(const SoftmaxDesc& desc, int dtype, hipStream_t s) {
+  // the backward's block cost follows its bytes (qb + 1 key tiles), which
+  // the snake deal evens out; the forward's follows its VALU work per
+  // 512-key chunk, which the plain order already spreads as evenly (and
+  // measures faster)
+  SoftmaxDesc d = desc;
+  d.xcd_cus = BWD ? xcd_cus() : 0;
   const int V = dtype == ABFT_FP32 ? 4 : 8;
   const int ch = (d.S + 64 * V - 1) / (64 * V);
   dim3 grid(unsigned((d.S / d.R) * d.B * d.nh));
