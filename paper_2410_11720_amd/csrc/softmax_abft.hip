@@ -114,7 +114,9 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   extern __shared__ __align__(16) char smem[];
   float* colacc = reinterpret_cast<float*>(smem);  // [8][S]
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform over the wave: row indices and row
+  // addresses stay in scalar registers
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // One-dimensional grid, (batch, head) fastest: consecutive workgroups go
   // to different XCDs, so every XCD gets whole heads and the same mix of
   // block costs; under a causal mask the longest query blocks come first.
@@ -166,9 +168,8 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
 
   const float l2e = 1.4426950408889634f;
   // Rows of this wave: rl = wave + 4 * (it * RPI + u), u < RPI. With PF the
-  // loads of iteration it + 1 are issued before iteration it is computed
-  // (two register buffers, the loop unrolled by two so that buffer indices
-  // stay compile-time constants).
+  // loads of iteration it + 1 are issued once iteration it's loaded values
+  // are unpacked, before it is computed (one register buffer).
   // Loads are unconditional (a chunk past s_valid, or under the causal
   // mask wholly past the diagonal, reads the row's chunk holding the
   // diagonal instead, an address another lane of the same load reads, and
@@ -199,20 +200,68 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
     const int hi = 64 * (t + 1) * V;
     return hi <= s_valid && (!d.causal || hi - 1 <= i);
   };
+  const int n_it = R / (4 * RPI);
+  // With PF an iteration's stores (the output chunks and, for R = 128, the
+  // row checksum pairs) are issued in the next iteration, after its wait:
+  // the compiler's wait for loaded data also drains every store in flight,
+  // so stores issued just before a wait would stall it.
+  uint4 pb[RPI][CH];
+  float2 prc[RPI][CH];
+  const bool rc_late = PF && PERM && CHK && R == 128 && d.row_chk != nullptr;
+  auto flush = [&](int it) {
+#pragma unroll
+    for (int u = 0; u < RPI; ++u) {
+      const int i = qb * R + wave + 4 * (it * RPI + u);
+#pragma unroll
+      for (int t = 0; t < CH; ++t) {
+        if (64 * t * V >= s_valid) continue;
+        const int j0 = (lc + 64 * t) * V;
+        if (j0 < s_valid) *reinterpret_cast<uint4*>(dst + int64_t(i) * S + j0) = pb[u][t];
+        const int k0 = 64 * t * V + 128 * (lane >> 4);
+        if (rc_late && (lane & 15) == 0 && k0 < s_valid)
+          *reinterpret_cast<float2*>(d.row_chk + ((int64_t(z) * S + i) * nq + k0 / 128) * 2) =
+              prc[u][t];
+      }
+    }
+  };
   auto process_rows = [&](uint4 (&xr)[RPI][CH], uint4 (&yr)[RPI][CH], int it) {
+    // keys a chunk holds past s_valid, or past the diagonal, are the
+    // masked tail of its live prefix (n_live), which is all that the
+    // arithmetic below masks
+    float xs[RPI][CH][V], ys[RPI][CH][V];
+#pragma unroll
+    for (int u = 0; u < RPI; ++u)
+#pragma unroll
+      for (int t = 0; t < CH; ++t) {
+        Vec<T>::unpack(xr[u][t], xs[u][t]);
+        if (BWD) Vec<T>::unpack(yr[u][t], ys[u][t]);
+      }
+    if constexpr (PF) {
+      // The load registers are free once unpacked: the next iteration's
+      // loads go out now and run during this iteration's arithmetic. The
+      // empty statements pin that order (the wait for this iteration's
+      // data, which also drains the stores still in flight, comes first;
+      // a load hoisted above it would be waited for at once).
+#pragma unroll
+      for (int u = 0; u < RPI; ++u)
+#pragma unroll
+        for (int t = 0; t < CH; ++t)
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            asm volatile("" : "+v"(xs[u][t][e]));
+            if (BWD) asm volatile("" : "+v"(ys[u][t][e]));
+          }
+      asm volatile("" ::: "memory");
+      if (it + 1 < n_it) load_rows(xr, yr, it + 1);
+      if (it > 0) flush(it - 1);
+    }
 #pragma unroll
     for (int u = 0; u < RPI; ++u) {
       const int rl = wave + 4 * (it * RPI + u);
       const int i = qb * R + rl;
-      // keys a chunk holds past s_valid, or past the diagonal, are the
-      // masked tail of its live prefix (n_live), which is all that the
-      // arithmetic below masks
-      float x[CH][V], y[CH][V];
-#pragma unroll
-      for (int t = 0; t < CH; ++t) {
-        Vec<T>::unpack(xr[u][t], x[t]);
-        if (BWD) Vec<T>::unpack(yr[u][t], y[t]);
-      }
+      float* const rc_row = d.row_chk + (int64_t(z) * S + i) * nq * 2;  // [S / R][2] of row i
+      float (&x)[CH][V] = xs[u];
+      float (&y)[CH][V] = ys[u];
       // chunk t holds data only if 64 t V < s_valid (a wave-uniform test)
       if (!BWD) {
         // AP = softmax(scale * AS) over live keys, in base 2
@@ -294,8 +343,9 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
         uint4 bits;
         round_chunk(x[t], bits);
         float r1 = 0.f, rw = 0.f;
+        if constexpr (PF) pb[u][t] = bits;
         if (j0 < s_valid) {
-          *reinterpret_cast<uint4*>(dst + int64_t(i) * S + j0) = bits;
+          if constexpr (!PF) *reinterpret_cast<uint4*>(dst + int64_t(i) * S + j0) = bits;
           if constexpr (CHK) {
 #pragma unroll
             for (int e = 0; e < V; ++e) {
@@ -319,23 +369,35 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
             floatx4 dw;
 #pragma unroll
             for (int r = 0; r < 4; ++r) dw[r] = dpp_mov<DPP_XOR1>(dq[r]);
-            if ((lane & 15) == 0) {
-              const int gq = lane >> 4;
-              float b1 = 0.f, b2 = 0.f;
+            // lane group g = lane / 16 (lane 16 g holds its sums) covers
+            // keys k0 .. k0 + 127: one key block of R = 128, or 128 / R
+            // whole blocks, whose checksum pairs are contiguous in the row's
+            // [S / R][2] record
+            const int k0 = 64 * t * V + 128 * (lane >> 4);
+            if (rc_late) {
+              prc[u][t] = make_float2((dq[0] + dq[1]) + (dq[2] + dq[3]),
+                                      ((dw[0] + dq[0]) + (dw[1] + 33.f * dq[1])) +
+                                          ((dw[2] + 65.f * dq[2]) + (dw[3] + 97.f * dq[3])));
+            } else if ((lane & 15) == 0 && k0 < s_valid) {
+              float q1[4], q2[4];  // per 32-key quarter: sum, weighted sum
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
-                const int q0 = 64 * t * V + 128 * gq + 32 * r;  // first key of the quarter
-                const int pos = q0 & (R - 1);                    // its offset in the block
-                b1 += dq[r];
-                b2 += dw[r] + float(pos + 1) * dq[r];
-                if (((q0 + 32) & (R - 1)) == 0) {  // the block ends with this quarter
-                  if (q0 - pos < s_valid) {
-                    float* rc = d.row_chk + ((int64_t(z) * S + i) * nq + (q0 - pos) / R) * 2;
-                    rc[0] = b1;
-                    rc[1] = b2;
-                  }
-                  b1 = b2 = 0.f;
-                }
+                q1[r] = dq[r];
+                q2[r] = dw[r] + float(((32 * r) & (R - 1)) + 1) * dq[r];
+              }
+              float* rc = rc_row + (k0 / R) * 2;
+              if (R == 128) {
+                *reinterpret_cast<float2*>(rc) =
+                    make_float2((q1[0] + q1[1]) + (q1[2] + q1[3]), (q2[0] + q2[1]) + (q2[2] + q2[3]));
+              } else if (R == 64) {
+                *reinterpret_cast<float2*>(rc) = make_float2(q1[0] + q1[1], q2[0] + q2[1]);
+                if (k0 + 64 < s_valid)
+                  *reinterpret_cast<float2*>(rc + 2) = make_float2(q1[2] + q1[3], q2[2] + q2[3]);
+              } else {  // R == 32
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                  if (k0 + 32 * r < s_valid)
+                    *reinterpret_cast<float2*>(rc + 2 * r) = make_float2(q1[r], q2[r]);
               }
             }
           }
@@ -352,23 +414,13 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
     }
   };
 
-  const int n_it = R / (4 * RPI);
   uint4 xa[RPI][CH], ya[RPI][CH];
-  if constexpr (PF) {
-    uint4 xb[RPI][CH], yb[RPI][CH];
-    load_rows(xa, ya, 0);
-    for (int it = 0; it < n_it; it += 2) {
-      if (it + 1 < n_it) load_rows(xb, yb, it + 1);
-      process_rows(xa, ya, it);
-      if (it + 2 < n_it) load_rows(xa, ya, it + 2);
-      if (it + 1 < n_it) process_rows(xb, yb, it + 1);
-    }
-  } else {
-    for (int it = 0; it < n_it; ++it) {
-      load_rows(xa, ya, it);
-      process_rows(xa, ya, it);
-    }
+  if constexpr (PF) load_rows(xa, ya, 0);
+  for (int it = 0; it < n_it; ++it) {
+    if constexpr (!PF) load_rows(xa, ya, it);
+    process_rows(xa, ya, it);
   }
+  if constexpr (PF) flush(n_it - 1);
 
   // combine the four waves' column checksums in a fixed order: each wave's
   // partials go to a slab of its own, then every thread sums the four
@@ -420,6 +472,10 @@ hipError_t launch_sm(const SoftmaxDesc& desc, int dtype, hipStream_t s) {
   SoftmaxDesc d = desc;
   d.xcd_cus = BWD ? xcd_cus() : 0;
   const int V = dtype == ABFT_FP32 ? 4 : 8;
+  // key blocks: a power of two, whole 16-byte lane chunks, at most one
+  // 128-key lane group (bf16: whole 32-key MFMA quarters)
+  if ((d.R & (d.R - 1)) != 0 || d.R > 128 || d.R < (dtype == ABFT_FP32 ? 16 : 32))
+    return hipErrorInvalidValue;
   const int ch = (d.S + 64 * V - 1) / (64 * V);
   dim3 grid(unsigned((d.S / d.R) * d.B * d.nh));
   const size_t lds = size_t(d.S) * 8 * sizeof(float);
