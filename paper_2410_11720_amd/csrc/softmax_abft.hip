@@ -465,12 +465,8 @@ int xcd_cus() {
 
 template <bool BWD>
 hipError_t launch_sm(const SoftmaxDesc& desc, int dtype, hipStream_t s) {
-  // the backward's block cost follows its bytes (qb + 1 key tiles), which
-  // the snake deal evens out; the forward's follows its VALU work per
-  // 512-key chunk, which the plain order already spreads as evenly (and
-  // measures faster)
   SoftmaxDesc d = desc;
-  d.xcd_cus = BWD ? xcd_cus() : 0;
+  d.xcd_cus = xcd_cus();
   const int V = dtype == ABFT_FP32 ? 4 : 8;
   // key blocks: a power of two, whole 16-byte lane chunks, at most one
   // 128-key lane group (bf16: whole 32-key MFMA quarters)
