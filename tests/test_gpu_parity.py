@@ -143,6 +143,7 @@ SHAPES = [
     W.make_shape(1, 384, 256, 4, causal=True, block_rows=64),  # R = 64, seq not a power of two
     W.make_shape(2, 192, 128, 2, causal=True, block_rows=64),  # seq 192: ragged score tiles
     W.make_shape(1, 256, 64, 1, causal=False, block_rows=32),
+    W.make_shape(1, 320, 64, 1, causal=True, block_rows=32),   # R = 32 causal, seq 320: blocks past it
     W.make_shape(4, 512, 128, 2, causal=True),                 # long K: split-K weight gradients
 ]
 
