@@ -106,13 +106,25 @@ KERNEL_SOURCES = {
 }
 
 
-def kernel_source_hash(symbol):
-    """Hash of the sources the kernel `symbol` is built from."""
+def code_only(text):
+    """Source text without comments and blank lines (what the compiler
+    sees, up to layout): comment edits keep stored counters valid."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = (re.sub(r"//.*$", "", ln).rstrip() for ln in text.split("\n"))
+    return "\n".join(ln for ln in lines if ln.strip())
+
+
+def kernel_source_hash(symbol, read=None):
+    """Hash of the code of the sources the kernel `symbol` is built from
+    (`read(path)` returns a file's text; by default the working tree's)."""
     files = KERNEL_SOURCES[symbol.split("<")[0]]
+    if read is None:
+        def read(f):
+            with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
+                return fh.read()
     h = hashlib.sha256()
     for f in files:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+        h.update(os.path.basename(f).encode() + b"\0" + code_only(read(f)).encode())
     return h.hexdigest()[:16]
 
 

@@ -119,7 +119,8 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // One-dimensional grid, (batch, head) fastest: consecutive workgroups go
   // to different XCDs, so every XCD gets whole heads and the same mix of
-  // block costs; under a causal mask the longest query blocks come first.
+  // block costs; under a causal mask the cost order runs from the longest
+  // query blocks to the shortest.
   const int S = d.S, R = d.R;
   const int nq = S / R, nbh = d.B * d.nh;
   // Under a causal mask block costs differ up to nq times, and at these
@@ -173,9 +174,9 @@ __global__ __launch_bounds__(NT) void softmax_kernel(SoftmaxDesc d) {
   // Loads are unconditional (a chunk past s_valid, or under the causal
   // mask wholly past the diagonal, reads the row's chunk holding the
   // diagonal instead, an address another lane of the same load reads, and
-  // is zeroed or masked when unpacked), so every load of an iteration is
-  // in flight at once: a load under a divergent branch would make the
-  // compiler wait for it at the branch's join.
+  // lies past the live prefix that the arithmetic keeps), so every load of
+  // an iteration is in flight at once: a load under a divergent branch
+  // would make the compiler wait for it at the branch's join.
   auto load_rows = [&](uint4 (&x)[RPI][CH], uint4 (&y)[RPI][CH], int it) {
 #pragma unroll
     for (int u = 0; u < RPI; ++u) {
