@@ -7,9 +7,13 @@ storing the score matrix AS or the probabilities AP: an online-softmax
 The projection before and the output projection after are the layer's
 (`layer.project`, `layer.output_projection`).
 
-Per (batch, head), query tile of TQ = 128 queries and key tile of TK = 128
-keys, key tiles in increasing order (causal: key tiles up to the diagonal):
-  1. S = Q_t K_j^T, not rounded (it is never stored); AS faults are
+Per (batch, head), all queries at once, the keys visited a block at a
+time, in increasing order (the online softmax of Milakov and Gimelshein
+takes its key blocks in any size; by default one checksum block of R keys,
+the unit of the row check of Sec. 4.4). Under a causal mask a query takes
+the keys of the R-key blocks up to its own (the block-lower-triangular
+region at R granularity that the materialised form checks too):
+  1. S = Q K_kb^T, not rounded (it is never stored); AS faults are
      applied to S ("set" writes the value, "flip" flips the exponent MSB of
      S as an fp32 value).
   2. Row check of S (Sec. 4.4 AS^r = Q (K^c)^T, one vector per query and
@@ -22,7 +26,7 @@ keys, key tiles in increasing order (causal: key tiles up to the diagonal):
      p = exp(scale S - m') (masked: 0), alpha = exp(m - m'),
      l = alpha l + sum_j p, P = storage-rounded p,
      A = alpha A + P V_j, A^r = alpha A^r + P V^r_j.
-  4. After the last key tile: CL = rounded A / l; CL faults are applied;
+  4. After the last key block: CL = rounded A / l; CL faults are applied;
      CL^r = A^r / l is the propagated row checksum of CL (V^r = X W^V r,
      Sec. 4.4; the rescaling multiplies A and A^r alike). Row check of CL
      (one vector per query over the head's d columns); a located element
@@ -49,8 +53,6 @@ from .eec import col_checksums, eec_locate, fix_by_checksum, row_checksums
 from .layer import OracleParams, _Run, project, output_projection
 from .numerics import classify, flip_exponent_msb, round_to, stored_threshold
 
-TQ = 128
-TK = 128
 
 
 def _check_rows(v2, c1, c2, e_rel, tn, recompute, tc, store=lambda x: x):
@@ -77,16 +79,19 @@ def _check_rows(v2, c1, c2, e_rel, tn, recompute, tc, store=lambda x: x):
     return events, unc
 
 
-def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None, stats=None):
+def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None, stats=None,
+                    key_block=None):
     """Steps 1-5 for every (batch, head), or for the (batch, head) pairs in
     `only` (the others' CL stays zero). Returns CL [B,S,H] and CL^c
     [B,nq,2,H]; events go to run.events. With a dict `stats`, also stores
     there the final max m and sum l of every query ([B,nh,S], natural
-    units) and CL^r = A^r / l ([B,S,nh,2])."""
+    units) and CL^r = A^r / l ([B,S,nh,2]). key_block: keys per step of the
+    online softmax (a multiple of R dividing S; default R)."""
     B, S, H, nh, d, R, nq, scale = (pr[k] for k in ("B", "S", "H", "nh", "d", "R", "nq", "scale"))
+    KB = R if key_block is None else key_block
+    if KB % R or S % KB:
+        raise ValueError("the key block must be a multiple of R that divides seq")
     Qh, Kh, Vh, Kch, Vr = pr["Qh"], pr["Kh"], pr["Vh"], pr["Kch"], pr["Vr"]
-    if S % TQ or R > TK or TK % R:
-        raise ValueError("the fused form takes seq in whole 128-row tiles and R dividing 128")
     e_rel = p.e_rel_value()
     tn_s = stored_threshold(p.t_near_inf, "f32")
     tn_cl = stored_threshold(p.t_near_inf, p.dtype)
@@ -97,6 +102,7 @@ def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None, stats=None)
     CLh = np.zeros((B, nh, S, d))
     M_all, L_all = np.zeros((B, nh, S)), np.zeros((B, nh, S))
     CLr_all = np.zeros((B, S, nh, 2))
+    queries = np.arange(S)
     for b in range(B):
         for h in range(nh):
             if only is not None and (b, h) not in only:
@@ -104,71 +110,73 @@ def fused_attention(run: _Run, pr: dict, p: OracleParams, only=None, stats=None)
             Q, K, V = Qh[b, h], Kh[b, h], Vh[b, h]
             Kc = Kch[b, h]                      # [nq, 2, d]
             vr = Vr[b, :, h, :]                 # [S, 2]
-            for qt in range(S // TQ):
-                q0 = qt * TQ
-                rows = np.arange(q0, q0 + TQ)
-                m = np.full(TQ, -np.inf)
-                l = np.zeros(TQ)
-                A = np.zeros((TQ, d))
-                Ar = np.zeros((TQ, 2))
-                last = qt if p.causal else S // TK - 1
-                for kt in range(last + 1):
-                    k0 = kt * TK
-                    s = Q[q0:q0 + TQ] @ K[k0:k0 + TK].T                # 1.
-                    for (fb, fh, fr, fc, val, *mode) in faults_as:
-                        if fb == b and fh == h and q0 <= fr < q0 + TQ and k0 <= fc < k0 + TK:
-                            i, j = fr - q0, fc - k0
-                            if mode and mode[0] == "flip":
-                                s[i, j] = flip_exponent_msb(float(round_to(s[i, j], "f32")), "f32")
-                            else:
-                                s[i, j] = round_to(np.array([val]), "f32")[0]
-                    if check_as:                                        # 2.
-                        for kb in range(TK // R):
-                            blk = (k0 + kb * R) // R
-                            cs = Q[q0:q0 + TQ] @ Kc[blk].T             # [TQ, 2]
-                            seg = s[:, kb * R:(kb + 1) * R]
-                            rec = ((lambda i, j, kb=kb: Q[q0 + i] @ K[k0 + kb * R + j])
-                                   if recompute_ok else None)
-                            evs, unc = _check_rows(seg, cs[:, 0], cs[:, 1], e_rel, tn_s, rec,
-                                                   p.t_correct,
-                                                   store=lambda x: float(round_to(np.array([x]), "f32")[0]))
-                            s[:, kb * R:(kb + 1) * R] = seg
-                            for (i, j, kind, action) in evs:
-                                run.events.append(("AS", b, h, q0 + i, k0 + kb * R + j, kind, action))
-                            for i in unc:
-                                run.events.append(("AS", b, h, q0 + i, k0 + kb * R, "-", "UNCORRECTABLE"))
-                    keys = np.arange(k0, k0 + TK)                       # 3.
-                    allowed = (keys[None, :] <= rows[:, None]) if p.causal else np.ones((TQ, TK), bool)
-                    with np.errstate(invalid="ignore", over="ignore"):
-                        z = np.where(allowed, scale * s, -np.inf)
-                        m_new = np.maximum(m, z.max(axis=1))
-                        pz = np.where(allowed, np.exp(z - m_new[:, None]), 0.0)
-                        alpha = np.where(np.isfinite(m), np.exp(m - m_new), 0.0)
-                    l = alpha * l + pz.sum(axis=1)
-                    P = run.rnd(pz)
-                    A = alpha[:, None] * A + P @ V[k0:k0 + TK]
-                    Ar = alpha[:, None] * Ar + P @ vr[k0:k0 + TK]
-                    m = m_new
-                CLt = run.rnd(A / l[:, None])                           # 4.
-                CLr = Ar / l[:, None]
-                M_all[b, h, q0:q0 + TQ], L_all[b, h, q0:q0 + TQ] = m, l
-                CLr_all[b, q0:q0 + TQ, h] = CLr
-                for (fb, fh, fr, fc, val, *mode) in faults_cl:
-                    if fb == b and fh == h and q0 <= fr < q0 + TQ:
-                        i = fr - q0
+            m = np.full(S, -np.inf)
+            l = np.zeros(S)
+            A = np.zeros((S, d))
+            Ar = np.zeros((S, 2))
+            for k0 in range(0, S, KB):
+                # queries that see keys from k0 on: all, or those from the
+                # R-block of k0 on (the block-lower-triangular region)
+                q0 = k0 if p.causal else 0
+                rows = queries[q0:]
+                s = Q[q0:] @ K[k0:k0 + KB].T                             # 1.
+                for (fb, fh, fr, fc, val, *mode) in faults_as:
+                    if fb == b and fh == h and fr >= q0 and k0 <= fc < k0 + KB and \
+                            (not p.causal or fc // R <= fr // R):
+                        i, j = fr - q0, fc - k0
                         if mode and mode[0] == "flip":
-                            CLt[i, fc] = flip_exponent_msb(float(CLt[i, fc]), p.dtype)
+                            s[i, j] = flip_exponent_msb(float(round_to(s[i, j], "f32")), "f32")
                         else:
-                            CLt[i, fc] = run.rnd(np.array([val]))[0]
-                if check_cl:
-                    evs, unc = _check_rows(CLt, CLr[:, 0], CLr[:, 1], e_rel, tn_cl, None,
-                                           p.t_correct,
-                                           store=lambda x: float(run.rnd(np.array([x]))[0]))
-                    for (i, j, kind, action) in evs:
-                        run.events.append(("CL", b, h, q0 + i, j, kind, action))
-                    for i in unc:
-                        run.events.append(("CL", b, h, q0 + i, 0, "-", "UNCORRECTABLE"))
-                CLh[b, h, q0:q0 + TQ] = CLt
+                            s[i, j] = round_to(np.array([val]), "f32")[0]
+                if check_as:                                            # 2.
+                    for kb in range(k0 // R, (k0 + KB) // R):
+                        # the (query, R-key block) vectors of the region
+                        r0 = kb * R - q0 if p.causal else 0
+                        seg = s[r0:, kb * R - k0:(kb + 1) * R - k0]
+                        cs = Q[q0 + r0:] @ Kc[kb].T                     # [rows, 2]
+                        rec = ((lambda i, j, r0=r0, kb=kb: Q[q0 + r0 + i] @ K[kb * R + j])
+                               if recompute_ok else None)
+                        evs, unc = _check_rows(seg, cs[:, 0], cs[:, 1], e_rel, tn_s, rec,
+                                               p.t_correct,
+                                               store=lambda x: float(round_to(np.array([x]), "f32")[0]))
+                        s[r0:, kb * R - k0:(kb + 1) * R - k0] = seg
+                        for (i, j, kind, action) in evs:
+                            run.events.append(("AS", b, h, q0 + r0 + i, kb * R + j, kind, action))
+                        for i in unc:
+                            run.events.append(("AS", b, h, q0 + r0 + i, kb * R, "-",
+                                               "UNCORRECTABLE"))
+                keys = np.arange(k0, k0 + KB)                           # 3.
+                allowed = (keys[None, :] <= rows[:, None]) if p.causal else np.ones(s.shape, bool)
+                mq = m[q0:]
+                with np.errstate(invalid="ignore", over="ignore"):
+                    z = np.where(allowed, scale * s, -np.inf)
+                    m_new = np.maximum(mq, z.max(axis=1))
+                    pz = np.where(allowed, np.exp(z - m_new[:, None]), 0.0)
+                    alpha = np.where(np.isfinite(mq), np.exp(mq - m_new), 0.0)
+                l[q0:] = alpha * l[q0:] + pz.sum(axis=1)
+                P = run.rnd(pz)
+                A[q0:] = alpha[:, None] * A[q0:] + P @ V[k0:k0 + KB]
+                Ar[q0:] = alpha[:, None] * Ar[q0:] + P @ vr[k0:k0 + KB]
+                m[q0:] = m_new
+            CLt = run.rnd(A / l[:, None])                               # 4.
+            CLr = Ar / l[:, None]
+            M_all[b, h], L_all[b, h] = m, l
+            CLr_all[b, :, h] = CLr
+            for (fb, fh, fr, fc, val, *mode) in faults_cl:
+                if fb == b and fh == h:
+                    if mode and mode[0] == "flip":
+                        CLt[fr, fc] = flip_exponent_msb(float(CLt[fr, fc]), p.dtype)
+                    else:
+                        CLt[fr, fc] = run.rnd(np.array([val]))[0]
+            if check_cl:
+                evs, unc = _check_rows(CLt, CLr[:, 0], CLr[:, 1], e_rel, tn_cl, None,
+                                       p.t_correct,
+                                       store=lambda x: float(run.rnd(np.array([x]))[0]))
+                for (i, j, kind, action) in evs:
+                    run.events.append(("CL", b, h, i, j, kind, action))
+                for i in unc:
+                    run.events.append(("CL", b, h, i, 0, "-", "UNCORRECTABLE"))
+            CLh[b, h] = CLt
     CL = CLh.transpose(0, 2, 1, 3).reshape(B, S, H)
     CLc = col_checksums(CL, R)                                          # 5.
     if stats is not None:
@@ -187,14 +195,14 @@ def regenerate_ap(run: _Run, pr: dict, p: OracleParams, m, l):
     return AP, row_checksums(AP, R)
 
 
-def fused_forward(X, Wqkv, Wo, p: OracleParams, faults=()):
+def fused_forward(X, Wqkv, Wo, p: OracleParams, faults=(), key_block=None):
     """Protected forward of one attention layer with the fused attention
     core. Returns O, CL, its checksums, the projection outputs and the
     event list."""
     run = _Run(p, faults)
     pr = project(run, X, Wqkv, p)
     st = {}
-    CL, CLc = fused_attention(run, pr, p, stats=st)
+    CL, CLc = fused_attention(run, pr, p, stats=st, key_block=key_block)
     Wo = np.asarray(Wo, dtype=np.float64)
     O, Oc = output_projection(run, CL, CLc, Wo, p)
     AP, APr = regenerate_ap(run, pr, p, st["m"], st["l"])

@@ -32,12 +32,14 @@ computes.
 
 Masked products (a reading; the paper uses dense products): a product
 over keys with a causally masked factor (AP V, dAS K, and over queries
-AP^T dCL, dAS^T Q) is formed per tile of KEY_TILE = 128 queries (keys):
-query i takes keys j < the end of the 128-key tile that holds i, and key
-j takes queries from the start of the tile that holds j. The terms left
-out are exact zeros, so this equals the dense product whenever the other
-factor is finite; it differs only where a masked zero would meet an INF
-or NaN (0 * INF = NaN), i.e. in the unprotected or paper-literal modes.
+AP^T dCL, dAS^T Q) is the sum over the pairs the mask allows, as Eq. 1
+defines attention under a causal mask: query i takes keys j <= i and key
+j takes queries i >= j; a checksum row of an R-query block takes the keys
+up to the block's last query, a checksum row of an R-key block the
+queries from the block's first key. The terms left out are exact zeros,
+so this equals the dense product whenever the other factor is finite; a
+dense product would also multiply an INF or NaN by a masked zero
+(0 * INF = NaN), which this definition never does.
 """
 from __future__ import annotations
 
@@ -50,71 +52,87 @@ from .numerics import flip_exponent_msb, round_to, stored_threshold
 from .eec import col_checksums, row_checksums, Verifier
 
 SECTIONS = ("AS", "CL", "O", "BWD")
-KEY_TILE = 128
-
-
-def _kend(i, S):
-    """End (exclusive) of the key range query i multiplies under a mask."""
-    return min(S, (i // KEY_TILE + 1) * KEY_TILE)
-
-
-def _kstart(j):
-    """Start of the query range key j multiplies under a mask."""
-    return (j // KEY_TILE) * KEY_TILE
 
 
 def masked_rows_product(P, M, causal):
-    """C_i = sum_j P_ij M_j over the key range of query i (dense if not
-    causal). P [..., S, S], M [..., S, n]."""
+    """C_i = sum over keys j <= i of P_ij M_j (all keys if not causal).
+    P [..., S, S], M [..., S, n]."""
     if not causal:
         return P @ M
     S = P.shape[-1]
     out = np.empty(P.shape[:-1] + M.shape[-1:])
     with np.errstate(invalid="ignore", over="ignore"):
-        for t0 in range(0, S, KEY_TILE):
-            t1 = min(S, t0 + KEY_TILE)
-            out[..., t0:t1, :] = P[..., t0:t1, :t1] @ M[..., :t1, :]
+        for i in range(S):
+            out[..., i:i + 1, :] = P[..., i:i + 1, :i + 1] @ M[..., :i + 1, :]
     return out
 
 
 def masked_cols_product(P, M, causal):
-    """C_j = sum_i P_ij M_i over the query range of key j (dense P^T M if
-    not causal)."""
+    """C_j = sum over queries i >= j of P_ij M_i (dense P^T M if not
+    causal)."""
     if not causal:
         return P.swapaxes(-1, -2) @ M
     S = P.shape[-1]
     out = np.empty(P.shape[:-2] + (S, M.shape[-1]))
     with np.errstate(invalid="ignore", over="ignore"):
-        for t0 in range(0, S, KEY_TILE):
-            t1 = min(S, t0 + KEY_TILE)
-            out[..., t0:t1, :] = P[..., t0:, t0:t1].swapaxes(-1, -2) @ M[..., t0:, :]
+        for j in range(S):
+            out[..., j:j + 1, :] = P[..., j:, j:j + 1].swapaxes(-1, -2) @ M[..., j:, :]
     return out
 
 
 def masked_block_rows_product(Pc, M, R, causal):
     """Checksum rows of a rows-product: Pc [..., nq, 2, S] are checksum rows
-    over R-query blocks; block qb takes the key range of its queries."""
+    over R-query blocks; block qb takes the keys up to its last query,
+    j < (qb + 1) R."""
     if not causal:
         return Pc @ M[..., None, :, :]
-    nq, S = Pc.shape[-3], Pc.shape[-1]
+    nq = Pc.shape[-3]
     out = np.empty(Pc.shape[:-1] + M.shape[-1:])
     with np.errstate(invalid="ignore", over="ignore"):
         for qb in range(nq):
-            e = _kend(qb * R, S)
+            e = (qb + 1) * R
             out[..., qb, :, :] = Pc[..., qb, :, :e] @ M[..., :e, :]
     return out
 
 
 def masked_block_cols_product(Pr, M, R, causal):
     """Checksum rows of a cols-product: Pr [..., S, nq, 2] are row checksums
-    over R-key blocks; block kb takes the query range of its keys."""
-    S, nq = Pr.shape[-3], Pr.shape[-2]
+    over R-key blocks; block kb takes the queries from its first key,
+    i >= kb R."""
+    nq = Pr.shape[-2]
     out = np.empty(Pr.shape[:-3] + (nq, 2, M.shape[-1]))
     with np.errstate(invalid="ignore", over="ignore"):
         for kb in range(nq):
-            s0 = _kstart(kb * R) if causal else 0
+            s0 = kb * R if causal else 0
             out[..., kb, :, :] = Pr[..., s0:, kb, :].swapaxes(-1, -2) @ M[..., s0:, :]
     return out
+
+
+def _allowed(S, causal):
+    """Pairs (query i, key j) the mask lets through: j <= i, or all."""
+    return np.tril(np.ones((S, S), dtype=bool)) if causal else np.ones((S, S), dtype=bool)
+
+
+def softmax_forward(AS, scale, causal, rnd):
+    """AP = softmax over keys of scale * AS (Eq. 1), masked keys selected
+    to -INF so their probabilities are exact zeros; the row maximum is
+    subtracted first; the result is rounded by rnd (to storage)."""
+    mask = _allowed(AS.shape[-1], causal)
+    with np.errstate(invalid="ignore", over="ignore"):
+        Z = np.where(mask, scale * AS, -np.inf)
+        m = Z.max(axis=-1, keepdims=True)
+        Ez = np.where(mask, np.exp(Z - m), 0.0)
+        return rnd(Ez / Ez.sum(axis=-1, keepdims=True))
+
+
+def softmax_backward(AP, dAP, scale, causal, rnd):
+    """dAS = scale * AP * (dAP - sum_j AP_ij dAP_ij) on the allowed pairs,
+    exact zeros on masked ones (the softmax Jacobian applied to dAP, with
+    the scale of the forward's argument); rounded by rnd."""
+    mask = _allowed(AP.shape[-1], causal)
+    with np.errstate(invalid="ignore", over="ignore"):
+        Dr = np.where(mask, dAP * AP, 0.0).sum(axis=-1, keepdims=True)
+        return rnd(np.where(mask, scale * AP * (dAP - Dr), 0.0))
 
 
 @dataclasses.dataclass
@@ -234,14 +252,14 @@ class _Run:
 
 
 def _row_dot(prow, mcol, i, S, causal):
-    """One element of a rows-product over query i's key range."""
-    e = _kend(i, S) if causal else S
+    """One element of a rows-product: query i over keys j <= i."""
+    e = i + 1 if causal else S
     return prow[:e] @ mcol[:e]
 
 
 def _col_dot(pcol, mcol, j, causal):
-    """One element of a cols-product over key j's query range."""
-    s0 = _kstart(j) if causal else 0
+    """One element of a cols-product: key j over queries i >= j."""
+    s0 = j if causal else 0
     return pcol[s0:] @ mcol[s0:]
 
 
@@ -350,12 +368,7 @@ def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
                    recompute=lambda k, i, j: Qh[k // nh, k % nh, i] @ Kh[k // nh, k % nh, j])
 
     # softmax with the causal mask applied by selection (unprotected)
-    mask = np.tril(np.ones((S, S), dtype=bool)) if p.causal else np.ones((S, S), dtype=bool)
-    with np.errstate(invalid="ignore", over="ignore"):
-        Z = np.where(mask, scale * AS, -np.inf)
-        m = Z.max(axis=-1, keepdims=True)
-        Ez = np.where(mask, np.exp(Z - m), 0.0)
-        AP = rnd(Ez / Ez.sum(axis=-1, keepdims=True))          # [B,nh,S,S]
+    AP = softmax_forward(AS, scale, p.causal, rnd)             # [B,nh,S,S]
     APc = col_checksums(AP, R)                                 # [B,nh,nq,2,S]
     APr = row_checksums(AP, R)                                 # [B,nh,S,nq,2]
 
@@ -452,10 +465,7 @@ def backward(fwd: dict, dO, p: OracleParams, faults=()):
                                                       dCLh[k // nh, k % nh, :, j], i, cz))
 
     # softmax backward (unprotected), masked entries selected to zero
-    mask = np.tril(np.ones((S, S), dtype=bool)) if p.causal else np.ones((S, S), dtype=bool)
-    with np.errstate(invalid="ignore", over="ignore"):
-        Dr = np.where(mask, dAP * AP, 0.0).sum(axis=-1, keepdims=True)
-        dAS = rnd(np.where(mask, scale * AP * (dAP - Dr), 0.0))
+    dAS = softmax_backward(AP, dAP, scale, p.causal, rnd)
     dASc = col_checksums(dAS, R)                               # [B,nh,nq,2,S]
     dASr = row_checksums(dAS, R)                               # [B,nh,S,nq,2]
 

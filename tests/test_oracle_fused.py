@@ -8,7 +8,7 @@ import pytest
 import workloads as W
 from oracle import OracleParams, forward
 from oracle.eec import col_checksums, row_checksums
-from oracle.fused import TK, TQ, fused_attention, fused_forward
+from oracle.fused import fused_attention, fused_forward
 from oracle.layer import _Run
 
 
@@ -21,7 +21,7 @@ def _inputs(S=256, H=128, nh=2, seed=3, dtype="bf16"):
 @pytest.mark.parametrize("R", [128, 64])
 def test_matches_materialised_attention_in_fp32(causal, R):
     """With fp32 storage the two forms differ only by where fp32 rounding
-    is applied (AS and AP stored vs P rounded per key tile)."""
+    is applied (AS and AP stored vs P rounded per key block)."""
     inp = _inputs(dtype="f32")
     p = OracleParams(heads=2, dtype="f32", causal=causal, block_rows=R)
     a = forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
@@ -149,11 +149,19 @@ def test_context_fault_is_fixed_from_the_row_checksum(val, action):
     assert abs(f["CL"][0, 99, 17] - f0["CL"][0, 99, 17]) <= 2.0 ** -7 * np.abs(row).sum()
 
 
-def test_tiles_cover_the_sequence():
-    assert TQ == TK == 128
-    with pytest.raises(ValueError):
-        fused_forward(*(_inputs(S=192)[k] for k in ("X", "Wqkv", "Wo")),
-                      OracleParams(heads=2, block_rows=64))
+@pytest.mark.parametrize("causal", [False, True])
+def test_key_block_size_changes_rounding_only(causal):
+    """The online softmax visits keys one checksum block at a time; in the
+    unrounded (f64) mode the block size leaves the result unchanged up to
+    fp64 rounding, and a sequence that is not a multiple of 128 works."""
+    inp = _inputs(S=192, dtype="f32")
+    outs = []
+    for R in (32, 64):
+        p = OracleParams(heads=2, dtype="f64", causal=causal, block_rows=R)
+        f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+        assert f["events"] == []
+        outs.append(f["CL"])
+    assert np.abs(outs[0] - outs[1]).max() <= 1e-12 * np.abs(outs[0]).max()
 
 
 @pytest.mark.parametrize("causal", [False, True])

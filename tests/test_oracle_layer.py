@@ -338,8 +338,8 @@ def test_disabled_section_leaves_faults_in_place():
 
 
 def test_masked_products_equal_dense_products_on_finite_inputs():
-    """The per-tile key ranges of masked products leave out exact zeros
-    only, so on finite inputs they equal the dense products."""
+    """Masked products leave out exact zeros only, so on finite inputs
+    they equal the dense products."""
     from oracle.layer import (masked_rows_product, masked_cols_product,
                               masked_block_rows_product, masked_block_cols_product)
     rng = np.random.default_rng(4)
@@ -356,8 +356,49 @@ def test_masked_products_equal_dense_products_on_finite_inputs():
     Pr = row_checksums(P, R)
     dense = (Pr.reshape(2, S, -1).swapaxes(-1, -2) @ M).reshape(2, S // R, 2, n)
     assert np.allclose(masked_block_cols_product(Pr, M, R, True), dense, rtol=1e-12, atol=1e-9)
-    # an INF meets masked zeros only inside the tile holding the diagonal
-    M2 = M.copy()
-    M2[0, 200, 1] = np.inf
-    C = masked_rows_product(P, M2, True)
-    assert np.all(np.isfinite(C[0, :128, 1])) and np.all(~np.isfinite(C[0, 128:256, 1]))
+
+
+def test_masked_products_match_brute_force_sums_with_nonfinite_operands():
+    """Eq. 1 under a causal mask: query i sums over keys j <= i only, key j
+    over queries i >= j. Pinned against plain Python sums over the allowed
+    pairs, with INF and NaN in the unmasked factor: a masked zero never
+    meets them, so rows before an INF key stay finite."""
+    from oracle.layer import (masked_rows_product, masked_cols_product,
+                              masked_block_rows_product, masked_block_cols_product)
+    from oracle.eec import row_checksums
+    rng = np.random.default_rng(5)
+    S, R, n = 12, 4, 3
+    P = np.tril(rng.integers(-3, 4, (S, S)).astype(np.float64))
+    M = rng.integers(-3, 4, (S, n)).astype(np.float64)
+    M[7, 1] = np.inf
+    M[3, 2] = np.nan
+
+    def add(terms):
+        acc = 0.0
+        for t in terms:
+            acc = acc + t
+        return acc
+
+    rows = np.array([[add(P[i, j] * M[j, c] for j in range(i + 1)) for c in range(n)]
+                     for i in range(S)])
+    cols = np.array([[add(P[i, j] * M[i, c] for i in range(j, S)) for c in range(n)]
+                     for j in range(S)])
+    with np.errstate(invalid="ignore"):
+        assert np.array_equal(masked_rows_product(P, M, True), rows, equal_nan=True)
+        assert np.array_equal(masked_cols_product(P, M, True), cols, equal_nan=True)
+    # query rows before the INF key are finite (no 0 * INF), later ones not
+    got = masked_rows_product(P, M, True)
+    assert np.all(np.isfinite(got[:7, 1]))
+    assert all(not np.isfinite(got[i, 1]) for i in range(7, S) if P[i, 7] != 0)
+    # checksum rows of query blocks take the keys up to the block's last
+    # query; of key blocks the queries from the block's first key
+    Pc = col_checksums(P, R)
+    want = np.array([[[add(Pc[qb, w, j] * M[j, c] for j in range((qb + 1) * R))
+                       for c in range(n)] for w in range(2)] for qb in range(S // R)])
+    with np.errstate(invalid="ignore"):
+        assert np.array_equal(masked_block_rows_product(Pc, M, R, True), want, equal_nan=True)
+    Pr = row_checksums(P, R)
+    want = np.array([[[add(Pr[i, kb, w] * M[i, c] for i in range(kb * R, S))
+                       for c in range(n)] for w in range(2)] for kb in range(S // R)])
+    with np.errstate(invalid="ignore"):
+        assert np.array_equal(masked_block_cols_product(Pr, M, R, True), want, equal_nan=True)
