@@ -142,21 +142,27 @@ def optimize(secs: Sequence[Section], lam: Dict[str, float], fail_target: float)
     section in the input order."""
     if fail_target <= unsafe_att(secs, lam, [1.0] * len(secs)):
         return [1.0] * len(secs)   # unreachable: check every section always
-    order = sorted(range(len(secs)), key=lambda i: -fce(secs[i], lam))
     deficit = unsafe_att(secs, lam, [0.0] * len(secs)) - fail_target
-    t = [0.0] * len(secs)
-    for i in order:
+    f = [0.0] * len(secs)
+    # a section whose check costs nothing is always checked: its whole
+    # coverage gain comes first and for free
+    for i, s in enumerate(secs):
+        if s.cost <= 0.0:
+            f[i] = 1.0
+            deficit -= harmful_single(s, lam)
+    paid = [i for i, s in enumerate(secs) if s.cost > 0.0]
+    for i in sorted(paid, key=lambda i: -fce(secs[i], lam)):
         s = secs[i]
         if deficit <= 0.0:
             break
         gain = fce(s, lam)
         if gain * s.cost <= deficit:
-            t[i] = s.cost
+            f[i] = 1.0
             deficit -= gain * s.cost
         else:
-            t[i] = deficit / gain
+            f[i] = deficit / (gain * s.cost)
             deficit = 0.0
-    return [ti / s.cost if s.cost > 0 else 0.0 for ti, s in zip(t, secs)]
+    return f
 
 
 def schedule(freq: float, step: int) -> bool:

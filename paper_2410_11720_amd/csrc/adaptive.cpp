@@ -112,27 +112,34 @@ int attn_abft_optimize_frequencies(const abft_freq_op* ops, const abft_freq_sect
     std::copy(ones.begin(), ones.end(), freqs_out);
     return ABFT_OK;
   }
-  // coverage per unit of check time; a free section is the most efficient
-  std::vector<double> eff(n_secs);
-  for (int s = 0; s < n_secs; ++s)
-    eff[s] = secs[s].cost > 0.0 ? t[s].harmful / secs[s].cost : INFINITY;
-  std::vector<int> order(n_secs);
-  std::iota(order.begin(), order.end(), 0);
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return eff[a] > eff[b]; });
   double deficit = unsafe_att(t, zeros.data()) - fail_target;
-  std::vector<double> time(n_secs, 0.0);
+  // a check that costs nothing runs every step, and its coverage counts
+  // before any paid section is considered
+  std::vector<int> order;
+  for (int s = 0; s < n_secs; ++s) {
+    if (secs[s].cost > 0.0) {
+      order.push_back(s);
+      freqs_out[s] = 0.0;
+    } else {
+      freqs_out[s] = 1.0;
+      deficit -= t[s].harmful;
+    }
+  }
+  // paid sections by coverage gained per unit of check time, best first
+  std::vector<double> eff(n_secs, 0.0);
+  for (int s : order) eff[s] = t[s].harmful / secs[s].cost;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return eff[a] > eff[b]; });
   for (int s : order) {
     if (deficit <= 0.0) break;
-    const double gain = eff[s];
-    if (gain * secs[s].cost <= deficit) {
-      time[s] = secs[s].cost;
-      deficit -= gain * secs[s].cost;
+    const double whole = t[s].harmful;  // gain of checking it every step
+    if (whole <= deficit) {
+      freqs_out[s] = 1.0;
+      deficit -= whole;
     } else {
-      time[s] = deficit / gain;
+      freqs_out[s] = deficit / whole;
       deficit = 0.0;
     }
   }
-  for (int s = 0; s < n_secs; ++s) freqs_out[s] = secs[s].cost > 0.0 ? time[s] / secs[s].cost : 0.0;
   return ABFT_OK;
 }
 

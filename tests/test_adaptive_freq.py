@@ -94,3 +94,21 @@ def test_invalid_arguments_are_rejected():
     with pytest.raises(abft.AbftError):
         abft.attn_abft_unsafe_probability(good, [1e-20] * 3, [1.2])
     assert abft.attn_abft_sections_for_step([0.5] * 4, -1) == 0
+
+
+@pytest.mark.parametrize("free", [0, 1, 2])
+def test_free_section_matches_oracle_and_meets_the_target(free):
+    abft = _abft()
+    costs = [100.0, 60.0, 25.0]
+    costs[free] = 0.0
+    secs = F.layer_sections(8, 1024, 768, 12, True, "GPT-2",
+                            {"AS": costs[0], "CL": costs[1], "O": costs[2]})
+    L = {e: 1e-21 for e in F.TYPES}
+    u0, u1 = F.unsafe_att(secs, L, [0] * 3), F.unsafe_att(secs, L, [1] * 3)
+    for target in (u1 + 0.3 * (u0 - u1), u1 + 0.9 * (u0 - u1), u0 * 2):
+        got = abft.attn_abft_optimize_frequencies(to_abi(secs), lam3(L), target)
+        want = F.optimize(secs, L, target)
+        assert got[free] == 1.0
+        for a, b in zip(got, want):
+            assert math.isclose(a, b, rel_tol=1e-12, abs_tol=1e-15), (target, got, want)
+        assert abft.attn_abft_unsafe_probability(to_abi(secs), lam3(L), got) <= target * (1 + 1e-9)

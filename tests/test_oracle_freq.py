@@ -150,3 +150,29 @@ def test_table4_transcription_spot_values():
     assert F.table4_p("Neo", "K")["INF"] == 0.856
     assert F.table4_p("Roberta", "CL")["nINF"] == 0.004
     assert F.table4_p("GPT-2", "O") == {"INF": 1.0, "NaN": 1.0, "nINF": 1.0}
+
+
+@pytest.mark.parametrize("free", ["AS", "CL", "O"])
+def test_a_free_section_is_always_checked_and_the_target_is_met(free):
+    """A section whose check costs nothing adds coverage at no cost: it is
+    checked every step, and the paid sections then close what is left of
+    the deficit (GPT-2-shape layer, one section made free)."""
+    costs = {"AS": 100.0, "CL": 60.0, "O": 25.0}
+    costs[free] = 0.0
+    secs = F.layer_sections(8, 1024, 768, 12, True, "GPT-2", costs)
+    L = {e: 1e-21 for e in F.TYPES}
+    u0, u1 = F.unsafe_att(secs, L, [0] * 3), F.unsafe_att(secs, L, [1] * 3)
+    for target in (u1 + 0.3 * (u0 - u1), u1 + 0.9 * (u0 - u1), u1 + 0.05 * (u0 - u1)):
+        f = F.optimize(secs, L, target)
+        assert f[[s.name for s in secs].index(free)] == 1.0
+        assert F.unsafe_att(secs, L, f) <= target * (1 + 1e-9)
+        # no cheaper schedule on a grid of the paid sections meets the target
+        cost = sum(fi * s.cost for fi, s in zip(f, secs))
+        grid = np.linspace(0.0, 1.0, 21)
+        for a in grid:
+            for b in grid:
+                g = [1.0] * 3
+                paid = [i for i, s in enumerate(secs) if s.cost > 0]
+                g[paid[0]], g[paid[1]] = a, b
+                if F.unsafe_att(secs, L, g) <= target:
+                    assert sum(gi * s.cost for gi, s in zip(g, secs)) >= cost * (1 - 0.06)
