@@ -15,11 +15,14 @@
  * Conventions for every entry point
  * ---------------------------------
  * - Pointers marked (device) are caller-owned device memory on the current
- *   HIP device; the library allocates nothing and keeps no state between
- *   calls. Pointers marked (host) are read during the call only.
- * - `stream` is a hipStream_t (NULL = the null stream). All GPU work is
- *   enqueued asynchronously on it; outputs and the report are valid after
- *   the caller synchronises the stream.
+ *   HIP device; the library allocates nothing, creates no stream or event,
+ *   and keeps no state between calls beyond read-only facts about each
+ *   device it has run on (its architecture and the number of compute
+ *   units per XCD, read once). Pointers marked (host) are read during the
+ *   call only.
+ * - `stream` is a hipStream_t (NULL = the null stream). All GPU work of a
+ *   call is enqueued asynchronously on it and on no other stream; outputs
+ *   and the report are valid after the caller synchronises the stream.
  * - Layouts are dense row-major (C order), dimensions listed outermost first.
  * - bf16 storage is IEEE bfloat16 (round-to-nearest-even when produced);
  *   accumulation and all checksums are fp32.
@@ -181,11 +184,7 @@ int attn_abft_forward(const attn_abft_config* cfg, const void* X, const void* Wq
  *   dO [batch, seq, hidden] (device, dtype); X, Wqkv, Wo as in forward;
  *   workspace: the one the forward filled (its backward scratch is reused);
  *   dX [batch, seq, hidden] (device, dtype); dWqkv [hidden, 3*hidden] and
- *   dWo [hidden, hidden] (device, fp32).
- * The weight gradients run on a second stream of the device (created on
- * first use, default priority), forked from and joined back into `stream`
- * with events: all work of the call is ordered before later work on
- * `stream`, as for a single stream (also under graph capture). */
+ *   dWo [hidden, hidden] (device, fp32). */
 int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* X,
                        const void* Wqkv, const void* Wo, void* workspace,
                        size_t workspace_bytes, void* dX, float* dWqkv, float* dWo,
@@ -263,11 +262,18 @@ int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
 /* Human-readable text of a status code (static storage). */
 const char* attn_abft_strerror(int status);
 
-/* Byte offset inside the workspace of a saved tensor of the forward:
- * which = 0: QKV [B, S, 3H]; 1: AS [B, nh, S, S] (valid from the forward
- * until the next backward, which reuses its space); 2: AP [B, nh, S, S];
- * 3: CL [B, S, H]; storage dtype, row-major. Under a causal mask only the
- * key tiles up to the diagonal tile of each query block are written.
+/* Byte offset inside the workspace of a tensor the forward or backward
+ * leaves there (for inspection; row-major):
+ *   which = 0: QKV [B, S, 3H]; 1: AS [B, nh, S, S] (valid from the forward
+ *   until the next backward, which reuses its space for dAP); 2: AP
+ *   [B, nh, S, S]; 3: CL [B, S, H]; 4: dQKV [B, S, 3H] (backward: dQ|dK|dV);
+ *   5: dCL [B, S, H] (backward); 8: dAS [B, nh, S, S] (backward): storage
+ *   dtype. 6: AP^c [B, nh, S/R, 2, S] and 7: AP^r [B, nh, S, S/R, 2]: fp32
+ *   column and row checksums of the stored AP (unweighted, weighted) per
+ *   R-query and R-key block.
+ * Under a causal mask the score-shaped tensors hold meaningful values only
+ * on the pairs the mask allows (key <= query); other positions are zero
+ * where written and unspecified elsewhere.
  * Returns ABFT_ERR_INVALID for an invalid config or `which`. */
 int attn_abft_workspace_tensor(const attn_abft_config* cfg, int32_t which, size_t* offset);
 

@@ -356,23 +356,30 @@ class ProtectedAttention:
                            self.report_bwd)
         return dX, dWqkv, dWo
 
+    TENSORS = ("QKV", "AS", "AP", "CL", "dQKV", "dCL", "APc", "APr", "dAS")
+
     def tensor(self, which):
-        """View of a saved forward tensor in the workspace: "QKV", "AS",
-        "AP" or "CL" (AS until the next backward)."""
+        """View of a tensor the forward or backward leaves in the workspace:
+        "QKV", "AS" (until the next backward), "AP", "CL", "dQKV", "dCL",
+        "dAS" (storage dtype), "APc", "APr" (fp32 checksums of AP)."""
         c = self.cfg
-        k = ("QKV", "AS", "AP", "CL").index(which)
+        k = self.TENSORS.index(which)
         off = ctypes.c_size_t()
         _check(_lib.attn_abft_workspace_tensor(ctypes.byref(c.to_c()), k, ctypes.byref(off)),
                "workspace_tensor")
-        es = 4 if c.dtype == "f32" else 2
         B, S, H, nh = c.batch, c.seq, c.hidden, c.heads
+        nq = S // c.block_rows
         shape = {"QKV": (B, S, 3 * H), "AS": (B, nh, S, S), "AP": (B, nh, S, S),
-                 "CL": (B, S, H)}[which]
+                 "CL": (B, S, H), "dQKV": (B, S, 3 * H), "dCL": (B, S, H),
+                 "dAS": (B, nh, S, S), "APc": (B, nh, nq, 2, S),
+                 "APr": (B, nh, S, nq, 2)}[which]
+        dt = torch.float32 if which in ("APc", "APr") else c.torch_dtype
+        es = 4 if dt == torch.float32 else 2
         n = 1
         for x in shape:
             n *= x
         o = off.value
-        return self.workspace[o:o + n * es].view(c.torch_dtype).view(*shape)
+        return self.workspace[o:o + n * es].view(dt).view(*shape)
 
     def saved(self):
         """Views of the saved QKV, AP and CL inside the workspace."""

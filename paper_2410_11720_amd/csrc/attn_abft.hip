@@ -156,48 +156,6 @@ int check_device() {
   return cached[dev];
 }
 
-// The backward runs the weight gradients (dW^O, then dW^QKV) on a second
-// stream of the device, beside the chain that feeds dX: neither result is
-// read by a later kernel of the step, so they overlap dCL, dAP, ... and dX.
-// The second stream waits on an event the caller's stream records at each
-// fork, and the caller's stream waits for the second one before the call
-// returns, so the call is ordered on the caller's stream as if serial (and
-// captures into a graph like a single stream). One side stream and two
-// events per device, created on first use; the mutex orders the fork and
-// join events of calls from several host threads.
-struct SideStream {
-  hipStream_t st = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
-  std::mutex mu;
-};
-SideStream* side_stream() {
-  static std::mutex mu;
-  static SideStream sides[64];
-  static bool made[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  std::lock_guard<std::mutex> lk(mu);
-  if (!made[dev]) {
-    SideStream& ss = sides[dev];
-    if (hipStreamCreateWithFlags(&ss.st, hipStreamNonBlocking) != hipSuccess ||
-        hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess)
-      return nullptr;
-    made[dev] = true;
-  }
-  return &sides[dev];
-}
-// side waits for everything submitted to s so far
-hipError_t fork_to(SideStream* ss, hipStream_t s) {
-  hipError_t e = hipEventRecord(ss->fork, s);
-  return e != hipSuccess ? e : hipStreamWaitEvent(ss->st, ss->fork, 0);
-}
-// s waits for everything submitted to the side stream so far
-hipError_t join_from(SideStream* ss, hipStream_t s) {
-  hipError_t e = hipEventRecord(ss->join, ss->st);
-  return e != hipSuccess ? e : hipStreamWaitEvent(s, ss->join, 0);
-}
-
 struct Params {
   float e_rel, tn, tc, scale;
   bool prot, root, sec_as, sec_cl, sec_o, sec_bwd;
@@ -308,6 +266,11 @@ int attn_abft_workspace_tensor(const attn_abft_config* cfg, int32_t which, size_
     case 1: *offset = L.as; return ABFT_OK;
     case 2: *offset = L.ap; return ABFT_OK;
     case 3: *offset = L.cl; return ABFT_OK;
+    case 4: *offset = L.dqkv; return ABFT_OK;
+    case 5: *offset = L.dcl; return ABFT_OK;
+    case 6: *offset = L.apc; return ABFT_OK;
+    case 7: *offset = L.apr; return ABFT_OK;
+    case 8: *offset = L.das; return ABFT_OK;
   }
   return ABFT_ERR_INVALID;
 }
@@ -501,16 +464,6 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   const int64_t B = d.B, S = d.S, H = d.H, nh = d.nh, hd = d.d, R = d.R, nq = d.nq, T = d.T;
   const size_t es = d.es;
   const bool pb = p.sec_bwd;
-  // the weight gradients go to the side stream when both they and the
-  // chain beside them run
-  SideStream* side = nullptr;
-  if ((stages & (ABFT_STAGE_DWO | ABFT_STAGE_DWQKV)) && (stages & ~(ABFT_STAGE_DWO | ABFT_STAGE_DWQKV))) {
-    side = side_stream();
-    if (side == nullptr) return ABFT_ERR_HIP;
-  }
-  std::unique_lock<std::mutex> side_lock;
-  if (side) side_lock = std::unique_lock<std::mutex>(side->mu);
-  const hipStream_t sw = side ? side->st : s;  // stream of the weight gradients
 
   // dO^c (Sec. 4.6), with the report cleared in the same launch
   {
@@ -562,8 +515,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DWO;
-    if (side) CK(fork_to(side, s));  // after the encode, which clears the report
-    CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), sw));
+    CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
   // dAP = dCL_h V_h^T, dAP^c = dCL_h^c V_h^T
   if (stages & ABFT_STAGE_DAP) {
@@ -658,8 +610,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DWQ; g.map.op_span = int(H);
-    if (side) CK(fork_to(side, s));  // dQKV is complete
-    CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), sw));
+    CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
   // dX = dQKV Wqkv^T, dX^c = dQKV^c Wqkv^T
   if (stages & ABFT_STAGE_DX) {
@@ -675,7 +626,6 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     g.map.op_base = ABFT_OP_DX; g.map.rows_per_b = int(S);
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(), s));
   }
-  if (side) CK(join_from(side, s));
   return ABFT_OK;
 }
 
