@@ -1,0 +1,159 @@
+"""Fault-injection campaigns on the GPU at the encoder and GPT-2 shapes,
+as the workloads state them (Sec. 5.2: every injected INF, NaN and
+near-INF error detected and corrected, no false alarm).
+
+Each step runs the protected forward and backward through the C ABI. A
+faulty step must report exactly the injected faults (position and class,
+corrected by recomputation with the root check on) and give outputs
+within the bar of the fault-free run; a fault-free step must report
+nothing and give the fault-free outputs bit for bit (the kernels are
+deterministic). The campaign stops at its first mismatch. Sampled steps
+are run through the whole-layer oracle as well.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import OracleParams, backward, forward
+from oracle.numerics import classify, round_to, stored_threshold
+
+pytestmark = pytest.mark.gpu
+RTOL = 1e-2
+WEIGHT_OPS = ("dWO", "dWQ", "dWK", "dWV")
+KINDS = ["inf", "nan", "+1e10", "-1e10"]
+
+
+def _abft():
+    from paper_2410_11720_amd import abft
+    return abft
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda").to(torch.bfloat16)
+
+
+def rel_err(a, b):
+    a, b = a.float(), b.float()
+    if not torch.isfinite(a).all():
+        return float("inf")
+    scale = torch.clamp(b.abs(), min=float(b.pow(2).mean().sqrt()) + 1e-30)
+    return float(((a - b).abs() / scale).max())
+
+
+def expected_event(f, shape):
+    dt = "f32" if f.op in WEIGHT_OPS else shape.dtype
+    stored = float(round_to(np.array([f.value]), dt)[0])
+    return (f.op, f.b, f.h, f.row, f.col, classify(stored, stored_threshold(1e10, dt)),
+            "RECOMPUTE")
+
+
+class Campaign:
+    def __init__(self, shape, seed):
+        abft = _abft()
+        self.abft, self.shape = abft, shape
+        self.inp = W.make_inputs(shape, seed)
+        cfg = abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads,
+                               causal=shape.causal, block_rows=shape.block_rows)
+        self.X, self.Wqkv, self.Wo, self.dO = (dev(self.inp[k]) for k in ("X", "Wqkv", "Wo", "dO"))
+        self.layer = abft.ProtectedAttention(cfg)
+        self.ref, ev = self.step(())
+        assert ev == []
+        self.ref = {k: v.clone() for k, v in self.ref.items()}
+        self.injected = 0
+
+    def step(self, faults):
+        abft, L = self.abft, self.layer
+        fdev = abft.faults_to_device(list(faults))
+        O = L.forward(self.X, self.Wqkv, self.Wo, fdev)
+        dX, dWqkv, dWo = L.backward(self.dO, self.X, self.Wqkv, self.Wo, fdev)
+        torch.cuda.synchronize()
+        ev = abft.read_report(L.report)["events"] + abft.read_report(L.report_bwd)["events"]
+        return dict(O=O, dX=dX, dWqkv=dWqkv, dWo=dWo), ev
+
+    def run(self, step, faults):
+        out, ev = self.step(faults)
+        want = sorted(expected_event(f, self.shape) for f in faults)
+        assert sorted(ev) == want, f"step {step}: {faults}"
+        for k, v in out.items():
+            if faults:
+                assert rel_err(v, self.ref[k]) <= RTOL, f"step {step} {k}: {faults}"
+            else:
+                assert torch.equal(v, self.ref[k]), f"step {step} {k} differs without faults"
+        self.injected += len(faults)
+        return out, ev
+
+
+def check_with_oracle(c, faults, out, ev):
+    """The same step through the whole-layer oracle: identical events,
+    outputs within the bar."""
+    shape, inp = c.shape, c.inp
+    p = OracleParams(heads=shape.heads, causal=shape.causal, block_rows=shape.block_rows)
+    o = forward(inp["X"], inp["Wqkv"], inp["Wo"], p, faults)
+    ob = backward(o, inp["dO"], p, faults)
+    assert sorted(ev) == sorted(o["events"] + ob["events"])
+    for k, r in (("O", o["O"]), ("dX", ob["dX"]), ("dWqkv", ob["dWqkv"]), ("dWo", ob["dWo"])):
+        g = out[k].float().cpu().numpy().astype(np.float64)
+        scale = np.maximum(np.abs(r), np.sqrt(np.mean(r ** 2)))
+        assert np.max(np.abs(g - r) / scale) <= RTOL, k
+
+
+def test_c2_campaign_one_fault_per_step():
+    """Encoder shape (B8 S512 H768, 12 heads of 64, no mask): 200 steps, one
+    fault each, its output drawn from {Q, K, V, AS, CL, O, dX, dW} (dW: one
+    of dW^Q, dW^K, dW^V, dW^O) and its kind from {INF, NaN, +-1e10}."""
+    c = Campaign(W.C2, W.data_seed("c2"))
+    ops = ["Q", "K", "V", "AS", "CL", "O", "dX", "dW"]
+    seen = set()
+    for step in range(200):
+        rng = np.random.Generator(np.random.PCG64(W.fault_seed("c2", step)))
+        op = ops[int(rng.integers(len(ops)))]
+        if op == "dW":
+            op = WEIGHT_OPS[int(rng.integers(4))]
+        kind = KINDS[int(rng.integers(len(KINDS)))]
+        faults = W.draw_faults(c.shape, W.fault_seed("c2", step), 1, [op], [kind])
+        if step % 50 == 0:
+            print(f"[case] c2 campaign step {step}", flush=True)
+        out, ev = c.run(step, faults)
+        seen.add((op, kind))
+        if step == 0:
+            check_with_oracle(c, faults, out, ev)
+    assert c.injected == 200
+    assert {op for op, _ in seen} == set(ops[:-1]) | set(WEIGHT_OPS)
+
+
+def test_c3_campaign_faults_in_one_step_of_ten():
+    """GPT-2 shape (B8 S1024 H768, 12 heads of 64, causal): 120 steps; in
+    one step of every ten (drawn), 1-4 faults over all 16 protected outputs
+    of the forward and the backward, at most one per checksum row and
+    column; the other steps are fault-free."""
+    c = Campaign(W.C3, W.data_seed("c3"))
+    for block in range(12):
+        rng = np.random.Generator(np.random.PCG64(W.fault_seed("c3", 1000 + block)))
+        hit = 10 * block + int(rng.integers(10))
+        count = 1 + int(rng.integers(4))
+        print(f"[case] c3 campaign block {block}: step {hit}, {count} faults", flush=True)
+        for step in range(10 * block, 10 * block + 10):
+            faults = (W.draw_faults(c.shape, W.fault_seed("c3", step), count, W.ALL_OPS, KINDS)
+                      if step == hit else [])
+            c.run(step, faults)
+    assert c.injected >= 12
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_every_output_many_injections(causal):
+    """Many injections into every protected output (the paper injects
+    about 5,000 times per output matrix): 300 steps, each with one fault in
+    every one of the 16 outputs, kinds drawn from INF, -INF, NaN, +-1e10,
+    1e30 and 1e6, at a smaller shape (B2 S512 H256, 4 heads of 64)."""
+    shape = W.make_shape(2, 512, 256, 4, causal=causal)
+    c = Campaign(shape, 77)
+    kinds = ["inf", "-inf", "nan", "+1e10", "-1e10", "1e30", "1e6"]
+    for step in range(300):
+        seed = 50000 + 1000 * int(causal) + step
+        faults = [W.draw_faults(shape, seed * 17 + i, 1, [op], kinds)[0]
+                  for i, op in enumerate(W.ALL_OPS)]
+        if step % 100 == 0:
+            print(f"[case] every-output campaign causal={causal} step {step}", flush=True)
+        c.run(step, faults)
+    assert c.injected == 300 * 16

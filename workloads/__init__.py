@@ -147,6 +147,10 @@ KIND_VALUES = {
     "1e6": 1e6,
     "1e10": 1e10,
     "1e30": 1e30,
+    "+1e6": 1e6,
+    "-1e6": -1e6,
+    "+1e30": 1e30,
+    "-1e30": -1e30,
 }
 
 
