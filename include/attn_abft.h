@@ -191,6 +191,24 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
                        const abft_fault* faults, int32_t n_faults, abft_report* report,
                        void* stream);
 
+/* Allocation-free protected forward, for callers that cannot allocate
+ * device memory (code under graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): attn_abft_forward with ABFT_FLAG_FUSED (required,
+ * else ABFT_ERR_UNSUPPORTED), its workspace replaced by a buffer of 64 MiB
+ * that the library holds on every device it runs on until the process
+ * ends; no memory is allocated during the call. Arguments as for
+ * attn_abft_forward; nothing is saved for a backward (ABFT_SEC_BWD is
+ * ignored). The layer must fit the buffer: T = batch * seq tokens need
+ * about T * hidden * 8 bytes (storage bf16) plus T * heads * 32 bytes of
+ * checksums and softmax statistics (B8 S1024 H768 with 12 heads: 55 MB);
+ * a larger layer returns ABFT_ERR_WORKSPACE before anything is enqueued.
+ * Every call on a device shares that device's buffer and leaves its
+ * contents behind: calls that overlap on one device (other streams, other
+ * host threads) race and must be serialised by the caller. */
+int attn_abft_forward_noalloc(const attn_abft_config* cfg, const void* X, const void* Wqkv,
+                              const void* Wo, void* O, const abft_fault* faults,
+                              int32_t n_faults, abft_report* report, void* stream);
+
 /* Stages of the chains, for profiling one kernel at a time with
  * attn_abft_forward_stages / attn_abft_backward_stages. */
 #define ABFT_STAGE_ENCODE      0x001u  /* checksum encoders (fwd: W^V, X; bwd: dO) */

@@ -100,6 +100,7 @@ _sig = {
                                                       ctypes.POINTER(FreqSection), _i32, _vp,
                                                       ctypes.c_double, _vp]),
     "attn_abft_sections_for_step": (_u32, [_vp, _i64]),
+    "attn_abft_forward_noalloc": (ctypes.c_int, [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp]),
 }
 for _name, (_res, _args) in _sig.items():
     _f = getattr(_lib, _name)
@@ -193,6 +194,14 @@ def attn_abft_forward(cfg: LayerConfig, X, Wqkv, Wo, O, workspace, faults, n_fau
                                   _ptr(workspace), workspace.numel() * workspace.element_size(),
                                   _ptr(faults), n_faults, _ptr(report), _stream(stream)),
            "attn_abft_forward")
+
+
+def attn_abft_forward_noalloc(cfg: LayerConfig, X, Wqkv, Wo, O, faults, n_faults, report,
+                              stream=None, append=False):
+    c = cfg.to_c(append)
+    _check(_lib.attn_abft_forward_noalloc(ctypes.byref(c), _ptr(X), _ptr(Wqkv), _ptr(Wo), _ptr(O),
+                                          _ptr(faults), n_faults, _ptr(report), _stream(stream)),
+           "attn_abft_forward_noalloc")
 
 
 def attn_abft_backward(cfg: LayerConfig, dO, X, Wqkv, Wo, workspace, dX, dWqkv, dWo, faults,

@@ -122,6 +122,33 @@ Layout_ make_layout(const Dims& d) {
   return L;
 }
 
+// Forward-only layout of the fused form (what attn_abft_forward with
+// ABFT_FLAG_FUSED writes and reads when no backward follows): projections,
+// context, the checksums the fused kernel and the output projection take,
+// and the softmax statistics. Offsets of tensors outside it stay 0 and are
+// never used on that path.
+Layout_ make_layout_fused_forward(const Dims& d) {
+  Layout_ L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  const size_t f = 4;
+  L.qkv = take(size_t(d.T) * 3 * d.H * d.es);
+  L.cl = take(size_t(d.T) * d.H * d.es);
+  L.xc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.wvr = take(size_t(d.H) * d.nh * 2 * f);
+  L.qkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
+  L.vr = take(size_t(d.T) * d.nh * 2 * f);
+  L.clc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.clr = take(size_t(d.T) * d.nh * 2 * f);
+  L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
+  L.total = off;
+  return L;
+}
+
 int validate(const attn_abft_config* c, Dims* d) {
   if (!make_dims(c, d)) return ABFT_ERR_INVALID;
   if (c->dtype != ABFT_BF16 && c->dtype != ABFT_FP32) return ABFT_ERR_UNSUPPORTED;
@@ -275,23 +302,18 @@ int attn_abft_workspace_tensor(const attn_abft_config* cfg, int32_t which, size_
   return ABFT_ERR_INVALID;
 }
 
-int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const void* Wqkv,
-                             const void* Wo, void* O, void* workspace, size_t workspace_bytes,
-                             const abft_fault* faults, int32_t n_faults, abft_report* report,
-                             uint32_t stages, void* stream) {
-  Dims d;
-  int st = validate(cfg, &d);
-  if (st != ABFT_OK) return st;
-  if (!X || !Wqkv || !Wo || !O || !workspace || !report || n_faults < 0 ||
-      (n_faults > 0 && !faults))
-    return ABFT_ERR_INVALID;
-  const Layout_ L = make_layout(d);
-  if (workspace_bytes < L.total) return ABFT_ERR_WORKSPACE;
-  if ((st = check_device()) != ABFT_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const Params p = make_params(cfg, d);
+}  // extern "C"
+
+namespace abft {
+namespace {
+
+// The forward chain over a workspace at ws laid out by L (arguments
+// already validated).
+int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, const Params& p,
+                 const void* X, const void* Wqkv, const void* Wo, void* O, char* ws,
+                 const abft_fault* faults, int32_t n_faults, abft_report* report,
+                 uint32_t stages, hipStream_t s) {
   const int dt = cfg->dtype;
-  char* ws = static_cast<char*>(workspace);
   auto F = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
   const char* Xc = static_cast<const char*>(X);
   const char* Wc = static_cast<const char*>(Wqkv);
@@ -440,6 +462,29 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(), s));
   }
   return ABFT_OK;
+}
+
+}  // namespace
+}  // namespace abft
+
+extern "C" {
+
+int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const void* Wqkv,
+                             const void* Wo, void* O, void* workspace, size_t workspace_bytes,
+                             const abft_fault* faults, int32_t n_faults, abft_report* report,
+                             uint32_t stages, void* stream) {
+  Dims d;
+  int st = validate(cfg, &d);
+  if (st != ABFT_OK) return st;
+  if (!X || !Wqkv || !Wo || !O || !workspace || !report || n_faults < 0 ||
+      (n_faults > 0 && !faults))
+    return ABFT_ERR_INVALID;
+  const Layout_ L = make_layout(d);
+  if (workspace_bytes < L.total) return ABFT_ERR_WORKSPACE;
+  if ((st = check_device()) != ABFT_OK) return st;
+  return forward_impl(cfg, d, L, make_params(cfg, d), X, Wqkv, Wo, O,
+                      static_cast<char*>(workspace), faults, n_faults, report, stages,
+                      static_cast<hipStream_t>(stream));
 }
 
 int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const void* X,
@@ -699,6 +744,66 @@ const char* attn_abft_strerror(int status) {
     case ABFT_ERR_WORKSPACE: return "workspace too small";
   }
   return "unknown status";
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free forward: the fused protected forward with its workspace in
+// a buffer of the library's own, for callers that cannot allocate device
+// memory (code under graph capture, tight serving loops).
+namespace abft {
+
+constexpr size_t NOALLOC_SCRATCH_BYTES = size_t(64) << 20;
+
+// The buffer: one copy on every device the library runs on, held until the
+// process ends. In host code `scratch` names a host-side stand-in; kernels
+// get the device address that hipGetSymbolAddress returns for the current
+// device.
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+// Device address of `scratch` on the current device, looked up once per
+// device with that device current; nullptr if the lookup fails.
+char* scratch_on_current_device() {
+  static std::mutex mu;
+  static char* addr[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lk(mu);
+  if (addr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr)
+      return nullptr;
+    addr[dev] = static_cast<char*>(ptr);
+  }
+  return addr[dev];
+}
+
+}  // namespace
+}  // namespace abft
+
+extern "C" {
+
+int attn_abft_forward_noalloc(const attn_abft_config* cfg, const void* X, const void* Wqkv,
+                              const void* Wo, void* O, const abft_fault* faults,
+                              int32_t n_faults, abft_report* report, void* stream) {
+  Dims d;
+  int st = validate(cfg, &d);
+  if (st != ABFT_OK) return st;
+  if (!(cfg->flags & ABFT_FLAG_FUSED)) return ABFT_ERR_UNSUPPORTED;
+  if (!X || !Wqkv || !Wo || !O || !report || n_faults < 0 || (n_faults > 0 && !faults))
+    return ABFT_ERR_INVALID;
+  const Layout_ L = make_layout_fused_forward(d);
+  if (L.total > NOALLOC_SCRATCH_BYTES) return ABFT_ERR_WORKSPACE;
+  if ((st = check_device()) != ABFT_OK) return st;
+  char* ws = scratch_on_current_device();
+  if (ws == nullptr) return ABFT_ERR_HIP;
+  Params p = make_params(cfg, d);
+  p.sec_bwd = false;  // nothing is kept for a backward
+  return forward_impl(cfg, d, L, p, X, Wqkv, Wo, O, ws, faults, n_faults, report,
+                      ABFT_STAGE_ALL, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"
