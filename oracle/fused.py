@@ -50,7 +50,8 @@ from __future__ import annotations
 import numpy as np
 
 from .eec import col_checksums, eec_locate, fix_by_checksum, row_checksums
-from .layer import OracleParams, _Run, project, output_projection
+from .layer import (OracleParams, _Run, backward, masked_rows_product, output_projection,
+                    project)
 from .numerics import classify, flip_exponent_msb, round_to, stored_threshold
 
 
@@ -211,3 +212,104 @@ def fused_forward(X, Wqkv, Wo, p: OracleParams, faults=(), key_block=None):
                 X=pr["X"], Wqkv=pr["Wqkv"], Wo=Wo, Xc=pr["Xc"], Xr=pr["Xr"], AP=AP, APr=APr,
                 CLr=st["CLr"], m=st["m"], l=st["l"], scale=pr["scale"], events=run.events,
                 params=p)
+
+
+def _checked_scores(run, p, op, b, h, A, Bm, Bc, tn, recompute_ok):
+    """S = A Bm^T (fp64, not rounded) over the block-lower-triangular
+    region at R granularity (all of it without the mask), the faults of op
+    applied to the fp32 value, and the row check of every (row, R-column
+    block) vector against A (Bc_kb)^T (Sec. 4.4's AS^r form; EEC of
+    Sec. 4.2): a located element is recomputed from A and Bm (root check
+    on) or fixed from the checksums. Columns of a block past the region
+    stay exact products (they are masked later)."""
+    S, R = A.shape[0], p.block_rows
+    s = A @ Bm.T
+    for (fb, fh, fr, fc, val, *mode) in run.faults.get(op, ()):
+        if fb == b and fh == h and (not p.causal or fc // R <= fr // R):
+            if mode and mode[0] == "flip":
+                s[fr, fc] = flip_exponent_msb(float(round_to(s[fr, fc], "f32")), "f32")
+            else:
+                s[fr, fc] = round_to(np.array([val]), "f32")[0]
+    if not run.on("BWD"):   # checks of the backward's recomputation
+        return s
+    for kb in range(S // R):
+        r0 = kb * R if p.causal else 0
+        seg = s[r0:, kb * R:(kb + 1) * R]
+        cs = A[r0:] @ Bc[kb].T                                     # [rows, 2]
+        rec = (lambda i, j, r0=r0, kb=kb: A[r0 + i] @ Bm[kb * R + j]) if recompute_ok else None
+        evs, unc = _check_rows(seg, cs[:, 0], cs[:, 1], p.e_rel_value(), tn, rec, p.t_correct,
+                               store=lambda x: float(round_to(np.array([x]), "f32")[0]))
+        s[r0:, kb * R:(kb + 1) * R] = seg
+        for (i, j, kind, action) in evs:
+            run.events.append((op, b, h, r0 + i, kb * R + j, kind, action))
+        for i in unc:
+            run.events.append((op, b, h, r0 + i, kb * R, "-", "UNCORRECTABLE"))
+    return s
+
+
+def fused_backward_core(run, ctx, p):
+    """The fused backward's steps (an extension: the attention core's
+    backward without storing the scores, with Sec. 4.4's checks carried
+    over), per (batch, head), from the forward's softmax statistics m, l:
+      1. S = Q K^T recomputed, AS faults applied, rows checked against
+         Q (K^c)^T per R-key block (as in the forward);
+      2. P = exp(scale S - m) / l rounded to storage (0 on masked pairs),
+         stored as AP with its row checksums AP^r (for dV's check);
+      3. dP = dCL V^T (not rounded), dAP faults applied, rows checked
+         against dCL (V^c)^T per R-key block (V^c propagated from X^c W^V);
+      4. D = sum over the head's dims of dCL * CL (the softmax backward's
+         row term: sum_j P_ij dP_ij = dCL_i . CL_i);
+      5. dS = scale P (dP - D) rounded (0 on masked pairs), stored as dAS
+         with its row checksums dAS^r (for dK's check);
+      6. dQ = dS K rounded, dQ faults applied, each row checked against
+         dS K^r, K^r the row checksums of the stored K over the head's
+         dims (weights 1..d); a located element is fixed from the checksum
+         (DELTA / RECONSTRUCT, Sec. 4.2);
+      7. dQ^c, the column checksums per R-query block dX's check takes,
+         encoded from the verified dQ.
+    S and dP are compared with the near-INF threshold as fp32 values, dQ
+    as stored."""
+    B, S, nh, d, R, nq, scale = (ctx[k] for k in ("B", "S", "nh", "d", "R", "nq", "scale"))
+    rnd = run.rnd
+    tn_s = stored_threshold(p.t_near_inf, "f32")
+    tn = stored_threshold(p.t_near_inf, p.dtype)
+    allowed = np.tril(np.ones((S, S), dtype=bool)) if p.causal else np.ones((S, S), dtype=bool)
+    AP, dAS = np.zeros((B, nh, S, S)), np.zeros((B, nh, S, S))
+    dQh = np.zeros((B, nh, S, d))
+    faults_dq = run.faults.get("dQ", ())
+    for b in range(B):
+        for h in range(nh):
+            Q, K, V = ctx["Qh"][b, h], ctx["Kh"][b, h], ctx["Vh"][b, h]
+            dCL, CL = ctx["dCLh"][b, h], ctx["CLh"][b, h]
+            s = _checked_scores(run, p, "AS", b, h, Q, K, ctx["Kch"][b, h], tn_s, p.root_check)
+            with np.errstate(over="ignore", invalid="ignore"):
+                P = rnd(np.where(allowed, np.exp(scale * s - ctx["m"][b, h][:, None])
+                                 / ctx["l"][b, h][:, None], 0.0))
+            dP = _checked_scores(run, p, "dAP", b, h, dCL, V, ctx["Vch"][b, h], tn_s,
+                                 p.root_check)
+            D = (dCL * CL).sum(axis=1)
+            with np.errstate(over="ignore", invalid="ignore"):
+                dS = rnd(np.where(allowed, scale * P * (dP - D[:, None]), 0.0))
+            dQ = rnd(masked_rows_product(dS, K, p.causal))
+            for (fb, fh, fr, fc, val, *mode) in faults_dq:
+                if fb == b and fh == h:
+                    dQ[fr, fc] = (flip_exponent_msb(float(dQ[fr, fc]), p.dtype)
+                                  if mode and mode[0] == "flip" else rnd(np.array([val]))[0])
+            if run.on("BWD"):
+                Kr = row_checksums(K, d)[:, 0, :]                       # [S, 2]
+                cs = masked_rows_product(dS, Kr, p.causal)              # [S, 2]
+                evs, unc = _check_rows(dQ, cs[:, 0], cs[:, 1], p.e_rel_value(), tn, None,
+                                       p.t_correct, store=lambda x: float(rnd(np.array([x]))[0]))
+                for (i, j, kind, action) in evs:
+                    run.events.append(("dQ", b, h, i, j, kind, action))
+                for i in unc:
+                    run.events.append(("dQ", b, h, i, 0, "-", "UNCORRECTABLE"))
+            AP[b, h], dAS[b, h], dQh[b, h] = P, dS, dQ
+    return dict(AP=AP, APr=row_checksums(AP, R), dAS=dAS, dASr=row_checksums(dAS, R), dQ=dQh,
+                dQc=col_checksums(dQh, R))
+
+
+def fused_training_backward(fwd: dict, dO, p: OracleParams, faults=()):
+    """The layer's protected backward after a fused forward, with the
+    fused backward core in place of the stored-scores steps."""
+    return backward(fwd, dO, p, faults, core=fused_backward_core)

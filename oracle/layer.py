@@ -399,9 +399,13 @@ def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
                 events=run.events, params=p)
 
 
-def backward(fwd: dict, dO, p: OracleParams, faults=()):
+def backward(fwd: dict, dO, p: OracleParams, faults=(), core=None):
     """Protected backward chain (extension). Returns dX, dWqkv, dWo, the
-    intermediate gradients and the event list."""
+    intermediate gradients and the event list. core, if given, replaces
+    the steps from the scores' gradient to dQ (dAP, the softmax backward,
+    dQ): core(run, ctx, p) with ctx holding the per-head operands returns
+    AP, AP^r, dAS, dAS^r, dQ and dQ^c; dV and dK then take AP and dAS from
+    it."""
     run = _Run(p, faults)
     rnd, rndw = run.rnd, run.rndw
     X, Wqkv, Wo = fwd["X"], fwd["Wqkv"], fwd["Wo"]
@@ -442,42 +446,51 @@ def backward(fwd: dict, dO, p: OracleParams, faults=()):
         run.verify(dWo[None], dWoc, d, lambda k, i, j: ("dWO", 0, 0, i, j),
                    recompute=lambda k, i, j: CLf[:, i] @ dOf[:, j], weights=True)
 
-    # dAP = dCL_h V_h^T
     dCLh = heads_of(dCL)
-    dAP = rnd(dCLh @ Vh.swapaxes(-1, -2))                      # [B,nh,S,S]
-    dAPc = heads_of_c(dCLc) @ Vh.swapaxes(-1, -2)[:, :, None]  # [B,nh,nq,2,S]
-    run.inject("dAP", dAP, lambda b, h, r, c: (b, h, r, c))
-    if on:
-        colv = _causal_valid(B * nh, S, R)[0] if p.causal else None
-        run.verify(dAP.reshape(B * nh, S, S), dAPc.reshape(B * nh, nq, 2, S), R,
-                   lambda k, i, j: ("dAP", k // nh, k % nh, i, j), col_valid=colv,
-                   recompute=lambda k, i, j: dCLh[k // nh, k % nh, i] @ Vh[k // nh, k % nh, j])
+    cz = p.causal
+    if core is None:
+        APr = fwd["APr"]
+        # dAP = dCL_h V_h^T
+        dAP = rnd(dCLh @ Vh.swapaxes(-1, -2))                      # [B,nh,S,S]
+        dAPc = heads_of_c(dCLc) @ Vh.swapaxes(-1, -2)[:, :, None]  # [B,nh,nq,2,S]
+        run.inject("dAP", dAP, lambda b, h, r, c: (b, h, r, c))
+        if on:
+            colv = _causal_valid(B * nh, S, R)[0] if p.causal else None
+            run.verify(dAP.reshape(B * nh, S, S), dAPc.reshape(B * nh, nq, 2, S), R,
+                       lambda k, i, j: ("dAP", k // nh, k % nh, i, j), col_valid=colv,
+                       recompute=lambda k, i, j: dCLh[k // nh, k % nh, i] @ Vh[k // nh, k % nh, j])
+
+        # softmax backward (unprotected), masked entries selected to zero
+        dAS = softmax_backward(AP, dAP, scale, p.causal, rnd)
+        dASc = col_checksums(dAS, R)                               # [B,nh,nq,2,S]
+        dASr = row_checksums(dAS, R)                               # [B,nh,S,nq,2]
+
+        # dQ = dAS K_h
+        dQh = rnd(masked_rows_product(dAS, Kh, cz))
+        dQc = masked_block_rows_product(dASc, Kh, R, cz)           # [B,nh,nq,2,d]
+        run.inject("dQ", dQh, lambda b, h, r, c: (b, h, r, c))
+        if on:
+            run.verify(dQh.reshape(B * nh, S, d), dQc.reshape(B * nh, nq, 2, d), R,
+                       lambda k, i, j: ("dQ", k // nh, k % nh, i, j),
+                       recompute=lambda k, i, j: _row_dot(dAS[k // nh, k % nh, i],
+                                                          Kh[k // nh, k % nh, :, j], i, S, cz))
+    else:
+        ctx = dict(B=B, S=S, H=H, nh=nh, d=d, R=R, nq=nq, scale=scale, Qh=Qh, Kh=Kh, Vh=Vh,
+                   dCLh=dCLh, CLh=heads_of(CL), Kch=heads_of_c(fwd["QKVc"][..., H:2 * H]),
+                   Vch=heads_of_c(fwd["QKVc"][..., 2 * H:]), m=fwd["m"], l=fwd["l"])
+        c = core(run, ctx, p)
+        AP, APr, dAS, dASr, dQh, dQc = (c[k] for k in ("AP", "APr", "dAS", "dASr", "dQ", "dQc"))
+        dAP = None
 
     # dV = AP^T dCL_h; column checksums over key blocks from AP^r
-    cz = p.causal
     dVh = rnd(masked_cols_product(AP, dCLh, cz))               # [B,nh,S,d]
-    dVc = masked_block_cols_product(fwd["APr"], dCLh, R, cz)   # [B,nh,nq,2,d]
+    dVc = masked_block_cols_product(APr, dCLh, R, cz)          # [B,nh,nq,2,d]
     run.inject("dV", dVh, lambda b, h, r, c: (b, h, r, c))
     if on:
         run.verify(dVh.reshape(B * nh, S, d), dVc.reshape(B * nh, nq, 2, d), R,
                    lambda k, i, j: ("dV", k // nh, k % nh, i, j),
                    recompute=lambda k, i, j: _col_dot(AP[k // nh, k % nh, :, i],
                                                       dCLh[k // nh, k % nh, :, j], i, cz))
-
-    # softmax backward (unprotected), masked entries selected to zero
-    dAS = softmax_backward(AP, dAP, scale, p.causal, rnd)
-    dASc = col_checksums(dAS, R)                               # [B,nh,nq,2,S]
-    dASr = row_checksums(dAS, R)                               # [B,nh,S,nq,2]
-
-    # dQ = dAS K_h
-    dQh = rnd(masked_rows_product(dAS, Kh, cz))
-    dQc = masked_block_rows_product(dASc, Kh, R, cz)           # [B,nh,nq,2,d]
-    run.inject("dQ", dQh, lambda b, h, r, c: (b, h, r, c))
-    if on:
-        run.verify(dQh.reshape(B * nh, S, d), dQc.reshape(B * nh, nq, 2, d), R,
-                   lambda k, i, j: ("dQ", k // nh, k % nh, i, j),
-                   recompute=lambda k, i, j: _row_dot(dAS[k // nh, k % nh, i],
-                                                      Kh[k // nh, k % nh, :, j], i, S, cz))
 
     # dK = dAS^T Q_h; column checksums over key blocks from dAS^r
     dKh = rnd(masked_cols_product(dAS, Qh, cz))

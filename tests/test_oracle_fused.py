@@ -186,3 +186,61 @@ def test_regenerated_probabilities_feed_the_backward(causal):
     for k in ("dX", "dWqkv", "dWo"):
         assert np.abs(ba[k] - bf[k]).max() <= 1e-5 * np.abs(ba[k]).max(), k
     assert ba["events"] == [] and bf["events"] == []
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("R", [128, 64])
+def test_fused_backward_equals_the_materialised_backward_unrounded(causal, R):
+    """In the unrounded mode the fused backward core (scores recomputed
+    from the softmax statistics, the row term D = dCL . CL) gives the
+    materialised backward's gradients: sum_j P_ij dP_ij = dCL_i . CL_i."""
+    from oracle import backward
+    from oracle.fused import fused_training_backward
+    inp = _inputs(dtype="f32")
+    p = OracleParams(heads=2, dtype="f64", causal=causal, block_rows=R)
+    m = forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    mb = backward(m, inp["dO"], p)
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    fb = fused_training_backward(f, inp["dO"], p)
+    for k in ("dX", "dWqkv", "dWo", "dQKV", "dAS"):
+        assert np.abs(fb[k] - mb[k]).max() <= 1e-12 * np.abs(mb[k]).max(), k
+    assert fb["events"] == [] and mb["events"] == []
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_fused_backward_no_false_positives(seed):
+    from oracle.fused import fused_training_backward
+    inp = _inputs(seed=seed)
+    for causal in (False, True):
+        p = OracleParams(heads=2, causal=causal, block_rows=64)
+        f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+        assert fused_training_backward(f, inp["dO"], p)["events"] == []
+
+
+@pytest.mark.parametrize("op,val,action", [("AS", np.inf, "RECOMPUTE"), ("AS", np.nan, "RECOMPUTE"),
+                                           ("dAP", 1e10, "RECOMPUTE"), ("dAP", -np.inf, "RECOMPUTE"),
+                                           ("dQ", np.nan, "RECONSTRUCT"), ("dQ", 40.0, "DELTA")])
+def test_fused_backward_faults_are_located_and_fixed(op, val, action):
+    """A score fault in the recomputation, a fault in dP, and a fault in dQ
+    are located at their position; scores and dP are recomputed (the
+    gradients stay within a bf16 step of the fault-free ones at that one
+    element); dQ is fixed from its row checksum within the bf16
+    reconstruction bound."""
+    from oracle.fused import fused_training_backward
+    inp = _inputs()
+    p = OracleParams(heads=2, dtype="bf16", causal=True, block_rows=64)
+    f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    b0 = fused_training_backward(f0, inp["dO"], p)
+    fault = W.Fault(op, 0, 1, 150, 70 if op != "dQ" else 17, val)
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    b = fused_training_backward(f, inp["dO"], p, [fault])
+    ev = [e for e in b["events"]]
+    assert [(e[0], e[1], e[2], e[3], e[4], e[6]) for e in ev] == [(op, 0, 1, 150, fault.col, action)]
+    if op == "dQ":
+        row = b0["dQKV"][0, 150, 64:128]
+        assert abs(b["dQKV"][0, 150, 64 + 17] - row[17]) <= 2.0 ** -8 * (np.abs(row).sum() + abs(row[17]))
+    else:
+        for k in ("dX", "dWqkv", "dWo"):
+            ref = b0[k]
+            scale = np.maximum(np.abs(ref), np.sqrt(np.mean(ref ** 2)))
+            assert np.max(np.abs(b[k] - ref) / scale) <= 1e-2, k
