@@ -79,10 +79,22 @@ extern "C" {
                                        ABFT_ERR_UNSUPPORTED); the stage bits
                                        SCORE, SOFTMAX and CONTEXT each select
                                        that kernel. It saves each query's
-                                       softmax max and sum and CL^r; a backward
-                                       with the same flag first regenerates AP
-                                       and AP^r from Q, K and them (stage
-                                       REGEN), then runs the protected chain.   */
+                                       softmax max and sum and CL^r. A backward
+                                       with the same flag runs a fused core in
+                                       place of dAP, the softmax backward and
+                                       dQ (any of those stage bits or CORE_BWD
+                                       selects it): S = Q K^T recomputed and
+                                       row-checked against Q (K^c)^T, P from
+                                       the statistics, dP = dCL V^T row-checked
+                                       against dCL (V^c)^T, dS = scale P (dP -
+                                       D) with D = dCL . CL, dQ = dS K
+                                       row-checked against dS K^r (K^r: row
+                                       checksums of K over the head dims, a
+                                       located dQ element fixed from the
+                                       checksum); it stores AP and dS with their
+                                       row checksums for the protected dV and
+                                       dK GEMMs. AS faults are applied to the
+                                       recomputed scores too, dAP faults to dP. */
 
 /* ---- op tags of protected GEMM outputs (paper Table 1 + backward) ----- */
 enum abft_op {
@@ -226,8 +238,8 @@ int attn_abft_forward_noalloc(const attn_abft_config* cfg, const void* X, const 
 #define ABFT_STAGE_DK          0x080u  /* bwd: dK = dAS^T Q                         */
 #define ABFT_STAGE_DWQKV       0x100u  /* bwd: dWqkv = X^T [dQ|dK|dV]               */
 #define ABFT_STAGE_DX          0x200u  /* bwd: dX = [dQ|dK|dV] Wqkv^T               */
-#define ABFT_STAGE_REGEN       0x400u  /* bwd after a fused forward: AP, AP^r from
-                                          Q, K and the softmax statistics      */
+#define ABFT_STAGE_CORE_BWD    0x400u  /* bwd after a fused forward: the fused
+                                          backward core (AP, dAS, dQ)           */
 #define ABFT_STAGE_ALL         0x7ffu
 
 /* attn_abft_forward / attn_abft_backward restricted to the stages in the

@@ -142,20 +142,36 @@ struct FusedDesc {
 };
 hipError_t launch_fused_fwd(const FusedDesc& d, hipStream_t stream);
 
-// AP regenerated from Q, K and the fused forward's softmax statistics for
-// the backward: AP [B][nh][S][S] bf16 (key tiles up to the diagonal tile
-// under a causal mask, masked entries 0) and its row checksums
-// AP^r [B][nh][S][S/R][2] from the stored values.
-struct RegenDesc {
+// Fused backward core after a fused forward (no scores kept): per (batch,
+// head, 128-query tile) it recomputes S = Q K^T (row check against
+// Q (K^c)^T), takes P from the forward's softmax statistics, computes
+// dP = dCL V^T (row check against dCL (V^c)^T), dS = scale P (dP - D) with
+// D = dCL . CL, and dQ = dS K (row check against dS K^r, K^r the row
+// checksums of K over the head dims); it stores AP and dS with their row
+// checksums for the dV and dK GEMMs, and dQ.
+struct FusedBwdDesc {
   int B = 0, nh = 0, S = 0, H = 0, D = 0, R = 128;
   int causal = 0;
   float scale = 1.f;
-  const void* qkv = nullptr;
-  const float* stats = nullptr;
-  void* ap = nullptr;
-  float* apr = nullptr;
+  const void* qkv = nullptr;    // [B*S][3H] bf16: Q | K | V
+  const float* qkvc = nullptr;  // [B][S/R][2][3H] propagated column checksums (K^c, V^c)
+  const void* cl = nullptr;     // [B*S][H] bf16, the forward's context
+  const void* dcl = nullptr;    // [B*S][H] bf16
+  const float* stats = nullptr; // [B][nh][S][2]: log2-scaled max and sum per query
+  void* ap = nullptr;           // [B][nh][S][S] bf16 out (key tiles up to the diagonal)
+  float* apr = nullptr;         // [B][nh][S][S/R][2] out
+  void* das = nullptr;          // [B][nh][S][S] bf16 out
+  float* dasr = nullptr;        // [B][nh][S][S/R][2] out
+  void* dq = nullptr;           // dQ out: [B*S][ldq] bf16 (head h at column h D)
+  int64_t ldq = 0;
+  int check = 0;                // run the three row checks
+  int recompute = 1;            // located S / dP errors: recompute (else checksum fix)
+  float e_rel = 0.f, tn_s = 0.f, tn = 0.f, tc = 0.f;
+  const abft_fault* faults = nullptr;
+  int n_faults = 0;
+  abft_report* report = nullptr;
 };
-hipError_t launch_regen_ap(const RegenDesc& d, hipStream_t stream);
+hipError_t launch_fused_bwd(const FusedBwdDesc& d, hipStream_t stream);
 
 // Checksum encoder (public encode_checksums) and standalone verifier.
 hipError_t launch_encode(const void* A, int dtype, int64_t batch, int64_t rows, int64_t cols,
@@ -177,6 +193,7 @@ struct EncodeJob {
   int Rb = 0, Cb = 0;
   float* col_chk = nullptr;
   float* row_chk = nullptr;
+  int64_t ldcc = 0;  // elements between column-checksum rows (0: cols)
 };
 hipError_t launch_encode_jobs(const EncodeJob* jobs, int n, int dtype, abft_report* reset,
                               hipStream_t stream);

@@ -324,7 +324,9 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
   // (the backward's propagated checksums come from the forward: X^r for dW,
   // AP^r for dV, CL^r for dWo; a forward that precedes a protected backward
   // must have ABFT_SEC_BWD set).
-  const bool need_xc = p.sec_as || (p.root && p.sec_cl);  // Q^c, K^c; V root check
+  const bool fused = (cfg->flags & ABFT_FLAG_FUSED) != 0;
+  // Q^c, K^c; the V root check; K^c and V^c for a fused backward's checks
+  const bool need_xc = p.sec_as || (p.root && p.sec_cl) || (fused && p.sec_bwd);
   const bool need_vr = p.sec_cl || p.sec_bwd;             // V^r -> CL^r
   const bool need_apc = p.sec_cl || p.sec_o;              // AP^c -> CL^c -> O^c
   // encode (Sec. 4.6): W^V row checksums per head; X column and row
@@ -372,7 +374,6 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     g.map.head_cols = int(hd);
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, proj_tile(), s));
   }
-  const bool fused = (cfg->flags & ABFT_FLAG_FUSED) != 0;
   if (fused && (stages & (ABFT_STAGE_SCORE | ABFT_STAGE_SOFTMAX | ABFT_STAGE_CONTEXT))) {
     // score, softmax and context in one kernel (no AS or AP in memory)
     FusedDesc fd;
@@ -520,19 +521,6 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
                           s));
   }
 
-  // after a fused forward: AP (and AP^r) regenerated from Q, K and the
-  // softmax statistics the forward saved
-  if ((cfg->flags & ABFT_FLAG_FUSED) && (stages & ABFT_STAGE_REGEN)) {
-    RegenDesc rd;
-    rd.B = int(B); rd.nh = int(nh); rd.S = int(S); rd.H = int(H); rd.D = int(hd); rd.R = int(R);
-    rd.causal = cfg->causal;
-    rd.scale = p.scale;
-    rd.qkv = ws + L.qkv;
-    rd.stats = F(L.stats);
-    rd.ap = ws + L.ap;
-    rd.apr = F(L.apr);
-    CK(launch_regen_ap(rd, s));
-  }
   // dCL = dO Wo^T, dCL^c = dO^c Wo^T
   if (stages & ABFT_STAGE_DCL) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
@@ -562,8 +550,42 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     g.map.op_base = ABFT_OP_DWO;
     CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
+  // after a fused forward (no scores kept): the fused backward core, from
+  // the forward's softmax statistics, stores AP, dAS (with their row
+  // checksums) and the checked dQ; dQ^c for dX's check is encoded from it
+  const bool fused = (cfg->flags & ABFT_FLAG_FUSED) != 0;
+  if (fused && (stages & (ABFT_STAGE_CORE_BWD | ABFT_STAGE_DAP | ABFT_STAGE_SOFTMAX_BWD |
+                          ABFT_STAGE_DQ))) {
+    FusedBwdDesc fd;
+    fd.B = int(B); fd.nh = int(nh); fd.S = int(S); fd.H = int(H); fd.D = int(hd); fd.R = int(R);
+    fd.causal = cfg->causal;
+    fd.scale = p.scale;
+    fd.qkv = ws + L.qkv;
+    fd.qkvc = pb ? F(L.qkvc) : nullptr;
+    fd.cl = ws + L.cl;
+    fd.dcl = ws + L.dcl;
+    fd.stats = F(L.stats);
+    fd.ap = ws + L.ap; fd.apr = F(L.apr);
+    fd.das = ws + L.das; fd.dasr = F(L.dasr);
+    fd.dq = ws + L.dqkv; fd.ldq = 3 * H;
+    fd.check = pb ? 1 : 0;
+    fd.recompute = p.root ? 1 : 0;
+    fd.e_rel = p.e_rel;
+    fd.tn_s = stored_threshold(cfg->t_near_inf > 0.f ? cfg->t_near_inf : 1e10f, ABFT_FP32);
+    fd.tn = p.tn;
+    fd.tc = p.tc;
+    fd.faults = faults; fd.n_faults = n_faults; fd.report = report;
+    CK(launch_fused_bwd(fd, s));
+    if (pb) {
+      EncodeJob e;
+      e.A = ws + L.dqkv; e.batch = B; e.rows = S; e.cols = H; e.ld = 3 * H;
+      e.batch_stride = S * 3 * H; e.Rb = int(R); e.Cb = int(hd);
+      e.col_chk = F(L.dqkvc); e.ldcc = 3 * H;
+      CK(launch_encode_jobs(&e, 1, dt, nullptr, s));
+    }
+  }
   // dAP = dCL_h V_h^T, dAP^c = dCL_h^c V_h^T
-  if (stages & ABFT_STAGE_DAP) {
+  if (!fused && (stages & ABFT_STAGE_DAP)) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(S); g.K = int(hd);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -598,7 +620,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     CK(launch_gemm(g, dt, false, Layout::MNMajor, Layout::MNMajor, td, s));
   }
   // dAS = scale * AP * (dAP - rowdot), with column and row checksums
-  if (stages & ABFT_STAGE_SOFTMAX_BWD) {
+  if (!fused && (stages & ABFT_STAGE_SOFTMAX_BWD)) {
     SoftmaxDesc sd;
     sd.B = int(B); sd.nh = int(nh); sd.S = int(S); sd.R = int(R); sd.causal = cfg->causal;
     sd.kv_align = 128;
@@ -609,7 +631,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     CK(launch_softmax_bwd(sd, dt, s));
   }
   // dQ = dAS K_h, dQ^c = dAS^c K_h
-  if (stages & ABFT_STAGE_DQ) {
+  if (!fused && (stages & ABFT_STAGE_DQ)) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(hd); g.K = int(S);
     g.nb0 = int(B); g.nb1 = int(nh);

@@ -48,7 +48,8 @@ __device__ __forceinline__ void load_vec(const T* p, float* out) {
 template <class T, int V, int CPS>
 __device__ __forceinline__ void encode_block(const T* A, int64_t rows, int64_t cols, int64_t ld,
                                              int64_t bstride, int Rb, int Cb, float* col_chk,
-                                             float* row_chk, int64_t bx, int64_t rb, int64_t b) {
+                                             float* row_chk, int64_t bx, int64_t rb, int64_t b,
+                                             int64_t ldcc) {
   constexpr int RG = NT / CPS, W = CPS * V;
   __shared__ float part[RG][W][2];
   const int c = threadIdx.x % CPS, g = threadIdx.x / CPS;
@@ -110,7 +111,7 @@ __device__ __forceinline__ void encode_block(const T* A, int64_t rows, int64_t c
     if (threadIdx.x < 2 * W && bx * W + col < cols) {
       float acc = 0.f;
       for (int q = 0; q < RG; ++q) acc += part[q][col][which];
-      col_chk[((b * (rows / Rb) + rb) * 2 + which) * cols + bx * W + col] = acc;
+      col_chk[((b * (rows / Rb) + rb) * 2 + which) * ldcc + bx * W + col] = acc;
     }
   }
 }
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, in
                                                     int64_t ld, int64_t bstride, int Rb, int Cb,
                                                     float* col_chk, float* row_chk) {
   encode_block<T, V, CPS>(A, rows, cols, ld, bstride, Rb, Cb, col_chk, row_chk, blockIdx.x,
-                          blockIdx.y, blockIdx.z);
+                          blockIdx.y, blockIdx.z, cols);
 }
 
 __device__ __forceinline__ void clear_counters(abft_report* rep) {
@@ -141,13 +142,14 @@ struct EncJob {
   float* col_chk;
   float* row_chk;
   unsigned gx, gy, nblk;  // workgroups: gx column slabs x gy row blocks x batch
+  int64_t ldcc;           // elements between column-checksum rows
 };
 
 template <class T, int V, int CPS>
 __device__ __forceinline__ void encode_job(const EncJob& j, unsigned id) {
   const unsigned bx = id % j.gx, by = (id / j.gx) % j.gy, bz = id / (j.gx * j.gy);
   encode_block<T, V, CPS>(static_cast<const T*>(j.A), j.rows, j.cols, j.ld, j.bs, j.Rb, j.Cb,
-                          j.col_chk, j.row_chk, bx, by, bz);
+                          j.col_chk, j.row_chk, bx, by, bz, j.ldcc);
 }
 
 template <class T, int V, int CPS>
@@ -358,7 +360,7 @@ bool job_of(const EncodeJob& e, EncJob& j, int& cps) {
   const int64_t gx = (e.cols + W - 1) / W, gy = e.rows / e.Rb, n = gx * gy * e.batch;
   if (n <= 0 || n > (int64_t(1) << 30)) return false;
   j = EncJob{e.A, e.rows, e.cols, e.ld, e.batch_stride, e.Rb, e.Cb, e.col_chk, e.row_chk,
-             unsigned(gx), unsigned(gy), unsigned(n)};
+             unsigned(gx), unsigned(gy), unsigned(n), e.ldcc > 0 ? e.ldcc : e.cols};
   return true;
 }
 
@@ -376,6 +378,8 @@ hipError_t encode_jobs_t(const EncodeJob* jobs, int n, abft_report* reset, hipSt
     }
     for (int i = 0; i < n; ++i) {
       const EncodeJob& e = jobs[i];
+      // the separate kernels write dense column checksums only
+      if (e.col_chk != nullptr && e.ldcc > 0 && e.ldcc != e.cols) return hipErrorInvalidValue;
       hipError_t r = launch_encode(e.A, sizeof(T) == 4 ? ABFT_FP32 : ABFT_BF16, e.batch, e.rows,
                                    e.cols, e.ld, e.batch_stride, e.Rb, e.Cb, e.col_chk,
                                    e.row_chk, s);

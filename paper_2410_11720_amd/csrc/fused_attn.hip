@@ -599,132 +599,535 @@ struct FusedAttn {
   }
 };
 
-// AP regeneration for the backward: per (batch, head, 128-query tile)
-// the same S^T = K Q^T products as the fused forward, then
-// AP = exp2(log2(e) scale S - m) / l (the forward's final max and sum of
-// each query) rounded to bf16 and stored, 0 past the diagonal under a
-// causal mask; AP^r (sum and 1-based weighted sum over each R-key block of
-// a row) from the stored values.
+// Fused backward core (after a fused forward, which keeps no scores). Per
+// (batch, head, tile of 128 queries), each of the four waves owning 32
+// queries, key tiles of 128 keys pass through LDS (K and V as K-major
+// images, the K^c and V^c strips, and a K^r strip computed from the K
+// image); per key tile each wave computes
+//   S^T = K Q^T (AS^r = Q (K^c)^T from the strip) and checks every
+//     (query, R-key block) vector, as the forward does;
+//   P = exp2(log2(e) scale S - m) / l from the forward's statistics,
+//     rounded, stored as AP with its row checksums AP^r;
+//   dP^T = V dCL^T (dP^r = dCL (V^c)^T from the strip) and the same row
+//     check;
+//   dS = scale P (dP - D), D = dCL . CL per query, rounded, stored with
+//     its row checksums dAS^r;
+//   dQ^T += K^T dS^T and (dQ^r)^T += (K^r)^T dS^T, the K^T fragments read
+//     from the K image with transposing reads in the key order of the
+//     dS^T fragment a lane assembles from its accumulators.
+// After the last key tile dQ is rounded, row-checked against dQ^r (a
+// located element fixed from the checksum) and stored.
 template <int D>
-struct RegenAP {
-  static constexpr int KH = D / 64, KS = D / 32;
-  using DK = Direct<true, FT>;
-  static constexpr int STAGE_BYTES = KH * DK::BYTES;
-  static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+struct FusedBwd {
+  static constexpr int KH = D / 64, KS = D / 32, DB = D / 16;
+  using DK = Direct<true, FT>;                 // one 64-dim half: [128 keys][64]
+  static constexpr int IMG = KH * DK::BYTES;   // a [128 keys][D] K-major image
+  static constexpr int SCL = D + 8;            // strip row (elements), padded
+  static constexpr int STRIP = 16 * SCL * 2;
+  static constexpr int OFF_V = IMG, OFF_KC = 2 * IMG, OFF_VC = OFF_KC + STRIP;
+  static constexpr int OFF_KR = OFF_VC + STRIP;
+  static constexpr int STAGE_BYTES = OFF_KR + FT * 16 * 2;
+  static constexpr int SCR = 160;              // floats of rare-path scratch per wave
+  static constexpr int LDS_BYTES = STAGE_BYTES + 4 * SCR * 4;
 
-  __device__ static void run(const RegenDesc& rd, char* smem) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // K^T operand fragment (rows: dims rb + lane % 16; k: keys kb + 4g + 0..3
+  // and kb + 16 + 4g + 0..3) from the K-major image
+  __device__ static __forceinline__ TrPair kt_frag(const char* img, int rb, int kb, int lane) {
+    const int s = lane & 15, g = lane >> 4;
+    const int k1 = kb + 4 * g + (s >> 2), k2 = k1 + 16;
+    const int m = rb + 4 * (s & 3);
+    const char* half = img + (m >> 6) * DK::BYTES;
+    const int mm = m & 63, c = mm >> 3, off = (mm & 7) * 2;
+    return tr_pair_intrinsic(half + k1 * 128 + ((c ^ (k1 & 7)) << 4) + off,
+                             half + k2 * 128 + ((c ^ (k2 & 7)) << 4) + off);
+  }
+  // (K^r)^T fragment from the [128 keys][16] strip, same key order
+  __device__ static __forceinline__ TrPair kr_frag(const bf16_t* krs, int kb, int lane) {
+    const int s = lane & 15, g = lane >> 4;
+    const int k1 = kb + 4 * g + (s >> 2), k2 = k1 + 16;
+    const int m = 4 * (s & 3);
+    return tr_pair_intrinsic(krs + k1 * 16 + m, krs + k2 * 16 + m);
+  }
+
+  // Row check of a 128-key x 32-query tile t (keys along the lane's
+  // registers) per (query, R-key block) against the strip result cs (rows
+  // 4b..4b+3 of lane group b: hi/lo of c1, c2): a flagged vector is
+  // gathered into the wave's scratch, located by EEC and its element
+  // recomputed as the dot product of row q of A and row key of Bm (length
+  // D, leading dimensions lda, ldb) or fixed from the checksums.
+  __device__ static void check_tile(floatx4 (&t)[8][2], const floatx4 (&cs)[2],
+                                    const FusedBwdDesc& fd, int op, int b, int h, int qw,
+                                    int key0, const bf16_t* A, const bf16_t* Bm, int64_t lda,
+                                    int64_t ldb, float* scr, int lane) {
     const int lq = lane & 15, g = lane >> 4;
-    const int nqt = rd.S / FT, nbh = rd.B * rd.nh;
-    const int z = blockIdx.x % nbh;
-    const int qt = rd.causal ? nqt - 1 - int(blockIdx.x) / nbh : int(blockIdx.x) / nbh;
-    const int b = z / rd.nh, h = z % rd.nh;
-    const int q0 = qt * FT, qw = q0 + wave * 32;
-    const int S = rd.S, H = rd.H, R = rd.R, NB = FT / R, nqR = S / R;
-    const int64_t ld = 3 * int64_t(H);
-    const bf16_t* base = static_cast<const bf16_t*>(rd.qkv) + int64_t(b) * S * ld;
-    const bf16_t* Qp = base + h * D;
-    const bf16_t* Kp = base + H + h * D;
-    const int nkt = rd.causal ? qt + 1 : nqt;
-    const float sl2 = rd.scale * 1.4426950408889634f;
-    const int lg_jpb = __builtin_ctz(R / 16);
-
-    bf16x8 qf[2][KS];
-    float mq[2], il[2];
+    const int R = fd.R, NB = FT / R, lg_jpb = __builtin_ctz(R / 16);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      const int q = qw + 16 * qb + lq;
+      float sj[8], aj[8];
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-        qf[qb][kk] = *reinterpret_cast<const bf16x8*>(Qp + int64_t(q) * ld + 32 * kk + 8 * g);
-      const float* st = rd.stats + ((int64_t(b) * rd.nh + h) * S + q) * 2;
-      mq[qb] = st[0];
-      il[qb] = 1.f / st[1];
+      for (int j = 0; j < 8; ++j) {
+        sj[j] = (t[j][qb][0] + t[j][qb][1]) + (t[j][qb][2] + t[j][qb][3]);
+        aj[j] = (fabsf(t[j][qb][0]) + fabsf(t[j][qb][1])) +
+                (fabsf(t[j][qb][2]) + fabsf(t[j][qb][3]));
+      }
+      float r1[4], ra[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        r1[i] = sj[2 * i] + sj[2 * i + 1];
+        ra[i] = aj[2 * i] + aj[2 * i + 1];
+      }
+      if (lg_jpb >= 2) {
+        r1[0] += r1[1]; ra[0] += ra[1];
+        r1[1] = r1[2] + r1[3]; ra[1] = ra[2] + ra[3];
+      }
+      if (lg_jpb >= 3) { r1[0] += r1[1]; ra[0] += ra[1]; }
+      float mine1 = 0.f, minea = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (i < NB) {
+          const float t1 = group4_sum(r1[i]), ta = group4_sum(ra[i]);
+          if (g == i) { mine1 = t1; minea = ta; }
+        }
+      }
+      const float c1 = cs[qb][0] + cs[qb][1];
+      const bool fl = g < NB && flagged(c1 - mine1, minea, fd.e_rel);
+      uint64_t mask = __ballot(fl);
+      while (mask) {  // rare: locate and correct inside the wave
+        const int L = __builtin_ctzll(mask);
+        mask &= mask - 1;
+        const int vq = L & 15, vb = L >> 4;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (lq == vq && (j >> lg_jpb) == vb) scr[(16 * j + 4 * g + r) - vb * R] = t[j][qb][r];
+        const float v1 = __shfl(cs[qb][0] + cs[qb][1], L, 64);
+        const float v2 = __shfl(cs[qb][2] + cs[qb][3], L, 64);
+        wave_sync_lds();
+        if (lane == 0) {
+          const int q = qw + 16 * qb + vq;
+          const EecResult res = eec_locate<float>(scr, 1, R, v1, v2, fd.e_rel, fd.tn_s);
+          int idx = -1;
+          float nv = 0.f;
+          if (res.status == EEC_LOCATED) {
+            idx = res.index;
+            const int key = key0 + vb * R + idx;
+            const float old = scr[idx];
+            int action = ABFT_ACT_RECOMPUTE;
+            if (fd.recompute) {
+              float acc = 0.f;
+              for (int dd = 0; dd < D; ++dd)
+                acc = fmaf(bf2f(A[int64_t(q) * lda + dd]), bf2f(Bm[int64_t(key) * ldb + dd]), acc);
+              nv = acc;
+            } else {
+              nv = fix_by_checksum<float>(scr, 1, R, idx, v1, res.d1, fd.tc, &action);
+            }
+            scr[idx] = nv;
+            record_event(fd.report, op, b, h, q, key, classify(old, fd.tn_s), action, old);
+          }
+          if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, R, v1, fd.e_rel))
+            record_event(fd.report, op, b, h, q, key0 + vb * R, ABFT_KIND_NONE,
+                         ABFT_ACT_UNCORRECTABLE, 0.f);
+          scr[R] = __int_as_float(idx);
+          scr[R + 1] = nv;
+        }
+        wave_sync_lds();
+        const int idx = __float_as_int(scr[R]);
+        const float nv = scr[R + 1];
+        if (idx >= 0) {
+          const int kl = vb * R + idx;
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (lane == vq + 16 * ((kl & 15) >> 2) && j == (kl >> 4) && r == (kl & 3))
+                t[j][qb][r] = nv;
+        }
+        wave_sync_lds();
+      }
     }
-    auto issue = [&](int kt, int stg) {
-      char* sb = smem + stg * STAGE_BYTES;
-#pragma unroll
-      for (int hf = 0; hf < KH; ++hf)
-        DK::issue(Kp, ld, kt * FT, S, hf * 64, sb + hf * DK::BYTES, wave, lane);
-    };
-    bf16_t* AP = static_cast<bf16_t*>(rd.ap) + (int64_t(b) * rd.nh + h) * S * S;
-    float* APr = rd.apr + (int64_t(b) * rd.nh + h) * S * nqR * 2;
+  }
 
-    issue(0, 0);
-    for (int kt = 0; kt < nkt; ++kt) {
-      const int stg = kt & 1;
-      wait_vmcnt<0>();
-      __syncthreads();  // tile kt visible; every wave is done with tile kt - 1
-      if (kt + 1 < nkt) issue(kt + 1, stg ^ 1);
-      const char* sb = smem + stg * STAGE_BYTES;
-      const int key0 = kt * FT;
-      floatx4 s[8][2];
+  // injected faults of op (test-only) on a 128-key x 32-query fp32 tile
+  __device__ static void inject_tile(floatx4 (&t)[8][2], const FusedBwdDesc& fd, int op, int b,
+                                     int h, int qw, int key0, int lane) {
+    for (int f = 0; f < fd.n_faults; ++f) {
+      const abft_fault ft = fd.faults[f];
+      if (ft.op != op || ft.b != b || ft.h != h) continue;
+      const int qi = ft.row - qw, ki = ft.col - key0;
+      if (qi < 0 || qi >= 32 || ki < 0 || ki >= FT) continue;
+      // under the mask only the block-lower-triangular region is computed
+      if (fd.causal && ft.col / fd.R > ft.row / fd.R) continue;
+      const int oq = qi >> 4, olane = (qi & 15) + 16 * ((ki & 15) >> 2);
 #pragma unroll
       for (int j = 0; j < 8; ++j)
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) s[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (lane == olane && qb == oq && j == (ki >> 4) && r == (ki & 3))
+              t[j][qb][r] = ft.mode == ABFT_FAULT_FLIP ? flip_f32(t[j][qb][r]) : ft.value;
+    }
+  }
+
+  __device__ static void run(const FusedBwdDesc& fd, char* smem) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lq = lane & 15, g = lane >> 4;
+    const int S = fd.S, H = fd.H, R = fd.R, NB = FT / R, nqR = S / R;
+    const int nqt = S / FT, nbh = fd.B * fd.nh;
+    const int z = blockIdx.x % nbh;
+    const int qt = fd.causal ? nqt - 1 - int(blockIdx.x) / nbh : int(blockIdx.x) / nbh;
+    const int b = z / fd.nh, h = z % fd.nh;
+    const int q0 = qt * FT, qw = q0 + wave * 32;
+    const int64_t ld = 3 * int64_t(H);
+    const bf16_t* base = static_cast<const bf16_t*>(fd.qkv) + int64_t(b) * S * ld;
+    const bf16_t* Qp = base + h * D;
+    const bf16_t* Kp = base + H + h * D;
+    const bf16_t* Vp = base + 2 * H + h * D;
+    const bf16_t* dCLp = static_cast<const bf16_t*>(fd.dcl) + int64_t(b) * S * H + h * D;
+    const bf16_t* CLp = static_cast<const bf16_t*>(fd.cl) + int64_t(b) * S * H + h * D;
+    const int nkt = fd.causal ? qt + 1 : nqt;
+    const float sl2 = fd.scale * 1.4426950408889634f;
+    const int lg_jpb = __builtin_ctz(R / 16);
+    const bool chk = fd.check != 0;
+
+    // Q and dCL as the B operands of S^T and dP^T; the statistics and the
+    // softmax backward's row term D = dCL . CL of the lane's queries
+    bf16x8 qf[2][KS], gf[2][KS];
+    float mq[2], il[2], dq[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int q = qw + 16 * qb + lq;
+      float acc = 0.f;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
-        const char* sk = sb + (kk >> 1) * DK::BYTES;
+        qf[qb][kk] = *reinterpret_cast<const bf16x8*>(Qp + int64_t(q) * ld + 32 * kk + 8 * g);
+        gf[qb][kk] = *reinterpret_cast<const bf16x8*>(dCLp + int64_t(q) * H + 32 * kk + 8 * g);
+        const bf16x8 cf = *reinterpret_cast<const bf16x8*>(CLp + int64_t(q) * H + 32 * kk + 8 * g);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = fmaf(float(gf[qb][kk][e]), float(cf[e]), acc);
+      }
+      dq[qb] = group4_sum(acc);
+      const float* st = fd.stats + ((int64_t(b) * fd.nh + h) * S + q) * 2;
+      mq[qb] = st[0];
+      il[qb] = 1.f / st[1];
+    }
+
+    float kcv[4] = {0.f, 0.f, 0.f, 0.f}, vcv[4] = {0.f, 0.f, 0.f, 0.f};
+    auto issue = [&](int kt) {
+      const int key0 = kt * FT;
+#pragma unroll
+      for (int hf = 0; hf < KH; ++hf) {
+        DK::issue(Kp, ld, key0, S, hf * 64, smem + hf * DK::BYTES, wave, lane);
+        DK::issue(Vp, ld, key0, S, hf * 64, smem + OFF_V + hf * DK::BYTES, wave, lane);
+      }
+      if (chk) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int e = tid + p * FNT;
+          const int ee = e < NB * 2 * D ? e : 0;
+          const int blk = ee / (2 * D), c = (ee / D) & 1, dd = ee % D;
+          const float* row =
+              fd.qkvc + ((int64_t(b) * nqR + key0 / R + blk) * 2 + c) * ld + h * D + dd;
+          kcv[p] = row[H];
+          vcv[p] = row[2 * H];
+        }
+      }
+    };
+    auto commit = [&]() {
+      if (chk) {
+        bf16_t* kcs = reinterpret_cast<bf16_t*>(smem + OFF_KC);
+        bf16_t* vcs = reinterpret_cast<bf16_t*>(smem + OFF_VC);
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int e = tid + p * FNT;
+          if (e < NB * 2 * D) {
+            const int blk = e / (2 * D), c = (e / D) & 1, dd = e % D;
+            const int r = (4 * blk + 2 * c) * SCL + dd;
+            kcs[r] = f2bf(kcv[p]);
+            kcs[r + SCL] = f2bf(kcv[p] - bf2f(f2bf(kcv[p])));
+            vcs[r] = f2bf(vcv[p]);
+            vcs[r + SCL] = f2bf(vcv[p] - bf2f(f2bf(vcv[p])));
+          }
+        }
+      }
+    };
+    // K^r strip: columns 0..3 per key (hi/lo of the sum and of the 1-based
+    // weighted sum over the head dims) from the K image; columns 4..15 zero
+    bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
+    if (chk)
+      for (int e = tid; e < FT * 12; e += FNT) krs[(e / 12) * 16 + 4 + e % 12] = 0;
+    auto make_kr = [&]() {
+      const int k = tid >> 1, hh = tid & 1;
+      float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) {
+        const int ch = hh * (D / 16) + i;      // 8-dim chunk of the key row
+        const char* half = smem + (ch >> 3) * DK::BYTES;
+        const bf16x8 v =
+            *reinterpret_cast<const bf16x8*>(half + k * 128 + (((ch & 7) ^ (k & 7)) << 4));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = float(v[e]);
+          s1 += x;
+          s2 = fmaf(float(8 * ch + e + 1), x, s2);
+        }
+      }
+      s1 += __shfl_xor(s1, 1, 64);
+      s2 += __shfl_xor(s2, 1, 64);
+      if (hh == 0) {
+        krs[k * 16 + 0] = f2bf(s1);
+        krs[k * 16 + 1] = f2bf(s1 - bf2f(f2bf(s1)));
+        krs[k * 16 + 2] = f2bf(s2);
+        krs[k * 16 + 3] = f2bf(s2 - bf2f(f2bf(s2)));
+      }
+    };
+
+    floatx4 dqa[DB][2], kra[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) dqa[db][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      kra[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    float* scr = reinterpret_cast<float*>(smem + STAGE_BYTES) + wave * SCR;
+    bf16_t* AP = static_cast<bf16_t*>(fd.ap) + (int64_t(b) * fd.nh + h) * S * S;
+    bf16_t* dAS = static_cast<bf16_t*>(fd.das) + (int64_t(b) * fd.nh + h) * S * S;
+    float* APr = fd.apr + (int64_t(b) * fd.nh + h) * S * nqR * 2;
+    float* dASr = fd.dasr + (int64_t(b) * fd.nh + h) * S * nqR * 2;
+
+    for (int kt = 0; kt < nkt; ++kt) {
+      issue(kt);
+      wait_vmcnt<0>();
+      commit();
+      __syncthreads();  // tile kt in LDS
+      if (chk) {
+        make_kr();
+        __syncthreads();
+      }
+      const int key0 = kt * FT;
+
+      // S^T = K Q^T and dP^T = V dCL^T with their strip rows
+      floatx4 s[8][2], dp[8][2], ks[2], vs[2];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s[j][qb] = dp[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        ks[qb] = vs[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const char* sk = smem + (kk >> 1) * DK::BYTES;
+        const char* sv = smem + OFF_V + (kk >> 1) * DK::BYTES;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const bf16x8 kf = DK::frag(sk, 16 * j, (kk & 1) * 32, lane);
+          const bf16x8 vf = DK::frag(sv, 16 * j, (kk & 1) * 32, lane);
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
+          for (int qb = 0; qb < 2; ++qb) {
             s[j][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][kk], s[j][qb], 0, 0, 0);
+            dp[j][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf[qb][kk], dp[j][qb], 0, 0, 0);
+          }
+        }
+        if (chk) {
+          const bf16_t* kcs = reinterpret_cast<const bf16_t*>(smem + OFF_KC);
+          const bf16_t* vcs = reinterpret_cast<const bf16_t*>(smem + OFF_VC);
+          const bf16x8 kc = *reinterpret_cast<const bf16x8*>(kcs + lq * SCL + 32 * kk + 8 * g);
+          const bf16x8 vc = *reinterpret_cast<const bf16x8*>(vcs + lq * SCL + 32 * kk + 8 * g);
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb) {
+            ks[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc, qf[qb][kk], ks[qb], 0, 0, 0);
+            vs[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vc, gf[qb][kk], vs[qb], 0, 0, 0);
+          }
         }
       }
-      const bool diag = rd.causal && kt == qt;
+      if (fd.n_faults > 0) {
+        inject_tile(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
+        inject_tile(dp, fd, ABFT_OP_DAP, b, h, qw, key0, lane);
+      }
+      if (chk) {
+        check_tile(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
+        check_tile(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr, lane);
+      }
+
+      // P and dS, stored with their row checksums; dS kept (rounded) in s
+      const bool diag = fd.causal && kt == qt;
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         const int q = qw + 16 * qb + lq;
-        float c1[4] = {0.f, 0.f, 0.f, 0.f}, c2[4] = {0.f, 0.f, 0.f, 0.f};
+        float a1[4] = {0.f, 0.f, 0.f, 0.f}, a2[4] = {0.f, 0.f, 0.f, 0.f};
+        float d1[4] = {0.f, 0.f, 0.f, 0.f}, d2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          float a[4];
+          float a[4], ds[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int key = key0 + 16 * j + 4 * g + r;
-            const float p = (diag && key > q)
-                                ? 0.f
-                                : __builtin_amdgcn_exp2f(s[j][qb][r] * sl2 - mq[qb]) * il[qb];
+            const bool live = !(diag && key > q);
+            const float p =
+                live ? __builtin_amdgcn_exp2f(s[j][qb][r] * sl2 - mq[qb]) * il[qb] : 0.f;
             a[r] = bf2f(f2bf(p));
+            ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][qb][r] - dq[qb]))) : 0.f;
+            s[j][qb][r] = ds[r];
           }
-          const uint2 w = {pack2(a[0], a[1]), pack2(a[2], a[3])};
-          *reinterpret_cast<uint2*>(AP + int64_t(q) * S + key0 + 16 * j + 4 * g) = w;
+          const int64_t off = int64_t(q) * S + key0 + 16 * j + 4 * g;
+          *reinterpret_cast<uint2*>(AP + off) = uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
+          *reinterpret_cast<uint2*>(dAS + off) = uint2{pack2(ds[0], ds[1]), pack2(ds[2], ds[3])};
           // the 16-key group j lies in block j >> lg_jpb; weights 1..R in it
           const int wb = ((16 * j) & (R - 1)) + 4 * g + 1;
-          const float s1 = (a[0] + a[1]) + (a[2] + a[3]);
-          const float s2 = float(wb) * a[0] + float(wb + 1) * a[1] + float(wb + 2) * a[2] +
-                           float(wb + 3) * a[3];
+          const float sa1 = (a[0] + a[1]) + (a[2] + a[3]);
+          const float sa2 = float(wb) * a[0] + float(wb + 1) * a[1] + float(wb + 2) * a[2] +
+                            float(wb + 3) * a[3];
+          const float sd1 = (ds[0] + ds[1]) + (ds[2] + ds[3]);
+          const float sd2 = float(wb) * ds[0] + float(wb + 1) * ds[1] + float(wb + 2) * ds[2] +
+                            float(wb + 3) * ds[3];
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             if ((j >> lg_jpb) == i) {
-              c1[i] += s1;
-              c2[i] += s2;
+              a1[i] += sa1; a2[i] += sa2; d1[i] += sd1; d2[i] += sd2;
             }
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (i < NB) {
-            const float t1 = group4_sum(c1[i]), t2 = group4_sum(c2[i]);
+            const float t1 = group4_sum(a1[i]), t2 = group4_sum(a2[i]);
+            const float u1 = group4_sum(d1[i]), u2 = group4_sum(d2[i]);
             if (g == i) {
-              float* o = APr + (int64_t(q) * nqR + key0 / R + i) * 2;
-              o[0] = t1;
-              o[1] = t2;
+              const int64_t o = (int64_t(q) * nqR + key0 / R + i) * 2;
+              APr[o] = t1;
+              APr[o + 1] = t2;
+              dASr[o] = u1;
+              dASr[o + 1] = u2;
             }
           }
         }
+      }
+
+      // dQ^T += K^T dS^T and (dQ^r)^T += (K^r)^T dS^T
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        bf16x8 pf[2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const uint4 u = {pack2(s[2 * t][qb][0], s[2 * t][qb][1]),
+                           pack2(s[2 * t][qb][2], s[2 * t][qb][3]),
+                           pack2(s[2 * t + 1][qb][0], s[2 * t + 1][qb][1]),
+                           pack2(s[2 * t + 1][qb][2], s[2 * t + 1][qb][3])};
+          pf[qb] = __builtin_bit_cast(bf16x8, u);
+        }
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          TrPair kp = kt_frag(smem, 16 * db, 32 * t, lane);
+          const bf16x8 kf = tr_join(kp);
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+            dqa[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, pf[qb], dqa[db][qb], 0, 0, 0);
+        }
+        if (chk) {
+          TrPair rp = kr_frag(krs, 32 * t, lane);
+          const bf16x8 rf = tr_join(rp);
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+            kra[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf[qb], kra[qb], 0, 0, 0);
+        }
+      }
+      __syncthreads();  // the one stage is reloaded next
+    }
+
+    // dQ: round, check against dQ^r, store
+    bf16_t* dQp = static_cast<bf16_t*>(fd.dq) + int64_t(b) * S * fd.ldq + h * D;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int q = qw + 16 * qb + lq;
+      float ov[DB][4];
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ov[db][r] = bf2f(f2bf(dqa[db][qb][r]));
+      if (fd.n_faults > 0) {
+        for (int f = 0; f < fd.n_faults; ++f) {
+          const abft_fault ft = fd.faults[f];
+          if (ft.op != ABFT_OP_DQ || ft.b != b || ft.h != h || ft.row != q) continue;
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (ft.col == 16 * db + 4 * g + r)
+                ov[db][r] = ft.mode == ABFT_FAULT_FLIP ? bf2f(flip_exponent_msb(f2bf(ov[db][r])))
+                                                       : bf2f(f2bf(ft.value));
+        }
+      }
+      if (chk) {
+        const float c1 = __shfl(kra[qb][0] + kra[qb][1], lq, 64);
+        const float c2 = __shfl(kra[qb][2] + kra[qb][3], lq, 64);
+        float r1 = 0.f, ra = 0.f;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            r1 += ov[db][r];
+            ra += fabsf(ov[db][r]);
+          }
+        r1 = group4_sum(r1);
+        ra = group4_sum(ra);
+        uint64_t mask = __ballot(g == 0 && flagged(c1 - r1, ra, fd.e_rel));
+        while (mask) {
+          const int L = __builtin_ctzll(mask);
+          mask &= mask - 1;
+          if (lq == L) {
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) scr[16 * db + 4 * g + r] = ov[db][r];
+          }
+          const float v1 = __shfl(c1, L, 64), v2 = __shfl(c2, L, 64);
+          wave_sync_lds();
+          if (lane == 0) {
+            const int qq = qw + 16 * qb + L;
+            const EecResult res = eec_locate<float>(scr, 1, D, v1, v2, fd.e_rel, fd.tn);
+            int idx = -1;
+            float nv = 0.f;
+            if (res.status == EEC_LOCATED) {
+              idx = res.index;
+              const float old = scr[idx];
+              int action = 0;
+              nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, D, idx, v1, res.d1, fd.tc, &action)));
+              scr[idx] = nv;
+              record_event(fd.report, ABFT_OP_DQ, b, h, qq, idx, classify(old, fd.tn), action, old);
+            }
+            if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, D, v1, fd.e_rel))
+              record_event(fd.report, ABFT_OP_DQ, b, h, qq, 0, ABFT_KIND_NONE,
+                           ABFT_ACT_UNCORRECTABLE, 0.f);
+            scr[D] = __int_as_float(idx);
+            scr[D + 1] = nv;
+          }
+          wave_sync_lds();
+          const int idx = __float_as_int(scr[D]);
+          const float nv = scr[D + 1];
+          if (idx >= 0 && lq == L) {
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (idx == 16 * db + 4 * g + r) ov[db][r] = nv;
+          }
+          wave_sync_lds();
+        }
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const uint2 w = {pack2(ov[db][0], ov[db][1]), pack2(ov[db][2], ov[db][3])};
+        *reinterpret_cast<uint2*>(dQp + int64_t(q) * fd.ldq + 16 * db + 4 * g) = w;
       }
     }
   }
 };
 
 template <int D>
-__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(2)))
-void regen_ap_kernel(RegenDesc rd) {
+__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(D == 64 ? 2 : 1)))
+void fused_bwd_kernel(FusedBwdDesc fd) {
   extern __shared__ __align__(16) char smem[];
-  RegenAP<D>::run(rd, smem);
+  FusedBwd<D>::run(fd, smem);
 }
 
 template <int D, bool PROT>
@@ -753,31 +1156,32 @@ hipError_t launch_d(const FusedDesc& fd, hipStream_t s) {
 }
 
 template <int D>
-hipError_t launch_regen_d(const RegenDesc& rd, hipStream_t s) {
-  using F = RegenAP<D>;
+hipError_t launch_bwd_d(const FusedBwdDesc& fd, hipStream_t s) {
+  using F = FusedBwd<D>;
   static bool attr = false;
   if (!attr) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(regen_ap_kernel<D>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fused_bwd_kernel<D>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
                                              F::LDS_BYTES);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const int64_t grid = int64_t(rd.B) * rd.nh * (rd.S / FT);
+  const int64_t grid = int64_t(fd.B) * fd.nh * (fd.S / FT);
   if (grid == 0) return hipSuccess;
-  auto kern = regen_ap_kernel<D>;
-  hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(FNT), F::LDS_BYTES, s, rd);
+  hipLaunchKernelGGL(fused_bwd_kernel<D>, dim3(unsigned(grid)), dim3(FNT), F::LDS_BYTES, s, fd);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_regen_ap(const RegenDesc& rd, hipStream_t s) {
-  if (rd.S % FT != 0 || rd.R < 16 || FT % rd.R != 0 || rd.H != rd.nh * rd.D ||
-      rd.stats == nullptr || rd.ap == nullptr || rd.apr == nullptr)
+hipError_t launch_fused_bwd(const FusedBwdDesc& fd, hipStream_t s) {
+  if (fd.S % FT != 0 || fd.R < 32 || FT % fd.R != 0 || fd.H != fd.nh * fd.D ||
+      fd.qkv == nullptr || fd.cl == nullptr || fd.dcl == nullptr || fd.stats == nullptr ||
+      fd.ap == nullptr || fd.apr == nullptr || fd.das == nullptr || fd.dasr == nullptr ||
+      fd.dq == nullptr || fd.ldq < fd.H || (fd.check && fd.qkvc == nullptr))
     return hipErrorInvalidValue;
-  if (rd.D == 64) return launch_regen_d<64>(rd, s);
-  if (rd.D == 128) return launch_regen_d<128>(rd, s);
+  if (fd.D == 64) return launch_bwd_d<64>(fd, s);
+  if (fd.D == 128) return launch_bwd_d<128>(fd, s);
   return hipErrorInvalidValue;
 }
 

@@ -230,9 +230,9 @@ def test_fused_rejects_unsupported_shapes():
 
 
 def run_fused_training(shape, faults=(), seed=1):
-    """Fused forward, then the backward (AP regenerated from the softmax
-    statistics), against the fused oracle followed by the layer oracle's
-    backward."""
+    """Fused forward, then the backward with the fused core (scores
+    recomputed from the softmax statistics), against the fused oracle's
+    forward and backward."""
     abft = _abft()
     print(f"[case] fused fwd+bwd {shape.name} causal={shape.causal} R={shape.block_rows} "
           f"faults={len(faults)}", flush=True)
@@ -250,9 +250,10 @@ def run_fused_training(shape, faults=(), seed=1):
              dWo=host(dWo), rep_f=abft.read_report(layer.report),
              rep_b=abft.read_report(layer.report_bwd))
     from oracle import backward
+    from oracle.fused import fused_training_backward
     p = OracleParams(heads=shape.heads, causal=shape.causal, block_rows=shape.block_rows)
     o = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, list(faults))
-    ob = backward(o, inp["dO"], p, list(faults))
+    ob = fused_training_backward(o, inp["dO"], p, list(faults))
     # the materialised layer, fault-free
     m = forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
     o["mat"], o["mat_bwd"], o["dO"] = m, backward(m, inp["dO"], p), inp["dO"]
@@ -281,13 +282,13 @@ def test_fused_forward_backward(causal, R):
 
 
 def check_training_outputs(g, o, ob, shape):
-    """dX and dW^QKV take AP regenerated from the softmax statistics, which
+    """dX and dW^QKV take AP recomputed from the softmax statistics, which
     do not depend on how the keys were grouped: within 1e-2 of the fused
     oracle's backward. O and dW^O take CL: within the rounding bounds of
     the fused oracle's. Against the materialised layer (no fused step on
     the CPU side) the two forms round at different points (AS and AP
-    stored, or P rounded unnormalised): O within its bound, the gradients
-    within 1e-2 in relative norm."""
+    stored, or P rounded unnormalised; dP stored or not): O within its
+    bound, the gradients within 1e-2 in relative norm."""
     m = o["mat"]
     bcl, bo = rounding_bounds(m, shape, False)
     dO = o["dO"].reshape(-1, shape.hidden).astype(np.float64)
@@ -304,12 +305,19 @@ def check_training_outputs(g, o, ob, shape):
         assert nrel <= RTOL, f"{k} vs materialised: relative norm {nrel:.3g}"
 
 
-def test_fused_backward_faults():
-    shape = W.make_shape(1, 256, 128, 2, causal=True, block_rows=128, name="trainf")
+@pytest.mark.parametrize("R", [128, 64])
+def test_fused_backward_faults(R):
+    """Faults in the scores (the forward's and the backward's recomputation
+    both see them), dP, dV, dQ and dX: each located where injected and
+    corrected, events identical to the fused oracle's."""
+    shape = W.make_shape(1, 256, 128, 2, causal=True, block_rows=R, name="trainf")
     faults = [W.Fault("AS", 0, 1, 200, 3, np.inf), W.Fault("dV", 0, 0, 17, 9, np.nan),
-              W.Fault("dQ", 0, 1, 130, 60, 1e10), W.Fault("dX", 0, 0, 77, 100, np.inf)]
+              W.Fault("dQ", 0, 1, 130, 60, 1e10), W.Fault("dX", 0, 0, 77, 100, np.inf),
+              W.Fault("dAP", 0, 0, 250, 249, -1e10), W.Fault("dQ", 0, 0, 31, 5, 40.0),
+              W.Fault("dAP", 0, 1, 100, 7, 0.0, mode="flip")]
     g, o, ob = run_fused_training(shape, faults)
+    assert g["rep_f"]["overflow"] == 0 and g["rep_b"]["overflow"] == 0
     assert sorted(g["rep_f"]["events"]) == sorted(o["events"])
     assert sorted(g["rep_b"]["events"]) == sorted(ob["events"])
-    assert len(o["events"]) + len(ob["events"]) == 4
+    assert len(o["events"]) == 1 and len(ob["events"]) == len(faults)
     check_training_outputs(g, o, ob, shape)
