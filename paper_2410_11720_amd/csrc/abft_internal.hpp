@@ -147,14 +147,15 @@ hipError_t launch_fused_fwd(const FusedDesc& d, hipStream_t stream);
 // Q (K^c)^T), takes P from the forward's softmax statistics, computes
 // dP = dCL V^T (row check against dCL (V^c)^T), dS = scale P (dP - D) with
 // D = dCL . CL, and dQ = dS K (row check against dS K^r, K^r the row
-// checksums of K over the head dims); it stores AP and dS with their row
-// checksums for the dV and dK GEMMs, and dQ.
+// checksums of K over the head dims, encoded beforehand); it stores AP and
+// dS with their row checksums for the dV and dK GEMMs, and dQ.
 struct FusedBwdDesc {
   int B = 0, nh = 0, S = 0, H = 0, D = 0, R = 128;
   int causal = 0;
   float scale = 1.f;
   const void* qkv = nullptr;    // [B*S][3H] bf16: Q | K | V
   const float* qkvc = nullptr;  // [B][S/R][2][3H] propagated column checksums (K^c, V^c)
+  const float* kr = nullptr;    // [B*S][nh][2] row checksums of K over each head's dims
   const void* cl = nullptr;     // [B*S][H] bf16, the forward's context
   const void* dcl = nullptr;    // [B*S][H] bf16
   const float* stats = nullptr; // [B][nh][S][2]: log2-scaled max and sum per query

@@ -49,6 +49,7 @@ struct Layout_ {
   size_t xc, xr, wvr, qkvc, vr, apc, apr, clc, clr, doc, dclc, dasc, dasr, dqkvc;
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
+  size_t kr;        // fused backward: row checksums of K per head [T][nh][2]
   size_t total;
 };
 
@@ -118,6 +119,7 @@ Layout_ make_layout(const Dims& d) {
   L.skp = take((p1 > p2 ? p1 : p2) * f);
   L.skc = take((c1 > c2 ? c1 : c2) * f);
   L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
+  L.kr = take(size_t(d.T) * d.nh * 2 * f);
   L.total = off;
   return L;
 }
@@ -511,13 +513,24 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   const size_t es = d.es;
   const bool pb = p.sec_bwd;
 
-  // dO^c (Sec. 4.6), with the report cleared in the same launch
+  const bool fused = (cfg->flags & ABFT_FLAG_FUSED) != 0;
+  // dO^c (Sec. 4.6) and, for the fused backward core, the row checksums of
+  // K per head (K^r, from the checked K), with the report cleared in the
+  // same launch
   {
-    EncodeJob e;
-    const int nj = ((stages & ABFT_STAGE_ENCODE) && pb) ? 1 : 0;
-    e.A = dO; e.batch = B; e.rows = S; e.cols = H; e.ld = H; e.batch_stride = S * H;
-    e.Rb = int(R); e.Cb = int(hd); e.col_chk = F(L.doc);
-    CK(launch_encode_jobs(&e, nj, dt, (cfg->flags & ABFT_FLAG_REPORT_APPEND) ? nullptr : report,
+    EncodeJob e[2];
+    int nj = 0;
+    if ((stages & ABFT_STAGE_ENCODE) && pb) {
+      EncodeJob& j = e[nj++];
+      j.A = dO; j.batch = B; j.rows = S; j.cols = H; j.ld = H; j.batch_stride = S * H;
+      j.Rb = int(R); j.Cb = int(hd); j.col_chk = F(L.doc);
+    }
+    if ((stages & ABFT_STAGE_ENCODE) && pb && fused) {
+      EncodeJob& j = e[nj++];
+      j.A = ws + L.qkv + H * es; j.batch = B; j.rows = S; j.cols = H; j.ld = 3 * H;
+      j.batch_stride = S * 3 * H; j.Rb = int(R); j.Cb = int(hd); j.row_chk = F(L.kr);
+    }
+    CK(launch_encode_jobs(e, nj, dt, (cfg->flags & ABFT_FLAG_REPORT_APPEND) ? nullptr : report,
                           s));
   }
 
@@ -553,7 +566,6 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   // after a fused forward (no scores kept): the fused backward core, from
   // the forward's softmax statistics, stores AP, dAS (with their row
   // checksums) and the checked dQ; dQ^c for dX's check is encoded from it
-  const bool fused = (cfg->flags & ABFT_FLAG_FUSED) != 0;
   if (fused && (stages & (ABFT_STAGE_CORE_BWD | ABFT_STAGE_DAP | ABFT_STAGE_SOFTMAX_BWD |
                           ABFT_STAGE_DQ))) {
     FusedBwdDesc fd;
@@ -562,6 +574,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     fd.scale = p.scale;
     fd.qkv = ws + L.qkv;
     fd.qkvc = pb ? F(L.qkvc) : nullptr;
+    fd.kr = pb ? F(L.kr) : nullptr;
     fd.cl = ws + L.cl;
     fd.dcl = ws + L.dcl;
     fd.stats = F(L.stats);

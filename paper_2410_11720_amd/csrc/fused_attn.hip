@@ -602,8 +602,8 @@ struct FusedAttn {
 // Fused backward core (after a fused forward, which keeps no scores). Per
 // (batch, head, tile of 128 queries), each of the four waves owning 32
 // queries, key tiles of 128 keys pass through LDS (K and V as K-major
-// images, the K^c and V^c strips, and a K^r strip computed from the K
-// image); per key tile each wave computes
+// images, the K^c and V^c strips, and the strip of K^r, the row checksums
+// of K over the head dims); per key tile each wave computes
 //   S^T = K Q^T (AS^r = Q (K^c)^T from the strip) and checks every
 //     (query, R-key block) vector, as the forward does;
 //   P = exp2(log2(e) scale S - m) / l from the forward's statistics,
@@ -617,7 +617,7 @@ struct FusedAttn {
 //     dS^T fragment a lane assembles from its accumulators.
 // After the last key tile dQ is rounded, row-checked against dQ^r (a
 // located element fixed from the checksum) and stored.
-template <int D>
+template <int D, bool CHK>
 struct FusedBwd {
   static constexpr int KH = D / 64, KS = D / 32, DB = D / 16;
   using DK = Direct<true, FT>;                 // one 64-dim half: [128 keys][64]
@@ -627,8 +627,12 @@ struct FusedBwd {
   static constexpr int OFF_V = IMG, OFF_KC = 2 * IMG, OFF_VC = OFF_KC + STRIP;
   static constexpr int OFF_KR = OFF_VC + STRIP;
   static constexpr int STAGE_BYTES = OFF_KR + FT * 16 * 2;
+  // the workgroup's Q and dCL rows, [128 queries][D] K-major images read as
+  // the B operands of S^T and dP^T (loaded once)
+  static constexpr int OFF_Q = STAGE_BYTES, OFF_G = OFF_Q + IMG;
   static constexpr int SCR = 160;              // floats of rare-path scratch per wave
-  static constexpr int LDS_BYTES = STAGE_BYTES + 4 * SCR * 4;
+  static constexpr int OFF_SCR = OFF_G + IMG;
+  static constexpr int LDS_BYTES = OFF_SCR + 4 * SCR * 4;
 
   // K^T operand fragment (rows: dims rb + lane % 16; k: keys kb + 4g + 0..3
   // and kb + 16 + 4g + 0..3) from the K-major image
@@ -789,11 +793,10 @@ struct FusedBwd {
     const int nkt = fd.causal ? qt + 1 : nqt;
     const float sl2 = fd.scale * 1.4426950408889634f;
     const int lg_jpb = __builtin_ctz(R / 16);
-    const bool chk = fd.check != 0;
+    constexpr bool chk = CHK;
 
-    // Q and dCL as the B operands of S^T and dP^T; the statistics and the
-    // softmax backward's row term D = dCL . CL of the lane's queries
-    bf16x8 qf[2][KS], gf[2][KS];
+    // the statistics and the softmax backward's row term D = dCL . CL of
+    // the lane's queries
     float mq[2], il[2], dq[2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
@@ -801,19 +804,24 @@ struct FusedBwd {
       float acc = 0.f;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
-        qf[qb][kk] = *reinterpret_cast<const bf16x8*>(Qp + int64_t(q) * ld + 32 * kk + 8 * g);
-        gf[qb][kk] = *reinterpret_cast<const bf16x8*>(dCLp + int64_t(q) * H + 32 * kk + 8 * g);
-        const bf16x8 cf = *reinterpret_cast<const bf16x8*>(CLp + int64_t(q) * H + 32 * kk + 8 * g);
+        const bf16x8 gv = *reinterpret_cast<const bf16x8*>(dCLp + int64_t(q) * H + 32 * kk + 8 * g);
+        const bf16x8 cv = *reinterpret_cast<const bf16x8*>(CLp + int64_t(q) * H + 32 * kk + 8 * g);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc = fmaf(float(gf[qb][kk][e]), float(cf[e]), acc);
+        for (int e = 0; e < 8; ++e) acc = fmaf(float(gv[e]), float(cv[e]), acc);
       }
       dq[qb] = group4_sum(acc);
       const float* st = fd.stats + ((int64_t(b) * fd.nh + h) * S + q) * 2;
       mq[qb] = st[0];
       il[qb] = 1.f / st[1];
     }
+    // Q and dCL images of the workgroup's queries (complete with tile 0)
+#pragma unroll
+    for (int hf = 0; hf < KH; ++hf) {
+      DK::issue(Qp, ld, q0, S, hf * 64, smem + OFF_Q + hf * DK::BYTES, wave, lane);
+      DK::issue(dCLp, H, q0, S, hf * 64, smem + OFF_G + hf * DK::BYTES, wave, lane);
+    }
 
-    float kcv[4] = {0.f, 0.f, 0.f, 0.f}, vcv[4] = {0.f, 0.f, 0.f, 0.f};
+    float kcv[4] = {0.f, 0.f, 0.f, 0.f}, vcv[4] = {0.f, 0.f, 0.f, 0.f}, krv = 0.f;
     auto issue = [&](int kt) {
       const int key0 = kt * FT;
 #pragma unroll
@@ -832,6 +840,7 @@ struct FusedBwd {
           kcv[p] = row[H];
           vcv[p] = row[2 * H];
         }
+        krv = fd.kr[((int64_t(b) * S + key0 + (tid >> 1)) * fd.nh + h) * 2 + (tid & 1)];
       }
     };
     auto commit = [&]() {
@@ -850,38 +859,16 @@ struct FusedBwd {
             vcs[r + SCL] = f2bf(vcv[p] - bf2f(f2bf(vcv[p])));
           }
         }
+        bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
+        krs[(tid >> 1) * 16 + 2 * (tid & 1)] = f2bf(krv);
+        krs[(tid >> 1) * 16 + 2 * (tid & 1) + 1] = f2bf(krv - bf2f(f2bf(krv)));
       }
     };
     // K^r strip: columns 0..3 per key (hi/lo of the sum and of the 1-based
-    // weighted sum over the head dims) from the K image; columns 4..15 zero
+    // weighted sum over the head dims, written with each tile); 4..15 zero
     bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
     if (chk)
       for (int e = tid; e < FT * 12; e += FNT) krs[(e / 12) * 16 + 4 + e % 12] = 0;
-    auto make_kr = [&]() {
-      const int k = tid >> 1, hh = tid & 1;
-      float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-      for (int i = 0; i < D / 16; ++i) {
-        const int ch = hh * (D / 16) + i;      // 8-dim chunk of the key row
-        const char* half = smem + (ch >> 3) * DK::BYTES;
-        const bf16x8 v =
-            *reinterpret_cast<const bf16x8*>(half + k * 128 + (((ch & 7) ^ (k & 7)) << 4));
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float x = float(v[e]);
-          s1 += x;
-          s2 = fmaf(float(8 * ch + e + 1), x, s2);
-        }
-      }
-      s1 += __shfl_xor(s1, 1, 64);
-      s2 += __shfl_xor(s2, 1, 64);
-      if (hh == 0) {
-        krs[k * 16 + 0] = f2bf(s1);
-        krs[k * 16 + 1] = f2bf(s1 - bf2f(f2bf(s1)));
-        krs[k * 16 + 2] = f2bf(s2);
-        krs[k * 16 + 3] = f2bf(s2 - bf2f(f2bf(s2)));
-      }
-    };
 
     floatx4 dqa[DB][2], kra[2];
 #pragma unroll
@@ -890,7 +877,7 @@ struct FusedBwd {
       for (int db = 0; db < DB; ++db) dqa[db][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
       kra[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
-    float* scr = reinterpret_cast<float*>(smem + STAGE_BYTES) + wave * SCR;
+    float* scr = reinterpret_cast<float*>(smem + OFF_SCR) + wave * SCR;
     bf16_t* AP = static_cast<bf16_t*>(fd.ap) + (int64_t(b) * fd.nh + h) * S * S;
     bf16_t* dAS = static_cast<bf16_t*>(fd.das) + (int64_t(b) * fd.nh + h) * S * S;
     float* APr = fd.apr + (int64_t(b) * fd.nh + h) * S * nqR * 2;
@@ -901,103 +888,146 @@ struct FusedBwd {
       wait_vmcnt<0>();
       commit();
       __syncthreads();  // tile kt in LDS
-      if (chk) {
-        make_kr();
-        __syncthreads();
-      }
       const int key0 = kt * FT;
 
-      // S^T = K Q^T and dP^T = V dCL^T with their strip rows
-      floatx4 s[8][2], dp[8][2], ks[2], vs[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) s[j][qb] = dp[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        ks[qb] = vs[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-      }
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        const char* sk = smem + (kk >> 1) * DK::BYTES;
-        const char* sv = smem + OFF_V + (kk >> 1) * DK::BYTES;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const bf16x8 kf = DK::frag(sk, 16 * j, (kk & 1) * 32, lane);
-          const bf16x8 vf = DK::frag(sv, 16 * j, (kk & 1) * 32, lane);
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            s[j][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][kk], s[j][qb], 0, 0, 0);
-            dp[j][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf[qb][kk], dp[j][qb], 0, 0, 0);
-          }
-        }
-        if (chk) {
-          const bf16_t* kcs = reinterpret_cast<const bf16_t*>(smem + OFF_KC);
-          const bf16_t* vcs = reinterpret_cast<const bf16_t*>(smem + OFF_VC);
-          const bf16x8 kc = *reinterpret_cast<const bf16x8*>(kcs + lq * SCL + 32 * kk + 8 * g);
-          const bf16x8 vc = *reinterpret_cast<const bf16x8*>(vcs + lq * SCL + 32 * kk + 8 * g);
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            ks[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc, qf[qb][kk], ks[qb], 0, 0, 0);
-            vs[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vc, gf[qb][kk], vs[qb], 0, 0, 0);
-          }
-        }
-      }
-      if (fd.n_faults > 0) {
-        inject_tile(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
-        inject_tile(dp, fd, ABFT_OP_DAP, b, h, qw, key0, lane);
-      }
-      if (chk) {
-        check_tile(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
-        check_tile(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr, lane);
-      }
-
-      // P and dS, stored with their row checksums; dS kept (rounded) in s
       const bool diag = fd.causal && kt == qt;
+      // B operand fragments of the wave's queries (rows of the Q or dCL image)
+      auto bfrag = [&](int off, int qb, int kk) {
+        return DK::frag(smem + off + (kk >> 1) * DK::BYTES, wave * 32 + 16 * qb, (kk & 1) * 32, lane);
+      };
+      // P^T, then dS^T, packed to bf16: pk[j][qb] holds keys 16 j + 4 g + 0..3
+      // of query 16 qb + lane % 16
+      uint2 pk[8][2];
+      {
+        // S^T = K Q^T with its strip rows, checked; P from the statistics
+        floatx4 s[8][2], ks[2];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        const int q = qw + 16 * qb + lq;
-        float a1[4] = {0.f, 0.f, 0.f, 0.f}, a2[4] = {0.f, 0.f, 0.f, 0.f};
-        float d1[4] = {0.f, 0.f, 0.f, 0.f}, d2[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int qb = 0; qb < 2; ++qb) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          float a[4], ds[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int key = key0 + 16 * j + 4 * g + r;
-            const bool live = !(diag && key > q);
-            const float p =
-                live ? __builtin_amdgcn_exp2f(s[j][qb][r] * sl2 - mq[qb]) * il[qb] : 0.f;
-            a[r] = bf2f(f2bf(p));
-            ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][qb][r] - dq[qb]))) : 0.f;
-            s[j][qb][r] = ds[r];
-          }
-          const int64_t off = int64_t(q) * S + key0 + 16 * j + 4 * g;
-          *reinterpret_cast<uint2*>(AP + off) = uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
-          *reinterpret_cast<uint2*>(dAS + off) = uint2{pack2(ds[0], ds[1]), pack2(ds[2], ds[3])};
-          // the 16-key group j lies in block j >> lg_jpb; weights 1..R in it
-          const int wb = ((16 * j) & (R - 1)) + 4 * g + 1;
-          const float sa1 = (a[0] + a[1]) + (a[2] + a[3]);
-          const float sa2 = float(wb) * a[0] + float(wb + 1) * a[1] + float(wb + 2) * a[2] +
-                            float(wb + 3) * a[3];
-          const float sd1 = (ds[0] + ds[1]) + (ds[2] + ds[3]);
-          const float sd2 = float(wb) * ds[0] + float(wb + 1) * ds[1] + float(wb + 2) * ds[2] +
-                            float(wb + 3) * ds[3];
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if ((j >> lg_jpb) == i) {
-              a1[i] += sa1; a2[i] += sa2; d1[i] += sd1; d2[i] += sd2;
-            }
+          for (int j = 0; j < 8; ++j) s[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+          ks[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (i < NB) {
-            const float t1 = group4_sum(a1[i]), t2 = group4_sum(a2[i]);
-            const float u1 = group4_sum(d1[i]), u2 = group4_sum(d2[i]);
-            if (g == i) {
-              const int64_t o = (int64_t(q) * nqR + key0 / R + i) * 2;
-              APr[o] = t1;
-              APr[o + 1] = t2;
-              dASr[o] = u1;
-              dASr[o + 1] = u2;
+        for (int kk = 0; kk < KS; ++kk) {
+          const bf16x8 qf0 = bfrag(OFF_Q, 0, kk), qf1 = bfrag(OFF_Q, 1, kk);
+          const char* sk = smem + (kk >> 1) * DK::BYTES;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const bf16x8 kf = DK::frag(sk, 16 * j, (kk & 1) * 32, lane);
+            s[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf0, s[j][0], 0, 0, 0);
+            s[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf1, s[j][1], 0, 0, 0);
+          }
+          if (chk) {
+            const bf16_t* kcs = reinterpret_cast<const bf16_t*>(smem + OFF_KC);
+            const bf16x8 kc = *reinterpret_cast<const bf16x8*>(kcs + lq * SCL + 32 * kk + 8 * g);
+            ks[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc, qf0, ks[0], 0, 0, 0);
+            ks[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc, qf1, ks[1], 0, 0, 0);
+          }
+        }
+        if (fd.n_faults > 0) inject_tile(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
+        if (chk) check_tile(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const int q = qw + 16 * qb + lq;
+          float a1[4] = {0.f, 0.f, 0.f, 0.f}, a2[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            float a[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
+              a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][qb][r] * sl2 - mq[qb]) * il[qb]))
+                          : 0.f;
+            }
+            pk[j][qb] = uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
+            *reinterpret_cast<uint2*>(AP + int64_t(q) * S + key0 + 16 * j + 4 * g) = pk[j][qb];
+            if (!chk) continue;
+            // the 16-key group j lies in block j >> lg_jpb; weights 1..R in it
+            const int wb = ((16 * j) & (R - 1)) + 4 * g + 1;
+            const float sa1 = (a[0] + a[1]) + (a[2] + a[3]);
+            const float sa2 = float(wb) * a[0] + float(wb + 1) * a[1] + float(wb + 2) * a[2] +
+                              float(wb + 3) * a[3];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if ((j >> lg_jpb) == i) { a1[i] += sa1; a2[i] += sa2; }
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (chk && i < NB) {
+              const float t1 = group4_sum(a1[i]), t2 = group4_sum(a2[i]);
+              if (g == i) {
+                const int64_t o = (int64_t(q) * nqR + key0 / R + i) * 2;
+                APr[o] = t1;
+                APr[o + 1] = t2;
+              }
+            }
+          }
+        }
+      }
+      {
+        // dP^T = V dCL^T with its strip rows, checked; dS from P and dP
+        floatx4 dp[8][2], vs[2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) dp[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+          vs[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          const bf16x8 gf0 = bfrag(OFF_G, 0, kk), gf1 = bfrag(OFF_G, 1, kk);
+          const char* sv = smem + OFF_V + (kk >> 1) * DK::BYTES;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const bf16x8 vf = DK::frag(sv, 16 * j, (kk & 1) * 32, lane);
+            dp[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf0, dp[j][0], 0, 0, 0);
+            dp[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf1, dp[j][1], 0, 0, 0);
+          }
+          if (chk) {
+            const bf16_t* vcs = reinterpret_cast<const bf16_t*>(smem + OFF_VC);
+            const bf16x8 vc = *reinterpret_cast<const bf16x8*>(vcs + lq * SCL + 32 * kk + 8 * g);
+            vs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vc, gf0, vs[0], 0, 0, 0);
+            vs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vc, gf1, vs[1], 0, 0, 0);
+          }
+        }
+        if (fd.n_faults > 0) inject_tile(dp, fd, ABFT_OP_DAP, b, h, qw, key0, lane);
+        if (chk) check_tile(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr, lane);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const int q = qw + 16 * qb + lq;
+          float d1[4] = {0.f, 0.f, 0.f, 0.f}, d2[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float a[4] = {__uint_as_float(pk[j][qb].x << 16),
+                                __uint_as_float(pk[j][qb].x & 0xffff0000u),
+                                __uint_as_float(pk[j][qb].y << 16),
+                                __uint_as_float(pk[j][qb].y & 0xffff0000u)};
+            float ds[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
+              ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][qb][r] - dq[qb]))) : 0.f;
+            }
+            pk[j][qb] = uint2{pack2(ds[0], ds[1]), pack2(ds[2], ds[3])};
+            *reinterpret_cast<uint2*>(dAS + int64_t(q) * S + key0 + 16 * j + 4 * g) = pk[j][qb];
+            if (!chk) continue;
+            const int wb = ((16 * j) & (R - 1)) + 4 * g + 1;
+            const float sd1 = (ds[0] + ds[1]) + (ds[2] + ds[3]);
+            const float sd2 = float(wb) * ds[0] + float(wb + 1) * ds[1] + float(wb + 2) * ds[2] +
+                              float(wb + 3) * ds[3];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if ((j >> lg_jpb) == i) { d1[i] += sd1; d2[i] += sd2; }
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (chk && i < NB) {
+              const float u1 = group4_sum(d1[i]), u2 = group4_sum(d2[i]);
+              if (g == i) {
+                const int64_t o = (int64_t(q) * nqR + key0 / R + i) * 2;
+                dASr[o] = u1;
+                dASr[o + 1] = u2;
+              }
             }
           }
         }
@@ -1009,10 +1039,8 @@ struct FusedBwd {
         bf16x8 pf[2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-          const uint4 u = {pack2(s[2 * t][qb][0], s[2 * t][qb][1]),
-                           pack2(s[2 * t][qb][2], s[2 * t][qb][3]),
-                           pack2(s[2 * t + 1][qb][0], s[2 * t + 1][qb][1]),
-                           pack2(s[2 * t + 1][qb][2], s[2 * t + 1][qb][3])};
+          const uint4 u = {pk[2 * t][qb].x, pk[2 * t][qb].y, pk[2 * t + 1][qb].x,
+                           pk[2 * t + 1][qb].y};
           pf[qb] = __builtin_bit_cast(bf16x8, u);
         }
 #pragma unroll
@@ -1123,11 +1151,13 @@ struct FusedBwd {
   }
 };
 
-template <int D>
-__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(D == 64 ? 2 : 1)))
+// one wave per SIMD for the checked kernels: their registers fit without
+// spills (two waves per SIMD spilled and ran slower)
+template <int D, bool CHK>
+__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(D == 64 && !CHK ? 2 : 1)))
 void fused_bwd_kernel(FusedBwdDesc fd) {
   extern __shared__ __align__(16) char smem[];
-  FusedBwd<D>::run(fd, smem);
+  FusedBwd<D, CHK>::run(fd, smem);
 }
 
 template <int D, bool PROT>
@@ -1155,20 +1185,21 @@ hipError_t launch_d(const FusedDesc& fd, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int D>
+template <int D, bool CHK>
 hipError_t launch_bwd_d(const FusedBwdDesc& fd, hipStream_t s) {
-  using F = FusedBwd<D>;
+  using F = FusedBwd<D, CHK>;
   static bool attr = false;
   if (!attr) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fused_bwd_kernel<D>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             F::LDS_BYTES);
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(fused_bwd_kernel<D, CHK>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, F::LDS_BYTES);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int64_t grid = int64_t(fd.B) * fd.nh * (fd.S / FT);
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL(fused_bwd_kernel<D>, dim3(unsigned(grid)), dim3(FNT), F::LDS_BYTES, s, fd);
+  hipLaunchKernelGGL((fused_bwd_kernel<D, CHK>), dim3(unsigned(grid)), dim3(FNT), F::LDS_BYTES, s,
+                     fd);
   return hipGetLastError();
 }
 
@@ -1178,10 +1209,10 @@ hipError_t launch_fused_bwd(const FusedBwdDesc& fd, hipStream_t s) {
   if (fd.S % FT != 0 || fd.R < 32 || FT % fd.R != 0 || fd.H != fd.nh * fd.D ||
       fd.qkv == nullptr || fd.cl == nullptr || fd.dcl == nullptr || fd.stats == nullptr ||
       fd.ap == nullptr || fd.apr == nullptr || fd.das == nullptr || fd.dasr == nullptr ||
-      fd.dq == nullptr || fd.ldq < fd.H || (fd.check && fd.qkvc == nullptr))
+      fd.dq == nullptr || fd.ldq < fd.H || (fd.check && (fd.qkvc == nullptr || fd.kr == nullptr)))
     return hipErrorInvalidValue;
-  if (fd.D == 64) return launch_bwd_d<64>(fd, s);
-  if (fd.D == 128) return launch_bwd_d<128>(fd, s);
+  if (fd.D == 64) return fd.check ? launch_bwd_d<64, true>(fd, s) : launch_bwd_d<64, false>(fd, s);
+  if (fd.D == 128) return fd.check ? launch_bwd_d<128, true>(fd, s) : launch_bwd_d<128, false>(fd, s);
   return hipErrorInvalidValue;
 }
 
