@@ -7,16 +7,23 @@ accumulation) on seeded synthetic inputs already resident in HBM, with
 the workload's fault schedule: 1 to 4 extreme faults (INF, NaN, +-1e10)
 in one step out of ten, spread over forward and backward GEMM outputs.
 
+The headline runs the fused path (the attention core's forward in one
+kernel, its backward in one kernel that recomputes the scores; no score
+matrix kept between the passes); the materialised path (scores and
+probabilities stored) is measured beside it.
+
 Printed (one JSON line): protected-layer TFLOP/s (useful GEMM flops only;
 checksum work is overhead), the ABFT overhead against the same kernels
 unprotected, the dominant kernel's roofline fraction measured with HIP
-events, and the CPU oracle timed on a bounded sample on the host.
+events, every stage's fraction of its bound, the other workloads' step
+times, a vendor-library yardstick, and the CPU oracle timed on a bounded
+sample on the host.
 
 Profiling helpers (they run committed code only):
-  --pmc-workload        launch the largest kernels (QKV projection, score
-                        GEMM, softmax forward and backward) and a plain copy
-                        of known size, for `rocprofv3 --pmc FETCH_SIZE` /
-                        `WRITE_SIZE`
+  --pmc-workload        launch the largest kernels (fused backward core,
+                        fused forward, QKV projection, score GEMM, softmax
+                        forward and backward) and a plain copy of known size,
+                        for `rocprofv3 --pmc FETCH_SIZE` / `WRITE_SIZE`
   --summarize DIR...    print a short summary of rocprofv3 result databases
   --traffic-from F W    HBM bytes per launch of those kernels from the
                         FETCH_SIZE (F) and WRITE_SIZE (W) runs, scaled by the
@@ -51,48 +58,56 @@ def useful_flops(B, S, H, nh, causal, backward=True):
     return fwd * (3 if backward else 1)
 
 
-# stages made of more than one kernel launch (checksum encodes; split-K
-# weight gradients = slice GEMM + reduce/check): not used for the roofline
-MULTI_KERNEL = {"encode", "dWo", "dWqkv"}
+def stage_table(B, S, H, nh, causal, fused, es=2):
+    """Algorithmic work of each stage of a path: (name, is_bwd, mask, kind,
+    amount, launches) with kind 'flop' (GEMM) or 'byte' (HBM-bound).
+    Masked products count only the unmasked pairs."""
+    d, T = H // nh, B * S
+    P = S * (S + 1) // 2 if causal else S * S
+    sq = B * nh * P            # unmasked score entries
+    stats = B * nh * S * 2 * 4
+    enc = ("encode", False, 0x001, "byte",
+           (T * H + 3 * H * H) * es + (B * S // 128 * 2 * H + 4 * T * nh) * 4, 1)
+    head = [enc, ("qkv", False, 0x002, "flop", 2 * T * H * 3 * H, 1)]
+    tail_f = [("out", False, 0x020, "flop", 2 * T * H * H, 1)]
+    gemms_b = [("dCL", True, 0x002, "flop", 2 * T * H * H, 1),
+               ("dWo", True, 0x004, "flop", 2 * T * H * H, 2)]
+    tail_b = [("dV", True, 0x010, "flop", 2 * sq * d, 1),
+              ("dK", True, 0x080, "flop", 2 * sq * d, 1),
+              ("dWqkv", True, 0x100, "flop", 2 * T * H * 3 * H, 2),
+              ("dX", True, 0x200, "flop", 2 * T * H * 3 * H, 1)]
+    if fused:
+        # the fused forward: Q, K, V read, CL written, statistics; the core:
+        # Q, K, V, dCL, CL and the statistics read, AP and dAS written over
+        # the unmasked pairs, dQ written. The output projection and dX
+        # stages encode CL^c and dQ^c first (two launches)
+        return head + [
+            ("attn", False, 0x004, "flop", 4 * sq * d, 1)] + [
+            ("out", False, 0x020, "flop", 2 * T * H * H, 2)] + [
+            ("encode_dO", True, 0x001, "byte", 2 * T * H * es, 1)] + gemms_b + [
+            ("core_bwd", True, 0x400, "byte", 2 * sq * es + 6 * T * H * es + stats, 1)] + \
+            tail_b[:3] + [("dX", True, 0x200, "flop", 2 * T * H * 3 * H, 2)]
+    return head + [
+        # K = head_dim: the score-shaped output is the traffic
+        ("score", False, 0x004, "byte", sq * es + 2 * T * H * es, 1),
+        ("softmax", False, 0x008, "byte", 2 * sq * es, 1),
+        ("context", False, 0x010, "flop", 2 * sq * d, 1)] + tail_f + [
+        ("encode_dO", True, 0x001, "byte", T * H * es, 1)] + gemms_b + [
+        ("dAP", True, 0x008, "byte", sq * es + 2 * T * H * es, 1),
+        ("softmax_bwd", True, 0x020, "byte", 3 * sq * es, 1),
+        ("dQ", True, 0x040, "flop", 2 * sq * d, 1)] + tail_b
 
-# kernel symbol (as rocprofv3 names it) of single-kernel stages at the
-# workload shape, protected instantiation
-# (kernel symbol, grid size in workgroups): the QKV and output projections
-# share one instantiation and differ by grid
+
+# kernel symbol (as rocprofv3 names it) and grid (workgroups) of the stages
+# whose HBM traffic is recorded, at the workload shape, protected
 KERNEL_OF_STAGE = {
+    "core_bwd": ("fused_bwd_kernel<64, true>", 768),
+    "attn": ("fused_attn_kernel<64, true>", 768),
     "qkv": ("gemm_kernel<unsigned short, unsigned short, true, false, 128, 128, true, 2, true, true>", 1152),
     "softmax_bwd": ("softmax_kernel<unsigned short, 2, true, 1, true, true>", 768),
     "softmax": ("softmax_kernel<unsigned short, 2, false, 1, true, true>", 768),
     "score": ("gemm_kernel<unsigned short, unsigned short, true, true, 128, 128, true, 1, true, true>", 3456),
 }
-
-
-def stage_table(B, S, H, nh, causal, es=2):
-    """Algorithmic work of each stage: (name, is_bwd, mask, kind, amount)
-    with kind 'flop' (GEMM) or 'byte' (HBM-bound). Masked products count
-    only the unmasked pairs."""
-    d, T = H // nh, B * S
-    P = S * (S + 1) // 2 if causal else S * S
-    sq = B * nh * P            # unmasked score entries
-    return [
-        ("encode", False, 0x001, "byte", (T * H + 3 * H * H) * es + (B * S // 128 * 2 * H + 4 * T * nh) * 4),
-        ("qkv", False, 0x002, "flop", 2 * T * H * 3 * H),
-        # K = head_dim: the score-shaped output is the traffic
-        ("score", False, 0x004, "byte", sq * es + 2 * T * H * es),
-        ("softmax", False, 0x008, "byte", 2 * sq * es),
-        ("context", False, 0x010, "flop", 2 * sq * d),
-        ("out", False, 0x020, "flop", 2 * T * H * H),
-        ("encode_dO", True, 0x001, "byte", T * H * es),
-        ("dCL", True, 0x002, "flop", 2 * T * H * H),
-        ("dWo", True, 0x004, "flop", 2 * T * H * H),
-        ("dAP", True, 0x008, "byte", sq * es + 2 * T * H * es),
-        ("dV", True, 0x010, "flop", 2 * sq * d),
-        ("softmax_bwd", True, 0x020, "byte", 3 * sq * es),
-        ("dQ", True, 0x040, "flop", 2 * sq * d),
-        ("dK", True, 0x080, "flop", 2 * sq * d),
-        ("dWqkv", True, 0x100, "flop", 2 * T * H * 3 * H),
-        ("dX", True, 0x200, "flop", 2 * T * H * 3 * H),
-    ]
 
 
 # the sources each kernel family is built from: counters taken on other
@@ -103,6 +118,10 @@ KERNEL_SOURCES = {
     "gemm_kernel": ("paper_2410_11720_amd/csrc/gemm_abft.hip",
                     "paper_2410_11720_amd/csrc/direct_lds.hpp") + _COMMON_SOURCES,
     "softmax_kernel": ("paper_2410_11720_amd/csrc/softmax_abft.hip",) + _COMMON_SOURCES,
+    "fused_attn_kernel": ("paper_2410_11720_amd/csrc/fused_attn.hip",
+                          "paper_2410_11720_amd/csrc/direct_lds.hpp") + _COMMON_SOURCES,
+    "fused_bwd_kernel": ("paper_2410_11720_amd/csrc/fused_attn.hip",
+                         "paper_2410_11720_amd/csrc/direct_lds.hpp") + _COMMON_SOURCES,
 }
 
 
@@ -144,38 +163,38 @@ def stored_traffic(kernel):
     return None
 
 
-def cpu_baseline(shape, seed, batch=None):
-    """The oracle, as it stands, on `batch` batch elements of the workload
-    (all of them by default; forward + backward with one injected fault);
-    throughput in the metric's unit."""
+def cpu_baseline(shape, seed, batch):
+    """The oracle of the headline path (fused forward and fused backward
+    core), as it stands, on `batch` batch elements of the workload (forward
+    + backward with one injected fault); throughput in the metric's unit."""
     import workloads as W
-    from oracle import OracleParams, forward, backward
+    from oracle import OracleParams
+    from oracle.fused import fused_forward, fused_training_backward
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    nb = batch or shape.batch
-    sample = W.make_shape(nb, shape.seq, shape.hidden, shape.heads, causal=shape.causal,
+    sample = W.make_shape(batch, shape.seq, shape.hidden, shape.heads, causal=shape.causal,
                           dtype=shape.dtype, block_rows=shape.block_rows)
     inp = W.make_inputs(sample, seed)
     faults = W.draw_faults(sample, seed + 1, 1, W.ALL_OPS, ["inf"])
     p = OracleParams(heads=sample.heads, causal=sample.causal, dtype=sample.dtype,
                      block_rows=sample.block_rows)
     t0 = time.perf_counter()
-    f = forward(inp["X"], inp["Wqkv"], inp["Wo"], p, faults)
-    b = backward(f, inp["dO"], p, faults)
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, faults)
+    b = fused_training_backward(f, inp["dO"], p, faults)
     dt = time.perf_counter() - t0
-    assert len(f["events"]) + len(b["events"]) == 1
-    fl = useful_flops(nb, sample.seq, sample.hidden, sample.heads, sample.causal)
+    assert 1 <= len(f["events"]) + len(b["events"]) <= 2
+    fl = useful_flops(batch, sample.seq, sample.hidden, sample.heads, sample.causal)
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{nb} of {shape.batch} batch elements ({sample.name}), fwd+bwd with one "
-                      f"injected fault, float64 numpy; {dt:.2f} s"}
+            "sample": f"{batch} of {shape.batch} batch elements of {shape.name}, fused "
+                      f"forward + fused backward core oracle, fwd+bwd with one injected "
+                      f"fault, float64 numpy; {dt:.2f} s"}
 
 
-class Layer:
-    """The workload's layer on the GPU: inputs, outputs and one protected
-    and one unprotected instance of the library's layer."""
+class Workload:
+    """One workload's inputs and outputs on the GPU."""
 
     def __init__(self, key):
         import torch
@@ -184,57 +203,315 @@ class Layer:
         self.torch, self.W, self.abft = torch, W, abft
         self.key = key
         self.shape = shape = W.CONFIGS[key]
-        B, S, H, nh = shape.batch, shape.seq, shape.hidden, shape.heads
-        dev = "cuda"
+        B, S, H = shape.batch, shape.seq, shape.hidden
         torch.cuda.set_device(0)
         inp = W.make_inputs(shape, W.data_seed(key))
         self.tdt = tdt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
         self.X, self.Wqkv, self.Wo, self.dO = (
-            torch.from_numpy(inp[k]).to(dev).to(tdt) for k in ("X", "Wqkv", "Wo", "dO"))
+            torch.from_numpy(inp[k]).to("cuda").to(tdt) for k in ("X", "Wqkv", "Wo", "dO"))
+        self.O = torch.empty((B, S, H), dtype=tdt, device="cuda")
+        self.dX = torch.empty_like(self.O)
+        self.dWqkv = torch.empty((H, 3 * H), dtype=torch.float32, device="cuda")
+        self.dWo = torch.empty((H, H), dtype=torch.float32, device="cuda")
+        self.stream = torch.cuda.current_stream()
+
+    def fused_ok(self):
+        s = self.shape
+        return s.dtype == "bf16" and s.seq % 128 == 0 and s.head_dim in (64, 128)
+
+
+class Path:
+    """A protected and an unprotected instance of the library's layer, with
+    the attention core fused or materialised."""
+
+    def __init__(self, wl, fused, root_check=True):
+        self.wl, self.fused = wl, fused
+        abft, s = wl.abft, wl.shape
 
         def make(protect):
-            cfg = abft.LayerConfig(B, S, H, nh, dtype=shape.dtype, causal=shape.causal,
-                                   block_rows=shape.block_rows, protect=protect)
-            return cfg, abft.ProtectedAttention(cfg, dev)
+            cfg = abft.LayerConfig(s.batch, s.seq, s.hidden, s.heads, dtype=s.dtype,
+                                   causal=s.causal, block_rows=s.block_rows, protect=protect,
+                                   root_check=root_check, fused=fused)
+            return cfg, abft.ProtectedAttention(cfg, "cuda")
 
         self.cfg_p, self.lay_p = make(True)
         self.cfg_u, self.lay_u = make(False)
-        self.O = torch.empty((B, S, H), dtype=tdt, device=dev)
-        self.dX = torch.empty_like(self.O)
-        self.dWqkv = torch.empty((H, 3 * H), dtype=torch.float32, device=dev)
-        self.dWo = torch.empty((H, H), dtype=torch.float32, device=dev)
-        self.stream = torch.cuda.current_stream()
 
     def step(self, lay, faults):
-        lay.forward(self.X, self.Wqkv, self.Wo, faults, O=self.O)
-        lay.backward(self.dO, self.X, self.Wqkv, self.Wo, faults, dX=self.dX, dWqkv=self.dWqkv,
-                     dWo=self.dWo)
+        wl = self.wl
+        lay.forward(wl.X, wl.Wqkv, wl.Wo, faults, O=wl.O)
+        if wl.shape.backward:
+            lay.backward(wl.dO, wl.X, wl.Wqkv, wl.Wo, faults, dX=wl.dX, dWqkv=wl.dWqkv,
+                         dWo=wl.dWo)
+
+    def events(self, lay):
+        a = self.wl.abft
+        rf = a.read_report(lay.report)
+        ev, unc = list(rf["events"]), rf["n_uncorrectable"]
+        if self.wl.shape.backward:
+            rb = a.read_report(lay.report_bwd)
+            ev += rb["events"]
+            unc += rb["n_uncorrectable"]
+        return ev, unc
 
     def run_stage(self, mask, is_bwd, protect=True):
-        a = self.abft
+        wl, a = self.wl, self.wl.abft
         cfg, lay = (self.cfg_p, self.lay_p) if protect else (self.cfg_u, self.lay_u)
         if is_bwd:
-            a.attn_abft_backward_stages(cfg, self.dO, self.X, self.Wqkv, self.Wo,
-                                        lay.workspace, self.dX, self.dWqkv, self.dWo, None, 0,
-                                        lay.report_bwd, mask, self.stream, append=True)
+            a.attn_abft_backward_stages(cfg, wl.dO, wl.X, wl.Wqkv, wl.Wo, lay.workspace, wl.dX,
+                                        wl.dWqkv, wl.dWo, None, 0, lay.report_bwd, mask,
+                                        wl.stream, append=True)
         else:
-            a.attn_abft_forward_stages(cfg, self.X, self.Wqkv, self.Wo, self.O,
-                                       lay.workspace, None, 0, lay.report, mask, self.stream,
-                                       append=True)
+            a.attn_abft_forward_stages(cfg, wl.X, wl.Wqkv, wl.Wo, wl.O, lay.workspace, None, 0,
+                                       lay.report, mask, wl.stream, append=True)
+
+
+def timed(path, lay, schedule):
+    """Wall time per step over the whole loop, and per-step durations from
+    HIP events on the launch stream."""
+    torch, st = path.wl.torch, path.wl.stream
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(schedule) + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(st)
+    for i, f in enumerate(schedule):
+        path.step(lay, f)
+        ev[i + 1].record(st)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / len(schedule) * 1e3
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(len(schedule))])
+    return wall, per
+
+
+def stage_us(path, mask, is_bwd, protect, reps):
+    """Mean duration of one call of a stage, from HIP events on the launch
+    stream around `reps` back-to-back calls."""
+    torch, st = path.wl.torch, path.wl.stream
+    path.run_stage(mask, is_bwd, protect)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(reps):
+        path.run_stage(mask, is_bwd, protect)
+    e1.record(st)
+    e1.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+KINDS = ["inf", "nan", "+1e10", "-1e10"]
+
+
+def fault_lists(key, shape, steps):
+    """Each step's faults (host lists) as the workload states them:
+    c1  one INF in Q, one NaN in the scores, one near-INF (1e10) in the
+        context output, every other step (the others fault-free);
+    c2  one fault per step in Q, K, V, the scores, the context, O, dX or a
+        weight gradient, kind uniform over INF, NaN and +-1e10;
+    c3  1-4 faults in one step of ten over every protected output;
+    c4  one fault per step in the scores, Q or dW^Q, INF, NaN or +-1e10;
+    c5  {0, 1, 4, 16} faults per step (cycling) over every protected
+        output, magnitudes 1e6, 1e10, 1e30 (cycling per four steps)."""
+    import workloads as W
+    out = []
+    for k in range(steps):
+        seed = W.fault_seed(key, k)
+        rng = np.random.default_rng(seed)
+        if key == "c1":
+            fl = [] if k % 2 else (W.draw_faults(shape, seed, 1, ["Q"], ["inf"])
+                                   + W.draw_faults(shape, seed + 1, 1, ["AS"], ["nan"])
+                                   + W.draw_faults(shape, seed + 2, 1, ["CL"], ["1e10"]))
+        elif key == "c2":
+            fl = W.draw_faults(shape, seed, 1, ["Q", "K", "V", "AS", "CL", "O", "dX", "dWQ",
+                                                "dWK", "dWV", "dWO"], KINDS)
+        elif key == "c3":
+            fl = (W.draw_faults(shape, seed, int(rng.integers(1, 5)), W.ALL_OPS, KINDS)
+                  if k % 10 == 0 else [])
+        elif key == "c4":
+            fl = W.draw_faults(shape, seed, 1, ["AS", "Q", "dWQ"], KINDS)
+        else:
+            n = (0, 1, 4, 16)[k % 4]
+            mag = ("1e6", "1e10", "1e30")[(k // 4) % 3]
+            fl = W.draw_faults(shape, seed, n, W.ALL_OPS, [mag]) if n else []
+        out.append(fl)
+    return out
+
+
+def verify_schedule(path, lists, limit=40):
+    """Untimed: every faulty step of the schedule (up to `limit`) run once
+    more, its report read: the positions reported must be exactly the
+    injected ones, none uncorrectable. Returns counts."""
+    abft = path.wl.abft
+    done = bad = inj = 0
+    for fl in lists:
+        if not fl or done >= limit:
+            continue
+        path.step(path.lay_p, abft.faults_to_device(fl, "cuda"))
+        path.wl.torch.cuda.synchronize()
+        ev, unc = path.events(path.lay_p)
+        got = {tuple(e[:5]) for e in ev}
+        want = {(f.op, f.b, f.h, f.row, f.col) for f in fl}
+        bad += int(got != want or unc != 0)
+        done += 1
+        inj += len(fl)
+    return {"faulty_steps_checked": done, "faults_injected": inj, "steps_mismatched": bad}
+
+
+def pct(a):
+    return {"p10": round(float(np.percentile(a, 10)), 4),
+            "p50": round(float(np.percentile(a, 50)), 4),
+            "p90": round(float(np.percentile(a, 90)), 4)}
+
+
+def measure_path(wl, fused, steps, stage_reps, one_fault_op="AS", full=False):
+    """One path at one workload: the workload's fault schedule, fault-free
+    protected and unprotected steps, steps with one INF (correction cost),
+    the stage table protected and unprotected, and the faulty steps
+    re-checked untimed."""
+    abft, W, shape = wl.abft, wl.W, wl.shape
+    B, S, H, nh = shape.batch, shape.seq, shape.hidden, shape.heads
+    P = Path(wl, fused)
+    lists = fault_lists(wl.key, shape, steps)
+    sched = [abft.faults_to_device(fl, "cuda") if fl else (None, 0) for fl in lists]
+    clean = [(None, 0)] * steps
+    one = [abft.faults_to_device(W.draw_faults(shape, W.fault_seed(wl.key, 10_000 + k), 1,
+                                               [one_fault_op], ["inf"]), "cuda")
+           for k in range(min(steps, 10))]
+    one = (one * (steps // len(one) + 1))[:steps]
+    for _ in range(3):
+        P.step(P.lay_p, (None, 0))
+        P.step(P.lay_u, (None, 0))
+    ms, per = timed(P, P.lay_p, sched)
+    ms_clean, per_clean = timed(P, P.lay_p, clean)
+    ms_unprot, per_unprot = timed(P, P.lay_u, clean)
+    ms_one, per_one = timed(P, P.lay_p, one)
+    check = verify_schedule(P, lists)
+    flops = useful_flops(B, S, H, nh, shape.causal, shape.backward)
+    stages = []
+    es = 2 if shape.dtype == "bf16" else 4
+    for name, is_bwd, mask, kind, amount, launches in stage_table(B, S, H, nh, shape.causal,
+                                                                  fused, es):
+        if is_bwd and not shape.backward:
+            continue
+        stages.append({"stage": name, "bwd": is_bwd, "mask": mask, "kind": kind,
+                       "amount": amount, "launches": launches,
+                       "us": stage_us(P, mask, is_bwd, True, stage_reps),
+                       "us_unprotected": stage_us(P, mask, is_bwd, False, stage_reps)})
+    P.step(P.lay_p, (None, 0))     # a consistent workspace after the stage runs
+    wl.torch.cuda.synchronize()
+    for s_ in stages:
+        peak_t = (s_["amount"] / (PEAK_BF16_TFLOPS * 1e12) if s_["kind"] == "flop"
+                  else s_["amount"] / (PEAK_HBM_GBS * 1e9))
+        s_["frac_of_bound"] = round(peak_t / (s_["us"] * 1e-6), 4)
+        s_["model_us"] = peak_t * 1e6
+    rec = {
+        "path": "fused" if fused else "materialised",
+        "tflops": round(flops / (ms * 1e-3) / 1e12, 3),
+        "ms_per_step": round(ms, 4),
+        "ms_protected_fault_free": round(ms_clean, 4),
+        "ms_unprotected": round(ms_unprot, 4),
+        "ms_one_fault": round(ms_one, 4),
+        "tflops_unprotected": round(flops / (ms_unprot * 1e-3) / 1e12, 3),
+        "abft_overhead_pct": round((ms_clean - ms_unprot) / ms_unprot * 100, 2),
+        "abft_overhead_pct_p50": round(float((np.median(per_clean) - np.median(per_unprot))
+                                             / np.median(per_unprot) * 100), 2),
+        "correction_cost_pct": round(float((np.median(per_one) - np.median(per_clean))
+                                           / np.median(per_clean) * 100), 2),
+        "one_fault_op": one_fault_op,
+        "schedule_check": check,
+        "stages_us": {s_["stage"]: round(s_["us"], 2) for s_ in stages},
+        "stages_us_unprotected": {s_["stage"]: round(s_["us_unprotected"], 2) for s_ in stages},
+        "stages_frac_of_bound": {s_["stage"]: s_["frac_of_bound"] for s_ in stages},
+        "roofline_model": {"model_us": round(sum(s_["model_us"] for s_ in stages), 2),
+                           "measured_us": round(ms_clean * 1e3, 2),
+                           "frac": round(sum(s_["model_us"] for s_ in stages) * 1e-3 / ms_clean,
+                                         4)},
+    }
+    if full:
+        rec["step_ms_events"] = {"workload": pct(per), "protected_fault_free": pct(per_clean),
+                                 "unprotected": pct(per_unprot), "one_fault": pct(per_one)}
+        rec["_path"], rec["_stages"] = P, stages
+        rec["_per"] = (per, per_clean, per_unprot)
+    return rec
+
+
+def roofline_of(stages, fused):
+    """The roofline record of the stage that takes the most time per step
+    (all stages eligible, multi-kernel ones included)."""
+    dom = max(stages, key=lambda s_: s_["us"])
+    us, amount = dom["us"], dom["amount"]
+    if dom["kind"] == "flop":
+        achieved = amount / (us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
+    else:
+        achieved = amount / (us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    kern = KERNEL_OF_STAGE.get(dom["stage"]) if dom["launches"] == 1 else None
+    tr = stored_traffic(kern) if kern else None
+    roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
+                 "kernel": dom["stage"], "symbol": kern[0] if kern else None,
+                 "grid": kern[1] if kern else None, "avg_us": round(us, 2),
+                 "algorithmic": amount, "launches_per_call": dom["launches"],
+                 "per_launch": ("one call of the stage: one kernel" if dom["launches"] == 1 else
+                                f"one call of the stage: {dom['launches']} kernels")})
+    if tr:
+        roof["traffic_split"] = {"fetch": tr["fetch_bytes"], "write": tr["write_bytes"]}
+    return roof
+
+
+def vendor_reference(wl, steps):
+    """The same layer step, unprotected, from vendor library calls (torch
+    matmuls and the flash backend of scaled_dot_product_attention, bf16,
+    autograd for the backward): a yardstick for the unprotected path."""
+    torch = wl.torch
+    s = wl.shape
+    B, S, H, nh, d = s.batch, s.seq, s.hidden, s.heads, s.head_dim
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    import torch.nn.functional as F
+    X = wl.X.reshape(B * S, H).clone().requires_grad_(True)
+    Wqkv = wl.Wqkv.clone().requires_grad_(True)
+    Wo = wl.Wo.clone().requires_grad_(True)
+    dO = wl.dO.reshape(B * S, H)
+
+    def step():
+        qkv = (X @ Wqkv).view(B, S, 3, nh, d)
+        q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            cl = F.scaled_dot_product_attention(q, k, v, is_causal=s.causal)
+        o = cl.transpose(1, 2).reshape(B * S, H) @ Wo
+        return torch.autograd.grad(o, (X, Wqkv, Wo), dO)
+
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(wl.stream)
+    for _ in range(steps):
+        step()
+    ev[1].record(wl.stream)
+    ev[1].synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / steps
+    fl = useful_flops(B, S, H, nh, s.causal)
+    return {"what": "torch bf16 matmuls + SDPA flash backend, autograd backward, unprotected",
+            "ms_per_step": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 3)}
 
 
 def pmc_workload(key, reps):
-    """Launches for the traffic counters: one protected step (a consistent
-    workspace), then `reps` launches each of the QKV projection, the score
-    GEMM, the softmax forward and the softmax backward, then `reps` plain
-    copies of COPY_BYTES (reads and writes COPY_BYTES each). The step also
-    launches these kernels once; the per-launch means cover both."""
-    L = Layer(key)
-    torch = L.torch
-    L.step(L.lay_p, None)
-    for mask, is_bwd in ((0x002, False), (0x004, False), (0x008, False), (0x020, True)):
+    """Launches for the traffic counters: one protected step of each path
+    (consistent workspaces), then `reps` launches each of the fused
+    backward core, the fused forward, the QKV projection, the score GEMM,
+    the softmax forward and the softmax backward, then `reps` plain copies
+    of COPY_BYTES (reads and writes COPY_BYTES each). Each step also
+    launches its kernels once; the per-launch means cover both."""
+    wl = Workload(key)
+    torch = wl.torch
+    fz, mat = Path(wl, True), Path(wl, False)
+    fz.step(fz.lay_p, None)
+    mat.step(mat.lay_p, None)
+    for path, mask, is_bwd in ((fz, 0x400, True), (fz, 0x004, False), (mat, 0x002, False),
+                               (mat, 0x004, False), (mat, 0x008, False), (mat, 0x020, True)):
         for _ in range(reps):
-            L.run_stage(mask, is_bwd)
+            path.run_stage(mask, is_bwd)
     src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda").normal_()
     dst = torch.empty_like(src)
     for _ in range(reps):
@@ -311,7 +588,7 @@ def summarize(dirs):
         print(f"{short_name(k[0])} | grid={k[1]} | {vals}")
 
 
-def traffic_from(fetch_dir, write_dir, stages=("qkv", "score", "softmax", "softmax_bwd")):
+def traffic_from(fetch_dir, write_dir, stages=tuple(KERNEL_OF_STAGE)):
     """HBM bytes per launch of the stages' kernels (symbol, grid) from a
     FETCH_SIZE and a WRITE_SIZE run of --pmc-workload, each counter scaled
     by what it reads for the reference copy (COPY_BYTES in, COPY_BYTES
@@ -349,129 +626,25 @@ FAIL_TARGET = 1e-11   # one failure per 1e11 executions of the layer (Sec. 5)
 SECTION_NAMES = ("AS", "CL", "O", "BWD")
 
 
-def fused_forward(L, steps):
-    """The fused attention forward (ABFT_FLAG_FUSED: score, softmax and
-    context in one kernel) against the materialised forward, protected and
-    unprotected: whole-forward times and the fused kernel alone, with one
-    score fault to show it is corrected."""
-    torch, abft, W = L.torch, L.abft, L.W
-    shape = L.shape
-    B, S, H, nh = shape.batch, shape.seq, shape.hidden, shape.heads
-    d = H // nh
-    lays = {}
-    for prot in (True, False):
-        cfg = abft.LayerConfig(B, S, H, nh, dtype=shape.dtype, causal=shape.causal,
-                               block_rows=shape.block_rows, protect=prot, fused=True)
-        lays[prot] = (cfg, abft.ProtectedAttention(cfg, "cuda"))
-
-    def per_forward(lay, n):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-        lay.forward(L.X, L.Wqkv, L.Wo, O=L.O)
-        torch.cuda.synchronize()
-        ev[0].record(L.stream)
-        for i in range(n):
-            lay.forward(L.X, L.Wqkv, L.Wo, O=L.O)
-            ev[i + 1].record(L.stream)
-        torch.cuda.synchronize()
-        return float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(n)]))
-
-    def core_us(cfg, lay, n):
-        run = lambda: abft.attn_abft_forward_stages(cfg, L.X, L.Wqkv, L.Wo, L.O, lay.workspace,
-                                                    None, 0, lay.report, 0x4, L.stream,
-                                                    append=True)
-        run()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(L.stream)
-        for _ in range(n):
-            run()
-        e1.record(L.stream)
-        e1.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / n
-
-    def per_step(lay, n):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-        L.step(lay, (None, 0))
-        torch.cuda.synchronize()
-        ev[0].record(L.stream)
-        for i in range(n):
-            L.step(lay, (None, 0))
-            ev[i + 1].record(L.stream)
-        torch.cuda.synchronize()
-        return float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(n)]))
-
-    def regen_us(cfg, lay, n):
-        run = lambda: abft.attn_abft_backward_stages(cfg, L.dO, L.X, L.Wqkv, L.Wo, lay.workspace,
-                                                     L.dX, L.dWqkv, L.dWo, None, 0,
-                                                     lay.report_bwd, 0x400, L.stream,
-                                                     append=True)
-        run()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(L.stream)
-        for _ in range(n):
-            run()
-        e1.record(L.stream)
-        e1.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / n
-
-    ms_fp, ms_fu = per_forward(lays[True][1], steps), per_forward(lays[False][1], steps)
-    ms_mp, ms_mu = per_forward(L.lay_p, steps), per_forward(L.lay_u, steps)
-    us_p = core_us(*lays[True], steps)
-    us_u = core_us(*lays[False], steps)
-    st_fp, st_fu = per_step(lays[True][1], steps), per_step(lays[False][1], steps)
-    st_mp, st_mu = per_step(L.lay_p, steps), per_step(L.lay_u, steps)
-    us_regen = regen_us(*lays[True], steps)
-    # the training step with the fused forward: useful flops as the workload's
-    step_flops = useful_flops(B, S, H, nh, shape.causal)
-    P = S * (S + 1) // 2 if shape.causal else S * S
-    core_flops = 4.0 * B * nh * d * P          # Q K^T and P V over the unmasked pairs
-    tf = core_flops / (us_p * 1e-6) / 1e12
-    fl = W.draw_faults(shape, W.fault_seed(L.key, 20_000), 1, ["AS"], ["inf"])
-    cfg_p, lay_p = lays[True]
-    lay_p.forward(L.X, L.Wqkv, L.Wo, abft.faults_to_device(fl, "cuda"), O=L.O)
-    torch.cuda.synchronize()
-    rep = abft.read_report(lay_p.report)
-    return {
-        "ms_forward_protected": round(ms_fp, 4), "ms_forward_unprotected": round(ms_fu, 4),
-        "abft_overhead_pct": round((ms_fp - ms_fu) / ms_fu * 100, 2),
-        "ms_forward_materialised_protected": round(ms_mp, 4),
-        "ms_forward_materialised_unprotected": round(ms_mu, 4),
-        "speedup_vs_materialised_protected": round(ms_mp / ms_fp, 3),
-        "kernel": "fused_attn_kernel<%d, true>" % d,
-        "kernel_us_protected": round(us_p, 2), "kernel_us_unprotected": round(us_u, 2),
-        "kernel_tflops_protected": round(tf, 2),
-        "kernel_frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
-        "kernel_flops": core_flops,
-        "one_score_fault": {"corrected": rep["n_corrected"],
-                            "uncorrectable": rep["n_uncorrectable"]},
-        "step": {"note": "fused forward, AP regenerated, protected backward chain",
-                 "ms_protected": round(st_fp, 4), "ms_unprotected": round(st_fu, 4),
-                 "abft_overhead_pct": round((st_fp - st_fu) / st_fu * 100, 2),
-                 "tflops_protected": round(step_flops / (st_fp * 1e-3) / 1e12, 3),
-                 "ms_materialised_protected": round(st_mp, 4),
-                 "ms_materialised_unprotected": round(st_mu, 4),
-                 "speedup_vs_materialised_protected": round(st_mp / st_fp, 3),
-                 "regen_kernel_us": round(us_regen, 2)},
-    }
-
-
-def adaptive_frequencies(L, timed, per_unprot, steps):
+def adaptive_frequencies(path, per_unprot, steps):
     """Adaptive detection frequencies (Sec. 4.5) at the workload: the check
     time of each section measured alone, the library's Algorithm 1 over a
     sweep of error rates (GPT-2 vulnerabilities of Table 4; the backward
     counted as fatal), and one measured run of the per-step masks at the
     sweep point with fractional frequencies."""
     from paper_2410_11720_amd import adaptive
-    abft, torch = L.abft, L.torch
-    shape = L.shape
+    wl = path.wl
+    abft, torch = wl.abft, wl.torch
+    shape = wl.shape
     bits = (abft.SEC_AS, abft.SEC_CL, abft.SEC_O, abft.SEC_BWD)
     base = float(np.median(per_unprot))
     clean = [(None, 0)] * steps
     costs = []
     for bit in bits:
-        L.lay_p.cfg.sections = bit
-        _, per_s = timed(L.lay_p, clean)
+        path.lay_p.cfg.sections = bit
+        _, per_s = timed(path, path.lay_p, clean)
         costs.append(max(0.0, float(np.median(per_s)) - base) * 1e3)
-    L.lay_p.cfg.sections = abft.SEC_ALL
+    path.lay_p.cfg.sections = abft.SEC_ALL
     secs = adaptive.layer_sections(shape.batch, shape.seq, shape.hidden, shape.heads,
                                    shape.causal, costs, "GPT-2", backward=True)
     sweep = []
@@ -489,13 +662,13 @@ def adaptive_frequencies(L, timed, per_unprot, steps):
     n = max(steps, 40)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
-    ev[0].record(L.stream)
+    ev[0].record(wl.stream)
     for k in range(n):
-        L.lay_p.cfg.sections = abft.attn_abft_sections_for_step(freqs, k)
-        L.step(L.lay_p, (None, 0))
-    ev[1].record(L.stream)
+        path.lay_p.cfg.sections = abft.attn_abft_sections_for_step(freqs, k)
+        path.step(path.lay_p, (None, 0))
+    ev[1].record(wl.stream)
     ev[1].synchronize()
-    L.lay_p.cfg.sections = abft.SEC_ALL
+    path.lay_p.cfg.sections = abft.SEC_ALL
     mean_ms = ev[0].elapsed_time(ev[1]) / n
     return {"fail_target": FAIL_TARGET, "vulnerability": "GPT-2 row of Table 4",
             "section_cost_us": {nm: round(c, 2) for nm, c in zip(SECTION_NAMES, costs)},
@@ -505,14 +678,15 @@ def adaptive_frequencies(L, timed, per_unprot, steps):
                          "measured_overhead_pct": round((mean_ms - base) / base * 100, 2)}}
 
 
-def recovery_costs(L, timed, per_clean, steps):
+def recovery_costs(path, per_clean, steps):
     """Recovery overhead per step (Sec. 5, recovery): correction by the
     protected layer for one fault of a given class against fault-free
     protected steps, and checkpoint/restore, which copies the layer's
     inputs and weights back from a pinned host checkpoint and re-runs the
     step (the paper's CR baseline, checkpoint taken every step)."""
-    abft, torch, W = L.abft, L.torch, L.W
-    shape, key = L.shape, L.key
+    wl = path.wl
+    abft, torch, W = wl.abft, wl.torch, wl.W
+    shape, key = wl.shape, wl.key
     base = float(np.median(per_clean))
 
     def one(op, kinds, k):
@@ -520,35 +694,32 @@ def recovery_costs(L, timed, per_clean, steps):
             W.draw_faults(shape, W.fault_seed(key, 20_000 + 97 * k), 1, [op], kinds), "cuda")
 
     out = {}
-    cases = [("AS_0D", "AS", L.lay_p), ("O", "O", L.lay_p), ("dX", "dX", L.lay_p),
-             ("dWQ", "dWQ", L.lay_p), ("Q_root_check", "Q", L.lay_p)]
-    # the paper's own path for a Q fault: no root check, it reaches AS as a
-    # row (1R) and is corrected there by the row pass
-    cfg_lit = L.abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads,
-                                 dtype=shape.dtype, causal=shape.causal,
-                                 block_rows=shape.block_rows, root_check=False)
-    lay_lit = abft.ProtectedAttention(cfg_lit, "cuda")
-    _, per_lit = timed(lay_lit, [(None, 0)] * steps)
-    for name, op, lay in cases:
+    cases = [("AS_0D", "AS"), ("O", "O"), ("dX", "dX"), ("dWQ", "dWQ"), ("Q_root_check", "Q")]
+    # without the root check a Q fault is fixed from checksums: in the
+    # materialised path at AS as a row (1R) by the row pass; the fused path
+    # verifies Q at the projection in every mode
+    lit = Path(wl, path.fused, root_check=False)
+    _, per_lit = timed(lit, lit.lay_p, [(None, 0)] * steps)
+    for name, op in cases:
         sched = [one(op, ["inf"], k) for k in range(steps)]
-        _, per = timed(lay, sched)
+        _, per = timed(path, path.lay_p, sched)
         out[name] = round((float(np.median(per)) - base) / base * 100, 2)
     sched = [one("Q", ["inf"], k) for k in range(steps)]
-    _, per = timed(lay_lit, sched)
-    out["Q_1R_no_root_check"] = round((float(np.median(per)) - float(np.median(per_lit)))
+    _, per = timed(lit, lit.lay_p, sched)
+    out["Q_no_root_check"] = round((float(np.median(per)) - float(np.median(per_lit)))
                                       / float(np.median(per_lit)) * 100, 2)
     # checkpoint/restore: pinned host copies of everything the step reads
-    ckpt = [t.detach().to("cpu").pin_memory() for t in (L.X, L.Wqkv, L.Wo, L.dO)]
-    dsts = (L.X, L.Wqkv, L.Wo, L.dO)
+    ckpt = [t.detach().to("cpu").pin_memory() for t in (wl.X, wl.Wqkv, wl.Wo, wl.dO)]
+    dsts = (wl.X, wl.Wqkv, wl.Wo, wl.dO)
     e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
     restore, rerun = [], []
     for _ in range(max(5, steps // 2)):
-        e0.record(L.stream)
+        e0.record(wl.stream)
         for d_, c_ in zip(dsts, ckpt):
             d_.copy_(c_, non_blocking=True)
-        e1.record(L.stream)
-        L.step(L.lay_p, (None, 0))
-        e2.record(L.stream)
+        e1.record(wl.stream)
+        path.step(path.lay_p, (None, 0))
+        e2.record(wl.stream)
         e2.synchronize()
         restore.append(e0.elapsed_time(e1))
         rerun.append(e1.elapsed_time(e2))
@@ -560,13 +731,29 @@ def recovery_costs(L, timed, per_clean, steps):
             "cr_over_worst_correction": round(cr / worst, 1) if worst > 0 else None}
 
 
+PUBLIC_KEYS = ("path", "tflops", "ms_per_step", "ms_protected_fault_free", "ms_unprotected",
+               "ms_one_fault", "tflops_unprotected", "abft_overhead_pct",
+               "abft_overhead_pct_p50", "correction_cost_pct", "one_fault_op", "schedule_check",
+               "stages_us", "stages_us_unprotected", "stages_frac_of_bound", "roofline_model",
+               "step_ms_events")
+
+
+def public(rec):
+    return {k: rec[k] for k in PUBLIC_KEYS if k in rec}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c3")
+    ap.add_argument("--configs", default="c1,c2,c4,c5",
+                    help="other workloads measured beside the headline ('' for none)")
+    ap.add_argument("--config-steps", type=int, default=12)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-batch", type=int, default=2)
+    ap.add_argument("--no-vendor", action="store_true")
     ap.add_argument("--stage-reps", type=int, default=20)
     ap.add_argument("--adaptive-steps", type=int, default=30)
     ap.add_argument("--pmc-workload", action="store_true")
@@ -588,121 +775,50 @@ def main():
         return
 
     key = args.config
-    L = Layer(key)
-    torch, W, abft = L.torch, L.W, L.abft
-    shape = L.shape
+    wl = Workload(key)
+    torch, shape = wl.torch, wl.shape
     B, S, H, nh = shape.batch, shape.seq, shape.hidden, shape.heads
-
-    # fault schedule: 1-4 faults in one step of every ten, prepared on device
-    sched = []
-    n_faulty = 0
-    for k in range(args.steps):
-        if k % 10 == 0:
-            rng = np.random.default_rng(W.fault_seed(key, k))
-            fl = W.draw_faults(shape, W.fault_seed(key, k), int(rng.integers(1, 5)), W.ALL_OPS,
-                               ["inf", "nan", "+1e10", "-1e10"])
-            sched.append(abft.faults_to_device(fl, "cuda"))
-            n_faulty += 1
-        else:
-            sched.append((None, 0))
-
-    def timed(lay, schedule):
-        """Wall time per step over the whole loop, and per-step durations
-        from HIP events on the launch stream."""
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(schedule) + 1)]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        ev[0].record(L.stream)
-        for i, f in enumerate(schedule):
-            L.step(lay, f)
-            ev[i + 1].record(L.stream)
-        torch.cuda.synchronize()
-        wall = (time.perf_counter() - t0) / len(schedule) * 1e3
-        per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(len(schedule))])
-        return wall, per
-
+    fused = wl.fused_ok()
     for _ in range(args.warmup):
-        L.step(L.lay_p, (None, 0))
-        L.step(L.lay_u, (None, 0))
-    clean = [(None, 0)] * args.steps
-    ms, per = timed(L.lay_p, sched)                 # the workload: faults 1 step in 10
-    ms_clean, per_clean = timed(L.lay_p, clean)
-    ms_unprot, per_unprot = timed(L.lay_u, clean)
-    # correction cost: steps with exactly one fault (an INF in AS, located
-    # and recomputed) against the fault-free protected step
-    one = [abft.faults_to_device(W.draw_faults(shape, W.fault_seed(key, 10_000 + k), 1, ["AS"],
-                                               ["inf"]), "cuda") for k in range(10)]
-    ms_one, per_one = timed(L.lay_p, one * max(1, args.steps // 10))
+        for f in ((True, False) if fused else (False,)):
+            p_ = Path(wl, f)
+            p_.step(p_.lay_p, (None, 0))
+            p_.step(p_.lay_u, (None, 0))
+    print(f"[bench] {shape.name}: headline path", file=sys.stderr, flush=True)
+    head = measure_path(wl, fused, args.steps, args.stage_reps, full=True)
+    other = None
+    if fused:
+        print(f"[bench] {shape.name}: materialised path", file=sys.stderr, flush=True)
+        other = public(measure_path(wl, False, args.steps, args.stage_reps))
+    P, stages = head["_path"], head["_stages"]
+    per, per_clean, per_unprot = head["_per"]
+    roof = roofline_of(stages, fused)
+    print("[bench] adaptive frequencies, recovery", file=sys.stderr, flush=True)
+    adaptive = adaptive_frequencies(P, per_unprot, args.adaptive_steps)
+    recovery = recovery_costs(P, per_clean, args.adaptive_steps)
+    vendor = None
+    if not args.no_vendor and shape.dtype == "bf16" and shape.backward:
+        print("[bench] vendor yardstick", file=sys.stderr, flush=True)
+        try:
+            vendor = vendor_reference(wl, args.stage_reps)
+        except Exception as e:   # a backend this torch build lacks: recorded, not fatal
+            vendor = {"error": f"{type(e).__name__}: {e}"[:300]}
+    configs = {}
+    for k in [c for c in args.configs.split(",") if c and c != key]:
+        print(f"[bench] workload {k}", file=sys.stderr, flush=True)
+        wk = Workload(k)
+        one_op = "AS"
+        entry = {"workload": wk.shape.name}
+        for f in ((True, False) if wk.fused_ok() and wk.shape.backward else (False,)):
+            r = public(measure_path(wk, f, args.config_steps, max(3, args.stage_reps // 4),
+                                    one_fault_op=one_op))
+            entry["fused" if f else "materialised"] = r
+        configs[k] = entry
+        del wk
+        torch.cuda.empty_cache()
 
-    # every fault of a faulty step is detected and corrected
-    f0 = sched[0]
-    L.step(L.lay_p, f0)
-    torch.cuda.synchronize()
-    rf, rb = abft.read_report(L.lay_p.report), abft.read_report(L.lay_p.report_bwd)
-    corrected = rf["n_corrected"] + rb["n_corrected"]
-    uncorrectable = rf["n_uncorrectable"] + rb["n_uncorrectable"]
-
-    # per-stage kernel durations with HIP events on the launch stream, for
-    # the protected layer and (same kernels, checks off) the unprotected one
-    def stage_us(mask, is_bwd, protect):
-        L.run_stage(mask, is_bwd, protect)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(L.stream)
-        for _ in range(args.stage_reps):
-            L.run_stage(mask, is_bwd, protect)
-        e1.record(L.stream)
-        e1.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / args.stage_reps
-
-    L.step(L.lay_u, None)
-    stages, stages_unprot = [], {}
-    for name, is_bwd, mask, kind, amount in stage_table(B, S, H, nh, shape.causal):
-        stages.append((name, kind, amount, stage_us(mask, is_bwd, True)))
-        stages_unprot[name] = round(stage_us(mask, is_bwd, False), 2)
-    # restore a consistent workspace after the stage runs
-    L.step(L.lay_p, (None, 0))
-    torch.cuda.synchronize()
-
-    fused = fused_forward(L, args.stage_reps) if shape.dtype == "bf16" and S % 128 == 0 else None
-    adaptive = adaptive_frequencies(L, timed, per_unprot, args.adaptive_steps)
-    recovery = recovery_costs(L, timed, per_clean, args.adaptive_steps)
-
-    dom = max((s for s in stages if s[0] not in MULTI_KERNEL), key=lambda s: s[3])
-    name, kind, amount, us = dom
-    if kind == "flop":
-        achieved = amount / (us * 1e-6) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
-    else:
-        achieved = amount / (us * 1e-6) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    kern = KERNEL_OF_STAGE.get(name)
-    tr = stored_traffic(kern) if kern else None
-    roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
-                 "kernel": name, "symbol": kern[0] if kern else None,
-                 "grid": kern[1] if kern else None, "avg_us": round(us, 2),
-                 "algorithmic": amount, "per_launch": "one call of the stage (one kernel)"})
-    if tr:
-        roof["traffic_split"] = {"fetch": tr["fetch_bytes"], "write": tr["write_bytes"]}
-
-    # roofline model of the step: each stage at its bound's peak (flops at
-    # the MFMA peak, bytes at the HBM peak), summed, over the measured
-    # fault-free protected step; and each stage's own fraction of its peak
-    model_s, stage_frac = 0.0, {}
-    for s_name, s_kind, s_amount, s_us in stages:
-        t = s_amount / (PEAK_BF16_TFLOPS * 1e12) if s_kind == "flop" else s_amount / (PEAK_HBM_GBS * 1e9)
-        model_s += t
-        stage_frac[s_name] = round(t / (s_us * 1e-6), 4)
-    roofline_model = {"model_us": round(model_s * 1e6, 2), "measured_us": round(ms_clean * 1e3, 2),
-                      "frac": round(model_s * 1e3 / ms_clean, 4)}
-
-    def pct(a):
-        return {"p10": round(float(np.percentile(a, 10)), 4),
-                "p50": round(float(np.percentile(a, 50)), 4),
-                "p90": round(float(np.percentile(a, 90)), 4)}
-
-    flops = useful_flops(B, S, H, nh, shape.causal)
+    ms = head["ms_per_step"]
+    flops = useful_flops(B, S, H, nh, shape.causal, shape.backward)
     value = flops / (ms * 1e-3) / 1e12
     out = {
         "metric": "protected attn-layer TFLOP/s + ABFT overhead % vs unprotected, GPT-2 shape",
@@ -713,32 +829,24 @@ def main():
         "config": {"workload": f"{shape.name} fwd+bwd, faults in 1 of 10 steps",
                    "batch": B, "seq": S, "hidden": H, "heads": nh, "head_dim": H // nh,
                    "causal": shape.causal, "block_rows": shape.block_rows,
-                   "parallelism": "single GPU"},
-        "abft_overhead_pct": round((ms_clean - ms_unprot) / ms_unprot * 100, 2),
-        "abft_overhead_pct_p50": round(float((np.median(per_clean) - np.median(per_unprot))
-                                             / np.median(per_unprot) * 100), 2),
-        "ms_per_step_protected_fault_free": round(ms_clean, 4),
-        "ms_per_step_unprotected": round(ms_unprot, 4),
-        "ms_per_step_one_fault": round(ms_one, 4),
-        "correction_cost_pct": round(float((np.median(per_one) - np.median(per_clean))
-                                           / np.median(per_clean) * 100), 2),
-        "step_ms_events": {"workload": pct(per), "protected_fault_free": pct(per_clean),
-                           "unprotected": pct(per_unprot), "one_fault": pct(per_one)},
-        "unprotected_tflops": round(flops / (ms_unprot * 1e-3) / 1e12, 3),
+                   "path": head["path"], "parallelism": "single GPU"},
+        "abft_overhead_pct": head["abft_overhead_pct"],
+        "ms_per_step_protected_fault_free": head["ms_protected_fault_free"],
+        "ms_per_step_unprotected": head["ms_unprotected"],
+        "correction_cost_pct": head["correction_cost_pct"],
         "mfma_frac_layer": round(value / PEAK_BF16_TFLOPS, 4),
-        "faulty_steps": n_faulty,
-        "check": {"faults_injected": f0[1], "corrected": corrected, "uncorrectable": uncorrectable},
+        "check": head["schedule_check"],
         "roofline": roof,
-        "stages_us": {s[0]: round(s[3], 2) for s in stages},
-        "stages_us_unprotected": stages_unprot,
-        "stages_frac_of_peak": stage_frac,
-        "roofline_model": roofline_model,
+        "headline_path": public(head),
+        "materialised_path": other,
+        "configs": configs,
+        "vendor_reference": vendor,
         "adaptive_frequencies": adaptive,
         "recovery": recovery,
-        "fused_forward": fused,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(shape, W.data_seed(key))
+        print("[bench] cpu baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(shape, wl.W.data_seed(key), args.cpu_batch)
     print(json.dumps(out), flush=True)
 
 

@@ -74,8 +74,11 @@ extern "C" {
                                        Q (K^c)^T, CL against the V^r row
                                        checksum carried through the online
                                        softmax; CL^c encoded from the verified
-                                       CL). Needs bf16 storage and seq a
-                                       multiple of 128 (else
+                                       CL; Q verified at the projection even
+                                       without ABFT_FLAG_ROOT_CHECK, fixed from
+                                       its checksums then, as the row side
+                                       cannot see a Q error). Needs bf16
+                                       storage and seq a multiple of 128 (else
                                        ABFT_ERR_UNSUPPORTED); the stage bits
                                        SCORE, SOFTMAX and CONTEXT each select
                                        that kernel. It saves each query's
@@ -228,7 +231,7 @@ int attn_abft_forward_noalloc(const attn_abft_config* cfg, const void* X, const 
 #define ABFT_STAGE_SCORE       0x004u  /* fwd: AS = Q K^T                           */
 #define ABFT_STAGE_SOFTMAX     0x008u  /* fwd: AP = softmax(scale AS)               */
 #define ABFT_STAGE_CONTEXT     0x010u  /* fwd: CL = AP V                            */
-#define ABFT_STAGE_OUT         0x020u  /* fwd: O = CL Wo                            */
+#define ABFT_STAGE_OUT         0x020u  /* fwd: O = CL Wo (fused: CL^c encoded first) */
 #define ABFT_STAGE_DCL         0x002u  /* bwd: dCL = dO Wo^T                        */
 #define ABFT_STAGE_DWO         0x004u  /* bwd: dWo = CL^T dO                        */
 #define ABFT_STAGE_DAP         0x008u  /* bwd: dAP = dCL V^T                        */
@@ -237,7 +240,8 @@ int attn_abft_forward_noalloc(const attn_abft_config* cfg, const void* X, const 
 #define ABFT_STAGE_DQ          0x040u  /* bwd: dQ = dAS K                           */
 #define ABFT_STAGE_DK          0x080u  /* bwd: dK = dAS^T Q                         */
 #define ABFT_STAGE_DWQKV       0x100u  /* bwd: dWqkv = X^T [dQ|dK|dV]               */
-#define ABFT_STAGE_DX          0x200u  /* bwd: dX = [dQ|dK|dV] Wqkv^T               */
+#define ABFT_STAGE_DX          0x200u  /* bwd: dX = [dQ|dK|dV] Wqkv^T (fused: dQ^c
+                                          encoded first)                        */
 #define ABFT_STAGE_CORE_BWD    0x400u  /* bwd after a fused forward: the fused
                                           backward core (AP, dAS, dQ)           */
 #define ABFT_STAGE_ALL         0x7ffu

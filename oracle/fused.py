@@ -20,8 +20,11 @@ region at R granularity that the materialised form checks too):
      R-key block; EEC of Sec. 4.2): a located element is recomputed from Q
      and K (root check on: the operands are clean) or fixed from the
      checksums (root check off). The column side (AS^c) is not checked
-     here: with the root check a 1R pattern in AS (a Q error, Sec. 4.3)
-     cannot arise, and 0D and 1C patterns are located by the rows.
+     here: a 1R pattern in AS (a Q error, Sec. 4.3) changes a score row
+     together with its checksums and is invisible to the rows, so Q is
+     verified at the projection in every mode (with the root check off
+     it is fixed from its checksums there); 0D and 1C patterns are located
+     by the rows.
   3. Online softmax: m' = max(m, max_j scale S_ij) over unmasked keys,
      p = exp(scale S - m') (masked: 0), alpha = exp(m - m'),
      l = alpha l + sum_j p, P = storage-rounded p,
@@ -33,12 +36,13 @@ region at R granularity that the materialised form checks too):
      is fixed from the checksum (DELTA / RECONSTRUCT, Sec. 4.2).
   5. CL^c, needed by the output projection, is encoded from the verified
      CL (column checksums per R-query block).
-For the backward (the materialised chain of the layer), the softmax
-statistics of every query (the final max m and sum l of step 3) are kept,
-and AP is regenerated from Q, K and them: AP = storage-rounded
-exp(scale Q K^T - m) / l on the unmasked pairs (0 on masked ones), with its
-row checksums AP^r encoded from the stored values; CL^r = A^r / l is the
-propagated row checksum of CL the backward's dW^O check takes.
+For the backward, the softmax statistics of every query (the final max m
+and sum l of step 3) are kept; the fused backward core recomputes the
+scores from them (`fused_backward_core`), and CL^r = A^r / l is the
+propagated row checksum of CL the backward's dW^O check takes. For
+comparisons with the materialised forward, AP is also formed from Q, K
+and the statistics: AP = storage-rounded exp(scale Q K^T - m) / l on the
+unmasked pairs (0 on masked ones), with its row checksums AP^r.
 
 Rounding: S and the accumulators are kept unrounded (fp64 here, fp32 on
 the GPU); P is rounded to the storage dtype (it feeds the P V product);
@@ -201,7 +205,7 @@ def fused_forward(X, Wqkv, Wo, p: OracleParams, faults=(), key_block=None):
     core. Returns O, CL, its checksums, the projection outputs and the
     event list."""
     run = _Run(p, faults)
-    pr = project(run, X, Wqkv, p)
+    pr = project(run, X, Wqkv, p, verify_q=True)
     st = {}
     CL, CLc = fused_attention(run, pr, p, stats=st, key_block=key_block)
     Wo = np.asarray(Wo, dtype=np.float64)

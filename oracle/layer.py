@@ -276,10 +276,13 @@ def _causal_valid(n, S, R):
     return colv, rowv
 
 
-def project(run, X, Wqkv, p: OracleParams):
+def project(run, X, Wqkv, p: OracleParams, verify_q=False):
     """Encoding and the protected QKV projection (Sec. 4.4 S_AS / S_CL
-    members X W^Q, X W^K, X W^V), with the root check. Returns the
-    projection outputs, their checksums and the layer's dimensions."""
+    members X W^Q, X W^K, X W^V), with the root check. `verify_q` checks
+    Q at the projection with the root check off too (a score check that
+    has rows only cannot see a Q error, Sec. 4.3's 1R pattern); the fix is
+    then from the checksums. Returns the projection outputs, their
+    checksums and the layer's dimensions."""
     X = np.asarray(X, dtype=np.float64)
     Wqkv = np.asarray(Wqkv, dtype=np.float64)
     B, S, H = X.shape
@@ -303,11 +306,11 @@ def project(run, X, Wqkv, p: OracleParams):
     Vr = (X @ WVr).reshape(B, S, nh, 2)                        # [B,S,nh,2]
     for i, op in enumerate(("Q", "K", "V")):
         run.inject(op, QKV, lambda b, h, r, c, i=i: (b, r, i * H + h * d + c))
-    if p.protect and p.root_check:
+    if p.protect and (p.root_check or verify_q):
         colmask = np.zeros(3 * H, dtype=bool)
         if "AS" in p.sections:
-            colmask[:2 * H] = True
-        if "CL" in p.sections:
+            colmask[:2 * H if p.root_check else H] = True
+        if "CL" in p.sections and p.root_check:
             colmask[2 * H:] = True
         if colmask.any():
             run.verify(QKV, QKVc, R,

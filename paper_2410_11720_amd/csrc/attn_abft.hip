@@ -371,6 +371,13 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
       g.verify = 1;
       g.verify_n_lo = p.sec_as ? 0 : int(2 * H);
       g.verify_n_hi = p.sec_cl ? int(3 * H) : int(2 * H);
+    } else if (fused && p.sec_as) {
+      // the fused score check has rows only, which cannot see a Q error
+      // (it moves a score row and its checksums together): Q is verified
+      // here in every mode, fixed from its checksums without the root check
+      g.verify = 1;
+      g.verify_n_lo = 0;
+      g.verify_n_hi = int(H);
     }
     g.map.op_base = ABFT_OP_Q; g.map.op_span = int(H); g.map.rows_per_b = int(S);
     g.map.head_cols = int(hd);
@@ -397,8 +404,6 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     fd.stats = F(L.stats);
     fd.clr = F(L.clr);
     CK(launch_fused_fwd(fd, s));
-    if (p.sec_o)  // CL^c for O^c = CL^c Wo, encoded from the verified CL
-      CK(launch_encode(ws + L.cl, dt, B, S, H, H, S * H, int(R), int(hd), F(L.clc), nullptr, s));
   }
   // AS = Q K^T per head (unscaled, before the mask), two-sided checksums
   if (!fused && (stages & ABFT_STAGE_SCORE)) {
@@ -452,6 +457,8 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
   }
   // O = CL Wo, O^c = CL^c Wo
   if (stages & ABFT_STAGE_OUT) {
+    if (fused && p.sec_o)  // the fused forward keeps no CL^c: encoded from the verified CL
+      CK(launch_encode(ws + L.cl, dt, B, S, H, H, S * H, int(R), int(hd), F(L.clc), nullptr, s));
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(H);
     g.A = ws + L.cl; g.lda = H;
@@ -565,7 +572,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   }
   // after a fused forward (no scores kept): the fused backward core, from
   // the forward's softmax statistics, stores AP, dAS (with their row
-  // checksums) and the checked dQ; dQ^c for dX's check is encoded from it
+  // checksums) and the checked dQ (dQ^c is encoded at the dX stage)
   if (fused && (stages & (ABFT_STAGE_CORE_BWD | ABFT_STAGE_DAP | ABFT_STAGE_SOFTMAX_BWD |
                           ABFT_STAGE_DQ))) {
     FusedBwdDesc fd;
@@ -589,13 +596,6 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     fd.tc = p.tc;
     fd.faults = faults; fd.n_faults = n_faults; fd.report = report;
     CK(launch_fused_bwd(fd, s));
-    if (pb) {
-      EncodeJob e;
-      e.A = ws + L.dqkv; e.batch = B; e.rows = S; e.cols = H; e.ld = 3 * H;
-      e.batch_stride = S * 3 * H; e.Rb = int(R); e.Cb = int(hd);
-      e.col_chk = F(L.dqkvc); e.ldcc = 3 * H;
-      CK(launch_encode_jobs(&e, 1, dt, nullptr, s));
-    }
   }
   // dAP = dCL_h V_h^T, dAP^c = dCL_h^c V_h^T
   if (!fused && (stages & ABFT_STAGE_DAP)) {
@@ -694,6 +694,13 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   }
   // dX = dQKV Wqkv^T, dX^c = dQKV^c Wqkv^T
   if (stages & ABFT_STAGE_DX) {
+    if (fused && pb) {  // the fused core writes no dQ^c: encoded from the checked dQ
+      EncodeJob e;
+      e.A = ws + L.dqkv; e.batch = B; e.rows = S; e.cols = H; e.ld = 3 * H;
+      e.batch_stride = S * 3 * H; e.Rb = int(R); e.Cb = int(hd);
+      e.col_chk = F(L.dqkvc); e.ldcc = 3 * H;
+      CK(launch_encode_jobs(&e, 1, dt, nullptr, s));
+    }
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(3 * H);
     g.A = ws + L.dqkv; g.lda = 3 * H;

@@ -69,3 +69,33 @@ def test_trace_summary_means_back_to_back_runs(tmp_path):
     assert abs(a["avg_us"] - (6 * 1.0 + bench.REP_RUN * 1.5) / (6 + bench.REP_RUN)) < 1e-9
     assert a["rep_launches"] == bench.REP_RUN and abs(a["rep_avg_us"] - 1.5) < 1e-9
     assert "rep_launches" not in b and b["launches"] == 6 + bench.REP_RUN - 1
+
+
+def test_fault_schedules_follow_the_workloads():
+    import workloads as W
+    c1 = bench.fault_lists("c1", W.C1, 4)
+    assert [sorted(f.op for f in fl) for fl in c1] == [["AS", "CL", "Q"], [], ["AS", "CL", "Q"], []]
+    c3 = bench.fault_lists("c3", W.C3, 30)
+    assert all(bool(fl) == (k % 10 == 0) for k, fl in enumerate(c3))
+    assert all(1 <= len(fl) <= 4 for fl in c3 if fl)
+    c4 = bench.fault_lists("c4", W.C4, 8)
+    assert all(len(fl) == 1 and fl[0].op in ("AS", "Q", "dWQ") for fl in c4)
+    c5 = bench.fault_lists("c5", W.C5, 12)
+    assert [len(fl) for fl in c5] == [0, 1, 4, 16] * 3
+    mags = [{abs(f.value) for f in fl} for fl in c5]
+    assert mags[1] == {1e6} and mags[5] == {1e10} and mags[11] == {1e30}
+    # distinct rows and columns within one output of one step
+    for fl in c5:
+        rows = [(f.op, f.b, f.h, f.row) for f in fl]
+        cols = [(f.op, f.b, f.h, f.col) for f in fl]
+        assert len(set(rows)) == len(rows) and len(set(cols)) == len(cols)
+
+
+def test_stage_tables_cover_each_path_once():
+    for fused in (False, True):
+        t = bench.stage_table(8, 1024, 768, 12, True, fused)
+        fwd = [m for _, b, m, *_ in t if not b]
+        bwd = [m for _, b, m, *_ in t if b]
+        assert len(set(fwd)) == len(fwd) and len(set(bwd)) == len(bwd)
+        names = {n for n, *_ in t}
+        assert ("core_bwd" in names) == fused and ("softmax_bwd" in names) != fused

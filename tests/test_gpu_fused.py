@@ -182,6 +182,22 @@ def test_fused_key_fault_without_root_check():
     check_outputs(g, o, shape)
 
 
+def test_fused_query_fault_without_root_check():
+    """Root check off: the fused score check has rows only, which cannot
+    see a Q error (a score row moves with its checksums), so the fused form
+    verifies Q at the projection in every mode; without the root check the
+    element is fixed from Q's checksums, and CL and O stay within their
+    rounding bounds of the fused oracle and of the fault-free materialised
+    run."""
+    shape = W.make_shape(1, 256, 128, 2, causal=True, block_rows=128, name="qfault")
+    faults = [W.Fault("Q", 0, 1, 200, 3, 1e8)]
+    g, o = run_fused(shape, faults, root_check=False)
+    want = [("Q", 0, 1, 200, 3, "RECONSTRUCT")]
+    assert [(e[0], e[1], e[2], e[3], e[4], e[6]) for e in o["events"]] == want
+    assert [(e[0], e[1], e[2], e[3], e[4], e[6]) for e in g["rep"]["events"]] == want
+    check_outputs(g, o, shape)
+
+
 def test_fused_gpt2_shape_sampled_heads():
     """The benchmark shape (B8 S1024 H768, 12 heads of 64, causal, R 128):
     no events on the GPU, and two sampled heads equal the oracle's."""

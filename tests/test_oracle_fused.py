@@ -117,19 +117,27 @@ def test_key_fault_without_root_check_is_corrected_along_its_column():
     assert err <= 2.0 ** -6 * np.abs(f0["CL"]).max()
 
 
-def test_query_fault_needs_the_root_check():
+def test_query_fault_is_caught_at_the_projection():
     """A Q error corrupts a whole score row (1R) together with that row's
-    propagated checksums AS^r = Q (K^c)^T, so the row checks cannot see it:
-    with the root check off it reaches CL unnoticed; with the root check on
-    it is corrected at the projection and the run equals the fault-free
-    one."""
+    propagated checksums AS^r = Q (K^c)^T, so the row checks cannot see it
+    (shown on the attention core alone, Q unverified); the fused form
+    therefore verifies Q at the projection in every mode: with the root
+    check on it is recomputed and the run equals the fault-free one, with
+    it off it is fixed from the checksums and CL stays within rounding."""
+    from oracle.fused import fused_attention
+    from oracle.layer import _Run, project
     inp = _inputs()
     fault = [W.Fault("Q", 0, 1, 200, 3, 1e8)]
     p_off = OracleParams(heads=2, dtype="bf16", causal=True, block_rows=128, root_check=False)
     f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p_off)
+    run = _Run(p_off, fault)
+    pr = project(run, inp["X"], inp["Wqkv"], p_off)          # Q not verified
+    CL, _ = fused_attention(run, pr, p_off)
+    assert run.events == []
+    assert not np.array_equal(CL[0, 200, 64:], f0["CL"][0, 200, 64:])
     f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p_off, fault)
-    assert [e for e in f["events"] if e[0] == "AS"] == []
-    assert not np.array_equal(f["CL"][0, 200, 64:], f0["CL"][0, 200, 64:])
+    assert [(e[0], e[3], e[4], e[6]) for e in f["events"]] == [("Q", 200, 3, "RECONSTRUCT")]
+    assert np.abs(f["CL"] - f0["CL"]).max() <= 2.0 ** -6 * np.abs(f0["CL"]).max()
     p_on = OracleParams(heads=2, dtype="bf16", causal=True, block_rows=128)
     g = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p_on, fault)
     assert [(e[0], e[3], e[4], e[6]) for e in g["events"]] == [("Q", 200, 3, "RECOMPUTE")]
