@@ -59,49 +59,62 @@ def useful_flops(B, S, H, nh, causal, backward=True):
 
 
 def stage_table(B, S, H, nh, causal, fused, es=2):
-    """Algorithmic work of each stage of a path: (name, is_bwd, mask, kind,
-    amount, launches) with kind 'flop' (GEMM) or 'byte' (HBM-bound).
-    Masked products count only the unmasked pairs."""
+    """Algorithmic work of each stage of a path: (name, is_bwd, mask, flops,
+    bytes, launches): useful GEMM flops (masked products count only the
+    unmasked pairs) and compulsory HBM bytes (each operand read once, each
+    output written once; fp32 checksums and statistics included where
+    large)."""
     d, T = H // nh, B * S
     P = S * (S + 1) // 2 if causal else S * S
     sq = B * nh * P            # unmasked score entries
+    th = T * H * es            # one activation tensor
     stats = B * nh * S * 2 * 4
-    enc = ("encode", False, 0x001, "byte",
-           (T * H + 3 * H * H) * es + (B * S // 128 * 2 * H + 4 * T * nh) * 4, 1)
-    head = [enc, ("qkv", False, 0x002, "flop", 2 * T * H * 3 * H, 1)]
-    tail_f = [("out", False, 0x020, "flop", 2 * T * H * H, 1)]
-    gemms_b = [("dCL", True, 0x002, "flop", 2 * T * H * H, 1),
-               ("dWo", True, 0x004, "flop", 2 * T * H * H, 2)]
-    tail_b = [("dV", True, 0x010, "flop", 2 * sq * d, 1),
-              ("dK", True, 0x080, "flop", 2 * sq * d, 1),
-              ("dWqkv", True, 0x100, "flop", 2 * T * H * 3 * H, 2),
-              ("dX", True, 0x200, "flop", 2 * T * H * 3 * H, 1)]
+    f32 = 4
+    head = [("encode", False, 0x001, 0, (T * H + 3 * H * H) * es + 2 * T * nh * 2 * f32, 1),
+            ("qkv", False, 0x002, 2 * T * H * 3 * H, th + 3 * H * H * es + 3 * th, 1)]
+    gemms_b = [("encode_dO", True, 0x001, 0, th, 1),
+               ("dCL", True, 0x002, 2 * T * H * H, 2 * th + H * H * es, 1),
+               ("dWo", True, 0x004, 2 * T * H * H, 2 * th + H * H * f32, 2)]
+    wq = ("dWqkv", True, 0x100, 2 * T * H * 3 * H, 4 * th + 3 * H * H * f32, 2)
     if fused:
-        # the fused forward: Q, K, V read, CL written, statistics; the core:
-        # Q, K, V, dCL, CL and the statistics read, AP and dAS written over
-        # the unmasked pairs, dQ written. The output projection and dX
-        # stages encode CL^c and dQ^c first (two launches)
         return head + [
-            ("attn", False, 0x004, "flop", 4 * sq * d, 1)] + [
-            ("out", False, 0x020, "flop", 2 * T * H * H, 2)] + [
-            ("encode_dO", True, 0x001, "byte", 2 * T * H * es, 1)] + gemms_b + [
-            ("core_bwd", True, 0x400, "byte", 2 * sq * es + 6 * T * H * es + stats, 1)] + \
-            tail_b[:3] + [("dX", True, 0x200, "flop", 2 * T * H * 3 * H, 2)]
+            ("attn", False, 0x004, 4 * sq * d, 4 * th + stats, 1),
+            # the output projection encodes CL^c first
+            ("out", False, 0x020, 2 * T * H * H, 3 * th + H * H * es, 2)] + gemms_b + [
+            ("core_enc", True, 0x008, 0, 3 * th + 3 * T * nh * 2 * f32, 1),
+            ("core_q", True, 0x040, 6 * sq * d, 6 * th + stats + B * nh * S * f32, 1),
+            ("core_kv", True, 0x010, 8 * sq * d, 6 * th + stats + B * nh * S * f32, 1),
+            wq,
+            # dX encodes [dQ|dK|dV]^c first
+            ("dX", True, 0x200, 2 * T * H * 3 * H, 7 * th + 3 * H * H * es, 2)]
+    mm = 2 * sq * d
     return head + [
-        # K = head_dim: the score-shaped output is the traffic
-        ("score", False, 0x004, "byte", sq * es + 2 * T * H * es, 1),
-        ("softmax", False, 0x008, "byte", 2 * sq * es, 1),
-        ("context", False, 0x010, "flop", 2 * sq * d, 1)] + tail_f + [
-        ("encode_dO", True, 0x001, "byte", T * H * es, 1)] + gemms_b + [
-        ("dAP", True, 0x008, "byte", sq * es + 2 * T * H * es, 1),
-        ("softmax_bwd", True, 0x020, "byte", 3 * sq * es, 1),
-        ("dQ", True, 0x040, "flop", 2 * sq * d, 1)] + tail_b
+        ("score", False, 0x004, mm, sq * es + 2 * th, 1),
+        ("softmax", False, 0x008, 0, 2 * sq * es, 1),
+        ("context", False, 0x010, mm, sq * es + 2 * th, 1),
+        ("out", False, 0x020, 2 * T * H * H, 2 * th + H * H * es, 1)] + gemms_b + [
+        ("dAP", True, 0x008, mm, sq * es + 2 * th, 1),
+        ("softmax_bwd", True, 0x020, 0, 3 * sq * es, 1),
+        ("dQ", True, 0x040, mm, sq * es + 2 * th, 1),
+        ("dV", True, 0x010, mm, sq * es + 2 * th, 1),
+        ("dK", True, 0x080, mm, sq * es + 2 * th, 1),
+        wq,
+        ("dX", True, 0x200, 2 * T * H * 3 * H, 4 * th + 3 * H * H * es, 1)]
+
+
+def stage_bound(flops, nbytes):
+    """The roof that binds a stage: (kind, time at that roof in seconds),
+    kind 'mfma' or 'hbm', whichever takes longer at its peak."""
+    tf = flops / (PEAK_BF16_TFLOPS * 1e12)
+    tb = nbytes / (PEAK_HBM_GBS * 1e9)
+    return ("mfma", tf) if tf >= tb else ("hbm", tb)
 
 
 # kernel symbol (as rocprofv3 names it) and grid (workgroups) of the stages
 # whose HBM traffic is recorded, at the workload shape, protected
 KERNEL_OF_STAGE = {
-    "core_bwd": ("fused_bwd_kernel<64, true>", 768),
+    "core_kv": ("fused_bwd_kv_kernel<64, true>", 768),
+    "core_q": ("fused_bwd_q_kernel<64, true>", 768),
     "attn": ("fused_attn_kernel<64, true>", 768),
     "qkv": ("gemm_kernel<unsigned short, unsigned short, true, false, 128, 128, true, 2, true, true>", 1152),
     "softmax_bwd": ("softmax_kernel<unsigned short, 2, true, 1, true, true>", 768),
@@ -120,8 +133,10 @@ KERNEL_SOURCES = {
     "softmax_kernel": ("paper_2410_11720_amd/csrc/softmax_abft.hip",) + _COMMON_SOURCES,
     "fused_attn_kernel": ("paper_2410_11720_amd/csrc/fused_attn.hip",
                           "paper_2410_11720_amd/csrc/direct_lds.hpp") + _COMMON_SOURCES,
-    "fused_bwd_kernel": ("paper_2410_11720_amd/csrc/fused_attn.hip",
-                         "paper_2410_11720_amd/csrc/direct_lds.hpp") + _COMMON_SOURCES,
+    "fused_bwd_q_kernel": ("paper_2410_11720_amd/csrc/fused_attn.hip",
+                           "paper_2410_11720_amd/csrc/direct_lds.hpp") + _COMMON_SOURCES,
+    "fused_bwd_kv_kernel": ("paper_2410_11720_amd/csrc/fused_attn.hip",
+                            "paper_2410_11720_amd/csrc/direct_lds.hpp") + _COMMON_SOURCES,
 }
 
 
@@ -387,19 +402,20 @@ def measure_path(wl, fused, steps, stage_reps, one_fault_op="AS", full=False):
     flops = useful_flops(B, S, H, nh, shape.causal, shape.backward)
     stages = []
     es = 2 if shape.dtype == "bf16" else 4
-    for name, is_bwd, mask, kind, amount, launches in stage_table(B, S, H, nh, shape.causal,
-                                                                  fused, es):
+    for name, is_bwd, mask, fl_, by_, launches in stage_table(B, S, H, nh, shape.causal,
+                                                              fused, es):
         if is_bwd and not shape.backward:
             continue
+        kind, _ = stage_bound(fl_, by_)
         stages.append({"stage": name, "bwd": is_bwd, "mask": mask, "kind": kind,
-                       "amount": amount, "launches": launches,
+                       "amount": fl_ if kind == "mfma" else by_, "flops": fl_, "bytes": by_,
+                       "launches": launches,
                        "us": stage_us(P, mask, is_bwd, True, stage_reps),
                        "us_unprotected": stage_us(P, mask, is_bwd, False, stage_reps)})
     P.step(P.lay_p, (None, 0))     # a consistent workspace after the stage runs
     wl.torch.cuda.synchronize()
     for s_ in stages:
-        peak_t = (s_["amount"] / (PEAK_BF16_TFLOPS * 1e12) if s_["kind"] == "flop"
-                  else s_["amount"] / (PEAK_HBM_GBS * 1e9))
+        _, peak_t = stage_bound(s_["flops"], s_["bytes"])
         s_["frac_of_bound"] = round(peak_t / (s_["us"] * 1e-6), 4)
         s_["model_us"] = peak_t * 1e6
     rec = {
@@ -420,6 +436,7 @@ def measure_path(wl, fused, steps, stage_reps, one_fault_op="AS", full=False):
         "stages_us": {s_["stage"]: round(s_["us"], 2) for s_ in stages},
         "stages_us_unprotected": {s_["stage"]: round(s_["us_unprotected"], 2) for s_ in stages},
         "stages_frac_of_bound": {s_["stage"]: s_["frac_of_bound"] for s_ in stages},
+        "stages_bound": {s_["stage"]: s_["kind"] for s_ in stages},
         "roofline_model": {"model_us": round(sum(s_["model_us"] for s_ in stages), 2),
                            "measured_us": round(ms_clean * 1e3, 2),
                            "frac": round(sum(s_["model_us"] for s_ in stages) * 1e-3 / ms_clean,
@@ -438,7 +455,7 @@ def roofline_of(stages, fused):
     (all stages eligible, multi-kernel ones included)."""
     dom = max(stages, key=lambda s_: s_["us"])
     us, amount = dom["us"], dom["amount"]
-    if dom["kind"] == "flop":
+    if dom["kind"] == "mfma":
         achieved = amount / (us * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
@@ -499,7 +516,8 @@ def vendor_reference(wl, steps):
 def pmc_workload(key, reps):
     """Launches for the traffic counters: one protected step of each path
     (consistent workspaces), then `reps` launches each of the fused
-    backward core, the fused forward, the QKV projection, the score GEMM,
+    backward's key pass and query pass, the fused forward, the QKV
+    projection, the score GEMM,
     the softmax forward and the softmax backward, then `reps` plain copies
     of COPY_BYTES (reads and writes COPY_BYTES each). Each step also
     launches its kernels once; the per-launch means cover both."""
@@ -508,8 +526,9 @@ def pmc_workload(key, reps):
     fz, mat = Path(wl, True), Path(wl, False)
     fz.step(fz.lay_p, None)
     mat.step(mat.lay_p, None)
-    for path, mask, is_bwd in ((fz, 0x400, True), (fz, 0x004, False), (mat, 0x002, False),
-                               (mat, 0x004, False), (mat, 0x008, False), (mat, 0x020, True)):
+    for path, mask, is_bwd in ((fz, 0x010, True), (fz, 0x040, True), (fz, 0x004, False),
+                               (mat, 0x002, False), (mat, 0x004, False), (mat, 0x008, False),
+                               (mat, 0x020, True)):
         for _ in range(reps):
             path.run_stage(mask, is_bwd)
     src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda").normal_()

@@ -85,19 +85,29 @@ extern "C" {
                                        softmax max and sum and CL^r. A backward
                                        with the same flag runs a fused core in
                                        place of dAP, the softmax backward and
-                                       dQ (any of those stage bits or CORE_BWD
-                                       selects it): S = Q K^T recomputed and
-                                       row-checked against Q (K^c)^T, P from
+                                       the dQ, dK and dV GEMMs, storing no
+                                       score-shaped tensor (the workspace holds
+                                       none: attn_abft_workspace_bytes is
+                                       smaller): the row checksums of K, Q and
+                                       dCL over each head's dims are encoded
+                                       (stage bit DAP), then a query pass
+                                       (bits SOFTMAX_BWD, DQ) recomputes
+                                       S = Q K^T, row-checked per (query, R-key
+                                       block) against Q (K^c)^T, takes P from
                                        the statistics, dP = dCL V^T row-checked
                                        against dCL (V^c)^T, dS = scale P (dP -
-                                       D) with D = dCL . CL, dQ = dS K
-                                       row-checked against dS K^r (K^r: row
-                                       checksums of K over the head dims, a
-                                       located dQ element fixed from the
-                                       checksum); it stores AP and dS with their
-                                       row checksums for the protected dV and
-                                       dK GEMMs. AS faults are applied to the
-                                       recomputed scores too, dAP faults to dP. */
+                                       D) with D = dCL . CL, and dQ = dS K
+                                       row-checked against dS K^r; a key pass
+                                       (bits DV, DK) recomputes S and dP again,
+                                       column-checked per (R-query block, key)
+                                       against (Q^c) K^T and (dCL^c) V^T, and
+                                       forms dV = P^T dCL and dK = dS^T Q,
+                                       row-checked against P^T dCL^r and
+                                       dS^T Q^r (CORE_BWD selects all three).
+                                       A located dQ, dK or dV element is fixed
+                                       from the checksum. AS faults reach both
+                                       passes' recomputed scores (two events),
+                                       dAP faults both passes' dP. */
 
 /* ---- op tags of protected GEMM outputs (paper Table 1 + backward) ----- */
 enum abft_op {
@@ -234,16 +244,18 @@ int attn_abft_forward_noalloc(const attn_abft_config* cfg, const void* X, const 
 #define ABFT_STAGE_OUT         0x020u  /* fwd: O = CL Wo (fused: CL^c encoded first) */
 #define ABFT_STAGE_DCL         0x002u  /* bwd: dCL = dO Wo^T                        */
 #define ABFT_STAGE_DWO         0x004u  /* bwd: dWo = CL^T dO                        */
-#define ABFT_STAGE_DAP         0x008u  /* bwd: dAP = dCL V^T                        */
-#define ABFT_STAGE_DV          0x010u  /* bwd: dV = AP^T dCL                        */
-#define ABFT_STAGE_SOFTMAX_BWD 0x020u  /* bwd: dAS = scale AP (dAP - rowdot)        */
-#define ABFT_STAGE_DQ          0x040u  /* bwd: dQ = dAS K                           */
-#define ABFT_STAGE_DK          0x080u  /* bwd: dK = dAS^T Q                         */
+#define ABFT_STAGE_DAP         0x008u  /* bwd: dAP = dCL V^T (fused: the core's row
+                                          checksums of K, Q, dCL)               */
+#define ABFT_STAGE_DV          0x010u  /* bwd: dV = AP^T dCL (fused: the key pass)  */
+#define ABFT_STAGE_SOFTMAX_BWD 0x020u  /* bwd: dAS = scale AP (dAP - rowdot)
+                                          (fused: the query pass)               */
+#define ABFT_STAGE_DQ          0x040u  /* bwd: dQ = dAS K (fused: the query pass)   */
+#define ABFT_STAGE_DK          0x080u  /* bwd: dK = dAS^T Q (fused: the key pass)   */
 #define ABFT_STAGE_DWQKV       0x100u  /* bwd: dWqkv = X^T [dQ|dK|dV]               */
-#define ABFT_STAGE_DX          0x200u  /* bwd: dX = [dQ|dK|dV] Wqkv^T (fused: dQ^c
-                                          encoded first)                        */
-#define ABFT_STAGE_CORE_BWD    0x400u  /* bwd after a fused forward: the fused
-                                          backward core (AP, dAS, dQ)           */
+#define ABFT_STAGE_DX          0x200u  /* bwd: dX = [dQ|dK|dV] Wqkv^T (fused:
+                                          [dQ|dK|dV]^c encoded first)           */
+#define ABFT_STAGE_CORE_BWD    0x400u  /* bwd after a fused forward: the whole
+                                          fused backward core                   */
 #define ABFT_STAGE_ALL         0x7ffu
 
 /* attn_abft_forward / attn_abft_backward restricted to the stages in the
@@ -289,7 +301,9 @@ int verify_and_correct(void* C, int32_t dtype, int64_t batch, int64_t rows, int6
 /* Byte offsets of the saved tensors inside the workspace (for inspection):
  * QKV [batch, seq, 3*hidden] dtype, AP [batch, heads, seq, seq] dtype
  * (only blocks with key block <= query block are written under a causal
- * mask), CL [batch, seq, hidden] dtype. Returns ABFT_OK or ABFT_ERR_INVALID. */
+ * mask), CL [batch, seq, hidden] dtype. Returns ABFT_OK, ABFT_ERR_INVALID,
+ * or ABFT_ERR_UNSUPPORTED when ap_offset is requested for a config with
+ * ABFT_FLAG_FUSED (that workspace holds no AP). */
 int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
                                 size_t* ap_offset, size_t* cl_offset);
 
@@ -307,7 +321,8 @@ const char* attn_abft_strerror(int status);
  *   R-query and R-key block.
  * Under a causal mask the score-shaped tensors hold meaningful values only
  * on the pairs the mask allows (key <= query); other positions are zero
- * where written and unspecified elsewhere.
+ * where written and unspecified elsewhere. With ABFT_FLAG_FUSED the
+ * score-shaped tensors (1, 2, 6, 7, 8) do not exist: ABFT_ERR_UNSUPPORTED.
  * Returns ABFT_ERR_INVALID for an invalid config or `which`. */
 int attn_abft_workspace_tensor(const attn_abft_config* cfg, int32_t which, size_t* offset);
 

@@ -21,10 +21,11 @@ region at R granularity that the materialised form checks too):
      and K (root check on: the operands are clean) or fixed from the
      checksums (root check off). The column side (AS^c) is not checked
      here: a 1R pattern in AS (a Q error, Sec. 4.3) changes a score row
-     together with its checksums and is invisible to the rows, so Q is
-     verified at the projection in every mode (with the root check off
-     it is fixed from its checksums there); 0D and 1C patterns are located
-     by the rows.
+     together with its checksums and is invisible to the rows, and the
+     backward's key pass checks columns only, which cannot see a K or V
+     error; so Q, K and V are verified at the projection in every mode
+     (with the root check off they are fixed from their checksums there),
+     and the score checks see the 0D pattern that remains.
   3. Online softmax: m' = max(m, max_j scale S_ij) over unmasked keys,
      p = exp(scale S - m') (masked: 0), alpha = exp(m - m'),
      l = alpha l + sum_j p, P = storage-rounded p,
@@ -54,8 +55,8 @@ from __future__ import annotations
 import numpy as np
 
 from .eec import col_checksums, eec_locate, fix_by_checksum, row_checksums
-from .layer import (OracleParams, _Run, backward, masked_rows_product, output_projection,
-                    project)
+from .layer import (OracleParams, _Run, backward, masked_cols_product, masked_rows_product,
+                    output_projection, project)
 from .numerics import classify, flip_exponent_msb, round_to, stored_threshold
 
 
@@ -205,7 +206,7 @@ def fused_forward(X, Wqkv, Wo, p: OracleParams, faults=(), key_block=None):
     core. Returns O, CL, its checksums, the projection outputs and the
     event list."""
     run = _Run(p, faults)
-    pr = project(run, X, Wqkv, p, verify_q=True)
+    pr = project(run, X, Wqkv, p, verify_always=True)
     st = {}
     CL, CLc = fused_attention(run, pr, p, stats=st, key_block=key_block)
     Wo = np.asarray(Wo, dtype=np.float64)
@@ -251,69 +252,140 @@ def _checked_scores(run, p, op, b, h, A, Bm, Bc, tn, recompute_ok):
     return s
 
 
+def _checked_scores_cols(run, p, op, b, h, A, Bm, Ac, tn, recompute_ok):
+    """S = A Bm^T (fp64, not rounded), the faults of op applied to the fp32
+    value, and the column check of every (R-row block, column) vector
+    against (Ac_qb) Bm^T (Sec. 4.4's AS^c form; Ac the column checksums of
+    A per R-row block; EEC of Sec. 4.2) over the block-lower-triangular
+    region at R granularity (all of it without the mask): a located
+    element is recomputed from A and Bm (root check on) or fixed from the
+    checksums."""
+    S, R = A.shape[0], p.block_rows
+    s = A @ Bm.T
+    for (fb, fh, fr, fc, val, *mode) in run.faults.get(op, ()):
+        if fb == b and fh == h and (not p.causal or fc // R <= fr // R):
+            if mode and mode[0] == "flip":
+                s[fr, fc] = flip_exponent_msb(float(round_to(s[fr, fc], "f32")), "f32")
+            else:
+                s[fr, fc] = round_to(np.array([val]), "f32")[0]
+    if not run.on("BWD"):
+        return s
+    for qb in range(S // R):
+        c_end = (qb + 1) * R if p.causal else S
+        seg = s[qb * R:(qb + 1) * R, :c_end].T.copy()              # one vector per column
+        cs = Ac[qb] @ Bm[:c_end].T                                 # [2, columns]
+        rec = (lambda j, i, qb=qb: A[qb * R + i] @ Bm[j]) if recompute_ok else None
+        evs, unc = _check_rows(seg, cs[0], cs[1], p.e_rel_value(), tn, rec, p.t_correct,
+                               store=lambda x: float(round_to(np.array([x]), "f32")[0]))
+        s[qb * R:(qb + 1) * R, :c_end] = seg.T
+        for (j, i, kind, action) in evs:
+            run.events.append((op, b, h, qb * R + i, j, kind, action))
+        for j in unc:
+            run.events.append((op, b, h, qb * R, j, "-", "UNCORRECTABLE"))
+    return s
+
+
+def _checked_output(run, p, op, b, h, M, cs, tn):
+    """The faults of op applied to the stored output M [rows, d] of one
+    head, then each row checked against its checksums cs [rows, 2]
+    (unweighted, and weighted 1..d over the head's dims); a located element
+    is fixed from the checksum (DELTA / RECONSTRUCT, Sec. 4.2)."""
+    rnd = run.rnd
+    for (fb, fh, fr, fc, val, *mode) in run.faults.get(op, ()):
+        if fb == b and fh == h:
+            M[fr, fc] = (flip_exponent_msb(float(M[fr, fc]), p.dtype)
+                         if mode and mode[0] == "flip" else rnd(np.array([val]))[0])
+    if run.on("BWD"):
+        evs, unc = _check_rows(M, cs[:, 0], cs[:, 1], p.e_rel_value(), tn, None, p.t_correct,
+                               store=lambda x: float(rnd(np.array([x]))[0]))
+        for (i, j, kind, action) in evs:
+            run.events.append((op, b, h, i, j, kind, action))
+        for i in unc:
+            run.events.append((op, b, h, i, 0, "-", "UNCORRECTABLE"))
+    return M
+
+
 def fused_backward_core(run, ctx, p):
-    """The fused backward's steps (an extension: the attention core's
+    """The fused backward of the attention core (an extension: the
     backward without storing the scores, with Sec. 4.4's checks carried
-    over), per (batch, head), from the forward's softmax statistics m, l:
-      1. S = Q K^T recomputed, AS faults applied, rows checked against
-         Q (K^c)^T per R-key block (as in the forward);
-      2. P = exp(scale S - m) / l rounded to storage (0 on masked pairs),
-         stored as AP with its row checksums AP^r (for dV's check);
-      3. dP = dCL V^T (not rounded), dAP faults applied, rows checked
-         against dCL (V^c)^T per R-key block (V^c propagated from X^c W^V);
+    over), per (batch, head), from the forward's softmax statistics m, l,
+    in two passes that each recompute the scores.
+    Key pass (dK and dV, a key's gradients summed over the queries):
+      1. S = Q K^T, AS faults applied, every (R-query block, key) column
+         checked against (Q^c) K^T (Q^c propagated from X^c W^Q);
+      2. P = exp(scale S - m) / l rounded to storage (0 on masked pairs);
+      3. dP = dCL V^T (not rounded), dAP faults applied, columns checked
+         against (dCL^c) V^T (dCL^c propagated from dO^c W^O^T);
       4. D = sum over the head's dims of dCL * CL (the softmax backward's
          row term: sum_j P_ij dP_ij = dCL_i . CL_i);
-      5. dS = scale P (dP - D) rounded (0 on masked pairs), stored as dAS
-         with its row checksums dAS^r (for dK's check);
-      6. dQ = dS K rounded, dQ faults applied, each row checked against
-         dS K^r, K^r the row checksums of the stored K over the head's
-         dims (weights 1..d); a located element is fixed from the checksum
-         (DELTA / RECONSTRUCT, Sec. 4.2);
-      7. dQ^c, the column checksums per R-query block dX's check takes,
-         encoded from the verified dQ.
-    S and dP are compared with the near-INF threshold as fp32 values, dQ
-    as stored."""
+      5. dS = scale P (dP - D) rounded (0 on masked pairs);
+      6. dV = P^T dCL rounded, dV faults applied, each row checked against
+         P^T dCL^r, dCL^r the row checksums of the stored dCL over the
+         head's dims (weights 1..d); dK = dS^T Q rounded, dK faults, rows
+         checked against dS^T Q^r (Q^r likewise from the stored Q); a
+         located element is fixed from the checksum (DELTA / RECONSTRUCT).
+    Query pass (dQ, a query's gradient summed over the keys):
+      7. S recomputed, AS faults applied, every (query, R-key block) row
+         checked against Q (K^c)^T; P as in 2;
+      8. dP recomputed, dAP faults applied, rows checked against
+         dCL (V^c)^T; D and dS as in 4-5;
+      9. dQ = dS K rounded, dQ faults applied, rows checked against dS K^r.
+    A fault of AS or dAP thus reaches both passes and is located in each.
+    S and dP are compared with the near-INF threshold as fp32 values, the
+    gradients as stored. dQ^c, dK^c and dV^c, the column checksums per
+    R-row block that dX's check takes, are encoded from the verified
+    gradients."""
     B, S, nh, d, R, nq, scale = (ctx[k] for k in ("B", "S", "nh", "d", "R", "nq", "scale"))
     rnd = run.rnd
     tn_s = stored_threshold(p.t_near_inf, "f32")
     tn = stored_threshold(p.t_near_inf, p.dtype)
     allowed = np.tril(np.ones((S, S), dtype=bool)) if p.causal else np.ones((S, S), dtype=bool)
-    AP, dAS = np.zeros((B, nh, S, S)), np.zeros((B, nh, S, S))
-    dQh = np.zeros((B, nh, S, d))
-    faults_dq = run.faults.get("dQ", ())
+    out = {k: np.zeros((B, nh, S, d)) for k in ("dQ", "dK", "dV")}
+
+    def probs(s, b, h):
+        with np.errstate(over="ignore", invalid="ignore"):
+            return rnd(np.where(allowed, np.exp(scale * s - ctx["m"][b, h][:, None])
+                                / ctx["l"][b, h][:, None], 0.0))
+
+    def grads(P, dP, D):
+        with np.errstate(over="ignore", invalid="ignore"):
+            return rnd(np.where(allowed, scale * P * (dP - D[:, None]), 0.0))
+
     for b in range(B):
         for h in range(nh):
             Q, K, V = ctx["Qh"][b, h], ctx["Kh"][b, h], ctx["Vh"][b, h]
             dCL, CL = ctx["dCLh"][b, h], ctx["CLh"][b, h]
+            D = (dCL * CL).sum(axis=1)
+            # key pass
+            s = _checked_scores_cols(run, p, "AS", b, h, Q, K, ctx["Qch"][b, h], tn_s,
+                                     p.root_check)
+            P = probs(s, b, h)
+            dP = _checked_scores_cols(run, p, "dAP", b, h, dCL, V, ctx["dCLch"][b, h], tn_s,
+                                      p.root_check)
+            dS = grads(P, dP, D)
+            dCLr = row_checksums(dCL, d)[:, 0, :]                      # [S, 2]
+            Qr = row_checksums(Q, d)[:, 0, :]
+            out["dV"][b, h] = _checked_output(run, p, "dV", b, h,
+                                              rnd(masked_cols_product(P, dCL, p.causal)),
+                                              masked_cols_product(P, dCLr, p.causal), tn)
+            out["dK"][b, h] = _checked_output(run, p, "dK", b, h,
+                                              rnd(masked_cols_product(dS, Q, p.causal)),
+                                              masked_cols_product(dS, Qr, p.causal), tn)
+            # query pass
             s = _checked_scores(run, p, "AS", b, h, Q, K, ctx["Kch"][b, h], tn_s, p.root_check)
-            with np.errstate(over="ignore", invalid="ignore"):
-                P = rnd(np.where(allowed, np.exp(scale * s - ctx["m"][b, h][:, None])
-                                 / ctx["l"][b, h][:, None], 0.0))
+            P = probs(s, b, h)
             dP = _checked_scores(run, p, "dAP", b, h, dCL, V, ctx["Vch"][b, h], tn_s,
                                  p.root_check)
-            D = (dCL * CL).sum(axis=1)
-            with np.errstate(over="ignore", invalid="ignore"):
-                dS = rnd(np.where(allowed, scale * P * (dP - D[:, None]), 0.0))
-            dQ = rnd(masked_rows_product(dS, K, p.causal))
-            for (fb, fh, fr, fc, val, *mode) in faults_dq:
-                if fb == b and fh == h:
-                    dQ[fr, fc] = (flip_exponent_msb(float(dQ[fr, fc]), p.dtype)
-                                  if mode and mode[0] == "flip" else rnd(np.array([val]))[0])
-            if run.on("BWD"):
-                Kr = row_checksums(K, d)[:, 0, :]                       # [S, 2]
-                cs = masked_rows_product(dS, Kr, p.causal)              # [S, 2]
-                evs, unc = _check_rows(dQ, cs[:, 0], cs[:, 1], p.e_rel_value(), tn, None,
-                                       p.t_correct, store=lambda x: float(rnd(np.array([x]))[0]))
-                for (i, j, kind, action) in evs:
-                    run.events.append(("dQ", b, h, i, j, kind, action))
-                for i in unc:
-                    run.events.append(("dQ", b, h, i, 0, "-", "UNCORRECTABLE"))
-            AP[b, h], dAS[b, h], dQh[b, h] = P, dS, dQ
-    return dict(AP=AP, APr=row_checksums(AP, R), dAS=dAS, dASr=row_checksums(dAS, R), dQ=dQh,
-                dQc=col_checksums(dQh, R))
+            dS = grads(P, dP, D)
+            Kr = row_checksums(K, d)[:, 0, :]
+            out["dQ"][b, h] = _checked_output(run, p, "dQ", b, h,
+                                              rnd(masked_rows_product(dS, K, p.causal)),
+                                              masked_rows_product(dS, Kr, p.causal), tn)
+    return dict(dQ=out["dQ"], dK=out["dK"], dV=out["dV"], dQc=col_checksums(out["dQ"], R),
+                dKc=col_checksums(out["dK"], R), dVc=col_checksums(out["dV"], R))
 
 
 def fused_training_backward(fwd: dict, dO, p: OracleParams, faults=()):
     """The layer's protected backward after a fused forward, with the
-    fused backward core in place of the stored-scores steps."""
+    fused backward core in place of the steps from dCL to dQ, dK and dV."""
     return backward(fwd, dO, p, faults, core=fused_backward_core)

@@ -276,13 +276,14 @@ def _causal_valid(n, S, R):
     return colv, rowv
 
 
-def project(run, X, Wqkv, p: OracleParams, verify_q=False):
+def project(run, X, Wqkv, p: OracleParams, verify_always=False):
     """Encoding and the protected QKV projection (Sec. 4.4 S_AS / S_CL
-    members X W^Q, X W^K, X W^V), with the root check. `verify_q` checks
-    Q at the projection with the root check off too (a score check that
-    has rows only cannot see a Q error, Sec. 4.3's 1R pattern); the fix is
-    then from the checksums. Returns the projection outputs, their
-    checksums and the layer's dimensions."""
+    members X W^Q, X W^K, X W^V), with the root check. `verify_always`
+    checks Q, K and V at the projection with the root check off too (a
+    score check with one side cannot see an error of the operand on that
+    side, Sec. 4.3's 1R and 1C patterns); the fix is then from the
+    checksums. Returns the projection outputs, their checksums and the
+    layer's dimensions."""
     X = np.asarray(X, dtype=np.float64)
     Wqkv = np.asarray(Wqkv, dtype=np.float64)
     B, S, H = X.shape
@@ -306,11 +307,11 @@ def project(run, X, Wqkv, p: OracleParams, verify_q=False):
     Vr = (X @ WVr).reshape(B, S, nh, 2)                        # [B,S,nh,2]
     for i, op in enumerate(("Q", "K", "V")):
         run.inject(op, QKV, lambda b, h, r, c, i=i: (b, r, i * H + h * d + c))
-    if p.protect and (p.root_check or verify_q):
+    if p.protect and (p.root_check or verify_always):
         colmask = np.zeros(3 * H, dtype=bool)
         if "AS" in p.sections:
-            colmask[:2 * H if p.root_check else H] = True
-        if "CL" in p.sections and p.root_check:
+            colmask[:2 * H] = True
+        if "CL" in p.sections:
             colmask[2 * H:] = True
         if colmask.any():
             run.verify(QKV, QKVc, R,
@@ -405,10 +406,10 @@ def forward(X, Wqkv, Wo, p: OracleParams, faults=()):
 def backward(fwd: dict, dO, p: OracleParams, faults=(), core=None):
     """Protected backward chain (extension). Returns dX, dWqkv, dWo, the
     intermediate gradients and the event list. core, if given, replaces
-    the steps from the scores' gradient to dQ (dAP, the softmax backward,
-    dQ): core(run, ctx, p) with ctx holding the per-head operands returns
-    AP, AP^r, dAS, dAS^r, dQ and dQ^c; dV and dK then take AP and dAS from
-    it."""
+    the steps from dCL to dQ, dK and dV (dAP, the softmax backward and the
+    three products): core(run, ctx, p) with ctx holding the per-head
+    operands returns dQ, dK, dV and their column checksums dQ^c, dK^c,
+    dV^c."""
     run = _Run(p, faults)
     rnd, rndw = run.rnd, run.rndw
     X, Wqkv, Wo = fwd["X"], fwd["Wqkv"], fwd["Wo"]
@@ -479,12 +480,26 @@ def backward(fwd: dict, dO, p: OracleParams, faults=(), core=None):
                                                           Kh[k // nh, k % nh, :, j], i, S, cz))
     else:
         ctx = dict(B=B, S=S, H=H, nh=nh, d=d, R=R, nq=nq, scale=scale, Qh=Qh, Kh=Kh, Vh=Vh,
-                   dCLh=dCLh, CLh=heads_of(CL), Kch=heads_of_c(fwd["QKVc"][..., H:2 * H]),
-                   Vch=heads_of_c(fwd["QKVc"][..., 2 * H:]), m=fwd["m"], l=fwd["l"])
+                   dCLh=dCLh, CLh=heads_of(CL), Qch=heads_of_c(fwd["QKVc"][..., :H]),
+                   Kch=heads_of_c(fwd["QKVc"][..., H:2 * H]),
+                   Vch=heads_of_c(fwd["QKVc"][..., 2 * H:]), dCLch=heads_of_c(dCLc),
+                   m=fwd["m"], l=fwd["l"])
         c = core(run, ctx, p)
-        AP, APr, dAS, dASr, dQh, dQc = (c[k] for k in ("AP", "APr", "dAS", "dASr", "dQ", "dQc"))
-        dAP = None
+        dQh, dKh, dVh, dQc, dKc, dVc = (c[k] for k in ("dQ", "dK", "dV", "dQc", "dKc", "dVc"))
+        dAP = dAS = None
 
+    if core is None:
+        dVh, dVc, dKh, dKc = _materialised_dv_dk(run, AP, APr, dAS, dASr, dCLh, Qh, p, R, on)
+    return _weight_and_input_grads(run, fwd, p, dQh, dKh, dVh, dQc, dKc, dVc, dWo, dCL, dAP,
+                                   dAS, B, S, H, nh, d, nq, T)
+
+
+def _materialised_dv_dk(run, AP, APr, dAS, dASr, dCLh, Qh, p, R, on):
+    """dV = AP^T dCL and dK = dAS^T Q with their propagated column
+    checksums over key blocks (from AP^r and dAS^r), checked."""
+    rnd, cz = run.rnd, p.causal
+    B, nh, S = AP.shape[:3]
+    d, nq = dCLh.shape[3], S // R
     # dV = AP^T dCL_h; column checksums over key blocks from AP^r
     dVh = rnd(masked_cols_product(AP, dCLh, cz))               # [B,nh,S,d]
     dVc = masked_block_cols_product(APr, dCLh, R, cz)          # [B,nh,nq,2,d]
@@ -504,6 +519,16 @@ def backward(fwd: dict, dO, p: OracleParams, faults=(), core=None):
                    lambda k, i, j: ("dK", k // nh, k % nh, i, j),
                    recompute=lambda k, i, j: _col_dot(dAS[k // nh, k % nh, :, i],
                                                       Qh[k // nh, k % nh, :, j], i, cz))
+    return dVh, dVc, dKh, dKc
+
+
+def _weight_and_input_grads(run, fwd, p, dQh, dKh, dVh, dQc, dKc, dVc, dWo, dCL, dAP, dAS,
+                            B, S, H, nh, d, nq, T):
+    """dWqkv and dX from the three head gradients, checked; the backward's
+    result dictionary."""
+    rnd, rndw, on = run.rnd, run.rndw, run.on("BWD")
+    R = p.block_rows
+    X, Wqkv = fwd["X"], fwd["Wqkv"]
 
     def merge(Mh):          # [B,nh,S,d] -> [B,S,H]
         return Mh.transpose(0, 2, 1, 3).reshape(B, S, H)

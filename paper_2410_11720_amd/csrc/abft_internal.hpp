@@ -142,37 +142,35 @@ struct FusedDesc {
 };
 hipError_t launch_fused_fwd(const FusedDesc& d, hipStream_t stream);
 
-// Fused backward core after a fused forward (no scores kept): per (batch,
-// head, 128-query tile) it recomputes S = Q K^T (row check against
-// Q (K^c)^T), takes P from the forward's softmax statistics, computes
-// dP = dCL V^T (row check against dCL (V^c)^T), dS = scale P (dP - D) with
-// D = dCL . CL, and dQ = dS K (row check against dS K^r, K^r the row
-// checksums of K over the head dims, encoded beforehand); it stores AP and
-// dS with their row checksums for the dV and dK GEMMs, and dQ.
+// Fused backward core after a fused forward (no scores kept), in two
+// passes that each recompute the scores from the softmax statistics: the
+// query pass (dQ; it also leaves D = dCL . CL per query) and the key pass
+// (dK and dV), which reads D.
 struct FusedBwdDesc {
   int B = 0, nh = 0, S = 0, H = 0, D = 0, R = 128;
   int causal = 0;
   float scale = 1.f;
   const void* qkv = nullptr;    // [B*S][3H] bf16: Q | K | V
-  const float* qkvc = nullptr;  // [B][S/R][2][3H] propagated column checksums (K^c, V^c)
-  const float* kr = nullptr;    // [B*S][nh][2] row checksums of K over each head's dims
+  const float* qkvc = nullptr;  // [B][S/R][2][3H] propagated column checksums (Q^c, K^c, V^c)
+  const float* qr = nullptr;    // [B*S][nh][2] row checksums of Q over each head's dims
+  const float* kr = nullptr;    // [B*S][nh][2] the same of K
+  const float* dclr = nullptr;  // [B*S][nh][2] the same of dCL
+  const float* dclc = nullptr;  // [B][S/R][2][H] propagated column checksums of dCL
   const void* cl = nullptr;     // [B*S][H] bf16, the forward's context
   const void* dcl = nullptr;    // [B*S][H] bf16
   const float* stats = nullptr; // [B][nh][S][2]: log2-scaled max and sum per query
-  void* ap = nullptr;           // [B][nh][S][S] bf16 out (key tiles up to the diagonal)
-  float* apr = nullptr;         // [B][nh][S][S/R][2] out
-  void* das = nullptr;          // [B][nh][S][S] bf16 out
-  float* dasr = nullptr;        // [B][nh][S][S/R][2] out
-  void* dq = nullptr;           // dQ out: [B*S][ldq] bf16 (head h at column h D)
-  int64_t ldq = 0;
-  int check = 0;                // run the three row checks
+  float* drow = nullptr;        // [B][nh][S]: D per query (query pass out, key pass in)
+  void* dqkv = nullptr;         // out: [B*S][ld] bf16, dQ | dK | dV (head h at h D of each)
+  int64_t ld = 0;
+  int check = 0;                // run the checks
   int recompute = 1;            // located S / dP errors: recompute (else checksum fix)
   float e_rel = 0.f, tn_s = 0.f, tn = 0.f, tc = 0.f;
   const abft_fault* faults = nullptr;
   int n_faults = 0;
   abft_report* report = nullptr;
 };
-hipError_t launch_fused_bwd(const FusedBwdDesc& d, hipStream_t stream);
+hipError_t launch_fused_bwd_q(const FusedBwdDesc& d, hipStream_t stream);
+hipError_t launch_fused_bwd_kv(const FusedBwdDesc& d, hipStream_t stream);
 
 // Checksum encoder (public encode_checksums) and standalone verifier.
 hipError_t launch_encode(const void* A, int dtype, int64_t batch, int64_t rows, int64_t cols,
@@ -185,9 +183,10 @@ hipError_t launch_verify(void* C, int dtype, int64_t batch, int64_t rows, int64_
 hipError_t launch_report_reset(abft_report* report, int capacity, bool set_capacity,
                                hipStream_t stream);
 
-// Up to two encodes (each as launch_encode) and, when `reset` is given, the
-// report's counters cleared as launch_report_reset(reset, 0, false) does;
-// in one launch when both take the vector path (else one launch each).
+// Up to three encodes (each as launch_encode) and, when `reset` is given,
+// the report's counters cleared as launch_report_reset(reset, 0, false)
+// does; in one launch when all take the vector path with one slab width
+// (else one launch each).
 struct EncodeJob {
   const void* A = nullptr;
   int64_t batch = 0, rows = 0, cols = 0, ld = 0, batch_stride = 0;

@@ -49,7 +49,8 @@ struct Layout_ {
   size_t xc, xr, wvr, qkvc, vr, apc, apr, clc, clr, doc, dclc, dasc, dasr, dqkvc;
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
-  size_t kr;        // fused backward: row checksums of K per head [T][nh][2]
+  size_t kr, qr, dclr;  // fused backward: row checksums of K, Q, dCL per head [T][nh][2]
+  size_t drow;      // fused backward: D = dCL . CL per query [B][nh][S]
   size_t total;
 };
 
@@ -118,8 +119,6 @@ Layout_ make_layout(const Dims& d) {
   const size_t c2 = ks2 > 1 ? size_t(ks2) * 2 * d.nh * d.H : 0;
   L.skp = take((p1 > p2 ? p1 : p2) * f);
   L.skc = take((c1 > c2 ? c1 : c2) * f);
-  L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
-  L.kr = take(size_t(d.T) * d.nh * 2 * f);
   L.total = off;
   return L;
 }
@@ -149,6 +148,53 @@ Layout_ make_layout_fused_forward(const Dims& d) {
   L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
   L.total = off;
   return L;
+}
+
+// Layout of the fused form with a backward: no score-shaped tensor (AS,
+// AP, dAS and their checksums); the fused backward core's row checksums
+// and row terms instead. Offsets of tensors outside it stay 0 and are
+// never used on the fused path.
+Layout_ make_layout_fused(const Dims& d) {
+  Layout_ L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  const size_t f = 4;
+  L.qkv = take(size_t(d.T) * 3 * d.H * d.es);
+  L.cl = take(size_t(d.T) * d.H * d.es);
+  L.dcl = take(size_t(d.T) * d.H * d.es);
+  L.dqkv = take(size_t(d.T) * 3 * d.H * d.es);
+  L.xc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.xr = take(size_t(d.T) * d.nh * 2 * f);
+  L.wvr = take(size_t(d.H) * d.nh * 2 * f);
+  L.qkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
+  L.vr = take(size_t(d.T) * d.nh * 2 * f);
+  L.clc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.clr = take(size_t(d.T) * d.nh * 2 * f);
+  L.doc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.dclc = take(size_t(d.B) * d.nq * 2 * d.H * f);
+  L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
+  const int ks1 = splitk_for(d.H, 3 * d.H, d.T), ks2 = splitk_for(d.H, d.H, d.T);
+  const size_t p1 = ks1 > 1 ? size_t(ks1) * d.H * 3 * d.H : 0;
+  const size_t p2 = ks2 > 1 ? size_t(ks2) * d.H * d.H : 0;
+  const size_t c1 = ks1 > 1 ? size_t(ks1) * 2 * d.nh * 3 * d.H : 0;
+  const size_t c2 = ks2 > 1 ? size_t(ks2) * 2 * d.nh * d.H : 0;
+  L.skp = take((p1 > p2 ? p1 : p2) * f);
+  L.skc = take((c1 > c2 ? c1 : c2) * f);
+  L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
+  L.kr = take(size_t(d.T) * d.nh * 2 * f);
+  L.qr = take(size_t(d.T) * d.nh * 2 * f);
+  L.dclr = take(size_t(d.T) * d.nh * 2 * f);
+  L.drow = take(size_t(d.B) * d.nh * d.S * f);
+  L.total = off;
+  return L;
+}
+
+Layout_ layout_for(const attn_abft_config* c, const Dims& d) {
+  return (c->flags & ABFT_FLAG_FUSED) ? make_layout_fused(d) : make_layout(d);
 }
 
 int validate(const attn_abft_config* c, Dims* d) {
@@ -261,7 +307,7 @@ extern "C" {
 size_t attn_abft_workspace_bytes(const attn_abft_config* cfg) {
   Dims d;
   if (validate(cfg, &d) != ABFT_OK) return 0;
-  return make_layout(d).total;
+  return layout_for(cfg, d).total;
 }
 
 size_t attn_abft_report_bytes(int32_t capacity) {
@@ -279,7 +325,8 @@ int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
                                 size_t* ap_offset, size_t* cl_offset) {
   Dims d;
   if (validate(cfg, &d) != ABFT_OK) return ABFT_ERR_INVALID;
-  const Layout_ L = make_layout(d);
+  if ((cfg->flags & ABFT_FLAG_FUSED) && ap_offset) return ABFT_ERR_UNSUPPORTED;  // no AP kept
+  const Layout_ L = layout_for(cfg, d);
   if (qkv_offset) *qkv_offset = L.qkv;
   if (ap_offset) *ap_offset = L.ap;
   if (cl_offset) *cl_offset = L.cl;
@@ -289,7 +336,10 @@ int attn_abft_workspace_offsets(const attn_abft_config* cfg, size_t* qkv_offset,
 int attn_abft_workspace_tensor(const attn_abft_config* cfg, int32_t which, size_t* offset) {
   Dims d;
   if (validate(cfg, &d) != ABFT_OK || !offset) return ABFT_ERR_INVALID;
-  const Layout_ L = make_layout(d);
+  const Layout_ L = layout_for(cfg, d);
+  // the fused form keeps no score-shaped tensor
+  if ((cfg->flags & ABFT_FLAG_FUSED) && (which == 1 || which == 2 || which >= 6))
+    return which <= 8 ? ABFT_ERR_UNSUPPORTED : ABFT_ERR_INVALID;
   switch (which) {
     case 0: *offset = L.qkv; return ABFT_OK;
     case 1: *offset = L.as; return ABFT_OK;
@@ -327,8 +377,9 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
   // AP^r for dV, CL^r for dWo; a forward that precedes a protected backward
   // must have ABFT_SEC_BWD set).
   const bool fused = (cfg->flags & ABFT_FLAG_FUSED) != 0;
-  // Q^c, K^c; the V root check; K^c and V^c for a fused backward's checks
-  const bool need_xc = p.sec_as || (p.root && p.sec_cl) || (fused && p.sec_bwd);
+  // Q^c, K^c; the V root check (the fused form verifies V in every mode);
+  // Q^c, K^c and V^c for a fused backward's checks
+  const bool need_xc = p.sec_as || ((p.root || fused) && p.sec_cl) || (fused && p.sec_bwd);
   const bool need_vr = p.sec_cl || p.sec_bwd;             // V^r -> CL^r
   const bool need_apc = p.sec_cl || p.sec_o;              // AP^c -> CL^c -> O^c
   // encode (Sec. 4.6): W^V row checksums per head; X column and row
@@ -367,17 +418,14 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
       g.Br = F(L.wvr); g.ldbr = 2 * nh; g.Rn = int(hd); g.cr_n_begin = int(2 * H);
       g.Cr = F(L.vr); g.ldcr = 2 * nh;
     }
-    if (p.root && (p.sec_as || p.sec_cl)) {
+    // the fused form's score checks have one side per pass, which cannot
+    // see an error of the operand on that side (it moves a score row or
+    // column together with its checksums): it verifies Q, K and V here in
+    // every mode, fixed from their checksums without the root check
+    if ((p.root || fused) && (p.sec_as || p.sec_cl)) {
       g.verify = 1;
       g.verify_n_lo = p.sec_as ? 0 : int(2 * H);
       g.verify_n_hi = p.sec_cl ? int(3 * H) : int(2 * H);
-    } else if (fused && p.sec_as) {
-      // the fused score check has rows only, which cannot see a Q error
-      // (it moves a score row and its checksums together): Q is verified
-      // here in every mode, fixed from its checksums without the root check
-      g.verify = 1;
-      g.verify_n_lo = 0;
-      g.verify_n_hi = int(H);
     }
     g.map.op_base = ABFT_OP_Q; g.map.op_span = int(H); g.map.rows_per_b = int(S);
     g.map.head_cols = int(hd);
@@ -489,7 +537,7 @@ int attn_abft_forward_stages(const attn_abft_config* cfg, const void* X, const v
   if (!X || !Wqkv || !Wo || !O || !workspace || !report || n_faults < 0 ||
       (n_faults > 0 && !faults))
     return ABFT_ERR_INVALID;
-  const Layout_ L = make_layout(d);
+  const Layout_ L = layout_for(cfg, d);
   if (workspace_bytes < L.total) return ABFT_ERR_WORKSPACE;
   if ((st = check_device()) != ABFT_OK) return st;
   return forward_impl(cfg, d, L, make_params(cfg, d), X, Wqkv, Wo, O,
@@ -508,7 +556,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   if (!dO || !X || !Wqkv || !Wo || !workspace || !dX || !dWqkv || !dWo || !report ||
       n_faults < 0 || (n_faults > 0 && !faults))
     return ABFT_ERR_INVALID;
-  const Layout_ L = make_layout(d);
+  const Layout_ L = layout_for(cfg, d);
   if (workspace_bytes < L.total) return ABFT_ERR_WORKSPACE;
   if ((st = check_device()) != ABFT_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -521,21 +569,14 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   const bool pb = p.sec_bwd;
 
   const bool fused = (cfg->flags & ABFT_FLAG_FUSED) != 0;
-  // dO^c (Sec. 4.6) and, for the fused backward core, the row checksums of
-  // K per head (K^r, from the checked K), with the report cleared in the
-  // same launch
+  // dO^c (Sec. 4.6), with the report cleared in the same launch
   {
-    EncodeJob e[2];
+    EncodeJob e[1];
     int nj = 0;
     if ((stages & ABFT_STAGE_ENCODE) && pb) {
       EncodeJob& j = e[nj++];
       j.A = dO; j.batch = B; j.rows = S; j.cols = H; j.ld = H; j.batch_stride = S * H;
       j.Rb = int(R); j.Cb = int(hd); j.col_chk = F(L.doc);
-    }
-    if ((stages & ABFT_STAGE_ENCODE) && pb && fused) {
-      EncodeJob& j = e[nj++];
-      j.A = ws + L.qkv + H * es; j.batch = B; j.rows = S; j.cols = H; j.ld = 3 * H;
-      j.batch_stride = S * 3 * H; j.Rb = int(R); j.Cb = int(hd); j.row_chk = F(L.kr);
     }
     CK(launch_encode_jobs(e, nj, dt, (cfg->flags & ABFT_FLAG_REPORT_APPEND) ? nullptr : report,
                           s));
@@ -571,23 +612,42 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
   // after a fused forward (no scores kept): the fused backward core, from
-  // the forward's softmax statistics, stores AP, dAS (with their row
-  // checksums) and the checked dQ (dQ^c is encoded at the dX stage)
-  if (fused && (stages & (ABFT_STAGE_CORE_BWD | ABFT_STAGE_DAP | ABFT_STAGE_SOFTMAX_BWD |
-                          ABFT_STAGE_DQ))) {
+  // the forward's softmax statistics, in three launches: the row checksums
+  // of K, Q and dCL per head over the head dims (from the checked
+  // tensors), the query pass (dQ, and D per query) and the key pass (dK
+  // and dV); nothing score-shaped is stored (dQ^c, dK^c and dV^c are
+  // encoded at the dX stage)
+  if (fused) {
+    const uint32_t st_enc = ABFT_STAGE_CORE_BWD | ABFT_STAGE_DAP;
+    const uint32_t st_q = ABFT_STAGE_CORE_BWD | ABFT_STAGE_SOFTMAX_BWD | ABFT_STAGE_DQ;
+    const uint32_t st_kv = ABFT_STAGE_CORE_BWD | ABFT_STAGE_DV | ABFT_STAGE_DK;
+    if ((stages & st_enc) && pb) {
+      EncodeJob e[3];
+      const void* src[3] = {ws + L.qkv + H * es, ws + L.qkv, ws + L.dcl};
+      const int64_t lds[3] = {3 * H, 3 * H, H};
+      float* dst[3] = {F(L.kr), F(L.qr), F(L.dclr)};
+      for (int i = 0; i < 3; ++i) {
+        e[i].A = src[i]; e[i].batch = B; e[i].rows = S; e[i].cols = H; e[i].ld = lds[i];
+        e[i].batch_stride = S * lds[i]; e[i].Rb = int(R); e[i].Cb = int(hd);
+        e[i].row_chk = dst[i];
+      }
+      CK(launch_encode_jobs(e, 3, dt, nullptr, s));
+    }
     FusedBwdDesc fd;
     fd.B = int(B); fd.nh = int(nh); fd.S = int(S); fd.H = int(H); fd.D = int(hd); fd.R = int(R);
     fd.causal = cfg->causal;
     fd.scale = p.scale;
     fd.qkv = ws + L.qkv;
     fd.qkvc = pb ? F(L.qkvc) : nullptr;
+    fd.qr = pb ? F(L.qr) : nullptr;
     fd.kr = pb ? F(L.kr) : nullptr;
+    fd.dclr = pb ? F(L.dclr) : nullptr;
+    fd.dclc = pb ? F(L.dclc) : nullptr;
     fd.cl = ws + L.cl;
     fd.dcl = ws + L.dcl;
     fd.stats = F(L.stats);
-    fd.ap = ws + L.ap; fd.apr = F(L.apr);
-    fd.das = ws + L.das; fd.dasr = F(L.dasr);
-    fd.dq = ws + L.dqkv; fd.ldq = 3 * H;
+    fd.drow = F(L.drow);
+    fd.dqkv = ws + L.dqkv; fd.ld = 3 * H;
     fd.check = pb ? 1 : 0;
     fd.recompute = p.root ? 1 : 0;
     fd.e_rel = p.e_rel;
@@ -595,7 +655,8 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     fd.tn = p.tn;
     fd.tc = p.tc;
     fd.faults = faults; fd.n_faults = n_faults; fd.report = report;
-    CK(launch_fused_bwd(fd, s));
+    if (stages & st_q) CK(launch_fused_bwd_q(fd, s));
+    if (stages & st_kv) CK(launch_fused_bwd_kv(fd, s));
   }
   // dAP = dCL_h V_h^T, dAP^c = dCL_h^c V_h^T
   if (!fused && (stages & ABFT_STAGE_DAP)) {
@@ -615,7 +676,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   }
   const Tile td = hd == 64 ? Tile::T128x64 : Tile::T128x128;
   // dV = AP^T dCL_h, column checksums over key blocks from AP^r
-  if (stages & ABFT_STAGE_DV) {
+  if (!fused && (stages & ABFT_STAGE_DV)) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(hd); g.K = int(S);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -661,7 +722,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::MNMajor, td, s));
   }
   // dK = dAS^T Q_h, column checksums over key blocks from dAS^r
-  if (stages & ABFT_STAGE_DK) {
+  if (!fused && (stages & ABFT_STAGE_DK)) {
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(S); g.N = int(hd); g.K = int(S);
     g.nb0 = int(B); g.nb1 = int(nh);
@@ -694,9 +755,9 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
   }
   // dX = dQKV Wqkv^T, dX^c = dQKV^c Wqkv^T
   if (stages & ABFT_STAGE_DX) {
-    if (fused && pb) {  // the fused core writes no dQ^c: encoded from the checked dQ
+    if (fused && pb) {  // the fused core writes no checksums: dQKV^c from the checked dQKV
       EncodeJob e;
-      e.A = ws + L.dqkv; e.batch = B; e.rows = S; e.cols = H; e.ld = 3 * H;
+      e.A = ws + L.dqkv; e.batch = B; e.rows = S; e.cols = 3 * H; e.ld = 3 * H;
       e.batch_stride = S * 3 * H; e.Rb = int(R); e.Cb = int(hd);
       e.col_chk = F(L.dqkvc); e.ldcc = 3 * H;
       CK(launch_encode_jobs(&e, 1, dt, nullptr, s));

@@ -153,14 +153,16 @@ __device__ __forceinline__ void encode_job(const EncJob& j, unsigned id) {
 }
 
 template <class T, int V, int CPS>
-__global__ __launch_bounds__(NT) void encode_jobs_kernel(EncJob j0, EncJob j1,
+__global__ __launch_bounds__(NT) void encode_jobs_kernel(EncJob j0, EncJob j1, EncJob j2,
                                                          abft_report* reset) {
   const unsigned id = blockIdx.x;
   if (reset != nullptr && id == 0 && threadIdx.x == 0) clear_counters(reset);
   if (id < j0.nblk)
     encode_job<T, V, CPS>(j0, id);
-  else
+  else if (id < j0.nblk + j1.nblk)
     encode_job<T, V, CPS>(j1, id - j0.nblk);
+  else
+    encode_job<T, V, CPS>(j2, id - j0.nblk - j1.nblk);
 }
 
 // Row checksums for block widths the lane-group reduction cannot cover:
@@ -366,11 +368,11 @@ bool job_of(const EncodeJob& e, EncJob& j, int& cps) {
 
 template <class T>
 hipError_t encode_jobs_t(const EncodeJob* jobs, int n, abft_report* reset, hipStream_t s) {
-  EncJob j[2] = {};
-  int cps[2] = {8, 8};
-  bool one = n >= 1 && n <= 2;
+  EncJob j[3] = {};
+  int cps[3] = {8, 8, 8};
+  bool one = n >= 1 && n <= 3;
   for (int i = 0; one && i < n; ++i) one = job_of<T>(jobs[i], j[i], cps[i]);
-  if (one && n == 2 && cps[0] != cps[1]) one = false;
+  for (int i = 1; one && i < n; ++i) one = cps[i] == cps[0];
   if (!one) {  // separate launches
     if (reset != nullptr) {
       hipError_t e = launch_report_reset(reset, 0, false, s);
@@ -388,13 +390,14 @@ hipError_t encode_jobs_t(const EncodeJob* jobs, int n, abft_report* reset, hipSt
     return hipSuccess;
   }
   constexpr int VV = 16 / sizeof(T);
-  const unsigned total = j[0].nblk + (n == 2 ? j[1].nblk : 0u);
+  unsigned total = 0;
+  for (int i = 0; i < n; ++i) total += j[i].nblk;   // unused jobs have nblk 0
   if (cps[0] == 8)
     hipLaunchKernelGGL((encode_jobs_kernel<T, VV, 8>), dim3(total), dim3(NT), 0, s, j[0], j[1],
-                       reset);
+                       j[2], reset);
   else
     hipLaunchKernelGGL((encode_jobs_kernel<T, VV, 16>), dim3(total), dim3(NT), 0, s, j[0], j[1],
-                       reset);
+                       j[2], reset);
   return hipGetLastError();
 }
 }  // namespace
@@ -402,11 +405,11 @@ hipError_t encode_jobs_t(const EncodeJob* jobs, int n, abft_report* reset, hipSt
 hipError_t launch_encode_jobs(const EncodeJob* jobs, int n, int dtype, abft_report* reset,
                               hipStream_t s) {
   // empty operands encode nothing
-  EncodeJob live[2];
+  EncodeJob live[3];
   int m = 0;
   for (int i = 0; i < n; ++i)
     if (jobs[i].batch > 0 && jobs[i].rows > 0 && jobs[i].cols > 0) {
-      if (m == 2) return hipErrorInvalidValue;
+      if (m == 3) return hipErrorInvalidValue;
       live[m++] = jobs[i];
     }
   if (m == 0) return reset != nullptr ? launch_report_reset(reset, 0, false, s) : hipSuccess;

@@ -24,10 +24,10 @@
 // After the last key tile CL = O / l is rounded, row-checked against
 // A^r / l (located elements fixed from the checksum, Sec. 4.2) and stored.
 // The column side of AS (AS^c = Q^c K^T) is not checked here: it would
-// need a reduction across the 16 lanes of a query group per key; with the
-// root check, Q errors (the 1R patterns only the column side locates) are
-// corrected before this kernel, and 0D and 1C errors are located by the
-// rows.
+// need a reduction across the 16 lanes of a query group per key. The fused
+// form verifies Q, K and V at their projection in every mode, so the 1R
+// and 1C patterns their errors would make cannot arise, and the rows
+// locate the 0D pattern that remains.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -599,44 +599,44 @@ struct FusedAttn {
   }
 };
 
-// Fused backward core (after a fused forward, which keeps no scores). Per
-// (batch, head, tile of 128 queries), each of the four waves owning 32
-// queries, key tiles of 128 keys pass through LDS (K and V as K-major
-// images, the K^c and V^c strips, and the strip of K^r, the row checksums
-// of K over the head dims); per key tile each wave computes
-//   S^T = K Q^T (AS^r = Q (K^c)^T from the strip) and checks every
-//     (query, R-key block) vector, as the forward does;
-//   P = exp2(log2(e) scale S - m) / l from the forward's statistics,
-//     rounded, stored as AP with its row checksums AP^r;
-//   dP^T = V dCL^T (dP^r = dCL (V^c)^T from the strip) and the same row
-//     check;
-//   dS = scale P (dP - D), D = dCL . CL per query, rounded, stored with
-//     its row checksums dAS^r;
-//   dQ^T += K^T dS^T and (dQ^r)^T += (K^r)^T dS^T, the K^T fragments read
-//     from the K image with transposing reads in the key order of the
-//     dS^T fragment a lane assembles from its accumulators.
-// After the last key tile dQ is rounded, row-checked against dQ^r (a
-// located element fixed from the checksum) and stored.
-template <int D, bool CHK>
-struct FusedBwd {
-  static constexpr int KH = D / 64, KS = D / 32, DB = D / 16;
-  using DK = Direct<true, FT>;                 // one 64-dim half: [128 keys][64]
-  static constexpr int IMG = KH * DK::BYTES;   // a [128 keys][D] K-major image
-  static constexpr int SCL = D + 8;            // strip row (elements), padded
-  static constexpr int STRIP = 16 * SCL * 2;
-  static constexpr int OFF_V = IMG, OFF_KC = 2 * IMG, OFF_VC = OFF_KC + STRIP;
-  static constexpr int OFF_KR = OFF_VC + STRIP;
-  static constexpr int STAGE_BYTES = OFF_KR + FT * 16 * 2;
-  // the workgroup's Q and dCL rows, [128 queries][D] K-major images read as
-  // the B operands of S^T and dP^T (loaded once)
-  static constexpr int OFF_Q = STAGE_BYTES, OFF_G = OFF_Q + IMG;
-  static constexpr int SCR = 160;              // floats of rare-path scratch per wave
-  static constexpr int OFF_SCR = OFF_G + IMG;
-  static constexpr int LDS_BYTES = OFF_SCR + 4 * SCR * 4;
+// Fused backward core (after a fused forward, which keeps no scores), in
+// two passes that each recompute the scores from the forward's softmax
+// statistics (no score-shaped tensor is read or written):
+//  - the query pass, per (batch, head, tile of 128 queries), each wave
+//    owning 32 queries and the key tiles passing through LDS: S^T = K Q^T
+//    row-checked per (query, R-key block) against Q (K^c)^T, P from the
+//    statistics, dP^T = V dCL^T row-checked against dCL (V^c)^T,
+//    dS = scale P (dP - D) with D = dCL . CL (left in memory for the key
+//    pass), dQ^T += K^T dS^T with (dQ^r)^T += (K^r)^T dS^T; dQ is rounded,
+//    row-checked (a located element fixed from the checksum) and stored;
+//  - the key pass, per (batch, head, tile of 128 keys), each wave owning 32
+//    keys and the query tiles passing through LDS: S = Q K^T column-checked
+//    per (R-query block, key) against (Q^c) K^T, P, dV^T += dCL^T P with
+//    (dV^r)^T += (dCL^r)^T P, dP = dCL V^T column-checked against
+//    (dCL^c) V^T, dS, dK^T += Q^T dS with (dK^r)^T += (Q^r)^T dS; dK and dV
+//    are rounded, row-checked and stored.
+// Each pass holds a 128 x 32 score tile per wave with the 128-long side
+// along a lane's registers and lane groups, so its checks and the packing
+// of P and dS into the next product's operand stay inside the wave; the
+// two passes differ in which entity (query or key) is the 32-wide side.
 
-  // K^T operand fragment (rows: dims rb + lane % 16; k: keys kb + 4g + 0..3
-  // and kb + 16 + 4g + 0..3) from the K-major image
-  __device__ static __forceinline__ TrPair kt_frag(const char* img, int rb, int kb, int lane) {
+// Shared pieces of the two passes. A score tile t[8][2] of a wave holds,
+// for lane (lq = lane % 16, g = lane / 16), the 4 rows 16 j + 4 g + r
+// (r = 0..3; rows: the 128-long side) of column 16 c + lq (c = 0, 1;
+// columns: the wave's 32).
+template <int D>
+struct BwdTile {
+  static constexpr int KH = D / 64, KS = D / 32, DB = D / 16;
+  using DK = Direct<true, FT>;                 // one 64-dim half: [128 rows][64]
+  static constexpr int IMG = KH * DK::BYTES;   // a [128 rows][D] K-major image
+  static constexpr int SCL = D + 8;            // strip row (elements), padded
+  static constexpr int STRIP = 16 * SCL * 2;   // 16 checksum rows of D
+  static constexpr int RSTRIP = FT * 16 * 2;   // [128 rows][16] row-checksum strip
+  static constexpr int SCR = 160;              // floats of rare-path scratch per wave
+
+  // transposed operand fragment (rows: dims rb + lane % 16; k: image rows
+  // kb + 4g + 0..3 and kb + 16 + 4g + 0..3) from a K-major image
+  __device__ static __forceinline__ TrPair t_frag(const char* img, int rb, int kb, int lane) {
     const int s = lane & 15, g = lane >> 4;
     const int k1 = kb + 4 * g + (s >> 2), k2 = k1 + 16;
     const int m = rb + 4 * (s & 3);
@@ -645,34 +645,40 @@ struct FusedBwd {
     return tr_pair_intrinsic(half + k1 * 128 + ((c ^ (k1 & 7)) << 4) + off,
                              half + k2 * 128 + ((c ^ (k2 & 7)) << 4) + off);
   }
-  // (K^r)^T fragment from the [128 keys][16] strip, same key order
-  __device__ static __forceinline__ TrPair kr_frag(const bf16_t* krs, int kb, int lane) {
+  // the same from a [128 rows][16] row-checksum strip
+  __device__ static __forceinline__ TrPair rs_frag(const bf16_t* rs, int kb, int lane) {
     const int s = lane & 15, g = lane >> 4;
     const int k1 = kb + 4 * g + (s >> 2), k2 = k1 + 16;
     const int m = 4 * (s & 3);
-    return tr_pair_intrinsic(krs + k1 * 16 + m, krs + k2 * 16 + m);
+    return tr_pair_intrinsic(rs + k1 * 16 + m, rs + k2 * 16 + m);
+  }
+  // the operand pair of the packed 32-row slab t of a packed tile
+  __device__ static __forceinline__ bf16x8 slab(const uint2 (&pk)[8][2], int t, int c) {
+    const uint4 u = {pk[2 * t][c].x, pk[2 * t][c].y, pk[2 * t + 1][c].x, pk[2 * t + 1][c].y};
+    return __builtin_bit_cast(bf16x8, u);
   }
 
-  // Row check of a 128-key x 32-query tile t (keys along the lane's
-  // registers) per (query, R-key block) against the strip result cs (rows
-  // 4b..4b+3 of lane group b: hi/lo of c1, c2): a flagged vector is
-  // gathered into the wave's scratch, located by EEC and its element
-  // recomputed as the dot product of row q of A and row key of Bm (length
-  // D, leading dimensions lda, ldb) or fixed from the checksums.
-  __device__ static void check_tile(floatx4 (&t)[8][2], const floatx4 (&cs)[2],
-                                    const FusedBwdDesc& fd, int op, int b, int h, int qw,
-                                    int key0, const bf16_t* A, const bf16_t* Bm, int64_t lda,
-                                    int64_t ldb, float* scr, int lane) {
+  // Check of a score tile per (column, R-row block) against the strip
+  // result cs (rows 4b..4b+3 of lane group b: hi/lo of c1, c2). A flagged
+  // vector is gathered into the wave's scratch, located by EEC and its
+  // element recomputed as the dot product of row `col` of A and row `row`
+  // of Bm (length D) or fixed from the checksums. Columns are entities
+  // cbase + 0..31, rows rbase + 0..127; events name (row, col) when TR
+  // (the tile is the score matrix itself), (col, row) otherwise (its
+  // transpose).
+  template <bool TR>
+  __device__ static void check(floatx4 (&t)[8][2], const floatx4 (&cs)[2], const FusedBwdDesc& fd,
+                               int op, int b, int h, int cbase, int rbase, const bf16_t* A,
+                               const bf16_t* Bm, int64_t lda, int64_t ldb, float* scr, int lane) {
     const int lq = lane & 15, g = lane >> 4;
     const int R = fd.R, NB = FT / R, lg_jpb = __builtin_ctz(R / 16);
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int c = 0; c < 2; ++c) {
       float sj[8], aj[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        sj[j] = (t[j][qb][0] + t[j][qb][1]) + (t[j][qb][2] + t[j][qb][3]);
-        aj[j] = (fabsf(t[j][qb][0]) + fabsf(t[j][qb][1])) +
-                (fabsf(t[j][qb][2]) + fabsf(t[j][qb][3]));
+        sj[j] = (t[j][c][0] + t[j][c][1]) + (t[j][c][2] + t[j][c][3]);
+        aj[j] = (fabsf(t[j][c][0]) + fabsf(t[j][c][1])) + (fabsf(t[j][c][2]) + fabsf(t[j][c][3]));
       }
       float r1[4], ra[4];
 #pragma unroll
@@ -693,7 +699,7 @@ struct FusedBwd {
           if (g == i) { mine1 = t1; minea = ta; }
         }
       }
-      const float c1 = cs[qb][0] + cs[qb][1];
+      const float c1 = cs[c][0] + cs[c][1];
       const bool fl = g < NB && flagged(c1 - mine1, minea, fd.e_rel);
       uint64_t mask = __ballot(fl);
       while (mask) {  // rare: locate and correct inside the wave
@@ -704,34 +710,35 @@ struct FusedBwd {
         for (int j = 0; j < 8; ++j)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (lq == vq && (j >> lg_jpb) == vb) scr[(16 * j + 4 * g + r) - vb * R] = t[j][qb][r];
-        const float v1 = __shfl(cs[qb][0] + cs[qb][1], L, 64);
-        const float v2 = __shfl(cs[qb][2] + cs[qb][3], L, 64);
+            if (lq == vq && (j >> lg_jpb) == vb) scr[(16 * j + 4 * g + r) - vb * R] = t[j][c][r];
+        const float v1 = __shfl(cs[c][0] + cs[c][1], L, 64);
+        const float v2 = __shfl(cs[c][2] + cs[c][3], L, 64);
         wave_sync_lds();
         if (lane == 0) {
-          const int q = qw + 16 * qb + vq;
+          const int col = cbase + 16 * c + vq;
           const EecResult res = eec_locate<float>(scr, 1, R, v1, v2, fd.e_rel, fd.tn_s);
           int idx = -1;
           float nv = 0.f;
           if (res.status == EEC_LOCATED) {
             idx = res.index;
-            const int key = key0 + vb * R + idx;
+            const int row = rbase + vb * R + idx;
             const float old = scr[idx];
             int action = ABFT_ACT_RECOMPUTE;
             if (fd.recompute) {
               float acc = 0.f;
               for (int dd = 0; dd < D; ++dd)
-                acc = fmaf(bf2f(A[int64_t(q) * lda + dd]), bf2f(Bm[int64_t(key) * ldb + dd]), acc);
+                acc = fmaf(bf2f(A[int64_t(col) * lda + dd]), bf2f(Bm[int64_t(row) * ldb + dd]), acc);
               nv = acc;
             } else {
               nv = fix_by_checksum<float>(scr, 1, R, idx, v1, res.d1, fd.tc, &action);
             }
             scr[idx] = nv;
-            record_event(fd.report, op, b, h, q, key, classify(old, fd.tn_s), action, old);
+            record_event(fd.report, op, b, h, TR ? row : col, TR ? col : row,
+                         classify(old, fd.tn_s), action, old);
           }
           if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, R, v1, fd.e_rel))
-            record_event(fd.report, op, b, h, q, key0 + vb * R, ABFT_KIND_NONE,
-                         ABFT_ACT_UNCORRECTABLE, 0.f);
+            record_event(fd.report, op, b, h, TR ? rbase + vb * R : col, TR ? col : rbase + vb * R,
+                         ABFT_KIND_NONE, ABFT_ACT_UNCORRECTABLE, 0.f);
           scr[R] = __int_as_float(idx);
           scr[R + 1] = nv;
         }
@@ -745,34 +752,179 @@ struct FusedBwd {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
               if (lane == vq + 16 * ((kl & 15) >> 2) && j == (kl >> 4) && r == (kl & 3))
-                t[j][qb][r] = nv;
+                t[j][c][r] = nv;
         }
         wave_sync_lds();
       }
     }
   }
 
-  // injected faults of op (test-only) on a 128-key x 32-query fp32 tile
-  __device__ static void inject_tile(floatx4 (&t)[8][2], const FusedBwdDesc& fd, int op, int b,
-                                     int h, int qw, int key0, int lane) {
+  // injected faults of op (test-only) on a score tile (coordinates as in
+  // check: fault rows are queries and columns keys)
+  template <bool TR>
+  __device__ static void inject(floatx4 (&t)[8][2], const FusedBwdDesc& fd, int op, int b, int h,
+                                int cbase, int rbase, int lane) {
     for (int f = 0; f < fd.n_faults; ++f) {
       const abft_fault ft = fd.faults[f];
       if (ft.op != op || ft.b != b || ft.h != h) continue;
-      const int qi = ft.row - qw, ki = ft.col - key0;
-      if (qi < 0 || qi >= 32 || ki < 0 || ki >= FT) continue;
       // under the mask only the block-lower-triangular region is computed
       if (fd.causal && ft.col / fd.R > ft.row / fd.R) continue;
-      const int oq = qi >> 4, olane = (qi & 15) + 16 * ((ki & 15) >> 2);
+      const int ci = (TR ? ft.col : ft.row) - cbase, ri = (TR ? ft.row : ft.col) - rbase;
+      if (ci < 0 || ci >= 32 || ri < 0 || ri >= FT) continue;
+      const int oc = ci >> 4, olane = (ci & 15) + 16 * ((ri & 15) >> 2);
 #pragma unroll
       for (int j = 0; j < 8; ++j)
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+        for (int c = 0; c < 2; ++c)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (lane == olane && qb == oq && j == (ki >> 4) && r == (ki & 3))
-              t[j][qb][r] = ft.mode == ABFT_FAULT_FLIP ? flip_f32(t[j][qb][r]) : ft.value;
+            if (lane == olane && c == oc && j == (ri >> 4) && r == (ri & 3))
+              t[j][c][r] = ft.mode == ABFT_FAULT_FLIP ? flip_f32(t[j][c][r]) : ft.value;
     }
   }
+
+  // A gradient's transposed accumulators acc[DB][2] (lane: dims
+  // 16 db + 4 g + r of entity cbase + 16 c + lq) and its strip results
+  // chk[2] (lane group 0: hi/lo of the sum and of the 1-based weighted sum
+  // over the dims): rounded, faults of op injected, each entity's row
+  // checked (a located element fixed from the checksum, Sec. 4.2) and
+  // stored at out + entity * ld.
+  __device__ static void finish(floatx4 (&acc)[DB][2], const floatx4 (&chk)[2],
+                                const FusedBwdDesc& fd, bool check, int op, int b, int h,
+                                int cbase, bf16_t* out, int64_t ld, float* scr, int lane) {
+    const int lq = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int e = cbase + 16 * c + lq;
+      float ov[DB][4];
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ov[db][r] = bf2f(f2bf(acc[db][c][r]));
+      if (fd.n_faults > 0) {
+        for (int f = 0; f < fd.n_faults; ++f) {
+          const abft_fault ft = fd.faults[f];
+          if (ft.op != op || ft.b != b || ft.h != h || ft.row != e) continue;
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (ft.col == 16 * db + 4 * g + r)
+                ov[db][r] = ft.mode == ABFT_FAULT_FLIP ? bf2f(flip_exponent_msb(f2bf(ov[db][r])))
+                                                       : bf2f(f2bf(ft.value));
+        }
+      }
+      if (check) {
+        const float c1 = __shfl(chk[c][0] + chk[c][1], lq, 64);
+        const float c2 = __shfl(chk[c][2] + chk[c][3], lq, 64);
+        float r1 = 0.f, ra = 0.f;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            r1 += ov[db][r];
+            ra += fabsf(ov[db][r]);
+          }
+        r1 = group4_sum(r1);
+        ra = group4_sum(ra);
+        uint64_t mask = __ballot(g == 0 && flagged(c1 - r1, ra, fd.e_rel));
+        while (mask) {
+          const int L = __builtin_ctzll(mask);
+          mask &= mask - 1;
+          if (lq == L) {
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) scr[16 * db + 4 * g + r] = ov[db][r];
+          }
+          const float v1 = __shfl(c1, L, 64), v2 = __shfl(c2, L, 64);
+          wave_sync_lds();
+          if (lane == 0) {
+            const int ee = cbase + 16 * c + L;
+            const EecResult res = eec_locate<float>(scr, 1, D, v1, v2, fd.e_rel, fd.tn);
+            int idx = -1;
+            float nv = 0.f;
+            if (res.status == EEC_LOCATED) {
+              idx = res.index;
+              const float old = scr[idx];
+              int action = 0;
+              nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, D, idx, v1, res.d1, fd.tc, &action)));
+              scr[idx] = nv;
+              record_event(fd.report, op, b, h, ee, idx, classify(old, fd.tn), action, old);
+            }
+            if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, D, v1, fd.e_rel))
+              record_event(fd.report, op, b, h, ee, 0, ABFT_KIND_NONE, ABFT_ACT_UNCORRECTABLE, 0.f);
+            scr[D] = __int_as_float(idx);
+            scr[D + 1] = nv;
+          }
+          wave_sync_lds();
+          const int idx = __float_as_int(scr[D]);
+          const float nv = scr[D + 1];
+          if (idx >= 0 && lq == L) {
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (idx == 16 * db + 4 * g + r) ov[db][r] = nv;
+          }
+          wave_sync_lds();
+        }
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const uint2 w = {pack2(ov[db][0], ov[db][1]), pack2(ov[db][2], ov[db][3])};
+        *reinterpret_cast<uint2*>(out + int64_t(e) * ld + 16 * db + 4 * g) = w;
+      }
+    }
+  }
+
+  // checksum strip of 16 rows (4 per R-row block: hi/lo of the sum and of
+  // the weighted sum) from fp32 column checksums; thread tid stages up to
+  // four values in v[] (issue) and writes them (commit)
+  __device__ static __forceinline__ void strip_issue(const float* cc, int64_t ldc, int64_t blk0,
+                                                     int NB, int tid, float (&v)[4]) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int e = tid + p * FNT;
+      const int ee = e < NB * 2 * D ? e : 0;
+      const int blk = ee / (2 * D), c = (ee / D) & 1, dd = ee % D;
+      v[p] = cc[((blk0 + blk) * 2 + c) * ldc + dd];
+    }
+  }
+  __device__ static __forceinline__ void strip_commit(bf16_t* st, int NB, int tid,
+                                                      const float (&v)[4]) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int e = tid + p * FNT;
+      if (e < NB * 2 * D) {
+        const int blk = e / (2 * D), c = (e / D) & 1, dd = e % D;
+        const int r = (4 * blk + 2 * c) * SCL + dd;
+        st[r] = f2bf(v[p]);
+        st[r + SCL] = f2bf(v[p] - bf2f(f2bf(v[p])));
+      }
+    }
+  }
+  // row-checksum strip [128 rows][16]: columns 0..3 the hi/lo of the sum
+  // and of the weighted sum of row tid / 2 (columns 4..15 stay zero)
+  __device__ static __forceinline__ void rstrip_commit(bf16_t* rs, int tid, float v) {
+    rs[(tid >> 1) * 16 + 2 * (tid & 1)] = f2bf(v);
+    rs[(tid >> 1) * 16 + 2 * (tid & 1) + 1] = f2bf(v - bf2f(f2bf(v)));
+  }
+};
+
+// The query pass. LDS: the key tile's K and V images and its K^c, V^c and
+// K^r strips (reloaded per key tile), the workgroup's Q and dCL images
+// (loaded once), scratch.
+template <int D, bool CHK>
+struct FusedBwdQ : BwdTile<D> {
+  using T = BwdTile<D>;
+  using typename T::DK;
+  static constexpr int KS = T::KS, DB = T::DB, KH = T::KH, IMG = T::IMG, SCL = T::SCL;
+  static constexpr int OFF_V = IMG, OFF_KC = 2 * IMG, OFF_VC = OFF_KC + T::STRIP;
+  static constexpr int OFF_KR = OFF_VC + T::STRIP;
+  static constexpr int OFF_Q = OFF_KR + T::RSTRIP, OFF_G = OFF_Q + IMG;
+  static constexpr int OFF_SCR = OFF_G + IMG;
+  static constexpr int LDS_BYTES = OFF_SCR + 4 * T::SCR * 4;
 
   __device__ static void run(const FusedBwdDesc& fd, char* smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -792,11 +944,10 @@ struct FusedBwd {
     const bf16_t* CLp = static_cast<const bf16_t*>(fd.cl) + int64_t(b) * S * H + h * D;
     const int nkt = fd.causal ? qt + 1 : nqt;
     const float sl2 = fd.scale * 1.4426950408889634f;
-    const int lg_jpb = __builtin_ctz(R / 16);
     constexpr bool chk = CHK;
 
     // the statistics and the softmax backward's row term D = dCL . CL of
-    // the lane's queries
+    // the lane's queries (D also kept for the key pass)
     float mq[2], il[2], dq[2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
@@ -813,6 +964,7 @@ struct FusedBwd {
       const float* st = fd.stats + ((int64_t(b) * fd.nh + h) * S + q) * 2;
       mq[qb] = st[0];
       il[qb] = 1.f / st[1];
+      if (g == 0) fd.drow[(int64_t(b) * fd.nh + h) * S + q] = dq[qb];
     }
     // Q and dCL images of the workgroup's queries (complete with tile 0)
 #pragma unroll
@@ -830,43 +982,20 @@ struct FusedBwd {
         DK::issue(Vp, ld, key0, S, hf * 64, smem + OFF_V + hf * DK::BYTES, wave, lane);
       }
       if (chk) {
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const int e = tid + p * FNT;
-          const int ee = e < NB * 2 * D ? e : 0;
-          const int blk = ee / (2 * D), c = (ee / D) & 1, dd = ee % D;
-          const float* row =
-              fd.qkvc + ((int64_t(b) * nqR + key0 / R + blk) * 2 + c) * ld + h * D + dd;
-          kcv[p] = row[H];
-          vcv[p] = row[2 * H];
-        }
+        const int64_t blk0 = int64_t(b) * nqR + key0 / R;
+        T::strip_issue(fd.qkvc + H + h * D, ld, blk0, NB, tid, kcv);
+        T::strip_issue(fd.qkvc + 2 * H + h * D, ld, blk0, NB, tid, vcv);
         krv = fd.kr[((int64_t(b) * S + key0 + (tid >> 1)) * fd.nh + h) * 2 + (tid & 1)];
       }
     };
+    bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
     auto commit = [&]() {
       if (chk) {
-        bf16_t* kcs = reinterpret_cast<bf16_t*>(smem + OFF_KC);
-        bf16_t* vcs = reinterpret_cast<bf16_t*>(smem + OFF_VC);
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const int e = tid + p * FNT;
-          if (e < NB * 2 * D) {
-            const int blk = e / (2 * D), c = (e / D) & 1, dd = e % D;
-            const int r = (4 * blk + 2 * c) * SCL + dd;
-            kcs[r] = f2bf(kcv[p]);
-            kcs[r + SCL] = f2bf(kcv[p] - bf2f(f2bf(kcv[p])));
-            vcs[r] = f2bf(vcv[p]);
-            vcs[r + SCL] = f2bf(vcv[p] - bf2f(f2bf(vcv[p])));
-          }
-        }
-        bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
-        krs[(tid >> 1) * 16 + 2 * (tid & 1)] = f2bf(krv);
-        krs[(tid >> 1) * 16 + 2 * (tid & 1) + 1] = f2bf(krv - bf2f(f2bf(krv)));
+        T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_KC), NB, tid, kcv);
+        T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_VC), NB, tid, vcv);
+        T::rstrip_commit(krs, tid, krv);
       }
     };
-    // K^r strip: columns 0..3 per key (hi/lo of the sum and of the 1-based
-    // weighted sum over the head dims, written with each tile); 4..15 zero
-    bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
     if (chk)
       for (int e = tid; e < FT * 12; e += FNT) krs[(e / 12) * 16 + 4 + e % 12] = 0;
 
@@ -877,11 +1006,7 @@ struct FusedBwd {
       for (int db = 0; db < DB; ++db) dqa[db][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
       kra[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
-    float* scr = reinterpret_cast<float*>(smem + OFF_SCR) + wave * SCR;
-    bf16_t* AP = static_cast<bf16_t*>(fd.ap) + (int64_t(b) * fd.nh + h) * S * S;
-    bf16_t* dAS = static_cast<bf16_t*>(fd.das) + (int64_t(b) * fd.nh + h) * S * S;
-    float* APr = fd.apr + (int64_t(b) * fd.nh + h) * S * nqR * 2;
-    float* dASr = fd.dasr + (int64_t(b) * fd.nh + h) * S * nqR * 2;
+    float* scr = reinterpret_cast<float*>(smem + OFF_SCR) + wave * T::SCR;
 
     for (int kt = 0; kt < nkt; ++kt) {
       issue(kt);
@@ -889,7 +1014,6 @@ struct FusedBwd {
       commit();
       __syncthreads();  // tile kt in LDS
       const int key0 = kt * FT;
-
       const bool diag = fd.causal && kt == qt;
       // B operand fragments of the wave's queries (rows of the Q or dCL image)
       auto bfrag = [&](int off, int qb, int kk) {
@@ -924,12 +1048,11 @@ struct FusedBwd {
             ks[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc, qf1, ks[1], 0, 0, 0);
           }
         }
-        if (fd.n_faults > 0) inject_tile(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
-        if (chk) check_tile(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
+        if (fd.n_faults > 0) T::template inject<false>(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
+        if (chk) T::template check<false>(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
           const int q = qw + 16 * qb + lq;
-          float a1[4] = {0.f, 0.f, 0.f, 0.f}, a2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             float a[4];
@@ -940,27 +1063,6 @@ struct FusedBwd {
                           : 0.f;
             }
             pk[j][qb] = uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
-            *reinterpret_cast<uint2*>(AP + int64_t(q) * S + key0 + 16 * j + 4 * g) = pk[j][qb];
-            if (!chk) continue;
-            // the 16-key group j lies in block j >> lg_jpb; weights 1..R in it
-            const int wb = ((16 * j) & (R - 1)) + 4 * g + 1;
-            const float sa1 = (a[0] + a[1]) + (a[2] + a[3]);
-            const float sa2 = float(wb) * a[0] + float(wb + 1) * a[1] + float(wb + 2) * a[2] +
-                              float(wb + 3) * a[3];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if ((j >> lg_jpb) == i) { a1[i] += sa1; a2[i] += sa2; }
-          }
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (chk && i < NB) {
-              const float t1 = group4_sum(a1[i]), t2 = group4_sum(a2[i]);
-              if (g == i) {
-                const int64_t o = (int64_t(q) * nqR + key0 / R + i) * 2;
-                APr[o] = t1;
-                APr[o + 1] = t2;
-              }
-            }
           }
         }
       }
@@ -990,12 +1092,11 @@ struct FusedBwd {
             vs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vc, gf1, vs[1], 0, 0, 0);
           }
         }
-        if (fd.n_faults > 0) inject_tile(dp, fd, ABFT_OP_DAP, b, h, qw, key0, lane);
-        if (chk) check_tile(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr, lane);
+        if (fd.n_faults > 0) T::template inject<false>(dp, fd, ABFT_OP_DAP, b, h, qw, key0, lane);
+        if (chk) T::template check<false>(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr, lane);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
           const int q = qw + 16 * qb + lq;
-          float d1[4] = {0.f, 0.f, 0.f, 0.f}, d2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const float a[4] = {__uint_as_float(pk[j][qb].x << 16),
@@ -1009,26 +1110,6 @@ struct FusedBwd {
               ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][qb][r] - dq[qb]))) : 0.f;
             }
             pk[j][qb] = uint2{pack2(ds[0], ds[1]), pack2(ds[2], ds[3])};
-            *reinterpret_cast<uint2*>(dAS + int64_t(q) * S + key0 + 16 * j + 4 * g) = pk[j][qb];
-            if (!chk) continue;
-            const int wb = ((16 * j) & (R - 1)) + 4 * g + 1;
-            const float sd1 = (ds[0] + ds[1]) + (ds[2] + ds[3]);
-            const float sd2 = float(wb) * ds[0] + float(wb + 1) * ds[1] + float(wb + 2) * ds[2] +
-                              float(wb + 3) * ds[3];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if ((j >> lg_jpb) == i) { d1[i] += sd1; d2[i] += sd2; }
-          }
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (chk && i < NB) {
-              const float u1 = group4_sum(d1[i]), u2 = group4_sum(d2[i]);
-              if (g == i) {
-                const int64_t o = (int64_t(q) * nqR + key0 / R + i) * 2;
-                dASr[o] = u1;
-                dASr[o + 1] = u2;
-              }
-            }
           }
         }
       }
@@ -1036,128 +1117,304 @@ struct FusedBwd {
       // dQ^T += K^T dS^T and (dQ^r)^T += (K^r)^T dS^T
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        bf16x8 pf[2];
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const uint4 u = {pk[2 * t][qb].x, pk[2 * t][qb].y, pk[2 * t + 1][qb].x,
-                           pk[2 * t + 1][qb].y};
-          pf[qb] = __builtin_bit_cast(bf16x8, u);
-        }
+        const bf16x8 pf0 = T::slab(pk, t, 0), pf1 = T::slab(pk, t, 1);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          TrPair kp = kt_frag(smem, 16 * db, 32 * t, lane);
+          TrPair kp = T::t_frag(smem, 16 * db, 32 * t, lane);
           const bf16x8 kf = tr_join(kp);
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
-            dqa[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, pf[qb], dqa[db][qb], 0, 0, 0);
+          dqa[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, pf0, dqa[db][0], 0, 0, 0);
+          dqa[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, pf1, dqa[db][1], 0, 0, 0);
         }
         if (chk) {
-          TrPair rp = kr_frag(krs, 32 * t, lane);
+          TrPair rp = T::rs_frag(krs, 32 * t, lane);
           const bf16x8 rf = tr_join(rp);
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
-            kra[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf[qb], kra[qb], 0, 0, 0);
+          kra[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf0, kra[0], 0, 0, 0);
+          kra[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf1, kra[1], 0, 0, 0);
         }
       }
       __syncthreads();  // the one stage is reloaded next
     }
 
-    // dQ: round, check against dQ^r, store
-    bf16_t* dQp = static_cast<bf16_t*>(fd.dq) + int64_t(b) * S * fd.ldq + h * D;
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const int q = qw + 16 * qb + lq;
-      float ov[DB][4];
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) ov[db][r] = bf2f(f2bf(dqa[db][qb][r]));
-      if (fd.n_faults > 0) {
-        for (int f = 0; f < fd.n_faults; ++f) {
-          const abft_fault ft = fd.faults[f];
-          if (ft.op != ABFT_OP_DQ || ft.b != b || ft.h != h || ft.row != q) continue;
-#pragma unroll
-          for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (ft.col == 16 * db + 4 * g + r)
-                ov[db][r] = ft.mode == ABFT_FAULT_FLIP ? bf2f(flip_exponent_msb(f2bf(ov[db][r])))
-                                                       : bf2f(f2bf(ft.value));
-        }
-      }
-      if (chk) {
-        const float c1 = __shfl(kra[qb][0] + kra[qb][1], lq, 64);
-        const float c2 = __shfl(kra[qb][2] + kra[qb][3], lq, 64);
-        float r1 = 0.f, ra = 0.f;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            r1 += ov[db][r];
-            ra += fabsf(ov[db][r]);
-          }
-        r1 = group4_sum(r1);
-        ra = group4_sum(ra);
-        uint64_t mask = __ballot(g == 0 && flagged(c1 - r1, ra, fd.e_rel));
-        while (mask) {
-          const int L = __builtin_ctzll(mask);
-          mask &= mask - 1;
-          if (lq == L) {
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-              for (int r = 0; r < 4; ++r) scr[16 * db + 4 * g + r] = ov[db][r];
-          }
-          const float v1 = __shfl(c1, L, 64), v2 = __shfl(c2, L, 64);
-          wave_sync_lds();
-          if (lane == 0) {
-            const int qq = qw + 16 * qb + L;
-            const EecResult res = eec_locate<float>(scr, 1, D, v1, v2, fd.e_rel, fd.tn);
-            int idx = -1;
-            float nv = 0.f;
-            if (res.status == EEC_LOCATED) {
-              idx = res.index;
-              const float old = scr[idx];
-              int action = 0;
-              nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, D, idx, v1, res.d1, fd.tc, &action)));
-              scr[idx] = nv;
-              record_event(fd.report, ABFT_OP_DQ, b, h, qq, idx, classify(old, fd.tn), action, old);
-            }
-            if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, D, v1, fd.e_rel))
-              record_event(fd.report, ABFT_OP_DQ, b, h, qq, 0, ABFT_KIND_NONE,
-                           ABFT_ACT_UNCORRECTABLE, 0.f);
-            scr[D] = __int_as_float(idx);
-            scr[D + 1] = nv;
-          }
-          wave_sync_lds();
-          const int idx = __float_as_int(scr[D]);
-          const float nv = scr[D + 1];
-          if (idx >= 0 && lq == L) {
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (idx == 16 * db + 4 * g + r) ov[db][r] = nv;
-          }
-          wave_sync_lds();
-        }
-      }
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const uint2 w = {pack2(ov[db][0], ov[db][1]), pack2(ov[db][2], ov[db][3])};
-        *reinterpret_cast<uint2*>(dQp + int64_t(q) * fd.ldq + 16 * db + 4 * g) = w;
-      }
-    }
+    bf16_t* dQp = static_cast<bf16_t*>(fd.dqkv) + int64_t(b) * S * fd.ld + h * D;
+    T::finish(dqa, kra, fd, chk, ABFT_OP_DQ, b, h, qw, dQp, fd.ld, scr, lane);
   }
 };
 
-// one wave per SIMD for the checked kernels: their registers fit without
-// spills (two waves per SIMD spilled and ran slower)
+// The key pass. LDS: the workgroup's K and V images (loaded once); per
+// query tile the Q and dCL images, the Q^c and dCL^c strips, the Q^r and
+// dCL^r row-checksum strips and the queries' max, 1 / sum and D; scratch.
 template <int D, bool CHK>
-__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(D == 64 && !CHK ? 2 : 1)))
-void fused_bwd_kernel(FusedBwdDesc fd) {
+struct FusedBwdKV : BwdTile<D> {
+  using T = BwdTile<D>;
+  using typename T::DK;
+  static constexpr int KS = T::KS, DB = T::DB, KH = T::KH, IMG = T::IMG, SCL = T::SCL;
+  static constexpr int OFF_V = IMG, OFF_Q = 2 * IMG, OFF_G = 3 * IMG;
+  static constexpr int OFF_QC = 4 * IMG, OFF_GC = OFF_QC + T::STRIP;
+  static constexpr int OFF_QR = OFF_GC + T::STRIP, OFF_GR = OFF_QR + T::RSTRIP;
+  static constexpr int OFF_ROW = OFF_GR + T::RSTRIP;           // [3][128] floats
+  static constexpr int OFF_SCR = OFF_ROW + 3 * FT * 4;
+  static constexpr int LDS_BYTES = OFF_SCR + 4 * T::SCR * 4;
+  static_assert(LDS_BYTES <= 160 * 1024, "one workgroup fits the LDS");
+
+  __device__ static void run(const FusedBwdDesc& fd, char* smem) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lq = lane & 15, g = lane >> 4;
+    const int S = fd.S, H = fd.H, R = fd.R, NB = FT / R, nqR = S / R;
+    const int nqt = S / FT, nbh = fd.B * fd.nh;
+    const int z = blockIdx.x % nbh;
+    const int kt = int(blockIdx.x) / nbh;   // causal: the first key tiles see the most queries
+    const int b = z / fd.nh, h = z % fd.nh;
+    const int key0 = kt * FT, kw = key0 + wave * 32;
+    const int64_t ld = 3 * int64_t(H);
+    const bf16_t* base = static_cast<const bf16_t*>(fd.qkv) + int64_t(b) * S * ld;
+    const bf16_t* Qp = base + h * D;
+    const bf16_t* Kp = base + H + h * D;
+    const bf16_t* Vp = base + 2 * H + h * D;
+    const bf16_t* dCLp = static_cast<const bf16_t*>(fd.dcl) + int64_t(b) * S * H + h * D;
+    const int qt0 = fd.causal ? kt : 0;
+    const float sl2 = fd.scale * 1.4426950408889634f;
+    constexpr bool chk = CHK;
+    const int64_t bh = int64_t(b) * fd.nh + h;
+
+    // K and V images of the workgroup's keys (complete with the first tile)
+#pragma unroll
+    for (int hf = 0; hf < KH; ++hf) {
+      DK::issue(Kp, ld, key0, S, hf * 64, smem + hf * DK::BYTES, wave, lane);
+      DK::issue(Vp, ld, key0, S, hf * 64, smem + OFF_V + hf * DK::BYTES, wave, lane);
+    }
+    bf16_t* qrs = reinterpret_cast<bf16_t*>(smem + OFF_QR);
+    bf16_t* grs = reinterpret_cast<bf16_t*>(smem + OFF_GR);
+    if (chk)
+      for (int e = tid; e < FT * 12; e += FNT) {
+        qrs[(e / 12) * 16 + 4 + e % 12] = 0;
+        grs[(e / 12) * 16 + 4 + e % 12] = 0;
+      }
+    float* rowf = reinterpret_cast<float*>(smem + OFF_ROW);
+
+    float qcv[4] = {0.f, 0.f, 0.f, 0.f}, gcv[4] = {0.f, 0.f, 0.f, 0.f};
+    float qrv = 0.f, grv = 0.f, rv0 = 0.f, rv1 = 0.f;
+    auto issue = [&](int qt) {
+      const int q0 = qt * FT;
+#pragma unroll
+      for (int hf = 0; hf < KH; ++hf) {
+        DK::issue(Qp, ld, q0, S, hf * 64, smem + OFF_Q + hf * DK::BYTES, wave, lane);
+        DK::issue(dCLp, H, q0, S, hf * 64, smem + OFF_G + hf * DK::BYTES, wave, lane);
+      }
+      // threads 0..127: max and sum of query q0 + tid; 128..255: its D
+      const int qi = q0 + (tid & (FT - 1));
+      if (tid < FT) {
+        rv0 = fd.stats[(bh * S + qi) * 2];
+        rv1 = fd.stats[(bh * S + qi) * 2 + 1];
+      } else {
+        rv0 = fd.drow[bh * S + qi];
+      }
+      if (chk) {
+        const int64_t blk0 = int64_t(b) * nqR + q0 / R;
+        T::strip_issue(fd.qkvc + h * D, ld, blk0, NB, tid, qcv);
+        T::strip_issue(fd.dclc + h * D, H, blk0, NB, tid, gcv);
+        const int64_t ri = ((int64_t(b) * S + q0 + (tid >> 1)) * fd.nh + h) * 2 + (tid & 1);
+        qrv = fd.qr[ri];
+        grv = fd.dclr[ri];
+      }
+    };
+    auto commit = [&]() {
+      if (tid < FT) {
+        rowf[tid] = rv0;
+        rowf[FT + tid] = 1.f / rv1;
+      } else {
+        rowf[2 * FT + tid - FT] = rv0;
+      }
+      if (chk) {
+        T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_QC), NB, tid, qcv);
+        T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_GC), NB, tid, gcv);
+        T::rstrip_commit(qrs, tid, qrv);
+        T::rstrip_commit(grs, tid, grv);
+      }
+    };
+
+    floatx4 dva[DB][2], dka[DB][2], vra[2], kra[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        dva[db][c] = floatx4{0.f, 0.f, 0.f, 0.f};
+        dka[db][c] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+      vra[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+      kra[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    float* scr = reinterpret_cast<float*>(smem + OFF_SCR) + wave * T::SCR;
+
+    for (int qt = qt0; qt < nqt; ++qt) {
+      issue(qt);
+      wait_vmcnt<0>();
+      commit();
+      __syncthreads();  // query tile qt in LDS
+      const int q0 = qt * FT;
+      const bool diag = fd.causal && qt == kt;
+      // A operand fragments of the tile's queries (rows 16 j..) and B
+      // operand fragments of the wave's keys (rows of the K or V image)
+      auto afrag = [&](int off, int j, int kk) {
+        return DK::frag(smem + off + (kk >> 1) * DK::BYTES, 16 * j, (kk & 1) * 32, lane);
+      };
+      auto kfrag = [&](int off, int c, int kk) {
+        return DK::frag(smem + off + (kk >> 1) * DK::BYTES, wave * 32 + 16 * c, (kk & 1) * 32, lane);
+      };
+      // P, then dS, packed to bf16: pk[j][c] holds queries 16 j + 4 g + 0..3
+      // of key kw + 16 c + lane % 16
+      uint2 pk[8][2];
+      {
+        // S = Q K^T with its strip rows (Q^c) K^T, column-checked; P
+        floatx4 s[8][2], cs[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) s[j][c] = floatx4{0.f, 0.f, 0.f, 0.f};
+          cs[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          const bf16x8 kf0 = kfrag(0, 0, kk), kf1 = kfrag(0, 1, kk);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const bf16x8 qf = afrag(OFF_Q, j, kk);
+            s[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, kf0, s[j][0], 0, 0, 0);
+            s[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, kf1, s[j][1], 0, 0, 0);
+          }
+          if (chk) {
+            const bf16_t* qcs = reinterpret_cast<const bf16_t*>(smem + OFF_QC);
+            const bf16x8 qc = *reinterpret_cast<const bf16x8*>(qcs + lq * SCL + 32 * kk + 8 * g);
+            cs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qc, kf0, cs[0], 0, 0, 0);
+            cs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qc, kf1, cs[1], 0, 0, 0);
+          }
+        }
+        if (fd.n_faults > 0) T::template inject<true>(s, fd, ABFT_OP_AS, b, h, kw, q0, lane);
+        if (chk) T::template check<true>(s, cs, fd, ABFT_OP_AS, b, h, kw, q0, Kp, Qp, ld, ld, scr, lane);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float4 m4 = *reinterpret_cast<const float4*>(rowf + 16 * j + 4 * g);
+          const float4 i4 = *reinterpret_cast<const float4*>(rowf + FT + 16 * j + 4 * g);
+          const float mv[4] = {m4.x, m4.y, m4.z, m4.w}, iv[4] = {i4.x, i4.y, i4.z, i4.w};
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const int key = kw + 16 * c + lq;
+            float a[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
+              a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][c][r] * sl2 - mv[r]) * iv[r]))
+                          : 0.f;
+            }
+            pk[j][c] = uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
+          }
+        }
+      }
+      // dV^T += dCL^T P and (dV^r)^T += (dCL^r)^T P
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const bf16x8 pf0 = T::slab(pk, t, 0), pf1 = T::slab(pk, t, 1);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          TrPair gp = T::t_frag(smem + OFF_G, 16 * db, 32 * t, lane);
+          const bf16x8 gf = tr_join(gp);
+          dva[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gf, pf0, dva[db][0], 0, 0, 0);
+          dva[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gf, pf1, dva[db][1], 0, 0, 0);
+        }
+        if (chk) {
+          TrPair rp = T::rs_frag(grs, 32 * t, lane);
+          const bf16x8 rf = tr_join(rp);
+          vra[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf0, vra[0], 0, 0, 0);
+          vra[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf1, vra[1], 0, 0, 0);
+        }
+      }
+      {
+        // dP = dCL V^T with its strip rows (dCL^c) V^T, column-checked; dS
+        floatx4 dp[8][2], cs[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) dp[j][c] = floatx4{0.f, 0.f, 0.f, 0.f};
+          cs[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          const bf16x8 vf0 = kfrag(OFF_V, 0, kk), vf1 = kfrag(OFF_V, 1, kk);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const bf16x8 gf = afrag(OFF_G, j, kk);
+            dp[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gf, vf0, dp[j][0], 0, 0, 0);
+            dp[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gf, vf1, dp[j][1], 0, 0, 0);
+          }
+          if (chk) {
+            const bf16_t* gcs = reinterpret_cast<const bf16_t*>(smem + OFF_GC);
+            const bf16x8 gc = *reinterpret_cast<const bf16x8*>(gcs + lq * SCL + 32 * kk + 8 * g);
+            cs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gc, vf0, cs[0], 0, 0, 0);
+            cs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gc, vf1, cs[1], 0, 0, 0);
+          }
+        }
+        if (fd.n_faults > 0) T::template inject<true>(dp, fd, ABFT_OP_DAP, b, h, kw, q0, lane);
+        if (chk) T::template check<true>(dp, cs, fd, ABFT_OP_DAP, b, h, kw, q0, Vp, dCLp, ld, H, scr, lane);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float4 d4 = *reinterpret_cast<const float4*>(rowf + 2 * FT + 16 * j + 4 * g);
+          const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const int key = kw + 16 * c + lq;
+            const float a[4] = {__uint_as_float(pk[j][c].x << 16),
+                                __uint_as_float(pk[j][c].x & 0xffff0000u),
+                                __uint_as_float(pk[j][c].y << 16),
+                                __uint_as_float(pk[j][c].y & 0xffff0000u)};
+            float ds[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
+              ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][c][r] - dv[r]))) : 0.f;
+            }
+            pk[j][c] = uint2{pack2(ds[0], ds[1]), pack2(ds[2], ds[3])};
+          }
+        }
+      }
+      // dK^T += Q^T dS and (dK^r)^T += (Q^r)^T dS
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const bf16x8 pf0 = T::slab(pk, t, 0), pf1 = T::slab(pk, t, 1);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          TrPair qp = T::t_frag(smem + OFF_Q, 16 * db, 32 * t, lane);
+          const bf16x8 qf = tr_join(qp);
+          dka[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, pf0, dka[db][0], 0, 0, 0);
+          dka[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, pf1, dka[db][1], 0, 0, 0);
+        }
+        if (chk) {
+          TrPair rp = T::rs_frag(qrs, 32 * t, lane);
+          const bf16x8 rf = tr_join(rp);
+          kra[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf0, kra[0], 0, 0, 0);
+          kra[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf1, kra[1], 0, 0, 0);
+        }
+      }
+      __syncthreads();  // the query tile's buffers are reloaded next
+    }
+
+    bf16_t* outp = static_cast<bf16_t*>(fd.dqkv) + int64_t(b) * S * fd.ld + h * D;
+    T::finish(dka, kra, fd, chk, ABFT_OP_DK, b, h, kw, outp + H, fd.ld, scr, lane);
+    T::finish(dva, vra, fd, chk, ABFT_OP_DV, b, h, kw, outp + 2 * H, fd.ld, scr, lane);
+  }
+};
+
+// one wave per SIMD: with two the registers of every variant spill
+template <int D, bool CHK>
+__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(1)))
+void fused_bwd_q_kernel(FusedBwdDesc fd) {
   extern __shared__ __align__(16) char smem[];
-  FusedBwd<D, CHK>::run(fd, smem);
+  FusedBwdQ<D, CHK>::run(fd, smem);
+}
+
+template <int D, bool CHK>
+__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(1)))
+void fused_bwd_kv_kernel(FusedBwdDesc fd) {
+  extern __shared__ __align__(16) char smem[];
+  FusedBwdKV<D, CHK>::run(fd, smem);
 }
 
 template <int D, bool PROT>
@@ -1185,34 +1442,52 @@ hipError_t launch_d(const FusedDesc& fd, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int D, bool CHK>
-hipError_t launch_bwd_d(const FusedBwdDesc& fd, hipStream_t s) {
-  using F = FusedBwd<D, CHK>;
+template <auto KERN>
+hipError_t launch_bwd_kernel(const FusedBwdDesc& fd, int lds, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
-    const hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(fused_bwd_kernel<D, CHK>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, F::LDS_BYTES);
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(KERN),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int64_t grid = int64_t(fd.B) * fd.nh * (fd.S / FT);
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL((fused_bwd_kernel<D, CHK>), dim3(unsigned(grid)), dim3(FNT), F::LDS_BYTES, s,
-                     fd);
+  hipLaunchKernelGGL(KERN, dim3(unsigned(grid)), dim3(FNT), lds, s, fd);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_fused_bwd(const FusedBwdDesc& fd, hipStream_t s) {
-  if (fd.S % FT != 0 || fd.R < 32 || FT % fd.R != 0 || fd.H != fd.nh * fd.D ||
-      fd.qkv == nullptr || fd.cl == nullptr || fd.dcl == nullptr || fd.stats == nullptr ||
-      fd.ap == nullptr || fd.apr == nullptr || fd.das == nullptr || fd.dasr == nullptr ||
-      fd.dq == nullptr || fd.ldq < fd.H || (fd.check && (fd.qkvc == nullptr || fd.kr == nullptr)))
+// shapes and operands both passes need
+static bool bwd_desc_ok(const FusedBwdDesc& fd) {
+  return fd.S % FT == 0 && fd.R >= 32 && FT % fd.R == 0 && fd.H == fd.nh * fd.D &&
+         fd.qkv != nullptr && fd.dcl != nullptr && fd.stats != nullptr && fd.drow != nullptr &&
+         fd.dqkv != nullptr && fd.ld >= 3 * int64_t(fd.H);
+}
+
+hipError_t launch_fused_bwd_q(const FusedBwdDesc& fd, hipStream_t s) {
+  if (!bwd_desc_ok(fd) || fd.cl == nullptr || (fd.check && (fd.qkvc == nullptr || fd.kr == nullptr)))
     return hipErrorInvalidValue;
-  if (fd.D == 64) return fd.check ? launch_bwd_d<64, true>(fd, s) : launch_bwd_d<64, false>(fd, s);
-  if (fd.D == 128) return fd.check ? launch_bwd_d<128, true>(fd, s) : launch_bwd_d<128, false>(fd, s);
+  if (fd.D == 64)
+    return fd.check ? launch_bwd_kernel<fused_bwd_q_kernel<64, true>>(fd, FusedBwdQ<64, true>::LDS_BYTES, s)
+                    : launch_bwd_kernel<fused_bwd_q_kernel<64, false>>(fd, FusedBwdQ<64, false>::LDS_BYTES, s);
+  if (fd.D == 128)
+    return fd.check ? launch_bwd_kernel<fused_bwd_q_kernel<128, true>>(fd, FusedBwdQ<128, true>::LDS_BYTES, s)
+                    : launch_bwd_kernel<fused_bwd_q_kernel<128, false>>(fd, FusedBwdQ<128, false>::LDS_BYTES, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_fused_bwd_kv(const FusedBwdDesc& fd, hipStream_t s) {
+  if (!bwd_desc_ok(fd) ||
+      (fd.check && (fd.qkvc == nullptr || fd.qr == nullptr || fd.dclr == nullptr || fd.dclc == nullptr)))
+    return hipErrorInvalidValue;
+  if (fd.D == 64)
+    return fd.check ? launch_bwd_kernel<fused_bwd_kv_kernel<64, true>>(fd, FusedBwdKV<64, true>::LDS_BYTES, s)
+                    : launch_bwd_kernel<fused_bwd_kv_kernel<64, false>>(fd, FusedBwdKV<64, false>::LDS_BYTES, s);
+  if (fd.D == 128)
+    return fd.check ? launch_bwd_kernel<fused_bwd_kv_kernel<128, true>>(fd, FusedBwdKV<128, true>::LDS_BYTES, s)
+                    : launch_bwd_kernel<fused_bwd_kv_kernel<128, false>>(fd, FusedBwdKV<128, false>::LDS_BYTES, s);
   return hipErrorInvalidValue;
 }
 

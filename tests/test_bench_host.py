@@ -98,4 +98,10 @@ def test_stage_tables_cover_each_path_once():
         bwd = [m for _, b, m, *_ in t if b]
         assert len(set(fwd)) == len(fwd) and len(set(bwd)) == len(bwd)
         names = {n for n, *_ in t}
-        assert ("core_bwd" in names) == fused and ("softmax_bwd" in names) != fused
+        assert ("core_kv" in names) == fused and ("softmax_bwd" in names) != fused
+        # every GEMM flop of the step is in some stage: the useful flops
+        # plus, in the fused backward, the recomputations (S in both
+        # passes, dP once more: three score-sized products)
+        sq = 8 * 12 * (1024 * 1025 // 2)
+        extra = 3 * 2 * sq * 64 if fused else 0
+        assert sum(f for _, _, _, f, _, _ in t) == bench.useful_flops(8, 1024, 768, 12, True) + extra

@@ -170,15 +170,15 @@ def test_fused_context_faults():
 
 
 def test_fused_key_fault_without_root_check():
-    """Root check off: a near-INF key element makes a 1C pattern in the
-    scores (Sec. 4.3), fixed row by row from the row checksums; |delta_1|
-    is far above T_correct in every row, so every fix reconstructs."""
+    """Root check off: the fused form still verifies K at the projection
+    (its backward's key pass checks score columns, which cannot see a K
+    error); the near-INF element is fixed there from K's checksums and the
+    scores see nothing."""
     shape = W.make_shape(1, 256, 128, 2, causal=False, block_rows=128, name="kfault")
     faults = [W.Fault("K", 0, 0, 77, 5, 1e10)]
     g, o = run_fused(shape, faults, root_check=False)
     assert sorted(g["rep"]["events"]) == sorted(o["events"])
-    assert len([e for e in o["events"] if e[0] == "AS"]) == 256
-    assert all(e[6] == "RECONSTRUCT" for e in g["rep"]["events"] if e[0] == "AS")
+    assert [(e[0], e[3], e[4], e[6]) for e in o["events"]] == [("K", 77, 5, "RECONSTRUCT")]
     check_outputs(g, o, shape)
 
 
@@ -256,13 +256,12 @@ def run_fused_training(shape, faults=(), seed=1):
     cfg = abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads,
                            causal=shape.causal, block_rows=shape.block_rows, fused=True)
     layer = abft.ProtectedAttention(cfg)
-    layer.tensor("AP").fill_(float("nan"))   # sentinel: unwritten stays NaN
     X, Wqkv, Wo, dO = (dev(inp[k]) for k in ("X", "Wqkv", "Wo", "dO"))
     fdev = abft.faults_to_device(list(faults))
     O = layer.forward(X, Wqkv, Wo, fdev)
     dX, dWqkv, dWo = layer.backward(dO, X, Wqkv, Wo, fdev)
     torch.cuda.synchronize()
-    g = dict(O=host(O), AP=host(layer.tensor("AP")), dX=host(dX), dWqkv=host(dWqkv),
+    g = dict(O=host(O), dQKV=host(layer.tensor("dQKV")), dX=host(dX), dWqkv=host(dWqkv),
              dWo=host(dWo), rep_f=abft.read_report(layer.report),
              rep_b=abft.read_report(layer.report_bwd))
     from oracle import backward
@@ -283,18 +282,23 @@ def test_fused_forward_backward(causal, R):
     g, o, ob = run_fused_training(shape)
     assert g["rep_f"]["events"] == [] and g["rep_b"]["events"] == []
     assert o["events"] == [] and ob["events"] == []
-    # the regenerated probabilities on the pairs the mask allows; masked
-    # ones are zero where written and keep the sentinel elsewhere
-    S = shape.seq
-    tri = np.tril(np.ones((S, S), dtype=bool)) if causal else np.ones((S, S), dtype=bool)
-    allowed = np.broadcast_to(tri, g["AP"].shape)
-    ap_g, ap_o = g["AP"][allowed], o["AP"][allowed]
-    # AP is rounded to bf16 on both sides from exponentials taken in fp32
-    # and fp64: one bf16 step apart at most
-    assert np.all(np.abs(ap_g - ap_o) <= 2.0 ** -7 * np.abs(ap_o))
-    up = g["AP"][~allowed]
-    assert np.all((up == 0.0) | np.isnan(up))
     check_training_outputs(g, o, ob, shape)
+
+
+def test_fused_workspace_holds_no_scores():
+    """The fused form keeps no score-shaped tensor: its workspace is
+    smaller than the materialised one by more than the four S x S tensors'
+    worth and the score tensors are not addressable."""
+    abft = _abft()
+    kw = dict(causal=True, block_rows=128)
+    fz = abft.LayerConfig(2, 512, 256, 4, fused=True, **kw)
+    mat = abft.LayerConfig(2, 512, 256, 4, **kw)
+    ss = 2 * 4 * 512 * 512 * 2
+    assert abft.attn_abft_workspace_bytes(fz) + 3 * ss < abft.attn_abft_workspace_bytes(mat)
+    layer = abft.ProtectedAttention(fz)
+    for name in ("AS", "AP", "APc", "APr", "dAS"):
+        with pytest.raises(abft.AbftError):
+            layer.tensor(name)
 
 
 def check_training_outputs(g, o, ob, shape):
@@ -330,10 +334,13 @@ def test_fused_backward_faults(R):
     faults = [W.Fault("AS", 0, 1, 200, 3, np.inf), W.Fault("dV", 0, 0, 17, 9, np.nan),
               W.Fault("dQ", 0, 1, 130, 60, 1e10), W.Fault("dX", 0, 0, 77, 100, np.inf),
               W.Fault("dAP", 0, 0, 250, 249, -1e10), W.Fault("dQ", 0, 0, 31, 5, 40.0),
-              W.Fault("dAP", 0, 1, 100, 7, 0.0, mode="flip")]
+              W.Fault("dAP", 0, 1, 100, 7, 0.0, mode="flip"), W.Fault("dK", 0, 1, 66, 40, -np.inf),
+              W.Fault("dK", 0, 0, 255, 0, 30.0)]
     g, o, ob = run_fused_training(shape, faults)
     assert g["rep_f"]["overflow"] == 0 and g["rep_b"]["overflow"] == 0
     assert sorted(g["rep_f"]["events"]) == sorted(o["events"])
     assert sorted(g["rep_b"]["events"]) == sorted(ob["events"])
-    assert len(o["events"]) == 1 and len(ob["events"]) == len(faults)
+    # score and dP faults reach both passes of the fused backward
+    twice = sum(f.op in ("AS", "dAP") for f in faults)
+    assert len(o["events"]) == 1 and len(ob["events"]) == len(faults) + twice
     check_training_outputs(g, o, ob, shape)

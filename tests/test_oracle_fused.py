@@ -102,19 +102,30 @@ def test_score_fault_is_recomputed_and_the_run_restored(kind, causal):
     assert np.array_equal(f["CL"], f0["CL"]) and np.array_equal(f["O"], f0["O"])
 
 
-def test_key_fault_without_root_check_is_corrected_along_its_column():
-    """Root check off: a K error corrupts one score column in every query
-    that sees the key (1C); each row vector locates it and fixes it from
-    the checksums (K^c came from the clean projection)."""
+def test_key_fault_without_root_check():
+    """Root check off. On the attention core alone (K unverified) a K error
+    corrupts one score column in every query that sees the key (1C), which
+    each row vector locates and fixes from the checksums (K^c came from the
+    clean projection). The fused form verifies K at the projection in every
+    mode (its backward's key pass checks score columns, which cannot see a
+    K error), so there the element is fixed from K's checksums and the
+    scores see nothing."""
+    from oracle.fused import fused_attention
+    from oracle.layer import _Run, project
     inp = _inputs()
     p = OracleParams(heads=2, dtype="bf16", causal=False, block_rows=128, root_check=False)
     f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
-    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, [W.Fault("K", 0, 0, 77, 5, 1e6)])
-    ev = [e for e in f["events"] if e[0] == "AS"]
+    fault = [W.Fault("K", 0, 0, 77, 5, 1e6)]
+    run = _Run(p, fault)
+    pr = project(run, inp["X"], inp["Wqkv"], p)               # K not verified
+    CL, _ = fused_attention(run, pr, p)
+    ev = [e for e in run.events if e[0] == "AS"]
     assert len(ev) == 256 and {e[4] for e in ev} == {77} and {e[3] for e in ev} == set(range(256))
     assert all(e[6] in ("DELTA", "RECONSTRUCT") for e in ev)
-    err = np.abs(f["CL"] - f0["CL"]).max()
-    assert err <= 2.0 ** -6 * np.abs(f0["CL"]).max()
+    assert np.abs(CL - f0["CL"]).max() <= 2.0 ** -6 * np.abs(f0["CL"]).max()
+    f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p, fault)
+    assert [(e[0], e[3], e[4]) for e in f["events"]] == [("K", 77, 5)]
+    assert np.abs(f["CL"] - f0["CL"]).max() <= 2.0 ** -6 * np.abs(f0["CL"]).max()
 
 
 def test_query_fault_is_caught_at_the_projection():
@@ -210,7 +221,7 @@ def test_fused_backward_equals_the_materialised_backward_unrounded(causal, R):
     mb = backward(m, inp["dO"], p)
     f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
     fb = fused_training_backward(f, inp["dO"], p)
-    for k in ("dX", "dWqkv", "dWo", "dQKV", "dAS"):
+    for k in ("dX", "dWqkv", "dWo", "dQKV"):
         assert np.abs(fb[k] - mb[k]).max() <= 1e-12 * np.abs(mb[k]).max(), k
     assert fb["events"] == [] and mb["events"] == []
 
@@ -227,28 +238,77 @@ def test_fused_backward_no_false_positives(seed):
 
 @pytest.mark.parametrize("op,val,action", [("AS", np.inf, "RECOMPUTE"), ("AS", np.nan, "RECOMPUTE"),
                                            ("dAP", 1e10, "RECOMPUTE"), ("dAP", -np.inf, "RECOMPUTE"),
-                                           ("dQ", np.nan, "RECONSTRUCT"), ("dQ", 40.0, "DELTA")])
+                                           ("dQ", np.nan, "RECONSTRUCT"), ("dQ", 40.0, "DELTA"),
+                                           ("dK", np.inf, "RECONSTRUCT"), ("dV", -30.0, "DELTA")])
 def test_fused_backward_faults_are_located_and_fixed(op, val, action):
-    """A score fault in the recomputation, a fault in dP, and a fault in dQ
-    are located at their position; scores and dP are recomputed (the
-    gradients stay within a bf16 step of the fault-free ones at that one
-    element); dQ is fixed from its row checksum within the bf16
-    reconstruction bound."""
+    """A score fault and a dP fault reach both passes of the fused backward
+    and are located in each (by a column in the key pass, by a row in the
+    query pass) and recomputed: the gradients stay within a bf16 step of
+    the fault-free ones at that element. A fault in dQ, dK or dV is fixed
+    from its row checksum within the bf16 reconstruction bound."""
     from oracle.fused import fused_training_backward
     inp = _inputs()
     p = OracleParams(heads=2, dtype="bf16", causal=True, block_rows=64)
     f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
     b0 = fused_training_backward(f0, inp["dO"], p)
-    fault = W.Fault(op, 0, 1, 150, 70 if op != "dQ" else 17, val)
+    fault = W.Fault(op, 0, 1, 150, 70 if op in ("AS", "dAP") else 17, val)
     f = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
     b = fused_training_backward(f, inp["dO"], p, [fault])
-    ev = [e for e in b["events"]]
-    assert [(e[0], e[1], e[2], e[3], e[4], e[6]) for e in ev] == [(op, 0, 1, 150, fault.col, action)]
-    if op == "dQ":
-        row = b0["dQKV"][0, 150, 64:128]
-        assert abs(b["dQKV"][0, 150, 64 + 17] - row[17]) <= 2.0 ** -8 * (np.abs(row).sum() + abs(row[17]))
+    n = 2 if op in ("AS", "dAP") else 1
+    assert [(e[0], e[1], e[2], e[3], e[4], e[6]) for e in b["events"]] == \
+        [(op, 0, 1, 150, fault.col, action)] * n
+    if op in ("dQ", "dK", "dV"):
+        c0 = {"dQ": 0, "dK": 128, "dV": 256}[op] + 64
+        row = b0["dQKV"][0, 150, c0:c0 + 64]
+        assert abs(b["dQKV"][0, 150, c0 + 17] - row[17]) <= 2.0 ** -8 * (np.abs(row).sum() + abs(row[17]))
     else:
         for k in ("dX", "dWqkv", "dWo"):
             ref = b0[k]
             scale = np.maximum(np.abs(ref), np.sqrt(np.mean(ref ** 2)))
             assert np.max(np.abs(b[k] - ref) / scale) <= 1e-2, k
+
+
+@pytest.mark.parametrize("op", ["AS", "dAP"])
+def test_fused_backward_without_root_check_fixes_from_both_sides(op):
+    """Root check off: a score or dP fault is fixed from the checksums in
+    each pass, from the column checksums (Q^c K^T, dCL^c V^T) in the key
+    pass and from the row checksums (Q (K^c)^T, dCL (V^c)^T) in the query
+    pass; the gradients stay within 1e-2 of the fault-free ones."""
+    from oracle.fused import fused_training_backward
+    inp = _inputs()
+    p = OracleParams(heads=2, dtype="bf16", causal=True, block_rows=64, root_check=False)
+    f0 = fused_forward(inp["X"], inp["Wqkv"], inp["Wo"], p)
+    b0 = fused_training_backward(f0, inp["dO"], p)
+    fault = W.Fault(op, 0, 0, 200, 131, 1e12)
+    b = fused_training_backward(f0, inp["dO"], p, [fault])
+    assert [(e[0], e[3], e[4], e[6]) for e in b["events"]] == [(op, 200, 131, "RECONSTRUCT")] * 2
+    for k in ("dX", "dWqkv", "dWo"):
+        ref = b0[k]
+        scale = np.maximum(np.abs(ref), np.sqrt(np.mean(ref ** 2)))
+        assert np.max(np.abs(b[k] - ref) / scale) <= 1e-2, k
+
+
+def test_key_pass_column_check_sees_a_dcl_row_error():
+    """The key pass checks dP = dCL V^T by columns against dCL^c V^T, with
+    dCL^c propagated from dO^c W^O^T rather than taken from the stored dCL:
+    an error in a dCL row that escaped dCL's own check (here simulated by
+    corrupting the operand) makes a 1R pattern in dP that every column
+    vector of its block sees, and the fix from the column checksums
+    restores the products of the clean operand."""
+    from oracle.fused import _checked_scores_cols
+    from oracle.layer import _Run
+    rng = np.random.default_rng(5)
+    S, d, R = 128, 64, 64
+    A, Bm = rng.standard_normal((S, d)), rng.standard_normal((S, d))
+    Ac = np.stack([np.stack([A[q * R:(q + 1) * R].sum(0),
+                             (np.arange(1, R + 1)[:, None] * A[q * R:(q + 1) * R]).sum(0)])
+                   for q in range(S // R)])
+    p = OracleParams(heads=1, dtype="bf16", causal=False, block_rows=R)
+    A2 = A.copy()
+    A2[70, 5] += 1e6
+    run = _Run(p, [])
+    s = _checked_scores_cols(run, p, "dAP", 0, 0, A2, Bm, Ac, 1e10, False)
+    assert sorted((e[3], e[4]) for e in run.events) == [(70, j) for j in range(S)]
+    assert {e[6] for e in run.events} <= {"DELTA", "RECONSTRUCT"}
+    ref = A @ Bm.T
+    assert np.abs(s - ref).max() <= 1e-6 * np.abs(ref).max()
