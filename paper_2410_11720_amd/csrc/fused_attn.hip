@@ -31,6 +31,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "abft_internal.hpp"
 #include "abft_device.hpp"
 #include "direct_lds.hpp"
@@ -615,154 +617,203 @@ struct FusedAttn {
 //    (dV^r)^T += (dCL^r)^T P, dP = dCL V^T column-checked against
 //    (dCL^c) V^T, dS, dK^T += Q^T dS with (dK^r)^T += (Q^r)^T dS; dK and dV
 //    are rounded, row-checked and stored.
-// Each pass holds a 128 x 32 score tile per wave with the 128-long side
-// along a lane's registers and lane groups, so its checks and the packing
-// of P and dS into the next product's operand stay inside the wave; the
-// two passes differ in which entity (query or key) is the 32-wide side.
+// A workgroup of eight waves (two per SIMD) owns 128 columns; each wave
+// works on a 128 x 16 score tile, the 128-long side along a lane's
+// registers and lane groups, so its checks and the packing of P and dS into
+// the next product's operand stay inside the wave; the two passes differ in
+// which entity (query or key) is the 16-wide side. The located-element
+// work of the checks runs out of line (it is rare and would otherwise hold
+// registers across the loops).
 
-// Shared pieces of the two passes. A score tile t[8][2] of a wave holds,
-// for lane (lq = lane % 16, g = lane / 16), the 4 rows 16 j + 4 g + r
-// (r = 0..3; rows: the 128-long side) of column 16 c + lq (c = 0, 1;
-// columns: the wave's 32).
+// Lane 0's part of fixing a flagged score vector gathered in scr[0..n):
+// locate by EEC (Sec. 4.2), recompute the element as the dot product of row
+// `col` of A and row `row` of Bm (length d) or fix it from the checksums,
+// record the event at (row, col) when tr, else (col, row); the located
+// index (or -1) and the new value go to scr[n], scr[n + 1].
+__device__ __noinline__ void score_fix(float* scr, int n, float v1, float v2, float e_rel,
+                                       float tn, float tc, int recompute, abft_report* report,
+                                       int op, int b, int h, int col, int rowbase, bool tr,
+                                       const bf16_t* A, const bf16_t* Bm, int64_t lda,
+                                       int64_t ldb, int d) {
+  const EecResult res = eec_locate<float>(scr, 1, n, v1, v2, e_rel, tn);
+  int idx = -1;
+  float nv = 0.f;
+  if (res.status == EEC_LOCATED) {
+    idx = res.index;
+    const int row = rowbase + idx;
+    const float old = scr[idx];
+    int action = ABFT_ACT_RECOMPUTE;
+    if (recompute) {
+      float acc = 0.f;
+      for (int dd = 0; dd < d; ++dd)
+        acc = fmaf(bf2f(A[int64_t(col) * lda + dd]), bf2f(Bm[int64_t(row) * ldb + dd]), acc);
+      nv = acc;
+    } else {
+      nv = fix_by_checksum<float>(scr, 1, n, idx, v1, res.d1, tc, &action);
+    }
+    scr[idx] = nv;
+    record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn), action, old);
+  }
+  if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, n, v1, e_rel))
+    record_event(report, op, b, h, tr ? rowbase : col, tr ? col : rowbase, ABFT_KIND_NONE,
+                 ABFT_ACT_UNCORRECTABLE, 0.f);
+  scr[n] = __int_as_float(idx);
+  scr[n + 1] = nv;
+}
+
+// The same for a flagged gradient row of length n (entity e): fixed from
+// the checksums, rounded to storage.
+__device__ __noinline__ void grad_fix(float* scr, int n, float v1, float v2, float e_rel, float tn,
+                                      float tc, abft_report* report, int op, int b, int h, int e) {
+  const EecResult res = eec_locate<float>(scr, 1, n, v1, v2, e_rel, tn);
+  int idx = -1;
+  float nv = 0.f;
+  if (res.status == EEC_LOCATED) {
+    idx = res.index;
+    const float old = scr[idx];
+    int action = 0;
+    nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, n, idx, v1, res.d1, tc, &action)));
+    scr[idx] = nv;
+    record_event(report, op, b, h, e, idx, classify(old, tn), action, old);
+  }
+  if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, n, v1, e_rel))
+    record_event(report, op, b, h, e, 0, ABFT_KIND_NONE, ABFT_ACT_UNCORRECTABLE, 0.f);
+  scr[n] = __int_as_float(idx);
+  scr[n + 1] = nv;
+}
+
+// Shared pieces of the two passes. A score tile t[8] of a wave holds, for
+// lane (lq = lane % 16, g = lane / 16), the 4 rows 16 j + 4 g + r (r = 0..3;
+// rows: the 128-long side) of column lq of a 16-column block.
+constexpr int BNT = 512;   // eight waves of 16 columns
+
 template <int D>
 struct BwdTile {
   static constexpr int KH = D / 64, KS = D / 32, DB = D / 16;
-  using DK = Direct<true, FT>;                 // one 64-dim half: [128 rows][64]
+  using DK = Direct<true, FT, BNT>;            // one 64-dim half: [128 rows][64]
   static constexpr int IMG = KH * DK::BYTES;   // a [128 rows][D] K-major image
   static constexpr int SCL = D + 8;            // strip row (elements), padded
   static constexpr int STRIP = 16 * SCL * 2;   // 16 checksum rows of D
-  static constexpr int RSTRIP = FT * 16 * 2;   // [128 rows][16] row-checksum strip
+  static constexpr int RSTRIP = FT * 4 * 2;    // [128 rows][4] row-checksum strip
+  static constexpr int ZERO = 64;              // zeros the strips' other 12 columns read
   static constexpr int SCR = 160;              // floats of rare-path scratch per wave
+  static constexpr int NSV = 1024 / BNT;       // strip values staged per thread
+  __host__ __device__ static constexpr int align1k(int x) { return (x + 1023) & ~1023; }
 
+  // the fragment of two transposing reads through the compiler's
+  // intrinsic (it tracks their completion itself: no wait is forced here)
+  __device__ static __forceinline__ bf16x8 join(const TrPair& t) {
+    typedef short short8_t __attribute__((ext_vector_type(8)));
+    const short8_t v = {t.lo[0], t.lo[1], t.lo[2], t.lo[3], t.hi[0], t.hi[1], t.hi[2], t.hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+  }
   // transposed operand fragment (rows: dims rb + lane % 16; k: image rows
   // kb + 4g + 0..3 and kb + 16 + 4g + 0..3) from a K-major image
-  __device__ static __forceinline__ TrPair t_frag(const char* img, int rb, int kb, int lane) {
+  __device__ static __forceinline__ bf16x8 t_frag(const char* img, int rb, int kb, int lane) {
     const int s = lane & 15, g = lane >> 4;
     const int k1 = kb + 4 * g + (s >> 2), k2 = k1 + 16;
     const int m = rb + 4 * (s & 3);
     const char* half = img + (m >> 6) * DK::BYTES;
     const int mm = m & 63, c = mm >> 3, off = (mm & 7) * 2;
-    return tr_pair_intrinsic(half + k1 * 128 + ((c ^ (k1 & 7)) << 4) + off,
-                             half + k2 * 128 + ((c ^ (k2 & 7)) << 4) + off);
+    return join(tr_pair_intrinsic(half + k1 * 128 + ((c ^ (k1 & 7)) << 4) + off,
+                                  half + k2 * 128 + ((c ^ (k2 & 7)) << 4) + off));
   }
-  // the same from a [128 rows][16] row-checksum strip
-  __device__ static __forceinline__ TrPair rs_frag(const bf16_t* rs, int kb, int lane) {
+  // the same from a [128 rows][4] row-checksum strip as the 16-row operand
+  // (rows 4..15 read zeros)
+  __device__ static __forceinline__ bf16x8 rs_frag(const bf16_t* rs, const bf16_t* zeros, int kb,
+                                                   int lane) {
     const int s = lane & 15, g = lane >> 4;
     const int k1 = kb + 4 * g + (s >> 2), k2 = k1 + 16;
-    const int m = 4 * (s & 3);
-    return tr_pair_intrinsic(rs + k1 * 16 + m, rs + k2 * 16 + m);
+    const bool real = (s & 3) == 0;
+    return join(tr_pair_intrinsic(real ? rs + k1 * 4 : zeros, real ? rs + k2 * 4 : zeros));
   }
-  // the operand pair of the packed 32-row slab t of a packed tile
-  __device__ static __forceinline__ bf16x8 slab(const uint2 (&pk)[8][2], int t, int c) {
-    const uint4 u = {pk[2 * t][c].x, pk[2 * t][c].y, pk[2 * t + 1][c].x, pk[2 * t + 1][c].y};
+  // the operand of the packed 32-row slab t of a packed tile
+  __device__ static __forceinline__ bf16x8 slab(const uint2 (&pk)[8], int t) {
+    const uint4 u = {pk[2 * t].x, pk[2 * t].y, pk[2 * t + 1].x, pk[2 * t + 1].y};
     return __builtin_bit_cast(bf16x8, u);
+  }
+  __device__ static __forceinline__ uint2 pack4(const float (&a)[4]) {
+    return uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
+  }
+  __device__ static __forceinline__ void unpack4(uint2 p, float (&a)[4]) {
+    a[0] = __uint_as_float(p.x << 16);
+    a[1] = __uint_as_float(p.x & 0xffff0000u);
+    a[2] = __uint_as_float(p.y << 16);
+    a[3] = __uint_as_float(p.y & 0xffff0000u);
   }
 
   // Check of a score tile per (column, R-row block) against the strip
-  // result cs (rows 4b..4b+3 of lane group b: hi/lo of c1, c2). A flagged
-  // vector is gathered into the wave's scratch, located by EEC and its
-  // element recomputed as the dot product of row `col` of A and row `row`
-  // of Bm (length D) or fixed from the checksums. Columns are entities
-  // cbase + 0..31, rows rbase + 0..127; events name (row, col) when TR
-  // (the tile is the score matrix itself), (col, row) otherwise (its
-  // transpose).
+  // result cs (rows 4b..4b+3 of lane group b: hi/lo of c1, c2); columns are
+  // entities cbase + 0..15, rows rbase + 0..127 (see score_fix for A, Bm
+  // and tr). A flagged vector is gathered into the wave's scratch and fixed
+  // by lane 0; the fixed element is put back into the tile.
   template <bool TR>
-  __device__ static void check(floatx4 (&t)[8][2], const floatx4 (&cs)[2], const FusedBwdDesc& fd,
-                               int op, int b, int h, int cbase, int rbase, const bf16_t* A,
+  __device__ static void check(floatx4 (&t)[8], const floatx4& cs, const FusedBwdDesc& fd, int op,
+                               int b, int h, int cbase, int rbase, const bf16_t* A,
                                const bf16_t* Bm, int64_t lda, int64_t ldb, float* scr, int lane) {
     const int lq = lane & 15, g = lane >> 4;
     const int R = fd.R, NB = FT / R, lg_jpb = __builtin_ctz(R / 16);
+    float sj[8], aj[8];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      float sj[8], aj[8];
+    for (int j = 0; j < 8; ++j) {
+      sj[j] = (t[j][0] + t[j][1]) + (t[j][2] + t[j][3]);
+      aj[j] = (fabsf(t[j][0]) + fabsf(t[j][1])) + (fabsf(t[j][2]) + fabsf(t[j][3]));
+    }
+    float r1[4], ra[4];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        sj[j] = (t[j][c][0] + t[j][c][1]) + (t[j][c][2] + t[j][c][3]);
-        aj[j] = (fabsf(t[j][c][0]) + fabsf(t[j][c][1])) + (fabsf(t[j][c][2]) + fabsf(t[j][c][3]));
-      }
-      float r1[4], ra[4];
+    for (int i = 0; i < 4; ++i) {
+      r1[i] = sj[2 * i] + sj[2 * i + 1];
+      ra[i] = aj[2 * i] + aj[2 * i + 1];
+    }
+    if (lg_jpb >= 2) {
+      r1[0] += r1[1]; ra[0] += ra[1];
+      r1[1] = r1[2] + r1[3]; ra[1] = ra[2] + ra[3];
+    }
+    if (lg_jpb >= 3) { r1[0] += r1[1]; ra[0] += ra[1]; }
+    float mine1 = 0.f, minea = 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        r1[i] = sj[2 * i] + sj[2 * i + 1];
-        ra[i] = aj[2 * i] + aj[2 * i + 1];
+    for (int i = 0; i < 4; ++i) {
+      if (i < NB) {
+        const float t1 = group4_sum(r1[i]), ta = group4_sum(ra[i]);
+        if (g == i) { mine1 = t1; minea = ta; }
       }
-      if (lg_jpb >= 2) {
-        r1[0] += r1[1]; ra[0] += ra[1];
-        r1[1] = r1[2] + r1[3]; ra[1] = ra[2] + ra[3];
-      }
-      if (lg_jpb >= 3) { r1[0] += r1[1]; ra[0] += ra[1]; }
-      float mine1 = 0.f, minea = 0.f;
+    }
+    const float c1 = cs[0] + cs[1];
+    uint64_t mask = __ballot(g < NB && flagged(c1 - mine1, minea, fd.e_rel));
+    while (mask) {  // rare
+      const int L = __builtin_ctzll(mask);
+      mask &= mask - 1;
+      const int vq = L & 15, vb = L >> 4;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (i < NB) {
-          const float t1 = group4_sum(r1[i]), ta = group4_sum(ra[i]);
-          if (g == i) { mine1 = t1; minea = ta; }
-        }
-      }
-      const float c1 = cs[c][0] + cs[c][1];
-      const bool fl = g < NB && flagged(c1 - mine1, minea, fd.e_rel);
-      uint64_t mask = __ballot(fl);
-      while (mask) {  // rare: locate and correct inside the wave
-        const int L = __builtin_ctzll(mask);
-        mask &= mask - 1;
-        const int vq = L & 15, vb = L >> 4;
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (lq == vq && (j >> lg_jpb) == vb) scr[(16 * j + 4 * g + r) - vb * R] = t[j][r];
+      const float v1 = __shfl(cs[0] + cs[1], L, 64);
+      const float v2 = __shfl(cs[2] + cs[3], L, 64);
+      wave_sync_lds();
+      if (lane == 0)
+        score_fix(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute, fd.report, op, b, h,
+                  cbase + vq, rbase + vb * R, TR, A, Bm, lda, ldb, D);
+      wave_sync_lds();
+      const int idx = __float_as_int(scr[R]);
+      const float nv = scr[R + 1];
+      if (idx >= 0) {
+        const int kl = vb * R + idx;
 #pragma unroll
         for (int j = 0; j < 8; ++j)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (lq == vq && (j >> lg_jpb) == vb) scr[(16 * j + 4 * g + r) - vb * R] = t[j][c][r];
-        const float v1 = __shfl(cs[c][0] + cs[c][1], L, 64);
-        const float v2 = __shfl(cs[c][2] + cs[c][3], L, 64);
-        wave_sync_lds();
-        if (lane == 0) {
-          const int col = cbase + 16 * c + vq;
-          const EecResult res = eec_locate<float>(scr, 1, R, v1, v2, fd.e_rel, fd.tn_s);
-          int idx = -1;
-          float nv = 0.f;
-          if (res.status == EEC_LOCATED) {
-            idx = res.index;
-            const int row = rbase + vb * R + idx;
-            const float old = scr[idx];
-            int action = ABFT_ACT_RECOMPUTE;
-            if (fd.recompute) {
-              float acc = 0.f;
-              for (int dd = 0; dd < D; ++dd)
-                acc = fmaf(bf2f(A[int64_t(col) * lda + dd]), bf2f(Bm[int64_t(row) * ldb + dd]), acc);
-              nv = acc;
-            } else {
-              nv = fix_by_checksum<float>(scr, 1, R, idx, v1, res.d1, fd.tc, &action);
-            }
-            scr[idx] = nv;
-            record_event(fd.report, op, b, h, TR ? row : col, TR ? col : row,
-                         classify(old, fd.tn_s), action, old);
-          }
-          if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, R, v1, fd.e_rel))
-            record_event(fd.report, op, b, h, TR ? rbase + vb * R : col, TR ? col : rbase + vb * R,
-                         ABFT_KIND_NONE, ABFT_ACT_UNCORRECTABLE, 0.f);
-          scr[R] = __int_as_float(idx);
-          scr[R + 1] = nv;
-        }
-        wave_sync_lds();
-        const int idx = __float_as_int(scr[R]);
-        const float nv = scr[R + 1];
-        if (idx >= 0) {
-          const int kl = vb * R + idx;
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (lane == vq + 16 * ((kl & 15) >> 2) && j == (kl >> 4) && r == (kl & 3))
-                t[j][c][r] = nv;
-        }
-        wave_sync_lds();
+            if (lane == vq + 16 * ((kl & 15) >> 2) && j == (kl >> 4) && r == (kl & 3)) t[j][r] = nv;
       }
+      wave_sync_lds();
     }
   }
 
   // injected faults of op (test-only) on a score tile (coordinates as in
   // check: fault rows are queries and columns keys)
   template <bool TR>
-  __device__ static void inject(floatx4 (&t)[8][2], const FusedBwdDesc& fd, int op, int b, int h,
+  __device__ static void inject(floatx4 (&t)[8], const FusedBwdDesc& fd, int op, int b, int h,
                                 int cbase, int rbase, int lane) {
     for (int f = 0; f < fd.n_faults; ++f) {
       const abft_fault ft = fd.faults[f];
@@ -770,37 +821,33 @@ struct BwdTile {
       // under the mask only the block-lower-triangular region is computed
       if (fd.causal && ft.col / fd.R > ft.row / fd.R) continue;
       const int ci = (TR ? ft.col : ft.row) - cbase, ri = (TR ? ft.row : ft.col) - rbase;
-      if (ci < 0 || ci >= 32 || ri < 0 || ri >= FT) continue;
-      const int oc = ci >> 4, olane = (ci & 15) + 16 * ((ri & 15) >> 2);
+      if (ci < 0 || ci >= 16 || ri < 0 || ri >= FT) continue;
+      const int olane = ci + 16 * ((ri & 15) >> 2);
 #pragma unroll
       for (int j = 0; j < 8; ++j)
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (lane == olane && c == oc && j == (ri >> 4) && r == (ri & 3))
-              t[j][c][r] = ft.mode == ABFT_FAULT_FLIP ? flip_f32(t[j][c][r]) : ft.value;
+        for (int r = 0; r < 4; ++r)
+          if (lane == olane && j == (ri >> 4) && r == (ri & 3))
+            t[j][r] = ft.mode == ABFT_FAULT_FLIP ? flip_f32(t[j][r]) : ft.value;
     }
   }
 
-  // A gradient's transposed accumulators acc[DB][2] (lane: dims
-  // 16 db + 4 g + r of entity cbase + 16 c + lq) and its strip results
-  // chk[2] (lane group 0: hi/lo of the sum and of the 1-based weighted sum
-  // over the dims): rounded, faults of op injected, each entity's row
-  // checked (a located element fixed from the checksum, Sec. 4.2) and
-  // stored at out + entity * ld.
-  __device__ static void finish(floatx4 (&acc)[DB][2], const floatx4 (&chk)[2],
-                                const FusedBwdDesc& fd, bool check, int op, int b, int h,
-                                int cbase, bf16_t* out, int64_t ld, float* scr, int lane) {
+  // A gradient's transposed accumulators acc[DB] (lane: dims 16 db + 4 g + r
+  // of entity cbase + lq) and its strip result chk (lane group 0: hi/lo of
+  // the sum and of the 1-based weighted sum over the dims): rounded, faults
+  // of op injected, each entity's row checked (a located element fixed
+  // from the checksum, Sec. 4.2) and stored at out + entity * ld.
+  __device__ static void finish(floatx4 (&acc)[DB], const floatx4& chk, const FusedBwdDesc& fd,
+                                bool check, int op, int b, int h, int cbase, bf16_t* out,
+                                int64_t ld, float* scr, int lane) {
     const int lq = lane & 15, g = lane >> 4;
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int e = cbase + 16 * c + lq;
+    {
+      const int e = cbase + lq;
       float ov[DB][4];
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) ov[db][r] = bf2f(f2bf(acc[db][c][r]));
+        for (int r = 0; r < 4; ++r) ov[db][r] = bf2f(f2bf(acc[db][r]));
       if (fd.n_faults > 0) {
         for (int f = 0; f < fd.n_faults; ++f) {
           const abft_fault ft = fd.faults[f];
@@ -815,8 +862,8 @@ struct BwdTile {
         }
       }
       if (check) {
-        const float c1 = __shfl(chk[c][0] + chk[c][1], lq, 64);
-        const float c2 = __shfl(chk[c][2] + chk[c][3], lq, 64);
+        const float c1 = __shfl(chk[0] + chk[1], lq, 64);
+        const float c2 = __shfl(chk[2] + chk[3], lq, 64);
         float r1 = 0.f, ra = 0.f;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
@@ -839,24 +886,8 @@ struct BwdTile {
           }
           const float v1 = __shfl(c1, L, 64), v2 = __shfl(c2, L, 64);
           wave_sync_lds();
-          if (lane == 0) {
-            const int ee = cbase + 16 * c + L;
-            const EecResult res = eec_locate<float>(scr, 1, D, v1, v2, fd.e_rel, fd.tn);
-            int idx = -1;
-            float nv = 0.f;
-            if (res.status == EEC_LOCATED) {
-              idx = res.index;
-              const float old = scr[idx];
-              int action = 0;
-              nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, D, idx, v1, res.d1, fd.tc, &action)));
-              scr[idx] = nv;
-              record_event(fd.report, op, b, h, ee, idx, classify(old, fd.tn), action, old);
-            }
-            if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, D, v1, fd.e_rel))
-              record_event(fd.report, op, b, h, ee, 0, ABFT_KIND_NONE, ABFT_ACT_UNCORRECTABLE, 0.f);
-            scr[D] = __int_as_float(idx);
-            scr[D + 1] = nv;
-          }
+          if (lane == 0)
+            grad_fix(scr, D, v1, v2, fd.e_rel, fd.tn, fd.tc, fd.report, op, b, h, cbase + L);
           wave_sync_lds();
           const int idx = __float_as_int(scr[D]);
           const float nv = scr[D + 1];
@@ -880,22 +911,22 @@ struct BwdTile {
 
   // checksum strip of 16 rows (4 per R-row block: hi/lo of the sum and of
   // the weighted sum) from fp32 column checksums; thread tid stages up to
-  // four values in v[] (issue) and writes them (commit)
+  // NSV values in v[] (issue) and writes them (commit)
   __device__ static __forceinline__ void strip_issue(const float* cc, int64_t ldc, int64_t blk0,
-                                                     int NB, int tid, float (&v)[4]) {
+                                                     int NB, int tid, float (&v)[NSV]) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int e = tid + p * FNT;
+    for (int p = 0; p < NSV; ++p) {
+      const int e = tid + p * BNT;
       const int ee = e < NB * 2 * D ? e : 0;
       const int blk = ee / (2 * D), c = (ee / D) & 1, dd = ee % D;
       v[p] = cc[((blk0 + blk) * 2 + c) * ldc + dd];
     }
   }
   __device__ static __forceinline__ void strip_commit(bf16_t* st, int NB, int tid,
-                                                      const float (&v)[4]) {
+                                                      const float (&v)[NSV]) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int e = tid + p * FNT;
+    for (int p = 0; p < NSV; ++p) {
+      const int e = tid + p * BNT;
       if (e < NB * 2 * D) {
         const int blk = e / (2 * D), c = (e / D) & 1, dd = e % D;
         const int r = (4 * blk + 2 * c) * SCL + dd;
@@ -904,11 +935,11 @@ struct BwdTile {
       }
     }
   }
-  // row-checksum strip [128 rows][16]: columns 0..3 the hi/lo of the sum
-  // and of the weighted sum of row tid / 2 (columns 4..15 stay zero)
+  // row-checksum strip [128 rows][4]: the hi/lo of the sum and of the
+  // weighted sum of row tid / 2 (threads 0..255)
   __device__ static __forceinline__ void rstrip_commit(bf16_t* rs, int tid, float v) {
-    rs[(tid >> 1) * 16 + 2 * (tid & 1)] = f2bf(v);
-    rs[(tid >> 1) * 16 + 2 * (tid & 1) + 1] = f2bf(v - bf2f(f2bf(v)));
+    rs[(tid >> 1) * 4 + 2 * (tid & 1)] = f2bf(v);
+    rs[(tid >> 1) * 4 + 2 * (tid & 1) + 1] = f2bf(v - bf2f(f2bf(v)));
   }
 };
 
@@ -921,10 +952,11 @@ struct FusedBwdQ : BwdTile<D> {
   using typename T::DK;
   static constexpr int KS = T::KS, DB = T::DB, KH = T::KH, IMG = T::IMG, SCL = T::SCL;
   static constexpr int OFF_V = IMG, OFF_KC = 2 * IMG, OFF_VC = OFF_KC + T::STRIP;
-  static constexpr int OFF_KR = OFF_VC + T::STRIP;
-  static constexpr int OFF_Q = OFF_KR + T::RSTRIP, OFF_G = OFF_Q + IMG;
+  static constexpr int OFF_KR = OFF_VC + T::STRIP, OFF_ZERO = OFF_KR + T::RSTRIP;
+  static constexpr int OFF_Q = T::align1k(OFF_ZERO + T::ZERO), OFF_G = OFF_Q + IMG;
   static constexpr int OFF_SCR = OFF_G + IMG;
-  static constexpr int LDS_BYTES = OFF_SCR + 4 * T::SCR * 4;
+  static constexpr int LDS_BYTES = OFF_SCR + (BNT / 64) * T::SCR * 4;
+  static_assert(LDS_BYTES <= 160 * 1024, "one workgroup fits the LDS");
 
   __device__ static void run(const FusedBwdDesc& fd, char* smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -934,7 +966,7 @@ struct FusedBwdQ : BwdTile<D> {
     const int z = blockIdx.x % nbh;
     const int qt = fd.causal ? nqt - 1 - int(blockIdx.x) / nbh : int(blockIdx.x) / nbh;
     const int b = z / fd.nh, h = z % fd.nh;
-    const int q0 = qt * FT, qw = q0 + wave * 32;
+    const int q0 = qt * FT, qw = q0 + wave * 16, q = qw + lq;
     const int64_t ld = 3 * int64_t(H);
     const bf16_t* base = static_cast<const bf16_t*>(fd.qkv) + int64_t(b) * S * ld;
     const bf16_t* Qp = base + h * D;
@@ -947,11 +979,9 @@ struct FusedBwdQ : BwdTile<D> {
     constexpr bool chk = CHK;
 
     // the statistics and the softmax backward's row term D = dCL . CL of
-    // the lane's queries (D also kept for the key pass)
-    float mq[2], il[2], dq[2];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const int q = qw + 16 * qb + lq;
+    // the lane's query (D also kept for the key pass)
+    float mq, il, dq;
+    {
       float acc = 0.f;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
@@ -960,11 +990,11 @@ struct FusedBwdQ : BwdTile<D> {
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc = fmaf(float(gv[e]), float(cv[e]), acc);
       }
-      dq[qb] = group4_sum(acc);
+      dq = group4_sum(acc);
       const float* st = fd.stats + ((int64_t(b) * fd.nh + h) * S + q) * 2;
-      mq[qb] = st[0];
-      il[qb] = 1.f / st[1];
-      if (g == 0) fd.drow[(int64_t(b) * fd.nh + h) * S + q] = dq[qb];
+      mq = st[0];
+      il = 1.f / st[1];
+      if (g == 0) fd.drow[(int64_t(b) * fd.nh + h) * S + q] = dq;
     }
     // Q and dCL images of the workgroup's queries (complete with tile 0)
 #pragma unroll
@@ -972,8 +1002,11 @@ struct FusedBwdQ : BwdTile<D> {
       DK::issue(Qp, ld, q0, S, hf * 64, smem + OFF_Q + hf * DK::BYTES, wave, lane);
       DK::issue(dCLp, H, q0, S, hf * 64, smem + OFF_G + hf * DK::BYTES, wave, lane);
     }
+    bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
+    const bf16_t* zeros = reinterpret_cast<const bf16_t*>(smem + OFF_ZERO);
+    if (chk && tid < T::ZERO / 4) reinterpret_cast<uint32_t*>(smem + OFF_ZERO)[tid] = 0u;
 
-    float kcv[4] = {0.f, 0.f, 0.f, 0.f}, vcv[4] = {0.f, 0.f, 0.f, 0.f}, krv = 0.f;
+    float kcv[T::NSV], vcv[T::NSV], krv = 0.f;
     auto issue = [&](int kt) {
       const int key0 = kt * FT;
 #pragma unroll
@@ -985,28 +1018,26 @@ struct FusedBwdQ : BwdTile<D> {
         const int64_t blk0 = int64_t(b) * nqR + key0 / R;
         T::strip_issue(fd.qkvc + H + h * D, ld, blk0, NB, tid, kcv);
         T::strip_issue(fd.qkvc + 2 * H + h * D, ld, blk0, NB, tid, vcv);
-        krv = fd.kr[((int64_t(b) * S + key0 + (tid >> 1)) * fd.nh + h) * 2 + (tid & 1)];
+        const int tr = tid & (2 * FT - 1);   // threads 0..255 hold the strip's 256 values
+        krv = fd.kr[((int64_t(b) * S + key0 + (tr >> 1)) * fd.nh + h) * 2 + (tr & 1)];
       }
     };
-    bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
     auto commit = [&]() {
       if (chk) {
         T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_KC), NB, tid, kcv);
         T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_VC), NB, tid, vcv);
-        T::rstrip_commit(krs, tid, krv);
+        if (tid < 2 * FT) T::rstrip_commit(krs, tid, krv);
       }
     };
-    if (chk)
-      for (int e = tid; e < FT * 12; e += FNT) krs[(e / 12) * 16 + 4 + e % 12] = 0;
 
-    floatx4 dqa[DB][2], kra[2];
+    floatx4 dqa[DB], kra = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-      for (int db = 0; db < DB; ++db) dqa[db][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-      kra[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int db = 0; db < DB; ++db) dqa[db] = floatx4{0.f, 0.f, 0.f, 0.f};
     float* scr = reinterpret_cast<float*>(smem + OFF_SCR) + wave * T::SCR;
+    // B operand fragment of the wave's queries (rows of the Q or dCL image)
+    auto bfrag = [&](int off, int kk) {
+      return DK::frag(smem + off + (kk >> 1) * DK::BYTES, wave * 16, (kk & 1) * 32, lane);
+    };
 
     for (int kt = 0; kt < nkt; ++kt) {
       issue(kt);
@@ -1015,122 +1046,87 @@ struct FusedBwdQ : BwdTile<D> {
       __syncthreads();  // tile kt in LDS
       const int key0 = kt * FT;
       const bool diag = fd.causal && kt == qt;
-      // B operand fragments of the wave's queries (rows of the Q or dCL image)
-      auto bfrag = [&](int off, int qb, int kk) {
-        return DK::frag(smem + off + (kk >> 1) * DK::BYTES, wave * 32 + 16 * qb, (kk & 1) * 32, lane);
-      };
-      // P^T, then dS^T, packed to bf16: pk[j][qb] holds keys 16 j + 4 g + 0..3
-      // of query 16 qb + lane % 16
-      uint2 pk[8][2];
+      // P^T, then dS^T, packed to bf16: pk[j] holds keys 16 j + 4 g + 0..3
+      uint2 pk[8];
       {
         // S^T = K Q^T with its strip rows, checked; P from the statistics
-        floatx4 s[8][2], ks[2];
+        floatx4 s[8], ks = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) s[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-          ks[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int j = 0; j < 8; ++j) s[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
-          const bf16x8 qf0 = bfrag(OFF_Q, 0, kk), qf1 = bfrag(OFF_Q, 1, kk);
+          const bf16x8 qf = bfrag(OFF_Q, kk);
           const char* sk = smem + (kk >> 1) * DK::BYTES;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const bf16x8 kf = DK::frag(sk, 16 * j, (kk & 1) * 32, lane);
-            s[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf0, s[j][0], 0, 0, 0);
-            s[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf1, s[j][1], 0, 0, 0);
-          }
+          for (int j = 0; j < 8; ++j)
+            s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(DK::frag(sk, 16 * j, (kk & 1) * 32, lane),
+                                                           qf, s[j], 0, 0, 0);
           if (chk) {
             const bf16_t* kcs = reinterpret_cast<const bf16_t*>(smem + OFF_KC);
-            const bf16x8 kc = *reinterpret_cast<const bf16x8*>(kcs + lq * SCL + 32 * kk + 8 * g);
-            ks[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc, qf0, ks[0], 0, 0, 0);
-            ks[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc, qf1, ks[1], 0, 0, 0);
+            ks = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                *reinterpret_cast<const bf16x8*>(kcs + lq * SCL + 32 * kk + 8 * g), qf, ks, 0, 0, 0);
           }
         }
         if (fd.n_faults > 0) T::template inject<false>(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
-        if (chk) T::template check<false>(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
+        if (chk)
+          T::template check<false>(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const int q = qw + 16 * qb + lq;
+        for (int j = 0; j < 8; ++j) {
+          float a[4];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            float a[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
-              a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][qb][r] * sl2 - mq[qb]) * il[qb]))
-                          : 0.f;
-            }
-            pk[j][qb] = uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
+          for (int r = 0; r < 4; ++r) {
+            const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
+            a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][r] * sl2 - mq) * il)) : 0.f;
           }
+          pk[j] = T::pack4(a);
         }
       }
       {
         // dP^T = V dCL^T with its strip rows, checked; dS from P and dP
-        floatx4 dp[8][2], vs[2];
+        floatx4 dp[8], vs = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) dp[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-          vs[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int j = 0; j < 8; ++j) dp[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
-          const bf16x8 gf0 = bfrag(OFF_G, 0, kk), gf1 = bfrag(OFF_G, 1, kk);
+          const bf16x8 gf = bfrag(OFF_G, kk);
           const char* sv = smem + OFF_V + (kk >> 1) * DK::BYTES;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const bf16x8 vf = DK::frag(sv, 16 * j, (kk & 1) * 32, lane);
-            dp[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf0, dp[j][0], 0, 0, 0);
-            dp[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf1, dp[j][1], 0, 0, 0);
-          }
+          for (int j = 0; j < 8; ++j)
+            dp[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(DK::frag(sv, 16 * j, (kk & 1) * 32, lane),
+                                                            gf, dp[j], 0, 0, 0);
           if (chk) {
             const bf16_t* vcs = reinterpret_cast<const bf16_t*>(smem + OFF_VC);
-            const bf16x8 vc = *reinterpret_cast<const bf16x8*>(vcs + lq * SCL + 32 * kk + 8 * g);
-            vs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vc, gf0, vs[0], 0, 0, 0);
-            vs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vc, gf1, vs[1], 0, 0, 0);
+            vs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                *reinterpret_cast<const bf16x8*>(vcs + lq * SCL + 32 * kk + 8 * g), gf, vs, 0, 0, 0);
           }
         }
         if (fd.n_faults > 0) T::template inject<false>(dp, fd, ABFT_OP_DAP, b, h, qw, key0, lane);
-        if (chk) T::template check<false>(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr, lane);
+        if (chk)
+          T::template check<false>(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr,
+                                   lane);
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const int q = qw + 16 * qb + lq;
+        for (int j = 0; j < 8; ++j) {
+          float a[4], ds[4];
+          T::unpack4(pk[j], a);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float a[4] = {__uint_as_float(pk[j][qb].x << 16),
-                                __uint_as_float(pk[j][qb].x & 0xffff0000u),
-                                __uint_as_float(pk[j][qb].y << 16),
-                                __uint_as_float(pk[j][qb].y & 0xffff0000u)};
-            float ds[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
-              ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][qb][r] - dq[qb]))) : 0.f;
-            }
-            pk[j][qb] = uint2{pack2(ds[0], ds[1]), pack2(ds[2], ds[3])};
+          for (int r = 0; r < 4; ++r) {
+            const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
+            ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][r] - dq))) : 0.f;
           }
+          pk[j] = T::pack4(ds);
         }
       }
-
       // dQ^T += K^T dS^T and (dQ^r)^T += (K^r)^T dS^T
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const bf16x8 pf0 = T::slab(pk, t, 0), pf1 = T::slab(pk, t, 1);
+        const bf16x8 pf = T::slab(pk, t);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          TrPair kp = T::t_frag(smem, 16 * db, 32 * t, lane);
-          const bf16x8 kf = tr_join(kp);
-          dqa[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, pf0, dqa[db][0], 0, 0, 0);
-          dqa[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, pf1, dqa[db][1], 0, 0, 0);
-        }
-        if (chk) {
-          TrPair rp = T::rs_frag(krs, 32 * t, lane);
-          const bf16x8 rf = tr_join(rp);
-          kra[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf0, kra[0], 0, 0, 0);
-          kra[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf1, kra[1], 0, 0, 0);
-        }
+        for (int db = 0; db < DB; ++db)
+          dqa[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::t_frag(smem, 16 * db, 32 * t, lane),
+                                                            pf, dqa[db], 0, 0, 0);
+        if (chk)
+          kra = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::rs_frag(krs, zeros, 32 * t, lane), pf,
+                                                        kra, 0, 0, 0);
       }
       __syncthreads();  // the one stage is reloaded next
     }
@@ -1143,7 +1139,12 @@ struct FusedBwdQ : BwdTile<D> {
 // The key pass. LDS: the workgroup's K and V images (loaded once); per
 // query tile the Q and dCL images, the Q^c and dCL^c strips, the Q^r and
 // dCL^r row-checksum strips and the queries' max, 1 / sum and D; scratch.
-template <int D, bool CHK>
+// PART 0 forms dV and dK together; where both sets of accumulators do not
+// fit the registers of two waves per SIMD (head dim 128) the pass runs as
+// PART 1 (S, P, dV) then PART 2 (S, P, dP, dS, dK), each recomputing and
+// checking the scores; injected score faults are applied in the part that
+// also forms dP, so that a fault is met once per pass whatever the split.
+template <int D, bool CHK, int PART>
 struct FusedBwdKV : BwdTile<D> {
   using T = BwdTile<D>;
   using typename T::DK;
@@ -1151,9 +1152,10 @@ struct FusedBwdKV : BwdTile<D> {
   static constexpr int OFF_V = IMG, OFF_Q = 2 * IMG, OFF_G = 3 * IMG;
   static constexpr int OFF_QC = 4 * IMG, OFF_GC = OFF_QC + T::STRIP;
   static constexpr int OFF_QR = OFF_GC + T::STRIP, OFF_GR = OFF_QR + T::RSTRIP;
-  static constexpr int OFF_ROW = OFF_GR + T::RSTRIP;           // [3][128] floats
+  static constexpr int OFF_ZERO = OFF_GR + T::RSTRIP;
+  static constexpr int OFF_ROW = OFF_ZERO + T::ZERO;           // [3][128] floats
   static constexpr int OFF_SCR = OFF_ROW + 3 * FT * 4;
-  static constexpr int LDS_BYTES = OFF_SCR + 4 * T::SCR * 4;
+  static constexpr int LDS_BYTES = OFF_SCR + (BNT / 64) * T::SCR * 4;
   static_assert(LDS_BYTES <= 160 * 1024, "one workgroup fits the LDS");
 
   __device__ static void run(const FusedBwdDesc& fd, char* smem) {
@@ -1164,7 +1166,7 @@ struct FusedBwdKV : BwdTile<D> {
     const int z = blockIdx.x % nbh;
     const int kt = int(blockIdx.x) / nbh;   // causal: the first key tiles see the most queries
     const int b = z / fd.nh, h = z % fd.nh;
-    const int key0 = kt * FT, kw = key0 + wave * 32;
+    const int key0 = kt * FT, kw = key0 + wave * 16, key = kw + lq;
     const int64_t ld = 3 * int64_t(H);
     const bf16_t* base = static_cast<const bf16_t*>(fd.qkv) + int64_t(b) * S * ld;
     const bf16_t* Qp = base + h * D;
@@ -1175,6 +1177,7 @@ struct FusedBwdKV : BwdTile<D> {
     const float sl2 = fd.scale * 1.4426950408889634f;
     constexpr bool chk = CHK;
     const int64_t bh = int64_t(b) * fd.nh + h;
+    constexpr bool DO_V = PART != 2, DO_K = PART != 1;
 
     // K and V images of the workgroup's keys (complete with the first tile)
 #pragma unroll
@@ -1184,14 +1187,11 @@ struct FusedBwdKV : BwdTile<D> {
     }
     bf16_t* qrs = reinterpret_cast<bf16_t*>(smem + OFF_QR);
     bf16_t* grs = reinterpret_cast<bf16_t*>(smem + OFF_GR);
-    if (chk)
-      for (int e = tid; e < FT * 12; e += FNT) {
-        qrs[(e / 12) * 16 + 4 + e % 12] = 0;
-        grs[(e / 12) * 16 + 4 + e % 12] = 0;
-      }
+    const bf16_t* zeros = reinterpret_cast<const bf16_t*>(smem + OFF_ZERO);
+    if (chk && tid < T::ZERO / 4) reinterpret_cast<uint32_t*>(smem + OFF_ZERO)[tid] = 0u;
     float* rowf = reinterpret_cast<float*>(smem + OFF_ROW);
 
-    float qcv[4] = {0.f, 0.f, 0.f, 0.f}, gcv[4] = {0.f, 0.f, 0.f, 0.f};
+    float qcv[T::NSV], gcv[T::NSV];
     float qrv = 0.f, grv = 0.f, rv0 = 0.f, rv1 = 0.f;
     auto issue = [&](int qt) {
       const int q0 = qt * FT;
@@ -1205,14 +1205,15 @@ struct FusedBwdKV : BwdTile<D> {
       if (tid < FT) {
         rv0 = fd.stats[(bh * S + qi) * 2];
         rv1 = fd.stats[(bh * S + qi) * 2 + 1];
-      } else {
+      } else if (tid < 2 * FT) {
         rv0 = fd.drow[bh * S + qi];
       }
       if (chk) {
         const int64_t blk0 = int64_t(b) * nqR + q0 / R;
         T::strip_issue(fd.qkvc + h * D, ld, blk0, NB, tid, qcv);
         T::strip_issue(fd.dclc + h * D, H, blk0, NB, tid, gcv);
-        const int64_t ri = ((int64_t(b) * S + q0 + (tid >> 1)) * fd.nh + h) * 2 + (tid & 1);
+        const int tr = tid & (2 * FT - 1);   // threads 0..255 hold the strips' 256 values
+        const int64_t ri = ((int64_t(b) * S + q0 + (tr >> 1)) * fd.nh + h) * 2 + (tr & 1);
         qrv = fd.qr[ri];
         grv = fd.dclr[ri];
       }
@@ -1221,29 +1222,34 @@ struct FusedBwdKV : BwdTile<D> {
       if (tid < FT) {
         rowf[tid] = rv0;
         rowf[FT + tid] = 1.f / rv1;
-      } else {
+      } else if (tid < 2 * FT) {
         rowf[2 * FT + tid - FT] = rv0;
       }
       if (chk) {
         T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_QC), NB, tid, qcv);
         T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_GC), NB, tid, gcv);
-        T::rstrip_commit(qrs, tid, qrv);
-        T::rstrip_commit(grs, tid, grv);
+        if (tid < 2 * FT) {
+          T::rstrip_commit(qrs, tid, qrv);
+          T::rstrip_commit(grs, tid, grv);
+        }
       }
     };
 
-    floatx4 dva[DB][2], dka[DB][2], vra[2], kra[2];
+    floatx4 dva[DB], dka[DB], vra = {0.f, 0.f, 0.f, 0.f}, kra = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        dva[db][c] = floatx4{0.f, 0.f, 0.f, 0.f};
-        dka[db][c] = floatx4{0.f, 0.f, 0.f, 0.f};
-      }
-      vra[c] = floatx4{0.f, 0.f, 0.f, 0.f};
-      kra[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int db = 0; db < DB; ++db) {
+      dva[db] = floatx4{0.f, 0.f, 0.f, 0.f};
+      dka[db] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
     float* scr = reinterpret_cast<float*>(smem + OFF_SCR) + wave * T::SCR;
+    // A operand fragments of the tile's queries (rows 16 j..) and the B
+    // operand fragment of the wave's keys (rows of the K or V image)
+    auto afrag = [&](int off, int j, int kk) {
+      return DK::frag(smem + off + (kk >> 1) * DK::BYTES, 16 * j, (kk & 1) * 32, lane);
+    };
+    auto kfrag = [&](int off, int kk) {
+      return DK::frag(smem + off + (kk >> 1) * DK::BYTES, wave * 16, (kk & 1) * 32, lane);
+    };
 
     for (int qt = qt0; qt < nqt; ++qt) {
       issue(qt);
@@ -1252,169 +1258,123 @@ struct FusedBwdKV : BwdTile<D> {
       __syncthreads();  // query tile qt in LDS
       const int q0 = qt * FT;
       const bool diag = fd.causal && qt == kt;
-      // A operand fragments of the tile's queries (rows 16 j..) and B
-      // operand fragments of the wave's keys (rows of the K or V image)
-      auto afrag = [&](int off, int j, int kk) {
-        return DK::frag(smem + off + (kk >> 1) * DK::BYTES, 16 * j, (kk & 1) * 32, lane);
-      };
-      auto kfrag = [&](int off, int c, int kk) {
-        return DK::frag(smem + off + (kk >> 1) * DK::BYTES, wave * 32 + 16 * c, (kk & 1) * 32, lane);
-      };
-      // P, then dS, packed to bf16: pk[j][c] holds queries 16 j + 4 g + 0..3
-      // of key kw + 16 c + lane % 16
-      uint2 pk[8][2];
+      // P, then dS, packed to bf16: pk[j] holds queries 16 j + 4 g + 0..3
+      uint2 pk[8];
       {
         // S = Q K^T with its strip rows (Q^c) K^T, column-checked; P
-        floatx4 s[8][2], cs[2];
+        floatx4 s[8], cs = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) s[j][c] = floatx4{0.f, 0.f, 0.f, 0.f};
-          cs[c] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int j = 0; j < 8; ++j) s[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
-          const bf16x8 kf0 = kfrag(0, 0, kk), kf1 = kfrag(0, 1, kk);
+          const bf16x8 kf = kfrag(0, kk);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const bf16x8 qf = afrag(OFF_Q, j, kk);
-            s[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, kf0, s[j][0], 0, 0, 0);
-            s[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, kf1, s[j][1], 0, 0, 0);
-          }
+          for (int j = 0; j < 8; ++j)
+            s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag(OFF_Q, j, kk), kf, s[j], 0, 0, 0);
           if (chk) {
             const bf16_t* qcs = reinterpret_cast<const bf16_t*>(smem + OFF_QC);
-            const bf16x8 qc = *reinterpret_cast<const bf16x8*>(qcs + lq * SCL + 32 * kk + 8 * g);
-            cs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qc, kf0, cs[0], 0, 0, 0);
-            cs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qc, kf1, cs[1], 0, 0, 0);
+            cs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                *reinterpret_cast<const bf16x8*>(qcs + lq * SCL + 32 * kk + 8 * g), kf, cs, 0, 0, 0);
           }
         }
-        if (fd.n_faults > 0) T::template inject<true>(s, fd, ABFT_OP_AS, b, h, kw, q0, lane);
-        if (chk) T::template check<true>(s, cs, fd, ABFT_OP_AS, b, h, kw, q0, Kp, Qp, ld, ld, scr, lane);
+        if (DO_K && fd.n_faults > 0) T::template inject<true>(s, fd, ABFT_OP_AS, b, h, kw, q0, lane);
+        if (chk)
+          T::template check<true>(s, cs, fd, ABFT_OP_AS, b, h, kw, q0, Kp, Qp, ld, ld, scr, lane);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const float4 m4 = *reinterpret_cast<const float4*>(rowf + 16 * j + 4 * g);
           const float4 i4 = *reinterpret_cast<const float4*>(rowf + FT + 16 * j + 4 * g);
           const float mv[4] = {m4.x, m4.y, m4.z, m4.w}, iv[4] = {i4.x, i4.y, i4.z, i4.w};
+          float a[4];
 #pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const int key = kw + 16 * c + lq;
-            float a[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
-              a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][c][r] * sl2 - mv[r]) * iv[r]))
-                          : 0.f;
-            }
-            pk[j][c] = uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
+          for (int r = 0; r < 4; ++r) {
+            const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
+            a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][r] * sl2 - mv[r]) * iv[r])) : 0.f;
           }
+          pk[j] = T::pack4(a);
         }
       }
       // dV^T += dCL^T P and (dV^r)^T += (dCL^r)^T P
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const bf16x8 pf0 = T::slab(pk, t, 0), pf1 = T::slab(pk, t, 1);
+      for (int t = 0; t < 4 && DO_V; ++t) {
+        const bf16x8 pf = T::slab(pk, t);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          TrPair gp = T::t_frag(smem + OFF_G, 16 * db, 32 * t, lane);
-          const bf16x8 gf = tr_join(gp);
-          dva[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gf, pf0, dva[db][0], 0, 0, 0);
-          dva[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gf, pf1, dva[db][1], 0, 0, 0);
-        }
-        if (chk) {
-          TrPair rp = T::rs_frag(grs, 32 * t, lane);
-          const bf16x8 rf = tr_join(rp);
-          vra[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf0, vra[0], 0, 0, 0);
-          vra[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf1, vra[1], 0, 0, 0);
-        }
+        for (int db = 0; db < DB; ++db)
+          dva[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              T::t_frag(smem + OFF_G, 16 * db, 32 * t, lane), pf, dva[db], 0, 0, 0);
+        if (chk)
+          vra = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::rs_frag(grs, zeros, 32 * t, lane), pf,
+                                                        vra, 0, 0, 0);
       }
-      {
+      if (DO_K) {
         // dP = dCL V^T with its strip rows (dCL^c) V^T, column-checked; dS
-        floatx4 dp[8][2], cs[2];
+        floatx4 dp[8], cs = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) dp[j][c] = floatx4{0.f, 0.f, 0.f, 0.f};
-          cs[c] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int j = 0; j < 8; ++j) dp[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
-          const bf16x8 vf0 = kfrag(OFF_V, 0, kk), vf1 = kfrag(OFF_V, 1, kk);
+          const bf16x8 vf = kfrag(OFF_V, kk);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const bf16x8 gf = afrag(OFF_G, j, kk);
-            dp[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gf, vf0, dp[j][0], 0, 0, 0);
-            dp[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gf, vf1, dp[j][1], 0, 0, 0);
-          }
+          for (int j = 0; j < 8; ++j)
+            dp[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag(OFF_G, j, kk), vf, dp[j], 0, 0, 0);
           if (chk) {
             const bf16_t* gcs = reinterpret_cast<const bf16_t*>(smem + OFF_GC);
-            const bf16x8 gc = *reinterpret_cast<const bf16x8*>(gcs + lq * SCL + 32 * kk + 8 * g);
-            cs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gc, vf0, cs[0], 0, 0, 0);
-            cs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gc, vf1, cs[1], 0, 0, 0);
+            cs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                *reinterpret_cast<const bf16x8*>(gcs + lq * SCL + 32 * kk + 8 * g), vf, cs, 0, 0, 0);
           }
         }
         if (fd.n_faults > 0) T::template inject<true>(dp, fd, ABFT_OP_DAP, b, h, kw, q0, lane);
-        if (chk) T::template check<true>(dp, cs, fd, ABFT_OP_DAP, b, h, kw, q0, Vp, dCLp, ld, H, scr, lane);
+        if (chk)
+          T::template check<true>(dp, cs, fd, ABFT_OP_DAP, b, h, kw, q0, Vp, dCLp, ld, H, scr,
+                                  lane);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const float4 d4 = *reinterpret_cast<const float4*>(rowf + 2 * FT + 16 * j + 4 * g);
           const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+          float a[4], ds[4];
+          T::unpack4(pk[j], a);
 #pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const int key = kw + 16 * c + lq;
-            const float a[4] = {__uint_as_float(pk[j][c].x << 16),
-                                __uint_as_float(pk[j][c].x & 0xffff0000u),
-                                __uint_as_float(pk[j][c].y << 16),
-                                __uint_as_float(pk[j][c].y & 0xffff0000u)};
-            float ds[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
-              ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][c][r] - dv[r]))) : 0.f;
-            }
-            pk[j][c] = uint2{pack2(ds[0], ds[1]), pack2(ds[2], ds[3])};
+          for (int r = 0; r < 4; ++r) {
+            const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
+            ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][r] - dv[r]))) : 0.f;
           }
+          pk[j] = T::pack4(ds);
         }
       }
       // dK^T += Q^T dS and (dK^r)^T += (Q^r)^T dS
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const bf16x8 pf0 = T::slab(pk, t, 0), pf1 = T::slab(pk, t, 1);
+      for (int t = 0; t < 4 && DO_K; ++t) {
+        const bf16x8 pf = T::slab(pk, t);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          TrPair qp = T::t_frag(smem + OFF_Q, 16 * db, 32 * t, lane);
-          const bf16x8 qf = tr_join(qp);
-          dka[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, pf0, dka[db][0], 0, 0, 0);
-          dka[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, pf1, dka[db][1], 0, 0, 0);
-        }
-        if (chk) {
-          TrPair rp = T::rs_frag(qrs, 32 * t, lane);
-          const bf16x8 rf = tr_join(rp);
-          kra[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf0, kra[0], 0, 0, 0);
-          kra[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf1, kra[1], 0, 0, 0);
-        }
+        for (int db = 0; db < DB; ++db)
+          dka[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              T::t_frag(smem + OFF_Q, 16 * db, 32 * t, lane), pf, dka[db], 0, 0, 0);
+        if (chk)
+          kra = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::rs_frag(qrs, zeros, 32 * t, lane), pf,
+                                                        kra, 0, 0, 0);
       }
       __syncthreads();  // the query tile's buffers are reloaded next
     }
 
     bf16_t* outp = static_cast<bf16_t*>(fd.dqkv) + int64_t(b) * S * fd.ld + h * D;
-    T::finish(dka, kra, fd, chk, ABFT_OP_DK, b, h, kw, outp + H, fd.ld, scr, lane);
-    T::finish(dva, vra, fd, chk, ABFT_OP_DV, b, h, kw, outp + 2 * H, fd.ld, scr, lane);
+    if (DO_K) T::finish(dka, kra, fd, chk, ABFT_OP_DK, b, h, kw, outp + H, fd.ld, scr, lane);
+    if (DO_V) T::finish(dva, vra, fd, chk, ABFT_OP_DV, b, h, kw, outp + 2 * H, fd.ld, scr, lane);
   }
 };
 
-// one wave per SIMD: with two the registers of every variant spill
+// eight waves, two per SIMD
 template <int D, bool CHK>
-__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(1)))
+__global__ __launch_bounds__(BNT) __attribute__((amdgpu_waves_per_eu(2)))
 void fused_bwd_q_kernel(FusedBwdDesc fd) {
   extern __shared__ __align__(16) char smem[];
   FusedBwdQ<D, CHK>::run(fd, smem);
 }
 
-template <int D, bool CHK>
-__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(1)))
+template <int D, bool CHK, int PART>
+__global__ __launch_bounds__(BNT) __attribute__((amdgpu_waves_per_eu(2)))
 void fused_bwd_kv_kernel(FusedBwdDesc fd) {
   extern __shared__ __align__(16) char smem[];
-  FusedBwdKV<D, CHK>::run(fd, smem);
+  FusedBwdKV<D, CHK, PART>::run(fd, smem);
 }
 
 template <int D, bool PROT>
@@ -1453,7 +1413,7 @@ hipError_t launch_bwd_kernel(const FusedBwdDesc& fd, int lds, hipStream_t s) {
   }
   const int64_t grid = int64_t(fd.B) * fd.nh * (fd.S / FT);
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL(KERN, dim3(unsigned(grid)), dim3(FNT), lds, s, fd);
+  hipLaunchKernelGGL(KERN, dim3(unsigned(grid)), dim3(BNT), lds, s, fd);
   return hipGetLastError();
 }
 
@@ -1483,11 +1443,20 @@ hipError_t launch_fused_bwd_kv(const FusedBwdDesc& fd, hipStream_t s) {
       (fd.check && (fd.qkvc == nullptr || fd.qr == nullptr || fd.dclr == nullptr || fd.dclc == nullptr)))
     return hipErrorInvalidValue;
   if (fd.D == 64)
-    return fd.check ? launch_bwd_kernel<fused_bwd_kv_kernel<64, true>>(fd, FusedBwdKV<64, true>::LDS_BYTES, s)
-                    : launch_bwd_kernel<fused_bwd_kv_kernel<64, false>>(fd, FusedBwdKV<64, false>::LDS_BYTES, s);
-  if (fd.D == 128)
-    return fd.check ? launch_bwd_kernel<fused_bwd_kv_kernel<128, true>>(fd, FusedBwdKV<128, true>::LDS_BYTES, s)
-                    : launch_bwd_kernel<fused_bwd_kv_kernel<128, false>>(fd, FusedBwdKV<128, false>::LDS_BYTES, s);
+    return fd.check
+               ? launch_bwd_kernel<fused_bwd_kv_kernel<64, true, 0>>(fd, FusedBwdKV<64, true, 0>::LDS_BYTES, s)
+               : launch_bwd_kernel<fused_bwd_kv_kernel<64, false, 0>>(fd, FusedBwdKV<64, false, 0>::LDS_BYTES, s);
+  if (fd.D == 128 && !fd.check)
+    return launch_bwd_kernel<fused_bwd_kv_kernel<128, false, 0>>(fd, FusedBwdKV<128, false, 0>::LDS_BYTES, s);
+  if (fd.D == 128) {
+    hipError_t e = fd.check
+        ? launch_bwd_kernel<fused_bwd_kv_kernel<128, true, 1>>(fd, FusedBwdKV<128, true, 1>::LDS_BYTES, s)
+        : launch_bwd_kernel<fused_bwd_kv_kernel<128, false, 1>>(fd, FusedBwdKV<128, false, 1>::LDS_BYTES, s);
+    if (e != hipSuccess) return e;
+    return fd.check
+        ? launch_bwd_kernel<fused_bwd_kv_kernel<128, true, 2>>(fd, FusedBwdKV<128, true, 2>::LDS_BYTES, s)
+        : launch_bwd_kernel<fused_bwd_kv_kernel<128, false, 2>>(fd, FusedBwdKV<128, false, 2>::LDS_BYTES, s);
+  }
   return hipErrorInvalidValue;
 }
 

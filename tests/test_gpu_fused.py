@@ -276,9 +276,9 @@ def run_fused_training(shape, faults=(), seed=1):
 
 
 @pytest.mark.parametrize("causal", [False, True])
-@pytest.mark.parametrize("R", [128, 64])
-def test_fused_forward_backward(causal, R):
-    shape = W.make_shape(2, 256, 128, 2, causal=causal, block_rows=R, name="train")
+@pytest.mark.parametrize("R,H", [(128, 128), (64, 128), (128, 256)], ids=["d64r128", "d64r64", "d128"])
+def test_fused_forward_backward(causal, R, H):
+    shape = W.make_shape(2, 256, H, 2, causal=causal, block_rows=R, name="train")
     g, o, ob = run_fused_training(shape)
     assert g["rep_f"]["events"] == [] and g["rep_b"]["events"] == []
     assert o["events"] == [] and ob["events"] == []
@@ -325,12 +325,14 @@ def check_training_outputs(g, o, ob, shape):
         assert nrel <= RTOL, f"{k} vs materialised: relative norm {nrel:.3g}"
 
 
-@pytest.mark.parametrize("R", [128, 64])
-def test_fused_backward_faults(R):
-    """Faults in the scores (the forward's and the backward's recomputation
-    both see them), dP, dV, dQ and dX: each located where injected and
-    corrected, events identical to the fused oracle's."""
-    shape = W.make_shape(1, 256, 128, 2, causal=True, block_rows=R, name="trainf")
+@pytest.mark.parametrize("R,H", [(128, 128), (64, 128), (128, 256)], ids=["d64r128", "d64r64", "d128"])
+def test_fused_backward_faults(R, H):
+    """Faults in the scores (the forward's and both backward passes'
+    recomputations see them), dP, dV, dK, dQ and dX: each located where
+    injected and corrected, events identical to the fused oracle's (at
+    head dim 128 the key pass runs in two parts; the event count is the
+    same)."""
+    shape = W.make_shape(1, 256, H, 2, causal=True, block_rows=R, name="trainf")
     faults = [W.Fault("AS", 0, 1, 200, 3, np.inf), W.Fault("dV", 0, 0, 17, 9, np.nan),
               W.Fault("dQ", 0, 1, 130, 60, 1e10), W.Fault("dX", 0, 0, 77, 100, np.inf),
               W.Fault("dAP", 0, 0, 250, 249, -1e10), W.Fault("dQ", 0, 0, 31, 5, 40.0),
