@@ -56,12 +56,16 @@ struct Layout_ {
 
 // K slices for a weight-gradient GEMM (M x N tiles of 128 x 128, long K):
 // enough slices to give about 512 workgroups, each slice at least 512 deep.
-int splitk_for(int64_t M, int64_t N, int64_t K) {
+int splitk_for(int64_t M, int64_t N, int64_t K, bool prot) {
   const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
   int ks = 1;
   // smallest power of two that fills every CU once (fewer slices, less
   // partial-sum traffic), with K slices of at least 256
   while (tiles * ks < 256 && K / (2 * ks) >= 256 && ks < 16) ks *= 2;
+  // a checked weight gradient in one slice stages its fp32 tile in LDS for
+  // the column check, which leaves one workgroup per CU; in two slices the
+  // K loop keeps two per CU and the check moves to the reduction
+  if (prot && ks == 1 && K / 2 >= 256) ks = 2;
   return ks;
 }
 
@@ -112,7 +116,7 @@ Layout_ make_layout(const Dims& d) {
   L.dasc = take(size_t(d.B) * d.nh * d.nq * 2 * d.S * f);
   L.dasr = take(size_t(d.B) * d.nh * d.S * d.nq * 2 * f);
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
-  const int ks1 = splitk_for(d.H, 3 * d.H, d.T), ks2 = splitk_for(d.H, d.H, d.T);
+  const int ks1 = splitk_for(d.H, 3 * d.H, d.T, true), ks2 = splitk_for(d.H, d.H, d.T, true);
   const size_t p1 = ks1 > 1 ? size_t(ks1) * d.H * 3 * d.H : 0;
   const size_t p2 = ks2 > 1 ? size_t(ks2) * d.H * d.H : 0;
   const size_t c1 = ks1 > 1 ? size_t(ks1) * 2 * d.nh * 3 * d.H : 0;
@@ -177,7 +181,7 @@ Layout_ make_layout_fused(const Dims& d) {
   L.doc = take(size_t(d.B) * d.nq * 2 * d.H * f);
   L.dclc = take(size_t(d.B) * d.nq * 2 * d.H * f);
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
-  const int ks1 = splitk_for(d.H, 3 * d.H, d.T), ks2 = splitk_for(d.H, d.H, d.T);
+  const int ks1 = splitk_for(d.H, 3 * d.H, d.T, true), ks2 = splitk_for(d.H, d.H, d.T, true);
   const size_t p1 = ks1 > 1 ? size_t(ks1) * d.H * 3 * d.H : 0;
   const size_t p2 = ks2 > 1 ? size_t(ks2) * d.H * d.H : 0;
   const size_t c1 = ks1 > 1 ? size_t(ks1) * 2 * d.nh * 3 * d.H : 0;
@@ -265,7 +269,7 @@ Tile proj_tile() { return Tile::T128x128; }
 // A weight-gradient GEMM (MN-major operands, fp32 output): split over K
 // into partials when that fills the GPU better, then reduced and verified.
 hipError_t launch_wgrad(const GemmDesc& g, int dt, float* part, float* part_c, hipStream_t s) {
-  const int ks = splitk_for(g.M, g.N, g.K);
+  const int ks = splitk_for(g.M, g.N, g.K, g.Ac != nullptr || g.Br != nullptr || g.verify != 0);
   if (ks <= 1)
     return launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s);
   GemmDesc sg = g;

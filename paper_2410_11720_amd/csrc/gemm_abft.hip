@@ -483,38 +483,26 @@ struct Gemm {
 #pragma unroll
         for (int j = 0; j < JN; ++j) acc[i][j] = Mfma<T>::mma(af[i], bfr[j], acc[i][j]);
       if (PROT) {
-        // wave-uniform branches keep every fragment index a compile-time
-        // constant (a runtime index would send the arrays to scratch)
-        if (cc && WLC) {
+        // the strip operands a wave takes are selected, not branched to:
+        // every fragment index stays a compile-time constant (a runtime
+        // index would send the arrays to scratch) and the k step stays one
+        // block of straight-line code
+        if (cc) {
           const auto sf = Mfma<T>::load(sS + fr * LDK + kk + fk);
 #pragma unroll
-          for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[j], accs[j]);
-        } else if (cc) {
-          const auto sf = Mfma<T>::load(sS + fr * LDK + kk + fk);
-          if (wm == 0) {
-#pragma unroll
-            for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[j], accs[j]);
-          } else {
-#pragma unroll
-            for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[JS + j], accs[j]);
+          for (int j = 0; j < JS; ++j) {
+            const auto bsel = (WLC || wm == 0) ? bfr[j] : bfr[WLC ? j : JS + j];
+            accs[j] = Mfma<T>::mma(sf, bsel, accs[j]);
           }
         }
-        if (cr && WLC) {
+        if (cr) {
           const auto rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
 #pragma unroll
-          for (int w = 0; w < WGN; ++w)
-            if (wn == w) {
+          for (int i = 0; i < IS; ++i) {
+            auto asel = af[i];
 #pragma unroll
-              for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[IS * w + i], accr[i]);
-            }
-        } else if (cr) {
-          const auto rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
-          if (wn == 0) {
-#pragma unroll
-            for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[i], accr[i]);
-          } else {
-#pragma unroll
-            for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[IS + i], accr[i]);
+            for (int w = 1; w < WGN; ++w) asel = wn == w ? af[IS * w + i] : asel;
+            accr[i] = Mfma<T>::mma(rf, asel, accr[i]);
           }
         }
       }
