@@ -113,7 +113,7 @@ def stage_bound(flops, nbytes):
 # kernel symbol (as rocprofv3 names it) and grid (workgroups) of the stages
 # whose HBM traffic is recorded, at the workload shape, protected
 KERNEL_OF_STAGE = {
-    "core_kv": ("fused_bwd_kv_kernel<64, true>", 768),
+    "core_kv": ("fused_bwd_kv_kernel<64, true, 0>", 768),
     "core_q": ("fused_bwd_q_kernel<64, true>", 768),
     "attn": ("fused_attn_kernel<64, true>", 768),
     "qkv": ("gemm_kernel<unsigned short, unsigned short, true, false, 128, 128, true, 2, true, true>", 1152),
@@ -753,8 +753,8 @@ def recovery_costs(path, per_clean, steps):
 PUBLIC_KEYS = ("path", "tflops", "ms_per_step", "ms_protected_fault_free", "ms_unprotected",
                "ms_one_fault", "tflops_unprotected", "abft_overhead_pct",
                "abft_overhead_pct_p50", "correction_cost_pct", "one_fault_op", "schedule_check",
-               "stages_us", "stages_us_unprotected", "stages_frac_of_bound", "roofline_model",
-               "step_ms_events")
+               "stages_us", "stages_us_unprotected", "stages_frac_of_bound", "stages_bound",
+               "roofline_model", "step_ms_events")
 
 
 def public(rec):
