@@ -10,6 +10,8 @@ depends on how the keys are grouped; the materialised form rounds AS and
 AP instead). A context element fixed from its row checksum is within the
 reconstruction bound of the fault-free value.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -346,3 +348,86 @@ def test_fused_backward_faults(R, H):
     twice = sum(f.op in ("AS", "dAP") for f in faults)
     assert len(o["events"]) == 1 and len(ob["events"]) == len(faults) + twice
     check_training_outputs(g, o, ob, shape)
+
+
+def sampled_core(inp, shape, p, only, faults=()):
+    """The fused oracle on the sampled (batch, head) pairs only: the
+    projection of the whole layer, the fused attention of the pairs (CL and
+    the softmax statistics), dCL = dO W^O^T, then the fused backward core
+    on a one-head context per pair (faults of the score and gradient ops
+    of a pair moved to its (0, 0)). Returns per pair dQ, dK, dV and the
+    core's events, and the forward's events."""
+    from oracle.eec import col_checksums
+    from oracle.fused import fused_backward_core
+    run = _Run(p, list(faults))
+    pr = project(run, inp["X"], inp["Wqkv"], p, verify_always=True)
+    st = {}
+    CL, _ = fused_attention(run, pr, p, only=set(only), stats=st)
+    B, S, H, nh, d, R, nq = (pr[k] for k in ("B", "S", "H", "nh", "d", "R", "nq"))
+    dO = np.asarray(inp["dO"], dtype=np.float64)
+    Wo = np.asarray(inp["Wo"], dtype=np.float64)
+    dCL = run.rnd(dO @ Wo.T)
+    dCLc = col_checksums(dO, R) @ Wo.T
+
+    def heads_of(M):
+        return M.reshape(B, S, nh, d).transpose(0, 2, 1, 3)
+
+    def heads_of_c(Mc):
+        return Mc.reshape(B, nq, 2, nh, d).transpose(0, 3, 1, 2, 4)
+
+    Vch = heads_of_c(pr["QKVc"][..., 2 * H:])
+    out = {}
+    for (b, h) in only:
+        sl = (slice(b, b + 1), slice(h, h + 1))
+        ctx = dict(B=1, S=S, H=d, nh=1, d=d, R=R, nq=nq, scale=pr["scale"],
+                   Qh=pr["Qh"][sl], Kh=pr["Kh"][sl], Vh=pr["Vh"][sl], dCLh=heads_of(dCL)[sl],
+                   CLh=heads_of(CL)[sl], Qch=pr["Qch"][sl], Kch=pr["Kch"][sl], Vch=Vch[sl],
+                   dCLch=heads_of_c(dCLc)[sl], m=st["m"][sl], l=st["l"][sl])
+        mine = [dataclasses.replace(f, b=0, h=0) for f in faults
+                if (f.b, f.h) == (b, h) and f.op in ("AS", "dAP", "dQ", "dK", "dV")]
+        crun = _Run(p, mine)
+        c = fused_backward_core(crun, ctx, p)
+        out[(b, h)] = dict(dQ=c["dQ"][0, 0], dK=c["dK"][0, 0], dV=c["dV"][0, 0],
+                           events=[(e[0], b, h) + tuple(e[3:]) for e in crun.events])
+    return out, run.events
+
+
+@pytest.mark.parametrize("with_faults", [False, True])
+def test_fused_gpt2_training_sampled_heads(with_faults):
+    """The benchmark's workload and launch configuration (B8 S1024 H768,
+    12 heads of 64, causal, R 128, the fused forward and backward): the
+    gradients dQ, dK, dV of sampled heads against the fused oracle's core
+    for those heads, within 1e-2 in relative norm (reading 18: cascaded
+    roundings), and, with faults in the sampled heads' scores, dP and
+    gradients, events identical to the oracle's (a score or dP fault in the
+    forward and both backward passes)."""
+    abft = _abft()
+    shape = W.CONFIGS["c3"]
+    inp = W.make_inputs(shape, W.data_seed("c3"))
+    only = [(0, 0), (7, 11), (3, 5)]
+    faults = [W.Fault("AS", 3, 5, 700, 131, np.inf), W.Fault("dAP", 7, 11, 1000, 3, -1e10),
+              W.Fault("dQ", 0, 0, 513, 60, np.nan), W.Fault("dK", 3, 5, 64, 7, 1e10),
+              W.Fault("dV", 7, 11, 1023, 63, np.inf)] if with_faults else []
+    print(f"[case] fused c3 training sampled heads faults={len(faults)}", flush=True)
+    cfg = abft.LayerConfig(shape.batch, shape.seq, shape.hidden, shape.heads, causal=True,
+                           block_rows=shape.block_rows, fused=True)
+    layer = abft.ProtectedAttention(cfg)
+    X, Wqkv, Wo, dO = (dev(inp[k]) for k in ("X", "Wqkv", "Wo", "dO"))
+    fdev = abft.faults_to_device(faults)
+    layer.forward(X, Wqkv, Wo, fdev)
+    layer.backward(dO, X, Wqkv, Wo, fdev)
+    torch.cuda.synchronize()
+    rep_f, rep_b = abft.read_report(layer.report), abft.read_report(layer.report_bwd)
+    dQKV = host(layer.tensor("dQKV"))
+    p = OracleParams(heads=shape.heads, causal=True, block_rows=shape.block_rows)
+    ref, fwd_events = sampled_core(inp, shape, p, only, faults)
+    H, d = shape.hidden, shape.head_dim
+    assert rep_f["n_uncorrectable"] == 0 and rep_b["n_uncorrectable"] == 0
+    assert sorted(rep_f["events"]) == sorted(fwd_events)
+    assert sorted(rep_b["events"]) == sorted(e for r in ref.values() for e in r["events"])
+    for (b, h), r in ref.items():
+        for i, k in enumerate(("dQ", "dK", "dV")):
+            got = dQKV[b, :, i * H + h * d:i * H + (h + 1) * d]
+            assert np.isfinite(got).all(), (b, h, k)
+            nrel = np.linalg.norm(got - r[k]) / np.linalg.norm(r[k])
+            assert nrel <= RTOL, f"{k}[{b},{h}]: relative norm {nrel:.3g}"
