@@ -81,7 +81,6 @@ def stage_table(B, S, H, nh, causal, fused, es=2):
             ("attn", False, 0x004, 4 * sq * d, 4 * th + stats, 1),
             # the output projection encodes CL^c first
             ("out", False, 0x020, 2 * T * H * H, 3 * th + H * H * es, 2)] + gemms_b + [
-            ("core_enc", True, 0x008, 0, 3 * th + 3 * T * nh * 2 * f32, 1),
             ("core_q", True, 0x040, 6 * sq * d, 6 * th + stats + B * nh * S * f32, 1),
             ("core_kv", True, 0x010, 8 * sq * d, 6 * th + stats + B * nh * S * f32, 1),
             wq,

@@ -88,10 +88,8 @@ extern "C" {
                                        the dQ, dK and dV GEMMs, storing no
                                        score-shaped tensor (the workspace holds
                                        none: attn_abft_workspace_bytes is
-                                       smaller): the row checksums of K, Q and
-                                       dCL over each head's dims are encoded
-                                       (stage bit DAP), then a query pass
-                                       (bits SOFTMAX_BWD, DQ) recomputes
+                                       smaller): a query pass (stage bits
+                                       SOFTMAX_BWD, DQ) recomputes
                                        S = Q K^T, row-checked per (query, R-key
                                        block) against Q (K^c)^T, takes P from
                                        the statistics, dP = dCL V^T row-checked
@@ -103,7 +101,10 @@ extern "C" {
                                        against (Q^c) K^T and (dCL^c) V^T, and
                                        forms dV = P^T dCL and dK = dS^T Q,
                                        row-checked against P^T dCL^r and
-                                       dS^T Q^r (CORE_BWD selects all three).
+                                       dS^T Q^r (CORE_BWD selects both; each
+                                       pass forms the row checksums K^r, Q^r
+                                       and dCL^r over each head's dims from
+                                       the tiles it loads).
                                        A located dQ, dK or dV element is fixed
                                        from the checksum. AS faults reach both
                                        passes' recomputed scores (two events),
@@ -244,8 +245,7 @@ int attn_abft_forward_noalloc(const attn_abft_config* cfg, const void* X, const 
 #define ABFT_STAGE_OUT         0x020u  /* fwd: O = CL Wo (fused: CL^c encoded first) */
 #define ABFT_STAGE_DCL         0x002u  /* bwd: dCL = dO Wo^T                        */
 #define ABFT_STAGE_DWO         0x004u  /* bwd: dWo = CL^T dO                        */
-#define ABFT_STAGE_DAP         0x008u  /* bwd: dAP = dCL V^T (fused: the core's row
-                                          checksums of K, Q, dCL)               */
+#define ABFT_STAGE_DAP         0x008u  /* bwd: dAP = dCL V^T (fused: no work)       */
 #define ABFT_STAGE_DV          0x010u  /* bwd: dV = AP^T dCL (fused: the key pass)  */
 #define ABFT_STAGE_SOFTMAX_BWD 0x020u  /* bwd: dAS = scale AP (dAP - rowdot)
                                           (fused: the query pass)               */

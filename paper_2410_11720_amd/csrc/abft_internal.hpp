@@ -145,16 +145,15 @@ hipError_t launch_fused_fwd(const FusedDesc& d, hipStream_t stream);
 // Fused backward core after a fused forward (no scores kept), in two
 // passes that each recompute the scores from the softmax statistics: the
 // query pass (dQ; it also leaves D = dCL . CL per query) and the key pass
-// (dK and dV), which reads D.
+// (dK and dV), which reads D. The row checksums over each head's dims
+// (K^r in the query pass, Q^r and dCL^r in the key pass) are formed in the
+// passes from the tiles they stage.
 struct FusedBwdDesc {
   int B = 0, nh = 0, S = 0, H = 0, D = 0, R = 128;
   int causal = 0;
   float scale = 1.f;
   const void* qkv = nullptr;    // [B*S][3H] bf16: Q | K | V
   const float* qkvc = nullptr;  // [B][S/R][2][3H] propagated column checksums (Q^c, K^c, V^c)
-  const float* qr = nullptr;    // [B*S][nh][2] row checksums of Q over each head's dims
-  const float* kr = nullptr;    // [B*S][nh][2] the same of K
-  const float* dclr = nullptr;  // [B*S][nh][2] the same of dCL
   const float* dclc = nullptr;  // [B][S/R][2][H] propagated column checksums of dCL
   const void* cl = nullptr;     // [B*S][H] bf16, the forward's context
   const void* dcl = nullptr;    // [B*S][H] bf16

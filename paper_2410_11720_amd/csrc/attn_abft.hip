@@ -49,7 +49,6 @@ struct Layout_ {
   size_t xc, xr, wvr, qkvc, vr, apc, apr, clc, clr, doc, dclc, dasc, dasr, dqkvc;
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
-  size_t kr, qr, dclr;  // fused backward: row checksums of K, Q, dCL per head [T][nh][2]
   size_t drow;      // fused backward: D = dCL . CL per query [B][nh][S]
   size_t total;
 };
@@ -189,9 +188,6 @@ Layout_ make_layout_fused(const Dims& d) {
   L.skp = take((p1 > p2 ? p1 : p2) * f);
   L.skc = take((c1 > c2 ? c1 : c2) * f);
   L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
-  L.kr = take(size_t(d.T) * d.nh * 2 * f);
-  L.qr = take(size_t(d.T) * d.nh * 2 * f);
-  L.dclr = take(size_t(d.T) * d.nh * 2 * f);
   L.drow = take(size_t(d.B) * d.nh * d.S * f);
   L.total = off;
   return L;
@@ -616,36 +612,20 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
   // after a fused forward (no scores kept): the fused backward core, from
-  // the forward's softmax statistics, in three launches: the row checksums
-  // of K, Q and dCL per head over the head dims (from the checked
-  // tensors), the query pass (dQ, and D per query) and the key pass (dK
-  // and dV); nothing score-shaped is stored (dQ^c, dK^c and dV^c are
-  // encoded at the dX stage)
+  // the forward's softmax statistics, in two launches: the query pass (dQ,
+  // and D per query) and the key pass (dK and dV); each forms the row
+  // checksums over the head dims that it needs (K^r; Q^r and dCL^r) from
+  // the tiles it stages; nothing score-shaped is stored (dQ^c, dK^c and
+  // dV^c are encoded at the dX stage)
   if (fused) {
-    const uint32_t st_enc = ABFT_STAGE_CORE_BWD | ABFT_STAGE_DAP;
     const uint32_t st_q = ABFT_STAGE_CORE_BWD | ABFT_STAGE_SOFTMAX_BWD | ABFT_STAGE_DQ;
     const uint32_t st_kv = ABFT_STAGE_CORE_BWD | ABFT_STAGE_DV | ABFT_STAGE_DK;
-    if ((stages & st_enc) && pb) {
-      EncodeJob e[3];
-      const void* src[3] = {ws + L.qkv + H * es, ws + L.qkv, ws + L.dcl};
-      const int64_t lds[3] = {3 * H, 3 * H, H};
-      float* dst[3] = {F(L.kr), F(L.qr), F(L.dclr)};
-      for (int i = 0; i < 3; ++i) {
-        e[i].A = src[i]; e[i].batch = B; e[i].rows = S; e[i].cols = H; e[i].ld = lds[i];
-        e[i].batch_stride = S * lds[i]; e[i].Rb = int(R); e[i].Cb = int(hd);
-        e[i].row_chk = dst[i];
-      }
-      CK(launch_encode_jobs(e, 3, dt, nullptr, s));
-    }
     FusedBwdDesc fd;
     fd.B = int(B); fd.nh = int(nh); fd.S = int(S); fd.H = int(H); fd.D = int(hd); fd.R = int(R);
     fd.causal = cfg->causal;
     fd.scale = p.scale;
     fd.qkv = ws + L.qkv;
     fd.qkvc = pb ? F(L.qkvc) : nullptr;
-    fd.qr = pb ? F(L.qr) : nullptr;
-    fd.kr = pb ? F(L.kr) : nullptr;
-    fd.dclr = pb ? F(L.dclr) : nullptr;
     fd.dclc = pb ? F(L.dclc) : nullptr;
     fd.cl = ws + L.cl;
     fd.dcl = ws + L.dcl;

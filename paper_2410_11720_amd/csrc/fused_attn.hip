@@ -753,29 +753,56 @@ struct BwdTile {
                                const bf16_t* Bm, int64_t lda, int64_t ldb, float* scr, int lane) {
     const int lq = lane & 15, g = lane >> 4;
     const int R = fd.R, NB = FT / R, lg_jpb = __builtin_ctz(R / 16);
-    float sj[8], aj[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      sj[j] = (t[j][0] + t[j][1]) + (t[j][2] + t[j][3]);
-      aj[j] = (fabsf(t[j][0]) + fabsf(t[j][1])) + (fabsf(t[j][2]) + fabsf(t[j][3]));
-    }
-    float r1[4], ra[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      r1[i] = sj[2 * i] + sj[2 * i + 1];
-      ra[i] = aj[2 * i] + aj[2 * i + 1];
-    }
-    if (lg_jpb >= 2) {
-      r1[0] += r1[1]; ra[0] += ra[1];
-      r1[1] = r1[2] + r1[3]; ra[1] = ra[2] + ra[3];
-    }
-    if (lg_jpb >= 3) { r1[0] += r1[1]; ra[0] += ra[1]; }
     float mine1 = 0.f, minea = 0.f;
+    if constexpr (D == 64) {
+      // Each column's sums over the rows of every R-row block on the matrix
+      // cores: the values and their magnitudes packed to bf16 (a rounding of
+      // 2^-9 relative, far inside the detection bound E) as the B operand,
+      // one slab of 32 rows per MFMA, against a block-indicator A operand
+      // whose row 4 b is block b's: row 4 b of the result, register 0 of
+      // lane group b, is block b's sum.
+      floatx4 vs = {0.f, 0.f, 0.f, 0.f}, as = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (i < NB) {
-        const float t1 = group4_sum(r1[i]), ta = group4_sum(ra[i]);
-        if (g == i) { mine1 = t1; minea = ta; }
+      for (int q = 0; q < 4; ++q) {
+        float a0[4], a1[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) { a0[r] = t[2 * q][r]; a1[r] = t[2 * q + 1][r]; }
+        const uint2 p0 = pack4(a0), p1 = pack4(a1);
+        const uint4 u = {p0.x, p0.y, p1.x, p1.y};
+        const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu, u.w & 0x7fff7fffu};
+        const uint32_t one = lq == 4 * ((32 * q) >> (lg_jpb + 4)) ? 0x3f803f80u : 0u;
+        const bf16x8 ind = __builtin_bit_cast(bf16x8, uint4{one, one, one, one});
+        vs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ind, __builtin_bit_cast(bf16x8, u), vs, 0, 0, 0);
+        as = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ind, __builtin_bit_cast(bf16x8, ua), as, 0, 0, 0);
+      }
+      mine1 = vs[0];
+      minea = as[0];
+    } else {
+      // the same sums on the vector ALUs (head dim 128: the matrix-core
+      // form holds registers the key pass does not have)
+      float sj[8], aj[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        sj[j] = (t[j][0] + t[j][1]) + (t[j][2] + t[j][3]);
+        aj[j] = (fabsf(t[j][0]) + fabsf(t[j][1])) + (fabsf(t[j][2]) + fabsf(t[j][3]));
+      }
+      float r1[4], ra[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        r1[i] = sj[2 * i] + sj[2 * i + 1];
+        ra[i] = aj[2 * i] + aj[2 * i + 1];
+      }
+      if (lg_jpb >= 2) {
+        r1[0] += r1[1]; ra[0] += ra[1];
+        r1[1] = r1[2] + r1[3]; ra[1] = ra[2] + ra[3];
+      }
+      if (lg_jpb >= 3) { r1[0] += r1[1]; ra[0] += ra[1]; }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (i < NB) {
+          const float t1 = group4_sum(r1[i]), ta = group4_sum(ra[i]);
+          if (g == i) { mine1 = t1; minea = ta; }
+        }
       }
     }
     const float c1 = cs[0] + cs[1];
@@ -935,11 +962,44 @@ struct BwdTile {
       }
     }
   }
-  // row-checksum strip [128 rows][4]: the hi/lo of the sum and of the
-  // weighted sum of row tid / 2 (threads 0..255)
-  __device__ static __forceinline__ void rstrip_commit(bf16_t* rs, int tid, float v) {
-    rs[(tid >> 1) * 4 + 2 * (tid & 1)] = f2bf(v);
-    rs[(tid >> 1) * 4 + 2 * (tid & 1) + 1] = f2bf(v - bf2f(f2bf(v)));
+  // Row checksums over the head dims (the sum and the 1-based weighted
+  // sum) of the 128 rows row0.. of a row-major [rows][ld] bf16 tensor, as
+  // the hi/lo bf16 pairs of a [128 rows][4] strip: four threads per row,
+  // D / 4 dims each, loaded with the tile (rstrip_issue) and summed when
+  // it has landed (rstrip_commit).
+  static constexpr int CPP = D / 32;  // 8-element chunks per thread
+  __device__ static __forceinline__ void rstrip_issue(const bf16_t* base, int64_t ld, int row0,
+                                                      int nrows, int tid, bf16x8 (&v)[CPP]) {
+    const bf16_t* p = base + int64_t(min(row0 + (tid >> 2), nrows - 1)) * ld + (tid & 3) * (8 * CPP);
+#pragma unroll
+    for (int cc = 0; cc < CPP; ++cc) v[cc] = *reinterpret_cast<const bf16x8*>(p + 8 * cc);
+  }
+  __device__ static __forceinline__ void rstrip_commit(bf16_t* rs, int tid, const bf16x8 (&v)[CPP]) {
+    const int row = tid >> 2, part = tid & 3;
+    // two elements per step: dot products of bf16 pairs with (1, 1) and
+    // with their 1-based indices in the thread's range
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 ones = {__bf16(1.f), __bf16(1.f)};
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int cc = 0; cc < CPP; ++cc) {
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const bf16x2 x = {v[cc][e], v[cc][e + 1]};
+        const bf16x2 w = {__bf16(float(8 * cc + e + 1)), __bf16(float(8 * cc + e + 2))};
+        s1 = __builtin_amdgcn_fdot2_f32_bf16(x, ones, s1, false);
+        s2 = __builtin_amdgcn_fdot2_f32_bf16(x, w, s2, false);
+      }
+    }
+    s2 = fmaf(float(8 * CPP * part), s1, s2);    // the range starts at dim 8 CPP part
+    s1 += __shfl_xor(s1, 1, 64);
+    s2 += __shfl_xor(s2, 1, 64);
+    s1 += __shfl_xor(s1, 2, 64);
+    s2 += __shfl_xor(s2, 2, 64);
+    if (part == 0) {
+      const uint2 w = {pack2(s1, s1 - bf2f(f2bf(s1))), pack2(s2, s2 - bf2f(f2bf(s2)))};
+      *reinterpret_cast<uint2*>(rs + row * 4) = w;
+    }
   }
 };
 
@@ -1006,7 +1066,8 @@ struct FusedBwdQ : BwdTile<D> {
     const bf16_t* zeros = reinterpret_cast<const bf16_t*>(smem + OFF_ZERO);
     if (chk && tid < T::ZERO / 4) reinterpret_cast<uint32_t*>(smem + OFF_ZERO)[tid] = 0u;
 
-    float kcv[T::NSV], vcv[T::NSV], krv = 0.f;
+    float kcv[T::NSV], vcv[T::NSV];
+    bf16x8 krv[T::CPP];
     auto issue = [&](int kt) {
       const int key0 = kt * FT;
 #pragma unroll
@@ -1018,15 +1079,14 @@ struct FusedBwdQ : BwdTile<D> {
         const int64_t blk0 = int64_t(b) * nqR + key0 / R;
         T::strip_issue(fd.qkvc + H + h * D, ld, blk0, NB, tid, kcv);
         T::strip_issue(fd.qkvc + 2 * H + h * D, ld, blk0, NB, tid, vcv);
-        const int tr = tid & (2 * FT - 1);   // threads 0..255 hold the strip's 256 values
-        krv = fd.kr[((int64_t(b) * S + key0 + (tr >> 1)) * fd.nh + h) * 2 + (tr & 1)];
+        T::rstrip_issue(Kp, ld, key0, S, tid, krv);
       }
     };
     auto commit = [&]() {
       if (chk) {
         T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_KC), NB, tid, kcv);
         T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_VC), NB, tid, vcv);
-        if (tid < 2 * FT) T::rstrip_commit(krs, tid, krv);
+        T::rstrip_commit(krs, tid, krv);
       }
     };
 
@@ -1192,7 +1252,8 @@ struct FusedBwdKV : BwdTile<D> {
     float* rowf = reinterpret_cast<float*>(smem + OFF_ROW);
 
     float qcv[T::NSV], gcv[T::NSV];
-    float qrv = 0.f, grv = 0.f, rv0 = 0.f, rv1 = 0.f;
+    bf16x8 qrv[T::CPP], grv[T::CPP];
+    float rv0 = 0.f, rv1 = 0.f;
     auto issue = [&](int qt) {
       const int q0 = qt * FT;
 #pragma unroll
@@ -1212,10 +1273,8 @@ struct FusedBwdKV : BwdTile<D> {
         const int64_t blk0 = int64_t(b) * nqR + q0 / R;
         T::strip_issue(fd.qkvc + h * D, ld, blk0, NB, tid, qcv);
         T::strip_issue(fd.dclc + h * D, H, blk0, NB, tid, gcv);
-        const int tr = tid & (2 * FT - 1);   // threads 0..255 hold the strips' 256 values
-        const int64_t ri = ((int64_t(b) * S + q0 + (tr >> 1)) * fd.nh + h) * 2 + (tr & 1);
-        qrv = fd.qr[ri];
-        grv = fd.dclr[ri];
+        if (DO_K) T::rstrip_issue(Qp, ld, q0, S, tid, qrv);
+        if (DO_V) T::rstrip_issue(dCLp, H, q0, S, tid, grv);
       }
     };
     auto commit = [&]() {
@@ -1228,10 +1287,8 @@ struct FusedBwdKV : BwdTile<D> {
       if (chk) {
         T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_QC), NB, tid, qcv);
         T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_GC), NB, tid, gcv);
-        if (tid < 2 * FT) {
-          T::rstrip_commit(qrs, tid, qrv);
-          T::rstrip_commit(grs, tid, grv);
-        }
+        if (DO_K) T::rstrip_commit(qrs, tid, qrv);
+        if (DO_V) T::rstrip_commit(grs, tid, grv);
       }
     };
 
@@ -1427,7 +1484,7 @@ static bool bwd_desc_ok(const FusedBwdDesc& fd) {
 }
 
 hipError_t launch_fused_bwd_q(const FusedBwdDesc& fd, hipStream_t s) {
-  if (!bwd_desc_ok(fd) || fd.cl == nullptr || (fd.check && (fd.qkvc == nullptr || fd.kr == nullptr)))
+  if (!bwd_desc_ok(fd) || fd.cl == nullptr || (fd.check && fd.qkvc == nullptr))
     return hipErrorInvalidValue;
   if (fd.D == 64)
     return fd.check ? launch_bwd_kernel<fused_bwd_q_kernel<64, true>>(fd, FusedBwdQ<64, true>::LDS_BYTES, s)
@@ -1440,7 +1497,7 @@ hipError_t launch_fused_bwd_q(const FusedBwdDesc& fd, hipStream_t s) {
 
 hipError_t launch_fused_bwd_kv(const FusedBwdDesc& fd, hipStream_t s) {
   if (!bwd_desc_ok(fd) ||
-      (fd.check && (fd.qkvc == nullptr || fd.qr == nullptr || fd.dclr == nullptr || fd.dclc == nullptr)))
+      (fd.check && (fd.qkvc == nullptr || fd.dclc == nullptr)))
     return hipErrorInvalidValue;
   if (fd.D == 64)
     return fd.check
