@@ -72,6 +72,14 @@ __device__ __forceinline__ float group4_sum(float x) { return xsum32(xsum16(x));
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
   return uint32_t(f2bf(a)) | (uint32_t(f2bf(b)) << 16);
 }
+// the same in one packed conversion (the same rounding; used where the
+// register allocation of the surrounding code allows it)
+__device__ __forceinline__ uint32_t pack2v(float a, float b) {
+  typedef float float2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const float2_t f = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
 __device__ __forceinline__ float flip_f32(float x) {
   return __uint_as_float(__float_as_uint(x) ^ 0x40000000u);
 }
@@ -735,6 +743,9 @@ struct BwdTile {
   __device__ static __forceinline__ uint2 pack4(const float (&a)[4]) {
     return uint2{pack2(a[0], a[1]), pack2(a[2], a[3])};
   }
+  __device__ static __forceinline__ uint2 pack4v(const float (&a)[4]) {
+    return uint2{pack2v(a[0], a[1]), pack2v(a[2], a[3])};
+  }
   __device__ static __forceinline__ void unpack4(uint2 p, float (&a)[4]) {
     a[0] = __uint_as_float(p.x << 16);
     a[1] = __uint_as_float(p.x & 0xffff0000u);
@@ -1003,16 +1014,21 @@ struct BwdTile {
   }
 };
 
-// The query pass. LDS: the key tile's K and V images and its K^c, V^c and
-// K^r strips (reloaded per key tile), the workgroup's Q and dCL images
-// (loaded once), scratch.
+// The query pass. LDS: per key tile a stage of the K and V images and the
+// K^c, V^c and K^r strips (two stages at head dim 64: the next tile loads
+// while this one is used), the workgroup's Q and dCL images (loaded once),
+// scratch.
 template <int D, bool CHK>
 struct FusedBwdQ : BwdTile<D> {
   using T = BwdTile<D>;
   using typename T::DK;
   static constexpr int KS = T::KS, DB = T::DB, KH = T::KH, IMG = T::IMG, SCL = T::SCL;
+  static constexpr int NBUF = D == 64 ? 2 : 1;
+  // offsets within a stage
   static constexpr int OFF_V = IMG, OFF_KC = 2 * IMG, OFF_VC = OFF_KC + T::STRIP;
-  static constexpr int OFF_KR = OFF_VC + T::STRIP, OFF_ZERO = OFF_KR + T::RSTRIP;
+  static constexpr int OFF_KR = OFF_VC + T::STRIP;
+  static constexpr int STAGE = T::align1k(OFF_KR + T::RSTRIP);
+  static constexpr int OFF_ZERO = NBUF * STAGE;
   static constexpr int OFF_Q = T::align1k(OFF_ZERO + T::ZERO), OFF_G = OFF_Q + IMG;
   static constexpr int OFF_SCR = OFF_G + IMG;
   static constexpr int LDS_BYTES = OFF_SCR + (BNT / 64) * T::SCR * 4;
@@ -1062,31 +1078,34 @@ struct FusedBwdQ : BwdTile<D> {
       DK::issue(Qp, ld, q0, S, hf * 64, smem + OFF_Q + hf * DK::BYTES, wave, lane);
       DK::issue(dCLp, H, q0, S, hf * 64, smem + OFF_G + hf * DK::BYTES, wave, lane);
     }
-    bf16_t* krs = reinterpret_cast<bf16_t*>(smem + OFF_KR);
     const bf16_t* zeros = reinterpret_cast<const bf16_t*>(smem + OFF_ZERO);
     if (chk && tid < T::ZERO / 4) reinterpret_cast<uint32_t*>(smem + OFF_ZERO)[tid] = 0u;
 
+    // loads of key tile kt into stage st: the images by direct-to-LDS
+    // copies, the strips' values into registers (written by commit)
     float kcv[T::NSV], vcv[T::NSV];
     bf16x8 krv[T::CPP];
-    auto issue = [&](int kt) {
+    auto issue = [&](int kt, int st) {
       const int key0 = kt * FT;
-#pragma unroll
-      for (int hf = 0; hf < KH; ++hf) {
-        DK::issue(Kp, ld, key0, S, hf * 64, smem + hf * DK::BYTES, wave, lane);
-        DK::issue(Vp, ld, key0, S, hf * 64, smem + OFF_V + hf * DK::BYTES, wave, lane);
-      }
       if (chk) {
         const int64_t blk0 = int64_t(b) * nqR + key0 / R;
         T::strip_issue(fd.qkvc + H + h * D, ld, blk0, NB, tid, kcv);
         T::strip_issue(fd.qkvc + 2 * H + h * D, ld, blk0, NB, tid, vcv);
         T::rstrip_issue(Kp, ld, key0, S, tid, krv);
       }
+      char* sb = smem + st * STAGE;
+#pragma unroll
+      for (int hf = 0; hf < KH; ++hf) {
+        DK::issue(Kp, ld, key0, S, hf * 64, sb + hf * DK::BYTES, wave, lane);
+        DK::issue(Vp, ld, key0, S, hf * 64, sb + OFF_V + hf * DK::BYTES, wave, lane);
+      }
     };
-    auto commit = [&]() {
+    auto commit = [&](int st) {
       if (chk) {
-        T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_KC), NB, tid, kcv);
-        T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_VC), NB, tid, vcv);
-        T::rstrip_commit(krs, tid, krv);
+        char* sb = smem + st * STAGE;
+        T::strip_commit(reinterpret_cast<bf16_t*>(sb + OFF_KC), NB, tid, kcv);
+        T::strip_commit(reinterpret_cast<bf16_t*>(sb + OFF_VC), NB, tid, vcv);
+        T::rstrip_commit(reinterpret_cast<bf16_t*>(sb + OFF_KR), tid, krv);
       }
     };
 
@@ -1099,11 +1118,24 @@ struct FusedBwdQ : BwdTile<D> {
       return DK::frag(smem + off + (kk >> 1) * DK::BYTES, wave * 16, (kk & 1) * 32, lane);
     };
 
-    for (int kt = 0; kt < nkt; ++kt) {
-      issue(kt);
+    if (NBUF == 2) {
+      issue(0, 0);
       wait_vmcnt<0>();
-      commit();
-      __syncthreads();  // tile kt in LDS
+      commit(0);
+    }
+    for (int kt = 0; kt < nkt; ++kt) {
+      const int st = NBUF == 2 ? (kt & 1) : 0;
+      if (NBUF == 1) {
+        issue(kt, 0);
+        wait_vmcnt<0>();
+        commit(0);
+      }
+      // tile kt in LDS (double-buffered: the other stage is free)
+      __syncthreads();
+      const bool pre = NBUF == 2 && kt + 1 < nkt;
+      if (pre) issue(kt + 1, st ^ 1);
+      const char* sb = smem + st * STAGE;
+      const bf16_t* krs = reinterpret_cast<const bf16_t*>(sb + OFF_KR);
       const int key0 = kt * FT;
       const bool diag = fd.causal && kt == qt;
       // P^T, then dS^T, packed to bf16: pk[j] holds keys 16 j + 4 g + 0..3
@@ -1116,13 +1148,13 @@ struct FusedBwdQ : BwdTile<D> {
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
           const bf16x8 qf = bfrag(OFF_Q, kk);
-          const char* sk = smem + (kk >> 1) * DK::BYTES;
+          const char* sk = sb + (kk >> 1) * DK::BYTES;
 #pragma unroll
           for (int j = 0; j < 8; ++j)
             s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(DK::frag(sk, 16 * j, (kk & 1) * 32, lane),
                                                            qf, s[j], 0, 0, 0);
           if (chk) {
-            const bf16_t* kcs = reinterpret_cast<const bf16_t*>(smem + OFF_KC);
+            const bf16_t* kcs = reinterpret_cast<const bf16_t*>(sb + OFF_KC);
             ks = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 *reinterpret_cast<const bf16x8*>(kcs + lq * SCL + 32 * kk + 8 * g), qf, ks, 0, 0, 0);
           }
@@ -1130,15 +1162,37 @@ struct FusedBwdQ : BwdTile<D> {
         if (fd.n_faults > 0) T::template inject<false>(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
         if (chk)
           T::template check<false>(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
+        // masked keys (diagonal tile only) enter the exponential as -inf
+        auto probs = [&](auto masked) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          float a[4];
+          for (int j = 0; j < 8; ++j) {
+            float a[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
-            a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][r] * sl2 - mq) * il)) : 0.f;
+            for (int r = 0; r < 4; ++r) {
+              const bool cut = masked && key0 + 16 * j + 4 * g + r > q;
+              a[r] = __builtin_amdgcn_exp2f(cut ? -INFINITY : s[j][r] * sl2 - mq) * il;
+            }
+            pk[j] = T::pack4v(a);
           }
-          pk[j] = T::pack4(a);
+        };
+        // (head dim 64: a copy without the mask for the other tiles; head
+        // dim 128: one copy, per element, as its registers allow)
+        if constexpr (D == 64) {
+          if (diag)
+            probs(std::true_type{});
+          else
+            probs(std::false_type{});
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            float a[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
+              a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][r] * sl2 - mq) * il)) : 0.f;
+            }
+            pk[j] = T::pack4(a);
+          }
         }
       }
       {
@@ -1149,13 +1203,13 @@ struct FusedBwdQ : BwdTile<D> {
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
           const bf16x8 gf = bfrag(OFF_G, kk);
-          const char* sv = smem + OFF_V + (kk >> 1) * DK::BYTES;
+          const char* sv = sb + OFF_V + (kk >> 1) * DK::BYTES;
 #pragma unroll
           for (int j = 0; j < 8; ++j)
             dp[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(DK::frag(sv, 16 * j, (kk & 1) * 32, lane),
                                                             gf, dp[j], 0, 0, 0);
           if (chk) {
-            const bf16_t* vcs = reinterpret_cast<const bf16_t*>(smem + OFF_VC);
+            const bf16_t* vcs = reinterpret_cast<const bf16_t*>(sb + OFF_VC);
             vs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 *reinterpret_cast<const bf16x8*>(vcs + lq * SCL + 32 * kk + 8 * g), gf, vs, 0, 0, 0);
           }
@@ -1164,31 +1218,58 @@ struct FusedBwdQ : BwdTile<D> {
         if (chk)
           T::template check<false>(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr,
                                    lane);
+        auto grads = [&](auto masked) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          float a[4], ds[4];
-          T::unpack4(pk[j], a);
+          for (int j = 0; j < 8; ++j) {
+            float a[4], ds[4];
+            T::unpack4(pk[j], a);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
-            ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][r] - dq))) : 0.f;
+            for (int r = 0; r < 4; ++r) {
+              const bool cut = masked && key0 + 16 * j + 4 * g + r > q;
+              ds[r] = cut ? 0.f : fd.scale * a[r] * (dp[j][r] - dq);
+            }
+            pk[j] = T::pack4v(ds);
           }
-          pk[j] = T::pack4(ds);
+        };
+        // (head dim 64: a copy without the mask for the other tiles; head
+        // dim 128: one copy, per element, as its registers allow)
+        if constexpr (D == 64) {
+          if (diag)
+            grads(std::true_type{});
+          else
+            grads(std::false_type{});
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            float a[4], ds[4];
+            T::unpack4(pk[j], a);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool live = !(diag && key0 + 16 * j + 4 * g + r > q);
+              ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][r] - dq))) : 0.f;
+            }
+            pk[j] = T::pack4(ds);
+          }
         }
       }
+      // the next tile's strips into the free stage
+      if (pre) commit(st ^ 1);
       // dQ^T += K^T dS^T and (dQ^r)^T += (K^r)^T dS^T
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const bf16x8 pf = T::slab(pk, t);
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-          dqa[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::t_frag(smem, 16 * db, 32 * t, lane),
+          dqa[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::t_frag(sb, 16 * db, 32 * t, lane),
                                                             pf, dqa[db], 0, 0, 0);
         if (chk)
           kra = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::rs_frag(krs, zeros, 32 * t, lane), pf,
                                                         kra, 0, 0, 0);
       }
-      __syncthreads();  // the one stage is reloaded next
+      if (NBUF == 2)
+        wait_vmcnt<0>();  // the next tile's copies
+      else
+        __syncthreads();  // the one stage is reloaded next
     }
 
     bf16_t* dQp = static_cast<bf16_t*>(fd.dqkv) + int64_t(b) * S * fd.ld + h * D;
@@ -1197,8 +1278,10 @@ struct FusedBwdQ : BwdTile<D> {
 };
 
 // The key pass. LDS: the workgroup's K and V images (loaded once); per
-// query tile the Q and dCL images, the Q^c and dCL^c strips, the Q^r and
-// dCL^r row-checksum strips and the queries' max, 1 / sum and D; scratch.
+// query tile a stage of the Q and dCL images, the Q^c and dCL^c strips,
+// the Q^r and dCL^r row-checksum strips and the queries' max, 1 / sum and D
+// (two stages at head dim 64: the next tile loads while this one is used);
+// scratch.
 // PART 0 forms dV and dK together; where both sets of accumulators do not
 // fit the registers of two waves per SIMD (head dim 128) the pass runs as
 // PART 1 (S, P, dV) then PART 2 (S, P, dP, dS, dK), each recomputing and
@@ -1209,12 +1292,16 @@ struct FusedBwdKV : BwdTile<D> {
   using T = BwdTile<D>;
   using typename T::DK;
   static constexpr int KS = T::KS, DB = T::DB, KH = T::KH, IMG = T::IMG, SCL = T::SCL;
-  static constexpr int OFF_V = IMG, OFF_Q = 2 * IMG, OFF_G = 3 * IMG;
-  static constexpr int OFF_QC = 4 * IMG, OFF_GC = OFF_QC + T::STRIP;
+  static constexpr int NBUF = D == 64 ? 2 : 1;
+  static constexpr int OFF_V = IMG, OFF_ST = 2 * IMG;
+  // offsets within a stage
+  static constexpr int OFF_Q = 0, OFF_G = IMG;
+  static constexpr int OFF_QC = 2 * IMG, OFF_GC = OFF_QC + T::STRIP;
   static constexpr int OFF_QR = OFF_GC + T::STRIP, OFF_GR = OFF_QR + T::RSTRIP;
-  static constexpr int OFF_ZERO = OFF_GR + T::RSTRIP;
-  static constexpr int OFF_ROW = OFF_ZERO + T::ZERO;           // [3][128] floats
-  static constexpr int OFF_SCR = OFF_ROW + 3 * FT * 4;
+  static constexpr int OFF_ROW = OFF_GR + T::RSTRIP;            // [3][128] floats
+  static constexpr int STAGE = T::align1k(OFF_ROW + 3 * FT * 4);
+  static constexpr int OFF_ZERO = OFF_ST + NBUF * STAGE;
+  static constexpr int OFF_SCR = OFF_ZERO + T::ZERO;
   static constexpr int LDS_BYTES = OFF_SCR + (BNT / 64) * T::SCR * 4;
   static_assert(LDS_BYTES <= 160 * 1024, "one workgroup fits the LDS");
 
@@ -1245,22 +1332,17 @@ struct FusedBwdKV : BwdTile<D> {
       DK::issue(Kp, ld, key0, S, hf * 64, smem + hf * DK::BYTES, wave, lane);
       DK::issue(Vp, ld, key0, S, hf * 64, smem + OFF_V + hf * DK::BYTES, wave, lane);
     }
-    bf16_t* qrs = reinterpret_cast<bf16_t*>(smem + OFF_QR);
-    bf16_t* grs = reinterpret_cast<bf16_t*>(smem + OFF_GR);
     const bf16_t* zeros = reinterpret_cast<const bf16_t*>(smem + OFF_ZERO);
     if (chk && tid < T::ZERO / 4) reinterpret_cast<uint32_t*>(smem + OFF_ZERO)[tid] = 0u;
-    float* rowf = reinterpret_cast<float*>(smem + OFF_ROW);
 
     float qcv[T::NSV], gcv[T::NSV];
     bf16x8 qrv[T::CPP], grv[T::CPP];
     float rv0 = 0.f, rv1 = 0.f;
-    auto issue = [&](int qt) {
+    // loads of query tile qt into stage st: the images by direct-to-LDS
+    // copies, the statistics' and strips' values into registers (written by
+    // commit)
+    auto issue_values = [&](int qt) {
       const int q0 = qt * FT;
-#pragma unroll
-      for (int hf = 0; hf < KH; ++hf) {
-        DK::issue(Qp, ld, q0, S, hf * 64, smem + OFF_Q + hf * DK::BYTES, wave, lane);
-        DK::issue(dCLp, H, q0, S, hf * 64, smem + OFF_G + hf * DK::BYTES, wave, lane);
-      }
       // threads 0..127: max and sum of query q0 + tid; 128..255: its D
       const int qi = q0 + (tid & (FT - 1));
       if (tid < FT) {
@@ -1277,7 +1359,18 @@ struct FusedBwdKV : BwdTile<D> {
         if (DO_V) T::rstrip_issue(dCLp, H, q0, S, tid, grv);
       }
     };
-    auto commit = [&]() {
+    auto issue_copies = [&](int qt, int st) {
+      const int q0 = qt * FT;
+      char* sb = smem + OFF_ST + st * STAGE;
+#pragma unroll
+      for (int hf = 0; hf < KH; ++hf) {
+        DK::issue(Qp, ld, q0, S, hf * 64, sb + OFF_Q + hf * DK::BYTES, wave, lane);
+        DK::issue(dCLp, H, q0, S, hf * 64, sb + OFF_G + hf * DK::BYTES, wave, lane);
+      }
+    };
+    auto commit = [&](int st) {
+      char* sb = smem + OFF_ST + st * STAGE;
+      float* rowf = reinterpret_cast<float*>(sb + OFF_ROW);
       if (tid < FT) {
         rowf[tid] = rv0;
         rowf[FT + tid] = 1.f / rv1;
@@ -1285,10 +1378,10 @@ struct FusedBwdKV : BwdTile<D> {
         rowf[2 * FT + tid - FT] = rv0;
       }
       if (chk) {
-        T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_QC), NB, tid, qcv);
-        T::strip_commit(reinterpret_cast<bf16_t*>(smem + OFF_GC), NB, tid, gcv);
-        if (DO_K) T::rstrip_commit(qrs, tid, qrv);
-        if (DO_V) T::rstrip_commit(grs, tid, grv);
+        T::strip_commit(reinterpret_cast<bf16_t*>(sb + OFF_QC), NB, tid, qcv);
+        T::strip_commit(reinterpret_cast<bf16_t*>(sb + OFF_GC), NB, tid, gcv);
+        if (DO_K) T::rstrip_commit(reinterpret_cast<bf16_t*>(sb + OFF_QR), tid, qrv);
+        if (DO_V) T::rstrip_commit(reinterpret_cast<bf16_t*>(sb + OFF_GR), tid, grv);
       }
     };
 
@@ -1301,18 +1394,35 @@ struct FusedBwdKV : BwdTile<D> {
     float* scr = reinterpret_cast<float*>(smem + OFF_SCR) + wave * T::SCR;
     // A operand fragments of the tile's queries (rows 16 j..) and the B
     // operand fragment of the wave's keys (rows of the K or V image)
-    auto afrag = [&](int off, int j, int kk) {
-      return DK::frag(smem + off + (kk >> 1) * DK::BYTES, 16 * j, (kk & 1) * 32, lane);
+    auto afrag = [&](const char* img, int j, int kk) {
+      return DK::frag(img + (kk >> 1) * DK::BYTES, 16 * j, (kk & 1) * 32, lane);
     };
     auto kfrag = [&](int off, int kk) {
       return DK::frag(smem + off + (kk >> 1) * DK::BYTES, wave * 16, (kk & 1) * 32, lane);
     };
 
-    for (int qt = qt0; qt < nqt; ++qt) {
-      issue(qt);
+    if (NBUF == 2) {
+      issue_values(qt0);
+      issue_copies(qt0, 0);
       wait_vmcnt<0>();
-      commit();
-      __syncthreads();  // query tile qt in LDS
+      commit(0);
+    }
+    for (int qt = qt0; qt < nqt; ++qt) {
+      const int st = NBUF == 2 ? ((qt - qt0) & 1) : 0;
+      if (NBUF == 1) {
+        issue_values(qt);
+        issue_copies(qt, 0);
+        wait_vmcnt<0>();
+        commit(0);
+      }
+      // query tile qt in LDS (double-buffered: the other stage is free)
+      __syncthreads();
+      const bool pre = NBUF == 2 && qt + 1 < nqt;
+      if (pre) issue_copies(qt + 1, st ^ 1);
+      const char* sb = smem + OFF_ST + st * STAGE;
+      const float* rowf = reinterpret_cast<const float*>(sb + OFF_ROW);
+      const bf16_t* qrs = reinterpret_cast<const bf16_t*>(sb + OFF_QR);
+      const bf16_t* grs = reinterpret_cast<const bf16_t*>(sb + OFF_GR);
       const int q0 = qt * FT;
       const bool diag = fd.causal && qt == kt;
       // P, then dS, packed to bf16: pk[j] holds queries 16 j + 4 g + 0..3
@@ -1327,9 +1437,9 @@ struct FusedBwdKV : BwdTile<D> {
           const bf16x8 kf = kfrag(0, kk);
 #pragma unroll
           for (int j = 0; j < 8; ++j)
-            s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag(OFF_Q, j, kk), kf, s[j], 0, 0, 0);
+            s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag(sb + OFF_Q, j, kk), kf, s[j], 0, 0, 0);
           if (chk) {
-            const bf16_t* qcs = reinterpret_cast<const bf16_t*>(smem + OFF_QC);
+            const bf16_t* qcs = reinterpret_cast<const bf16_t*>(sb + OFF_QC);
             cs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 *reinterpret_cast<const bf16x8*>(qcs + lq * SCL + 32 * kk + 8 * g), kf, cs, 0, 0, 0);
           }
@@ -1337,20 +1447,47 @@ struct FusedBwdKV : BwdTile<D> {
         if (DO_K && fd.n_faults > 0) T::template inject<true>(s, fd, ABFT_OP_AS, b, h, kw, q0, lane);
         if (chk)
           T::template check<true>(s, cs, fd, ABFT_OP_AS, b, h, kw, q0, Kp, Qp, ld, ld, scr, lane);
+        // masked queries (diagonal tile only) enter the exponential as -inf
+        auto probs = [&](auto masked) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float4 m4 = *reinterpret_cast<const float4*>(rowf + 16 * j + 4 * g);
-          const float4 i4 = *reinterpret_cast<const float4*>(rowf + FT + 16 * j + 4 * g);
-          const float mv[4] = {m4.x, m4.y, m4.z, m4.w}, iv[4] = {i4.x, i4.y, i4.z, i4.w};
-          float a[4];
+          for (int j = 0; j < 8; ++j) {
+            const float4 m4 = *reinterpret_cast<const float4*>(rowf + 16 * j + 4 * g);
+            const float4 i4 = *reinterpret_cast<const float4*>(rowf + FT + 16 * j + 4 * g);
+            const float mv[4] = {m4.x, m4.y, m4.z, m4.w}, iv[4] = {i4.x, i4.y, i4.z, i4.w};
+            float a[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
-            a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][r] * sl2 - mv[r]) * iv[r])) : 0.f;
+            for (int r = 0; r < 4; ++r) {
+              const bool cut = masked && key > q0 + 16 * j + 4 * g + r;
+              a[r] = __builtin_amdgcn_exp2f(cut ? -INFINITY : s[j][r] * sl2 - mv[r]) * iv[r];
+            }
+            pk[j] = T::pack4v(a);
           }
-          pk[j] = T::pack4(a);
+        };
+        // (head dim 64: a copy without the mask for the other tiles; head
+        // dim 128: one copy, per element, as its registers allow)
+        if constexpr (D == 64) {
+          if (diag)
+            probs(std::true_type{});
+          else
+            probs(std::false_type{});
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float4 m4 = *reinterpret_cast<const float4*>(rowf + 16 * j + 4 * g);
+            const float4 i4 = *reinterpret_cast<const float4*>(rowf + FT + 16 * j + 4 * g);
+            const float mv[4] = {m4.x, m4.y, m4.z, m4.w}, iv[4] = {i4.x, i4.y, i4.z, i4.w};
+            float a[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
+              a[r] = live ? bf2f(f2bf(__builtin_amdgcn_exp2f(s[j][r] * sl2 - mv[r]) * iv[r])) : 0.f;
+            }
+            pk[j] = T::pack4(a);
+          }
         }
       }
+      // the next tile's values, written to the free stage at the end
+      if (pre) issue_values(qt + 1);
       // dV^T += dCL^T P and (dV^r)^T += (dCL^r)^T P
 #pragma unroll
       for (int t = 0; t < 4 && DO_V; ++t) {
@@ -1358,7 +1495,7 @@ struct FusedBwdKV : BwdTile<D> {
 #pragma unroll
         for (int db = 0; db < DB; ++db)
           dva[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              T::t_frag(smem + OFF_G, 16 * db, 32 * t, lane), pf, dva[db], 0, 0, 0);
+              T::t_frag(sb + OFF_G, 16 * db, 32 * t, lane), pf, dva[db], 0, 0, 0);
         if (chk)
           vra = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::rs_frag(grs, zeros, 32 * t, lane), pf,
                                                         vra, 0, 0, 0);
@@ -1373,9 +1510,9 @@ struct FusedBwdKV : BwdTile<D> {
           const bf16x8 vf = kfrag(OFF_V, kk);
 #pragma unroll
           for (int j = 0; j < 8; ++j)
-            dp[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag(OFF_G, j, kk), vf, dp[j], 0, 0, 0);
+            dp[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag(sb + OFF_G, j, kk), vf, dp[j], 0, 0, 0);
           if (chk) {
-            const bf16_t* gcs = reinterpret_cast<const bf16_t*>(smem + OFF_GC);
+            const bf16_t* gcs = reinterpret_cast<const bf16_t*>(sb + OFF_GC);
             cs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 *reinterpret_cast<const bf16x8*>(gcs + lq * SCL + 32 * kk + 8 * g), vf, cs, 0, 0, 0);
           }
@@ -1384,18 +1521,42 @@ struct FusedBwdKV : BwdTile<D> {
         if (chk)
           T::template check<true>(dp, cs, fd, ABFT_OP_DAP, b, h, kw, q0, Vp, dCLp, ld, H, scr,
                                   lane);
+        auto grads = [&](auto masked) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float4 d4 = *reinterpret_cast<const float4*>(rowf + 2 * FT + 16 * j + 4 * g);
-          const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
-          float a[4], ds[4];
-          T::unpack4(pk[j], a);
+          for (int j = 0; j < 8; ++j) {
+            const float4 d4 = *reinterpret_cast<const float4*>(rowf + 2 * FT + 16 * j + 4 * g);
+            const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+            float a[4], ds[4];
+            T::unpack4(pk[j], a);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
-            ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][r] - dv[r]))) : 0.f;
+            for (int r = 0; r < 4; ++r) {
+              const bool cut = masked && key > q0 + 16 * j + 4 * g + r;
+              ds[r] = cut ? 0.f : fd.scale * a[r] * (dp[j][r] - dv[r]);
+            }
+            pk[j] = T::pack4v(ds);
           }
-          pk[j] = T::pack4(ds);
+        };
+        // (head dim 64: a copy without the mask for the other tiles; head
+        // dim 128: one copy, per element, as its registers allow)
+        if constexpr (D == 64) {
+          if (diag)
+            grads(std::true_type{});
+          else
+            grads(std::false_type{});
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float4 d4 = *reinterpret_cast<const float4*>(rowf + 2 * FT + 16 * j + 4 * g);
+            const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+            float a[4], ds[4];
+            T::unpack4(pk[j], a);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool live = !(diag && key > q0 + 16 * j + 4 * g + r);
+              ds[r] = live ? bf2f(f2bf(fd.scale * a[r] * (dp[j][r] - dv[r]))) : 0.f;
+            }
+            pk[j] = T::pack4(ds);
+          }
         }
       }
       // dK^T += Q^T dS and (dK^r)^T += (Q^r)^T dS
@@ -1405,12 +1566,17 @@ struct FusedBwdKV : BwdTile<D> {
 #pragma unroll
         for (int db = 0; db < DB; ++db)
           dka[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              T::t_frag(smem + OFF_Q, 16 * db, 32 * t, lane), pf, dka[db], 0, 0, 0);
+              T::t_frag(sb + OFF_Q, 16 * db, 32 * t, lane), pf, dka[db], 0, 0, 0);
         if (chk)
           kra = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T::rs_frag(qrs, zeros, 32 * t, lane), pf,
                                                         kra, 0, 0, 0);
       }
-      __syncthreads();  // the query tile's buffers are reloaded next
+      if (NBUF == 2) {
+        if (pre) commit(st ^ 1);  // the next tile's values into the free stage
+        wait_vmcnt<0>();          // and its copies
+      } else {
+        __syncthreads();  // the one stage is reloaded next
+      }
     }
 
     bf16_t* outp = static_cast<bf16_t*>(fd.dqkv) + int64_t(b) * S * fd.ld + h * D;
