@@ -416,22 +416,29 @@ struct FusedAttn {
         }
       }
 
-      // online softmax, then O^T += V^T P^T (and the V^r rows)
-      const bool diag = arg->causal && kt == qt;
+      // online softmax, then O^T += V^T P^T (and the V^r rows). The
+      // running max is kept in the log2-scaled domain; the tile's max is
+      // taken over the raw scores and scaled once (the scale is positive,
+      // so the result is the same), and each probability is exp2 of one
+      // fused multiply-add.
+      if (arg->causal && kt == qt) {
+        // the diagonal tile's masked scores
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (key0 + 16 * j + 4 * g + r > qw + 16 * qb + lq) s[j][qb][r] = -INFINITY;
+      }
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        const int q = qw + 16 * qb + lq;
         float mx = -INFINITY;
 #pragma unroll
         for (int j = 0; j < 8; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float x = s[j][qb][r] * sl2;
-            if (diag && key0 + 16 * j + 4 * g + r > q) x = -INFINITY;
-            s[j][qb][r] = x;
-            mx = fmaxf(mx, x);
-          }
-        mx = xmax32(xmax16(mx));
+          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[j][qb][r]);
+        mx = xmax32(xmax16(mx)) * sl2;
         const float mn = fmaxf(m[qb], mx);
         const float alpha = __builtin_amdgcn_exp2f(m[qb] - mn);
         m[qb] = mn;
@@ -440,7 +447,7 @@ struct FusedAttn {
         for (int j = 0; j < 8; ++j)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = __builtin_amdgcn_exp2f(s[j][qb][r] - mn);
+            const float p = __builtin_amdgcn_exp2f(fmaf(s[j][qb][r], sl2, -mn));
             s[j][qb][r] = p;
             ls += p;
           }
@@ -458,10 +465,10 @@ struct FusedAttn {
         bf16x8 pf[2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-          const uint4 u = {pack2(s[2 * t][qb][0], s[2 * t][qb][1]),
-                           pack2(s[2 * t][qb][2], s[2 * t][qb][3]),
-                           pack2(s[2 * t + 1][qb][0], s[2 * t + 1][qb][1]),
-                           pack2(s[2 * t + 1][qb][2], s[2 * t + 1][qb][3])};
+          const uint4 u = {pack2v(s[2 * t][qb][0], s[2 * t][qb][1]),
+                           pack2v(s[2 * t][qb][2], s[2 * t][qb][3]),
+                           pack2v(s[2 * t + 1][qb][0], s[2 * t + 1][qb][1]),
+                           pack2v(s[2 * t + 1][qb][2], s[2 * t + 1][qb][3])};
           pf[qb] = __builtin_bit_cast(bf16x8, u);
         }
         const bool with_vr = PROT && arg->vr != nullptr;
