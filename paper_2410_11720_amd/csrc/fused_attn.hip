@@ -1063,7 +1063,7 @@ struct FusedBwdQ : BwdTile<D> {
 
     // the statistics and the softmax backward's row term D = dCL . CL of
     // the lane's query (D also kept for the key pass)
-    float mq, il, dq;
+    float mq, il, ml, dq;
     {
       float acc = 0.f;
 #pragma unroll
@@ -1077,6 +1077,7 @@ struct FusedBwdQ : BwdTile<D> {
       const float* st = fd.stats + ((int64_t(b) * fd.nh + h) * S + q) * 2;
       mq = st[0];
       il = 1.f / st[1];
+      ml = mq + __log2f(st[1]);  // P = exp2(scaled score - ml)
       if (g == 0) fd.drow[(int64_t(b) * fd.nh + h) * S + q] = dq;
     }
     // Q and dCL images of the workgroup's queries (complete with tile 0)
@@ -1177,7 +1178,7 @@ struct FusedBwdQ : BwdTile<D> {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const bool cut = masked && key0 + 16 * j + 4 * g + r > q;
-              a[r] = __builtin_amdgcn_exp2f(cut ? -INFINITY : s[j][r] * sl2 - mq) * il;
+              a[r] = __builtin_amdgcn_exp2f(cut ? -INFINITY : s[j][r] * sl2 - ml);
             }
             pk[j] = T::pack4v(a);
           }
@@ -1379,7 +1380,9 @@ struct FusedBwdKV : BwdTile<D> {
       char* sb = smem + OFF_ST + st * STAGE;
       float* rowf = reinterpret_cast<float*>(sb + OFF_ROW);
       if (tid < FT) {
-        rowf[tid] = rv0;
+        // head dim 64: max + log2(sum), so that P = exp2(scaled score -
+        // that); 128: the max and 1 / sum
+        rowf[tid] = D == 64 ? rv0 + __log2f(rv1) : rv0;
         rowf[FT + tid] = 1.f / rv1;
       } else if (tid < 2 * FT) {
         rowf[2 * FT + tid - FT] = rv0;
@@ -1459,13 +1462,12 @@ struct FusedBwdKV : BwdTile<D> {
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const float4 m4 = *reinterpret_cast<const float4*>(rowf + 16 * j + 4 * g);
-            const float4 i4 = *reinterpret_cast<const float4*>(rowf + FT + 16 * j + 4 * g);
-            const float mv[4] = {m4.x, m4.y, m4.z, m4.w}, iv[4] = {i4.x, i4.y, i4.z, i4.w};
+            const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
             float a[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const bool cut = masked && key > q0 + 16 * j + 4 * g + r;
-              a[r] = __builtin_amdgcn_exp2f(cut ? -INFINITY : s[j][r] * sl2 - mv[r]) * iv[r];
+              a[r] = __builtin_amdgcn_exp2f(cut ? -INFINITY : s[j][r] * sl2 - mv[r]);
             }
             pk[j] = T::pack4v(a);
           }
