@@ -80,23 +80,31 @@ template <class T>
 __device__ EecResult eec_locate(const T* v, int stride, int n, float c1, float c2, float e_rel,
                                 float tn) {
   float r1 = 0.f, r2 = 0.f, sa = 0.f;
+  // (unrolled: the loads of a rare path go out together instead of one
+  // memory latency each)
+#pragma unroll 8
   for (int k = 0; k < n; ++k) {
     const float x = Storage<T>::load(v[k * stride]);
     r1 += x;
     r2 += float(k + 1) * x;
-    if (is_finite(x)) sa += fabsf(x);
+    sa += is_finite(x) ? fabsf(x) : 0.f;
   }
   const float d1 = c1 - r1, d2 = c2 - r2;
   EecResult res{EEC_CLEAN, -1, d1};
   if (!flagged(d1, sa, e_rel)) return res;
   const int mode = is_finite(d1) ? 1 : (is_inf(d1) ? 2 : 3);
+  // candidates counted with selects (straight-line code: a branch per
+  // element turns the unrolled loop into nested divergent loops)
+  const bool any_inf = mode == 2, any_nonfin = mode == 3;
   int cnt = 0, idx = -1;
+#pragma unroll 8
   for (int k = 0; k < n; ++k) {
     const float x = Storage<T>::load(v[k * stride]);
     const bool fin = is_finite(x);
     const bool nearv = fin && fabsf(x) >= tn;
-    const bool cand = mode == 1 ? nearv : (mode == 2 ? (is_inf(x) || nearv) : (!fin || nearv));
-    if (cand) { ++cnt; idx = k; }
+    const bool cand = nearv || (any_inf && is_inf(x)) || (any_nonfin && !fin);
+    cnt += cand ? 1 : 0;
+    idx = cand ? k : idx;
   }
   res.status = EEC_PROPAGATED;
   if (cnt >= 2) return res;
@@ -136,8 +144,11 @@ __device__ float fix_by_checksum(const T* v, int stride, int n, int i, float c1,
     return Storage<T>::load(v[i * stride]) + d1;
   }
   float s = 0.f;
-  for (int k = 0; k < n; ++k)
-    if (k != i) s += Storage<T>::load(v[k * stride]);
+#pragma unroll 8
+  for (int k = 0; k < n; ++k) {
+    const float x = Storage<T>::load(v[k * stride]);
+    s += k != i ? x : 0.f;
+  }
   *action = ABFT_ACT_RECONSTRUCT;
   return c1 - s;
 }
@@ -146,6 +157,7 @@ __device__ float fix_by_checksum(const T* v, int stride, int n, int i, float c1,
 template <class T>
 __device__ void vec_checksums(const T* v, int stride, int n, float* c1, float* c2) {
   float r1 = 0.f, r2 = 0.f;
+#pragma unroll 8
   for (int k = 0; k < n; ++k) {
     const float x = Storage<T>::load(v[k * stride]);
     r1 += x;

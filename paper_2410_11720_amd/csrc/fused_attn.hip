@@ -111,6 +111,77 @@ struct ArgRef<Desc, true> {
 };
 #endif
 
+// Fixing a flagged score vector gathered in scr[0..n) (Sec. 4.2), in up to
+// three steps. score_locate (lane 0) locates by EEC; a located element is
+// fixed from the checksums unless recompute is set, the event recorded at
+// (row, col) when tr, else (col, row), and an unfixable vector reported;
+// scr[n] takes the located index (or -1), scr[n + 1] the new value. With
+// recompute, a located element is left to the wave: score_dot forms the
+// dot product of row `col` of A and row `rowbase + index` of Bm (length
+// d <= 128) across the lanes, then score_close (lane 0) stores it, records
+// the event and reports a vector that is still flagged.
+__device__ __noinline__ void score_locate(float* scr, int n, float v1, float v2, float e_rel,
+                                          float tn, float tc, int recompute, abft_report* report,
+                                          int op, int b, int h, int col, int rowbase, bool tr) {
+  const EecResult res = eec_locate<float>(scr, 1, n, v1, v2, e_rel, tn);
+  int idx = -1;
+  float nv = 0.f;
+  if (res.status == EEC_LOCATED) {
+    idx = res.index;
+    if (recompute) {  // the rest after score_dot
+      scr[n] = __int_as_float(idx);
+      scr[n + 1] = scr[idx];
+      return;
+    }
+    const int row = rowbase + idx;
+    const float old = scr[idx];
+    int action = ABFT_ACT_RECOMPUTE;
+    nv = fix_by_checksum<float>(scr, 1, n, idx, v1, res.d1, tc, &action);
+    scr[idx] = nv;
+    record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn), action, old);
+  }
+  if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, n, v1, e_rel))
+    record_event(report, op, b, h, tr ? rowbase : col, tr ? col : rowbase, ABFT_KIND_NONE,
+                 ABFT_ACT_UNCORRECTABLE, 0.f);
+  scr[n] = __int_as_float(idx);
+  scr[n + 1] = nv;
+}
+__device__ __noinline__ float score_dot(const bf16_t* A, const bf16_t* Bm, int64_t lda,
+                                           int64_t ldb, int col, int row, int d, int lane) {
+  float acc = 0.f;
+  for (int dd = lane; dd < d; dd += 64)
+    acc = fmaf(bf2f(A[int64_t(col) * lda + dd]), bf2f(Bm[int64_t(row) * ldb + dd]), acc);
+  return group_sum<64>(acc);
+}
+__device__ __noinline__ void score_close(float* scr, int n, float nv, float v1, float e_rel,
+                                         float tn, abft_report* report, int op, int b, int h,
+                                         int col, int rowbase, bool tr) {
+  const int idx = __float_as_int(scr[n]);
+  const int row = rowbase + idx;
+  const float old = scr[idx];
+  scr[idx] = nv;
+  record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn),
+               ABFT_ACT_RECOMPUTE, old);
+  if (vec_flagged<float>(scr, 1, n, v1, e_rel))
+    record_event(report, op, b, h, tr ? rowbase : col, tr ? col : rowbase, ABFT_KIND_NONE,
+                 ABFT_ACT_UNCORRECTABLE, 0.f);
+  scr[n + 1] = nv;
+}
+
+// Whether an injected fault (test-only) of an op in mask targets head
+// (b, h) of a batch element: read once per workgroup, so that the
+// workgroups no fault reaches skip the per-tile injection code (each of its
+// passes reads the fault list from memory).
+__device__ __forceinline__ bool faults_at(const abft_fault* f, int n, int b, int h,
+                                          uint32_t mask) {
+  bool any = false;
+  for (int i = 0; i < n; ++i) {
+    const abft_fault ft = f[i];
+    any |= ft.op >= 0 && ft.op < 32 && ((mask >> ft.op) & 1u) && ft.b == b && ft.h == h;
+  }
+  return any;
+}
+
 template <int D, bool PROT>
 struct FusedAttn {
   static constexpr int NSTAGE = D == 64 ? 2 : 1;
@@ -175,6 +246,9 @@ struct FusedAttn {
     const int R = arg->R, NB = FT / R;                  // checksum blocks per key tile
     const int lg_jpb = __builtin_ctz(R / 16);         // 16-key groups per block (log2)
     const float sl2 = arg->scale * 1.4426950408889634f;
+    const bool wf = arg->n_faults > 0 &&
+                    faults_at(arg->faults, arg->n_faults, b, h,
+                              (1u << ABFT_OP_AS) | (1u << ABFT_OP_CL));
 
     // Q as the B operand of S^T: query qw + 16 qb + lane % 16, dims 32 kk + 8 g..
     bf16x8 qf[2][KS];
@@ -303,7 +377,7 @@ struct FusedAttn {
       }
 
       // injected score faults (test-only), on the unrounded scores
-      if (arg->n_faults > 0) {
+      if (wf) {
         for (int f = 0; f < arg->n_faults; ++f) {
           const abft_fault ft = arg->faults[f];
           if (ft.op != ABFT_OP_AS || ft.b != b || ft.h != h) continue;
@@ -370,33 +444,17 @@ struct FusedAttn {
               const float v1 = __shfl(ks[qb][0] + ks[qb][1], L, 64);
               const float v2 = __shfl(ks[qb][2] + ks[qb][3], L, 64);
               wave_sync_lds();
-              if (lane == 0) {
-                const int q = qw + 16 * qb + vq;
-                const EecResult res = eec_locate<float>(scr, 1, R, v1, v2, arg->e_rel, arg->tn_s);
-                int idx = -1;
-                float nv = 0.f;
-                if (res.status == EEC_LOCATED) {
-                  idx = res.index;
-                  const int key = key0 + vb * R + idx;
-                  const float old = scr[idx];
-                  int action = ABFT_ACT_RECOMPUTE;
-                  if (arg->recompute) {
-                    float acc = 0.f;
-                    for (int dd = 0; dd < D; ++dd)
-                      acc = fmaf(bf2f(Qp[int64_t(q) * ld + dd]), bf2f(Kp[int64_t(key) * ld + dd]), acc);
-                    nv = acc;
-                  } else {
-                    nv = fix_by_checksum<float>(scr, 1, R, idx, v1, res.d1, arg->tc, &action);
-                  }
-                  scr[idx] = nv;
-                  record_event(arg->report, ABFT_OP_AS, b, h, q, key, classify(old, arg->tn_s), action,
-                               old);
-                }
-                if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, R, v1, arg->e_rel))
-                  record_event(arg->report, ABFT_OP_AS, b, h, q, key0 + vb * R, ABFT_KIND_NONE,
-                               ABFT_ACT_UNCORRECTABLE, 0.f);
-                scr[R] = __int_as_float(idx);
-                scr[R + 1] = nv;
+              if (lane == 0)
+                score_locate(scr, R, v1, v2, arg->e_rel, arg->tn_s, arg->tc, arg->recompute,
+                             arg->report, ABFT_OP_AS, b, h, qw + 16 * qb + vq, key0 + vb * R,
+                             false);
+              wave_sync_lds();
+              if (arg->recompute && __float_as_int(scr[R]) >= 0) {
+                const float nv = score_dot(Qp, Kp, ld, ld, qw + 16 * qb + vq,
+                                           key0 + vb * R + __float_as_int(scr[R]), D, lane);
+                if (lane == 0)
+                  score_close(scr, R, nv, v1, arg->e_rel, arg->tn_s, arg->report, ABFT_OP_AS, b,
+                              h, qw + 16 * qb + vq, key0 + vb * R, false);
               }
               wave_sync_lds();
               const int idx = __float_as_int(scr[R]);
@@ -532,7 +590,7 @@ struct FusedAttn {
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int r = 0; r < 4; ++r) ov[db][r] = bf2f(f2bf(o[db][qb][r] * inv));
-      if (arg->n_faults > 0) {
+      if (wf) {
         for (int f = 0; f < arg->n_faults; ++f) {
           const abft_fault ft = arg->faults[f];
           if (ft.op != ABFT_OP_CL || ft.b != b || ft.h != h || ft.row != q) continue;
@@ -640,42 +698,6 @@ struct FusedAttn {
 // work of the checks runs out of line (it is rare and would otherwise hold
 // registers across the loops).
 
-// Lane 0's part of fixing a flagged score vector gathered in scr[0..n):
-// locate by EEC (Sec. 4.2), recompute the element as the dot product of row
-// `col` of A and row `row` of Bm (length d) or fix it from the checksums,
-// record the event at (row, col) when tr, else (col, row); the located
-// index (or -1) and the new value go to scr[n], scr[n + 1].
-__device__ __noinline__ void score_fix(float* scr, int n, float v1, float v2, float e_rel,
-                                       float tn, float tc, int recompute, abft_report* report,
-                                       int op, int b, int h, int col, int rowbase, bool tr,
-                                       const bf16_t* A, const bf16_t* Bm, int64_t lda,
-                                       int64_t ldb, int d) {
-  const EecResult res = eec_locate<float>(scr, 1, n, v1, v2, e_rel, tn);
-  int idx = -1;
-  float nv = 0.f;
-  if (res.status == EEC_LOCATED) {
-    idx = res.index;
-    const int row = rowbase + idx;
-    const float old = scr[idx];
-    int action = ABFT_ACT_RECOMPUTE;
-    if (recompute) {
-      float acc = 0.f;
-      for (int dd = 0; dd < d; ++dd)
-        acc = fmaf(bf2f(A[int64_t(col) * lda + dd]), bf2f(Bm[int64_t(row) * ldb + dd]), acc);
-      nv = acc;
-    } else {
-      nv = fix_by_checksum<float>(scr, 1, n, idx, v1, res.d1, tc, &action);
-    }
-    scr[idx] = nv;
-    record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn), action, old);
-  }
-  if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, n, v1, e_rel))
-    record_event(report, op, b, h, tr ? rowbase : col, tr ? col : rowbase, ABFT_KIND_NONE,
-                 ABFT_ACT_UNCORRECTABLE, 0.f);
-  scr[n] = __int_as_float(idx);
-  scr[n + 1] = nv;
-}
-
 // The same for a flagged gradient row of length n (entity e): fixed from
 // the checksums, rounded to storage.
 __device__ __noinline__ void grad_fix(float* scr, int n, float v1, float v2, float e_rel, float tn,
@@ -762,7 +784,7 @@ struct BwdTile {
 
   // Check of a score tile per (column, R-row block) against the strip
   // result cs (rows 4b..4b+3 of lane group b: hi/lo of c1, c2); columns are
-  // entities cbase + 0..15, rows rbase + 0..127 (see score_fix for A, Bm
+  // entities cbase + 0..15, rows rbase + 0..127 (see score_locate for A, Bm
   // and tr). A flagged vector is gathered into the wave's scratch and fixed
   // by lane 0; the fixed element is put back into the tile.
   template <bool TR>
@@ -838,9 +860,17 @@ struct BwdTile {
       const float v2 = __shfl(cs[2] + cs[3], L, 64);
       wave_sync_lds();
       if (lane == 0)
-        score_fix(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute, fd.report, op, b, h,
-                  cbase + vq, rbase + vb * R, TR, A, Bm, lda, ldb, D);
+        score_locate(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute, fd.report, op, b, h,
+                     cbase + vq, rbase + vb * R, TR);
       wave_sync_lds();
+      if (fd.recompute && __float_as_int(scr[R]) >= 0) {
+        const float nv = score_dot(A, Bm, lda, ldb, cbase + vq, rbase + vb * R +
+                                   __float_as_int(scr[R]), D, lane);
+        if (lane == 0)
+          score_close(scr, R, nv, v1, fd.e_rel, fd.tn_s, fd.report, op, b, h, cbase + vq,
+                      rbase + vb * R, TR);
+        wave_sync_lds();
+      }
       const int idx = __float_as_int(scr[R]);
       const float nv = scr[R + 1];
       if (idx >= 0) {
@@ -883,7 +913,7 @@ struct BwdTile {
   // of op injected, each entity's row checked (a located element fixed
   // from the checksum, Sec. 4.2) and stored at out + entity * ld.
   __device__ static void finish(floatx4 (&acc)[DB], const floatx4& chk, const FusedBwdDesc& fd,
-                                bool check, int op, int b, int h, int cbase, bf16_t* out,
+                                bool check, bool wf, int op, int b, int h, int cbase, bf16_t* out,
                                 int64_t ld, float* scr, int lane) {
     const int lq = lane & 15, g = lane >> 4;
     {
@@ -893,7 +923,7 @@ struct BwdTile {
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int r = 0; r < 4; ++r) ov[db][r] = bf2f(f2bf(acc[db][r]));
-      if (fd.n_faults > 0) {
+      if (wf) {
         for (int f = 0; f < fd.n_faults; ++f) {
           const abft_fault ft = fd.faults[f];
           if (ft.op != op || ft.b != b || ft.h != h || ft.row != e) continue;
@@ -1060,6 +1090,9 @@ struct FusedBwdQ : BwdTile<D> {
     const int nkt = fd.causal ? qt + 1 : nqt;
     const float sl2 = fd.scale * 1.4426950408889634f;
     constexpr bool chk = CHK;
+    const bool wf = fd.n_faults > 0 &&
+                    faults_at(fd.faults, fd.n_faults, b, h,
+                              (1u << ABFT_OP_AS) | (1u << ABFT_OP_DAP) | (1u << ABFT_OP_DQ));
 
     // the statistics and the softmax backward's row term D = dCL . CL of
     // the lane's query (D also kept for the key pass)
@@ -1167,7 +1200,7 @@ struct FusedBwdQ : BwdTile<D> {
                 *reinterpret_cast<const bf16x8*>(kcs + lq * SCL + 32 * kk + 8 * g), qf, ks, 0, 0, 0);
           }
         }
-        if (fd.n_faults > 0) T::template inject<false>(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
+        if (wf) T::template inject<false>(s, fd, ABFT_OP_AS, b, h, qw, key0, lane);
         if (chk)
           T::template check<false>(s, ks, fd, ABFT_OP_AS, b, h, qw, key0, Qp, Kp, ld, ld, scr, lane);
         // masked keys (diagonal tile only) enter the exponential as -inf
@@ -1222,7 +1255,7 @@ struct FusedBwdQ : BwdTile<D> {
                 *reinterpret_cast<const bf16x8*>(vcs + lq * SCL + 32 * kk + 8 * g), gf, vs, 0, 0, 0);
           }
         }
-        if (fd.n_faults > 0) T::template inject<false>(dp, fd, ABFT_OP_DAP, b, h, qw, key0, lane);
+        if (wf) T::template inject<false>(dp, fd, ABFT_OP_DAP, b, h, qw, key0, lane);
         if (chk)
           T::template check<false>(dp, vs, fd, ABFT_OP_DAP, b, h, qw, key0, dCLp, Vp, H, ld, scr,
                                    lane);
@@ -1281,7 +1314,7 @@ struct FusedBwdQ : BwdTile<D> {
     }
 
     bf16_t* dQp = static_cast<bf16_t*>(fd.dqkv) + int64_t(b) * S * fd.ld + h * D;
-    T::finish(dqa, kra, fd, chk, ABFT_OP_DQ, b, h, qw, dQp, fd.ld, scr, lane);
+    T::finish(dqa, kra, fd, chk, wf, ABFT_OP_DQ, b, h, qw, dQp, fd.ld, scr, lane);
   }
 };
 
@@ -1333,6 +1366,10 @@ struct FusedBwdKV : BwdTile<D> {
     constexpr bool chk = CHK;
     const int64_t bh = int64_t(b) * fd.nh + h;
     constexpr bool DO_V = PART != 2, DO_K = PART != 1;
+    const bool wf = fd.n_faults > 0 &&
+                    faults_at(fd.faults, fd.n_faults, b, h,
+                              (1u << ABFT_OP_AS) | (1u << ABFT_OP_DAP) | (1u << ABFT_OP_DK) |
+                                  (1u << ABFT_OP_DV));
 
     // K and V images of the workgroup's keys (complete with the first tile)
 #pragma unroll
@@ -1454,7 +1491,7 @@ struct FusedBwdKV : BwdTile<D> {
                 *reinterpret_cast<const bf16x8*>(qcs + lq * SCL + 32 * kk + 8 * g), kf, cs, 0, 0, 0);
           }
         }
-        if (DO_K && fd.n_faults > 0) T::template inject<true>(s, fd, ABFT_OP_AS, b, h, kw, q0, lane);
+        if (DO_K && wf) T::template inject<true>(s, fd, ABFT_OP_AS, b, h, kw, q0, lane);
         if (chk)
           T::template check<true>(s, cs, fd, ABFT_OP_AS, b, h, kw, q0, Kp, Qp, ld, ld, scr, lane);
         // masked queries (diagonal tile only) enter the exponential as -inf
@@ -1526,7 +1563,7 @@ struct FusedBwdKV : BwdTile<D> {
                 *reinterpret_cast<const bf16x8*>(gcs + lq * SCL + 32 * kk + 8 * g), vf, cs, 0, 0, 0);
           }
         }
-        if (fd.n_faults > 0) T::template inject<true>(dp, fd, ABFT_OP_DAP, b, h, kw, q0, lane);
+        if (wf) T::template inject<true>(dp, fd, ABFT_OP_DAP, b, h, kw, q0, lane);
         if (chk)
           T::template check<true>(dp, cs, fd, ABFT_OP_DAP, b, h, kw, q0, Vp, dCLp, ld, H, scr,
                                   lane);
@@ -1589,8 +1626,9 @@ struct FusedBwdKV : BwdTile<D> {
     }
 
     bf16_t* outp = static_cast<bf16_t*>(fd.dqkv) + int64_t(b) * S * fd.ld + h * D;
-    if (DO_K) T::finish(dka, kra, fd, chk, ABFT_OP_DK, b, h, kw, outp + H, fd.ld, scr, lane);
-    if (DO_V) T::finish(dva, vra, fd, chk, ABFT_OP_DV, b, h, kw, outp + 2 * H, fd.ld, scr, lane);
+    if (DO_K) T::finish(dka, kra, fd, chk, wf, ABFT_OP_DK, b, h, kw, outp + H, fd.ld, scr, lane);
+    if (DO_V)
+      T::finish(dva, vra, fd, chk, wf, ABFT_OP_DV, b, h, kw, outp + 2 * H, fd.ld, scr, lane);
   }
 };
 

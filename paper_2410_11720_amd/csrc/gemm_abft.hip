@@ -271,6 +271,7 @@ template <class T, class TC, bool AK, bool BKM>
 __device__ float recompute_elem(const GemmDesc& g, const T* A, const T* B, int m, int n, int k_lo,
                                 int k_hi) {
   float s = 0.f;
+#pragma unroll 8
   for (int k = k_lo; k < k_hi; ++k)
     s = fmaf(Storage<T>::load(A[op_off<AK>(m, k, g.lda)]),
              Storage<T>::load(B[op_off<BKM>(n, k, g.ldb)]), s);
@@ -436,6 +437,19 @@ struct Gemm {
     const T* A = static_cast<const T*>(g.A) + b0 * g.sA0 + b1 * g.sA1;
     const T* B = static_cast<const T*>(g.B) + b0 * g.sB0 + b1 * g.sB1;
     TC* C = static_cast<TC*>(g.C) + b0 * g.sC0 + b1 * g.sC1 + int64_t(kslice) * g.sCk;
+
+    // whether an injected fault (test-only) lands in this tile: the list is
+    // read here, and only such tiles take the injection step of the
+    // epilogue (with its barriers)
+    bool wf = false;
+    if (g.n_faults > 0 && !split) {
+      for (int f = 0; f < g.n_faults; ++f) {
+        const abft_fault ft = g.faults[f];
+        int fz, fm, fn;
+        wf |= fault_target(g.map, g.N, ft, &fz, &fm, &fn) && fz == z && fm >= m0 &&
+              fm < m0 + BM && fn >= n0 && fn < n0 + BN;
+      }
+    }
 
     const bool cc = PROT && g.Ac != nullptr;
     const bool cr = PROT && g.Br != nullptr && n0 >= g.cr_n_begin;
@@ -744,7 +758,7 @@ struct Gemm {
     }
     // injected faults (test-only): written into the rounded tile before any
     // verification
-    if (g.n_faults > 0 && !split) {
+    if (wf) {
       __syncthreads();
       if (tid == 0) {
         for (int f = 0; f < g.n_faults; ++f) {
@@ -1309,6 +1323,7 @@ struct Gemm {
         const int lr = qe[3 * q], lc = qe[3 * q + 1];
         const int m = m0 + lr, n = n0 + lc;
         float part = 0.f;
+#pragma unroll 8
         for (int k = k_lo + tid; k < k_hi; k += NT)
           part = fmaf(Storage<T>::load(A[op_off<AK>(m, k, g.lda)]),
                       Storage<T>::load(B[op_off<BKM>(n, k, g.ldb)]), part);
@@ -1563,6 +1578,13 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
   const int rb = blockIdx.y, m_base = rb * RB;
   const int64_t MN = int64_t(g.M) * g.N;
   const bool col_ok = n < g.N;  // N % 4 == 0: a quad is all in or all out
+  // whether an injected fault (test-only) lands in this workgroup's block
+  bool wf = false;
+  for (int f = 0; f < g.n_faults; ++f) {
+    int fz, fm, fn;
+    wf |= fault_target(g.map, g.N, g.faults[f], &fz, &fm, &fn) && fm >= m_base &&
+          fm < m_base + RB && fn >= int(blockIdx.x) * RED_COLS && fn < int(blockIdx.x + 1) * RED_COLS;
+  }
 
   // checksum rows of the slices: thread (c, sg) sums slices sg, sg+SG, ...
   const bool chk = verify && m_base + RB <= g.M;
@@ -1604,7 +1626,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
   for (int u = 0; u < RPT; ++u) {
     const int rr = rg + RED_GROUPS * u, m = m_base + rr;
     float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-    for (int f = 0; f < g.n_faults; ++f) {  // injected faults (tests only)
+    for (int f = 0; wf && f < g.n_faults; ++f) {  // injected faults (tests only)
       int fz, fm, fn;
       if (col_ok && fault_target(g.map, g.N, g.faults[f], &fz, &fm, &fn) && fm == m &&
           fn >= n && fn < n + 4) {
@@ -1681,6 +1703,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmDesc g, const fl
     const T* A = static_cast<const T*>(g.A);
     const T* B = static_cast<const T*>(g.B);
     float part = 0.f;
+#pragma unroll 8
     for (int k = threadIdx.x; k < g.K; k += 256)
       part = fmaf(Storage<T>::load(A[op_off<AK>(m, k, g.lda)]),
                   Storage<T>::load(B[op_off<BKM>(n, k, g.ldb)]), part);
