@@ -807,7 +807,7 @@ struct BwdTile {
         float a0[4], a1[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) { a0[r] = t[2 * q][r]; a1[r] = t[2 * q + 1][r]; }
-        const uint2 p0 = pack4(a0), p1 = pack4(a1);
+        const uint2 p0 = pack4v(a0), p1 = pack4v(a1);
         const uint4 u = {p0.x, p0.y, p1.x, p1.y};
         const uint4 ua = {u.x & 0x7fff7fffu, u.y & 0x7fff7fffu, u.z & 0x7fff7fffu, u.w & 0x7fff7fffu};
         const uint32_t one = lq == 4 * ((32 * q) >> (lg_jpb + 4)) ? 0x3f803f80u : 0u;
