@@ -76,13 +76,14 @@ struct EecResult {
 // EEC-ABFT on one vector of n stored values v[k * stride] (Sec. 4.2 cases
 // 1-4 with the mixed-type candidate sets of Sec. 4.3). c1, c2: propagated
 // unweighted and weighted (1-based weights) checksums.
-template <class T>
+template <class T, int UNR = 8>
 __device__ EecResult eec_locate(const T* v, int stride, int n, float c1, float c2, float e_rel,
                                 float tn) {
   float r1 = 0.f, r2 = 0.f, sa = 0.f;
-  // (unrolled: the loads of a rare path go out together instead of one
-  // memory latency each)
-#pragma unroll 8
+  // (unrolled UNR ways: the loads of a rare path go out together instead
+  // of one memory latency each; callers short of registers keep UNR = 1,
+  // since the unrolled copy's registers count against the caller's)
+#pragma unroll UNR
   for (int k = 0; k < n; ++k) {
     const float x = Storage<T>::load(v[k * stride]);
     r1 += x;
@@ -97,7 +98,7 @@ __device__ EecResult eec_locate(const T* v, int stride, int n, float c1, float c
   // element turns the unrolled loop into nested divergent loops)
   const bool any_inf = mode == 2, any_nonfin = mode == 3;
   int cnt = 0, idx = -1;
-#pragma unroll 8
+#pragma unroll UNR
   for (int k = 0; k < n; ++k) {
     const float x = Storage<T>::load(v[k * stride]);
     const bool fin = is_finite(x);
@@ -136,7 +137,7 @@ __device__ EecResult eec_locate(const T* v, int stride, int n, float c1, float c
 
 // Correction from the checksums alone (Sec. 4.2): DELTA when |d1| <=
 // t_correct, otherwise RECONSTRUCT v_i = c1 - sum_{k != i} v_k.
-template <class T>
+template <class T, int UNR = 8>
 __device__ float fix_by_checksum(const T* v, int stride, int n, int i, float c1, float d1,
                                  float tc, int* action) {
   if (is_finite(d1) && fabsf(d1) <= tc) {
@@ -144,7 +145,7 @@ __device__ float fix_by_checksum(const T* v, int stride, int n, int i, float c1,
     return Storage<T>::load(v[i * stride]) + d1;
   }
   float s = 0.f;
-#pragma unroll 8
+#pragma unroll UNR
   for (int k = 0; k < n; ++k) {
     const float x = Storage<T>::load(v[k * stride]);
     s += k != i ? x : 0.f;

@@ -120,10 +120,13 @@ struct ArgRef<Desc, true> {
 // dot product of row `col` of A and row `rowbase + index` of Bm (length
 // d <= 128) across the lanes, then score_close (lane 0) stores it, records
 // the event and reports a vector that is still flagged.
+// (UNR: the unroll of the vector loops; 1 where the caller's registers are
+// tight, head dim 128)
+template <int UNR>
 __device__ __noinline__ void score_locate(float* scr, int n, float v1, float v2, float e_rel,
                                           float tn, float tc, int recompute, abft_report* report,
                                           int op, int b, int h, int col, int rowbase, bool tr) {
-  const EecResult res = eec_locate<float>(scr, 1, n, v1, v2, e_rel, tn);
+  const EecResult res = eec_locate<float, UNR>(scr, 1, n, v1, v2, e_rel, tn);
   int idx = -1;
   float nv = 0.f;
   if (res.status == EEC_LOCATED) {
@@ -136,7 +139,7 @@ __device__ __noinline__ void score_locate(float* scr, int n, float v1, float v2,
     const int row = rowbase + idx;
     const float old = scr[idx];
     int action = ABFT_ACT_RECOMPUTE;
-    nv = fix_by_checksum<float>(scr, 1, n, idx, v1, res.d1, tc, &action);
+    nv = fix_by_checksum<float, UNR>(scr, 1, n, idx, v1, res.d1, tc, &action);
     scr[idx] = nv;
     record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn), action, old);
   }
@@ -445,7 +448,7 @@ struct FusedAttn {
               const float v2 = __shfl(ks[qb][2] + ks[qb][3], L, 64);
               wave_sync_lds();
               if (lane == 0)
-                score_locate(scr, R, v1, v2, arg->e_rel, arg->tn_s, arg->tc, arg->recompute,
+                score_locate<D == 64 ? 8 : 1>(scr, R, v1, v2, arg->e_rel, arg->tn_s, arg->tc, arg->recompute,
                              arg->report, ABFT_OP_AS, b, h, qw + 16 * qb + vq, key0 + vb * R,
                              false);
               wave_sync_lds();
@@ -633,14 +636,14 @@ struct FusedAttn {
             wave_sync_lds();
             if (lane == 0) {
               const int qq = qw + 16 * qb + L;
-              const EecResult res = eec_locate<float>(scr, 1, D, v1, v2, arg->e_rel, arg->tn_cl);
+              const EecResult res = eec_locate<float, 1>(scr, 1, D, v1, v2, arg->e_rel, arg->tn_cl);
               int idx = -1;
               float nv = 0.f;
               if (res.status == EEC_LOCATED) {
                 idx = res.index;
                 const float old = scr[idx];
                 int action = 0;
-                nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, D, idx, v1, res.d1, arg->tc, &action)));
+                nv = bf2f(f2bf(fix_by_checksum<float, 1>(scr, 1, D, idx, v1, res.d1, arg->tc, &action)));
                 scr[idx] = nv;
                 record_event(arg->report, ABFT_OP_CL, b, h, qq, idx, classify(old, arg->tn_cl), action,
                              old);
@@ -700,16 +703,17 @@ struct FusedAttn {
 
 // The same for a flagged gradient row of length n (entity e): fixed from
 // the checksums, rounded to storage.
+template <int UNR>
 __device__ __noinline__ void grad_fix(float* scr, int n, float v1, float v2, float e_rel, float tn,
                                       float tc, abft_report* report, int op, int b, int h, int e) {
-  const EecResult res = eec_locate<float>(scr, 1, n, v1, v2, e_rel, tn);
+  const EecResult res = eec_locate<float, UNR>(scr, 1, n, v1, v2, e_rel, tn);
   int idx = -1;
   float nv = 0.f;
   if (res.status == EEC_LOCATED) {
     idx = res.index;
     const float old = scr[idx];
     int action = 0;
-    nv = bf2f(f2bf(fix_by_checksum<float>(scr, 1, n, idx, v1, res.d1, tc, &action)));
+    nv = bf2f(f2bf(fix_by_checksum<float, UNR>(scr, 1, n, idx, v1, res.d1, tc, &action)));
     scr[idx] = nv;
     record_event(report, op, b, h, e, idx, classify(old, tn), action, old);
   }
@@ -860,7 +864,7 @@ struct BwdTile {
       const float v2 = __shfl(cs[2] + cs[3], L, 64);
       wave_sync_lds();
       if (lane == 0)
-        score_locate(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute, fd.report, op, b, h,
+        score_locate<D == 64 ? 8 : 1>(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute, fd.report, op, b, h,
                      cbase + vq, rbase + vb * R, TR);
       wave_sync_lds();
       if (fd.recompute && __float_as_int(scr[R]) >= 0) {
@@ -962,7 +966,7 @@ struct BwdTile {
           const float v1 = __shfl(c1, L, 64), v2 = __shfl(c2, L, 64);
           wave_sync_lds();
           if (lane == 0)
-            grad_fix(scr, D, v1, v2, fd.e_rel, fd.tn, fd.tc, fd.report, op, b, h, cbase + L);
+            grad_fix<D == 64 ? 8 : 1>(scr, D, v1, v2, fd.e_rel, fd.tn, fd.tc, fd.report, op, b, h, cbase + L);
           wave_sync_lds();
           const int idx = __float_as_int(scr[D]);
           const float nv = scr[D + 1];
