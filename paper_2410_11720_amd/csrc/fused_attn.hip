@@ -403,33 +403,46 @@ struct FusedAttn {
         if (arg->check_as) {
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb) {
-            float sj[8], aj[8];
+            // block sums of the values and, only when a vector needs them,
+            // of the magnitudes (2, 4 or 8 groups of 16 keys, reduced over
+            // the 4 lanes): as |sum| <= sum of magnitudes, a vector whose
+            // sum is within e_rel |sum| (shrunk by 0.1%, far beyond the
+            // rounding of either sum) of its checksum passes the rule
+            // whatever its magnitude sum
+            auto block_sums = [&](auto mag) {
+              float sj[8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              sj[j] = (s[j][qb][0] + s[j][qb][1]) + (s[j][qb][2] + s[j][qb][3]);
-              aj[j] = (fabsf(s[j][qb][0]) + fabsf(s[j][qb][1])) +
-                      (fabsf(s[j][qb][2]) + fabsf(s[j][qb][3]));
-            }
-            // block sums (2, 4 or 8 groups of 16 keys), reduced over the 4 lanes
-            float r1[4], ra[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              r1[i] = sj[2 * i] + sj[2 * i + 1];
-              ra[i] = aj[2 * i] + aj[2 * i + 1];
-            }
-            if (lg_jpb >= 2) {
-              r1[0] += r1[1]; ra[0] += ra[1];
-              r1[1] = r1[2] + r1[3]; ra[1] = ra[2] + ra[3];
-            }
-            if (lg_jpb >= 3) { r1[0] += r1[1]; ra[0] += ra[1]; }
-            float mine1 = 0.f, minea = 0.f;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              if (i < NB) {
-                const float t1 = group4_sum(r1[i]), ta = group4_sum(ra[i]);
-                if (g == i) { mine1 = t1; minea = ta; }
+              for (int j = 0; j < 8; ++j) {
+                if constexpr (decltype(mag)::value)
+                  sj[j] = (fabsf(s[j][qb][0]) + fabsf(s[j][qb][1])) +
+                          (fabsf(s[j][qb][2]) + fabsf(s[j][qb][3]));
+                else
+                  sj[j] = (s[j][qb][0] + s[j][qb][1]) + (s[j][qb][2] + s[j][qb][3]);
               }
-            }
+              float r1[4];
+#pragma unroll
+              for (int i = 0; i < 4; ++i) r1[i] = sj[2 * i] + sj[2 * i + 1];
+              if (lg_jpb >= 2) {
+                r1[0] += r1[1];
+                r1[1] = r1[2] + r1[3];
+              }
+              if (lg_jpb >= 3) r1[0] += r1[1];
+              float mine = 0.f;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                if (i < NB) {
+                  const float t1 = group4_sum(r1[i]);
+                  if (g == i) mine = t1;
+                }
+              }
+              return mine;
+            };
+            const float mine1 = block_sums(std::false_type{});
+            const float d = ks[qb][0] + ks[qb][1] - mine1;
+            const bool clear =
+                g >= NB || (is_finite(d) && fabsf(d) <= arg->e_rel * fabsf(mine1) * 0.999f);
+            float minea = INFINITY;
+            if (__ballot(!clear) != 0) minea = block_sums(std::true_type{});
             const float c1 = ks[qb][0] + ks[qb][1];
             const bool fl = g < NB && flagged(c1 - mine1, minea, arg->e_rel);
             uint64_t mask = __ballot(fl);
