@@ -3,10 +3,12 @@
 // Sec. 4.4, in an online-softmax form that keeps neither the scores AS nor
 // the probabilities AP in memory (an extension: the paper stores both).
 //
-// One workgroup per (batch, head, tile of 128 queries); each of its four
-// waves owns 32 queries. Key tiles of 128 keys pass through LDS in order
-// (causal: up to the diagonal tile), double-buffered for head_dim 64. Per
-// key tile each wave computes
+// One workgroup per (batch, head, tile of 128 queries): four waves of 32
+// queries (two workgroups per CU), or, protected at head dim 128, eight
+// waves of 16 (one workgroup per CU; the registers of 32 queries spill
+// there). Key tiles of 128 keys pass through LDS in order (causal: up to
+// the diagonal tile), double-buffered where the LDS allows. Per key tile
+// each wave computes
 //   S^T = K Q^T on the matrix cores, keys as rows and queries as columns,
 //     so a lane holds 32 keys of one query: the reductions over keys stay
 //     in the lane and its three partners, and P^T feeds the next product
@@ -41,7 +43,6 @@ namespace abft {
 namespace {
 
 constexpr int FT = 128;   // queries per workgroup, keys per key tile
-constexpr int FNT = 256;  // four waves of 32 queries
 
 // x combined with the value of lane l ^ 16 (l ^ 32): the gfx950 lane-swap
 // moves hand back both halves of the exchanged pair, so every lane gets
@@ -187,12 +188,19 @@ __device__ __forceinline__ bool faults_at(const abft_fault* f, int n, int b, int
 
 template <int D, bool PROT>
 struct FusedAttn {
-  static constexpr int NSTAGE = D == 64 ? 2 : 1;
+  // 16-query blocks per wave: one for the protected kernel at head dim 128
+  // (two would spill), else two (fewer LDS reads per MFMA)
+  static constexpr int QB = D == 128 && PROT ? 1 : 2;
+  static constexpr int NTH = 64 * (FT / (16 * QB));   // threads per workgroup
+  static constexpr int NW = NTH / 64;
+  // LDS stages of key tiles: two, except where two workgroups per CU leave
+  // room for one (head dim 128, four waves)
+  static constexpr int NSTAGE = D == 64 || QB == 1 ? 2 : 1;
   static constexpr int KH = D / 64;    // 64-wide halves of the head dim (K images)
   static constexpr int KS = D / 32;    // k steps of the score product
   static constexpr int DB = D / 16;    // 16-row blocks of O^T
-  using DK = Direct<true, FT>;         // K half [128 keys][64 dims], swizzled
-  using DV = Direct<false, D>;         // V image [64 keys][D dims], swizzled
+  using DK = Direct<true, FT, NTH>;    // K half [128 keys][64 dims], swizzled
+  using DV = Direct<false, D, NTH>;    // V image [64 keys][D dims], swizzled
   static constexpr int K_BYTES = KH * DK::BYTES;
   static constexpr int V_BYTES = 2 * DV::BYTES;
   static constexpr int KCL = D + 8;    // K^c strip row (elements), padded
@@ -200,8 +208,8 @@ struct FusedAttn {
   static constexpr int VR_BYTES = PROT ? FT * 16 * 2 : 0;
   static constexpr int STAGE_BYTES = K_BYTES + V_BYTES + KC_BYTES + VR_BYTES;
   static constexpr int SCR = 160;      // floats of rare-path scratch per wave
-  static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES + (PROT ? 4 * SCR * 4 : 0);
-  static_assert(LDS_BYTES <= 80 * 1024, "two workgroups per CU");
+  static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES + (PROT ? NW * SCR * 4 : 0);
+  static_assert(LDS_BYTES <= (QB == 2 ? 80 : 160) * 1024, "two (one) workgroups per CU");
 
   // V^T operand fragment for keys {kb + 4g + v, kb + 16 + 4g + v} (g = lane
   // group, v = 0..3), rows (dims) rb + lane % 16: the key order of the P^T
@@ -238,7 +246,7 @@ struct FusedAttn {
     // causal: the heaviest query tiles (most key tiles) start first
     const int qt = arg->causal ? nqt - 1 - int(blockIdx.x) / nbh : int(blockIdx.x) / nbh;
     const int b = z / arg->nh, h = z % arg->nh;
-    const int q0 = qt * FT, qw = q0 + wave * 32;
+    const int q0 = qt * FT, qw = q0 + wave * 16 * QB;
     const int S = arg->S, H = arg->H;
     const int64_t ld = 3 * int64_t(H);
     const bf16_t* base = static_cast<const bf16_t*>(arg->qkv) + int64_t(b) * S * ld;
@@ -254,9 +262,9 @@ struct FusedAttn {
                               (1u << ABFT_OP_AS) | (1u << ABFT_OP_CL));
 
     // Q as the B operand of S^T: query qw + 16 qb + lane % 16, dims 32 kk + 8 g..
-    bf16x8 qf[2][KS];
+    bf16x8 qf[QB][KS];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk)
         qf[qb][kk] = *reinterpret_cast<const bf16x8*>(Qp + int64_t(qw + 16 * qb + lq) * ld +
@@ -278,7 +286,7 @@ struct FusedAttn {
           const int nqR = S / R;
 #pragma unroll
           for (int p = 0; p < 4; ++p) {
-            const int e = tid + p * FNT;
+            const int e = tid + p * NTH;
             const bool ok = e < NB * 2 * D;
             const int ee = ok ? e : 0;
             const int blk = ee / (2 * D), c = (ee / D) & 1, dd = ee % D;
@@ -287,7 +295,8 @@ struct FusedAttn {
             kcv[p] = arg->qkvc[((int64_t(b) * nqR + key0 / R + blk) * 2 + c) * ld + H + h * D + dd];
           }
         }
-        if (arg->vr != nullptr)
+        // threads 0..255: the tile's 128 keys x (c1, c2)
+        if (arg->vr != nullptr && tid < 2 * FT)
           vrv = arg->vr[((int64_t(b) * S + key0 + (tid >> 1)) * arg->nh + h) * 2 + (tid & 1)];
       }
     };
@@ -298,7 +307,7 @@ struct FusedAttn {
           bf16_t* kcs = reinterpret_cast<bf16_t*>(sb + K_BYTES + V_BYTES);
 #pragma unroll
           for (int p = 0; p < 4; ++p) {
-            const int e = tid + p * FNT;
+            const int e = tid + p * NTH;
             if (e < NB * 2 * D) {
               const int blk = e / (2 * D), c = (e / D) & 1, dd = e % D;
               const bf16_t hi = f2bf(kcv[p]);
@@ -308,7 +317,7 @@ struct FusedAttn {
             }
           }
         }
-        if (arg->vr != nullptr) {
+        if (arg->vr != nullptr && tid < 2 * FT) {
           bf16_t* vrs = reinterpret_cast<bf16_t*>(sb + K_BYTES + V_BYTES + KC_BYTES);
           const bf16_t hi = f2bf(vrv);
           const bf16_t lo = f2bf(vrv - bf2f(hi));
@@ -320,14 +329,14 @@ struct FusedAttn {
     if constexpr (PROT) {  // the V^r strip columns past the four used ones stay zero
       for (int st = 0; st < NSTAGE; ++st) {
         bf16_t* vrs = reinterpret_cast<bf16_t*>(smem + st * STAGE_BYTES + K_BYTES + V_BYTES + KC_BYTES);
-        for (int e = tid; e < FT * 12; e += FNT) vrs[(e / 12) * 16 + 4 + e % 12] = 0;
+        for (int e = tid; e < FT * 12; e += NTH) vrs[(e / 12) * 16 + 4 + e % 12] = 0;
       }
     }
 
-    floatx4 o[DB][2], vra[2];
-    float m[2], l[2];
+    floatx4 o[DB][QB], vra[QB];
+    float m[QB], l[QB];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[db][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
       vra[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -352,12 +361,13 @@ struct FusedAttn {
       const int key0 = kt * FT;
 
       // S^T (and AS^r from the strip)
-      floatx4 s[8][2], ks[2];
+      floatx4 s[8][QB], ks[QB];
 #pragma unroll
       for (int j = 0; j < 8; ++j)
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) s[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
-      ks[0] = ks[1] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int qb = 0; qb < QB; ++qb) s[j][qb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) ks[qb] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
         const char* sk = sb + (kk >> 1) * DK::BYTES;
@@ -365,7 +375,7 @@ struct FusedAttn {
         for (int j = 0; j < 8; ++j) {
           const bf16x8 kf = DK::frag(sk, 16 * j, (kk & 1) * 32, lane);
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
+          for (int qb = 0; qb < QB; ++qb)
             s[j][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][kk], s[j][qb], 0, 0, 0);
         }
         if constexpr (PROT) {
@@ -373,7 +383,7 @@ struct FusedAttn {
             const bf16_t* kcs = reinterpret_cast<const bf16_t*>(sb + K_BYTES + V_BYTES);
             const bf16x8 sf = *reinterpret_cast<const bf16x8*>(kcs + lq * KCL + 32 * kk + 8 * g);
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
+            for (int qb = 0; qb < QB; ++qb)
               ks[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sf, qf[qb][kk], ks[qb], 0, 0, 0);
           }
         }
@@ -385,12 +395,12 @@ struct FusedAttn {
           const abft_fault ft = arg->faults[f];
           if (ft.op != ABFT_OP_AS || ft.b != b || ft.h != h) continue;
           const int qi = ft.row - qw, ki = ft.col - key0;
-          if (qi < 0 || qi >= 32 || ki < 0 || ki >= FT) continue;
+          if (qi < 0 || qi >= 16 * QB || ki < 0 || ki >= FT) continue;
           const int oq = qi >> 4, olane = (qi & 15) + 16 * ((ki & 15) >> 2);
 #pragma unroll
           for (int j = 0; j < 8; ++j)
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
+            for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
               for (int r = 0; r < 4; ++r)
                 if (lane == olane && qb == oq && j == (ki >> 4) && r == (ki & 3))
@@ -402,7 +412,7 @@ struct FusedAttn {
       if constexpr (PROT) {
         if (arg->check_as) {
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
+          for (int qb = 0; qb < QB; ++qb) {
             // block sums of the values and, only when a vector needs them,
             // of the magnitudes (2, 4 or 8 groups of 16 keys, reduced over
             // the 4 lanes): as |sum| <= sum of magnitudes, a vector whose
@@ -498,7 +508,7 @@ struct FusedAttn {
       if (arg->causal && kt == qt) {
         // the diagonal tile's masked scores
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+        for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
           for (int j = 0; j < 8; ++j)
 #pragma unroll
@@ -506,7 +516,7 @@ struct FusedAttn {
               if (key0 + 16 * j + 4 * g + r > qw + 16 * qb + lq) s[j][qb][r] = -INFINITY;
       }
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < QB; ++qb) {
         float mx = -INFINITY;
 #pragma unroll
         for (int j = 0; j < 8; ++j)
@@ -536,9 +546,9 @@ struct FusedAttn {
         // the first V^T read goes out before P is packed; each later one
         // before the MFMAs of the previous (one read pair in flight)
         TrPair cur = vt_frag(sv, 0, (t & 1) * 32, lane);
-        bf16x8 pf[2];
+        bf16x8 pf[QB];
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
+        for (int qb = 0; qb < QB; ++qb) {
           const uint4 u = {pack2v(s[2 * t][qb][0], s[2 * t][qb][1]),
                            pack2v(s[2 * t][qb][2], s[2 * t][qb][3]),
                            pack2v(s[2 * t + 1][qb][0], s[2 * t + 1][qb][1]),
@@ -566,7 +576,7 @@ struct FusedAttn {
           else lds_wait_all();
           const bf16x8 vf = tr_join(cur);
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
+          for (int qb = 0; qb < QB; ++qb)
             o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb], o[db][qb], 0, 0, 0);
           cur = nxt;
         }
@@ -575,7 +585,7 @@ struct FusedAttn {
           lds_wait_all();
           const bf16x8 rf = tr_join(cur);
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
+          for (int qb = 0; qb < QB; ++qb)
             vra[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf, pf[qb], vra[qb], 0, 0, 0);
         }
       }
@@ -585,7 +595,7 @@ struct FusedAttn {
     // CL = O / l: round, check against A^r / l, store
     bf16_t* CLp = static_cast<bf16_t*>(arg->cl) + int64_t(b) * S * H + h * D;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
       const int q = qw + 16 * qb + lq;
       const float lsum = group4_sum(l[qb]);
       const float inv = 1.f / lsum;
@@ -1665,7 +1675,7 @@ void fused_bwd_kv_kernel(FusedBwdDesc fd) {
 }
 
 template <int D, bool PROT>
-__global__ __launch_bounds__(FNT) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__((FusedAttn<D, PROT>::NTH)) __attribute__((amdgpu_waves_per_eu(2)))
 void fused_attn_kernel(FusedDesc fd) {
   extern __shared__ __align__(16) char smem[];
   FusedAttn<D, PROT>::run(fd, smem);
@@ -1685,7 +1695,7 @@ hipError_t launch_d(const FusedDesc& fd, hipStream_t s) {
   const int64_t grid = int64_t(fd.B) * fd.nh * (fd.S / FT);
   if (grid == 0) return hipSuccess;
   auto kern = fused_attn_kernel<D, PROT>;
-  hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(FNT), F::LDS_BYTES, s, fd);
+  hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(F::NTH), F::LDS_BYTES, s, fd);
   return hipGetLastError();
 }
 
