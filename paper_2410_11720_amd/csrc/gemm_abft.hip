@@ -1087,6 +1087,10 @@ struct Gemm {
     // g4), and the same 16 bytes are the B operand of the row sums of a
     // two-sided output: one LDS read for both
     constexpr bool ROWS_IN_STORE = WN == 4 * V && WN == SEG;
+    // a score-shaped output (causal 1) leaves the chunks wholly above the
+    // diagonal unwritten: no consumer reads them (the softmax selects masked
+    // keys to zero whatever is stored)
+    const bool tri = g.causal == 1;
     if constexpr (ROWS_IN_STORE) {
       const bf16x8 ones = __builtin_bit_cast(
           bf16x8, uint4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
@@ -1098,7 +1102,7 @@ struct Gemm {
         const int m = m0 + row, n = n0 + col;
         const TC* srcp = tile + row * LDT + col;
         const uint4 u = *reinterpret_cast<const uint4*>(srcp);
-        if (m < g.M) {
+        if (m < g.M && !(tri && n > m)) {
           TC* dstp = C + int64_t(m) * g.ldc + n;
           if (n + V <= g.N) {
             *reinterpret_cast<uint4*>(dstp) = u;
@@ -1120,7 +1124,7 @@ struct Gemm {
         const int c = lane + q * 64;
         const int row = c / CPW, col = wn * WN + (c % CPW) * V;
         const int m = m0 + row, n = n0 + col;
-        if (m < g.M) {
+        if (m < g.M && !(tri && n > m)) {
           const TC* srcp = tile + row * LDT + col;
           TC* dstp = C + int64_t(m) * g.ldc + n;
           if (n + V <= g.N) {
