@@ -1123,7 +1123,7 @@ struct FusedBwdQ : BwdTile<D> {
 
     // the statistics and the softmax backward's row term D = dCL . CL of
     // the lane's query (D also kept for the key pass)
-    float mq, il, ml, dq;
+    float mq, il, ml, dq, sdq;
     {
       float acc = 0.f;
 #pragma unroll
@@ -1138,6 +1138,7 @@ struct FusedBwdQ : BwdTile<D> {
       mq = st[0];
       il = 1.f / st[1];
       ml = mq + __log2f(st[1]);  // P = exp2(scaled score - ml)
+      sdq = fd.scale * dq;       // dS = P (scale dP - scale D)
       if (g == 0) fd.drow[(int64_t(b) * fd.nh + h) * S + q] = dq;
     }
     // Q and dCL images of the workgroup's queries (complete with tile 0)
@@ -1294,7 +1295,7 @@ struct FusedBwdQ : BwdTile<D> {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const bool cut = masked && key0 + 16 * j + 4 * g + r > q;
-              ds[r] = cut ? 0.f : fd.scale * a[r] * (dp[j][r] - dq);
+              ds[r] = cut ? 0.f : a[r] * fmaf(fd.scale, dp[j][r], -sdq);
             }
             pk[j] = T::pack4v(ds);
           }
@@ -1449,7 +1450,8 @@ struct FusedBwdKV : BwdTile<D> {
         rowf[tid] = D == 64 ? rv0 + __log2f(rv1) : rv0;
         rowf[FT + tid] = 1.f / rv1;
       } else if (tid < 2 * FT) {
-        rowf[2 * FT + tid - FT] = rv0;
+        // D per query (head dim 64: scale D, for dS = P (scale dP - scale D))
+        rowf[2 * FT + tid - FT] = D == 64 ? fd.scale * rv0 : rv0;
       }
       if (chk) {
         T::strip_commit(reinterpret_cast<bf16_t*>(sb + OFF_QC), NB, tid, qcv);
@@ -1604,7 +1606,7 @@ struct FusedBwdKV : BwdTile<D> {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const bool cut = masked && key > q0 + 16 * j + 4 * g + r;
-              ds[r] = cut ? 0.f : fd.scale * a[r] * (dp[j][r] - dv[r]);
+              ds[r] = cut ? 0.f : a[r] * fmaf(fd.scale, dp[j][r], -dv[r]);
             }
             pk[j] = T::pack4v(ds);
           }
