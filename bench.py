@@ -508,8 +508,27 @@ def vendor_reference(wl, steps):
     ev[1].synchronize()
     ms = ev[0].elapsed_time(ev[1]) / steps
     fl = useful_flops(B, S, H, nh, s.causal)
+
+    # the layer's six projection GEMMs one by one, in the layer's operand
+    # layouts, for a per-GEMM comparison with the stage times
+    Xd, Wq, Wod = X.detach(), Wqkv.detach(), Wo.detach()
+    dQKV = torch.randn(B * S, 3 * H, device="cuda", dtype=Xd.dtype)
+    gemms = {"qkv": lambda: Xd @ Wq, "out": lambda: Xd @ Wod, "dCL": lambda: dO @ Wod.t(),
+             "dWo": lambda: Xd.t() @ dO, "dWqkv": lambda: Xd.t() @ dQKV,
+             "dX": lambda: dQKV @ Wq.t()}
+    gemm_us = {}
+    for name, f in gemms.items():
+        for _ in range(3):
+            f()
+        ev[0].record(wl.stream)
+        for _ in range(steps):
+            f()
+        ev[1].record(wl.stream)
+        ev[1].synchronize()
+        gemm_us[name] = round(ev[0].elapsed_time(ev[1]) / steps * 1e3, 2)
     return {"what": "torch bf16 matmuls + SDPA flash backend, autograd backward, unprotected",
-            "ms_per_step": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 3)}
+            "ms_per_step": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 3),
+            "gemm_us": gemm_us}
 
 
 def pmc_workload(key, reps):
