@@ -488,36 +488,46 @@ struct Gemm {
 
     const int nk = k_hi > k_lo ? (k_hi - k_lo + BK - 1) / BK : 0;
     const int fr = lane & 15, fk = (lane >> 4) * FRAG;
+    // the checksum strips' fragments of one KI-wide k step, read with the
+    // tile's fragments so that one wait covers them all (a GEMM without a
+    // column strip reads the stage's first rows instead: a valid address,
+    // the value unused)
+    using Frag = typename Mfma<T>::frag;
+    auto strip_frags = [&](const T* st0, const T* sS, const T* sR, int kk, Frag& sf, Frag& rf) {
+      if (PROT) {
+        sf = Mfma<T>::load((cc ? sS : st0) + fr * LDK + kk + fk);
+        if (cr) rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
+      }
+    };
+    // the waves' positions in the wave grid as scalars: the strip blocks a
+    // wave multiplies are chosen by uniform branches, so every fragment
+    // index stays a compile-time constant (a runtime index would send the
+    // arrays to scratch) and no per-lane selects are spent on them
+    const int wmu = __builtin_amdgcn_readfirstlane(wm), wnu = __builtin_amdgcn_readfirstlane(wn);
     // the MFMAs of one KI-wide k step: the tile, then the checksum strips
-    auto mma_kk = [&](const typename Mfma<T>::frag (&af)[IM],
-                      const typename Mfma<T>::frag (&bfr)[JN], const T* sS, const T* sR,
-                      int kk) {
+    auto mma_kk = [&](const Frag (&af)[IM], const Frag (&bfr)[JN], const Frag& sf,
+                      const Frag& rf) {
 #pragma unroll
       for (int i = 0; i < IM; ++i)
 #pragma unroll
         for (int j = 0; j < JN; ++j) acc[i][j] = Mfma<T>::mma(af[i], bfr[j], acc[i][j]);
       if (PROT) {
-        // the strip operands a wave takes are selected, not branched to:
-        // every fragment index stays a compile-time constant (a runtime
-        // index would send the arrays to scratch) and the k step stays one
-        // block of straight-line code
         if (cc) {
-          const auto sf = Mfma<T>::load(sS + fr * LDK + kk + fk);
+          if (WLC || wmu == 0) {
 #pragma unroll
-          for (int j = 0; j < JS; ++j) {
-            const auto bsel = (WLC || wm == 0) ? bfr[j] : bfr[WLC ? j : JS + j];
-            accs[j] = Mfma<T>::mma(sf, bsel, accs[j]);
+            for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[j], accs[j]);
+          } else {
+#pragma unroll
+            for (int j = 0; j < JS; ++j) accs[j] = Mfma<T>::mma(sf, bfr[WLC ? j : JS + j], accs[j]);
           }
         }
         if (cr) {
-          const auto rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
 #pragma unroll
-          for (int i = 0; i < IS; ++i) {
-            auto asel = af[i];
+          for (int w = 0; w < WGN; ++w)
+            if (wnu == w) {
 #pragma unroll
-            for (int w = 1; w < WGN; ++w) asel = wn == w ? af[IS * w + i] : asel;
-            accr[i] = Mfma<T>::mma(rf, asel, accr[i]);
-          }
+              for (int i = 0; i < IS; ++i) accr[i] = Mfma<T>::mma(rf, af[IS * w + i], accr[i]);
+            }
         }
       }
     };
@@ -570,6 +580,8 @@ struct Gemm {
               if constexpr (BKM) bfr[j] = DB::frag(st + DA_BYTES, wn * WN + j * 16, kk, lane);
               else bp[j] = DB::frag_tr(st + DA_BYTES, wn * WN + j * 16, kk, lane);
             }
+            Frag sf, rf;
+            strip_frags(reinterpret_cast<const T*>(st), sS, sR, kk, sf, rf);
             if constexpr (!AK || !BKM) {
               lds_wait_all();
               if constexpr (!AK) {
@@ -581,7 +593,7 @@ struct Gemm {
                 for (int j = 0; j < JN; ++j) bfr[j] = tr_join(bp[j]);
               }
             }
-            mma_kk(af, bfr, sS, sR, kk);
+            mma_kk(af, bfr, sf, rf);
           }
         };
         // strip rows past the used ones are never written: each only feeds
@@ -650,7 +662,9 @@ struct Gemm {
 #pragma unroll
         for (int j = 0; j < JN; ++j)
           bfr[j] = Mfma<T>::load(sB + (wn * WN + j * 16 + fr) * LDK + kk + fk);
-        mma_kk(af, bfr, sS, sR, kk);
+        Frag sf, rf;
+        strip_frags(sA, sS, sR, kk, sf, rf);
+        mma_kk(af, bfr, sf, rf);
       }
       if (more) {
         if (NSTAGE == 1) __syncthreads();  // every wave is done reading the one stage
