@@ -47,6 +47,9 @@ struct Dims {
 struct Layout_ {
   size_t qkv, ap, cl, as, das, dcl, dqkv;
   size_t xc, xr, wvr, qkvc, vr, apc, apr, clc, clr, doc, dclc, dasc, dasr, dqkvc;
+  // bf16 images of X^c, dO^c and dQKV^c (four rows per block): the GEMMs
+  // that take them as column strips copy them like operand tiles
+  size_t xci, doci, dqkvci;
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
   size_t drow;      // fused backward: D = dCL . CL per query [B][nh][S]
@@ -115,6 +118,9 @@ Layout_ make_layout(const Dims& d) {
   L.dasc = take(size_t(d.B) * d.nh * d.nq * 2 * d.S * f);
   L.dasr = take(size_t(d.B) * d.nh * d.S * d.nq * 2 * f);
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
+  L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
+  L.doci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
+  L.dqkvci = take(size_t(d.B) * d.nq * 4 * 3 * d.H * 2);
   const int ks1 = splitk_for(d.H, 3 * d.H, d.T, true), ks2 = splitk_for(d.H, d.H, d.T, true);
   const size_t p1 = ks1 > 1 ? size_t(ks1) * d.H * 3 * d.H : 0;
   const size_t p2 = ks2 > 1 ? size_t(ks2) * d.H * d.H : 0;
@@ -149,6 +155,7 @@ Layout_ make_layout_fused_forward(const Dims& d) {
   L.clc = take(size_t(d.B) * d.nq * 2 * d.H * f);
   L.clr = take(size_t(d.T) * d.nh * 2 * f);
   L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
+  L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.total = off;
   return L;
 }
@@ -180,6 +187,9 @@ Layout_ make_layout_fused(const Dims& d) {
   L.doc = take(size_t(d.B) * d.nq * 2 * d.H * f);
   L.dclc = take(size_t(d.B) * d.nq * 2 * d.H * f);
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
+  L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
+  L.doci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
+  L.dqkvci = take(size_t(d.B) * d.nq * 4 * 3 * d.H * 2);
   const int ks1 = splitk_for(d.H, 3 * d.H, d.T, true), ks2 = splitk_for(d.H, d.H, d.T, true);
   const size_t p1 = ks1 > 1 ? size_t(ks1) * d.H * 3 * d.H : 0;
   const size_t p2 = ks2 > 1 ? size_t(ks2) * d.H * d.H : 0;
@@ -398,6 +408,10 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
       e.Rb = int(R); e.Cb = int(hd);
       e.col_chk = need_xc ? F(L.xc) : nullptr;
       e.row_chk = p.sec_bwd ? F(L.xr) : nullptr;
+      if (need_xc && es == 2) {
+        e.col_img = reinterpret_cast<uint16_t*>(ws + L.xci);
+        e.ldci = H;
+      }
     }
     CK(launch_encode_jobs(jobs, nj, dt,
                           (cfg->flags & ABFT_FLAG_REPORT_APPEND) ? nullptr : report, s));
@@ -413,6 +427,7 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     if (need_xc) {
       g.Ac = F(L.xc); g.ldac = H; g.Rm = int(R);
       g.Cc = F(L.qkvc); g.ldcc = 3 * H;
+      if (es == 2) { g.Aci = reinterpret_cast<const uint16_t*>(ws + L.xci); g.ldaci = H; }
     }
     if (need_vr) {
       g.Br = F(L.wvr); g.ldbr = 2 * nh; g.Rn = int(hd); g.cr_n_begin = int(2 * H);
@@ -577,6 +592,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       EncodeJob& j = e[nj++];
       j.A = dO; j.batch = B; j.rows = S; j.cols = H; j.ld = H; j.batch_stride = S * H;
       j.Rb = int(R); j.Cb = int(hd); j.col_chk = F(L.doc);
+      if (es == 2) { j.col_img = reinterpret_cast<uint16_t*>(ws + L.doci); j.ldci = H; }
     }
     CK(launch_encode_jobs(e, nj, dt, (cfg->flags & ABFT_FLAG_REPORT_APPEND) ? nullptr : report,
                           s));
@@ -591,6 +607,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     g.C = ws + L.dcl; g.ldc = H;
     if (pb) {
       g.Ac = F(L.doc); g.ldac = H; g.Rm = int(R);
+      if (es == 2) { g.Aci = reinterpret_cast<const uint16_t*>(ws + L.doci); g.ldaci = H; }
       g.Cc = F(L.dclc); g.ldcc = H;
       g.verify = 1;
     }
@@ -744,6 +761,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       e.A = ws + L.dqkv; e.batch = B; e.rows = S; e.cols = 3 * H; e.ld = 3 * H;
       e.batch_stride = S * 3 * H; e.Rb = int(R); e.Cb = int(hd);
       e.col_chk = F(L.dqkvc); e.ldcc = 3 * H;
+      if (es == 2) { e.col_img = reinterpret_cast<uint16_t*>(ws + L.dqkvci); e.ldci = 3 * H; }
       CK(launch_encode_jobs(&e, 1, dt, nullptr, s));
     }
     GemmDesc g = base_desc(p, faults, n_faults, report);
@@ -753,6 +771,9 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     g.C = dX; g.ldc = H;
     if (pb) {
       g.Ac = F(L.dqkvc); g.ldac = 3 * H; g.Rm = int(R);
+      if (fused && es == 2) {  // the image the encode above wrote
+        g.Aci = reinterpret_cast<const uint16_t*>(ws + L.dqkvci); g.ldaci = 3 * H;
+      }
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DX; g.map.rows_per_b = int(S);

@@ -49,7 +49,7 @@ template <class T, int V, int CPS>
 __device__ __forceinline__ void encode_block(const T* A, int64_t rows, int64_t cols, int64_t ld,
                                              int64_t bstride, int Rb, int Cb, float* col_chk,
                                              float* row_chk, int64_t bx, int64_t rb, int64_t b,
-                                             int64_t ldcc) {
+                                             int64_t ldcc, uint16_t* col_img, int64_t ldci) {
   constexpr int RG = NT / CPS, W = CPS * V;
   __shared__ float part[RG][W][2];
   const int c = threadIdx.x % CPS, g = threadIdx.x / CPS;
@@ -112,6 +112,12 @@ __device__ __forceinline__ void encode_block(const T* A, int64_t rows, int64_t c
       float acc = 0.f;
       for (int q = 0; q < RG; ++q) acc += part[q][col][which];
       col_chk[((b * (rows / Rb) + rb) * 2 + which) * ldcc + bx * W + col] = acc;
+      if (col_img != nullptr) {  // the bf16 image: hi and lo rows of this checksum
+        const bf16_t hi = f2bf(acc), lo = f2bf(acc - bf2f(hi));
+        uint16_t* ip = col_img + ((b * (rows / Rb) + rb) * 4 + 2 * which) * ldci + bx * W + col;
+        ip[0] = hi;
+        ip[ldci] = lo;
+      }
     }
   }
 }
@@ -121,7 +127,7 @@ __global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, in
                                                     int64_t ld, int64_t bstride, int Rb, int Cb,
                                                     float* col_chk, float* row_chk) {
   encode_block<T, V, CPS>(A, rows, cols, ld, bstride, Rb, Cb, col_chk, row_chk, blockIdx.x,
-                          blockIdx.y, blockIdx.z, cols);
+                          blockIdx.y, blockIdx.z, cols, nullptr, 0);
 }
 
 __device__ __forceinline__ void clear_counters(abft_report* rep) {
@@ -143,13 +149,15 @@ struct EncJob {
   float* row_chk;
   unsigned gx, gy, nblk;  // workgroups: gx column slabs x gy row blocks x batch
   int64_t ldcc;           // elements between column-checksum rows
+  uint16_t* col_img;      // optional bf16 image of the column checksums
+  int64_t ldci;
 };
 
 template <class T, int V, int CPS>
 __device__ __forceinline__ void encode_job(const EncJob& j, unsigned id) {
   const unsigned bx = id % j.gx, by = (id / j.gx) % j.gy, bz = id / (j.gx * j.gy);
   encode_block<T, V, CPS>(static_cast<const T*>(j.A), j.rows, j.cols, j.ld, j.bs, j.Rb, j.Cb,
-                          j.col_chk, j.row_chk, bx, by, bz, j.ldcc);
+                          j.col_chk, j.row_chk, bx, by, bz, j.ldcc, j.col_img, j.ldci);
 }
 
 template <class T, int V, int CPS>
@@ -343,6 +351,19 @@ hipError_t launch_encode(const void* A, int dtype, int64_t batch, int64_t rows, 
 }
 
 namespace {
+// The bf16 image of dense column checksums ([nrow][cols] fp32, two rows per
+// block) for the separate-launch form: image rows 2r (hi) and 2r + 1 (lo).
+__global__ __launch_bounds__(NT) void chk_image_kernel(const float* chk, int64_t nrow,
+                                                       int64_t cols, uint16_t* img, int64_t ldci) {
+  const int64_t i = int64_t(blockIdx.x) * NT + threadIdx.x;
+  if (i >= nrow * cols) return;
+  const int64_t r = i / cols, c = i % cols;
+  const float v = chk[i];
+  const bf16_t hi = f2bf(v), lo = f2bf(v - bf2f(hi));
+  img[(2 * r) * ldci + c] = hi;
+  img[(2 * r + 1) * ldci + c] = lo;
+}
+
 // The single-launch form applies when every job takes the vector path with
 // its row checksums inline and the same slab width.
 template <class T>
@@ -362,7 +383,8 @@ bool job_of(const EncodeJob& e, EncJob& j, int& cps) {
   const int64_t gx = (e.cols + W - 1) / W, gy = e.rows / e.Rb, n = gx * gy * e.batch;
   if (n <= 0 || n > (int64_t(1) << 30)) return false;
   j = EncJob{e.A, e.rows, e.cols, e.ld, e.batch_stride, e.Rb, e.Cb, e.col_chk, e.row_chk,
-             unsigned(gx), unsigned(gy), unsigned(n), e.ldcc > 0 ? e.ldcc : e.cols};
+             unsigned(gx), unsigned(gy), unsigned(n), e.ldcc > 0 ? e.ldcc : e.cols,
+             e.col_img, e.ldci};
   return true;
 }
 
@@ -386,6 +408,13 @@ hipError_t encode_jobs_t(const EncodeJob* jobs, int n, abft_report* reset, hipSt
                                    e.cols, e.ld, e.batch_stride, e.Rb, e.Cb, e.col_chk,
                                    e.row_chk, s);
       if (r != hipSuccess) return r;
+      if (e.col_img != nullptr && e.col_chk != nullptr) {
+        const int64_t nrow = e.batch * (e.rows / e.Rb) * 2, nel = nrow * e.cols;
+        const unsigned nb = unsigned((nel + NT - 1) / NT);
+        hipLaunchKernelGGL(chk_image_kernel, dim3(nb), dim3(NT), 0, s, e.col_chk, nrow, e.cols,
+                           e.col_img, e.ldci);
+        if ((r = hipGetLastError()) != hipSuccess) return r;
+      }
     }
     return hipSuccess;
   }

@@ -493,9 +493,15 @@ struct Gemm {
     // column strip reads the stage's first rows instead: a valid address,
     // the value unused)
     using Frag = typename Mfma<T>::frag;
+    // the column strip copied from its bf16 image (direct path): 2 nc rows
+    // of 64 elements, unpadded; fragment rows past them repeat the rows
+    // (their MFMA result rows are not read)
+    bool img = false;
+    if constexpr (DIR) img = cc && g.Aci != nullptr && nc_valid > 0;
+    const int soff = img ? (fr & (2 * nc - 1)) * BK + fk : fr * LDK + fk;
     auto strip_frags = [&](const T* st0, const T* sS, const T* sR, int kk, Frag& sf, Frag& rf) {
       if (PROT) {
-        sf = Mfma<T>::load((cc ? sS : st0) + fr * LDK + kk + fk);
+        sf = Mfma<T>::load((cc ? sS + soff : st0 + fr * LDK + fk) + kk);
         if (cr) rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
       }
     };
@@ -553,13 +559,25 @@ struct Gemm {
         };
         auto issue_strip = [&](int kt) {
           const int kn = k_lo + kt * BK;
-          if (cc) ls.load(Ac, g.ldac, rc0, nc_valid, kn, k_hi, tid);
+          if (cc && !img) ls.load(Ac, g.ldac, rc0, nc_valid, kn, k_hi, tid);
           if (cr) lr.load(Br, g.ldbr, qc0, nq_valid, kn, k_hi, tid);
         };
         auto commit_strip = [&](int kt) {
           T* st = reinterpret_cast<T*>(slot(kt) + DA_BYTES + DB_BYTES);
-          if (cc) ls.store(st, nc, tid);
+          if (cc && !img) ls.store(st, nc, tid);
           if (cr) lr.store(st + r_off, nq, tid);
+        };
+        // the column strip from its image: wave w copies image rows 8w ..
+        // 8w + 7 (eight 16-byte chunks each) into the stage's strip region;
+        // rows past the tile's valid ones read its last valid row
+        auto issue_img = [&](int kt) {
+          if (img && wave * 8 < 2 * nc) {
+            const int r = min(wave * 8 + (lane >> 3), 2 * nc_valid - 1);
+            const uint16_t* src =
+                g.Aci + int64_t(2 * rc0 + r) * g.ldaci + k_lo + kt * BK + (lane & 7) * 8;
+            __builtin_amdgcn_global_load_lds(
+                src, (lds_void*)(slot(kt) + DA_BYTES + DB_BYTES + wave * 1024), 16, 0, 0);
+          }
         };
         auto compute_d = [&](const char* st) {
           const T* sS = reinterpret_cast<const T*>(st + DA_BYTES + DB_BYTES);
@@ -602,6 +620,7 @@ struct Gemm {
           for (int kt = 0; kt < nk; ++kt) {
             if (PROT) issue_strip(kt);
             issue_dir(kt);
+            if (PROT) issue_img(kt);
             wait_vmcnt<0>();
             if (PROT) commit_strip(kt);
             __syncthreads();
@@ -609,8 +628,12 @@ struct Gemm {
             __syncthreads();
           }
         } else {
+          static_assert(NSTAGE <= 2, "the strip image copy is waited for with vmcnt(0)");
           if (nk > 0 && PROT) issue_strip(0);
-          for (int sl = 0; sl < NSTAGE - 1 && sl < nk; ++sl) issue_dir(sl);
+          for (int sl = 0; sl < NSTAGE - 1 && sl < nk; ++sl) {
+            issue_dir(sl);
+            if (PROT) issue_img(sl);
+          }
           for (int kt = 0; kt < nk; ++kt) {
             // stage kt is complete once only the later stages' loads remain
             const int later = min(NSTAGE - 2, nk - 1 - kt);
@@ -620,7 +643,10 @@ struct Gemm {
             if (PROT) commit_strip(kt);
             __syncthreads();  // stage kt visible; every wave is done with stage kt - 1
             if (PROT && kt + 1 < nk) issue_strip(kt + 1);
-            if (kt + NSTAGE - 1 < nk) issue_dir(kt + NSTAGE - 1);
+            if (kt + NSTAGE - 1 < nk) {
+              issue_dir(kt + NSTAGE - 1);
+              if (PROT) issue_img(kt + NSTAGE - 1);
+            }
             compute_d(slot(kt));
           }
           __syncthreads();  // the epilogue reuses the stages
