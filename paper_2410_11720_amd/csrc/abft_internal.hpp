@@ -46,10 +46,10 @@ struct GemmDesc {
   void* C = nullptr; int64_t ldc = 0, sC0 = 0, sC1 = 0;
 
   const float* Ac = nullptr; int64_t ldac = 0, sAc0 = 0, sAc1 = 0;
-  // optional bf16 image of Ac for an unbatched K-major A: per checksum
-  // block four rows (c1 hi, c1 lo, c2 hi, c2 lo, hi = bf16(c), lo =
-  // bf16(c - hi)), each ldaci elements long; the direct-to-LDS path then
-  // copies the column strip like an operand tile
+  // optional bf16 image of Ac for an unbatched A (either layout): per
+  // checksum block four rows (c1 hi, c1 lo, c2 hi, c2 lo, hi = bf16(c), lo
+  // = bf16(c - hi)) along k, each ldaci elements long; the direct-to-LDS
+  // path then copies the column strip like an operand tile
   const uint16_t* Aci = nullptr; int64_t ldaci = 0;
   float* Cc = nullptr; int64_t ldcc = 0, sCc0 = 0, sCc1 = 0;
   int Rm = 128;
@@ -203,6 +203,11 @@ struct EncodeJob {
   // bf16(c), lo = bf16(c - hi)
   uint16_t* col_img = nullptr;
   int64_t ldci = 0;
+  // optional bf16 image of the row checksums, transposed: per Cb-column
+  // block four rows (c1 hi, c1 lo, c2 hi, c2 lo) over all batch x rows
+  // rows of the operand, each ldri elements long
+  uint16_t* row_img = nullptr;
+  int64_t ldri = 0;
 };
 hipError_t launch_encode_jobs(const EncodeJob* jobs, int n, int dtype, abft_report* reset,
                               hipStream_t stream);

@@ -50,6 +50,7 @@ struct Layout_ {
   // bf16 images of X^c, dO^c and dQKV^c (four rows per block): the GEMMs
   // that take them as column strips copy them like operand tiles
   size_t xci, doci, dqkvci;
+  size_t xri;  // bf16 image of X^r, transposed ([nh][4][T]): dW^QKV's strip
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
   size_t drow;      // fused backward: D = dCL . CL per query [B][nh][S]
@@ -121,6 +122,7 @@ Layout_ make_layout(const Dims& d) {
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.doci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.dqkvci = take(size_t(d.B) * d.nq * 4 * 3 * d.H * 2);
+  L.xri = take(size_t(d.nh) * 4 * d.T * 2);
   const int ks1 = splitk_for(d.H, 3 * d.H, d.T, true), ks2 = splitk_for(d.H, d.H, d.T, true);
   const size_t p1 = ks1 > 1 ? size_t(ks1) * d.H * 3 * d.H : 0;
   const size_t p2 = ks2 > 1 ? size_t(ks2) * d.H * d.H : 0;
@@ -190,6 +192,7 @@ Layout_ make_layout_fused(const Dims& d) {
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.doci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.dqkvci = take(size_t(d.B) * d.nq * 4 * 3 * d.H * 2);
+  L.xri = take(size_t(d.nh) * 4 * d.T * 2);
   const int ks1 = splitk_for(d.H, 3 * d.H, d.T, true), ks2 = splitk_for(d.H, d.H, d.T, true);
   const size_t p1 = ks1 > 1 ? size_t(ks1) * d.H * 3 * d.H : 0;
   const size_t p2 = ks2 > 1 ? size_t(ks2) * d.H * d.H : 0;
@@ -408,6 +411,10 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
       e.Rb = int(R); e.Cb = int(hd);
       e.col_chk = need_xc ? F(L.xc) : nullptr;
       e.row_chk = p.sec_bwd ? F(L.xr) : nullptr;
+      if (p.sec_bwd && es == 2) {
+        e.row_img = reinterpret_cast<uint16_t*>(ws + L.xri);
+        e.ldri = T;
+      }
       if (need_xc && es == 2) {
         e.col_img = reinterpret_cast<uint16_t*>(ws + L.xci);
         e.ldci = H;
@@ -749,6 +756,7 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     g.C = dWqkv; g.ldc = 3 * H;
     if (pb) {
       g.Ac = F(L.xr); g.ldac = 2 * nh; g.Rm = int(hd);
+      if (es == 2) { g.Aci = reinterpret_cast<const uint16_t*>(ws + L.xri); g.ldaci = T; }
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DWQ; g.map.op_span = int(H);

@@ -49,15 +49,23 @@ template <class T, int V, int CPS>
 __device__ __forceinline__ void encode_block(const T* A, int64_t rows, int64_t cols, int64_t ld,
                                              int64_t bstride, int Rb, int Cb, float* col_chk,
                                              float* row_chk, int64_t bx, int64_t rb, int64_t b,
-                                             int64_t ldcc, uint16_t* col_img, int64_t ldci) {
+                                             int64_t ldcc, uint16_t* col_img, int64_t ldci,
+                                             uint16_t* row_img, int64_t ldri) {
   constexpr int RG = NT / CPS, W = CPS * V;
   __shared__ float part[RG][W][2];
+  // the transposed row-checksum image of this workgroup's blocks, staged
+  // so that it leaves in 16-byte row pieces: [4][block of the slab][row]
+  constexpr int RIMG = 1024;
+  __shared__ __align__(16) uint16_t rimg[4][RIMG];
   const int c = threadIdx.x % CPS, g = threadIdx.x / CPS;
   const int64_t c0 = bx * W + c * V;
   const bool live = c0 < cols;
   const T* base = A + b * bstride + rb * Rb * ld;
   const int lanes = Cb / V;
   const float wb = float((c0 % Cb) + 1);  // weight of the chunk's first column in its block
+  const int nbs = W / Cb;                 // column blocks of the slab (W is a multiple of Cb)
+  const bool stage_ri = row_img != nullptr && nbs * Rb <= RIMG && Rb % 8 == 0 && ldri % 8 == 0 &&
+                        reinterpret_cast<uintptr_t>(row_img) % 16 == 0;
   float c1[V], c2[V];
 #pragma unroll
   for (int e = 0; e < V; ++e) c1[e] = c2[e] = 0.f;
@@ -96,8 +104,32 @@ __device__ __forceinline__ void encode_block(const T* A, int64_t rows, int64_t c
           float* rc = row_chk + ((b * rows + rb * Rb + r) * (cols / Cb) + c0 / Cb) * 2;
           rc[0] = s1;
           rc[1] = s2;
+          if (row_img != nullptr) {  // the transposed bf16 image: hi and lo rows
+            const bf16_t h1 = f2bf(s1), h2 = f2bf(s2);
+            const bf16_t v[4] = {h1, f2bf(s1 - bf2f(h1)), h2, f2bf(s2 - bf2f(h2))};
+            if (stage_ri) {
+              const int e = int((c0 % W) / Cb) * Rb + r;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) rimg[q][e] = v[q];
+            } else {
+              uint16_t* ip = row_img + (4 * (c0 / Cb)) * ldri + b * rows + rb * Rb + r;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) ip[q * ldri] = v[q];
+            }
+          }
         }
       }
+    }
+  }
+  if (stage_ri) {  // every row of the block is staged: 16-byte pieces out
+    __syncthreads();
+    const int pieces = Rb / 8;
+    for (int u = threadIdx.x; u < 4 * nbs * pieces; u += NT) {
+      const int q = u / (nbs * pieces), bs = (u / pieces) % nbs, pc = u % pieces;
+      const int64_t blk = bx * W / Cb + bs;
+      if (blk * Cb < cols)
+        *reinterpret_cast<uint4*>(row_img + (4 * blk + q) * ldri + b * rows + rb * Rb + pc * 8) =
+            *reinterpret_cast<const uint4*>(&rimg[q][bs * Rb + pc * 8]);
     }
   }
   if (col_chk != nullptr) {
@@ -127,7 +159,7 @@ __global__ __launch_bounds__(NT) void encode_kernel(const T* A, int64_t rows, in
                                                     int64_t ld, int64_t bstride, int Rb, int Cb,
                                                     float* col_chk, float* row_chk) {
   encode_block<T, V, CPS>(A, rows, cols, ld, bstride, Rb, Cb, col_chk, row_chk, blockIdx.x,
-                          blockIdx.y, blockIdx.z, cols, nullptr, 0);
+                          blockIdx.y, blockIdx.z, cols, nullptr, 0, nullptr, 0);
 }
 
 __device__ __forceinline__ void clear_counters(abft_report* rep) {
@@ -151,13 +183,16 @@ struct EncJob {
   int64_t ldcc;           // elements between column-checksum rows
   uint16_t* col_img;      // optional bf16 image of the column checksums
   int64_t ldci;
+  uint16_t* row_img;      // optional transposed bf16 image of the row checksums
+  int64_t ldri;
 };
 
 template <class T, int V, int CPS>
 __device__ __forceinline__ void encode_job(const EncJob& j, unsigned id) {
   const unsigned bx = id % j.gx, by = (id / j.gx) % j.gy, bz = id / (j.gx * j.gy);
   encode_block<T, V, CPS>(static_cast<const T*>(j.A), j.rows, j.cols, j.ld, j.bs, j.Rb, j.Cb,
-                          j.col_chk, j.row_chk, bx, by, bz, j.ldcc, j.col_img, j.ldci);
+                          j.col_chk, j.row_chk, bx, by, bz, j.ldcc, j.col_img, j.ldci,
+                          j.row_img, j.ldri);
 }
 
 template <class T, int V, int CPS>
@@ -364,6 +399,24 @@ __global__ __launch_bounds__(NT) void chk_image_kernel(const float* chk, int64_t
   img[(2 * r + 1) * ldci + c] = lo;
 }
 
+// The transposed bf16 image of row checksums ([nrow][nblk][2] fp32) for the
+// separate-launch form: image rows 4 blk + (0 hi c1, 1 lo c1, 2 hi c2, 3 lo
+// c2), column = the operand row.
+__global__ __launch_bounds__(NT) void rowchk_image_kernel(const float* chk, int64_t nrow,
+                                                          int64_t nblk, uint16_t* img,
+                                                          int64_t ldri) {
+  const int64_t i = int64_t(blockIdx.x) * NT + threadIdx.x;
+  if (i >= nrow * nblk) return;
+  const int64_t r = i / nblk, blk = i % nblk;
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    const float v = chk[i * 2 + w];
+    const bf16_t hi = f2bf(v);
+    img[(4 * blk + 2 * w) * ldri + r] = hi;
+    img[(4 * blk + 2 * w + 1) * ldri + r] = f2bf(v - bf2f(hi));
+  }
+}
+
 // The single-launch form applies when every job takes the vector path with
 // its row checksums inline and the same slab width.
 template <class T>
@@ -384,7 +437,7 @@ bool job_of(const EncodeJob& e, EncJob& j, int& cps) {
   if (n <= 0 || n > (int64_t(1) << 30)) return false;
   j = EncJob{e.A, e.rows, e.cols, e.ld, e.batch_stride, e.Rb, e.Cb, e.col_chk, e.row_chk,
              unsigned(gx), unsigned(gy), unsigned(n), e.ldcc > 0 ? e.ldcc : e.cols,
-             e.col_img, e.ldci};
+             e.col_img, e.ldci, e.row_img, e.ldri};
   return true;
 }
 
@@ -413,6 +466,13 @@ hipError_t encode_jobs_t(const EncodeJob* jobs, int n, abft_report* reset, hipSt
         const unsigned nb = unsigned((nel + NT - 1) / NT);
         hipLaunchKernelGGL(chk_image_kernel, dim3(nb), dim3(NT), 0, s, e.col_chk, nrow, e.cols,
                            e.col_img, e.ldci);
+        if ((r = hipGetLastError()) != hipSuccess) return r;
+      }
+      if (e.row_img != nullptr && e.row_chk != nullptr) {
+        const int64_t nrow = e.batch * e.rows, nblk = e.cols / e.Cb;
+        const unsigned nb = unsigned((nrow * nblk + NT - 1) / NT);
+        hipLaunchKernelGGL(rowchk_image_kernel, dim3(nb), dim3(NT), 0, s, e.row_chk, nrow, nblk,
+                           e.row_img, e.ldri);
         if ((r = hipGetLastError()) != hipSuccess) return r;
       }
     }
