@@ -144,6 +144,9 @@ struct FusedDesc {
   // the propagated row checksums of CL [B*S][nh][2]
   float* stats = nullptr;
   float* clr = nullptr;
+  // optional transposed bf16 image of CL^r [nh][4][B*S] (rows c1 hi, c1 lo,
+  // c2 hi, c2 lo per head): the column strip of the dW^O GEMM
+  uint16_t* clri = nullptr;
 };
 hipError_t launch_fused_fwd(const FusedDesc& d, hipStream_t stream);
 

@@ -51,6 +51,7 @@ struct Layout_ {
   // that take them as column strips copy them like operand tiles
   size_t xci, doci, dqkvci;
   size_t xri;  // bf16 image of X^r, transposed ([nh][4][T]): dW^QKV's strip
+  size_t clri; // the same of CL^r, written by the fused forward: dW^O's strip
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
   size_t drow;      // fused backward: D = dCL . CL per query [B][nh][S]
@@ -158,6 +159,7 @@ Layout_ make_layout_fused_forward(const Dims& d) {
   L.clr = take(size_t(d.T) * d.nh * 2 * f);
   L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
+  L.clri = take(size_t(d.nh) * 4 * d.T * 2);
   L.total = off;
   return L;
 }
@@ -202,6 +204,7 @@ Layout_ make_layout_fused(const Dims& d) {
   L.skc = take((c1 > c2 ? c1 : c2) * f);
   L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
   L.drow = take(size_t(d.B) * d.nh * d.S * f);
+  L.clri = take(size_t(d.nh) * 4 * d.T * 2);
   L.total = off;
   return L;
 }
@@ -473,6 +476,7 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     fd.faults = faults; fd.n_faults = n_faults; fd.report = report;
     fd.stats = F(L.stats);
     fd.clr = F(L.clr);
+    if (es == 2) fd.clri = reinterpret_cast<uint16_t*>(ws + L.clri);
     CK(launch_fused_fwd(fd, s));
   }
   // AS = Q K^T per head (unscaled, before the mask), two-sided checksums
@@ -630,6 +634,9 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     g.C = dWo; g.ldc = H;
     if (pb) {
       g.Ac = F(L.clr); g.ldac = 2 * nh; g.Rm = int(hd);
+      if (fused && es == 2) {  // the image the fused forward wrote with CL^r
+        g.Aci = reinterpret_cast<const uint16_t*>(ws + L.clri); g.ldaci = T;
+      }
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DWO;

@@ -607,8 +607,18 @@ struct FusedAttn {
       if constexpr (PROT) {
         if (arg->vr != nullptr && arg->clr != nullptr && g == 0) {
           float* cr = arg->clr + ((int64_t(b) * S + q) * arg->nh + h) * 2;
-          cr[0] = (vra[qb][0] + vra[qb][1]) * inv;
-          cr[1] = (vra[qb][2] + vra[qb][3]) * inv;
+          const float c1 = (vra[qb][0] + vra[qb][1]) * inv, c2 = (vra[qb][2] + vra[qb][3]) * inv;
+          cr[0] = c1;
+          cr[1] = c2;
+          if (arg->clri != nullptr) {  // 16 consecutive queries per store
+            const int64_t T = int64_t(arg->B) * S;
+            bf16_t* ip = reinterpret_cast<bf16_t*>(arg->clri) + int64_t(h) * 4 * T + int64_t(b) * S + q;
+            const bf16_t h1 = f2bf(c1), h2 = f2bf(c2);
+            ip[0] = h1;
+            ip[T] = f2bf(c1 - bf2f(h1));
+            ip[2 * T] = h2;
+            ip[3 * T] = f2bf(c2 - bf2f(h2));
+          }
         }
       }
       float ov[DB][4];
