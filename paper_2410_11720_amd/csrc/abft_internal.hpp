@@ -55,6 +55,9 @@ struct GemmDesc {
   int Rm = 128;
 
   const float* Br = nullptr; int64_t ldbr = 0, sBr0 = 0, sBr1 = 0;
+  // optional bf16 image of Br for an unbatched B, laid out like Aci (four
+  // rows per checksum block along k, ldbri elements each)
+  const uint16_t* Bri = nullptr; int64_t ldbri = 0;
   float* Cr = nullptr; int64_t ldcr = 0, sCr0 = 0, sCr1 = 0;
   int Rn = 128;
   int cr_n_begin = 0;

@@ -52,6 +52,7 @@ struct Layout_ {
   size_t xci, doci, dqkvci;
   size_t xri;  // bf16 image of X^r, transposed ([nh][4][T]): dW^QKV's strip
   size_t clri; // the same of CL^r, written by the fused forward: dW^O's strip
+  size_t wvri; // the same of W^V r ([nh][4][H]): the QKV GEMM's row strip
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
   size_t drow;      // fused backward: D = dCL . CL per query [B][nh][S]
@@ -121,6 +122,7 @@ Layout_ make_layout(const Dims& d) {
   L.dasr = take(size_t(d.B) * d.nh * d.S * d.nq * 2 * f);
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
+  L.wvri = take(size_t(d.nh) * 4 * d.H * 2);
   L.doci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.dqkvci = take(size_t(d.B) * d.nq * 4 * 3 * d.H * 2);
   L.xri = take(size_t(d.nh) * 4 * d.T * 2);
@@ -159,6 +161,7 @@ Layout_ make_layout_fused_forward(const Dims& d) {
   L.clr = take(size_t(d.T) * d.nh * 2 * f);
   L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
+  L.wvri = take(size_t(d.nh) * 4 * d.H * 2);
   L.clri = take(size_t(d.nh) * 4 * d.T * 2);
   L.total = off;
   return L;
@@ -192,6 +195,7 @@ Layout_ make_layout_fused(const Dims& d) {
   L.dclc = take(size_t(d.B) * d.nq * 2 * d.H * f);
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
+  L.wvri = take(size_t(d.nh) * 4 * d.H * 2);
   L.doci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.dqkvci = take(size_t(d.B) * d.nq * 4 * 3 * d.H * 2);
   L.xri = take(size_t(d.nh) * 4 * d.T * 2);
@@ -407,6 +411,7 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
       EncodeJob& e = jobs[nj++];
       e.A = Wc + 2 * H * es; e.batch = 1; e.rows = H; e.cols = H; e.ld = 3 * H;
       e.Rb = 32; e.Cb = int(hd); e.row_chk = F(L.wvr);
+      if (es == 2) { e.row_img = reinterpret_cast<uint16_t*>(ws + L.wvri); e.ldri = H; }
     }
     if ((stages & ABFT_STAGE_ENCODE) && (need_xc || p.sec_bwd)) {
       EncodeJob& e = jobs[nj++];
@@ -441,6 +446,7 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     }
     if (need_vr) {
       g.Br = F(L.wvr); g.ldbr = 2 * nh; g.Rn = int(hd); g.cr_n_begin = int(2 * H);
+      if (es == 2) { g.Bri = reinterpret_cast<const uint16_t*>(ws + L.wvri); g.ldbri = H; }
       g.Cr = F(L.vr); g.ldcr = 2 * nh;
     }
     // the fused form's score checks have one side per pass, which cannot

@@ -496,13 +496,17 @@ struct Gemm {
     // the column strip copied from its bf16 image (direct path): 2 nc rows
     // of 64 elements, unpadded; fragment rows past them repeat the rows
     // (their MFMA result rows are not read)
-    bool img = false;
-    if constexpr (DIR) img = cc && g.Aci != nullptr && nc_valid > 0;
+    bool img = false, imgr = false;
+    if constexpr (DIR) {
+      img = cc && g.Aci != nullptr && nc_valid > 0;
+      imgr = cr && g.Bri != nullptr && nq_valid > 0;
+    }
     const int soff = img ? (fr & (2 * nc - 1)) * BK + fk : fr * LDK + fk;
+    const int roff = imgr ? (fr & (2 * nq - 1)) * BK + fk : fr * LDK + fk;
     auto strip_frags = [&](const T* st0, const T* sS, const T* sR, int kk, Frag& sf, Frag& rf) {
       if (PROT) {
         sf = Mfma<T>::load((cc ? sS + soff : st0 + fr * LDK + fk) + kk);
-        if (cr) rf = Mfma<T>::load(sR + fr * LDK + kk + fk);
+        if (cr) rf = Mfma<T>::load(sR + roff + kk);
       }
     };
     // the waves' positions in the wave grid as scalars: the strip blocks a
@@ -560,23 +564,35 @@ struct Gemm {
         auto issue_strip = [&](int kt) {
           const int kn = k_lo + kt * BK;
           if (cc && !img) ls.load(Ac, g.ldac, rc0, nc_valid, kn, k_hi, tid);
-          if (cr) lr.load(Br, g.ldbr, qc0, nq_valid, kn, k_hi, tid);
+          if (cr && !imgr) lr.load(Br, g.ldbr, qc0, nq_valid, kn, k_hi, tid);
         };
         auto commit_strip = [&](int kt) {
           T* st = reinterpret_cast<T*>(slot(kt) + DA_BYTES + DB_BYTES);
           if (cc && !img) ls.store(st, nc, tid);
-          if (cr) lr.store(st + r_off, nq, tid);
+          if (cr && !imgr) lr.store(st + r_off, nq, tid);
         };
-        // the column strip from its image: wave w copies image rows 8w ..
-        // 8w + 7 (eight 16-byte chunks each) into the stage's strip region;
-        // rows past the tile's valid ones read its last valid row
+        // the strips from their images: the column strip's rows go to
+        // waves 0.., the row strip's to the waves after them; a wave copies
+        // eight image rows (eight 16-byte chunks each) into the stage's strip
+        // region; rows past the tile's valid ones read its last valid row
+        const int wc = img ? (2 * nc + 7) / 8 : 0;
         auto issue_img = [&](int kt) {
-          if (img && wave * 8 < 2 * nc) {
+          if (img && wave < wc) {
             const int r = min(wave * 8 + (lane >> 3), 2 * nc_valid - 1);
             const uint16_t* src =
                 g.Aci + int64_t(2 * rc0 + r) * g.ldaci + k_lo + kt * BK + (lane & 7) * 8;
             __builtin_amdgcn_global_load_lds(
                 src, (lds_void*)(slot(kt) + DA_BYTES + DB_BYTES + wave * 1024), 16, 0, 0);
+          }
+          if (imgr && wave >= wc && (wave - wc) * 8 < 2 * nq) {
+            const int w = wave - wc;
+            const int r = min(w * 8 + (lane >> 3), 2 * nq_valid - 1);
+            const uint16_t* src =
+                g.Bri + int64_t(2 * qc0 + r) * g.ldbri + k_lo + kt * BK + (lane & 7) * 8;
+            __builtin_amdgcn_global_load_lds(
+                src,
+                (lds_void*)(slot(kt) + DA_BYTES + DB_BYTES + r_off * int(sizeof(T)) + w * 1024),
+                16, 0, 0);
           }
         };
         auto compute_d = [&](const char* st) {
