@@ -53,6 +53,7 @@ struct Layout_ {
   size_t xri;  // bf16 image of X^r, transposed ([nh][4][T]): dW^QKV's strip
   size_t clri; // the same of CL^r, written by the fused forward: dW^O's strip
   size_t wvri; // the same of W^V r ([nh][4][H]): the QKV GEMM's row strip
+  size_t clci; // bf16 image of CL^c (fused form): the output projection's strip
   size_t skp, skc;  // split-K partials of the weight gradients and their checksums
   size_t stats;     // fused forward: softmax max and sum per query [B][nh][S][2]
   size_t drow;      // fused backward: D = dCL . CL per query [B][nh][S]
@@ -123,6 +124,7 @@ Layout_ make_layout(const Dims& d) {
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.wvri = take(size_t(d.nh) * 4 * d.H * 2);
+  L.clci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.doci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.dqkvci = take(size_t(d.B) * d.nq * 4 * 3 * d.H * 2);
   L.xri = take(size_t(d.nh) * 4 * d.T * 2);
@@ -162,6 +164,7 @@ Layout_ make_layout_fused_forward(const Dims& d) {
   L.stats = take(size_t(d.B) * d.nh * d.S * 2 * f);
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.wvri = take(size_t(d.nh) * 4 * d.H * 2);
+  L.clci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.clri = take(size_t(d.nh) * 4 * d.T * 2);
   L.total = off;
   return L;
@@ -196,6 +199,7 @@ Layout_ make_layout_fused(const Dims& d) {
   L.dqkvc = take(size_t(d.B) * d.nq * 2 * 3 * d.H * f);
   L.xci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.wvri = take(size_t(d.nh) * 4 * d.H * 2);
+  L.clci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.doci = take(size_t(d.B) * d.nq * 4 * d.H * 2);
   L.dqkvci = take(size_t(d.B) * d.nq * 4 * 3 * d.H * 2);
   L.xri = take(size_t(d.nh) * 4 * d.T * 2);
@@ -537,8 +541,13 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
   }
   // O = CL Wo, O^c = CL^c Wo
   if (stages & ABFT_STAGE_OUT) {
-    if (fused && p.sec_o)  // the fused forward keeps no CL^c: encoded from the verified CL
-      CK(launch_encode(ws + L.cl, dt, B, S, H, H, S * H, int(R), int(hd), F(L.clc), nullptr, s));
+    if (fused && p.sec_o) {  // the fused forward keeps no CL^c: encoded from the verified CL
+      EncodeJob e;
+      e.A = ws + L.cl; e.batch = B; e.rows = S; e.cols = H; e.ld = H; e.batch_stride = S * H;
+      e.Rb = int(R); e.Cb = int(hd); e.col_chk = F(L.clc);
+      if (es == 2) { e.col_img = reinterpret_cast<uint16_t*>(ws + L.clci); e.ldci = H; }
+      CK(launch_encode_jobs(&e, 1, dt, nullptr, s));
+    }
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(H);
     g.A = ws + L.cl; g.lda = H;
@@ -546,6 +555,9 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     g.C = O; g.ldc = H;
     if (p.sec_o) {
       g.Ac = F(L.clc); g.ldac = H; g.Rm = int(R);
+      if (fused && es == 2) {  // the image the encode above wrote
+        g.Aci = reinterpret_cast<const uint16_t*>(ws + L.clci); g.ldaci = H;
+      }
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_O; g.map.rows_per_b = int(S);
