@@ -496,15 +496,19 @@ struct Gemm {
     // the column strip copied from its bf16 image (direct path): 2 nc rows
     // of 64 elements, unpadded; fragment rows past them repeat the rows
     // (their MFMA result rows are not read)
+    // (the one-stage tile, held to three workgroups per CU, keeps the strip
+    // reads after the tile's MFMAs and per-lane selects: fewer live
+    // registers; it has no images)
+    constexpr bool EARLY = NSTAGE >= 2;
     bool img = false, imgr = false;
-    if constexpr (DIR) {
+    if constexpr (DIR && EARLY) {
       img = cc && g.Aci != nullptr && nc_valid > 0;
       imgr = cr && g.Bri != nullptr && nq_valid > 0;
     }
     const int soff = img ? (fr & (2 * nc - 1)) * BK + fk : fr * LDK + fk;
     const int roff = imgr ? (fr & (2 * nq - 1)) * BK + fk : fr * LDK + fk;
     auto strip_frags = [&](const T* st0, const T* sS, const T* sR, int kk, Frag& sf, Frag& rf) {
-      if (PROT) {
+      if (PROT && EARLY) {
         sf = Mfma<T>::load((cc ? sS + soff : st0 + fr * LDK + fk) + kk);
         if (cr) rf = Mfma<T>::load(sR + roff + kk);
       }
@@ -516,12 +520,32 @@ struct Gemm {
     const int wmu = __builtin_amdgcn_readfirstlane(wm), wnu = __builtin_amdgcn_readfirstlane(wn);
     // the MFMAs of one KI-wide k step: the tile, then the checksum strips
     auto mma_kk = [&](const Frag (&af)[IM], const Frag (&bfr)[JN], const Frag& sf,
-                      const Frag& rf) {
+                      const Frag& rf, const T* sS, const T* sR, int kk) {
 #pragma unroll
       for (int i = 0; i < IM; ++i)
 #pragma unroll
         for (int j = 0; j < JN; ++j) acc[i][j] = Mfma<T>::mma(af[i], bfr[j], acc[i][j]);
-      if (PROT) {
+      if (PROT && !EARLY) {
+        if (cc) {
+          const auto sfl = Mfma<T>::load(sS + fr * LDK + kk + fk);
+#pragma unroll
+          for (int j = 0; j < JS; ++j) {
+            const auto bsel = (WLC || wm == 0) ? bfr[j] : bfr[WLC ? j : JS + j];
+            accs[j] = Mfma<T>::mma(sfl, bsel, accs[j]);
+          }
+        }
+        if (cr) {
+          const auto rfl = Mfma<T>::load(sR + fr * LDK + kk + fk);
+#pragma unroll
+          for (int i = 0; i < IS; ++i) {
+            auto asel = af[i];
+#pragma unroll
+            for (int w = 1; w < WGN; ++w) asel = wn == w ? af[IS * w + i] : asel;
+            accr[i] = Mfma<T>::mma(rfl, asel, accr[i]);
+          }
+        }
+      }
+      if (PROT && EARLY) {
         if (cc) {
           if (WLC || wmu == 0) {
 #pragma unroll
@@ -627,7 +651,7 @@ struct Gemm {
                 for (int j = 0; j < JN; ++j) bfr[j] = tr_join(bp[j]);
               }
             }
-            mma_kk(af, bfr, sf, rf);
+            mma_kk(af, bfr, sf, rf, sS, sR, kk);
           }
         };
         // strip rows past the used ones are never written: each only feeds
@@ -706,7 +730,7 @@ struct Gemm {
           bfr[j] = Mfma<T>::load(sB + (wn * WN + j * 16 + fr) * LDK + kk + fk);
         Frag sf, rf;
         strip_frags(sA, sS, sR, kk, sf, rf);
-        mma_kk(af, bfr, sf, rf);
+        mma_kk(af, bfr, sf, rf, sS, sR, kk);
       }
       if (more) {
         if (NSTAGE == 1) __syncthreads();  // every wave is done reading the one stage
