@@ -411,6 +411,7 @@ struct FusedAttn {
       // row check of S per (query, R-key block)
       if constexpr (PROT) {
         if (arg->check_as) {
+          uint64_t fmask[QB];
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb) {
             // block sums of the values and, only when a vector needs them,
@@ -455,47 +456,69 @@ struct FusedAttn {
             if (__ballot(!clear) != 0) minea = block_sums(std::true_type{});
             const float c1 = ks[qb][0] + ks[qb][1];
             const bool fl = g < NB && flagged(c1 - mine1, minea, arg->e_rel);
-            uint64_t mask = __ballot(fl);
-            while (mask) {  // rare: locate and correct inside the wave
-              const int L = __builtin_ctzll(mask);
-              mask &= mask - 1;
-              const int vq = L & 15, vb = L >> 4;    // query lane, key block
-              // gather the vector S[q][block vb] into the scratch
+            fmask[qb] = __ballot(fl);
+          }
+          uint64_t any = 0;
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) any |= fmask[qb];
+          if (any) {  // rare: locate and correct inside the wave
+            // the tile's scores wait in private memory (indexed at run time,
+            // so they stay there): no score register is live while the
+            // flagged vectors are corrected
+            float sm[QB][8][4];
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
               for (int j = 0; j < 8; ++j)
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                  if (lq == vq && (j >> lg_jpb) == vb)
-                    scr[(16 * j + 4 * g + r) - vb * R] = s[j][qb][r];
-              const float v1 = __shfl(ks[qb][0] + ks[qb][1], L, 64);
-              const float v2 = __shfl(ks[qb][2] + ks[qb][3], L, 64);
-              wave_sync_lds();
-              if (lane == 0)
-                score_locate<D == 64 ? 8 : 1>(scr, R, v1, v2, arg->e_rel, arg->tn_s, arg->tc, arg->recompute,
-                             arg->report, ABFT_OP_AS, b, h, qw + 16 * qb + vq, key0 + vb * R,
-                             false);
-              wave_sync_lds();
-              if (arg->recompute && __float_as_int(scr[R]) >= 0) {
-                const float nv = score_dot(Qp, Kp, ld, ld, qw + 16 * qb + vq,
-                                           key0 + vb * R + __float_as_int(scr[R]), D, lane);
+                for (int r = 0; r < 4; ++r) sm[qb][j][r] = s[j][qb][r];
+            const int jpb = 1 << lg_jpb;
+            for (int qb = 0; qb < QB; ++qb) {
+              uint64_t mask = fmask[qb];
+              const float cs1 = ks[qb][0] + ks[qb][1], cs2 = ks[qb][2] + ks[qb][3];
+              while (mask) {
+                const int L = __builtin_ctzll(mask);
+                mask &= mask - 1;
+                const int vq = L & 15, vb = L >> 4;    // query lane, key block
+                // gather the vector S[q][block vb] into the scratch
+                if (lq == vq) {
+                  for (int jj = 0; jj < jpb; ++jj) {
+                    const int j = vb * jpb + jj;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) scr[16 * jj + 4 * g + r] = sm[qb][j][r];
+                  }
+                }
+                const float v1 = __shfl(cs1, L, 64);
+                const float v2 = __shfl(cs2, L, 64);
+                wave_sync_lds();
                 if (lane == 0)
-                  score_close(scr, R, nv, v1, arg->e_rel, arg->tn_s, arg->report, ABFT_OP_AS, b,
-                              h, qw + 16 * qb + vq, key0 + vb * R, false);
+                  score_locate<D == 64 ? 8 : 1>(scr, R, v1, v2, arg->e_rel, arg->tn_s, arg->tc,
+                                                arg->recompute, arg->report, ABFT_OP_AS, b, h,
+                                                qw + 16 * qb + vq, key0 + vb * R, false);
+                wave_sync_lds();
+                if (arg->recompute && __float_as_int(scr[R]) >= 0) {
+                  const float nv = score_dot(Qp, Kp, ld, ld, qw + 16 * qb + vq,
+                                             key0 + vb * R + __float_as_int(scr[R]), D, lane);
+                  if (lane == 0)
+                    score_close(scr, R, nv, v1, arg->e_rel, arg->tn_s, arg->report, ABFT_OP_AS,
+                                b, h, qw + 16 * qb + vq, key0 + vb * R, false);
+                }
+                wave_sync_lds();
+                const int idx = __float_as_int(scr[R]);
+                const float nv = scr[R + 1];
+                if (idx >= 0) {
+                  const int kl = vb * R + idx;
+                  if (lane == vq + 16 * ((kl & 15) >> 2)) sm[qb][kl >> 4][kl & 3] = nv;
+                }
+                wave_sync_lds();
               }
-              wave_sync_lds();
-              const int idx = __float_as_int(scr[R]);
-              const float nv = scr[R + 1];
-              if (idx >= 0) {
-                const int kl = vb * R + idx;
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-#pragma unroll
-                  for (int r = 0; r < 4; ++r)
-                    if (lane == vq + 16 * ((kl & 15) >> 2) && j == (kl >> 4) && r == (kl & 3))
-                      s[j][qb][r] = nv;
-              }
-              wave_sync_lds();
             }
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+              for (int j = 0; j < 8; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) s[j][qb][r] = sm[qb][j][r];
           }
         }
       }
