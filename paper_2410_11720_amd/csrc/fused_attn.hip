@@ -907,41 +907,55 @@ struct BwdTile {
     }
     const float c1 = cs[0] + cs[1];
     uint64_t mask = __ballot(g < NB && flagged(c1 - mine1, minea, fd.e_rel));
-    while (mask) {  // rare
-      const int L = __builtin_ctzll(mask);
-      mask &= mask - 1;
-      const int vq = L & 15, vb = L >> 4;
+    if (mask) {  // rare
+      // the tile waits in private memory (indexed at run time, so it stays
+      // there): none of its registers is live while the flagged vectors are
+      // corrected
+      float tm[8][4];
 #pragma unroll
       for (int j = 0; j < 8; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (lq == vq && (j >> lg_jpb) == vb) scr[(16 * j + 4 * g + r) - vb * R] = t[j][r];
-      const float v1 = __shfl(cs[0] + cs[1], L, 64);
-      const float v2 = __shfl(cs[2] + cs[3], L, 64);
-      wave_sync_lds();
-      if (lane == 0)
-        score_locate<D == 64 ? 8 : 1>(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute, fd.report, op, b, h,
-                     cbase + vq, rbase + vb * R, TR);
-      wave_sync_lds();
-      if (fd.recompute && __float_as_int(scr[R]) >= 0) {
-        const float nv = score_dot(A, Bm, lda, ldb, cbase + vq, rbase + vb * R +
-                                   __float_as_int(scr[R]), D, lane);
+        for (int r = 0; r < 4; ++r) tm[j][r] = t[j][r];
+      const float cs1 = cs[0] + cs[1], cs2 = cs[2] + cs[3];
+      const int jpb = 1 << lg_jpb;
+      while (mask) {
+        const int L = __builtin_ctzll(mask);
+        mask &= mask - 1;
+        const int vq = L & 15, vb = L >> 4;
+        if (lq == vq) {
+          for (int jj = 0; jj < jpb; ++jj) {
+            const int j = vb * jpb + jj;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) scr[16 * jj + 4 * g + r] = tm[j][r];
+          }
+        }
+        const float v1 = __shfl(cs1, L, 64);
+        const float v2 = __shfl(cs2, L, 64);
+        wave_sync_lds();
         if (lane == 0)
-          score_close(scr, R, nv, v1, fd.e_rel, fd.tn_s, fd.report, op, b, h, cbase + vq,
-                      rbase + vb * R, TR);
+          score_locate<D == 64 ? 8 : 1>(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute,
+                                        fd.report, op, b, h, cbase + vq, rbase + vb * R, TR);
+        wave_sync_lds();
+        if (fd.recompute && __float_as_int(scr[R]) >= 0) {
+          const float nv = score_dot(A, Bm, lda, ldb, cbase + vq, rbase + vb * R +
+                                     __float_as_int(scr[R]), D, lane);
+          if (lane == 0)
+            score_close(scr, R, nv, v1, fd.e_rel, fd.tn_s, fd.report, op, b, h, cbase + vq,
+                        rbase + vb * R, TR);
+          wave_sync_lds();
+        }
+        const int idx = __float_as_int(scr[R]);
+        const float nv = scr[R + 1];
+        if (idx >= 0) {
+          const int kl = vb * R + idx;
+          if (lane == vq + 16 * ((kl & 15) >> 2)) tm[kl >> 4][kl & 3] = nv;
+        }
         wave_sync_lds();
       }
-      const int idx = __float_as_int(scr[R]);
-      const float nv = scr[R + 1];
-      if (idx >= 0) {
-        const int kl = vb * R + idx;
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+      for (int j = 0; j < 8; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (lane == vq + 16 * ((kl & 15) >> 2) && j == (kl >> 4) && r == (kl & 3)) t[j][r] = nv;
-      }
-      wave_sync_lds();
+        for (int r = 0; r < 4; ++r) t[j][r] = tm[j][r];
     }
   }
 
