@@ -61,17 +61,17 @@ struct Layout_ {
 };
 
 // K slices for a weight-gradient GEMM (M x N tiles of 128 x 128, long K):
-// enough slices to give about 512 workgroups, each slice at least 512 deep.
+// enough slices to give at least 256 workgroups, each slice at least 256
+// deep.
 int splitk_for(int64_t M, int64_t N, int64_t K, bool prot) {
   const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
   int ks = 1;
   // smallest power of two that fills every CU once (fewer slices, less
-  // partial-sum traffic), with K slices of at least 256
+  // partial-sum traffic), with K slices of at least 256; a checked tile in
+  // one slice stages its fp32 tile for the column check in an epilogue
+  // area that still leaves two workgroups per CU
+  (void)prot;
   while (tiles * ks < 256 && K / (2 * ks) >= 256 && ks < 16) ks *= 2;
-  // a checked weight gradient in one slice stages its fp32 tile in LDS for
-  // the column check, which leaves one workgroup per CU; in two slices the
-  // K loop keeps two per CU and the check moves to the reduction
-  if (prot && ks == 1 && K / 2 >= 256) ks = 2;
   return ks;
 }
 

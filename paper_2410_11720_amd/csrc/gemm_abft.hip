@@ -396,10 +396,15 @@ struct Gemm {
   static constexpr int TPAD = 16 / sizeof(TC);
   static constexpr int LDT = BN + TPAD;
   static constexpr size_t TILE_BYTES = size_t(BM) * LDT * sizeof(TC);
-  static constexpr size_t STRIPS = 16 * BN + 16 * BM;
+  // bf16 operands with fp32 output are the weight gradients, checked on
+  // the column side only: no row strip, no row checksums (the launch
+  // refuses them), so that an unsplit checked tile keeps two workgroups
+  // per CU
+  static constexpr bool COLS_ONLY = sizeof(T) == 2 && sizeof(TC) == 4;
+  static constexpr size_t STRIPS = 16 * BN + (COLS_ONLY ? 0 : 16 * BM);
   // checksum pairs ([BM/MINB][BN][2], [BM][BN/MINB][2]); the segment sums
   // (sum, magnitude) have the same shapes
-  static constexpr size_t CCV = (BM / MINB) * BN * 2, RCV = BM * (BN / MINB) * 2;
+  static constexpr size_t CCV = (BM / MINB) * BN * 2, RCV = COLS_ONLY ? 0 : BM * (BN / MINB) * 2;
   static constexpr size_t CNT = BM * (BN / MINB) + (BM / MINB) * BN;
   // recompute queue of the correction passes: count, QMAX x (row, col,
   // observed value), and one partial sum per wave
@@ -881,7 +886,7 @@ struct Gemm {
       //     in registers until every thread has read the strips; row
       //     vectors are walked row-fastest, so only shifts divide
       constexpr int CI = int((CCV / 2 + NT - 1) / NT), RI = int((RCV / 2 + NT - 1) / NT);
-      float2 cv[CI], rv[RI];
+      float2 cv[CI], rv[RI > 0 ? RI : 1];
 #pragma unroll
       for (int i = 0; i < CI; ++i) {
         const int v = tid + i * NT, blk = v / BN, n = v % BN;
@@ -1545,6 +1550,7 @@ hipError_t set_lds_limit(size_t bytes) {
 template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int NSTAGE = 2>
 hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   using G = Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE>;
+  if (G::COLS_ONLY && (g.Br != nullptr || g.verify == 2)) return hipErrorInvalidValue;
   const bool gcc = PROT && g.Ac != nullptr, gcr = PROT && g.Br != nullptr;
   const bool direct = direct_ok<T>(g, AK, BKM);
   const size_t main = direct ? G::d_main_bytes(gcc, gcr) : G::main_bytes(gcc, gcr);
