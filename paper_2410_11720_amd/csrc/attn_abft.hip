@@ -414,7 +414,9 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     if ((stages & ABFT_STAGE_ENCODE) && need_vr) {
       EncodeJob& e = jobs[nj++];
       e.A = Wc + 2 * H * es; e.batch = 1; e.rows = H; e.cols = H; e.ld = 3 * H;
-      e.Rb = 32; e.Cb = int(hd); e.row_chk = F(L.wvr);
+      // row checksums only: any row block; 128 rows fill a workgroup's loads
+      e.Rb = H % 128 == 0 ? 128 : (H % 64 == 0 ? 64 : 32);
+      e.Cb = int(hd); e.row_chk = F(L.wvr);
       if (es == 2) { e.row_img = reinterpret_cast<uint16_t*>(ws + L.wvri); e.ldri = H; }
     }
     if ((stages & ABFT_STAGE_ENCODE) && (need_xc || p.sec_bwd)) {
