@@ -94,6 +94,14 @@ enum class Tile : int { T128x128 = 1, T128x64 = 2, T128x128S1 = 3 };
 hipError_t launch_gemm(const GemmDesc& g, int dtype, bool c_fp32, Layout la, Layout lb,
                        Tile tile, hipStream_t stream);
 
+// A weight gradient w (MN-major operands, fp32 output, whole or as its K
+// slices, as launch_gemm takes it) and a projection p (K-major operands,
+// bf16 output, 128 x 128 tiles) in one launch, when both take the direct
+// path and w's workgroups are a multiple of 8; hipErrorNotSupported when
+// they do not qualify (nothing launched: launch them one by one).
+hipError_t launch_gemm_pair(const GemmDesc& w, const GemmDesc& p, int dtype,
+                            hipStream_t stream);
+
 // Sum the split-K partials of a protected GEMM (fixed order), apply
 // injected faults, run the column pass (recompute correction from A and B)
 // and store C. g describes the full GEMM with its final C, Rm, map, faults

@@ -286,12 +286,13 @@ Tile proj_tile() { return Tile::T128x128; }
     if (e_ != hipSuccess) return ABFT_ERR_HIP;         \
   } while (0)
 
-// A weight-gradient GEMM (MN-major operands, fp32 output): split over K
-// into partials when that fills the GPU better, then reduced and verified.
-hipError_t launch_wgrad(const GemmDesc& g, int dt, float* part, float* part_c, hipStream_t s) {
+// The launch descriptor of a weight-gradient GEMM (MN-major operands, fp32
+// output) split over K into ks partials when that fills the GPU better
+// (the GEMM itself when ks is 1).
+GemmDesc wgrad_slices(const GemmDesc& g, float* part, float* part_c, int* ks_out) {
   const int ks = splitk_for(g.M, g.N, g.K, g.Ac != nullptr || g.Br != nullptr || g.verify != 0);
-  if (ks <= 1)
-    return launch_gemm(g, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s);
+  *ks_out = ks;
+  if (ks <= 1) return g;
   GemmDesc sg = g;
   sg.splitk = ks;
   sg.C = part;
@@ -302,11 +303,43 @@ hipError_t launch_wgrad(const GemmDesc& g, int dt, float* part, float* part_c, h
   sg.sCck = int64_t(2 * (g.M / g.Rm)) * g.N;
   sg.n_faults = 0;
   sg.faults = nullptr;
+  return sg;
+}
+
+// A weight-gradient GEMM: its slices, then (split) the reduction that sums
+// and verifies them.
+hipError_t launch_wgrad(const GemmDesc& g, int dt, float* part, float* part_c, hipStream_t s) {
+  int ks = 1;
+  const GemmDesc sg = wgrad_slices(g, part, part_c, &ks);
   hipError_t e = launch_gemm(sg, dt, true, Layout::MNMajor, Layout::MNMajor, Tile::T128x128, s);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || ks <= 1) return e;
   GemmDesc rg = g;
   rg.splitk = ks;
   return launch_splitk_reduce(rg, part, part_c, dt, Layout::MNMajor, Layout::MNMajor, s);
+}
+
+// A weight gradient w and an independent projection pj (K-major operands;
+// either may be absent): in one launch when they qualify, so that each
+// fills the CUs the other leaves idle in its last round; else pj, then w.
+hipError_t wgrad_with_proj(const GemmDesc* w, const GemmDesc* pj, int dt, float* part,
+                           float* part_c, hipStream_t s) {
+  if (w && pj) {
+    int ks = 1;
+    const GemmDesc sg = wgrad_slices(*w, part, part_c, &ks);
+    const hipError_t e = launch_gemm_pair(sg, *pj, dt, s);
+    if (e == hipSuccess) {
+      if (ks <= 1) return hipSuccess;
+      GemmDesc rg = *w;
+      rg.splitk = ks;
+      return launch_splitk_reduce(rg, part, part_c, dt, Layout::MNMajor, Layout::MNMajor, s);
+    }
+    if (e != hipErrorNotSupported) return e;
+  }
+  if (pj) {
+    const hipError_t e = launch_gemm(*pj, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(), s);
+    if (e != hipSuccess) return e;
+  }
+  return w ? launch_wgrad(*w, dt, part, part_c, s) : hipSuccess;
 }
 
 GemmDesc base_desc(const Params& p, const abft_fault* faults, int n_faults, abft_report* rep) {
@@ -629,9 +662,12 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
                           s));
   }
 
-  // dCL = dO Wo^T, dCL^c = dO^c Wo^T
+  // dCL = dO Wo^T, dCL^c = dO^c Wo^T, and dWo = CL^T dO (independent: one
+  // launch when both qualify)
+  GemmDesc gdcl, gdwo;
   if (stages & ABFT_STAGE_DCL) {
-    GemmDesc g = base_desc(p, faults, n_faults, report);
+    GemmDesc& g = gdcl;
+    g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(H);
     g.A = dO; g.lda = H;
     g.B = Wo; g.ldb = H;
@@ -643,11 +679,11 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DCL; g.map.rows_per_b = int(S); g.map.head_cols = int(hd);
-    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(), s));
   }
   // dWo = CL^T dO, column checksums over head blocks of rows from CL^r
   if (stages & ABFT_STAGE_DWO) {
-    GemmDesc g = base_desc(p, faults, n_faults, report);
+    GemmDesc& g = gdwo;
+    g = base_desc(p, faults, n_faults, report);
     g.M = int(H); g.N = int(H); g.K = int(T);
     g.A = ws + L.cl; g.lda = H;
     g.B = dO; g.ldb = H;
@@ -660,8 +696,9 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DWO;
-    CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
+  CK(wgrad_with_proj((stages & ABFT_STAGE_DWO) ? &gdwo : nullptr,
+                     (stages & ABFT_STAGE_DCL) ? &gdcl : nullptr, dt, F(L.skp), F(L.skc), s));
   // after a fused forward (no scores kept): the fused backward core, from
   // the forward's softmax statistics, in two launches: the query pass (dQ,
   // and D per query) and the key pass (dK and dV); each forms the row
@@ -774,9 +811,22 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
     g.map.op_base = ABFT_OP_DK; g.map.nb1 = int(nh);
     CK(launch_gemm(g, dt, false, Layout::MNMajor, Layout::MNMajor, td, s));
   }
-  // dWqkv = X^T dQKV, column checksums over head blocks of rows from X^r
+  // dX = dQKV Wqkv^T, dX^c = dQKV^c Wqkv^T, and dWqkv = X^T dQKV (independent:
+  // one launch when both qualify)
+  if ((stages & ABFT_STAGE_DX) && fused && pb) {
+    // the fused core writes no checksums: dQKV^c from the checked dQKV
+    EncodeJob e;
+    e.A = ws + L.dqkv; e.batch = B; e.rows = S; e.cols = 3 * H; e.ld = 3 * H;
+    e.batch_stride = S * 3 * H; e.Rb = int(R); e.Cb = int(hd);
+    e.col_chk = F(L.dqkvc); e.ldcc = 3 * H;
+    if (es == 2) { e.col_img = reinterpret_cast<uint16_t*>(ws + L.dqkvci); e.ldci = 3 * H; }
+    CK(launch_encode_jobs(&e, 1, dt, nullptr, s));
+  }
+  // dWqkv: column checksums over head blocks of rows from X^r
+  GemmDesc gdwq, gdx;
   if (stages & ABFT_STAGE_DWQKV) {
-    GemmDesc g = base_desc(p, faults, n_faults, report);
+    GemmDesc& g = gdwq;
+    g = base_desc(p, faults, n_faults, report);
     g.M = int(H); g.N = int(3 * H); g.K = int(T);
     g.A = X; g.lda = H;
     g.B = ws + L.dqkv; g.ldb = 3 * H;
@@ -787,19 +837,10 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DWQ; g.map.op_span = int(H);
-    CK(launch_wgrad(g, dt, F(L.skp), F(L.skc), s));
   }
-  // dX = dQKV Wqkv^T, dX^c = dQKV^c Wqkv^T
   if (stages & ABFT_STAGE_DX) {
-    if (fused && pb) {  // the fused core writes no checksums: dQKV^c from the checked dQKV
-      EncodeJob e;
-      e.A = ws + L.dqkv; e.batch = B; e.rows = S; e.cols = 3 * H; e.ld = 3 * H;
-      e.batch_stride = S * 3 * H; e.Rb = int(R); e.Cb = int(hd);
-      e.col_chk = F(L.dqkvc); e.ldcc = 3 * H;
-      if (es == 2) { e.col_img = reinterpret_cast<uint16_t*>(ws + L.dqkvci); e.ldci = 3 * H; }
-      CK(launch_encode_jobs(&e, 1, dt, nullptr, s));
-    }
-    GemmDesc g = base_desc(p, faults, n_faults, report);
+    GemmDesc& g = gdx;
+    g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(3 * H);
     g.A = ws + L.dqkv; g.lda = 3 * H;
     g.B = Wqkv; g.ldb = 3 * H;
@@ -812,8 +853,9 @@ int attn_abft_backward_stages(const attn_abft_config* cfg, const void* dO, const
       g.verify = 1;
     }
     g.map.op_base = ABFT_OP_DX; g.map.rows_per_b = int(S);
-    CK(launch_gemm(g, dt, false, Layout::KMajor, Layout::KMajor, proj_tile(), s));
   }
+  CK(wgrad_with_proj((stages & ABFT_STAGE_DWQKV) ? &gdwq : nullptr,
+                     (stages & ABFT_STAGE_DX) ? &gdx : nullptr, dt, F(L.skp), F(L.skc), s));
   return ABFT_OK;
 }
 

@@ -28,17 +28,18 @@ namespace {
 
 constexpr int NT = 256;  // threads per workgroup: 4 waves as 2 (M) x 2 (N)
 
-// The kernel's descriptor (its only argument, at the start of the
-// kernel-argument segment), reached through an opaque copy of the segment
-// address: fields read through it are loaded where they are used instead of
-// being held in scalar registers from the kernel's start.
-__device__ __forceinline__ const GemmDesc& desc_reload() {
+// The kernel's descriptor (argument `slot` of the kernel: the descriptors
+// are its first arguments), reached through an opaque copy of the
+// kernel-argument segment address: fields read through it are loaded where
+// they are used instead of being held in scalar registers from the
+// kernel's start.
+__device__ __forceinline__ const GemmDesc& desc_reload(int slot) {
 #if defined(__HIP_DEVICE_COMPILE__)
   // the copy stays in the constant address space, so the fields are read
   // with scalar loads
   auto gp = __builtin_amdgcn_kernarg_segment_ptr();
   asm volatile("" : "+s"(gp));
-  return *(const GemmDesc*)gp;
+  return *((const GemmDesc*)gp + slot);
 #else
   return *static_cast<const GemmDesc*>(nullptr);  // the host pass emits no device code
 #endif
@@ -300,14 +301,13 @@ __host__ __device__ inline bool tri_tiles(const GemmDesc& g, int bm, int bn) {
 }
 
 template <int BM, int BN>
-__device__ __forceinline__ TileIdx tile_of(const GemmDesc& g) {
+__device__ __forceinline__ TileIdx tile_of(const GemmDesc& g, int lin, int total) {
   const int ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
   const int nb = g.nb0 * g.nb1;
-  const int lin = blockIdx.x;
   TileIdx t;
   int r;
   if (nb == 1) {
-    const int total = gridDim.x, q = total / 8, rem = total % 8;
+    const int q = total / 8, rem = total % 8;
     const int x = lin % 8, j = lin / 8;
     const int v = x * q + min(x, rem) + j;
     const int per = tri_tiles(g, BM, BN) ? ntm * (ntm + 1) / 2 : ntm * ntn;
@@ -420,10 +420,15 @@ struct Gemm {
   // DIR selects the direct-to-LDS operand path (bf16 only) at compile time,
   // so each kernel carries the registers and code of one path only.
   template <bool DIR>
-  __device__ static __forceinline__ void run(const GemmDesc& g, char* smem) {
+  // lin, total: the workgroup's index among this GEMM's workgroups and
+  // their count (a launch of two GEMMs deals each its own range; the first
+  // range is a multiple of 8 long, so both keep the dealing to the XCDs);
+  // slot: the descriptor's argument slot
+  __device__ static __forceinline__ void run(const GemmDesc& g, char* smem, int lin, int total,
+                                             int slot) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
-    const TileIdx ti = tile_of<BM, BN>(g);
+    const TileIdx ti = tile_of<BM, BN>(g, lin, total);
     const int m0 = ti.mt * BM, n0 = ti.nt * BN;
     const int z = ti.bh, kslice = ti.ks;
     const int b0 = z / g.nb1, b1 = z % g.nb1;
@@ -751,7 +756,7 @@ struct Gemm {
 
     // ---- epilogue ----
     {
-    const GemmDesc& g = desc_reload();  // not held across the main loop
+    const GemmDesc& g = desc_reload(slot);  // not held across the main loop
     if constexpr (sizeof(TC) == 4) if (split) {
       // fp32 partials go straight from the accumulators to this slice; the
       // column-checksum strip is combined (hi + lo) through a small LDS
@@ -872,7 +877,7 @@ struct Gemm {
     if constexpr (WLC) {
       static_assert(MSUM, "the wave-local check is for protected bf16 tiles");
       epilogue_wlc(g, tile, A, B, C, z, b0, b1, m0, n0, k_lo, k_hi, cc, cr, rc0, qc0, pk, accs, accr,
-                   reinterpret_cast<float*>(smem + TILE_BYTES), tid);
+                   reinterpret_cast<float*>(smem + TILE_BYTES), tid, slot);
       return;
     }
     __syncthreads();
@@ -1062,7 +1067,7 @@ struct Gemm {
       // 3. correction, only for a tile with a flagged vector
       if (__syncthreads_or(my_flag))
         passes(tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, reinterpret_cast<int*>(colp), nrb, ncb,
-               verify, tid);
+               verify, tid, slot);
     }
 
     // 4. store the tile with 16-byte coalesced chunks
@@ -1124,7 +1129,7 @@ struct Gemm {
       const GemmDesc& g, TC* tile, const T* A, const T* B, TC* C, int z, int b0, int b1, int m0,
       int n0, int k_lo, int k_hi, bool cc, bool cr, int rc0, int qc0,
       const uint32_t (&pk)[IM][JN][2],
-      const floatx4 (&accs)[JS], const floatx4 (&accr)[IS], float* region, int tid) {
+      const floatx4 (&accs)[JS], const floatx4 (&accr)[IS], float* region, int tid, int slot) {
     const int lane = tid & 63, wn = tid >> 6;
     const int fr = lane & 15, g4 = lane >> 4;
     constexpr int SEG = MINB;
@@ -1319,7 +1324,7 @@ struct Gemm {
       }
     }
     __syncthreads();
-    passes(tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, work, nrb, ncb, verify, tid);
+    passes(tile, A, B, z, m0, n0, k_lo, k_hi, ccv, rcv, work, nrb, ncb, verify, tid, slot);
     for (int c = tid; c < BM * (BN / V); c += NT) {
       const int row = c / (BN / V), col = (c % (BN / V)) * V;
       const int m = m0 + row, n = n0 + col;
@@ -1361,8 +1366,8 @@ struct Gemm {
   // refresh of 1C-corrupted column checksums, final check (Sec. 4.2, 4.3).
   __device__ static __forceinline__ void passes(
       TC* tile, const T* A, const T* B, int z, int m0, int n0, int k_lo, int k_hi, float* ccv,
-      float* rcv, int* work, int nrb, int ncb, int verify, int tid) {
-    const GemmDesc& g = desc_reload();
+      float* rcv, int* work, int nrb, int ncb, int verify, int tid, int slot) {
+    const GemmDesc& g = desc_reload(slot);
     int* rowcnt = work;                        // [BM][BN / MINB]
     int* colcnt = work + BM * (BN / MINB);     // [BM / MINB][BN]
     for (int e = tid; e < int(CNT); e += NT) rowcnt[e] = 0;
@@ -1517,7 +1522,8 @@ template <class T, class TC, bool AK, bool BKM, int BM, int BN, bool PROT, int N
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<T, BM, BN, PROT, NSTAGE, WLC && DIR>())))
 void gemm_kernel(GemmDesc g) {
   extern __shared__ __align__(16) char smem[];
-  Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, WLC>::template run<DIR>(g, smem);
+  Gemm<T, TC, AK, BKM, BM, BN, PROT, NSTAGE, WLC>::template run<DIR>(g, smem, blockIdx.x,
+                                                                      gridDim.x, 0);
 }
 
 // The direct-to-LDS path needs bf16 operands, K ranges of whole 64-wide
@@ -1609,6 +1615,59 @@ hipError_t launch_t(const GemmDesc& g, hipStream_t s) {
   const int64_t total = tiles * nb * ks;
   if (total > 0x7fffffff / NT) return hipErrorInvalidValue;
   hipLaunchKernelGGL(kern, dim3(unsigned(total)), dim3(NT), lds, s, g);
+  return hipGetLastError();
+}
+
+// Two independent GEMMs of the layer's backward in one launch: workgroups
+// [0, n1) run a weight gradient (MN-major operands, fp32 output, whole or
+// in K slices: the longer work items first), the rest a projection with
+// K-major operands and bf16 output; both 128 x 128 tiles on the direct
+// path. Alone, each leaves CUs idle in its last round of workgroups.
+template <bool PROT>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2)))
+void gemm_pair_kernel(GemmDesc gw, GemmDesc gp, int n1) {
+  extern __shared__ __align__(16) char smem[];
+  if (int(blockIdx.x) < n1)
+    Gemm<bf16_t, float, false, false, 128, 128, PROT, 2, false>::template run<true>(
+        gw, smem, blockIdx.x, n1, 0);
+  else
+    Gemm<bf16_t, bf16_t, true, true, 128, 128, PROT, 2, PROT>::template run<true>(
+        gp, smem, int(blockIdx.x) - n1, int(gridDim.x) - n1, 1);
+}
+
+template <bool PROT>
+hipError_t pair_t(const GemmDesc& w, const GemmDesc& p, hipStream_t s) {
+  using GW = Gemm<bf16_t, float, false, false, 128, 128, PROT, 2, false>;
+  using GP = Gemm<bf16_t, bf16_t, true, true, 128, 128, PROT, 2, PROT>;
+  if (!direct_ok<bf16_t>(w, false, false) || !direct_ok<bf16_t>(p, true, true))
+    return hipErrorNotSupported;
+  if (w.nb0 * w.nb1 != 1 || p.nb0 * p.nb1 != 1 || p.splitk > 1 || w.causal != 0 ||
+      p.causal != 0)
+    return hipErrorNotSupported;
+  if (w.Br != nullptr || w.verify == 2) return hipErrorInvalidValue;  // columns only
+  // the projection's epilogue as a launch of its own would take it: the
+  // wave-local check when protected
+  if (PROT && !((p.verify <= 1 || 128 / 4 >= 32) && (p.Ac == nullptr || p.Rm <= 128)))
+    return hipErrorNotSupported;
+  const bool wcc = PROT && w.Ac != nullptr, pcc = PROT && p.Ac != nullptr;
+  const bool pcr = PROT && p.Br != nullptr;
+  const size_t lw = w.splitk > 1 ? std::max(GW::d_main_bytes(wcc, false), size_t(16 * 128 * 4))
+                                 : std::max(GW::d_main_bytes(wcc, false), GW::EPI_BYTES);
+  const size_t lp = std::max(GP::d_main_bytes(pcc, pcr), GP::EPI_BYTES);
+  const size_t lds = std::max(lw, lp);
+  const size_t lds_max =
+      std::max(std::max(GW::lds_bytes(PROT, PROT), GW::d_main_bytes(PROT, PROT)),
+               std::max(GP::lds_bytes(PROT, PROT), GP::d_main_bytes(PROT, PROT)));
+  if (lds_max > 160 * 1024) return hipErrorNotSupported;
+  const int64_t ksw = w.splitk > 1 ? w.splitk : 1;
+  const int64_t n1 = ((w.M + 127) / 128) * ((w.N + 127) / 128) * ksw;
+  const int64_t n2 = ((p.M + 127) / 128) * ((p.N + 127) / 128);
+  if (n1 == 0 || n2 == 0 || n1 % 8 != 0) return hipErrorNotSupported;  // keeps the XCD dealing
+  if (n1 + n2 > 0x7fffffff / NT) return hipErrorInvalidValue;
+  constexpr auto k = gemm_pair_kernel<PROT>;
+  hipError_t e = set_lds_limit<k>(lds_max);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k, dim3(unsigned(n1 + n2)), dim3(NT), lds, s, w, p, int(n1));
   return hipGetLastError();
 }
 
@@ -1869,6 +1928,17 @@ hipError_t launch_splitk_reduce(const GemmDesc& g, const float* P, const float* 
                                 Layout la, Layout lb, hipStream_t stream) {
   if (dtype == ABFT_FP32) return reduce_t<float>(g, P, Pc, la, lb, stream);
   return reduce_t<bf16_t>(g, P, Pc, la, lb, stream);
+}
+
+hipError_t launch_gemm_pair(const GemmDesc& w, const GemmDesc& p, int dtype,
+                            hipStream_t stream) {
+  auto pow2 = [](int x) { return x > 0 && (x & (x - 1)) == 0; };
+  if (dtype != ABFT_BF16) return hipErrorNotSupported;
+  if (!pow2(w.Rm) || !pow2(w.Rn) || !pow2(p.Rm) || !pow2(p.Rn)) return hipErrorInvalidValue;
+  const bool pw = w.Ac != nullptr || w.Br != nullptr || w.verify != 0;
+  const bool pp = p.Ac != nullptr || p.Br != nullptr || p.verify != 0;
+  if (pw != pp) return hipErrorNotSupported;
+  return pp ? pair_t<true>(w, p, stream) : pair_t<false>(w, p, stream);
 }
 
 hipError_t launch_gemm(const GemmDesc& g, int dtype, bool c_fp32, Layout la, Layout lb,
