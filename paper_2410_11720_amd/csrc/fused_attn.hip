@@ -112,43 +112,134 @@ struct ArgRef<Desc, true> {
 };
 #endif
 
+// Sums over a float vector scr[0..n) (n <= 128) in LDS across the wave:
+// lane l holds elements l and l + 64 (zero past n); every lane gets the
+// totals.
+struct WaveVec {
+  float x0, x1;
+  bool in0, in1;
+  __device__ WaveVec(const float* scr, int n, int lane)
+      : in0(lane < n), in1(lane + 64 < n) {
+    x0 = in0 ? scr[lane] : 0.f;
+    x1 = in1 ? scr[lane + 64] : 0.f;
+  }
+};
+
+// EEC-ABFT location (Sec. 4.2) of a flagged vector, wave-parallel: the
+// same decisions as the one-lane form in abft_device.hpp (sums in another
+// order: both are fp32 approximations of the exact sums), the candidates
+// counted by ballots, the located candidate the last one.
+__device__ EecResult eec_wave(const WaveVec& v, int lane, int n, float c1, float c2, float e_rel,
+                              float tn) {
+  const float r1 = group_sum<64>(v.x0 + v.x1);
+  const float r2 = group_sum<64>(fmaf(float(lane + 1), v.x0, float(lane + 65) * v.x1));
+  const float sa = group_sum<64>((is_finite(v.x0) ? fabsf(v.x0) : 0.f) +
+                                 (is_finite(v.x1) ? fabsf(v.x1) : 0.f));
+  const float d1 = c1 - r1, d2 = c2 - r2;
+  EecResult res{EEC_CLEAN, -1, d1};
+  if (!flagged(d1, sa, e_rel)) return res;
+  const int mode = is_finite(d1) ? 1 : (is_inf(d1) ? 2 : 3);
+  const bool any_inf = mode == 2, any_nonfin = mode == 3;
+  auto cand = [&](float x, bool in) {
+    const bool fin = is_finite(x);
+    return in && ((fin && fabsf(x) >= tn) || (any_inf && is_inf(x)) || (any_nonfin && !fin));
+  };
+  const uint64_t b0 = __ballot(cand(v.x0, v.in0)), b1 = __ballot(cand(v.x1, v.in1));
+  const int cnt = __popcll(b0) + __popcll(b1);
+  const int idx = b1 ? 127 - __clzll(b1) : (b0 ? 63 - __clzll(b0) : -1);
+  res.status = EEC_PROPAGATED;
+  if (cnt >= 2) return res;
+  if (mode == 1) {
+    if (cnt == 1) {
+      if (is_finite(d2)) {
+        const float q = d2 / d1;
+        if (!(fabsf(q - float(idx + 1)) < 0.25f)) return res;
+      }
+      res.status = EEC_LOCATED;
+      res.index = idx;
+      return res;
+    }
+    if (!is_finite(d2)) return res;
+    const float q = d2 / d1;
+    if (!(q >= 0.5f && q < float(n) + 0.5f)) return res;
+    const float qi = rintf(q);
+    if (!(fabsf(q - qi) < 0.25f)) return res;
+    res.status = EEC_LOCATED;
+    res.index = int(qi) - 1;
+    return res;
+  }
+  if (cnt == 1) {
+    res.status = EEC_LOCATED;
+    res.index = idx;
+  }
+  return res;
+}
+
+// The detection rule on a vector (sum against c1, bound from the
+// magnitudes), wave-parallel.
+__device__ bool flagged_wave(const WaveVec& v, float c1, float e_rel) {
+  const float r1 = group_sum<64>(v.x0 + v.x1);
+  const float sa = group_sum<64>(fabsf(v.x0) + fabsf(v.x1));
+  return flagged(c1 - r1, sa, e_rel);
+}
+
 // Fixing a flagged score vector gathered in scr[0..n) (Sec. 4.2), in up to
-// three steps. score_locate (lane 0) locates by EEC; a located element is
-// fixed from the checksums unless recompute is set, the event recorded at
-// (row, col) when tr, else (col, row), and an unfixable vector reported;
-// scr[n] takes the located index (or -1), scr[n + 1] the new value. With
-// recompute, a located element is left to the wave: score_dot forms the
-// dot product of row `col` of A and row `rowbase + index` of Bm (length
-// d <= 128) across the lanes, then score_close (lane 0) stores it, records
-// the event and reports a vector that is still flagged.
-// (UNR: the unroll of the vector loops; 1 where the caller's registers are
-// tight, head dim 128)
-template <int UNR>
+// three steps, by the whole wave (every lane calls them). score_locate
+// locates by EEC; a located element is fixed from the checksums (DELTA or
+// RECONSTRUCT) unless recompute is set, the event recorded at (row, col)
+// when tr, else (col, row), and an unfixable vector reported; scr[n] takes
+// the located index (or -1), scr[n + 1] the new value. With recompute, a
+// located element is left to score_dot, which forms the dot product of row
+// `col` of A and row `rowbase + index` of Bm (length d <= 128) across the
+// lanes, then score_close stores it, records the event and reports a vector
+// that is still flagged. Lane 0 writes scr[n], scr[n + 1] and the events.
 __device__ __noinline__ void score_locate(float* scr, int n, float v1, float v2, float e_rel,
                                           float tn, float tc, int recompute, abft_report* report,
-                                          int op, int b, int h, int col, int rowbase, bool tr) {
-  const EecResult res = eec_locate<float, UNR>(scr, 1, n, v1, v2, e_rel, tn);
+                                          int op, int b, int h, int col, int rowbase, bool tr,
+                                          int lane) {
+  const WaveVec v(scr, n, lane);
+  const EecResult res = eec_wave(v, lane, n, v1, v2, e_rel, tn);
   int idx = -1;
   float nv = 0.f;
+  bool still = false;
   if (res.status == EEC_LOCATED) {
     idx = res.index;
+    const float old = scr[idx];
     if (recompute) {  // the rest after score_dot
-      scr[n] = __int_as_float(idx);
-      scr[n + 1] = scr[idx];
+      if (lane == 0) {
+        scr[n] = __int_as_float(idx);
+        scr[n + 1] = old;
+      }
       return;
     }
+    int action;
+    if (is_finite(res.d1) && fabsf(res.d1) <= tc) {
+      action = ABFT_ACT_DELTA;
+      nv = old + res.d1;
+    } else {
+      action = ABFT_ACT_RECONSTRUCT;
+      const float rest = (lane == idx ? 0.f : v.x0) + (lane + 64 == idx ? 0.f : v.x1);
+      nv = v1 - group_sum<64>(rest);
+    }
     const int row = rowbase + idx;
-    const float old = scr[idx];
-    int action = ABFT_ACT_RECOMPUTE;
-    nv = fix_by_checksum<float, UNR>(scr, 1, n, idx, v1, res.d1, tc, &action);
-    scr[idx] = nv;
-    record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn), action, old);
+    if (lane == 0)
+      record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn), action,
+                   old);
+    WaveVec w = v;  // the vector with the fix
+    if (lane == idx) w.x0 = nv;
+    if (lane + 64 == idx) w.x1 = nv;
+    still = flagged_wave(w, v1, e_rel);
+    if (lane == 0) scr[idx] = nv;
+  } else if (res.status != EEC_CLEAN) {
+    still = flagged_wave(v, v1, e_rel);
   }
-  if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, n, v1, e_rel))
-    record_event(report, op, b, h, tr ? rowbase : col, tr ? col : rowbase, ABFT_KIND_NONE,
-                 ABFT_ACT_UNCORRECTABLE, 0.f);
-  scr[n] = __int_as_float(idx);
-  scr[n + 1] = nv;
+  if (lane == 0) {
+    if (still)
+      record_event(report, op, b, h, tr ? rowbase : col, tr ? col : rowbase, ABFT_KIND_NONE,
+                   ABFT_ACT_UNCORRECTABLE, 0.f);
+    scr[n] = __int_as_float(idx);
+    scr[n + 1] = nv;
+  }
 }
 __device__ __noinline__ float score_dot(const bf16_t* A, const bf16_t* Bm, int64_t lda,
                                            int64_t ldb, int col, int row, int d, int lane) {
@@ -159,17 +250,23 @@ __device__ __noinline__ float score_dot(const bf16_t* A, const bf16_t* Bm, int64
 }
 __device__ __noinline__ void score_close(float* scr, int n, float nv, float v1, float e_rel,
                                          float tn, abft_report* report, int op, int b, int h,
-                                         int col, int rowbase, bool tr) {
+                                         int col, int rowbase, bool tr, int lane) {
   const int idx = __float_as_int(scr[n]);
   const int row = rowbase + idx;
   const float old = scr[idx];
-  scr[idx] = nv;
-  record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn),
-               ABFT_ACT_RECOMPUTE, old);
-  if (vec_flagged<float>(scr, 1, n, v1, e_rel))
-    record_event(report, op, b, h, tr ? rowbase : col, tr ? col : rowbase, ABFT_KIND_NONE,
-                 ABFT_ACT_UNCORRECTABLE, 0.f);
-  scr[n + 1] = nv;
+  WaveVec w(scr, n, lane);
+  if (lane == idx) w.x0 = nv;
+  if (lane + 64 == idx) w.x1 = nv;
+  const bool still = flagged_wave(w, v1, e_rel);
+  if (lane == 0) {
+    scr[idx] = nv;
+    record_event(report, op, b, h, tr ? row : col, tr ? col : row, classify(old, tn),
+                 ABFT_ACT_RECOMPUTE, old);
+    if (still)
+      record_event(report, op, b, h, tr ? rowbase : col, tr ? col : rowbase, ABFT_KIND_NONE,
+                   ABFT_ACT_UNCORRECTABLE, 0.f);
+    scr[n + 1] = nv;
+  }
 }
 
 // Whether an injected fault (test-only) of an op in mask targets head
@@ -491,17 +588,15 @@ struct FusedAttn {
                 const float v1 = __shfl(cs1, L, 64);
                 const float v2 = __shfl(cs2, L, 64);
                 wave_sync_lds();
-                if (lane == 0)
-                  score_locate<D == 64 ? 8 : 1>(scr, R, v1, v2, arg->e_rel, arg->tn_s, arg->tc,
-                                                arg->recompute, arg->report, ABFT_OP_AS, b, h,
-                                                qw + 16 * qb + vq, key0 + vb * R, false);
+                score_locate(scr, R, v1, v2, arg->e_rel, arg->tn_s, arg->tc, arg->recompute,
+                             arg->report, ABFT_OP_AS, b, h, qw + 16 * qb + vq, key0 + vb * R,
+                             false, lane);
                 wave_sync_lds();
                 if (arg->recompute && __float_as_int(scr[R]) >= 0) {
                   const float nv = score_dot(Qp, Kp, ld, ld, qw + 16 * qb + vq,
                                              key0 + vb * R + __float_as_int(scr[R]), D, lane);
-                  if (lane == 0)
-                    score_close(scr, R, nv, v1, arg->e_rel, arg->tn_s, arg->report, ABFT_OP_AS,
-                                b, h, qw + 16 * qb + vq, key0 + vb * R, false);
+                  score_close(scr, R, nv, v1, arg->e_rel, arg->tn_s, arg->report, ABFT_OP_AS,
+                              b, h, qw + 16 * qb + vq, key0 + vb * R, false, lane);
                 }
                 wave_sync_lds();
                 const int idx = __float_as_int(scr[R]);
@@ -932,16 +1027,14 @@ struct BwdTile {
         const float v1 = __shfl(cs1, L, 64);
         const float v2 = __shfl(cs2, L, 64);
         wave_sync_lds();
-        if (lane == 0)
-          score_locate<D == 64 ? 8 : 1>(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute,
-                                        fd.report, op, b, h, cbase + vq, rbase + vb * R, TR);
+        score_locate(scr, R, v1, v2, fd.e_rel, fd.tn_s, fd.tc, fd.recompute, fd.report, op, b,
+                     h, cbase + vq, rbase + vb * R, TR, lane);
         wave_sync_lds();
         if (fd.recompute && __float_as_int(scr[R]) >= 0) {
           const float nv = score_dot(A, Bm, lda, ldb, cbase + vq, rbase + vb * R +
                                      __float_as_int(scr[R]), D, lane);
-          if (lane == 0)
-            score_close(scr, R, nv, v1, fd.e_rel, fd.tn_s, fd.report, op, b, h, cbase + vq,
-                        rbase + vb * R, TR);
+          score_close(scr, R, nv, v1, fd.e_rel, fd.tn_s, fd.report, op, b, h, cbase + vq,
+                      rbase + vb * R, TR, lane);
           wave_sync_lds();
         }
         const int idx = __float_as_int(scr[R]);
