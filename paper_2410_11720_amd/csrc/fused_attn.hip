@@ -269,6 +269,49 @@ __device__ __noinline__ void score_close(float* scr, int n, float nv, float v1, 
   }
 }
 
+// A flagged row vector of an output (CL in the forward; dQ, dK, dV in the
+// backward passes) gathered in scr[0..n) (n <= 128), by the whole wave:
+// located by EEC and fixed from its checksums (DELTA or RECONSTRUCT, the
+// new value rounded to bf16 as stored), the event recorded at (e, index),
+// an unfixable vector reported; scr[n] takes the located index (or -1),
+// scr[n + 1] the new value (lane 0 writes them and the events).
+__device__ __noinline__ void grad_fix(float* scr, int n, float v1, float v2, float e_rel, float tn,
+                                      float tc, abft_report* report, int op, int b, int h, int e,
+                                      int lane) {
+  const WaveVec v(scr, n, lane);
+  const EecResult res = eec_wave(v, lane, n, v1, v2, e_rel, tn);
+  int idx = -1;
+  float nv = 0.f;
+  bool still = false;
+  if (res.status == EEC_LOCATED) {
+    idx = res.index;
+    const float old = scr[idx];
+    int action;
+    if (is_finite(res.d1) && fabsf(res.d1) <= tc) {
+      action = ABFT_ACT_DELTA;
+      nv = old + res.d1;
+    } else {
+      action = ABFT_ACT_RECONSTRUCT;
+      const float rest = (lane == idx ? 0.f : v.x0) + (lane + 64 == idx ? 0.f : v.x1);
+      nv = v1 - group_sum<64>(rest);
+    }
+    nv = bf2f(f2bf(nv));
+    if (lane == 0) record_event(report, op, b, h, e, idx, classify(old, tn), action, old);
+    WaveVec w = v;
+    if (lane == idx) w.x0 = nv;
+    if (lane + 64 == idx) w.x1 = nv;
+    still = flagged_wave(w, v1, e_rel);
+    if (lane == 0) scr[idx] = nv;
+  } else if (res.status != EEC_CLEAN) {
+    still = flagged_wave(v, v1, e_rel);
+  }
+  if (lane == 0) {
+    if (still) record_event(report, op, b, h, e, 0, ABFT_KIND_NONE, ABFT_ACT_UNCORRECTABLE, 0.f);
+    scr[n] = __int_as_float(idx);
+    scr[n + 1] = nv;
+  }
+}
+
 // Whether an injected fault (test-only) of an op in mask targets head
 // (b, h) of a batch element: read once per workgroup, so that the
 // workgroups no fault reaches skip the per-tile injection code (each of its
@@ -785,26 +828,8 @@ struct FusedAttn {
             }
             const float v1 = __shfl(c1, L, 64), v2 = __shfl(c2, L, 64);
             wave_sync_lds();
-            if (lane == 0) {
-              const int qq = qw + 16 * qb + L;
-              const EecResult res = eec_locate<float, 1>(scr, 1, D, v1, v2, arg->e_rel, arg->tn_cl);
-              int idx = -1;
-              float nv = 0.f;
-              if (res.status == EEC_LOCATED) {
-                idx = res.index;
-                const float old = scr[idx];
-                int action = 0;
-                nv = bf2f(f2bf(fix_by_checksum<float, 1>(scr, 1, D, idx, v1, res.d1, arg->tc, &action)));
-                scr[idx] = nv;
-                record_event(arg->report, ABFT_OP_CL, b, h, qq, idx, classify(old, arg->tn_cl), action,
-                             old);
-              }
-              if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, D, v1, arg->e_rel))
-                record_event(arg->report, ABFT_OP_CL, b, h, qq, 0, ABFT_KIND_NONE,
-                             ABFT_ACT_UNCORRECTABLE, 0.f);
-              scr[D] = __int_as_float(idx);
-              scr[D + 1] = nv;
-            }
+            grad_fix(scr, D, v1, v2, arg->e_rel, arg->tn_cl, arg->tc, arg->report, ABFT_OP_CL, b,
+                     h, qw + 16 * qb + L, lane);
             wave_sync_lds();
             const int idx = __float_as_int(scr[D]);
             const float nv = scr[D + 1];
@@ -852,27 +877,6 @@ struct FusedAttn {
 // work of the checks runs out of line (it is rare and would otherwise hold
 // registers across the loops).
 
-// The same for a flagged gradient row of length n (entity e): fixed from
-// the checksums, rounded to storage.
-template <int UNR>
-__device__ __noinline__ void grad_fix(float* scr, int n, float v1, float v2, float e_rel, float tn,
-                                      float tc, abft_report* report, int op, int b, int h, int e) {
-  const EecResult res = eec_locate<float, UNR>(scr, 1, n, v1, v2, e_rel, tn);
-  int idx = -1;
-  float nv = 0.f;
-  if (res.status == EEC_LOCATED) {
-    idx = res.index;
-    const float old = scr[idx];
-    int action = 0;
-    nv = bf2f(f2bf(fix_by_checksum<float, UNR>(scr, 1, n, idx, v1, res.d1, tc, &action)));
-    scr[idx] = nv;
-    record_event(report, op, b, h, e, idx, classify(old, tn), action, old);
-  }
-  if (res.status != EEC_CLEAN && vec_flagged<float>(scr, 1, n, v1, e_rel))
-    record_event(report, op, b, h, e, 0, ABFT_KIND_NONE, ABFT_ACT_UNCORRECTABLE, 0.f);
-  scr[n] = __int_as_float(idx);
-  scr[n + 1] = nv;
-}
 
 // Shared pieces of the two passes. A score tile t[8] of a wave holds, for
 // lane (lq = lane % 16, g = lane / 16), the 4 rows 16 j + 4 g + r (r = 0..3;
@@ -1128,8 +1132,7 @@ struct BwdTile {
           }
           const float v1 = __shfl(c1, L, 64), v2 = __shfl(c2, L, 64);
           wave_sync_lds();
-          if (lane == 0)
-            grad_fix<D == 64 ? 8 : 1>(scr, D, v1, v2, fd.e_rel, fd.tn, fd.tc, fd.report, op, b, h, cbase + L);
+          grad_fix(scr, D, v1, v2, fd.e_rel, fd.tn, fd.tc, fd.report, op, b, h, cbase + L, lane);
           wave_sync_lds();
           const int idx = __float_as_int(scr[D]);
           const float nv = scr[D + 1];
