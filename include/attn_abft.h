@@ -73,8 +73,8 @@ extern "C" {
                                        row side per R-key block against
                                        Q (K^c)^T, CL against the V^r row
                                        checksum carried through the online
-                                       softmax; CL^c encoded from the verified
-                                       CL; Q verified at the projection even
+                                       softmax; CL^c summed in the kernel
+                                       from the checked, stored CL; Q verified at the projection even
                                        without ABFT_FLAG_ROOT_CHECK, fixed from
                                        its checksums then, as the row side
                                        cannot see a Q error). Needs bf16
@@ -242,7 +242,7 @@ int attn_abft_forward_noalloc(const attn_abft_config* cfg, const void* X, const 
 #define ABFT_STAGE_SCORE       0x004u  /* fwd: AS = Q K^T                           */
 #define ABFT_STAGE_SOFTMAX     0x008u  /* fwd: AP = softmax(scale AS)               */
 #define ABFT_STAGE_CONTEXT     0x010u  /* fwd: CL = AP V                            */
-#define ABFT_STAGE_OUT         0x020u  /* fwd: O = CL Wo (fused: CL^c encoded first) */
+#define ABFT_STAGE_OUT         0x020u  /* fwd: O = CL Wo (fused: CL^c from the fused kernel) */
 #define ABFT_STAGE_DCL         0x002u  /* bwd: dCL = dO Wo^T                        */
 #define ABFT_STAGE_DWO         0x004u  /* bwd: dWo = CL^T dO                        */
 #define ABFT_STAGE_DAP         0x008u  /* bwd: dAP = dCL V^T (fused: no work)       */

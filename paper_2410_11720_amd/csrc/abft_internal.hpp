@@ -158,6 +158,11 @@ struct FusedDesc {
   // optional transposed bf16 image of CL^r [nh][4][B*S] (rows c1 hi, c1 lo,
   // c2 hi, c2 lo per head): the column strip of the dW^O GEMM
   uint16_t* clri = nullptr;
+  // optional CL^c [B][S/R][2][H] (the column checksums of the stored,
+  // checked CL over each R-query block) and its bf16 image [B][S/R][4][H]
+  // (rows c1 hi, c1 lo, c2 hi, c2 lo): the output projection's strip
+  float* clc = nullptr;
+  uint16_t* clci = nullptr;
 };
 hipError_t launch_fused_fwd(const FusedDesc& d, hipStream_t stream);
 

@@ -522,6 +522,10 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     fd.stats = F(L.stats);
     fd.clr = F(L.clr);
     if (es == 2) fd.clri = reinterpret_cast<uint16_t*>(ws + L.clri);
+    if (p.sec_o) {  // CL^c of the checked CL for the output projection
+      fd.clc = F(L.clc);
+      if (es == 2) fd.clci = reinterpret_cast<uint16_t*>(ws + L.clci);
+    }
     CK(launch_fused_fwd(fd, s));
   }
   // AS = Q K^T per head (unscaled, before the mask), two-sided checksums
@@ -576,13 +580,6 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
   }
   // O = CL Wo, O^c = CL^c Wo
   if (stages & ABFT_STAGE_OUT) {
-    if (fused && p.sec_o) {  // the fused forward keeps no CL^c: encoded from the verified CL
-      EncodeJob e;
-      e.A = ws + L.cl; e.batch = B; e.rows = S; e.cols = H; e.ld = H; e.batch_stride = S * H;
-      e.Rb = int(R); e.Cb = int(hd); e.col_chk = F(L.clc);
-      if (es == 2) { e.col_img = reinterpret_cast<uint16_t*>(ws + L.clci); e.ldci = H; }
-      CK(launch_encode_jobs(&e, 1, dt, nullptr, s));
-    }
     GemmDesc g = base_desc(p, faults, n_faults, report);
     g.M = int(T); g.N = int(H); g.K = int(H);
     g.A = ws + L.cl; g.lda = H;
@@ -590,7 +587,7 @@ int forward_impl(const attn_abft_config* cfg, const Dims& d, const Layout_& L, c
     g.C = O; g.ldc = H;
     if (p.sec_o) {
       g.Ac = F(L.clc); g.ldac = H; g.Rm = int(R);
-      if (fused && es == 2) {  // the image the encode above wrote
+      if (fused && es == 2) {  // the image the fused forward wrote with CL^c
         g.Aci = reinterpret_cast<const uint16_t*>(ws + L.clci); g.ldaci = H;
       }
       g.verify = 1;

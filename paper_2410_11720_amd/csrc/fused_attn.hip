@@ -755,6 +755,14 @@ struct FusedAttn {
 
     // CL = O / l: round, check against A^r / l, store
     bf16_t* CLp = static_cast<bf16_t*>(arg->cl) + int64_t(b) * S * H + h * D;
+    // CL^c of the stored CL (given clc): the lane's sums over its queries of
+    // each of its dims (plain and weighted by the query's place in its
+    // R-query block, from 1)
+    float cs1[DB][4], cs2[DB][4];
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs1[db][r] = cs2[db][r] = 0.f;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       const int q = qw + 16 * qb + lq;
@@ -848,6 +856,53 @@ struct FusedAttn {
       for (int db = 0; db < DB; ++db) {
         const uint2 w = {pack2(ov[db][0], ov[db][1]), pack2(ov[db][2], ov[db][3])};
         *reinterpret_cast<uint2*>(CLp + int64_t(q) * H + 16 * db + 4 * g) = w;
+      }
+      if constexpr (PROT) {
+        const float wq = float((q - q0) % arg->R + 1);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float x = bf2f(f2bf(ov[db][r]));  // as stored
+            cs1[db][r] += x;
+            cs2[db][r] = fmaf(wq, x, cs2[db][r]);
+          }
+      }
+    }
+    if constexpr (PROT) {
+      if (arg->clc != nullptr) {
+        // sums over the wave's 16 query lanes (one DPP row per lane
+        // group), then over the waves of each R-query block through LDS
+        // (the stages are free once every wave is past the key loop), in
+        // a fixed order
+        __syncthreads();
+        float* part = reinterpret_cast<float*>(smem);  // [NW][2][D]
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float t1 = group_sum<16>(cs1[db][r]), t2 = group_sum<16>(cs2[db][r]);
+            if (lq == 0) {
+              part[(wave * 2) * D + 16 * db + 4 * g + r] = t1;
+              part[(wave * 2 + 1) * D + 16 * db + 4 * g + r] = t2;
+            }
+          }
+        __syncthreads();
+        const int R = arg->R, NBq = FT / R, wpb = NW / NBq;  // waves per R-query block
+        const int nqR = S / R;
+        for (int e = tid; e < NBq * 2 * D; e += NTH) {
+          const int blk = e / (2 * D), c = (e / D) & 1, d = e % D;
+          float v = 0.f;
+          for (int w = blk * wpb; w < (blk + 1) * wpb; ++w) v += part[(w * 2 + c) * D + d];
+          const int64_t row = int64_t(b) * nqR + q0 / R + blk;
+          arg->clc[(row * 2 + c) * H + h * D + d] = v;
+          if (arg->clci != nullptr) {
+            const bf16_t hi = f2bf(v);
+            bf16_t* ip = reinterpret_cast<bf16_t*>(arg->clci) + (row * 4 + 2 * c) * H + h * D + d;
+            ip[0] = hi;
+            ip[H] = f2bf(v - bf2f(hi));
+          }
+        }
       }
     }
   }
