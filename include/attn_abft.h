@@ -225,8 +225,9 @@ int attn_abft_backward(const attn_abft_config* cfg, const void* dO, const void* 
  * ends; no memory is allocated during the call. Arguments as for
  * attn_abft_forward; nothing is saved for a backward (ABFT_SEC_BWD is
  * ignored). The layer must fit the buffer: T = batch * seq tokens need
- * about T * hidden * 8 bytes (storage bf16) plus T * heads * 32 bytes of
- * checksums and softmax statistics (B8 S1024 H768 with 12 heads: 55 MB);
+ * about T * hidden * 8 bytes (storage bf16) plus T * heads * 32 bytes and
+ * (T / block_rows) * hidden * 56 bytes of checksums, their bf16 images and
+ * softmax statistics (B8 S1024 H768 with 12 heads: 56 MB);
  * a larger layer returns ABFT_ERR_WORKSPACE before anything is enqueued.
  * Every call on a device shares that device's buffer and leaves its
  * contents behind: calls that overlap on one device (other streams, other
